@@ -1,0 +1,442 @@
+"""Oracle for the xHC / xHC-Flash per-sublayer residual-stream connection.
+
+TEST INFRASTRUCTURE ONLY.  This module is a plain, slow, CPU, float64
+implementation of what the paper (xHC: Expanded Hyper-Connections,
+arXiv 2607.14530) defines, used to check the HIP library.  Only the test
+suite, the smoke check and the CPU-baseline leg of the benchmark may import
+it.  It shares no code with the HIP path: no kernels, no packing, no helpers.
+
+Conventions (readings of the paper where it is silent, see the ambiguity
+register in the design notes; each is repeated at the line that uses it):
+
+* The state of one token is X in R^{N x C}; ``flatten`` is stream-major,
+  x[i*C + c] = X[i, c].  The active state is gathered in slot order and
+  ``vec`` is slot-major, a[j*C + c] = X[I_j, c].
+* Projection operands are bfloat16 (Sec. "Infrastructure Design"): the
+  state already is; every projection weight is rounded fp32 -> bf16 (round
+  to nearest even) before use.  Everything else is exact float64 here.
+* ``mat_{k x k}`` and ``mat_{k x K_r}`` are row-major: H^res[j, l] =
+  z[j*k + l], H^post[j, r] = z[j*K_r + r].
+* Routing: slots 0..m-1 hold the fixed streams 0..m-1 (p = 1); slots
+  m..k-1 hold the k-m streams among m..N-1 with the largest router logit,
+  in descending logit order, ties to the lower stream index (eq:router_topk;
+  sigma is monotone, so ordering logits orders the scores).
+* Sinkhorn: each iteration normalises rows, then columns (eq:mhc_sinkhorn,
+  20 iterations per the hyperparameter table); afterwards each row i is
+  divided by its sum s_i when s_i > 1 + clamp_delta (the row-sum clamp of
+  App. A, "xHC Configuration"; clamp_delta = 0 is the literal max(s_i, 1)).
+* Temporal augmentation: g_j[t] = sum_{i < kappa_j} w_j[i] * out[t - i],
+  per channel, with out[t - i] = 0 before the start of t's sequence
+  (eq:aug and Sec. "Parameterization Details").  conv_w stacks the branch
+  kernels row-wise: rows [0, kappa_1) are w_1, the next kappa_2 rows w_2 ...
+* Gram-Schmidt follows the printed formula eq:gs; a coefficient whose
+  denominator <v_i, v_i> is zero is taken as zero.
+
+Parity status of each function is stated in its docstring; the pins live in
+``tests/test_oracle_*.py``.
+"""
+
+from __future__ import annotations
+
+import torch
+
+F64 = torch.float64
+
+
+# --------------------------------------------------------------------------
+# small pieces
+# --------------------------------------------------------------------------
+
+def bf16_operand(w: torch.Tensor) -> torch.Tensor:
+    """Round fp32 values to bfloat16 (nearest even) and return them as fp64.
+
+    The paper keeps projection operands in bfloat16 (Sec. "Infrastructure
+    Design").  The conversion is done from float32 so that a value is rounded
+    exactly once.
+    """
+    return w.to(torch.float32).to(torch.bfloat16).to(F64)
+
+
+def round_state_bf16(x: torch.Tensor) -> torch.Tensor:
+    """Round values of the residual state to bfloat16 (stored precision)."""
+    return x.to(torch.bfloat16).to(F64)
+
+
+def sigmoid(z: torch.Tensor) -> torch.Tensor:
+    return 1.0 / (1.0 + torch.exp(-z))
+
+
+def layer_norm(x: torch.Tensor, eps: float) -> torch.Tensor:
+    """LayerNorm over the last axis, biased variance, no affine (eq:router)."""
+    mu = x.mean(-1, keepdim=True)
+    var = ((x - mu) ** 2).mean(-1, keepdim=True)
+    return (x - mu) / torch.sqrt(var + eps)
+
+
+def rms_norm(x: torch.Tensor, eps: float) -> torch.Tensor:
+    """RMSNorm over the last axis, no gain (eq:param_pre, eq:param_res)."""
+    return x / torch.sqrt((x * x).mean(-1, keepdim=True) + eps)
+
+
+def sinkhorn(M: torch.Tensor, iters: int) -> torch.Tensor:
+    """Sinkhorn-Knopp on the last two axes: rows, then columns, per iteration."""
+    for _ in range(iters):
+        M = M / M.sum(-1, keepdim=True)
+        M = M / M.sum(-2, keepdim=True)
+    return M
+
+
+def row_clamp(H: torch.Tensor, delta: float) -> torch.Tensor:
+    """Divide each row by its sum when the sum exceeds 1 + delta (App. A)."""
+    s = H.sum(-1, keepdim=True)
+    return torch.where(s > 1.0 + delta, H / s, H)
+
+
+def residual_mapping(z_res: torch.Tensor, alpha_res, b_res, k: int,
+                     iters: int, delta: float) -> torch.Tensor:
+    """H^res = clamp(SK(exp(alpha * mat_{k x k}(z) + b)))  (eq:param_res)."""
+    T = z_res.shape[0]
+    logits = alpha_res * z_res + b_res
+    return row_clamp(sinkhorn(torch.exp(logits).reshape(T, k, k), iters), delta)
+
+
+def post_mapping(z_post: torch.Tensor, alpha_post, b_post, k: int, Kr: int) -> torch.Tensor:
+    """H^post = 2 sigma(alpha * mat_{k x K_r}(z) + b)  (eq:param_post)."""
+    T = z_post.shape[0]
+    return (2.0 * sigmoid(alpha_post * z_post + b_post)).reshape(T, k, Kr)
+
+
+def route(z_r: torch.Tensor, m: int, k: int):
+    """Fixed-plus-TopK routing (eq:router_topk).
+
+    Returns (idx [T,k] int64, p [T,k] fp64, gap [T] fp64).  ``gap`` is the
+    smallest difference between neighbouring logits in the sorted routed
+    list, taken over the k-m selected ones and the first unselected one; it
+    is +inf when nothing is routed.  A small gap marks a near-tie, where more
+    than one slot assignment is correct within rounding.
+    """
+    T, N = z_r.shape
+    idx = torch.empty(T, k, dtype=torch.int64)
+    idx[:, :m] = torch.arange(m)
+    gap = torch.full((T,), float("inf"), dtype=F64)
+    if k > m:
+        cand = z_r[:, m:]
+        order = torch.sort(-cand, dim=1, stable=True).indices   # ties keep lower index first
+        idx[:, m:] = order[:, : k - m] + m
+        n_look = min(k - m + 1, N - m)
+        srt = torch.gather(cand, 1, order[:, :n_look])
+        if n_look > 1:
+            gap = (srt[:, :-1] - srt[:, 1:]).min(dim=1).values
+    s = sigmoid(z_r)
+    p = torch.ones(T, k, dtype=F64)
+    if k > m:
+        p[:, m:] = torch.gather(s, 1, idx[:, m:])
+    return idx, p, gap
+
+
+def gather_rows(X: torch.Tensor, idx: torch.Tensor) -> torch.Tensor:
+    """X_act[t, j, :] = X[t, idx[t, j], :]."""
+    T = X.shape[0]
+    return X[torch.arange(T)[:, None], idx]
+
+
+# --------------------------------------------------------------------------
+# temporal feature augmentation + Gram-Schmidt
+# --------------------------------------------------------------------------
+
+def temporal_branches(F: torch.Tensor, conv_w: torch.Tensor, kappa, S: int,
+                      tokens: torch.Tensor) -> list:
+    """g_j[t] for t in ``tokens`` (eq:aug, Sec. "Parameterization Details").
+
+    F: [T, C] sublayer output of the whole batch (any float dtype); conv_w:
+    [sum(kappa), C].  Causal, per channel, zero before each sequence start.
+    """
+    w = conv_w.to(F64)
+    pos = tokens % S
+    out = []
+    row = 0
+    for kap in kappa:
+        g = torch.zeros(tokens.shape[0], F.shape[1], dtype=F64)
+        for i in range(kap):
+            valid = pos >= i
+            src = torch.where(valid, tokens - i, tokens)
+            g = g + torch.where(valid[:, None], w[row + i] * F[src].to(F64), 0.0)
+        out.append(g)
+        row += kap
+    return out
+
+
+def gram_schmidt(components: list) -> list:
+    """Orthogonalise [out, g_1, ..., g_r] per token over C (eq:gs)."""
+    v = [components[0]]
+    for g in components[1:]:
+        u = g
+        for vi in v:
+            nn = (vi * vi).sum(-1, keepdim=True)
+            dot = (g * vi).sum(-1, keepdim=True)
+            coef = torch.where(nn > 0, dot / torch.where(nn > 0, nn, 1.0), 0.0)
+            u = u - coef * vi
+        v.append(u)
+    return v
+
+
+def augmented_output(F, conv_w, kappa, S, tokens, gram_schmidt_on=True) -> list:
+    """out_aug for token list ``tokens``: K_r components, each [len(tokens), C]."""
+    out = F[tokens].to(F64)
+    if conv_w is None:
+        return [out]
+    comps = [out] + temporal_branches(F, conv_w, kappa, S, tokens)
+    return gram_schmidt(comps) if gram_schmidt_on else comps
+
+
+# --------------------------------------------------------------------------
+# full xHC sublayer (Alg. "Forward pass of one xHC sublayer")
+# --------------------------------------------------------------------------
+
+def xhc_pre(X, W_r, W_pre, W_res, W_post, alpha, b_pre, b_res, b_post, *,
+            m, k, Kr, eps=1e-5, sinkhorn_iters=20, clamp_delta=1e-6):
+    """Mapping generation + dense read of one xHC sublayer.
+
+    X: [T, N, C] float64 holding the exact state values.  W_r, W_pre: [N*C, N]
+    fp32; W_res: [k*C, k*k]; W_post: [k*C, k*Kr]; alpha = (alpha_pre,
+    alpha_res, alpha_post); b_pre [N], b_res [k*k], b_post [k*Kr].
+
+    Follows eq:router, eq:router_topk, eq:param_pre, eq:dense_read,
+    eq:param_res, eq:param_post.  Parity: pinned (see tests).
+    """
+    T, N, C = X.shape
+    a_pre, a_res, a_post = alpha
+    x = X.reshape(T, N * C)                                   # flatten, stream-major
+    z_r = layer_norm(x, eps) @ bf16_operand(W_r)              # router logits
+    z_pre = rms_norm(x, eps) @ bf16_operand(W_pre)
+    Hpre = sigmoid(a_pre * z_pre + torch.as_tensor(b_pre, dtype=F64))
+    idx, p, gap = route(z_r, m, k)
+    act = gather_rows(X, idx)                                 # [T, k, C]
+    a_n = rms_norm(act.reshape(T, k * C), eps)                # vec, slot-major
+    z_res = a_n @ bf16_operand(W_res)
+    z_post = a_n @ bf16_operand(W_post)
+    Hres = residual_mapping(z_res, a_res, torch.as_tensor(b_res, dtype=F64), k,
+                            sinkhorn_iters, clamp_delta)
+    Hpost = post_mapping(z_post, a_post, torch.as_tensor(b_post, dtype=F64), k, Kr)
+    inp = torch.einsum("tn,tnc->tc", Hpre, X)                 # dense read
+    return dict(input=inp, idx=idx, p=p, Hpre=Hpre, Hres=Hres, Hpost=Hpost,
+                z_r=z_r, z_pre=z_pre, z_res=z_res, z_post=z_post, gap=gap)
+
+
+def xhc_post(X, F, conv_w, idx, p, Hres, Hpost, *, S, kappa=(4, 8, 12),
+             tokens=None, gram_schmidt_on=True):
+    """Sparse write-back of one xHC sublayer (eq:sparse_write_delta, eq:sparse_write).
+
+    X: [Tt, N, C] float64 state of the tokens ``tokens`` (all tokens when
+    None) before the update; F: [T, C] sublayer output of the whole batch
+    (needed for the causal window); conv_w: [sum(kappa), C] or None (K_r = 1).
+    idx, p, Hres, Hpost belong to the same tokens as X.  Returns the updated
+    state (float64): rows idx replaced, every other row returned unchanged.
+    Parity: pinned (see tests).
+    """
+    Tt, N, C = X.shape
+    if tokens is None:
+        tokens = torch.arange(Tt)
+    comps = augmented_output(F, conv_w, kappa, S, tokens, gram_schmidt_on)
+    Kr = len(comps)
+    assert Hpost.shape[-1] == Kr
+    act = gather_rows(X, idx)                                            # [Tt, k, C]
+    mixed = torch.einsum("tjl,tlc->tjc", Hres, act)                      # H^res X_act
+    wb = sum(Hpost[:, :, r, None] * comps[r][:, None, :] for r in range(Kr))
+    Y = mixed + p[:, :, None] * wb                                       # p on write-back only
+    Xn = X.clone()
+    Xn[torch.arange(Tt)[:, None], idx] = Y
+    return Xn
+
+
+# --------------------------------------------------------------------------
+# dense mHC (separately written, used as a special-case pin)
+# --------------------------------------------------------------------------
+
+def mhc_dense(X, F, W_pre, W_post, W_res, alpha, b_pre, b_post, b_res, *,
+              eps=1e-5, sinkhorn_iters=20, clamp_delta=1e-6):
+    """Dense mHC sublayer, k = N, no router, one write-back component.
+
+    eq:hc with the mappings of eq:mhc_sinkhorn and the gated sigmoid
+    parameterisation of Sec. "Parameterization Details" applied to the full
+    RMS-normalised state.  X: [T, N, C]; F: [T, C]; W_pre, W_post: [N*C, N];
+    W_res: [N*C, N*N].  Returns (input, X_new, Hpre, Hpost, Hres).
+    """
+    T, N, C = X.shape
+    a_pre, a_res, a_post = alpha
+    xn = rms_norm(X.reshape(T, N * C), eps)
+    Hpre = sigmoid(a_pre * (xn @ bf16_operand(W_pre)) + torch.as_tensor(b_pre, dtype=F64))
+    Hpost = 2.0 * sigmoid(a_post * (xn @ bf16_operand(W_post)) + torch.as_tensor(b_post, dtype=F64))
+    E = torch.exp(a_res * (xn @ bf16_operand(W_res)) + torch.as_tensor(b_res, dtype=F64))
+    Hres = row_clamp(sinkhorn(E.reshape(T, N, N), sinkhorn_iters), clamp_delta)
+    inp = (Hpre[:, :, None] * X).sum(1)
+    Xn = torch.bmm(Hres, X) + Hpost[:, :, None] * F.to(F64)[:, None, :]
+    return inp, Xn, Hpre, Hpost, Hres
+
+
+# --------------------------------------------------------------------------
+# xHC-Flash (Alg. "xHC-Flash: one Transformer block"; App. E.1, E.2)
+# --------------------------------------------------------------------------
+
+def flash_sublayer_kind(q: int) -> str:
+    """Sublayer q (1-based) of a sharing group: odd = attention, even = MLP."""
+    return "attn" if q % 2 == 1 else "mlp"
+
+
+def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list,
+                    alpha_pre, b_pre, alpha_post, b_post, alpha_res, b_res, *,
+                    m, k, S, kappa=(4, 8, 12), eps=1e-5, sinkhorn_iters=20,
+                    clamp_delta=1e-6, round_state=True, gram_schmidt_on=True):
+    """One xHC-Flash sharing group of Q = len(F_list) sublayers (Q = 2 or 4).
+
+    Shared routing and Q pre-mappings come from the group-entry state X0
+    (eq:flash_dual_read, App. E.2 eq:app_four_sub_base).  Sublayers before
+    the last update the active rows without residual mixing
+    (eq:flash_attn_update, eq:app_general_writeback); the last sublayer
+    applies H^res (Alg. "xHC-Flash", MLP step).  Inputs of later sublayers
+    use the active-state form (eq:app_active_state_correction); for Q = 2
+    the scalar form of eq:read_reuse is also returned for comparison.
+
+    X0: [T, N, C] float64; F_list[q-1]: [T, C] output of sublayer q;
+    W_pre_list[q-1]: [N*C, N]; W_post_list[q-1]: [k*C, k*K_q] with K_q = 1 for
+    attention and 1 + len(kappa) for MLP; conv_w_list[q-1]: [sum kappa, C] or
+    None; alpha_pre/b_pre/alpha_post/b_post: per-sublayer lists.
+    ``round_state`` rounds each written active row to bfloat16 (the stored
+    state precision); pins of exact identities switch it off.
+
+    Returns a dict with idx, p, Hpre [Q,T,N], inputs (list of Q [T,C]), bases
+    (list, entry 0 is None), Hpost (list), Hres, X (final state), X_steps
+    (state after each sublayer) and, for Q = 2, input_scalar_form.
+    Parity: pinned (see tests).
+    """
+    Q = len(F_list)
+    assert Q in (2, 4), "a sharing group holds 2 or 4 sublayers"
+    T, N, C = X0.shape
+    x = X0.reshape(T, N * C)
+    z_r = layer_norm(x, eps) @ bf16_operand(W_r)
+    xr = rms_norm(x, eps)
+    Hpre = torch.stack([
+        sigmoid(alpha_pre[q] * (xr @ bf16_operand(W_pre_list[q])) +
+                torch.as_tensor(b_pre[q], dtype=F64))
+        for q in range(Q)])
+    idx, p, gap = route(z_r, m, k)
+    active = torch.zeros(T, N, dtype=torch.bool)
+    active[torch.arange(T)[:, None], idx] = True
+    inputs = [torch.einsum("tn,tnc->tc", Hpre[0], X0)]
+    bases = [None] + [torch.einsum("tn,tnc->tc", Hpre[q] * (~active), X0) for q in range(1, Q)]
+    inp_full = [torch.einsum("tn,tnc->tc", Hpre[q], X0) for q in range(Q)]
+
+    def post_from(a, q):
+        Kq = W_post_list[q].shape[1] // k
+        z = rms_norm(a.reshape(T, k * C), eps) @ bf16_operand(W_post_list[q])
+        return post_mapping(z, alpha_post[q], torch.as_tensor(b_post[q], dtype=F64), k, Kq)
+
+    def res_from(a):
+        z = rms_norm(a.reshape(T, k * C), eps) @ bf16_operand(W_res)
+        return residual_mapping(z, alpha_res, torch.as_tensor(b_res, dtype=F64), k,
+                                sinkhorn_iters, clamp_delta)
+
+    a = gather_rows(X0, idx)
+    Hpost = [post_from(a, 0)]
+    Hres = None
+    X = X0.clone()
+    X_steps = []
+    tokens = torch.arange(T)
+    ar = torch.arange(T)[:, None]
+    input_scalar = None
+    for q in range(Q):
+        comps = augmented_output(F_list[q], conv_w_list[q], kappa, S, tokens, gram_schmidt_on)
+        Hp = Hpost[q]
+        wb = sum(Hp[:, :, r, None] * comps[r][:, None, :] for r in range(len(comps)))
+        if q < Q - 1:
+            a_new = a + p[:, :, None] * wb
+        else:
+            a_new = torch.einsum("tjl,tlc->tjc", Hres, a) + p[:, :, None] * wb
+        if round_state:
+            a_new = round_state_bf16(a_new)
+        X = X.clone()
+        X[ar, idx] = a_new
+        X_steps.append(X)
+        if q < Q - 1:
+            hsel = torch.gather(Hpre[q + 1], 1, idx)                    # H^pre,q+1 at I_j
+            inputs.append(bases[q + 1] + (hsel[:, :, None] * a_new).sum(1))
+            if Q == 2:
+                gamma = (hsel * p * Hp[:, :, 0]).sum(1)                # eq:read_reuse
+                input_scalar = inp_full[1] + gamma[:, None] * F_list[0].to(F64)
+            Hpost.append(post_from(a_new, q + 1))
+            if q + 1 == Q - 1:
+                Hres = res_from(a_new)
+        a = a_new
+    return dict(idx=idx, p=p, gap=gap, Hpre=Hpre, inputs=inputs, bases=bases,
+                inp_full=inp_full, Hpost=Hpost, Hres=Hres, X=X, X_steps=X_steps,
+                input_scalar_form=input_scalar, z_r=z_r)
+
+
+# --------------------------------------------------------------------------
+# backward (reverse mode of the forward above)
+# --------------------------------------------------------------------------
+
+def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in, *,
+                       m, k, Kr, S, kappa=(4, 8, 12), eps=1e-5, sinkhorn_iters=20,
+                       clamp_delta=1e-6, gram_schmidt_on=True):
+    """L = <G_X, X'> + <G_in, input> for one full xHC sublayer, float64.
+
+    Same steps as xhc_pre followed by xhc_post, except that the projection
+    weights are taken as given (already the bf16 operand values), so that a
+    finite-difference probe can perturb them.  ``al`` = (alpha_pre,
+    alpha_res, alpha_post).  Returns (L, forward results dict).
+    """
+    T, N, C = Xv.shape
+    x = Xv.reshape(T, N * C)
+    z_r = layer_norm(x, eps) @ Wr
+    Hpre = sigmoid(al[0] * (rms_norm(x, eps) @ Wp) + bp)
+    idx, _, _ = route(z_r.detach(), m, k)       # piecewise constant decision
+    s = sigmoid(z_r)
+    p = torch.ones(T, k, dtype=F64)
+    if k > m:
+        p = torch.cat([p[:, :m], torch.gather(s, 1, idx[:, m:])], dim=1)
+    a_n = rms_norm(gather_rows(Xv, idx).reshape(T, k * C), eps)
+    Hres = residual_mapping(a_n @ Wre, al[1], bre, k, sinkhorn_iters, clamp_delta)
+    Hpost = post_mapping(a_n @ Wpo, al[2], bpo, k, Kr)
+    inp = torch.einsum("tn,tnc->tc", Hpre, Xv)
+    Xn = xhc_post(Xv, Fv, cw, idx, p, Hres, Hpost, S=S, kappa=kappa,
+                  gram_schmidt_on=gram_schmidt_on)
+    L = (G_X.to(F64) * Xn).sum() + (G_in.to(F64) * inp).sum()
+    fwd = dict(idx=idx, p=p, Hpre=Hpre, Hres=Hres, Hpost=Hpost, input=inp, X_new=Xn)
+    return L, fwd
+
+
+GRAD_NAMES = ("X", "F", "W_r", "W_pre", "W_res", "W_post", "alpha", "b_pre", "b_res",
+              "b_post", "conv_w")
+
+
+def xhc_sublayer_grads(X, F, conv_w, W_r, W_pre, W_res, W_post, alpha, b_pre, b_res,
+                       b_post, G_X, G_in, **kw):
+    """Gradients of sublayer_objective with respect to every input.
+
+    The sublayer output F stands in as an independent input.  The routing
+    decision is piecewise constant, so gradients reach the router only
+    through p of the routed slots (Sec. "Infrastructure Design").  Weights
+    enter as their bf16 operand values and their gradients are taken with
+    respect to those values.  The derivative is the plain definition
+    (reverse mode of the forward); the tests pin it by central finite
+    differences.  Returns a dict of float64 gradients keyed by GRAD_NAMES
+    (conv_w is None for K_r = 1) plus the forward results and the loss.
+    """
+    leaf = lambda t: torch.as_tensor(t).detach().to(F64).clone().requires_grad_(True)
+    vals = [leaf(X), leaf(F), leaf(conv_w) if conv_w is not None else None,
+            leaf(bf16_operand(W_r)), leaf(bf16_operand(W_pre)),
+            leaf(bf16_operand(W_res)), leaf(bf16_operand(W_post)),
+            leaf(alpha), leaf(b_pre), leaf(b_res), leaf(b_post)]
+    L, fwd = sublayer_objective(*vals, G_X, G_in, **kw)
+    order = [0, 1, 3, 4, 5, 6, 7, 8, 9, 10] + ([2] if conv_w is not None else [])
+    leaves = [vals[i] for i in order]
+    grads = torch.autograd.grad(L, leaves, allow_unused=True)
+    # an input the loss does not reach (W_r when every slot is fixed) has zero gradient
+    grads = [torch.zeros_like(v) if gr is None else gr for gr, v in zip(grads, leaves)]
+    out = dict(zip(GRAD_NAMES, grads))
+    if conv_w is None:
+        out["conv_w"] = None
+    out.update({k_: (v.detach() if torch.is_tensor(v) else v) for k_, v in fwd.items()})
+    out["loss"] = L.detach()
+    return out

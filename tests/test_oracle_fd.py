@@ -1,0 +1,76 @@
+"""Central finite differences pin the oracle's backward (reverse mode of the forward)."""
+
+import pytest
+import torch
+
+from oracle import xhc_oracle as O
+from paper_2607_14530_amd import synth
+
+F64 = torch.float64
+
+
+def _setup(N, Kr, stress, seed):
+    w = synth.Workload(T=8, S=8, N=N, k=4, m=2, C=32, Kr=Kr,
+                       alpha=(0.5, 1.0, 0.5) if stress else (0.01, 0.01, 0.01))
+    d = synth.sublayer_inputs(w, seed, grads=True, bias_std=2.0 if stress else 0.0)
+    vals = {
+        "X": d["X"].to(F64), "F": d["F"].to(F64),
+        "conv_w": d["conv_w"].to(F64) if d["conv_w"] is not None else None,
+        "W_r": O.bf16_operand(d["W_r"]), "W_pre": O.bf16_operand(d["W_pre"]),
+        "W_res": O.bf16_operand(d["W_res"]), "W_post": O.bf16_operand(d["W_post"]),
+        "alpha": d["alpha"].to(F64), "b_pre": d["b_pre"].to(F64),
+        "b_res": d["b_res"].to(F64), "b_post": d["b_post"].to(F64),
+    }
+    return w, d, vals
+
+
+def _objective(w, d, vals):
+    return O.sublayer_objective(
+        vals["X"], vals["F"], vals["conv_w"], vals["W_r"], vals["W_pre"], vals["W_res"],
+        vals["W_post"], vals["alpha"], vals["b_pre"], vals["b_res"], vals["b_post"],
+        d["G_X"], d["G_in"], m=w.m, k=w.k, Kr=w.Kr, S=w.S)
+
+
+@pytest.mark.parametrize("N,Kr,stress,seed", [(4, 4, False, 0), (8, 4, False, 1),
+                                               (8, 1, False, 2), (8, 4, True, 3)])
+def test_backward_matches_central_differences(N, Kr, stress, seed):
+    w, d, vals = _setup(N, Kr, stress, seed)
+    g = O.xhc_sublayer_grads(d["X"], d["F"], d["conv_w"], d["W_r"], d["W_pre"], d["W_res"],
+                             d["W_post"], d["alpha"], d["b_pre"], d["b_res"], d["b_post"],
+                             d["G_X"], d["G_in"], m=w.m, k=w.k, Kr=w.Kr, S=w.S)
+    gen = torch.Generator().manual_seed(100 + seed)
+    for name in O.GRAD_NAMES:
+        if vals[name] is None:
+            continue
+        base = vals[name]
+        direction = torch.randn(base.shape, generator=gen, dtype=F64)
+        h = 1e-6 * max(1.0, base.abs().max().item())
+        plus = dict(vals, **{name: base + h * direction})
+        minus = dict(vals, **{name: base - h * direction})
+        Lp, fp = _objective(w, d, plus)
+        Lm, fm = _objective(w, d, minus)
+        # the piecewise-constant routing decision must not flip inside the probe
+        assert torch.equal(fp["idx"], fm["idx"]), name
+        fd = ((Lp - Lm) / (2 * h)).item()
+        an = (g[name] * direction).sum().item()
+        assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (name, fd, an)
+
+
+def test_backward_routes_gradient_only_through_selected_logits():
+    """W_r receives gradient only via p of routed slots: with m = k there is none."""
+    w = synth.Workload(T=8, S=8, N=6, k=4, m=4, C=16, Kr=1)
+    d = synth.sublayer_inputs(w, 9, grads=True)
+    g = O.xhc_sublayer_grads(d["X"], d["F"], None, d["W_r"], d["W_pre"], d["W_res"],
+                             d["W_post"], d["alpha"], d["b_pre"], d["b_res"], d["b_post"],
+                             d["G_X"], d["G_in"], m=w.m, k=w.k, Kr=w.Kr, S=w.S)
+    assert torch.equal(g["W_r"], torch.zeros_like(g["W_r"]))
+
+
+def test_stress_case_exercises_the_row_clamp():
+    """The stressed finite-difference case must actually take the clamp branch."""
+    w, d, vals = _setup(8, 4, True, 3)
+    _, f = _objective(w, d, vals)
+    a_n = O.rms_norm(O.gather_rows(vals["X"], f["idx"]).reshape(w.T, -1), 1e-5)
+    logits = vals["alpha"][1] * (a_n @ vals["W_res"]) + vals["b_res"]
+    raw = O.sinkhorn(torch.exp(logits).reshape(w.T, w.k, w.k), 20)
+    assert (raw.sum(-1) > 1 + 1e-6).any()

@@ -1,0 +1,372 @@
+"""Pins of the float64 oracle against things other than itself.
+
+Each test ties one part of the oracle to a closed form the paper prints, a
+special case that reduces to a textbook formula or a library routine, an
+invariant, or brute force on tiny inputs, so that a dropped term, a wrong
+sign or index, or a transposed operand fails at least one of them.
+"""
+
+import itertools
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import xhc_oracle as O
+from paper_2607_14530_amd import synth
+
+F64 = torch.float64
+
+
+def _inputs(T=16, N=4, k=4, m=2, C=32, Kr=1, seed=0, S=0, alpha=(0.01, 0.01, 0.01), bias_std=0.0):
+    w = synth.Workload(T=T, N=N, k=k, m=m, C=C, Kr=Kr, S=S, alpha=alpha)
+    d = synth.sublayer_inputs(w, seed, bias_std=bias_std)
+    return w, d
+
+
+def _pre(w, d, **kw):
+    return O.xhc_pre(d["X"].to(F64), d["W_r"], d["W_pre"], d["W_res"], d["W_post"],
+                     tuple(d["alpha"].tolist()), d["b_pre"], d["b_res"], d["b_post"],
+                     m=w.m, k=w.k, Kr=w.Kr, **kw)
+
+
+# --------------------------------------------------------------- projection
+
+def test_fused_normalised_projection_identity():
+    """eq:fused_normalized_projection: project raw x, then correct with mu, nu."""
+    w, d = _inputs(T=24, N=8, k=4, C=64)
+    r = _pre(w, d)
+    x = d["X"].to(F64).reshape(w.T, -1)
+    eps = 1e-5
+    mu = x.mean(1, keepdim=True)
+    nu = (x * x).mean(1, keepdim=True)
+    Wr = O.bf16_operand(d["W_r"])
+    Wp = O.bf16_operand(d["W_pre"])
+    zr = (x @ Wr - mu * Wr.sum(0, keepdim=True)) / torch.sqrt(nu - mu * mu + eps)
+    zp = (x @ Wp) / torch.sqrt(nu + eps)
+    assert torch.allclose(r["z_r"], zr, rtol=0, atol=1e-11)
+    assert torch.allclose(r["z_pre"], zp, rtol=0, atol=1e-11)
+
+
+def test_bf16_operand_rounding_is_nearest_even():
+    # 1 + 2^-8 lies halfway between bf16 neighbours 1 and 1 + 2^-7: ties to even (1.0).
+    v = torch.tensor([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -1.0 - 2 ** -9, 0.02], dtype=torch.float32)
+    r = O.bf16_operand(v)
+    assert r[0].item() == 1.0
+    assert r[1].item() == 1.0 + 2 ** -6          # tie rounds to the even mantissa
+    assert r[2].item() == -1.0
+    assert abs(r[3].item() - 0.02) <= 0.02 * 2 ** -8
+
+
+# --------------------------------------------------------------- special cases
+
+def test_k_equals_N_reduces_to_dense_mhc():
+    """k = m = N, K_r = 1: xHC equals the separately written dense mHC (eq:hc + eq:mhc_sinkhorn)."""
+    w, d = _inputs(T=12, N=4, k=4, m=4, C=48, Kr=1, alpha=(0.3, 0.7, 0.5), bias_std=0.5)
+    r = _pre(w, d)
+    assert torch.equal(r["idx"], torch.arange(4).expand(12, 4))
+    assert torch.equal(r["p"], torch.ones(12, 4, dtype=F64))
+    X = d["X"].to(F64)
+    Xn = O.xhc_post(X, d["F"], None, r["idx"], r["p"], r["Hres"], r["Hpost"], S=w.S)
+    inp, Xm, Hpre, Hpost, Hres = O.mhc_dense(
+        X, d["F"], d["W_pre"], d["W_post"], d["W_res"], tuple(d["alpha"].tolist()),
+        d["b_pre"], d["b_post"], d["b_res"])
+    assert torch.allclose(r["input"], inp, rtol=0, atol=1e-12)
+    assert torch.allclose(r["Hpre"], Hpre, rtol=0, atol=1e-13)
+    assert torch.allclose(r["Hpost"][:, :, 0], Hpost, rtol=0, atol=1e-13)
+    assert torch.allclose(r["Hres"], Hres, rtol=0, atol=1e-13)
+    assert torch.allclose(Xn, Xm, rtol=0, atol=1e-12)
+
+
+def test_single_stream_identity_reduces_to_plain_residual():
+    """N = k = m = 1, pre = 1, post = 1: input = x and X' = x + F (eq:hc with N = 1)."""
+    w, d = _inputs(T=32, N=1, k=1, m=1, C=64, alpha=(0.0, 0.01, 0.0))
+    d["b_pre"][:] = 40.0      # sigma(40) is 1 in float64
+    r = _pre(w, d)
+    X = d["X"].to(F64)
+    assert torch.equal(r["input"], X[:, 0])
+    assert torch.equal(r["Hres"], torch.ones(32, 1, 1, dtype=F64))
+    assert torch.equal(r["Hpost"], torch.ones(32, 1, 1, dtype=F64))
+    Xn = O.xhc_post(X, d["F"], None, r["idx"], r["p"], r["Hres"], r["Hpost"], S=w.S)
+    ref = X[:, 0] + d["F"].to(F64)
+    assert torch.equal(Xn[:, 0], ref)
+    # one rounding to bf16 gives the same bits as rounding the exact sum
+    assert torch.equal(O.round_state_bf16(Xn[:, 0]).to(torch.bfloat16),
+                       ref.to(torch.bfloat16))
+
+
+# --------------------------------------------------------------- routing
+
+def _brute_route(z, m, k):
+    """Best (k-m)-subset of streams >= m by total logit, then sorted descending,
+    lower index first on ties.  Brute force over every subset."""
+    N = len(z)
+    cands = list(range(m, N))
+    best = None
+    for sub in itertools.combinations(cands, k - m):
+        key = (sum(z[i] for i in sub), [-i for i in sorted(sub)])
+        if best is None or key > best[0]:
+            best = (key, sub)
+    sub = sorted(best[1], key=lambda i: (-z[i], i))
+    return list(range(m)) + sub
+
+
+@pytest.mark.parametrize("N,k,m", [(4, 2, 1), (5, 3, 1), (6, 4, 2), (6, 3, 0), (4, 4, 2)])
+def test_route_matches_brute_force(N, k, m):
+    g = torch.Generator().manual_seed(N * 100 + k * 10 + m)
+    z = torch.randn(200, N, generator=g, dtype=F64)
+    idx, p, gap = O.route(z, m, k)
+    for t in range(z.shape[0]):
+        ref = _brute_route(z[t].tolist(), m, k)
+        assert idx[t].tolist() == ref
+        for j in range(k):
+            if j < m:
+                assert p[t, j].item() == 1.0
+            else:
+                assert p[t, j].item() == pytest.approx(1 / (1 + math.exp(-z[t, ref[j]].item())), abs=1e-15)
+
+
+def test_route_ties_prefer_lower_index():
+    z = torch.tensor([[5.0, 5.0, 1.0, 3.0, 3.0, 3.0, 0.0]], dtype=F64)
+    idx, _, gap = O.route(z, 2, 5)
+    assert idx[0].tolist() == [0, 1, 3, 4, 5]
+    assert gap[0].item() == 0.0
+    for t in range(20):  # integer logits with many ties against the brute force
+        zz = torch.randint(0, 3, (1, 6), generator=torch.Generator().manual_seed(t)).to(F64)
+        assert O.route(zz, 1, 4)[0][0].tolist() == _brute_route(zz[0].tolist(), 1, 4)
+
+
+def test_zero_router_weights_route_to_first_streams():
+    w, d = _inputs(T=8, N=8, k=4, m=2, C=32)
+    d["W_r"].zero_()
+    r = _pre(w, d)
+    assert torch.equal(r["idx"], torch.tensor([0, 1, 2, 3]).expand(8, 4))
+    assert torch.allclose(r["p"][:, 2:], torch.full((8, 2), 0.5, dtype=F64), atol=0)
+
+
+def test_all_streams_active_when_k_equals_N():
+    w, d = _inputs(T=8, N=6, k=6, m=2, C=32)
+    r = _pre(w, d)
+    for t in range(8):
+        assert sorted(r["idx"][t].tolist()) == list(range(6))
+
+
+# --------------------------------------------------------------- Sinkhorn + clamp
+
+def test_sinkhorn_doubly_stochastic_at_default_gating():
+    w, d = _inputs(T=64, N=8, k=4, m=2, C=64)
+    r = _pre(w, d)
+    H = r["Hres"]
+    assert (H.sum(-1) - 1).abs().max() < 1e-6
+    assert (H.sum(-2) - 1).abs().max() < 1e-6
+    assert (H > 0).all()
+
+
+def test_sinkhorn_closed_form_2x2():
+    """For a positive 2x2 matrix the Sinkhorn limit is [[x,1-x],[1-x,x]] with
+    x / (1 - x) = sqrt(ad / bc) (the cross ratio is invariant under diagonal scaling)."""
+    g = torch.Generator().manual_seed(3)
+    M = torch.exp(torch.randn(50, 2, 2, generator=g, dtype=F64) * 0.5)
+    H = O.sinkhorn(M, 200)
+    a, b, c, dd = M[:, 0, 0], M[:, 0, 1], M[:, 1, 0], M[:, 1, 1]
+    x = torch.sqrt(a * dd) / (torch.sqrt(a * dd) + torch.sqrt(b * c))
+    assert torch.allclose(H[:, 0, 0], x, atol=1e-12)
+    assert torch.allclose(H[:, 0, 1], 1 - x, atol=1e-12)
+
+
+def test_sinkhorn_rows_first_is_invariant_to_row_scaling():
+    """Rows are normalised first, so scaling rows of exp(.) changes nothing;
+    column scaling does change the 20-step result (pins the order)."""
+    g = torch.Generator().manual_seed(5)
+    M = torch.exp(torch.randn(20, 4, 4, generator=g, dtype=F64) * 2.0)
+    D = torch.exp(torch.randn(20, 4, 1, generator=g, dtype=F64))
+    assert torch.allclose(O.sinkhorn(M, 20), O.sinkhorn(M * D, 20), atol=1e-14, rtol=0)
+    Dc = torch.exp(torch.randn(20, 1, 4, generator=g, dtype=F64) * 2.0)
+    assert not torch.allclose(O.sinkhorn(M, 3), O.sinkhorn(M * Dc, 3), atol=1e-6)
+
+
+def test_sinkhorn_special_cases():
+    one = O.residual_mapping(torch.randn(5, 1, dtype=F64), 1.0, torch.zeros(1, dtype=F64), 1, 20, 1e-6)
+    assert torch.equal(one, torch.ones(5, 1, 1, dtype=F64))
+    const = O.residual_mapping(torch.full((3, 16), 2.5, dtype=F64), 0.7, torch.zeros(16, dtype=F64), 4, 20, 1e-6)
+    assert torch.allclose(const, torch.full((3, 4, 4), 0.25, dtype=F64), atol=1e-16, rtol=0)
+    # near-uniform input: 20 iterations already sit at the limit (Sinkhorn's theorem)
+    g = torch.Generator().manual_seed(9)
+    M = torch.exp(0.01 * torch.randn(10, 4, 4, generator=g, dtype=F64))
+    assert torch.allclose(O.sinkhorn(M, 20), O.sinkhorn(M, 1000), atol=1e-14, rtol=0)
+
+
+def test_row_clamp_only_shrinks_rows_above_one():
+    g = torch.Generator().manual_seed(11)
+    # extreme logits: 20 iterations do not converge, some row sums exceed one
+    z = torch.randn(400, 16, generator=g, dtype=F64) * 6.0
+    H = O.residual_mapping(z, 1.0, torch.zeros(16, dtype=F64), 4, 20, 1e-6)
+    raw = O.sinkhorn(torch.exp(z).reshape(400, 4, 4), 20)
+    s = raw.sum(-1)
+    assert (s > 1 + 1e-6).any(), "stress case should leave some rows above one"
+    assert (H.sum(-1) <= 1 + 1e-6 + 1e-15).all()
+    keep = s <= 1 + 1e-6
+    assert torch.equal(H[keep], raw[keep])
+    assert torch.allclose(H[~keep], raw[~keep] / s[~keep][:, None], atol=0, rtol=1e-15)
+    # delta = 0 is the literal H / max(s, 1)
+    H0 = O.row_clamp(raw, 0.0)
+    assert torch.allclose(H0, raw / torch.clamp(s, min=1.0)[..., None], atol=0, rtol=1e-15)
+
+
+# --------------------------------------------------------------- temporal augmentation
+
+def test_conv_impulse_response_and_sequence_boundary():
+    T, S, C = 40, 20, 8
+    kappa = (4, 8, 12)
+    g = torch.Generator().manual_seed(2)
+    w = torch.randn(sum(kappa), C, generator=g, dtype=torch.float32)
+    for t0 in (0, 5, 17, 19, 25):
+        F = torch.zeros(T, C, dtype=F64)
+        F[t0] = 1.0
+        gs = O.temporal_branches(F, w, kappa, S, torch.arange(T))
+        row = 0
+        for j, kap in enumerate(kappa):
+            for t in range(T):
+                same_seq = (t // S) == (t0 // S)
+                if same_seq and t0 <= t < t0 + kap:
+                    exp = w[row + t - t0].to(F64)
+                else:
+                    exp = torch.zeros(C, dtype=F64)
+                assert torch.equal(gs[j][t], exp), (t0, j, t)
+            row += kap
+
+
+def test_conv_matches_library_conv1d():
+    """Per-sequence causal depthwise conv == torch conv1d (groups = C) with left padding."""
+    T, S, C = 48, 16, 6
+    kappa = (4, 8, 12)
+    g = torch.Generator().manual_seed(4)
+    F = torch.randn(T, C, generator=g, dtype=F64)
+    w = torch.randn(sum(kappa), C, generator=g, dtype=torch.float32)
+    gs = O.temporal_branches(F, w, kappa, S, torch.arange(T))
+    row = 0
+    for j, kap in enumerate(kappa):
+        # conv1d computes cross-correlation: out[t] = sum_u ker[u] in[t+u]; causal
+        # tap i multiplies in[t - i], so the kernel is flipped.
+        ker = w[row:row + kap].to(F64).flip(0).t().unsqueeze(1)          # [C, 1, kap]
+        for b in range(T // S):
+            seq = F[b * S:(b + 1) * S].t().unsqueeze(0)                   # [1, C, S]
+            ref = torch.nn.functional.conv1d(torch.nn.functional.pad(seq, (kap - 1, 0)), ker, groups=C)
+            assert torch.allclose(gs[j][b * S:(b + 1) * S], ref[0].t(), atol=1e-12, rtol=0)
+        row += kap
+
+
+def test_gram_schmidt_matches_qr_and_is_orthogonal():
+    g = torch.Generator().manual_seed(6)
+    comps = [torch.randn(10, 64, generator=g, dtype=F64) for _ in range(4)]
+    comps[2] = comps[2] + 0.9 * comps[0]           # strongly correlated branches
+    v = O.gram_schmidt(comps)
+    assert torch.equal(v[0], comps[0])
+    for a in range(4):
+        for b in range(a):
+            cos = (v[a] * v[b]).sum(-1) / (v[a].norm(dim=-1) * v[b].norm(dim=-1))
+            assert cos.abs().max() < 1e-12
+    # library pin: Q R of [out, g1, g2, g3] gives v_i = q_i * r_ii
+    for t in range(10):
+        A = np.stack([c[t].numpy() for c in comps], axis=1)
+        q, r = np.linalg.qr(A)
+        for i in range(4):
+            assert np.allclose(v[i][t].numpy(), q[:, i] * r[i, i], atol=1e-11)
+
+
+def test_gram_schmidt_degenerate_components():
+    g = torch.Generator().manual_seed(7)
+    out = torch.randn(3, 32, generator=g, dtype=F64)
+    v = O.gram_schmidt([out, 2.5 * out, torch.zeros(3, 32, dtype=F64), out + 1.0])
+    assert v[1].abs().max() < 1e-12            # collinear branch vanishes
+    assert torch.equal(v[2], torch.zeros(3, 32, dtype=F64))
+    zero = O.gram_schmidt([torch.zeros(2, 8, dtype=F64), torch.ones(2, 8, dtype=F64)])
+    assert torch.equal(zero[1], torch.ones(2, 8, dtype=F64))     # zero-norm v_1: coefficient 0
+
+
+# --------------------------------------------------------------- write-back
+
+def test_post_leaves_inactive_rows_bit_identical_and_gates_only_writeback():
+    w, d = _inputs(T=20, N=8, k=4, m=2, C=32, Kr=4, S=10)
+    r = _pre(w, d)
+    X = d["X"].to(F64)
+    Xn = O.xhc_post(X, d["F"], d["conv_w"], r["idx"], r["p"], r["Hres"], r["Hpost"], S=w.S)
+    act = torch.zeros(20, 8, dtype=torch.bool)
+    act[torch.arange(20)[:, None], r["idx"]] = True
+    assert torch.equal(Xn[~act], X[~act])
+    assert not torch.equal(Xn[act], X[act])
+    # H^post = 0: the update is the residual mixing alone, whatever p is
+    Xz = O.xhc_post(X, d["F"], d["conv_w"], r["idx"], r["p"] * 7.0, r["Hres"], 0 * r["Hpost"], S=w.S)
+    mixed = torch.einsum("tjl,tlc->tjc", r["Hres"], O.gather_rows(X, r["idx"]))
+    assert torch.allclose(O.gather_rows(Xz, r["idx"]), mixed, atol=1e-14, rtol=0)
+
+
+def test_post_attention_closed_form():
+    """K_r = 1, H^res = I: x_{I_j} + p_j h_j out (eq:sparse_write with one component)."""
+    w, d = _inputs(T=10, N=6, k=3, m=1, C=16)
+    r = _pre(w, d)
+    X = d["X"].to(F64)
+    eye = torch.eye(3, dtype=F64).expand(10, 3, 3)
+    Xn = O.xhc_post(X, d["F"], None, r["idx"], r["p"], eye, r["Hpost"], S=w.S)
+    F = d["F"].to(F64)
+    for t in range(10):
+        for j in range(3):
+            i = r["idx"][t, j]
+            ref = X[t, i] + r["p"][t, j] * r["Hpost"][t, j, 0] * F[t]
+            assert torch.allclose(Xn[t, i], ref, atol=1e-14, rtol=0)
+
+
+# --------------------------------------------------------------- xHC-Flash
+
+def _flash(Q, round_state, seed=1, T=24, N=8, k=4, m=2, C=32, S=12):
+    w = synth.Workload(T=T, N=N, k=k, m=m, C=C, S=S)
+    d = synth.flash_inputs(w, Q, seed)
+    out = O.xhc_flash_group(
+        d["X"].to(F64), d["F_list"], d["W_r"], d["W_pre_list"], d["W_post_list"], d["W_res"],
+        d["conv_w_list"], d["alpha_pre"], d["b_pre"], d["alpha_post"], d["b_post"],
+        d["alpha_res"], d["b_res"], m=m, k=k, S=S, round_state=round_state)
+    return w, d, out
+
+
+@pytest.mark.parametrize("Q", [2, 4])
+def test_flash_correction_equals_direct_dense_read(Q):
+    """App. E: the active-state correction recovers the dense read of the updated state."""
+    w, d, out = _flash(Q, round_state=False)
+    for q in range(1, Q):
+        direct = torch.einsum("tn,tnc->tc", out["Hpre"][q], out["X_steps"][q - 1])
+        assert torch.allclose(out["inputs"][q], direct, atol=1e-12, rtol=0)
+    assert torch.allclose(out["inputs"][0], out["inp_full"][0], atol=0, rtol=0)
+
+
+def test_flash_two_sublayer_scalar_form():
+    """eq:read_reuse: inp_M + gamma * out_A equals the active-state form."""
+    w, d, out = _flash(2, round_state=False)
+    assert torch.allclose(out["input_scalar_form"], out["inputs"][1], atol=1e-12, rtol=0)
+    w, d, out = _flash(2, round_state=True)
+    assert torch.allclose(out["input_scalar_form"], out["inputs"][1], atol=5e-2, rtol=0)
+
+
+@pytest.mark.parametrize("Q", [2, 4])
+def test_flash_steps_match_full_post(Q):
+    """Intermediate sublayers are xhc_post with H^res = I; the last uses H^res."""
+    w, d, out = _flash(Q, round_state=False)
+    T, k = w.T, w.k
+    eye = torch.eye(k, dtype=F64).expand(T, k, k)
+    prev = d["X"].to(F64)
+    for q in range(Q):
+        H = out["Hres"] if q == Q - 1 else eye
+        ref = O.xhc_post(prev, d["F_list"][q], d["conv_w_list"][q], out["idx"], out["p"], H,
+                         out["Hpost"][q], S=w.S)
+        assert torch.allclose(out["X_steps"][q], ref, atol=1e-13, rtol=0)
+        prev = out["X_steps"][q]
+    # routing is decided once, on the entry state, exactly as the full pre does
+    r = O.route(out["z_r"], w.m, w.k)[0]
+    assert torch.equal(r, out["idx"])
+
+
+def test_flash_untouched_rows_are_never_written():
+    w, d, out = _flash(4, round_state=True)
+    act = torch.zeros(w.T, w.N, dtype=torch.bool)
+    act[torch.arange(w.T)[:, None], out["idx"]] = True
+    assert torch.equal(out["X"][~act], d["X"].to(F64)[~act])
