@@ -1,0 +1,134 @@
+/*
+ * xhc.h - C ABI of the MI355X (gfx950) implementation of the xHC per-sublayer
+ * residual-stream connection (xHC: Expanded Hyper-Connections, arXiv
+ * 2607.14530), in its full xHC and xHC-Flash forms.
+ *
+ * Notation follows the paper: T tokens (token t = b*S + s, S tokens per
+ * sequence), N residual streams of width C, k active streams of which m are
+ * fixed, K_r write-back components (1 for attention-type sublayers, 1 + r for
+ * MLP-type sublayers with r causal depthwise convolutions), Q sublayers per
+ * xHC-Flash sharing group.
+ *
+ * Conventions for every entry point:
+ *  - All tensor pointers are DEVICE pointers owned by the caller; the library
+ *    never allocates or frees memory inside a call.  `workspace` is caller
+ *    device memory of at least xhc_workspace_bytes() bytes; its contents on
+ *    entry are ignored and on return are unspecified.
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).  Calls
+ *    are asynchronous on that stream and enqueue device work only.
+ *  - Layouts are row-major and contiguous: X [T,N,C]; F, input [T,C];
+ *    idx [T,k] int32; p [T,k]; Hpre [T,N]; Hres [T,k,k]; Hpost [T,k,K].
+ *    The state X and the tensors F, input and base use `state_dtype`
+ *    (bf16 or fp32); coefficients are fp32.
+ *  - Slot order of idx (reading of eq:router_topk): slots 0..m-1 hold the
+ *    fixed streams 0..m-1 with p = 1; slots m..k-1 hold the routed streams in
+ *    descending router logit, ties to the lower stream index.
+ *  - Errors: arguments are validated before any device work is enqueued, so
+ *    an error return leaves every output untouched.  XHC_EINVAL: violated
+ *    constraint or NULL required pointer; XHC_EUNSUPPORTED: valid shape this
+ *    library does not implement; XHC_EWORKSPACE: workspace too small;
+ *    XHC_EHIP: a HIP launch failed (outputs unspecified).
+ *  - Thread safety: the library holds no mutable global state; calls on
+ *    different streams may overlap provided their buffers do not.
+ */
+#ifndef XHC_H_
+#define XHC_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  XHC_OK = 0,
+  XHC_EINVAL = 1,
+  XHC_EUNSUPPORTED = 2,
+  XHC_EWORKSPACE = 3,
+  XHC_EHIP = 4
+} xhc_status;
+
+typedef enum { XHC_BF16 = 0, XHC_F32 = 1 } xhc_dtype;
+
+/* Shape and hyperparameters of one sublayer connection (Sec. "Parameterization
+ * Details" and the hyperparameter table: N = 16, k = 4, m = 2, r = 3,
+ * kappa = {4, 8, 12}, 20 Sinkhorn iterations).  Constraints:
+ *   T >= 0, S >= 1, T % S == 0;  1 <= k <= N <= 64;  0 <= m <= k;  k <= 8;
+ *   C >= 32, C % 32 == 0;  Kr in 1..4;  kappa[j] in 1..16 for j < Kr - 1;
+ *   sinkhorn_iters in 0..1000;  eps > 0;  clamp_delta >= 0.               */
+typedef struct xhc_dims {
+  int64_t T;              /* tokens                                              */
+  int64_t S;              /* tokens per sequence (causal conv window resets)     */
+  int32_t N;              /* residual streams                                    */
+  int32_t k;              /* active streams                                      */
+  int32_t m;              /* fixed (always active) streams                       */
+  int32_t C;              /* width                                               */
+  int32_t Kr;             /* write-back components of an MLP-type sublayer       */
+  int32_t kappa[3];       /* conv kernel sizes of the Kr - 1 branches            */
+  int32_t sinkhorn_iters; /* Sinkhorn iterations (row then column normalisation) */
+  int32_t gram_schmidt;   /* 1: orthogonalise the components (eq:gs); 0: skip    */
+  float eps;              /* epsilon of the LayerNorm / RMSNorm statistics       */
+  float clamp_delta;      /* row clamp applies when a row sum exceeds 1 + delta  */
+  int32_t state_dtype;    /* xhc_dtype of X, F, input, base                      */
+} xhc_dims;
+
+/* ------------------------------------------------------------------ packing
+ * Projection operands are bf16 (Sec. "Infrastructure Design"): the packers
+ * round fp32 weights to bf16 (nearest even) into an opaque device layout used
+ * by the projection kernels.  Sizes come from the *_bytes queries.
+ *
+ * Full-state projection (eq:fused_normalized_projection): columns are
+ * [W_r | W_pre,1 | ... | W_pre,npre], W_r and each W_pre [N*C, N] fp32 with
+ * row index i*C + c (stream-major flatten).  Full xHC uses npre = 1;
+ * xHC-Flash uses npre = Q.  W_pre points at npre contiguous matrices.
+ * Also stores the column sums of bf16(W_r) used by the LayerNorm correction.
+ *
+ * Active projection (Sec. "Infrastructure Design", [W^post, W^res]): columns
+ * [W_post | W_res], W_post [k*C, k*Kq] and W_res [k*C, k*k] (may be NULL when
+ * the sublayer has no residual mixing), row index j*C + c (slot-major vec).  */
+size_t xhc_packed_full_bytes(const xhc_dims* d, int32_t npre);
+size_t xhc_packed_active_bytes(const xhc_dims* d, int32_t Kq, int32_t with_res);
+xhc_status xhc_pack_full(const xhc_dims* d, int32_t npre, const float* W_r, const float* W_pre,
+                         void* packed, void* stream);
+xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, const float* W_res,
+                           void* packed, void* stream);
+
+/* Workspace needed by an entry point (op: one of the XHC_OP_* values).        */
+enum { XHC_OP_PRE = 0, XHC_OP_POST = 1, XHC_OP_FLASH_PRE = 2, XHC_OP_FLASH_POST = 3 };
+size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q);
+
+/* ------------------------------------------------------------------ full xHC
+ * xhc_pre - mapping generation and dense read of one xHC sublayer
+ * (Alg. "Forward pass of one xHC sublayer", routing / mapping-generation / dense
+ * read steps; eq:router, eq:router_topk, eq:param_pre, eq:dense_read,
+ * eq:param_res, eq:param_post, row clamp of App. A).
+ *   X          [T,N,C] state (read only)
+ *   packed_full  xhc_pack_full(npre = 1) of W_r, W_pre
+ *   packed_act   xhc_pack_active(Kq = d->Kr, with_res = 1) of W_post, W_res
+ *   alpha      [3] fp32 device: alpha_pre, alpha_res, alpha_post
+ *   b_pre [N], b_res [k*k], b_post [k*Kr] fp32 device
+ * Outputs: input [T,C] (state dtype), idx [T,k], p [T,k], Hpre [T,N],
+ * Hres [T,k,k], Hpost [T,k,Kr].  Uses d->Kr as this sublayer's K_r.          */
+xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, const void* packed_act,
+                   const float* alpha, const float* b_pre, const float* b_res, const float* b_post,
+                   void* input, int32_t* idx, float* p, float* Hpre, float* Hres, float* Hpost,
+                   void* workspace, size_t workspace_bytes, void* stream);
+
+/* xhc_post - sparse write-back of one xHC sublayer (eq:aug, eq:gs,
+ * eq:sparse_write_delta, eq:sparse_write; Alg. "Forward pass of one xHC
+ * sublayer", write-back and scatter steps).
+ *   X       [T,N,C] in/out: only rows X[t, idx[t,j], :] are written, each to
+ *           sum_l Hres[t,j,l] X[t,idx[t,l],:] + p[t,j] sum_r Hpost[t,j,r] v_r[t]
+ *   F       [T,C] sublayer output (must not alias X)
+ *   conv_w  [sum_{j<Kr-1} kappa[j], C] fp32 (branch kernels stacked, row i of
+ *           branch j multiplies F[t-i]); NULL iff d->Kr == 1
+ *   idx, p, Hres, Hpost as produced by xhc_pre.                               */
+xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv_w,
+                    const int32_t* idx, const float* p, const float* Hres, const float* Hpost,
+                    void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* XHC_H_ */

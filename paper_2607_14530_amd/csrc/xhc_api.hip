@@ -1,0 +1,168 @@
+// C ABI of the xHC library: argument validation, workspace sizing, dispatch.
+// Every check happens before the first launch, so an error return leaves
+// all outputs untouched.
+#include <hip/hip_runtime.h>
+
+#include "xhc.h"
+#include "xhc_launch.h"
+
+using namespace xhc;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// shape constraints shared by every entry point (see xhc_dims in xhc.h)
+xhc_status check_dims(const xhc_dims* d) {
+  if (!d) return XHC_EINVAL;
+  if (d->T < 0 || d->S < 1 || (d->T % d->S) != 0) return XHC_EINVAL;
+  if (d->N < 1 || d->k < 1 || d->k > d->N || d->m < 0 || d->m > d->k) return XHC_EINVAL;
+  if (d->C < 1 || d->Kr < 1 || d->sinkhorn_iters < 0 || !(d->eps > 0.f) || !(d->clamp_delta >= 0.f))
+    return XHC_EINVAL;
+  if (d->state_dtype != XHC_BF16 && d->state_dtype != XHC_F32) return XHC_EINVAL;
+  if (d->N > kMaxN || d->k > kMaxK || d->Kr > kMaxKr || d->sinkhorn_iters > 1000) return XHC_EUNSUPPORTED;
+  if (d->C % 32 != 0) return XHC_EUNSUPPORTED;
+  for (int j = 0; j < d->Kr - 1; ++j)
+    if (d->kappa[j] < 1 || d->kappa[j] > 16) return XHC_EUNSUPPORTED;
+  return XHC_OK;
+}
+
+xhc_status hip_status(hipError_t e) { return e == hipSuccess ? XHC_OK : XHC_EHIP; }
+
+int64_t NC_of(const xhc_dims* d) { return (int64_t)d->N * d->C; }
+int64_t kC_of(const xhc_dims* d) { return (int64_t)d->k * d->C; }
+int64_t act_outs(const xhc_dims* d, int Kq, int with_res) { return (int64_t)d->k * Kq + (with_res ? d->k * d->k : 0); }
+
+size_t part_bytes(int64_t K, int64_t nout, int64_t T) {
+  return align_up((size_t)proj_chunks(K) * (size_t)(out_blocks(nout) * 16 + 2) * (size_t)T * sizeof(float));
+}
+
+size_t pre_ws(const xhc_dims* d) {
+  const size_t full = part_bytes(NC_of(d), 2 * d->N, d->T);
+  const size_t act = part_bytes(kC_of(d), act_outs(d, d->Kr, 1), d->T);
+  return full > act ? full : act;
+}
+
+size_t post_ws(const xhc_dims* d) {
+  if (d->Kr == 1) return 0;
+  const int np = d->Kr * (d->Kr + 1) / 2;
+  return align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)) +
+         align_up((size_t)d->T * d->k * d->Kr * sizeof(float));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t xhc_packed_full_bytes(const xhc_dims* d, int32_t npre) {
+  if (check_dims(d) != XHC_OK || npre < 1) return 0;
+  return packed_frag_bytes(NC_of(d), (int64_t)(1 + npre) * d->N) + kColsumBytes;
+}
+
+size_t xhc_packed_active_bytes(const xhc_dims* d, int32_t Kq, int32_t with_res) {
+  if (check_dims(d) != XHC_OK || Kq < 1 || Kq > kMaxKr) return 0;
+  return packed_frag_bytes(kC_of(d), act_outs(d, Kq, with_res));
+}
+
+xhc_status xhc_pack_full(const xhc_dims* d, int32_t npre, const float* W_r, const float* W_pre, void* packed,
+                         void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (npre < 1 || !W_r || !W_pre || !packed) return XHC_EINVAL;
+  if ((int64_t)(1 + npre) * d->N > 128) return XHC_EUNSUPPORTED;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int64_t K = NC_of(d);
+  hipError_t e = launch_pack(K, (int64_t)(1 + npre) * d->N, d->N, W_r, d->N, W_pre, npre, packed, s);
+  if (e != hipSuccess) return XHC_EHIP;
+  float* colsum = reinterpret_cast<float*>(reinterpret_cast<char*>(packed) +
+                                           packed_frag_bytes(K, (int64_t)(1 + npre) * d->N));
+  return hip_status(launch_colsum(K, d->N, W_r, colsum, s));
+}
+
+xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, const float* W_res, void* packed,
+                           void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (Kq < 1 || Kq > kMaxKr || !W_post || !packed) return XHC_EINVAL;
+  const int with_res = W_res != nullptr;
+  return hip_status(launch_pack(kC_of(d), act_outs(d, Kq, with_res), d->k * Kq, W_post, d->k * d->k, W_res,
+                                with_res ? 1 : 0, packed, reinterpret_cast<hipStream_t>(stream)));
+}
+
+size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q) {
+  (void)Q;
+  if (check_dims(d) != XHC_OK) return 0;
+  switch (op) {
+    case XHC_OP_PRE: return pre_ws(d);
+    case XHC_OP_POST: return post_ws(d);
+    default: return 0;
+  }
+}
+
+xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, const void* packed_act,
+                   const float* alpha, const float* b_pre, const float* b_res, const float* b_post, void* input,
+                   int32_t* idx, float* p, float* Hpre, float* Hres, float* Hpost, void* workspace,
+                   size_t workspace_bytes, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (d->T == 0) return XHC_OK;
+  if (!X || !packed_full || !packed_act || !alpha || !b_pre || !b_res || !b_post || !input || !idx || !p ||
+      !Hpre || !Hres || !Hpost || !workspace)
+    return XHC_EINVAL;
+  if (!aligned16(X) || !aligned16(input) || !aligned16(packed_full) || !aligned16(packed_act))
+    return XHC_EUNSUPPORTED;
+  if (workspace_bytes < pre_ws(d)) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  float* part = reinterpret_cast<float*>(workspace);
+  const int64_t NC = NC_of(d), kC = kC_of(d);
+  const int64_t nout_full = 2 * d->N, nout_act = act_outs(d, d->Kr, 1);
+  const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
+                                                       packed_frag_bytes(NC, nout_full));
+  hipError_t e = launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full, nullptr,
+                                     d->k, part, s);
+  if (e == hipSuccess)
+    e = launch_pre_route(part, proj_chunks(NC), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum, alpha, 1,
+                         b_pre, d->eps, idx, p, Hpre, s);
+  if (e == hipSuccess)
+    e = launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act, nout_act, idx, d->k, part, s);
+  if (e == hipSuccess)
+    e = launch_pre_coef(part, proj_chunks(kC), nout_act, d->T, d->k, d->Kr, 1, d->C, alpha + 2, alpha + 1,
+                        b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost, Hres, s);
+  if (e == hipSuccess) e = launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, s);
+  return hip_status(e);
+}
+
+xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv_w, const int32_t* idx,
+                    const float* p, const float* Hres, const float* Hpost, void* workspace, size_t workspace_bytes,
+                    void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (d->T == 0) return XHC_OK;
+  if (!X || !F || !idx || !p || !Hres || !Hpost) return XHC_EINVAL;
+  if ((d->Kr > 1) != (conv_w != nullptr)) return XHC_EINVAL;
+  if (X == F) return XHC_EINVAL;
+  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w))) return XHC_EUNSUPPORTED;
+  const size_t need = post_ws(d);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  float* wb = nullptr;
+  hipError_t e = hipSuccess;
+  if (d->Kr > 1) {
+    const int np = d->Kr * (d->Kr + 1) / 2;
+    float* gpart = reinterpret_cast<float*>(workspace);
+    wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
+                                  align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)));
+    e = launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, d->Kr, d->kappa, conv_w, gpart, s);
+    if (e == hipSuccess)
+      e = launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, d->Kr, d->gram_schmidt, p, Hpost, wb, s);
+  }
+  if (e == hipSuccess)
+    e = launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa, conv_w, idx, p,
+                          Hres, Hpost, wb, s);
+  return hip_status(e);
+}
+
+}  // extern "C"

@@ -1,0 +1,202 @@
+// Device-side building blocks shared by the xHC kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "xhc.h"
+#include "xhc_launch.h"
+
+namespace xhc {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------- bf16 <-> f32
+
+__device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// fp32 -> bf16 bits, round to nearest, ties to even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+__device__ __forceinline__ uint32_t pack2bf(float a, float b) { return f2bf(a) | (f2bf(b) << 16); }
+
+__device__ __forceinline__ void unpack8(const uint4 v, float (&f)[8]) {
+  f[0] = bf_lo(v.x); f[1] = bf_hi(v.x); f[2] = bf_lo(v.y); f[3] = bf_hi(v.y);
+  f[4] = bf_lo(v.z); f[5] = bf_hi(v.z); f[6] = bf_lo(v.w); f[7] = bf_hi(v.w);
+}
+__device__ __forceinline__ uint4 pack8(const float (&f)[8]) {
+  return make_uint4(pack2bf(f[0], f[1]), pack2bf(f[2], f[3]), pack2bf(f[4], f[5]), pack2bf(f[6], f[7]));
+}
+
+// Eight consecutive state elements <-> fp32, for bf16 (uint16_t) and fp32 states.
+template <typename TS> struct Vec8;
+template <> struct Vec8<uint16_t> {
+  static __device__ __forceinline__ void load(const uint16_t* p, float (&f)[8]) {
+    unpack8(*reinterpret_cast<const uint4*>(p), f);
+  }
+  static __device__ __forceinline__ void store(uint16_t* p, const float (&f)[8]) {
+    *reinterpret_cast<uint4*>(p) = pack8(f);
+  }
+  // bf16 operand bits of the same eight elements (exact for a bf16 state)
+  static __device__ __forceinline__ uint4 operand(const uint16_t* p, float (&f)[8]) {
+    uint4 v = *reinterpret_cast<const uint4*>(p);
+    unpack8(v, f);
+    return v;
+  }
+};
+template <> struct Vec8<float> {
+  static __device__ __forceinline__ void load(const float* p, float (&f)[8]) {
+    float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
+    f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float (&f)[8]) {
+    reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
+    reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
+  }
+  // an fp32 state enters the projection rounded to bf16 (projection operands are bf16)
+  static __device__ __forceinline__ uint4 operand(const float* p, float (&f)[8]) {
+    load(p, f);
+    return pack8(f);
+  }
+};
+
+// ---------------------------------------------------------------- MFMA
+// v_mfma_f32_16x16x32_bf16: D[16x16] += A[16x32] * B[32x16].
+// Lane l holds A[l%16][8*(l/16) .. +8], B[8*(l/16) .. +8][l%16] and
+// D[4*(l/16) + v][l%16], v = 0..3.
+__device__ __forceinline__ f32x4 mfma_16x16x32(uint4 a, uint4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------- math
+
+__device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + __expf(-z)); }
+
+// Fixed-plus-TopK routing of one token (eq:router_topk).  Slots 0..m-1 take
+// streams 0..m-1 with p = 1; slot j >= m takes the largest remaining logit
+// among streams m..N-1, ties to the lower index.  A NaN logit never wins a
+// comparison; a slot whose candidates all compare false takes the lowest free
+// stream, so every index stays in range.
+template <int NMAX>
+__device__ __forceinline__ void route_token(const float (&z)[NMAX], int N, int m, int k,
+                                            int32_t* idx_out, float* p_out) {
+  uint64_t used = 0;
+  for (int j = 0; j < m; ++j) {
+    idx_out[j] = j;
+    p_out[j] = 1.0f;
+  }
+  for (int j = m; j < k; ++j) {
+    int best = -1;
+    float bz = 0.0f;
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i) {
+      if (i >= m && i < N && !((used >> i) & 1ull)) {
+        if (best < 0 || z[i] > bz) { best = i; bz = z[i]; }
+      }
+    }
+    used |= 1ull << best;
+    idx_out[j] = best;
+    p_out[j] = sigmoidf(bz);
+  }
+}
+
+// Sinkhorn-Knopp (rows, then columns, per iteration) of exp(L) followed by
+// the row clamp, in place on a k x k row-major matrix holding L on entry.
+// The row maximum is subtracted before exp: exactly invariant because the
+// first operation of each iteration normalises rows.
+__device__ __forceinline__ void sinkhorn_clamp(float (&M)[kMaxK * kMaxK], int k, int iters, float delta) {
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    if (j >= k) break;
+    float mx = M[j * kMaxK];
+#pragma unroll
+    for (int l = 1; l < kMaxK; ++l) if (l < k) mx = fmaxf(mx, M[j * kMaxK + l]);
+#pragma unroll
+    for (int l = 0; l < kMaxK; ++l) if (l < k) M[j * kMaxK + l] = __expf(M[j * kMaxK + l] - mx);
+  }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < kMaxK; ++j) {
+      if (j < k) {
+        float s = 0.f;
+#pragma unroll
+        for (int l = 0; l < kMaxK; ++l) if (l < k) s += M[j * kMaxK + l];
+        float r = 1.0f / s;
+#pragma unroll
+        for (int l = 0; l < kMaxK; ++l) if (l < k) M[j * kMaxK + l] *= r;
+      }
+    }
+#pragma unroll
+    for (int l = 0; l < kMaxK; ++l) {
+      if (l < k) {
+        float s = 0.f;
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j) if (j < k) s += M[j * kMaxK + l];
+        float r = 1.0f / s;
+#pragma unroll
+        for (int j = 0; j < kMaxK; ++j) if (j < k) M[j * kMaxK + l] *= r;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kMaxK; ++j) {
+    if (j < k) {
+      float s = 0.f;
+#pragma unroll
+      for (int l = 0; l < kMaxK; ++l) if (l < k) s += M[j * kMaxK + l];
+      if (s > 1.0f + delta) {
+        float r = 1.0f / s;
+#pragma unroll
+        for (int l = 0; l < kMaxK; ++l) if (l < k) M[j * kMaxK + l] *= r;
+      }
+    }
+  }
+}
+
+// Gram-Schmidt of the components e_0 = out, e_1..e_r = conv branches, in the
+// basis {e_b}: given the Gram matrix G[a][b] = <e_a, e_b> of one token, returns
+// V with v_{i+1} = sum_b V[i][b] e_b following eq:gs (each coefficient uses the
+// raw g_j, as printed).  A component whose squared norm is at or below
+// 1e-6 of its raw squared norm is taken as zero: a Gram matrix summed in fp32
+// cannot resolve it, and its coefficient is then 0 as for an exact zero.
+__device__ __forceinline__ void gram_schmidt_basis(const double (&G)[kMaxKr][kMaxKr], int Kr,
+                                                   double (&V)[kMaxKr][kMaxKr]) {
+#pragma unroll
+  for (int i = 0; i < kMaxKr; ++i)
+#pragma unroll
+    for (int b = 0; b < kMaxKr; ++b) V[i][b] = (i == b) ? 1.0 : 0.0;
+  double nrm[kMaxKr];
+  bool zero[kMaxKr];
+#pragma unroll
+  for (int j = 0; j < kMaxKr; ++j) {
+    if (j >= Kr) break;
+    // v_{j+1} = e_j - sum_{i<j} <e_j, v_i> / <v_i, v_i> v_i
+#pragma unroll
+    for (int i = 0; i < kMaxKr; ++i) {
+      if (i >= j) break;
+      if (zero[i]) continue;
+      double dot = 0.0;
+#pragma unroll
+      for (int b = 0; b < kMaxKr; ++b) dot += V[i][b] * G[j][b];
+      double c = dot / nrm[i];
+#pragma unroll
+      for (int b = 0; b < kMaxKr; ++b) V[j][b] -= c * V[i][b];
+    }
+    double n = 0.0;
+#pragma unroll
+    for (int a = 0; a < kMaxKr; ++a)
+#pragma unroll
+      for (int b = 0; b < kMaxKr; ++b) n += V[j][a] * G[a][b] * V[j][b];
+    nrm[j] = n;
+    zero[j] = !(n > 1e-6 * G[j][j]);
+  }
+}
+
+}  // namespace xhc

@@ -1,0 +1,59 @@
+// Internal launchers of the xHC kernels (host side).  Every launcher enqueues
+// on `stream` and returns hipSuccess or the first launch error.  Shapes have
+// been validated by the C-ABI layer before any launcher is called.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "xhc.h"
+
+namespace xhc {
+
+constexpr int kWave = 64;
+constexpr int kMaxN = 64;   // streams
+constexpr int kMaxK = 8;    // active streams
+constexpr int kMaxKr = 4;   // write-back components
+
+// packed projection layout: fragments of 64 lanes x 8 bf16 (1 KiB), indexed
+// [k_block (32 rows)][out_block (16 columns)][lane]; lane l of fragment
+// (kb, ob) holds W[kb*32 + 8*(l/16) + e][ob*16 + l%16], e = 0..7.
+__host__ __device__ inline int64_t out_blocks(int64_t nout) { return (nout + 15) / 16; }
+inline size_t packed_frag_bytes(int64_t K, int64_t nout) { return (size_t)(K / 32) * out_blocks(nout) * 1024; }
+constexpr size_t kColsumBytes = 64 * sizeof(float);
+
+hipError_t launch_pack(int64_t K, int64_t nout, int ncols_a, const float* A, int ncols_b, const float* B,
+                       int64_t b_count, void* packed, hipStream_t s);
+hipError_t launch_colsum(int64_t K, int ncols, const float* W, float* out, hipStream_t s);
+
+// ---- pre (multi-kernel path)
+constexpr int kProjTile = 16;    // tokens per projection tile
+constexpr int kProjChunkBlocks = 64;  // 32-row blocks per split-K chunk
+
+__host__ __device__ inline int64_t proj_chunks(int64_t K) { return (K / 32 + kProjChunkBlocks - 1) / kProjChunkBlocks; }
+
+hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N, int C, int64_t K,
+                               const void* packed, int64_t nout, const int32_t* idx, int k,
+                               float* part, hipStream_t s);
+hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int64_t T, int N, int m, int k,
+                            int npre, int64_t C, const float* colsum, const float* alpha_pre, int alpha_stride,
+                            const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, hipStream_t s);
+hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int64_t T, int k, int Kq,
+                           int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
+                           const float* b_post, const float* b_res, float eps, int iters, float delta,
+                           float* Hpost, float* Hres, hipStream_t s);
+hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
+                             int nmap, const int32_t* idx, int k, void* out, hipStream_t s);
+
+// ---- post
+__host__ __device__ inline int64_t post_chunks(int C) { return ((int64_t)C / 8 + 255) / 256; }
+hipError_t launch_post_gram(int state_dtype, const void* F, int64_t T, int64_t S, int C, int Kr,
+                            const int32_t* kappa, const float* conv_w, float* gpart, hipStream_t s);
+hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k, int Kr, int gram_schmidt,
+                            const float* p, const float* Hpost, float* wb, hipStream_t s);
+hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T, int64_t S, int N, int C,
+                             int k, int Kr, const int32_t* kappa, const float* conv_w, const int32_t* idx,
+                             const float* p, const float* Hres, const float* Hpost, const float* wb,
+                             hipStream_t s);
+
+}  // namespace xhc

@@ -1,0 +1,206 @@
+"""Python binding of libxhc.so (ctypes): argument marshalling only.
+
+Every function named like a C entry point (xhc_pre, xhc_post, ...) takes the
+same arguments as in include/xhc.h, with torch CUDA tensors in place of device
+pointers; the stream defaults to torch's current stream.  All computation
+runs in the library's HIP kernels.  There is no CPU fallback: if the library
+is missing or no GPU is present, calls raise.
+
+``Sublayer`` / ``FlashGroup`` bundle packing, output allocation and the calls
+for convenience; they add no arithmetic.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libxhc.so")
+HEADER = os.path.join(os.path.dirname(PKG), "include", "xhc.h")
+
+XHC_OK, XHC_EINVAL, XHC_EUNSUPPORTED, XHC_EWORKSPACE, XHC_EHIP = range(5)
+STATUS_NAMES = {0: "XHC_OK", 1: "XHC_EINVAL", 2: "XHC_EUNSUPPORTED", 3: "XHC_EWORKSPACE", 4: "XHC_EHIP"}
+XHC_BF16, XHC_F32 = 0, 1
+XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST = range(4)
+
+
+class XhcError(RuntimeError):
+    def __init__(self, name, status):
+        super().__init__(f"{name} returned {STATUS_NAMES.get(status, status)}")
+        self.status = status
+
+
+class Dims(ctypes.Structure):
+    _fields_ = [
+        ("T", ctypes.c_int64), ("S", ctypes.c_int64),
+        ("N", ctypes.c_int32), ("k", ctypes.c_int32), ("m", ctypes.c_int32), ("C", ctypes.c_int32),
+        ("Kr", ctypes.c_int32), ("kappa", ctypes.c_int32 * 3),
+        ("sinkhorn_iters", ctypes.c_int32), ("gram_schmidt", ctypes.c_int32),
+        ("eps", ctypes.c_float), ("clamp_delta", ctypes.c_float), ("state_dtype", ctypes.c_int32),
+    ]
+
+
+def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, gram_schmidt=1,
+              eps=1e-5, clamp_delta=1e-6, state="bf16") -> Dims:
+    d = Dims()
+    d.T, d.S = T, (S if S else max(T, 1))
+    d.N, d.k, d.m, d.C, d.Kr = N, k, m, C, Kr
+    kap = list(kappa) + [0] * (3 - len(kappa))
+    d.kappa = (ctypes.c_int32 * 3)(*kap[:3])
+    d.sinkhorn_iters, d.gram_schmidt = sinkhorn_iters, gram_schmidt
+    d.eps, d.clamp_delta = eps, clamp_delta
+    d.state_dtype = XHC_BF16 if state == "bf16" else XHC_F32
+    return d
+
+
+def dims_for(w, **kw) -> Dims:
+    """Dims of a synth.Workload."""
+    return make_dims(w.T, w.N, w.k, w.m, w.C, Kr=w.Kr, S=w.S, kappa=w.kappa, state=w.state, **kw)
+
+
+_lib = None
+_P = ctypes.c_void_p
+_D = ctypes.POINTER(Dims)
+_SIGS = {
+    "xhc_packed_full_bytes": (ctypes.c_size_t, [_D, ctypes.c_int32]),
+    "xhc_packed_active_bytes": (ctypes.c_size_t, [_D, ctypes.c_int32, ctypes.c_int32]),
+    "xhc_pack_full": (ctypes.c_int, [_D, ctypes.c_int32, _P, _P, _P, _P]),
+    "xhc_pack_active": (ctypes.c_int, [_D, ctypes.c_int32, _P, _P, _P, _P]),
+    "xhc_workspace_bytes": (ctypes.c_size_t, [_D, ctypes.c_int32, ctypes.c_int32]),
+    "xhc_pre": (ctypes.c_int, [_D] + [_P] * 13 + [ctypes.c_size_t, _P]),
+    "xhc_post": (ctypes.c_int, [_D] + [_P] * 8 + [ctypes.c_size_t, _P]),
+}
+
+
+def lib():
+    """Load libxhc.so once; raise if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_14530_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def declared_functions():
+    """Names of the functions declared in include/xhc.h."""
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(xhc_[a-z0-9_]+)\s*\(", text)))
+
+
+# ---------------------------------------------------------------- marshalling helpers
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_cuda:
+        raise ValueError("tensor arguments must be CUDA tensors")
+    if not t.is_contiguous():
+        raise ValueError("tensor arguments must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _call(name, *args):
+    st = getattr(lib(), name)(*args)
+    if st != XHC_OK:
+        raise XhcError(name, st)
+
+
+def _expect(t, dtype, shape, name):
+    if t.dtype != dtype or tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: expected {dtype} {tuple(shape)}, got {t.dtype} {tuple(t.shape)}")
+
+
+# ---------------------------------------------------------------- C entry points
+
+def xhc_packed_full_bytes(d, npre):
+    return lib().xhc_packed_full_bytes(ctypes.byref(d), npre)
+
+
+def xhc_packed_active_bytes(d, Kq, with_res):
+    return lib().xhc_packed_active_bytes(ctypes.byref(d), Kq, int(with_res))
+
+
+def xhc_workspace_bytes(d, op, Q=0):
+    return lib().xhc_workspace_bytes(ctypes.byref(d), op, Q)
+
+
+def xhc_pack_full(d, npre, W_r, W_pre, packed, stream=None):
+    _call("xhc_pack_full", ctypes.byref(d), npre, _ptr(W_r), _ptr(W_pre), _ptr(packed), _stream(stream))
+
+
+def xhc_pack_active(d, Kq, W_post, W_res, packed, stream=None):
+    _call("xhc_pack_active", ctypes.byref(d), Kq, _ptr(W_post), _ptr(W_res), _ptr(packed), _stream(stream))
+
+
+def xhc_pre(d, X, packed_full, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre, Hres, Hpost,
+            workspace, stream=None):
+    _call("xhc_pre", ctypes.byref(d), _ptr(X), _ptr(packed_full), _ptr(packed_act), _ptr(alpha), _ptr(b_pre),
+          _ptr(b_res), _ptr(b_post), _ptr(input), _ptr(idx), _ptr(p), _ptr(Hpre), _ptr(Hres), _ptr(Hpost),
+          _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream(stream))
+
+
+def xhc_post(d, X, F, conv_w, idx, p, Hres, Hpost, workspace, stream=None):
+    _call("xhc_post", ctypes.byref(d), _ptr(X), _ptr(F), _ptr(conv_w), _ptr(idx), _ptr(p), _ptr(Hres),
+          _ptr(Hpost), _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream(stream))
+
+
+# ---------------------------------------------------------------- convenience bundle
+
+def _bytes(n, device):
+    return torch.empty(max(int(n), 1), dtype=torch.uint8, device=device)
+
+
+class Sublayer:
+    """One full xHC sublayer: packed weights, parameters and output buffers.
+
+    ``weights`` is a dict as produced by synth.sublayer_inputs (W_r, W_pre,
+    W_res, W_post fp32; alpha [3]; b_pre, b_res, b_post; conv_w or None).
+    """
+
+    def __init__(self, d: Dims, weights, device="cuda"):
+        self.d = d
+        T, N, k, C, Kr = d.T, d.N, d.k, d.C, d.Kr
+        dev = torch.device(device)
+        g = {n: (v.to(dev).contiguous() if torch.is_tensor(v) else v) for n, v in weights.items()}
+        self.packed_full = _bytes(xhc_packed_full_bytes(d, 1), dev)
+        self.packed_act = _bytes(xhc_packed_active_bytes(d, Kr, 1), dev)
+        xhc_pack_full(d, 1, g["W_r"], g["W_pre"], self.packed_full)
+        xhc_pack_active(d, Kr, g["W_post"], g["W_res"], self.packed_act)
+        self.alpha, self.b_pre, self.b_res, self.b_post = g["alpha"], g["b_pre"], g["b_res"], g["b_post"]
+        self.conv_w = g.get("conv_w")
+        sdt = torch.bfloat16 if d.state_dtype == XHC_BF16 else torch.float32
+        self.input = torch.empty(T, C, dtype=sdt, device=dev)
+        self.idx = torch.empty(T, k, dtype=torch.int32, device=dev)
+        self.p = torch.empty(T, k, dtype=torch.float32, device=dev)
+        self.Hpre = torch.empty(T, N, dtype=torch.float32, device=dev)
+        self.Hres = torch.empty(T, k, k, dtype=torch.float32, device=dev)
+        self.Hpost = torch.empty(T, k, Kr, dtype=torch.float32, device=dev)
+        self.ws_pre = _bytes(xhc_workspace_bytes(d, XHC_OP_PRE), dev)
+        self.ws_post = _bytes(xhc_workspace_bytes(d, XHC_OP_POST), dev)
+
+    def pre(self, X, stream=None):
+        xhc_pre(self.d, X, self.packed_full, self.packed_act, self.alpha, self.b_pre, self.b_res, self.b_post,
+                self.input, self.idx, self.p, self.Hpre, self.Hres, self.Hpost, self.ws_pre, stream)
+        return self.input
+
+    def post(self, X, F, stream=None):
+        xhc_post(self.d, X, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, self.ws_post, stream)
+        return X

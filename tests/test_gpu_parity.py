@@ -1,0 +1,91 @@
+"""HIP path vs the fp64 oracle, element by element, through the C ABI."""
+
+import pytest
+import torch
+
+from paper_2607_14530_amd import synth
+from paper_2607_14530_amd import xhc as X
+from tests.parity_util import assert_bf16_close, check_sublayer
+
+pytestmark = pytest.mark.gpu
+
+W = synth.Workload
+SMALL = [
+    synth.tiny_dense(),                                                   # dense mHC, fp32 state
+    W(T=256, S=128, N=16, k=4, m=2, C=1024, Kr=1, name="attn-T256-C1024"),
+    W(T=256, S=128, N=16, k=4, m=2, C=1024, Kr=4, name="mlp-T256-C1024"),
+    W(T=77, N=8, k=4, m=2, C=96, Kr=4, name="ragged-T77-C96"),            # ragged tile and channel tails
+    W(T=40, S=20, N=5, k=3, m=1, C=64, Kr=3, kappa=(2, 5), name="odd-N5-k3-Kr3"),
+    W(T=48, S=16, N=32, k=8, m=0, C=128, Kr=4, name="wide-N32-k8-m0"),
+    W(T=64, N=16, k=4, m=2, C=256, Kr=4, state="f32", name="f32-mlp"),
+]
+
+
+def _run(w, seed, device="cuda", **kw):
+    inp = synth.sublayer_inputs(w, seed, device=device, **kw)
+    d = X.dims_for(w)
+    sub = X.Sublayer(d, inp, device)
+    Xs = inp["X"].clone()
+    sub.pre(Xs)
+    before = Xs.clone()
+    sub.post(Xs, inp["F"])
+    torch.cuda.synchronize()
+    return inp, sub, before, Xs
+
+
+@pytest.mark.parametrize("w", SMALL, ids=lambda w: w.name)
+def test_sublayer_matches_oracle(w):
+    print(f"[parity] {w.name}", flush=True)
+    inp, sub, before, after = _run(w, seed=11)
+    check_sublayer(sub, inp, w, before, after)
+
+
+def test_stressed_mappings_match_oracle():
+    """alpha = (0.5, 1, 0.5), biases ~ N(0, 2): Sinkhorn does not converge and the clamp acts."""
+    w = W(T=128, S=64, N=16, k=4, m=2, C=512, Kr=4, alpha=(0.5, 1.0, 0.5), name="stress")
+    inp, sub, before, after = _run(w, seed=5, bias_std=2.0)
+    check_sublayer(sub, inp, w, before, after)
+    rows = sub.Hres.sum(-1)
+    assert bool((rows < 1 - 1e-3).any()), "stress case should clamp some rows"
+
+
+def test_single_stream_identity():
+    """N = k = m = 1, H^pre = 1, H^post = 1: input = x bit for bit and X' = x + F."""
+    w = W(T=64, N=1, k=1, m=1, C=256, Kr=1, alpha=(0.0, 0.01, 0.0), name="identity")
+    inp = synth.sublayer_inputs(w, 3, device="cuda")
+    inp["b_pre"].fill_(40.0)
+    sub = X.Sublayer(X.dims_for(w), inp, "cuda")
+    Xs = inp["X"].clone()
+    sub.pre(Xs)
+    sub.post(Xs, inp["F"])
+    torch.cuda.synchronize()
+    assert torch.equal(sub.input, inp["X"][:, 0])
+    ref = inp["X"][:, 0].double() + inp["F"].double()
+    assert_bf16_close(Xs[:, 0], ref, "x + F")
+
+
+def test_outputs_are_deterministic():
+    w = W(T=512, S=256, N=16, k=4, m=2, C=1024, Kr=4, name="det")
+    a = _run(w, seed=2)
+    b = _run(w, seed=2)
+    for name in ("input", "idx", "p", "Hpre", "Hres", "Hpost"):
+        assert torch.equal(getattr(a[1], name), getattr(b[1], name)), name
+    assert torch.equal(a[3], b[3])
+
+
+def _sample_tokens(T, S, n, seed):
+    g = torch.Generator().manual_seed(seed)
+    fixed = [0, 1, 2, S - 1, S, S + 1, T - 1] if T > S else [0, 1, 11, T - 1]
+    rnd = torch.randint(0, T, (n,), generator=g).tolist()
+    return torch.tensor(sorted(set(t for t in fixed + rnd if 0 <= t < T)))
+
+
+@pytest.mark.parametrize("w", [synth.sparse_c1024(1), synth.sparse_c1024(4),
+                               synth.sparse_c4096(1), synth.sparse_c4096(4)], ids=lambda w: w.name)
+def test_full_size_sampled_tokens(w):
+    """Full-size workloads in the benchmark's launch configuration, checked on sampled tokens."""
+    print(f"[parity-full] {w.name}", flush=True)
+    inp, sub, before, after = _run(w, seed=1)
+    tok = _sample_tokens(w.T, w.S, 40, seed=w.C + w.Kr)
+    tg = tok.to("cuda")
+    check_sublayer(sub, inp, w, before[tg], after[tg], tokens=tok)
