@@ -1,0 +1,161 @@
+"""Benchmark of the xHC sublayer connection on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+
+One step = the forward connection of one xHC block at the large-MoE width
+(T = 16384 tokens in 2 sequences of 8192, N = 16 streams, k = 4 active, m = 2
+fixed, C = 4096, bf16 state): an attention-type sublayer (xhc_pre + xhc_post,
+one write-back component) followed by an MLP-type sublayer (xhc_pre +
+xhc_post with the 4/8/12 causal convolutions and Gram-Schmidt).  The
+sublayer output F is a given tensor (the attention / MLP themselves are
+outside the connection).  `value` is sublayer-tokens per second, 2T / step
+time, i.e. tokens/s per xHC sublayer averaged over the block as the paper
+averages its traffic.
+
+Prints ONE JSON line.  Inputs are synthetic (seeded) and resident in HBM
+before the timed region.  The roofline object is for the dominant kernel;
+its achieved bandwidth is the algorithmic bytes per launch divided by the
+launch's average duration, both measured here with HIP events on the stream
+the kernel runs on.  cpu_baseline times the CPU fp64 oracle on a bounded
+sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2607_14530_amd import accounting as A  # noqa: E402
+from paper_2607_14530_amd import synth  # noqa: E402
+from paper_2607_14530_amd import xhc as X  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "tokens/s and achieved HBM GB/s per xHC sublayer (fwd) at N=16,k=4,C=4096"
+
+
+def cpu_baseline(seconds=15.0):
+    """Time the fp64 oracle (pre + post of both sublayer kinds) on a sample of
+    tokens of the same workload, growing the sample until it runs ~seconds."""
+    from oracle import xhc_oracle as O
+    F64 = torch.float64
+    n = 16
+    while True:
+        elapsed = 0.0
+        for Kr in (1, 4):
+            w = synth.sparse_c4096(Kr)
+            ws = synth.Workload(T=n, S=n, N=w.N, k=w.k, m=w.m, C=w.C, Kr=Kr)
+            inp = synth.sublayer_inputs(ws, 7)
+            Xd = inp["X"].to(F64)
+            t0 = time.perf_counter()
+            r = O.xhc_pre(Xd, inp["W_r"], inp["W_pre"], inp["W_res"], inp["W_post"],
+                          tuple(inp["alpha"].tolist()), inp["b_pre"], inp["b_res"], inp["b_post"],
+                          m=ws.m, k=ws.k, Kr=Kr)
+            O.xhc_post(Xd, inp["F"], inp["conv_w"], r["idx"], r["p"], r["Hres"], r["Hpost"],
+                       S=ws.S, kappa=ws.kappa)
+            elapsed += time.perf_counter() - t0
+        if elapsed >= seconds or n >= 4096:
+            break
+        n = max(n * 2, int(n * seconds / max(elapsed, 1e-3) * 1.1))
+        n = min(n, 4096)
+    return {"value": 2 * n / elapsed, "unit": "tokens/s", "cores": torch.get_num_threads(), "kind": "oracle",
+            "sample": f"{n} tokens x (attention-type + MLP-type sublayer), N=16 k=4 m=2 C=4096, fp64, "
+                      f"{elapsed:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: this build runs the connection on a single MI355X "
+              f"(--gpus {args.gpus} requested); see the sharding notes in DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w_attn, w_mlp = synth.sparse_c4096(1), synth.sparse_c4096(4)
+    T, N, k, C = w_attn.T, w_attn.N, w_attn.k, w_attn.C
+    inp_a = synth.sublayer_inputs(w_attn, 1, device=dev)
+    inp_m = synth.sublayer_inputs(w_mlp, 2, device=dev)
+    sub_a = X.Sublayer(X.dims_for(w_attn), inp_a, dev)
+    sub_m = X.Sublayer(X.dims_for(w_mlp), inp_m, dev)
+    state = inp_a["X"]                       # [T, N, C] bf16, updated in place
+    F_a, F_m = inp_a["F"], inp_m["F"]
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        sub_a.pre(state, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        sub_a.post(state, F_a, stream)
+        if ev is not None:
+            ev[2].record(stream)
+        sub_m.pre(state, stream)
+        if ev is not None:
+            ev[3].record(stream)
+        sub_m.post(state, F_m, stream)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    seg = [[e[j].elapsed_time(e[j + 1]) for e in evs] for j in range(4)]   # ms
+    mean = [sum(s) / len(s) for s in seg]
+    step_ms = sum(mean)
+    value = 2 * T / (step_ms * 1e-3)
+
+    b_pre = A.algorithmic_bytes_pre(N, k, C, 1) * T
+    b_post_a = A.algorithmic_bytes_post(N, k, C, 1) * T
+    b_pre_m = A.algorithmic_bytes_pre(N, k, C, 4) * T
+    b_post_m = A.algorithmic_bytes_post(N, k, C, 4) * T
+    total_bytes = b_pre + b_post_a + b_pre_m + b_post_m
+    gbps = total_bytes / (step_ms * 1e-3) / 1e9
+    pre_ms = (mean[0] + mean[2]) / 2
+    pre_bytes = (b_pre + b_pre_m) / 2
+    achieved = pre_bytes / (pre_ms * 1e-3) / 1e9
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "xHC forward block (attention-type + MLP-type sublayer), T=16384 (2 x 8192), "
+                               "N=16, k=4, m=2, C=4096, kappa=4/8/12, bf16 state, fp32 coefficients",
+                   "T": T, "S": w_attn.S, "N": N, "k": k, "m": w_attn.m, "C": C},
+        "achieved_GBps": gbps, "hbm_frac": gbps / HBM_PEAK_GBPS,
+        "bytes_per_token_C": total_bytes / (2 * T) / (2 * C),
+        "paper_bytes_per_token_C": 73.5,
+        "segments_ms": {"attn_pre": mean[0], "attn_post": mean[1], "mlp_pre": mean[2], "mlp_post": mean[3]},
+        "wall_s": wall,
+        "roofline": {"kernel": "xhc_pre (entry point)", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -73,6 +73,11 @@ typedef struct xhc_dims {
   int32_t state_dtype;    /* xhc_dtype of X, F, input, base                      */
 } xhc_dims;
 
+/* Name of a status code, and the name of the HIP error behind the last
+ * XHC_EHIP returned on the calling thread (static strings).               */
+const char* xhc_status_string(int32_t status);
+const char* xhc_last_hip_error(void);
+
 /* ------------------------------------------------------------------ packing
  * Projection operands are bf16 (Sec. "Infrastructure Design"): the packers
  * round fp32 weights to bf16 (nearest even) into an opaque device layout used

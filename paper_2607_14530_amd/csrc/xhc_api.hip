@@ -2,6 +2,7 @@
 // Every check happens before the first launch, so an error return leaves
 // all outputs untouched.
 #include <hip/hip_runtime.h>
+#include <stdio.h>
 
 #include "xhc.h"
 #include "xhc_launch.h"
@@ -30,7 +31,28 @@ xhc_status check_dims(const xhc_dims* d) {
   return XHC_OK;
 }
 
-xhc_status hip_status(hipError_t e) { return e == hipSuccess ? XHC_OK : XHC_EHIP; }
+thread_local hipError_t g_last_hip_error = hipSuccess;
+thread_local const char* g_failed_step = "";
+thread_local char g_error_text[160];
+
+// run one launcher unless an earlier one failed; remember which one failed
+#define XHC_STEP(name, call)              \
+  do {                                    \
+    if (e == hipSuccess) {                \
+      e = (call);                         \
+      if (e != hipSuccess) g_failed_step = name; \
+    }                                     \
+  } while (0)
+
+xhc_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return XHC_OK;
+  g_last_hip_error = e;
+  return XHC_EHIP;
+}
+
+// A runtime error left by an unrelated earlier call on this thread would be
+// reported by the first hipGetLastError() after our launch; clear it first.
+void clear_stale_error() { (void)hipGetLastError(); }
 
 int64_t NC_of(const xhc_dims* d) { return (int64_t)d->N * d->C; }
 int64_t kC_of(const xhc_dims* d) { return (int64_t)d->k * d->C; }
@@ -57,6 +79,22 @@ size_t post_ws(const xhc_dims* d) {
 
 extern "C" {
 
+const char* xhc_status_string(int32_t status) {
+  switch (status) {
+    case XHC_OK: return "XHC_OK";
+    case XHC_EINVAL: return "XHC_EINVAL";
+    case XHC_EUNSUPPORTED: return "XHC_EUNSUPPORTED";
+    case XHC_EWORKSPACE: return "XHC_EWORKSPACE";
+    case XHC_EHIP: return "XHC_EHIP";
+    default: return "unknown xhc_status";
+  }
+}
+
+const char* xhc_last_hip_error(void) {
+  snprintf(g_error_text, sizeof(g_error_text), "%s in %s", hipGetErrorName(g_last_hip_error), g_failed_step);
+  return g_error_text;
+}
+
 size_t xhc_packed_full_bytes(const xhc_dims* d, int32_t npre) {
   if (check_dims(d) != XHC_OK || npre < 1) return 0;
   return packed_frag_bytes(NC_of(d), (int64_t)(1 + npre) * d->N) + kColsumBytes;
@@ -74,12 +112,14 @@ xhc_status xhc_pack_full(const xhc_dims* d, int32_t npre, const float* W_r, cons
   if (npre < 1 || !W_r || !W_pre || !packed) return XHC_EINVAL;
   if ((int64_t)(1 + npre) * d->N > 128) return XHC_EUNSUPPORTED;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
   const int64_t K = NC_of(d);
-  hipError_t e = launch_pack(K, (int64_t)(1 + npre) * d->N, d->N, W_r, d->N, W_pre, npre, packed, s);
-  if (e != hipSuccess) return XHC_EHIP;
+  hipError_t e = hipSuccess;
+  XHC_STEP("pack", launch_pack(K, (int64_t)(1 + npre) * d->N, d->N, W_r, d->N, W_pre, npre, packed, s));
   float* colsum = reinterpret_cast<float*>(reinterpret_cast<char*>(packed) +
                                            packed_frag_bytes(K, (int64_t)(1 + npre) * d->N));
-  return hip_status(launch_colsum(K, d->N, W_r, colsum, s));
+  XHC_STEP("colsum", launch_colsum(K, d->N, W_r, colsum, s));
+  return hip_status(e);
 }
 
 xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, const float* W_res, void* packed,
@@ -88,8 +128,11 @@ xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, c
   if (st != XHC_OK) return st;
   if (Kq < 1 || Kq > kMaxKr || !W_post || !packed) return XHC_EINVAL;
   const int with_res = W_res != nullptr;
-  return hip_status(launch_pack(kC_of(d), act_outs(d, Kq, with_res), d->k * Kq, W_post, d->k * d->k, W_res,
-                                with_res ? 1 : 0, packed, reinterpret_cast<hipStream_t>(stream)));
+  clear_stale_error();
+  hipError_t e = hipSuccess;
+  XHC_STEP("pack", launch_pack(kC_of(d), act_outs(d, Kq, with_res), d->k * Kq, W_post, d->k * d->k, W_res,
+                               with_res ? 1 : 0, packed, reinterpret_cast<hipStream_t>(stream)));
+  return hip_status(e);
 }
 
 size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q) {
@@ -116,22 +159,23 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
     return XHC_EUNSUPPORTED;
   if (workspace_bytes < pre_ws(d)) return XHC_EWORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
   float* part = reinterpret_cast<float*>(workspace);
   const int64_t NC = NC_of(d), kC = kC_of(d);
   const int64_t nout_full = 2 * d->N, nout_act = act_outs(d, d->Kr, 1);
   const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
                                                        packed_frag_bytes(NC, nout_full));
-  hipError_t e = launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full, nullptr,
-                                     d->k, part, s);
-  if (e == hipSuccess)
-    e = launch_pre_route(part, proj_chunks(NC), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum, alpha, 1,
-                         b_pre, d->eps, idx, p, Hpre, s);
-  if (e == hipSuccess)
-    e = launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act, nout_act, idx, d->k, part, s);
-  if (e == hipSuccess)
-    e = launch_pre_coef(part, proj_chunks(kC), nout_act, d->T, d->k, d->Kr, 1, d->C, alpha + 2, alpha + 1,
-                        b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost, Hres, s);
-  if (e == hipSuccess) e = launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, s);
+  hipError_t e = hipSuccess;
+  XHC_STEP("proj_full", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full,
+                                            nullptr, d->k, part, s));
+  XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(NC), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,
+                                         alpha, 1, b_pre, d->eps, idx, p, Hpre, s));
+  XHC_STEP("proj_active", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act, nout_act, idx,
+                                              d->k, part, s));
+  XHC_STEP("pre_coef", launch_pre_coef(part, proj_chunks(kC), nout_act, d->T, d->k, d->Kr, 1, d->C, alpha + 2,
+                                       alpha + 1, b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost,
+                                       Hres, s));
+  XHC_STEP("dense_read", launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, s));
   return hip_status(e);
 }
 
@@ -148,6 +192,7 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
   const size_t need = post_ws(d);
   if (need > 0 && (!workspace || workspace_bytes < need)) return XHC_EWORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
   float* wb = nullptr;
   hipError_t e = hipSuccess;
   if (d->Kr > 1) {
@@ -155,13 +200,12 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
     float* gpart = reinterpret_cast<float*>(workspace);
     wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
                                   align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)));
-    e = launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, d->Kr, d->kappa, conv_w, gpart, s);
-    if (e == hipSuccess)
-      e = launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, d->Kr, d->gram_schmidt, p, Hpost, wb, s);
+    XHC_STEP("post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, d->Kr, d->kappa, conv_w, gpart, s));
+    XHC_STEP("post_coef",
+             launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, d->Kr, d->gram_schmidt, p, Hpost, wb, s));
   }
-  if (e == hipSuccess)
-    e = launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa, conv_w, idx, p,
-                          Hres, Hpost, wb, s);
+  XHC_STEP("post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa,
+                                           conv_w, idx, p, Hres, Hpost, wb, s));
   return hip_status(e);
 }
 

@@ -35,8 +35,10 @@ __device__ __forceinline__ uint4 pack8(const float (&f)[8]) {
 }
 
 // Eight consecutive state elements <-> fp32, for bf16 (uint16_t) and fp32 states.
+// kSplit: the state needs a second (lo) bf16 operand to enter the projection exactly.
 template <typename TS> struct Vec8;
 template <> struct Vec8<uint16_t> {
+  static constexpr bool kSplit = false;
   static __device__ __forceinline__ void load(const uint16_t* p, float (&f)[8]) {
     unpack8(*reinterpret_cast<const uint4*>(p), f);
   }
@@ -44,13 +46,15 @@ template <> struct Vec8<uint16_t> {
     *reinterpret_cast<uint4*>(p) = pack8(f);
   }
   // bf16 operand bits of the same eight elements (exact for a bf16 state)
-  static __device__ __forceinline__ uint4 operand(const uint16_t* p, float (&f)[8]) {
+  static __device__ __forceinline__ uint4 operand(const uint16_t* p, float (&f)[8], uint4& lo) {
     uint4 v = *reinterpret_cast<const uint4*>(p);
     unpack8(v, f);
+    lo = make_uint4(0, 0, 0, 0);
     return v;
   }
 };
 template <> struct Vec8<float> {
+  static constexpr bool kSplit = true;
   static __device__ __forceinline__ void load(const float* p, float (&f)[8]) {
     float4 a = reinterpret_cast<const float4*>(p)[0], b = reinterpret_cast<const float4*>(p)[1];
     f[0] = a.x; f[1] = a.y; f[2] = a.z; f[3] = a.w; f[4] = b.x; f[5] = b.y; f[6] = b.z; f[7] = b.w;
@@ -59,10 +63,18 @@ template <> struct Vec8<float> {
     reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
     reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
   }
-  // an fp32 state enters the projection rounded to bf16 (projection operands are bf16)
-  static __device__ __forceinline__ uint4 operand(const float* p, float (&f)[8]) {
+  // an fp32 state enters the projection as a bf16 pair hi + lo (hi = bf16(x),
+  // lo = bf16(x - hi)), which represents x to about 2^-16 relative
+  static __device__ __forceinline__ uint4 operand(const float* p, float (&f)[8], uint4& lo) {
     load(p, f);
-    return pack8(f);
+    float h[8], l[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      h[e] = __uint_as_float(f2bf(f[e]) << 16);
+      l[e] = f[e] - h[e];
+    }
+    lo = pack8(l);
+    return pack8(h);
   }
 };
 

@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, 
     const int64_t kb = chunk * kProjChunkBlocks + b;
     if (kb >= nblk) break;
     const int64_t kk = kb * 32 + grp * 8;
-    uint4 xb = make_uint4(0, 0, 0, 0);
+    uint4 xb = make_uint4(0, 0, 0, 0), xl = make_uint4(0, 0, 0, 0);
     if (valid) {
       const TS* src;
       if (GATHER) {
@@ -112,12 +112,16 @@ __global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, 
         src = X + (t * (int64_t)N * C + kk);
       }
       float f[8];
-      xb = Vec8<TS>::operand(src, f);
+      xb = Vec8<TS>::operand(src, f, xl);
 #pragma unroll
       for (int e = 0; e < 8; ++e) { s1 += f[e]; s2 += f[e] * f[e]; }
     }
 #pragma unroll
-    for (int ob = 0; ob < NOB; ++ob) acc[ob] = mfma_16x16x32(wpk[(kb * NOB + ob) * kWave + lane], xb, acc[ob]);
+    for (int ob = 0; ob < NOB; ++ob) {
+      const uint4 wa = wpk[(kb * NOB + ob) * kWave + lane];
+      acc[ob] = mfma_16x16x32(wa, xb, acc[ob]);
+      if (Vec8<TS>::kSplit) acc[ob] = mfma_16x16x32(wa, xl, acc[ob]);
+    }
   }
   s1 += __shfl_xor(s1, 16);
   s1 += __shfl_xor(s1, 32);

@@ -29,8 +29,8 @@ XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST = range(4)
 
 
 class XhcError(RuntimeError):
-    def __init__(self, name, status):
-        super().__init__(f"{name} returned {STATUS_NAMES.get(status, status)}")
+    def __init__(self, name, status, detail=""):
+        super().__init__(f"{name} returned {STATUS_NAMES.get(status, status)}{detail}")
         self.status = status
 
 
@@ -71,8 +71,10 @@ _SIGS = {
     "xhc_pack_full": (ctypes.c_int, [_D, ctypes.c_int32, _P, _P, _P, _P]),
     "xhc_pack_active": (ctypes.c_int, [_D, ctypes.c_int32, _P, _P, _P, _P]),
     "xhc_workspace_bytes": (ctypes.c_size_t, [_D, ctypes.c_int32, ctypes.c_int32]),
-    "xhc_pre": (ctypes.c_int, [_D] + [_P] * 13 + [ctypes.c_size_t, _P]),
+    "xhc_pre": (ctypes.c_int, [_D] + [_P] * 14 + [ctypes.c_size_t, _P]),
     "xhc_post": (ctypes.c_int, [_D] + [_P] * 8 + [ctypes.c_size_t, _P]),
+    "xhc_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
+    "xhc_last_hip_error": (ctypes.c_char_p, []),
 }
 
 
@@ -120,7 +122,8 @@ def _stream(stream):
 def _call(name, *args):
     st = getattr(lib(), name)(*args)
     if st != XHC_OK:
-        raise XhcError(name, st)
+        detail = f" ({lib().xhc_last_hip_error().decode()})" if st == XHC_EHIP else ""
+        raise XhcError(name, st, detail)
 
 
 def _expect(t, dtype, shape, name):

@@ -8,6 +8,17 @@ import pytest
 from paper_2607_14530_amd import xhc as X
 
 
+def test_binding_signatures_match_header():
+    """Each bound function passes as many arguments as the header declares."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", open(X.HEADER).read(), flags=re.S)
+    for name, (_, args) in X._SIGS.items():
+        m = re.search(name + r"\s*\(([^;]*)\)\s*;", text)
+        assert m, name
+        params = [a for a in m.group(1).split(",") if a.strip() and a.strip() != "void"]
+        assert len(params) == len(args), (name, len(params), len(args))
+
+
 def test_library_exports_every_declared_symbol():
     L = X.lib()
     names = X.declared_functions()
@@ -32,7 +43,7 @@ FAKE = 1 << 20  # a 16-byte aligned non-null address; never dereferenced below
 
 
 def _pre_status(d, ws_bytes=1 << 40, null_at=None):
-    ptrs = [FAKE] * 13
+    ptrs = [FAKE] * 14
     if null_at is not None:
         ptrs[null_at] = None
     return X.lib().xhc_pre(ctypes.byref(d), *ptrs, ws_bytes, None)
@@ -63,7 +74,7 @@ def test_invalid_dims_rejected_before_launch(kw, status):
 
 def test_null_pointer_and_workspace_errors():
     d = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=1)
-    for i in range(13):
+    for i in range(14):
         assert _pre_status(d, null_at=i) == X.XHC_EINVAL, i
     assert _pre_status(d, ws_bytes=16) == X.XHC_EWORKSPACE
     d4 = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=4)
@@ -75,7 +86,7 @@ def test_null_pointer_and_workspace_errors():
 
 def test_misaligned_pointers_rejected():
     d = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=1)
-    ptrs = [FAKE] * 13
+    ptrs = [FAKE] * 14
     ptrs[0] = FAKE + 2
     assert X.lib().xhc_pre(ctypes.byref(d), *ptrs, 1 << 40, None) == X.XHC_EUNSUPPORTED
 
