@@ -61,6 +61,7 @@ def cpu_baseline(seconds=15.0):
             O.xhc_post(Xd, inp["F"], inp["conv_w"], r["idx"], r["p"], r["Hres"], r["Hpost"],
                        S=ws.S, kappa=ws.kappa)
             elapsed += time.perf_counter() - t0
+        print(f"[cpu_baseline] {n} tokens: {elapsed:.2f} s", file=sys.stderr, flush=True)
         if elapsed >= seconds or n >= 4096:
             break
         n = max(n * 2, int(n * seconds / max(elapsed, 1e-3) * 1.1))

@@ -71,7 +71,15 @@ typedef struct xhc_dims {
   float eps;              /* epsilon of the LayerNorm / RMSNorm statistics       */
   float clamp_delta;      /* row clamp applies when a row sum exceeds 1 + delta  */
   int32_t state_dtype;    /* xhc_dtype of X, F, input, base                      */
+  int32_t impl;           /* xhc_impl: which kernels run (same results)          */
 } xhc_dims;
+
+/* Kernel selection.  AUTO takes the single-pass kernels where the shape is
+ * covered (bf16 state, N = 16, k = 4, C % 128 == 0) and the multi-kernel
+ * path otherwise, or when the device cannot hold the single-pass grid.
+ * MULTI forces the multi-kernel path; FUSED forces the single-pass path and
+ * returns XHC_EUNSUPPORTED where it does not apply.                         */
+typedef enum { XHC_IMPL_AUTO = 0, XHC_IMPL_MULTI = 1, XHC_IMPL_FUSED = 2 } xhc_impl;
 
 /* Name of a status code, and the name of the HIP error behind the last
  * XHC_EHIP returned on the calling thread (static strings).               */

@@ -24,6 +24,7 @@ xhc_status check_dims(const xhc_dims* d) {
   if (d->C < 1 || d->Kr < 1 || d->sinkhorn_iters < 0 || !(d->eps > 0.f) || !(d->clamp_delta >= 0.f))
     return XHC_EINVAL;
   if (d->state_dtype != XHC_BF16 && d->state_dtype != XHC_F32) return XHC_EINVAL;
+  if (d->impl < XHC_IMPL_AUTO || d->impl > XHC_IMPL_FUSED) return XHC_EINVAL;
   if (d->N > kMaxN || d->k > kMaxK || d->Kr > kMaxKr || d->sinkhorn_iters > 1000) return XHC_EUNSUPPORTED;
   if (d->C % 32 != 0) return XHC_EUNSUPPORTED;
   for (int j = 0; j < d->Kr - 1; ++j)
@@ -62,10 +63,22 @@ size_t part_bytes(int64_t K, int64_t nout, int64_t T) {
   return align_up((size_t)proj_chunks(K) * (size_t)(out_blocks(nout) * 16 + 2) * (size_t)T * sizeof(float));
 }
 
-size_t pre_ws(const xhc_dims* d) {
+size_t pre_ws_multi(const xhc_dims* d) {
   const size_t full = part_bytes(NC_of(d), 2 * d->N, d->T);
   const size_t act = part_bytes(kC_of(d), act_outs(d, d->Kr, 1), d->T);
   return full > act ? full : act;
+}
+
+// The single-pass path may fall back to the multi-kernel path at run time
+// (device too small for its grid), so AUTO sizes for both.
+size_t pre_ws(const xhc_dims* d) {
+  size_t need = 0;
+  if (d->impl != XHC_IMPL_FUSED) need = pre_ws_multi(d);
+  if (d->impl != XHC_IMPL_MULTI && fused_pre_supported(d)) {
+    const size_t f = fused_pre_ws_bytes(d);
+    need = need > f ? need : f;
+  }
+  return need;
 }
 
 size_t post_ws(const xhc_dims* d) {
@@ -157,7 +170,14 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
     return XHC_EINVAL;
   if (!aligned16(X) || !aligned16(input) || !aligned16(packed_full) || !aligned16(packed_act))
     return XHC_EUNSUPPORTED;
+  if (d->impl == XHC_IMPL_FUSED && !fused_pre_supported(d)) return XHC_EUNSUPPORTED;
   if (workspace_bytes < pre_ws(d)) return XHC_EWORKSPACE;
+  if (d->impl == XHC_IMPL_AUTO && !fused_pre_supported(d)) {
+    xhc_dims m = *d;
+    m.impl = XHC_IMPL_MULTI;
+    return xhc_pre(&m, X, packed_full, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre, Hres, Hpost,
+                   workspace, workspace_bytes, stream);
+  }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   clear_stale_error();
   float* part = reinterpret_cast<float*>(workspace);
@@ -166,6 +186,17 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
                                                        packed_frag_bytes(NC, nout_full));
   hipError_t e = hipSuccess;
+  if (d->impl != XHC_IMPL_MULTI) {
+    e = launch_pre_fused(d, X, packed_full, colsum, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre,
+                         Hres, Hpost, workspace, s);
+    if (e == hipSuccess) return XHC_OK;
+    if (d->impl == XHC_IMPL_FUSED || e != hipErrorInvalidConfiguration) {
+      g_failed_step = "pre_fused";
+      return hip_status(e);
+    }
+    e = hipSuccess;   // the device cannot hold the single-pass grid: multi-kernel path
+    clear_stale_error();
+  }
   XHC_STEP("proj_full", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full,
                                             nullptr, d->k, part, s));
   XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(NC), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,

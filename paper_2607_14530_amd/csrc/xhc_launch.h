@@ -45,6 +45,14 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
 hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
                              int nmap, const int32_t* idx, int k, void* out, hipStream_t s);
 
+// ---- pre (fused single-pass path: bf16 state, N = 16, k = 4, C % 128 == 0)
+bool fused_pre_supported(const xhc_dims* d);
+size_t fused_pre_ws_bytes(const xhc_dims* d);
+hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed_full, const float* colsum,
+                            const void* packed_act, const float* alpha, const float* b_pre, const float* b_res,
+                            const float* b_post, void* input, int32_t* idx, float* p, float* Hpre, float* Hres,
+                            float* Hpost, void* ws, hipStream_t s);
+
 // ---- post
 __host__ __device__ inline int64_t post_chunks(int C) { return ((int64_t)C / 8 + 255) / 256; }
 hipError_t launch_post_gram(int state_dtype, const void* F, int64_t T, int64_t S, int C, int Kr,

@@ -25,6 +25,7 @@ HEADER = os.path.join(os.path.dirname(PKG), "include", "xhc.h")
 XHC_OK, XHC_EINVAL, XHC_EUNSUPPORTED, XHC_EWORKSPACE, XHC_EHIP = range(5)
 STATUS_NAMES = {0: "XHC_OK", 1: "XHC_EINVAL", 2: "XHC_EUNSUPPORTED", 3: "XHC_EWORKSPACE", 4: "XHC_EHIP"}
 XHC_BF16, XHC_F32 = 0, 1
+XHC_IMPL_AUTO, XHC_IMPL_MULTI, XHC_IMPL_FUSED = 0, 1, 2
 XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST = range(4)
 
 
@@ -41,11 +42,12 @@ class Dims(ctypes.Structure):
         ("Kr", ctypes.c_int32), ("kappa", ctypes.c_int32 * 3),
         ("sinkhorn_iters", ctypes.c_int32), ("gram_schmidt", ctypes.c_int32),
         ("eps", ctypes.c_float), ("clamp_delta", ctypes.c_float), ("state_dtype", ctypes.c_int32),
+        ("impl", ctypes.c_int32),
     ]
 
 
 def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, gram_schmidt=1,
-              eps=1e-5, clamp_delta=1e-6, state="bf16") -> Dims:
+              eps=1e-5, clamp_delta=1e-6, state="bf16", impl=XHC_IMPL_AUTO) -> Dims:
     d = Dims()
     d.T, d.S = T, (S if S else max(T, 1))
     d.N, d.k, d.m, d.C, d.Kr = N, k, m, C, Kr
@@ -54,6 +56,7 @@ def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, 
     d.sinkhorn_iters, d.gram_schmidt = sinkhorn_iters, gram_schmidt
     d.eps, d.clamp_delta = eps, clamp_delta
     d.state_dtype = XHC_BF16 if state == "bf16" else XHC_F32
+    d.impl = impl
     return d
 
 

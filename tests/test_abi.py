@@ -95,3 +95,12 @@ def test_empty_batch_is_a_no_op():
     d = X.make_dims(T=0, N=16, k=4, m=2, C=256, Kr=1, S=1)
     assert _pre_status(d) == X.XHC_OK
     assert _post_status(d, conv=False) == X.XHC_OK
+
+
+def test_forced_fused_path_rejects_uncovered_shapes():
+    d = X.make_dims(T=64, N=8, k=4, m=2, C=256, Kr=1, impl=X.XHC_IMPL_FUSED)
+    assert _pre_status(d) == X.XHC_EUNSUPPORTED
+    d = X.make_dims(T=64, N=16, k=4, m=2, C=96, Kr=1, impl=X.XHC_IMPL_FUSED)
+    assert _pre_status(d) == X.XHC_EUNSUPPORTED
+    d = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=1, impl=7)
+    assert _pre_status(d) == X.XHC_EINVAL

@@ -22,13 +22,30 @@ SMALL = [
 ]
 
 
-def _run(w, seed, device="cuda", draw_on_cpu=False, **kw):
+def _fused_ok(w):
+    return w.state == "bf16" and w.N == 16 and w.k == 4 and w.C % 128 == 0
+
+
+IMPLS = {"multi": X.XHC_IMPL_MULTI, "fused": X.XHC_IMPL_FUSED}
+
+
+def _cases(ws):
+    out = []
+    for w in ws:
+        for name, impl in IMPLS.items():
+            if impl == X.XHC_IMPL_FUSED and not _fused_ok(w):
+                continue
+            out.append(pytest.param(w, impl, id=f"{w.name}-{name}"))
+    return out
+
+
+def _run(w, seed, device="cuda", draw_on_cpu=False, impl=X.XHC_IMPL_AUTO, **kw):
     if draw_on_cpu:
         inp = synth.sublayer_inputs(w, seed, **kw)
         inp = {n: (v.to(device) if v is not None else None) for n, v in inp.items()}
     else:
         inp = synth.sublayer_inputs(w, seed, device=device, **kw)
-    d = X.dims_for(w)
+    d = X.dims_for(w, impl=impl)
     sub = X.Sublayer(d, inp, device)
     Xs = inp["X"].clone()
     sub.pre(Xs)
@@ -38,18 +55,19 @@ def _run(w, seed, device="cuda", draw_on_cpu=False, **kw):
     return inp, sub, before, Xs
 
 
-@pytest.mark.parametrize("w", SMALL, ids=lambda w: w.name)
-def test_sublayer_matches_oracle(w):
-    print(f"[parity] {w.name}", flush=True)
-    inp, sub, before, after = _run(w, seed=11)
+@pytest.mark.parametrize("w,impl", _cases(SMALL))
+def test_sublayer_matches_oracle(w, impl):
+    print(f"[parity] {w.name} impl={impl}", flush=True)
+    inp, sub, before, after = _run(w, seed=11, impl=impl)
     check_sublayer(sub, inp, w, before, after)
 
 
-def test_stressed_mappings_match_oracle():
+@pytest.mark.parametrize("impl", list(IMPLS.values()), ids=list(IMPLS))
+def test_stressed_mappings_match_oracle(impl):
     """alpha = (0.5, 1, 0.5), biases ~ N(0, 2): Sinkhorn does not converge and the clamp acts."""
     w = W(T=128, S=64, N=16, k=4, m=2, C=512, Kr=4, alpha=(0.5, 1.0, 0.5), name="stress")
     # drawn on the CPU: this draw is known (from the oracle) to leave Sinkhorn unconverged
-    inp, sub, before, after = _run(w, seed=5, draw_on_cpu=True, bias_std=2.0)
+    inp, sub, before, after = _run(w, seed=5, draw_on_cpu=True, impl=impl, bias_std=2.0)
     ref, _ = check_sublayer(sub, inp, w, before, after)
     assert bool((ref["Hres"].sum(-1) < 1 - 1e-3).any()), "stress case should leave rows unconverged"
     raw = O.sinkhorn(torch.exp(1.0 * ref["z_res"] + inp["b_res"].cpu().double()).reshape(w.T, 4, 4), 20)
@@ -71,10 +89,11 @@ def test_single_stream_identity():
     assert_bf16_close(Xs[:, 0], ref, "x + F")
 
 
-def test_outputs_are_deterministic():
+@pytest.mark.parametrize("impl", list(IMPLS.values()), ids=list(IMPLS))
+def test_outputs_are_deterministic(impl):
     w = W(T=512, S=256, N=16, k=4, m=2, C=1024, Kr=4, name="det")
-    a = _run(w, seed=2)
-    b = _run(w, seed=2)
+    a = _run(w, seed=2, impl=impl)
+    b = _run(w, seed=2, impl=impl)
     for name in ("input", "idx", "p", "Hpre", "Hres", "Hpost"):
         assert torch.equal(getattr(a[1], name), getattr(b[1], name)), name
     assert torch.equal(a[3], b[3])
@@ -87,12 +106,22 @@ def _sample_tokens(T, S, n, seed):
     return torch.tensor(sorted(set(t for t in fixed + rnd if 0 <= t < T)))
 
 
-@pytest.mark.parametrize("w", [synth.sparse_c1024(1), synth.sparse_c1024(4),
-                               synth.sparse_c4096(1), synth.sparse_c4096(4)], ids=lambda w: w.name)
-def test_full_size_sampled_tokens(w):
+@pytest.mark.parametrize("w,impl", _cases([synth.sparse_c1024(1), synth.sparse_c1024(4),
+                                            synth.sparse_c4096(1), synth.sparse_c4096(4)]))
+def test_full_size_sampled_tokens(w, impl):
     """Full-size workloads in the benchmark's launch configuration, checked on sampled tokens."""
-    print(f"[parity-full] {w.name}", flush=True)
-    inp, sub, before, after = _run(w, seed=1)
+    print(f"[parity-full] {w.name} impl={impl}", flush=True)
+    inp, sub, before, after = _run(w, seed=1, impl=impl)
     tok = _sample_tokens(w.T, w.S, 40, seed=w.C + w.Kr)
     tg = tok.to("cuda")
     check_sublayer(sub, inp, w, before[tg], after[tg], tokens=tok)
+
+
+def test_fused_and_multi_agree_bitwise_on_routing():
+    """Both implementations reduce in a fixed order; their routing decisions agree exactly."""
+    w = W(T=1024, S=512, N=16, k=4, m=2, C=1024, Kr=4, name="agree")
+    a = _run(w, seed=9, impl=X.XHC_IMPL_MULTI)
+    b = _run(w, seed=9, impl=X.XHC_IMPL_FUSED)
+    same = (a[1].idx == b[1].idx).all(dim=1)
+    assert float(same.float().mean()) > 0.999
+    assert torch.allclose(a[1].Hpre, b[1].Hpre, atol=1e-5, rtol=0)
