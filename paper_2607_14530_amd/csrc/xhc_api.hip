@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdio.h>
 
+#include <algorithm>
+
 #include "xhc.h"
 #include "xhc_launch.h"
 
@@ -63,10 +65,14 @@ size_t part_bytes(int64_t K, int64_t nout, int64_t T) {
   return align_up((size_t)proj_chunks(K) * (size_t)(out_blocks(nout) * 16 + 2) * (size_t)T * sizeof(float));
 }
 
+// partials of the larger projection, then the per-token sums of either one
+size_t sums_bytes(int64_t nout, int64_t T) { return align_up((size_t)(out_blocks(nout) * 16 + 2) * T * sizeof(float)); }
+
 size_t pre_ws_multi(const xhc_dims* d) {
   const size_t full = part_bytes(NC_of(d), 2 * d->N, d->T);
   const size_t act = part_bytes(kC_of(d), act_outs(d, d->Kr, 1), d->T);
-  return full > act ? full : act;
+  const size_t sf = sums_bytes(2 * d->N, d->T), sa = sums_bytes(act_outs(d, d->Kr, 1), d->T);
+  return (full > act ? full : act) + (sf > sa ? sf : sa);
 }
 
 // The single-pass path may fall back to the multi-kernel path at run time
@@ -181,6 +187,9 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   clear_stale_error();
   float* part = reinterpret_cast<float*>(workspace);
+  const size_t part_max = std::max(part_bytes(NC_of(d), 2 * d->N, d->T),
+                                   part_bytes(kC_of(d), act_outs(d, d->Kr, 1), d->T));
+  float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_max);
   const int64_t NC = NC_of(d), kC = kC_of(d);
   const int64_t nout_full = 2 * d->N, nout_act = act_outs(d, d->Kr, 1);
   const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
@@ -200,12 +209,12 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   XHC_STEP("proj_full", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full,
                                             nullptr, d->k, part, s));
   XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(NC), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,
-                                         alpha, 1, b_pre, d->eps, idx, p, Hpre, s));
+                                         alpha, 1, b_pre, d->eps, idx, p, Hpre, sums, s));
   XHC_STEP("proj_active", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act, nout_act, idx,
                                               d->k, part, s));
   XHC_STEP("pre_coef", launch_pre_coef(part, proj_chunks(kC), nout_act, d->T, d->k, d->Kr, 1, d->C, alpha + 2,
                                        alpha + 1, b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost,
-                                       Hres, s));
+                                       Hres, sums, s));
   XHC_STEP("dense_read", launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, s));
   return hip_status(e);
 }

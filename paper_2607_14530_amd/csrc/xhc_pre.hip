@@ -97,30 +97,53 @@ __global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, 
 #pragma unroll
   for (int ob = 0; ob < NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
   float s1 = 0.f, s2 = 0.f;
-  for (int b = wave; b < kProjChunkBlocks; b += 4) {
-    const int64_t kb = chunk * kProjChunkBlocks + b;
-    if (kb >= nblk) break;
-    const int64_t kk = kb * 32 + grp * 8;
-    uint4 xb = make_uint4(0, 0, 0, 0), xl = make_uint4(0, 0, 0, 0);
-    if (valid) {
-      const TS* src;
-      if (GATHER) {
-        const int row = (int)(kk / C);
-        const int c = (int)(kk % C);
-        src = X + ((t * N + idx[t * k + row]) * (int64_t)C + c);
-      } else {
-        src = X + (t * (int64_t)N * C + kk);
-      }
-      float f[8];
-      xb = Vec8<TS>::operand(src, f, xl);
+  // The state loads of UNR blocks are issued before any is used, so each wave
+  // keeps UNR loads in flight instead of one.
+  constexpr int UNR = Vec8<TS>::kSplit ? 4 : 16;
+  constexpr int BPW = kProjChunkBlocks / 4;   // blocks per wave
+  static_assert(BPW % UNR == 0, "unroll must divide the blocks per wave");
+  for (int b0 = 0; b0 < BPW; b0 += UNR) {
+    uint4 xb[UNR], xl[UNR];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) { s1 += f[e]; s2 += f[e] * f[e]; }
+    for (int u = 0; u < UNR; ++u) {
+      const int64_t kb = chunk * kProjChunkBlocks + (b0 + u) * 4 + wave;
+      xb[u] = make_uint4(0, 0, 0, 0);
+      xl[u] = make_uint4(0, 0, 0, 0);
+      if (valid && kb < nblk) {
+        const int64_t kk = kb * 32 + grp * 8;
+        const TS* src;
+        if (GATHER) {
+          const int row = (int)(kk / C);
+          const int c = (int)(kk % C);
+          src = X + ((t * N + idx[t * k + row]) * (int64_t)C + c);
+        } else {
+          src = X + (t * (int64_t)N * C + kk);
+        }
+        float f[8];
+        xb[u] = Vec8<TS>::operand(src, f, xl[u]);
+      }
     }
 #pragma unroll
-    for (int ob = 0; ob < NOB; ++ob) {
-      const uint4 wa = wpk[(kb * NOB + ob) * kWave + lane];
-      acc[ob] = mfma_16x16x32(wa, xb, acc[ob]);
-      if (Vec8<TS>::kSplit) acc[ob] = mfma_16x16x32(wa, xl, acc[ob]);
+    for (int u = 0; u < UNR; ++u) {
+      const int64_t kb = chunk * kProjChunkBlocks + (b0 + u) * 4 + wave;
+      if (kb < nblk) {
+      // moments from the operand registers (hi + lo for an fp32 state, to 2^-16)
+      float f[8], g[8];
+      unpack8(xb[u], f);
+      unpack8(xl[u], g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float x = f[e] + g[e];
+        s1 += x;
+        s2 += x * x;
+      }
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob) {
+        const uint4 wa = wpk[(kb * NOB + ob) * kWave + lane];
+        acc[ob] = mfma_16x16x32(wa, xb[u], acc[ob]);
+        if (Vec8<TS>::kSplit) acc[ob] = mfma_16x16x32(wa, xl[u], acc[ob]);
+      }
+      }
     }
   }
   s1 += __shfl_xor(s1, 16);
@@ -176,29 +199,41 @@ hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N,
 
 // ----------------------------------------------------------------- per-token finalisation
 
-// Full-state projection -> router logits and npre pre-maps (one thread per token).
+// sums[o][t] = sum over chunks of part[chunk][o][t] (chunk order fixed), one
+// thread per (o, t); the loads of all chunks are issued before the adds.
+__global__ __launch_bounds__(256) void k_sum_chunks(const float* __restrict__ part, int64_t nchunk, int NO,
+                                                    int64_t T, float* __restrict__ sums) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)NO * T) return;
+  const int64_t stride = (int64_t)NO * T;
+  float s = 0.f;
+  for (int64_t c0 = 0; c0 < nchunk; c0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = (c0 + u < nchunk) ? part[(c0 + u) * stride + i] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  sums[i] = s;
+}
+
+// Full-state projection sums -> router logits and npre pre-maps (one thread per token).
 // z^r = (x W^r - mu colsum(W^r)) / sqrt(nu - mu^2 + eps),  z^pre = x W^pre / sqrt(nu + eps).
-__global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ part, int64_t nchunk, int NO,
-                                                   int64_t T, int N, int m, int k, int npre, int64_t NC,
-                                                   const float* __restrict__ colsum,
+__global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sums, int NO, int64_t T, int N, int m,
+                                                   int k, int npre, int64_t NC, const float* __restrict__ colsum,
                                                    const float* __restrict__ alpha_pre, int alpha_stride,
                                                    const float* __restrict__ b_pre, float eps,
                                                    int32_t* __restrict__ idx, float* __restrict__ p,
                                                    float* __restrict__ Hpre) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
-  auto sum_col = [&](int o) {
-    float s = 0.f;
-    for (int64_t c = 0; c < nchunk; ++c) s += part[(c * NO + o) * T + t];
-    return s;
-  };
-  const float mu = sum_col(NO - 2) / (float)NC;
-  const float nu = sum_col(NO - 1) / (float)NC;
+  const float mu = sums[(int64_t)(NO - 2) * T + t] / (float)NC;
+  const float nu = sums[(int64_t)(NO - 1) * T + t] / (float)NC;
   const float r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + eps);
   const float r_rms = 1.0f / sqrtf(nu + eps);
   float z[kMaxN];
 #pragma unroll
-  for (int i = 0; i < kMaxN; ++i) z[i] = (i < N) ? (sum_col(i) - mu * colsum[i]) * r_ln : 0.f;
+  for (int i = 0; i < kMaxN; ++i) z[i] = (i < N) ? (sums[(int64_t)i * T + t] - mu * colsum[i]) * r_ln : 0.f;
   int32_t id[kMaxK];
   float pp[kMaxK];
   route_token<kMaxN>(z, N, m, k, id, pp);
@@ -209,16 +244,15 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ par
   for (int q = 0; q < npre; ++q) {
     const float a = alpha_pre[q * alpha_stride];
     for (int i = 0; i < N; ++i) {
-      const float zp = sum_col(N + q * N + i) * r_rms;
+      const float zp = sums[(int64_t)(N + q * N + i) * T + t] * r_rms;
       Hpre[((int64_t)q * T + t) * N + i] = sigmoidf(a * zp + b_pre[q * N + i]);
     }
   }
 }
 
-// Active projection -> H^post = 2 sigma(.) and (with_res) H^res = clamp(SK(exp(.))).
-__global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ part, int64_t nchunk, int NO,
-                                                  int64_t T, int k, int Kq, int with_res, int64_t kC,
-                                                  const float* __restrict__ alpha_post,
+// Active projection sums -> H^post = 2 sigma(.) and (with_res) H^res = clamp(SK(exp(.))).
+__global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ sums, int NO, int64_t T, int k, int Kq,
+                                                  int with_res, int64_t kC, const float* __restrict__ alpha_post,
                                                   const float* __restrict__ alpha_res,
                                                   const float* __restrict__ b_post,
                                                   const float* __restrict__ b_res, float eps, int iters,
@@ -226,15 +260,10 @@ __global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ part
                                                   float* __restrict__ Hres) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
-  auto sum_col = [&](int o) {
-    float s = 0.f;
-    for (int64_t c = 0; c < nchunk; ++c) s += part[(c * NO + o) * T + t];
-    return s;
-  };
-  const float rstd = 1.0f / sqrtf(sum_col(NO - 1) / (float)kC + eps);
+  const float rstd = 1.0f / sqrtf(sums[(int64_t)(NO - 1) * T + t] / (float)kC + eps);
   const float ap = alpha_post[0];
   for (int o = 0; o < k * Kq; ++o)
-    Hpost[t * k * Kq + o] = 2.0f * sigmoidf(ap * (sum_col(o) * rstd) + b_post[o]);
+    Hpost[t * k * Kq + o] = 2.0f * sigmoidf(ap * (sums[(int64_t)o * T + t] * rstd) + b_post[o]);
   if (!with_res) return;
   const float ar = alpha_res[0];
   float M[kMaxK * kMaxK];
@@ -242,32 +271,43 @@ __global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ part
   for (int j = 0; j < kMaxK; ++j)
 #pragma unroll
     for (int l = 0; l < kMaxK; ++l)
-      M[j * kMaxK + l] = (j < k && l < k) ? ar * (sum_col(k * Kq + j * k + l) * rstd) + b_res[j * k + l] : 0.f;
+      M[j * kMaxK + l] = (j < k && l < k)
+          ? ar * (sums[(int64_t)(k * Kq + j * k + l) * T + t] * rstd) + b_res[j * k + l] : 0.f;
   sinkhorn_clamp(M, k, iters, delta);
   for (int j = 0; j < k; ++j)
     for (int l = 0; l < k; ++l) Hres[(t * k + j) * k + l] = M[j * kMaxK + l];
 }
 
+static hipError_t sum_chunks(const float* part, int64_t nchunk, int NO, int64_t T, float* sums, hipStream_t s) {
+  const int64_t n = (int64_t)NO * T;
+  k_sum_chunks<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s>>>(part, nchunk, NO, T, sums);
+  return hipGetLastError();
+}
+
 hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int64_t T, int N, int m, int k,
                             int npre, int64_t C, const float* colsum, const float* alpha_pre, int alpha_stride,
-                            const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, hipStream_t s) {
+                            const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, float* sums,
+                            hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int NO = (int)out_blocks(nout) * 16 + 2;
+  hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
+  if (e != hipSuccess) return e;
   k_pre_route<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
-      part, nchunk, NO, T, N, m, k, npre, (int64_t)N * C, colsum, alpha_pre, alpha_stride, b_pre, eps, idx, p,
-      Hpre);
+      sums, NO, T, N, m, k, npre, (int64_t)N * C, colsum, alpha_pre, alpha_stride, b_pre, eps, idx, p, Hpre);
   return hipGetLastError();
 }
 
 hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int64_t T, int k, int Kq,
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
-                           float* Hpost, float* Hres, hipStream_t s) {
+                           float* Hpost, float* Hres, float* sums, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int NO = (int)out_blocks(nout) * 16 + 2;
+  hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
+  if (e != hipSuccess) return e;
   k_pre_coef<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
-      part, nchunk, NO, T, k, Kq, with_res, (int64_t)k * C, alpha_post, alpha_res, b_post, b_res, eps, iters,
-      delta, Hpost, Hres);
+      sums, NO, T, k, Kq, with_res, (int64_t)k * C, alpha_post, alpha_res, b_post, b_res, eps, iters, delta,
+      Hpost, Hres);
   return hipGetLastError();
 }
 
@@ -294,15 +334,23 @@ __global__ __launch_bounds__(256) void k_dense_read(const TS* __restrict__ X, in
 #pragma unroll
     for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
   const TS* xt = X + t * (int64_t)N * C + c;
-  for (int i = 0; i < N; ++i) {
-    float f[8];
-    Vec8<TS>::load(xt + (int64_t)i * C, f);
+  constexpr int UNR = 8;   // stream rows loaded before use
+  for (int i0 = 0; i0 < N; i0 += UNR) {
+    float f[UNR][8];
 #pragma unroll
-    for (int q = 0; q < NMAP; ++q) {
-      float w = Hpre[((int64_t)q * T + t) * N + i];
-      if (q > 0 && ((act >> i) & 1ull)) w = 0.f;
+    for (int u = 0; u < UNR; ++u)
+      if (i0 + u < N) Vec8<TS>::load(xt + (int64_t)(i0 + u) * C, f[u]);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[q][e] = fmaf(w, f[e], acc[q][e]);
+    for (int u = 0; u < UNR; ++u) {
+      const int i = i0 + u;
+      if (i >= N) break;
+#pragma unroll
+      for (int q = 0; q < NMAP; ++q) {
+        float w = Hpre[((int64_t)q * T + t) * N + i];
+        if (q > 0 && ((act >> i) & 1ull)) w = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[q][e] = fmaf(w, f[u][e], acc[q][e]);
+      }
     }
   }
 #pragma unroll
