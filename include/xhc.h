@@ -141,6 +141,49 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
                     const int32_t* idx, const float* p, const float* Hres, const float* Hpost,
                     void* workspace, size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------------ xHC-Flash
+ * A sharing group of Q = 2 or 4 consecutive sublayers (Sec. "xHC-Flash",
+ * Alg. "xHC-Flash: one Transformer block", App. E).  Sublayer q (1-based) is
+ * attention-type (one write-back component) for odd q and MLP-type (d->Kr
+ * components with the temporal augmentation) for even q.  One routing
+ * decision and Q pre-maps come from the group-entry state; intermediate
+ * sublayers write the active rows without residual mixing; the last applies
+ * H^res.  Later inputs are formed from non-active base readouts plus the
+ * active rows as stored (eq:app_four_sub_base, eq:app_active_state_correction).
+ *
+ * xhc_flash_pre - once per group.
+ *   X            [T,N,C] group-entry state (read only)
+ *   packed_full  xhc_pack_full(npre = Q) of W_r and the Q matrices W_pre,q
+ *   packed_act1  xhc_pack_active(Kq = 1, W_res = NULL) of W_post,1
+ *   alpha_pre [Q], b_pre [Q,N], alpha_post1 [1], b_post1 [k] fp32 device
+ * Outputs: input1 [T,C] = sum_i H^pre,1_i x_i; base [Q-1,T,C] where base[q-2] =
+ * sum_{i not in I} H^pre,q_i x_i (q = 2..Q); idx, p as in xhc_pre; Hpre [Q,T,N];
+ * Hpost1 [T,k,1].                                                             */
+xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full,
+                         const void* packed_act1, const float* alpha_pre, const float* b_pre,
+                         const float* alpha_post1, const float* b_post1, void* input1, void* base, int32_t* idx,
+                         float* p, float* Hpre, float* Hpost1, void* workspace, size_t workspace_bytes,
+                         void* stream);
+
+/* xhc_flash_post - after sublayer q of the group (1 <= q <= Q).
+ *   X       [T,N,C] in/out: rows X[t, idx[t,j], :] <- (q == Q ? sum_l Hres[t,j,l]
+ *           X[t,idx[t,l],:] : X[t,idx[t,j],:]) + p[t,j] sum_r Hpost[t,j,r] v_r[t]
+ *   F       [T,C] output of sublayer q; conv_w as in xhc_post, non-NULL iff q is even
+ *   Hpost   [T,k,K_q] of sublayer q; Hres [T,k,k] iff q == Q (else NULL)
+ * For q < Q (else all NULL):
+ *   Hpre_next [T,N] = Hpre[q] from xhc_flash_pre; base_next [T,C] = base[q-1];
+ *   input_next [T,C] out: base_next + sum_j Hpre_next[t, idx[t,j]] X[t, idx[t,j], :]
+ *   packed_act_next  xhc_pack_active(K_{q+1}, W_res iff q + 1 == Q) of sublayer q+1
+ *   alpha_next [2] = (alpha_post_{q+1}, alpha_res); b_post_next [k*K_{q+1}];
+ *   b_res_next [k*k] iff q + 1 == Q; outputs Hpost_next [T,k,K_{q+1}] and
+ *   Hres_next [T,k,k] iff q + 1 == Q, both from the updated active rows.      */
+xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, const void* F, const float* conv_w,
+                          const int32_t* idx, const float* p, const float* Hpost, const float* Hres,
+                          const float* Hpre_next, const void* base_next, void* input_next,
+                          const void* packed_act_next, const float* alpha_next, const float* b_post_next,
+                          const float* b_res_next, float* Hpost_next, float* Hres_next, void* workspace,
+                          size_t workspace_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -286,7 +286,7 @@ def flash_sublayer_kind(q: int) -> str:
 def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list,
                     alpha_pre, b_pre, alpha_post, b_post, alpha_res, b_res, *,
                     m, k, S, kappa=(4, 8, 12), eps=1e-5, sinkhorn_iters=20,
-                    clamp_delta=1e-6, round_state=True, gram_schmidt_on=True):
+                    clamp_delta=1e-6, round_state=True, gram_schmidt_on=True, tokens=None):
     """One xHC-Flash sharing group of Q = len(F_list) sublayers (Q = 2 or 4).
 
     Shared routing and Q pre-mappings come from the group-entry state X0
@@ -302,7 +302,9 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
     attention and 1 + len(kappa) for MLP; conv_w_list[q-1]: [sum kappa, C] or
     None; alpha_pre/b_pre/alpha_post/b_post: per-sublayer lists.
     ``round_state`` rounds each written active row to bfloat16 (the stored
-    state precision); pins of exact identities switch it off.
+    state precision); pins of exact identities switch it off.  With
+    ``tokens`` (positions in the batch), X0 holds only those tokens' states
+    while F_list keeps the whole batch (the causal window needs it).
 
     Returns a dict with idx, p, Hpre [Q,T,N], inputs (list of Q [T,C]), bases
     (list, entry 0 is None), Hpost (list), Hres, X (final state), X_steps
@@ -341,7 +343,8 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
     Hres = None
     X = X0.clone()
     X_steps = []
-    tokens = torch.arange(T)
+    if tokens is None:
+        tokens = torch.arange(T)
     ar = torch.arange(T)[:, None]
     input_scalar = None
     for q in range(Q):
@@ -362,7 +365,7 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
             inputs.append(bases[q + 1] + (hsel[:, :, None] * a_new).sum(1))
             if Q == 2:
                 gamma = (hsel * p * Hp[:, :, 0]).sum(1)                # eq:read_reuse
-                input_scalar = inp_full[1] + gamma[:, None] * F_list[0].to(F64)
+                input_scalar = inp_full[1] + gamma[:, None] * F_list[0][tokens].to(F64)
             Hpost.append(post_from(a_new, q + 1))
             if q + 1 == Q - 1:
                 Hres = res_from(a_new)

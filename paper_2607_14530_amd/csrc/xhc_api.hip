@@ -87,6 +87,33 @@ size_t pre_ws(const xhc_dims* d) {
   return need;
 }
 
+// write-back components of sublayer q (1-based) of an xHC-Flash group:
+// attention-type (odd q) has one, MLP-type (even q) has d->Kr
+int flash_Kq(const xhc_dims* d, int q) { return (q % 2 == 1) ? 1 : d->Kr; }
+
+size_t flash_pre_ws(const xhc_dims* d, int Q) {
+  const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, 1, 0);
+  const size_t full = part_bytes(NC_of(d), nf, d->T), act = part_bytes(kC_of(d), na, d->T);
+  const size_t sf = sums_bytes(nf, d->T), sa = sums_bytes(na, d->T);
+  return (full > act ? full : act) + (sf > sa ? sf : sa);
+}
+
+size_t gram_bytes(const xhc_dims* d, int Kq) {
+  const int np = Kq * (Kq + 1) / 2;
+  return align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)) +
+         align_up((size_t)d->T * d->k * Kq * sizeof(float));
+}
+
+size_t flash_post_ws(const xhc_dims* d, int Q, int q) {
+  const int Kq = flash_Kq(d, q);
+  size_t need = Kq > 1 ? gram_bytes(d, Kq) : 0;
+  if (q < Q) {
+    const int64_t na = act_outs(d, flash_Kq(d, q + 1), q + 1 == Q);
+    need = std::max(need, part_bytes(kC_of(d), na, d->T) + sums_bytes(na, d->T));
+  }
+  return need;
+}
+
 size_t post_ws(const xhc_dims* d) {
   if (d->Kr == 1) return 0;
   const int np = d->Kr * (d->Kr + 1) / 2;
@@ -155,11 +182,17 @@ xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, c
 }
 
 size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q) {
-  (void)Q;
   if (check_dims(d) != XHC_OK) return 0;
   switch (op) {
     case XHC_OP_PRE: return pre_ws(d);
     case XHC_OP_POST: return post_ws(d);
+    case XHC_OP_FLASH_PRE: return (Q == 2 || Q == 4) ? flash_pre_ws(d, Q) : 0;
+    case XHC_OP_FLASH_POST: {
+      if (Q != 2 && Q != 4) return 0;
+      size_t need = 0;
+      for (int q = 1; q <= Q; ++q) need = std::max(need, flash_post_ws(d, Q, q));
+      return need;
+    }
     default: return 0;
   }
 }
@@ -215,7 +248,8 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   XHC_STEP("pre_coef", launch_pre_coef(part, proj_chunks(kC), nout_act, d->T, d->k, d->Kr, 1, d->C, alpha + 2,
                                        alpha + 1, b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost,
                                        Hres, sums, s));
-  XHC_STEP("dense_read", launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, s));
+  XHC_STEP("dense_read",
+           launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, nullptr, s));
   return hip_status(e);
 }
 
@@ -245,7 +279,106 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
              launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, d->Kr, d->gram_schmidt, p, Hpost, wb, s));
   }
   XHC_STEP("post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa,
-                                           conv_w, idx, p, Hres, Hpost, wb, s));
+                                           conv_w, idx, p, Hres, Hpost, wb, nullptr, nullptr, nullptr, s));
+  return hip_status(e);
+}
+
+// ---------------------------------------------------------------- xHC-Flash
+
+xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full,
+                         const void* packed_act1, const float* alpha_pre, const float* b_pre,
+                         const float* alpha_post1, const float* b_post1, void* input1, void* base, int32_t* idx,
+                         float* p, float* Hpre, float* Hpost1, void* workspace, size_t workspace_bytes,
+                         void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (Q != 2 && Q != 4) return XHC_EINVAL;
+  if ((int64_t)(Q + 1) * d->N > 128) return XHC_EUNSUPPORTED;
+  if (d->T == 0) return XHC_OK;
+  if (!X || !packed_full || !packed_act1 || !alpha_pre || !b_pre || !alpha_post1 || !b_post1 || !input1 || !base ||
+      !idx || !p || !Hpre || !Hpost1 || !workspace)
+    return XHC_EINVAL;
+  if (!aligned16(X) || !aligned16(input1) || !aligned16(base) || !aligned16(packed_full) || !aligned16(packed_act1))
+    return XHC_EUNSUPPORTED;
+  if (workspace_bytes < flash_pre_ws(d, Q)) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  const int64_t NC = NC_of(d), kC = kC_of(d);
+  const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, 1, 0);
+  float* part = reinterpret_cast<float*>(workspace);
+  float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
+                                         std::max(part_bytes(NC, nf, d->T), part_bytes(kC, na, d->T)));
+  const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
+                                                       packed_frag_bytes(NC, nf));
+  hipError_t e = hipSuccess;
+  XHC_STEP("flash_proj_full",
+           launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nf, nullptr, d->k, part, s));
+  XHC_STEP("flash_route", launch_pre_route(part, proj_chunks(NC), nf, d->T, d->N, d->m, d->k, Q, d->C, colsum,
+                                           alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, s));
+  XHC_STEP("flash_proj_active",
+           launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act1, na, idx, d->k, part, s));
+  XHC_STEP("flash_coef1", launch_pre_coef(part, proj_chunks(kC), na, d->T, d->k, 1, 0, d->C, alpha_post1, nullptr,
+                                          b_post1, nullptr, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost1,
+                                          nullptr, sums, s));
+  XHC_STEP("flash_dense_read",
+           launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, Q, idx, d->k, input1, base, s));
+  return hip_status(e);
+}
+
+xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, const void* F, const float* conv_w,
+                          const int32_t* idx, const float* p, const float* Hpost, const float* Hres,
+                          const float* Hpre_next, const void* base_next, void* input_next,
+                          const void* packed_act_next, const float* alpha_next, const float* b_post_next,
+                          const float* b_res_next, float* Hpost_next, float* Hres_next, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if ((Q != 2 && Q != 4) || q < 1 || q > Q) return XHC_EINVAL;
+  if (d->T == 0) return XHC_OK;
+  const int Kq = flash_Kq(d, q);
+  const bool last = q == Q;
+  if (!X || !F || !idx || !p || !Hpost || X == F) return XHC_EINVAL;
+  if ((Kq > 1) != (conv_w != nullptr)) return XHC_EINVAL;
+  if (last != (Hres != nullptr)) return XHC_EINVAL;
+  if (!last) {
+    if (!Hpre_next || !base_next || !input_next || !packed_act_next || !alpha_next || !b_post_next || !Hpost_next)
+      return XHC_EINVAL;
+    if ((q + 1 == Q) != (b_res_next != nullptr && Hres_next != nullptr)) return XHC_EINVAL;
+    if (!aligned16(base_next) || !aligned16(input_next) || !aligned16(packed_act_next)) return XHC_EUNSUPPORTED;
+  }
+  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w))) return XHC_EUNSUPPORTED;
+  const size_t need = flash_post_ws(d, Q, q);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  hipError_t e = hipSuccess;
+  float* wb = nullptr;
+  if (Kq > 1) {
+    const int np = Kq * (Kq + 1) / 2;
+    float* gpart = reinterpret_cast<float*>(workspace);
+    wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
+                                  align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)));
+    XHC_STEP("flash_post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, Kq, d->kappa, conv_w, gpart, s));
+    XHC_STEP("flash_post_coef",
+             launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, Kq, d->gram_schmidt, p, Hpost, wb, s));
+  }
+  XHC_STEP("flash_post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, Kq, d->kappa,
+                                                 conv_w, idx, p, Hres, Hpost, wb, last ? nullptr : Hpre_next,
+                                                 last ? nullptr : base_next, last ? nullptr : input_next, s));
+  if (!last) {
+    // mappings of sublayer q + 1 from the updated active rows (Alg. xHC-Flash, MLP step; App. E.2)
+    const int Kn = flash_Kq(d, q + 1);
+    const int with_res = (q + 1 == Q);
+    const int64_t kC = kC_of(d), na = act_outs(d, Kn, with_res);
+    float* part = reinterpret_cast<float*>(workspace);
+    float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_bytes(kC, na, d->T));
+    XHC_STEP("flash_proj_next",
+             launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act_next, na, idx, d->k, part, s));
+    XHC_STEP("flash_coef_next",
+             launch_pre_coef(part, proj_chunks(kC), na, d->T, d->k, Kn, with_res, d->C, alpha_next,
+                             with_res ? alpha_next + 1 : nullptr, b_post_next, b_res_next, d->eps, d->sinkhorn_iters,
+                             d->clamp_delta, Hpost_next, Hres_next, sums, s));
+  }
   return hip_status(e);
 }
 

@@ -45,6 +45,11 @@ template <> struct Vec8<uint16_t> {
   static __device__ __forceinline__ void store(uint16_t* p, const float (&f)[8]) {
     *reinterpret_cast<uint4*>(p) = pack8(f);
   }
+  // values as the state stores them (bf16, nearest even)
+  static __device__ __forceinline__ void round(float (&f)[8]) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) f[e] = __uint_as_float(f2bf(f[e]) << 16);
+  }
   // bf16 operand bits of the same eight elements (exact for a bf16 state)
   static __device__ __forceinline__ uint4 operand(const uint16_t* p, float (&f)[8], uint4& lo) {
     uint4 v = *reinterpret_cast<const uint4*>(p);
@@ -63,6 +68,7 @@ template <> struct Vec8<float> {
     reinterpret_cast<float4*>(p)[0] = make_float4(f[0], f[1], f[2], f[3]);
     reinterpret_cast<float4*>(p)[1] = make_float4(f[4], f[5], f[6], f[7]);
   }
+  static __device__ __forceinline__ void round(float (&)[8]) {}
   // an fp32 state enters the projection as a bf16 pair hi + lo (hi = bf16(x),
   // lo = bf16(x - hi)), which represents x to about 2^-16 relative
   static __device__ __forceinline__ uint4 operand(const float* p, float (&f)[8], uint4& lo) {

@@ -43,8 +43,10 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
                            float* Hpost, float* Hres, float* sums, hipStream_t s);
+// out0 gets map 0 (full dense read); maps 1..nmap-1 leave out the active
+// streams and go to outr + (q - 1) * T * C.
 hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
-                             int nmap, const int32_t* idx, int k, void* out, hipStream_t s);
+                             int nmap, const int32_t* idx, int k, void* out0, void* outr, hipStream_t s);
 
 // ---- pre (fused single-pass path: bf16 state, N = 16, k = 4, C % 128 == 0)
 bool fused_pre_supported(const xhc_dims* d);
@@ -63,6 +65,6 @@ hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k
 hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T, int64_t S, int N, int C,
                              int k, int Kr, const int32_t* kappa, const float* conv_w, const int32_t* idx,
                              const float* p, const float* Hres, const float* Hpost, const float* wb,
-                             hipStream_t s);
+                             const float* Hpre_next, const void* base_next, void* input_next, hipStream_t s);
 
 }  // namespace xhc

@@ -160,6 +160,10 @@ hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k
 
 // In-place update of the k active rows of one token, 8 channels per thread.
 // All k rows are read before any is written; each thread owns its channels.
+// Hres == nullptr means no residual mixing (an intermediate xHC-Flash
+// sublayer, eq:flash_attn_update).  With input_next, the thread also forms
+// the next sublayer's input from its non-active base and the active rows as
+// stored (App. E.2, eq:app_active_state_correction).
 template <typename TS, int KR>
 __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS* __restrict__ F, int64_t T,
                                                     int64_t S, int N, int C, int k, int kap0, int kap1, int kap2,
@@ -167,7 +171,10 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
                                                     const int32_t* __restrict__ idx, const float* __restrict__ p,
                                                     const float* __restrict__ Hres,
                                                     const float* __restrict__ Hpost,
-                                                    const float* __restrict__ wb) {
+                                                    const float* __restrict__ wb,
+                                                    const float* __restrict__ Hpre_next,
+                                                    const TS* __restrict__ base_next,
+                                                    TS* __restrict__ input_next) {
   const int64_t ncb = post_chunks(C);
   const int64_t t = blockIdx.x / ncb;
   const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
@@ -184,19 +191,26 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
       Vec8<TS>::load(X + (t * N + rows[l]) * (int64_t)C + c, a[l]);
     }
   }
+  float nxt[8];
+  if (input_next) Vec8<TS>::load(base_next + t * C + c, nxt);
 #pragma unroll
   for (int j = 0; j < kMaxK; ++j) {
     if (j >= k) break;
     float y[8];
+    if (Hres) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) y[q] = 0.f;
+      for (int q = 0; q < 8; ++q) y[q] = 0.f;
 #pragma unroll
-    for (int l = 0; l < kMaxK; ++l) {
-      if (l < k) {
-        const float h = Hres[(t * k + j) * k + l];
+      for (int l = 0; l < kMaxK; ++l) {
+        if (l < k) {
+          const float h = Hres[(t * k + j) * k + l];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) y[q] = fmaf(h, a[l][q], y[q]);
+          for (int q = 0; q < 8; ++q) y[q] = fmaf(h, a[l][q], y[q]);
+        }
       }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) y[q] = a[j][q];
     }
 #pragma unroll
     for (int b = 0; b < KR; ++b) {
@@ -205,18 +219,27 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
       for (int q = 0; q < 8; ++q) y[q] = fmaf(w, e[b][q], y[q]);
     }
     Vec8<TS>::store(X + (t * N + rows[j]) * (int64_t)C + c, y);
+    if (input_next) {
+      Vec8<TS>::round(y);
+      const float h = Hpre_next[t * N + rows[j]];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) nxt[q] = fmaf(h, y[q], nxt[q]);
+    }
   }
+  if (input_next) Vec8<TS>::store(input_next + t * C + c, nxt);
 }
 
 hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T, int64_t S, int N, int C, int k,
                              int Kr, const int32_t* kappa, const float* conv_w, const int32_t* idx, const float* p,
-                             const float* Hres, const float* Hpost, const float* wb, hipStream_t s) {
+                             const float* Hres, const float* Hpost, const float* wb, const float* Hpre_next,
+                             const void* base_next, void* input_next, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const dim3 grid((unsigned)(T * post_chunks(C)));
 #define XHC_APPLY(TS, KR)                                                                                       \
   k_post_apply<TS, KR><<<grid, dim3(256), 0, s>>>(reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(F), T, S, \
                                                   N, C, k, kappa[0], kappa[1], kappa[2], conv_w, idx, p, Hres,   \
-                                                  Hpost, wb)
+                                                  Hpost, wb, Hpre_next, reinterpret_cast<const TS*>(base_next),  \
+                                                  reinterpret_cast<TS*>(input_next))
   if (state_dtype == XHC_BF16) {
     switch (Kr) {
       case 1: XHC_APPLY(uint16_t, 1); break;

@@ -320,7 +320,7 @@ template <typename TS, int NMAP>
 __global__ __launch_bounds__(256) void k_dense_read(const TS* __restrict__ X, int64_t T, int N, int C,
                                                     const float* __restrict__ Hpre,
                                                     const int32_t* __restrict__ idx, int k,
-                                                    TS* __restrict__ out) {
+                                                    TS* __restrict__ out0, TS* __restrict__ outr) {
   const int64_t ncb = ((int64_t)C / 8 + 255) / 256;
   const int64_t t = blockIdx.x / ncb;
   const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
@@ -353,31 +353,32 @@ __global__ __launch_bounds__(256) void k_dense_read(const TS* __restrict__ X, in
       }
     }
   }
+  Vec8<TS>::store(out0 + t * C + c, acc[0]);
 #pragma unroll
-  for (int q = 0; q < NMAP; ++q) Vec8<TS>::store(out + ((int64_t)q * T + t) * C + c, acc[q]);
+  for (int q = 1; q < NMAP; ++q) Vec8<TS>::store(outr + ((int64_t)(q - 1) * T + t) * C + c, acc[q]);
 }
 
 template <typename TS>
 static hipError_t dense_dispatch(const TS* X, int64_t T, int N, int C, const float* Hpre, int nmap,
-                                 const int32_t* idx, int k, TS* out, hipStream_t s) {
+                                 const int32_t* idx, int k, TS* out0, TS* outr, hipStream_t s) {
   const dim3 grid((unsigned)(T * ((C / 8 + 255) / 256)));
   switch (nmap) {
-    case 1: k_dense_read<TS, 1><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out); break;
-    case 2: k_dense_read<TS, 2><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out); break;
-    case 4: k_dense_read<TS, 4><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out); break;
+    case 1: k_dense_read<TS, 1><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out0, outr); break;
+    case 2: k_dense_read<TS, 2><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out0, outr); break;
+    case 4: k_dense_read<TS, 4><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out0, outr); break;
     default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
 hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
-                             int nmap, const int32_t* idx, int k, void* out, hipStream_t s) {
+                             int nmap, const int32_t* idx, int k, void* out0, void* outr, hipStream_t s) {
   if (T == 0) return hipSuccess;
   if (state_dtype == XHC_BF16)
     return dense_dispatch<uint16_t>(reinterpret_cast<const uint16_t*>(X), T, N, C, Hpre, nmap, idx, k,
-                                    reinterpret_cast<uint16_t*>(out), s);
+                                    reinterpret_cast<uint16_t*>(out0), reinterpret_cast<uint16_t*>(outr), s);
   return dense_dispatch<float>(reinterpret_cast<const float*>(X), T, N, C, Hpre, nmap, idx, k,
-                               reinterpret_cast<float*>(out), s);
+                               reinterpret_cast<float*>(out0), reinterpret_cast<float*>(outr), s);
 }
 
 }  // namespace xhc

@@ -76,6 +76,8 @@ _SIGS = {
     "xhc_workspace_bytes": (ctypes.c_size_t, [_D, ctypes.c_int32, ctypes.c_int32]),
     "xhc_pre": (ctypes.c_int, [_D] + [_P] * 14 + [ctypes.c_size_t, _P]),
     "xhc_post": (ctypes.c_int, [_D] + [_P] * 8 + [ctypes.c_size_t, _P]),
+    "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 14 + [ctypes.c_size_t, _P]),
+    "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 17 + [ctypes.c_size_t, _P]),
     "xhc_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "xhc_last_hip_error": (ctypes.c_char_p, []),
 }
@@ -168,6 +170,25 @@ def xhc_post(d, X, F, conv_w, idx, p, Hres, Hpost, workspace, stream=None):
           _ptr(Hpost), _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream(stream))
 
 
+def _nbytes(t):
+    return t.numel() * t.element_size() if t is not None else 0
+
+
+def xhc_flash_pre(d, Q, X, packed_full, packed_act1, alpha_pre, b_pre, alpha_post1, b_post1, input1, base, idx,
+                  p, Hpre, Hpost1, workspace, stream=None):
+    _call("xhc_flash_pre", ctypes.byref(d), Q, _ptr(X), _ptr(packed_full), _ptr(packed_act1), _ptr(alpha_pre),
+          _ptr(b_pre), _ptr(alpha_post1), _ptr(b_post1), _ptr(input1), _ptr(base), _ptr(idx), _ptr(p), _ptr(Hpre),
+          _ptr(Hpost1), _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
+def xhc_flash_post(d, Q, q, X, F, conv_w, idx, p, Hpost, Hres, Hpre_next, base_next, input_next, packed_act_next,
+                   alpha_next, b_post_next, b_res_next, Hpost_next, Hres_next, workspace, stream=None):
+    _call("xhc_flash_post", ctypes.byref(d), Q, q, _ptr(X), _ptr(F), _ptr(conv_w), _ptr(idx), _ptr(p),
+          _ptr(Hpost), _ptr(Hres), _ptr(Hpre_next), _ptr(base_next), _ptr(input_next), _ptr(packed_act_next),
+          _ptr(alpha_next), _ptr(b_post_next), _ptr(b_res_next), _ptr(Hpost_next), _ptr(Hres_next),
+          _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
 # ---------------------------------------------------------------- convenience bundle
 
 def _bytes(n, device):
@@ -209,4 +230,78 @@ class Sublayer:
 
     def post(self, X, F, stream=None):
         xhc_post(self.d, X, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, self.ws_post, stream)
+        return X
+
+
+def flash_Kq(d, q):
+    """Write-back components of sublayer q (1-based) of a sharing group."""
+    return 1 if q % 2 == 1 else d.Kr
+
+
+class FlashGroup:
+    """One xHC-Flash sharing group of Q sublayers: packed weights, parameters
+    and output buffers.  ``weights`` is a dict as produced by
+    synth.flash_inputs.  ``run(X, F_list)`` calls xhc_flash_pre and then
+    xhc_flash_post for q = 1..Q; in a model the sublayer outputs F_q would be
+    computed from ``inputs[q-1]`` between the calls (``step`` does one)."""
+
+    def __init__(self, d: Dims, Q: int, weights, device="cuda"):
+        assert Q in (2, 4)
+        self.d, self.Q = d, Q
+        T, N, k, C = d.T, d.N, d.k, d.C
+        dev = torch.device(device)
+        g = {n: v for n, v in weights.items()}
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.packed_full = _bytes(xhc_packed_full_bytes(d, Q), dev)
+        W_pre = torch.stack([w.to(dev) for w in g["W_pre_list"]]).contiguous()
+        xhc_pack_full(d, Q, g["W_r"].to(dev).contiguous(), W_pre, self.packed_full)
+        self.packed_act = []
+        for q in range(1, Q + 1):
+            Kq = flash_Kq(d, q)
+            W_res = g["W_res"].to(dev).contiguous() if q == Q else None
+            buf = _bytes(xhc_packed_active_bytes(d, Kq, W_res is not None), dev)
+            xhc_pack_active(d, Kq, g["W_post_list"][q - 1].to(dev).contiguous(), W_res, buf)
+            self.packed_act.append(buf)
+        self.alpha_pre = torch.tensor(g["alpha_pre"], **f32)
+        self.b_pre = torch.stack([b.to(dev) for b in g["b_pre"]]).contiguous().float()
+        # alpha_next[q-1] = (alpha_post of sublayer q, alpha_res)
+        self.alpha_post = [torch.tensor([g["alpha_post"][q], g["alpha_res"]], **f32) for q in range(Q)]
+        self.b_post = [b.to(dev).contiguous().float() for b in g["b_post"]]
+        self.b_res = g["b_res"].to(dev).contiguous().float()
+        self.conv_w = [(c.to(dev).contiguous() if c is not None else None) for c in g["conv_w_list"]]
+        sdt = torch.bfloat16 if d.state_dtype == XHC_BF16 else torch.float32
+        self.inputs = [torch.empty(T, C, dtype=sdt, device=dev) for _ in range(Q)]
+        self.base = torch.empty(Q - 1, T, C, dtype=sdt, device=dev)
+        self.idx = torch.empty(T, k, dtype=torch.int32, device=dev)
+        self.p = torch.empty(T, k, **f32)
+        self.Hpre = torch.empty(Q, T, N, **f32)
+        self.Hpost = [torch.empty(T, k, flash_Kq(d, q), **f32) for q in range(1, Q + 1)]
+        self.Hres = torch.empty(T, k, k, **f32)
+        self.ws_pre = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_PRE, Q), dev)
+        self.ws_post = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_POST, Q), dev)
+
+    def pre(self, X, stream=None):
+        xhc_flash_pre(self.d, self.Q, X, self.packed_full, self.packed_act[0], self.alpha_pre, self.b_pre,
+                      self.alpha_post[0], self.b_post[0], self.inputs[0], self.base, self.idx, self.p, self.Hpre,
+                      self.Hpost[0], self.ws_pre, stream)
+
+    def step(self, q, X, F, stream=None):
+        """Write-back of sublayer q (1-based); for q < Q also forms inputs[q]."""
+        Q = self.Q
+        last = q == Q
+        nxt = None if last else q          # 0-based index of sublayer q + 1
+        xhc_flash_post(
+            self.d, Q, q, X, F, self.conv_w[q - 1], self.idx, self.p, self.Hpost[q - 1],
+            self.Hres if last else None,
+            None if last else self.Hpre[nxt], None if last else self.base[nxt - 1],
+            None if last else self.inputs[nxt], None if last else self.packed_act[nxt],
+            None if last else self.alpha_post[nxt], None if last else self.b_post[nxt],
+            self.b_res if (not last and q + 1 == Q) else None,
+            None if last else self.Hpost[nxt], self.Hres if (not last and q + 1 == Q) else None,
+            self.ws_post, stream)
+
+    def run(self, X, F_list, stream=None):
+        self.pre(X, stream)
+        for q in range(1, self.Q + 1):
+            self.step(q, X, F_list[q - 1], stream)
         return X
