@@ -108,7 +108,10 @@ xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, c
                            void* packed, void* stream);
 
 /* Workspace needed by an entry point (op: one of the XHC_OP_* values).        */
-enum { XHC_OP_PRE = 0, XHC_OP_POST = 1, XHC_OP_FLASH_PRE = 2, XHC_OP_FLASH_POST = 3 };
+enum {
+  XHC_OP_PRE = 0, XHC_OP_POST = 1, XHC_OP_FLASH_PRE = 2, XHC_OP_FLASH_POST = 3,
+  XHC_OP_POST_BWD = 4, XHC_OP_PRE_BWD = 5
+};
 size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q);
 
 /* ------------------------------------------------------------------ full xHC
@@ -126,7 +129,14 @@ size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q);
 xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, const void* packed_act,
                    const float* alpha, const float* b_pre, const float* b_res, const float* b_post,
                    void* input, int32_t* idx, float* p, float* Hpre, float* Hres, float* Hpost,
-                   void* workspace, size_t workspace_bytes, void* stream);
+                   float* saved, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Floats per token that xhc_pre writes to `saved` when it is non-NULL (for
+ * xhc_pre_bwd): [z_r (N) | z_pre (N) | z_post, z_res (k*Kr + k*k) | mu | nu |
+ * nu_a | pad], z = the normalised logits before gating, mu / nu = mean and
+ * mean square of the flattened state, nu_a = mean square of the active rows.
+ * Saving takes the multi-kernel path.                                      */
+size_t xhc_saved_floats(const xhc_dims* d);
 
 /* xhc_post - sparse write-back of one xHC sublayer (eq:aug, eq:gs,
  * eq:sparse_write_delta, eq:sparse_write; Alg. "Forward pass of one xHC
@@ -136,10 +146,54 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
  *   F       [T,C] sublayer output (must not alias X)
  *   conv_w  [sum_{j<Kr-1} kappa[j], C] fp32 (branch kernels stacked, row i of
  *           branch j multiplies F[t-i]); NULL iff d->Kr == 1
- *   idx, p, Hres, Hpost as produced by xhc_pre.                               */
+ *   idx, p, Hres, Hpost as produced by xhc_pre.
+ *   Xact_save  [T,k,C] or NULL: receives the active rows before the update
+ *           (slot order), as xhc_post_bwd needs them.                          */
 xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv_w,
                     const int32_t* idx, const float* p, const float* Hres, const float* Hpost,
-                    void* workspace, size_t workspace_bytes, void* stream);
+                    void* Xact_save, void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ backward
+ * Reverse mode of xhc_pre + xhc_post for a loss L(X', input) (X' = state after
+ * xhc_post, input = xhc_pre's output).  Routing is piecewise constant: the
+ * router receives gradient only through p of the routed slots; Sinkhorn is
+ * differentiated through its unrolled iterations (recomputed); projection
+ * weights receive the gradient of their bf16 operand values.  Call
+ * xhc_post_bwd first (it also gives dL/dF for the sublayer's own backward),
+ * then xhc_pre_bwd with dL/d input.
+ *
+ * xhc_post_bwd
+ *   dXn     [T,N,C] dL/dX' (read)
+ *   X       [T,N,C] in/out: the state after xhc_post; on return its active rows
+ *           are restored from Xact, i.e. X holds the state xhc_pre saw
+ *   Xact    [T,k,C] the active rows before the update (xhc_post's Xact_save)
+ *   F, conv_w, idx, p, Hres, Hpost as in xhc_post
+ * Outputs: dX [T,N,C] = dXn on untouched rows and sum_j Hres[t,j,l] dXn[t,I_j]
+ * on active row I_l (xhc_pre_bwd adds the rest); dF [T,C]; dHres [T,k,k];
+ * dHpost [T,k,Kr]; dp [T,k]; dconv_w [sum kappa, C] (NULL iff Kr == 1).
+ *
+ * xhc_pre_bwd (N in {4, 8, 16, 32}, C % 256 == 0, k*Kr + k*k <= 32)
+ *   X           [T,N,C] the state xhc_pre saw (after xhc_post_bwd's restore)
+ *   packed_full the packed [W_r | W_pre] of the forward (for sum_K bf16(W_r))
+ *   W_r, W_pre [N*C,N], W_res [k*C,k*k], W_post [k*C,k*Kr] fp32 (used as bf16)
+ *   alpha [3], b_res [k*k]; saved [T, xhc_saved_floats] from xhc_pre
+ *   idx, p, Hpre, Hpost from xhc_pre; d_input [T,C] dL/d input
+ *   dHres, dHpost, dp from xhc_post_bwd
+ *   dX [T,N,C] in/out: xhc_post_bwd's dX; on return the full dL/dX
+ * Outputs (overwritten): dW_r, dW_pre, dW_res, dW_post (shapes of the weights);
+ * dalpha [3]; db_pre [N]; db_res [k*k]; db_post [k*Kr].  Weight and bias
+ * gradients are summed over tokens in a fixed order (deterministic).       */
+xhc_status xhc_post_bwd(const xhc_dims* d, const void* dXn, void* X, const void* Xact, const void* F,
+                        const float* conv_w, const int32_t* idx, const float* p, const float* Hres,
+                        const float* Hpost, void* dX, void* dF, float* dHres, float* dHpost, float* dp,
+                        float* dconv_w, void* workspace, size_t workspace_bytes, void* stream);
+xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full, const float* W_r,
+                       const float* W_pre, const float* W_res, const float* W_post, const float* alpha,
+                       const float* b_res, const float* saved, const int32_t* idx, const float* p,
+                       const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
+                       const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
+                       float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------ xHC-Flash
  * A sharing group of Q = 2 or 4 consecutive sublayers (Sec. "xHC-Flash",

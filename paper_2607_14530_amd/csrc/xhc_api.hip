@@ -186,6 +186,8 @@ size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q) {
   switch (op) {
     case XHC_OP_PRE: return pre_ws(d);
     case XHC_OP_POST: return post_ws(d);
+    case XHC_OP_POST_BWD: return bwd_post_ws_bytes(d);
+    case XHC_OP_PRE_BWD: return bwd_pre_supported(d) ? bwd_pre_ws_bytes(d) : 0;
     case XHC_OP_FLASH_PRE: return (Q == 2 || Q == 4) ? flash_pre_ws(d, Q) : 0;
     case XHC_OP_FLASH_POST: {
       if (Q != 2 && Q != 4) return 0;
@@ -197,9 +199,14 @@ size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q) {
   }
 }
 
+size_t xhc_saved_floats(const xhc_dims* d) {
+  if (check_dims(d) != XHC_OK) return 0;
+  return (size_t)saved_floats(d->N, d->k, d->Kr);
+}
+
 xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, const void* packed_act,
                    const float* alpha, const float* b_pre, const float* b_res, const float* b_post, void* input,
-                   int32_t* idx, float* p, float* Hpre, float* Hres, float* Hpost, void* workspace,
+                   int32_t* idx, float* p, float* Hpre, float* Hres, float* Hpost, float* saved, void* workspace,
                    size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
@@ -211,11 +218,12 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
     return XHC_EUNSUPPORTED;
   if (d->impl == XHC_IMPL_FUSED && !fused_pre_supported(d)) return XHC_EUNSUPPORTED;
   if (workspace_bytes < pre_ws(d)) return XHC_EWORKSPACE;
-  if (d->impl == XHC_IMPL_AUTO && !fused_pre_supported(d)) {
+  if (d->impl == XHC_IMPL_FUSED && saved) return XHC_EUNSUPPORTED;
+  if (d->impl == XHC_IMPL_AUTO && (!fused_pre_supported(d) || saved)) {
     xhc_dims m = *d;
     m.impl = XHC_IMPL_MULTI;
     return xhc_pre(&m, X, packed_full, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre, Hres, Hpost,
-                   workspace, workspace_bytes, stream);
+                   saved, workspace, workspace_bytes, stream);
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   clear_stale_error();
@@ -225,6 +233,7 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_max);
   const int64_t NC = NC_of(d), kC = kC_of(d);
   const int64_t nout_full = 2 * d->N, nout_act = act_outs(d, d->Kr, 1);
+  const int nsave = saved_floats(d->N, d->k, d->Kr);
   const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
                                                        packed_frag_bytes(NC, nout_full));
   hipError_t e = hipSuccess;
@@ -242,27 +251,29 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   XHC_STEP("proj_full", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full,
                                             nullptr, d->k, part, s));
   XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(NC), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,
-                                         alpha, 1, b_pre, d->eps, idx, p, Hpre, sums, s));
+                                         alpha, 1, b_pre, d->eps, idx, p, Hpre, sums, saved, nsave,
+                                         nsave - 4, s));
   XHC_STEP("proj_active", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act, nout_act, idx,
                                               d->k, part, s));
   XHC_STEP("pre_coef", launch_pre_coef(part, proj_chunks(kC), nout_act, d->T, d->k, d->Kr, 1, d->C, alpha + 2,
                                        alpha + 1, b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost,
-                                       Hres, sums, s));
+                                       Hres, sums, saved, nsave, 2 * d->N, nsave - 2, s));
   XHC_STEP("dense_read",
            launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, nullptr, s));
   return hip_status(e);
 }
 
 xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv_w, const int32_t* idx,
-                    const float* p, const float* Hres, const float* Hpost, void* workspace, size_t workspace_bytes,
-                    void* stream) {
+                    const float* p, const float* Hres, const float* Hpost, void* Xact_save, void* workspace,
+                    size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
   if (d->T == 0) return XHC_OK;
   if (!X || !F || !idx || !p || !Hres || !Hpost) return XHC_EINVAL;
   if ((d->Kr > 1) != (conv_w != nullptr)) return XHC_EINVAL;
   if (X == F) return XHC_EINVAL;
-  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w))) return XHC_EUNSUPPORTED;
+  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w)) || (Xact_save && !aligned16(Xact_save)))
+    return XHC_EUNSUPPORTED;
   const size_t need = post_ws(d);
   if (need > 0 && (!workspace || workspace_bytes < need)) return XHC_EWORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -279,7 +290,8 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
              launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, d->Kr, d->gram_schmidt, p, Hpost, wb, s));
   }
   XHC_STEP("post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa,
-                                           conv_w, idx, p, Hres, Hpost, wb, nullptr, nullptr, nullptr, s));
+                                           conv_w, idx, p, Hres, Hpost, wb, nullptr, nullptr, nullptr, Xact_save,
+                                           s));
   return hip_status(e);
 }
 
@@ -314,12 +326,12 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
   XHC_STEP("flash_proj_full",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nf, nullptr, d->k, part, s));
   XHC_STEP("flash_route", launch_pre_route(part, proj_chunks(NC), nf, d->T, d->N, d->m, d->k, Q, d->C, colsum,
-                                           alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, s));
+                                           alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, nullptr, 0, 0, s));
   XHC_STEP("flash_proj_active",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act1, na, idx, d->k, part, s));
   XHC_STEP("flash_coef1", launch_pre_coef(part, proj_chunks(kC), na, d->T, d->k, 1, 0, d->C, alpha_post1, nullptr,
                                           b_post1, nullptr, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost1,
-                                          nullptr, sums, s));
+                                          nullptr, sums, nullptr, 0, 0, 0, s));
   XHC_STEP("flash_dense_read",
            launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, Q, idx, d->k, input1, base, s));
   return hip_status(e);
@@ -364,7 +376,7 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
   }
   XHC_STEP("flash_post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, Kq, d->kappa,
                                                  conv_w, idx, p, Hres, Hpost, wb, last ? nullptr : Hpre_next,
-                                                 last ? nullptr : base_next, last ? nullptr : input_next, s));
+                                                 last ? nullptr : base_next, last ? nullptr : input_next, nullptr, s));
   if (!last) {
     // mappings of sublayer q + 1 from the updated active rows (Alg. xHC-Flash, MLP step; App. E.2)
     const int Kn = flash_Kq(d, q + 1);
@@ -377,8 +389,63 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
     XHC_STEP("flash_coef_next",
              launch_pre_coef(part, proj_chunks(kC), na, d->T, d->k, Kn, with_res, d->C, alpha_next,
                              with_res ? alpha_next + 1 : nullptr, b_post_next, b_res_next, d->eps, d->sinkhorn_iters,
-                             d->clamp_delta, Hpost_next, Hres_next, sums, s));
+                             d->clamp_delta, Hpost_next, Hres_next, sums, nullptr, 0, 0, 0, s));
   }
+  return hip_status(e);
+}
+
+// ---------------------------------------------------------------- backward
+
+xhc_status xhc_post_bwd(const xhc_dims* d, const void* dXn, void* X, const void* Xact, const void* F,
+                        const float* conv_w, const int32_t* idx, const float* p, const float* Hres,
+                        const float* Hpost, void* dX, void* dF, float* dHres, float* dHpost, float* dp,
+                        float* dconv_w, void* workspace, size_t workspace_bytes, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (d->T == 0) return XHC_OK;
+  if (!dXn || !X || !Xact || !F || !idx || !p || !Hres || !Hpost || !dX || !dF || !dHres || !dHpost || !dp ||
+      !workspace)
+    return XHC_EINVAL;
+  if ((d->Kr > 1) != (conv_w != nullptr) || (d->Kr > 1) != (dconv_w != nullptr)) return XHC_EINVAL;
+  if (dX == dXn || dX == X || dF == F) return XHC_EINVAL;
+  if (!aligned16(dXn) || !aligned16(X) || !aligned16(Xact) || !aligned16(F) || !aligned16(dX) || !aligned16(dF) ||
+      (conv_w && !aligned16(conv_w)) || (dconv_w && !aligned16(dconv_w)))
+    return XHC_EUNSUPPORTED;
+  if (workspace_bytes < bwd_post_ws_bytes(d)) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  hipError_t e = hipSuccess;
+  XHC_STEP("post_bwd", launch_bwd_post(d, dXn, X, Xact, F, conv_w, idx, p, Hres, Hpost, dX, dF, dHres, dHpost, dp,
+                                       dconv_w, reinterpret_cast<char*>(workspace), s));
+  return hip_status(e);
+}
+
+xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full, const float* W_r,
+                       const float* W_pre, const float* W_res, const float* W_post, const float* alpha,
+                       const float* b_res, const float* saved, const int32_t* idx, const float* p,
+                       const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
+                       const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
+                       float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, void* workspace,
+                       size_t workspace_bytes, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (!bwd_pre_supported(d)) return XHC_EUNSUPPORTED;
+  if (d->T == 0) return XHC_OK;
+  if (!X || !packed_full || !W_r || !W_pre || !W_res || !W_post || !alpha || !b_res || !saved || !idx || !p ||
+      !Hpre || !Hpost || !d_input || !dHres || !dHpost || !dp || !dX || !dW_r || !dW_pre || !dW_res || !dW_post ||
+      !dalpha || !db_pre || !db_res || !db_post || !workspace)
+    return XHC_EINVAL;
+  if (dX == X) return XHC_EINVAL;
+  if (!aligned16(X) || !aligned16(d_input) || !aligned16(dX)) return XHC_EUNSUPPORTED;
+  if (workspace_bytes < bwd_pre_ws_bytes(d)) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
+                                                       packed_frag_bytes(NC_of(d), 2 * d->N));
+  hipError_t e = hipSuccess;
+  XHC_STEP("pre_bwd", launch_bwd_pre(d, X, colsum, W_r, W_pre, W_res, W_post, alpha, b_res, saved, idx, p, Hpre,
+                                     Hpost, d_input, dHres, dHpost, dp, dX, dW_r, dW_pre, dW_res, dW_post, dalpha,
+                                     db_pre, db_res, db_post, reinterpret_cast<char*>(workspace), s));
   return hip_status(e);
 }
 

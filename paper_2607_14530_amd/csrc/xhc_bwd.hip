@@ -1,0 +1,935 @@
+// Backward of a full xHC sublayer (reverse mode of xhc_pre + xhc_post).
+//
+// post backward
+//  k_bwd_post_dots    per token and channel chunk: <dY_j, a_l>, <dY_j, e_b> and the
+//                     Gram matrix of the components e_b (partials)
+//  k_bwd_post_token   per token: dH^res, dH^post, dp; reverse of the Gram-Schmidt
+//                     coefficients; coefficients of de_b in terms of dY_j and e_b'
+//  k_bwd_post_elem    per element: gradient pass-through of the untouched rows,
+//                     mixing gradient of the active rows, restore of the active rows,
+//                     de_b (component gradients)
+//  k_bwd_conv         dF = de_0 + anti-causal convolution of de_j;  k_bwd_convw: kernel
+//                     gradient partials over token chunks
+// pre backward
+//  k_bwd_dhpre        per token and chunk: <d input, x_i> partials
+//  k_bwd_pre_token    per token: sigmoid / Sinkhorn / routing reverses, norm-correction
+//                     scalars, per-token gating and bias gradients
+//  k_bwd_full_rows    weight-stationary over rows of [W_r | W_pre]: dX of every row,
+//                     dW_r and dW_pre
+//  k_bwd_act_rows     weight-stationary over rows of [W_post | W_res]: dX of the active
+//                     rows, dW_post and dW_res partials
+//  k_colsum_rows      deterministic column sums (token reductions)
+#include "xhc_device.h"
+#include "xhc_launch.h"
+
+namespace xhc {
+
+// ------------------------------------------------------------ small-matrix reverses
+
+// Reverse of gram_schmidt_basis: given G, V = GS(G) and the cotangent dV,
+// return dG (G's entries taken as independent).
+__device__ inline void gram_schmidt_basis_reverse(const double (&G)[kMaxKr][kMaxKr], int Kr,
+                                                  const double (&dV_in)[kMaxKr][kMaxKr],
+                                                  double (&dG)[kMaxKr][kMaxKr]) {
+  // recompute the forward quantities
+  double V[kMaxKr][kMaxKr], nrm[kMaxKr], dot[kMaxKr][kMaxKr], c[kMaxKr][kMaxKr];
+  bool zero[kMaxKr];
+  for (int i = 0; i < kMaxKr; ++i)
+    for (int b = 0; b < kMaxKr; ++b) { V[i][b] = (i == b) ? 1.0 : 0.0; dot[i][b] = 0.0; c[i][b] = 0.0; dG[i][b] = 0.0; }
+  for (int j = 0; j < Kr; ++j) {
+    for (int i = 0; i < j; ++i) {
+      if (zero[i]) continue;
+      double d = 0.0;
+      for (int b = 0; b < kMaxKr; ++b) d += V[i][b] * G[j][b];
+      dot[j][i] = d;
+      c[j][i] = d / nrm[i];
+      for (int b = 0; b < kMaxKr; ++b) V[j][b] -= c[j][i] * V[i][b];
+    }
+    double n = 0.0;
+    for (int a = 0; a < kMaxKr; ++a)
+      for (int b = 0; b < kMaxKr; ++b) n += V[j][a] * G[a][b] * V[j][b];
+    nrm[j] = n;
+    zero[j] = !(n > 1e-6 * G[j][j]);
+  }
+  double dV[kMaxKr][kMaxKr], dnrm[kMaxKr];
+  for (int i = 0; i < kMaxKr; ++i) {
+    dnrm[i] = 0.0;
+    for (int b = 0; b < kMaxKr; ++b) dV[i][b] = dV_in[i][b];
+  }
+  for (int j = Kr - 1; j >= 0; --j) {
+    // nrm[j] = V_j^T G V_j (the zero decision is piecewise constant)
+    if (dnrm[j] != 0.0) {
+      for (int a = 0; a < kMaxKr; ++a) {
+        double gv = 0.0;
+        for (int b = 0; b < kMaxKr; ++b) gv += G[a][b] * V[j][b];
+        dV[j][a] += 2.0 * gv * dnrm[j];
+        for (int b = 0; b < kMaxKr; ++b) dG[a][b] += dnrm[j] * V[j][a] * V[j][b];
+      }
+    }
+    // V_j = e_j - sum_i c_ji V_i with c_ji = <e_j, v_i> / nrm_i
+    for (int i = j - 1; i >= 0; --i) {
+      if (zero[i]) continue;
+      double dc = 0.0;
+      for (int b = 0; b < kMaxKr; ++b) dc -= dV[j][b] * V[i][b];
+      for (int b = 0; b < kMaxKr; ++b) dV[i][b] -= c[j][i] * dV[j][b];
+      const double ddot = dc / nrm[i];
+      dnrm[i] -= dc * dot[j][i] / (nrm[i] * nrm[i]);
+      for (int b = 0; b < kMaxKr; ++b) {
+        dV[i][b] += ddot * G[j][b];
+        dG[j][b] += ddot * V[i][b];
+      }
+    }
+  }
+}
+
+// Forward Sinkhorn state after `steps` normalisations (rows first) of exp(L - rowmax).
+__device__ inline void sinkhorn_steps(const float (&L)[kMaxK * kMaxK], int k, int steps, float (&M)[kMaxK * kMaxK]) {
+  for (int j = 0; j < k; ++j) {
+    float mx = L[j * kMaxK];
+    for (int l = 1; l < k; ++l) mx = fmaxf(mx, L[j * kMaxK + l]);
+    for (int l = 0; l < k; ++l) M[j * kMaxK + l] = __expf(L[j * kMaxK + l] - mx);
+  }
+  for (int s = 0; s < steps; ++s) {
+    if ((s & 1) == 0) {
+      for (int j = 0; j < k; ++j) {
+        float sum = 0.f;
+        for (int l = 0; l < k; ++l) sum += M[j * kMaxK + l];
+        const float r = 1.0f / sum;
+        for (int l = 0; l < k; ++l) M[j * kMaxK + l] *= r;
+      }
+    } else {
+      for (int l = 0; l < k; ++l) {
+        float sum = 0.f;
+        for (int j = 0; j < k; ++j) sum += M[j * kMaxK + l];
+        const float r = 1.0f / sum;
+        for (int j = 0; j < k; ++j) M[j * kMaxK + l] *= r;
+      }
+    }
+  }
+}
+
+// dL of H = clamp(SK_iters(exp(L))) given dH; the forward iterates are recomputed.
+__device__ inline void sinkhorn_clamp_reverse(const float (&L)[kMaxK * kMaxK], int k, int iters, float delta,
+                                              const float (&dH)[kMaxK * kMaxK], float (&dL)[kMaxK * kMaxK]) {
+  float M[kMaxK * kMaxK], g[kMaxK * kMaxK];
+  const int steps = 2 * iters;
+  sinkhorn_steps(L, k, steps, M);
+  // row clamp
+  for (int j = 0; j < k; ++j) {
+    float s = 0.f;
+    for (int l = 0; l < k; ++l) s += M[j * kMaxK + l];
+    if (s > 1.0f + delta) {
+      float dot = 0.f;
+      for (int l = 0; l < k; ++l) dot += dH[j * kMaxK + l] * (M[j * kMaxK + l] / s);
+      for (int l = 0; l < k; ++l) g[j * kMaxK + l] = (dH[j * kMaxK + l] - dot) / s;
+    } else {
+      for (int l = 0; l < k; ++l) g[j * kMaxK + l] = dH[j * kMaxK + l];
+    }
+  }
+  for (int s = steps - 1; s >= 0; --s) {
+    sinkhorn_steps(L, k, s, M);   // input of normalisation step s
+    if ((s & 1) == 0) {           // row normalisation: y = m / sum_l m
+      for (int j = 0; j < k; ++j) {
+        float sum = 0.f;
+        for (int l = 0; l < k; ++l) sum += M[j * kMaxK + l];
+        float dot = 0.f;
+        for (int l = 0; l < k; ++l) dot += g[j * kMaxK + l] * (M[j * kMaxK + l] / sum);
+        for (int l = 0; l < k; ++l) g[j * kMaxK + l] = (g[j * kMaxK + l] - dot) / sum;
+      }
+    } else {                      // column normalisation
+      for (int l = 0; l < k; ++l) {
+        float sum = 0.f;
+        for (int j = 0; j < k; ++j) sum += M[j * kMaxK + l];
+        float dot = 0.f;
+        for (int j = 0; j < k; ++j) dot += g[j * kMaxK + l] * (M[j * kMaxK + l] / sum);
+        for (int j = 0; j < k; ++j) g[j * kMaxK + l] = (g[j * kMaxK + l] - dot) / sum;
+      }
+    }
+  }
+  sinkhorn_steps(L, k, 0, M);     // exp(L - rowmax); the shift does not change H
+  for (int j = 0; j < k; ++j)
+    for (int l = 0; l < k; ++l) dL[j * kMaxK + l] = g[j * kMaxK + l] * M[j * kMaxK + l];
+}
+
+// ------------------------------------------------------------ post backward
+
+// Layout of the per-token dot products (compile-time strides, KM >= k):
+// [<dY_j, a_l> (KM x KM) | <dY_j, e_b> (KM x KR) | Gram of e (upper triangle)]
+template <int KR, int KM>
+struct PostDots {
+  static constexpr int NG = KR * (KR + 1) / 2;
+  static constexpr int ND = KM * KM + KM * KR + NG;
+  static __host__ __device__ constexpr int ya(int j, int l) { return j * KM + l; }
+  static __host__ __device__ constexpr int ye(int j, int b) { return KM * KM + j * KR + b; }
+  static __host__ __device__ constexpr int gram(int p) { return KM * KM + KM * KR + p; }
+};
+
+template <typename TS, int KR, int KM>
+__global__ __launch_bounds__(256) void k_bwd_post_dots(const TS* __restrict__ dXn, const TS* __restrict__ Xact,
+                                                       const TS* __restrict__ F, int64_t T, int64_t S, int N, int C,
+                                                       int k, int kap0, int kap1, int kap2,
+                                                       const float* __restrict__ conv_w,
+                                                       const int32_t* __restrict__ idx, float* __restrict__ part) {
+  using PD = PostDots<KR, KM>;
+  constexpr int MAXD = PD::ND;
+  __shared__ float red[4][MAXD];
+  const int nd = MAXD;
+  const int64_t ncb = post_chunks(C);
+  const int64_t t = blockIdx.x / ncb, cb = blockIdx.x % ncb;
+  const int c = (int)(cb * 256 + threadIdx.x) * 8;
+  float acc[MAXD];
+#pragma unroll
+  for (int i = 0; i < MAXD; ++i) acc[i] = 0.f;
+  if (c < C) {
+    const int kap[3] = {kap0, kap1, kap2};
+    float e[KR][8];
+    components<TS, KR>(F, conv_w, t, t % S, C, c, kap, e);
+    float dy[KM][8], a[KM][8];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) { dy[j][q] = 0.f; a[j][q] = 0.f; }
+      if (j < k) {
+        Vec8<TS>::load(dXn + (t * N + idx[t * k + j]) * (int64_t)C + c, dy[j]);
+        Vec8<TS>::load(Xact + (t * k + j) * (int64_t)C + c, a[j]);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+#pragma unroll
+      for (int l = 0; l < KM; ++l)
+        if (j < k && l < k)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[PD::ya(j, l)] = fmaf(dy[j][q], a[l][q], acc[PD::ya(j, l)]);
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+#pragma unroll
+      for (int b = 0; b < KR; ++b)
+        if (j < k)
+#pragma unroll
+          for (int q = 0; q < 8; ++q) acc[PD::ye(j, b)] = fmaf(dy[j][q], e[b][q], acc[PD::ye(j, b)]);
+    int pi = PD::gram(0);
+#pragma unroll
+    for (int a0 = 0; a0 < KR; ++a0)
+#pragma unroll
+      for (int b = a0; b < KR; ++b, ++pi)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) acc[pi] = fmaf(e[a0][q], e[b][q], acc[pi]);
+  }
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+#pragma unroll
+  for (int i = 0; i < MAXD; ++i) {
+    float v = acc[i];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if (lane == 0) red[wave][i] = v;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < nd; i += 256) part[(cb * nd + i) * T + t] = red[0][i] + red[1][i] + red[2][i] + red[3][i];
+}
+
+// Per token: dH^res, dH^post, dp and the coefficients of the component
+// gradients: de_b = sum_j CY[b][j] dY_j + sum_b' CE[b][b'] e_b'.
+template <int KR, int KM>
+__global__ __launch_bounds__(128) void k_bwd_post_token(const float* __restrict__ part, int64_t nchunk, int64_t T,
+                                                        int k, int gram_schmidt, const float* __restrict__ p,
+                                                        const float* __restrict__ Hpost, float* __restrict__ dHres,
+                                                        float* __restrict__ dHpost, float* __restrict__ dp,
+                                                        float* __restrict__ coef) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  using PD = PostDots<KR, KM>;
+  const int nd = PD::ND;
+  auto sum = [&](int i) {
+    float s = 0.f;
+    for (int64_t c = 0; c < nchunk; ++c) s += part[(c * nd + i) * T + t];
+    return s;
+  };
+  for (int j = 0; j < k; ++j)
+    for (int l = 0; l < k; ++l) dHres[(t * k + j) * k + l] = sum(PD::ya(j, l));
+  double D2[kMaxK][kMaxKr];   // <dY_j, e_b>
+  for (int j = 0; j < kMaxK; ++j)
+    for (int b = 0; b < kMaxKr; ++b) D2[j][b] = (j < k && b < KR) ? (double)sum(PD::ye(j, b)) : 0.0;
+  double G[kMaxKr][kMaxKr];
+  int pi = PD::gram(0);
+  for (int a = 0; a < kMaxKr; ++a)
+    for (int b = a; b < kMaxKr; ++b) {
+      if (a < KR && b < KR) {
+        G[a][b] = G[b][a] = sum(pi);
+        ++pi;
+      } else {
+        G[a][b] = G[b][a] = 0.0;
+      }
+    }
+  double V[kMaxKr][kMaxKr];
+  if (gram_schmidt && KR > 1) {
+    gram_schmidt_basis(G, KR, V);
+  } else {
+    for (int i = 0; i < kMaxKr; ++i)
+      for (int b = 0; b < kMaxKr; ++b) V[i][b] = (i == b) ? 1.0 : 0.0;
+  }
+  // <dY_j, v_r> = sum_b V[r][b] <dY_j, e_b>
+  double P[kMaxKr][kMaxKr];   // P[r][b] = <dv_r, e_b>, dv_r = sum_j p_j H^post[j][r] dY_j
+  for (int r = 0; r < kMaxKr; ++r)
+    for (int b = 0; b < kMaxKr; ++b) P[r][b] = 0.0;
+  for (int j = 0; j < k; ++j) {
+    const double pj = p[t * k + j];
+    double dpj = 0.0;
+    for (int r = 0; r < KR; ++r) {
+      double yv = 0.0;
+      for (int b = 0; b < KR; ++b) yv += V[r][b] * D2[j][b];
+      const double h = Hpost[(t * k + j) * KR + r];
+      dHpost[(t * k + j) * KR + r] = (float)(pj * yv);
+      dpj += h * yv;
+      for (int b = 0; b < KR; ++b) P[r][b] += pj * h * D2[j][b];
+    }
+    dp[t * k + j] = (float)dpj;
+  }
+  double dG[kMaxKr][kMaxKr];
+  for (int a = 0; a < kMaxKr; ++a)
+    for (int b = 0; b < kMaxKr; ++b) dG[a][b] = 0.0;
+  if (gram_schmidt && KR > 1) gram_schmidt_basis_reverse(G, KR, P, dG);
+  // coef layout per token: CY [KR][k] then CE [KR][KR]
+  float* cf = coef + t * (KR * kMaxK + KR * KR);
+  for (int b = 0; b < KR; ++b) {
+    for (int j = 0; j < k; ++j) {
+      double s = 0.0;
+      for (int r = 0; r < KR; ++r) s += V[r][b] * (double)Hpost[(t * k + j) * KR + r];
+      cf[b * kMaxK + j] = (float)((double)p[t * k + j] * s);
+    }
+    for (int b2 = 0; b2 < KR; ++b2) cf[KR * kMaxK + b * KR + b2] = (float)(dG[b][b2] + dG[b2][b]);
+  }
+}
+
+// Element pass of the post backward (8 channels of one token per thread).
+template <typename TS, int KR, int KM>
+__global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* __restrict__ dXn, TS* __restrict__ X,
+                                                       const TS* __restrict__ Xact, const TS* __restrict__ F,
+                                                       int64_t T, int64_t S, int N, int C, int k, int kap0, int kap1,
+                                                       int kap2, const float* __restrict__ conv_w,
+                                                       const int32_t* __restrict__ idx,
+                                                       const float* __restrict__ Hres,
+                                                       const float* __restrict__ coef, TS* __restrict__ dX,
+                                                       TS* __restrict__ dF, float* __restrict__ de) {
+  const int64_t ncb = post_chunks(C);
+  const int64_t t = blockIdx.x / ncb;
+  const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
+  if (c >= C) return;
+  uint64_t act = 0;
+  int32_t rows[kMaxK];
+  for (int j = 0; j < k; ++j) {
+    rows[j] = idx[t * k + j];
+    act |= 1ull << rows[j];
+  }
+  // untouched rows pass their gradient through
+  for (int i = 0; i < N; ++i) {
+    if ((act >> i) & 1ull) continue;
+    float g[8];
+    Vec8<TS>::load(dXn + (t * N + i) * (int64_t)C + c, g);
+    Vec8<TS>::store(dX + (t * N + i) * (int64_t)C + c, g);
+  }
+  float dy[KM][8];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) dy[j][q] = 0.f;
+    if (j < k) Vec8<TS>::load(dXn + (t * N + rows[j]) * (int64_t)C + c, dy[j]);
+  }
+  // active rows: mixing gradient sum_j H^res[j][l] dY_j; restore the pre-update rows
+  for (int l = 0; l < k; ++l) {
+    float g[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) g[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      if (j < k) {
+        const float h = Hres[(t * k + j) * k + l];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) g[q] = fmaf(h, dy[j][q], g[q]);
+      }
+    }
+    Vec8<TS>::store(dX + (t * N + rows[l]) * (int64_t)C + c, g);
+    float a[8];
+    Vec8<TS>::load(Xact + (t * k + l) * (int64_t)C + c, a);
+    Vec8<TS>::store(X + (t * N + rows[l]) * (int64_t)C + c, a);
+  }
+  const int kap[3] = {kap0, kap1, kap2};
+  float e[KR][8];
+  if (KR > 1) components<TS, KR>(F, conv_w, t, t % S, C, c, kap, e);
+  const float* cf = coef + t * (KR * kMaxK + KR * KR);
+#pragma unroll
+  for (int b = 0; b < KR; ++b) {
+    float g[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) g[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      if (j < k) {
+        const float w = cf[b * kMaxK + j];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) g[q] = fmaf(w, dy[j][q], g[q]);
+      }
+    }
+    if (KR > 1) {
+#pragma unroll
+      for (int b2 = 0; b2 < KR; ++b2) {
+        const float w = cf[KR * kMaxK + b * KR + b2];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) g[q] = fmaf(w, e[b2][q], g[q]);
+      }
+      float* dst = de + ((int64_t)b * T + t) * C + c;
+      reinterpret_cast<float4*>(dst)[0] = make_float4(g[0], g[1], g[2], g[3]);
+      reinterpret_cast<float4*>(dst)[1] = make_float4(g[4], g[5], g[6], g[7]);
+    } else {
+      Vec8<TS>::store(dF + t * C + c, g);
+    }
+  }
+}
+
+// dF[t] = de_0[t] + sum_j sum_{i < kappa_j} w_j[i] de_j[t + i] over the part of the
+// window inside t's sequence (the reverse of the causal convolution).
+template <typename TS>
+__global__ __launch_bounds__(256) void k_bwd_conv(const float* __restrict__ de, int64_t T, int64_t S, int C, int Kr,
+                                                  int kap0, int kap1, int kap2, const float* __restrict__ conv_w,
+                                                  TS* __restrict__ dF) {
+  const int64_t ncb = post_chunks(C);
+  const int64_t t = blockIdx.x / ncb;
+  const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
+  if (c >= C) return;
+  const int kap[3] = {kap0, kap1, kap2};
+  const int64_t room = S - 1 - (t % S);   // tokens after t in its sequence
+  float g[8];
+  {
+    const float4* p4 = reinterpret_cast<const float4*>(de + t * C + c);
+    const float4 u = p4[0], v = p4[1];
+    g[0] = u.x; g[1] = u.y; g[2] = u.z; g[3] = u.w; g[4] = v.x; g[5] = v.y; g[6] = v.z; g[7] = v.w;
+  }
+  int row = 0;
+  for (int j = 1; j < Kr; ++j) {
+    const int kj = kap[j - 1];
+    for (int i = 0; i < kj && i <= room; ++i) {
+      const float4* w4 = reinterpret_cast<const float4*>(conv_w + (int64_t)(row + i) * C + c);
+      const float4* d4 = reinterpret_cast<const float4*>(de + ((int64_t)j * T + t + i) * C + c);
+      const float4 wa = w4[0], wb = w4[1], da = d4[0], db = d4[1];
+      g[0] = fmaf(wa.x, da.x, g[0]); g[1] = fmaf(wa.y, da.y, g[1]);
+      g[2] = fmaf(wa.z, da.z, g[2]); g[3] = fmaf(wa.w, da.w, g[3]);
+      g[4] = fmaf(wb.x, db.x, g[4]); g[5] = fmaf(wb.y, db.y, g[5]);
+      g[6] = fmaf(wb.z, db.z, g[6]); g[7] = fmaf(wb.w, db.w, g[7]);
+    }
+    row += kj;
+  }
+  Vec8<TS>::store(dF + t * C + c, g);
+}
+
+// Kernel-gradient partials: part[chunk][row][c] = sum_{t in chunk} F[t - i][c] de_j[t][c]
+// for row = (branch j, tap i), only where t - i lies in t's sequence.
+constexpr int kConvChunk = 256;   // tokens per partial
+template <typename TS>
+__global__ __launch_bounds__(256) void k_bwd_convw(const float* __restrict__ de, const TS* __restrict__ F, int64_t T,
+                                                   int64_t S, int C, int Kr, int kap0, int kap1, int kap2,
+                                                   float* __restrict__ part) {
+  // grid: (channel blocks of 2048) x (conv rows) x (token chunks)
+  const int c = (int)(blockIdx.x * 256 + threadIdx.x) * 8;
+  const int row = blockIdx.y;
+  const int64_t chunk = blockIdx.z;
+  if (c >= C) return;
+  const int kap[3] = {kap0, kap1, kap2};
+  int j = 1, base = 0;
+  while (j < Kr && row >= base + kap[j - 1]) { base += kap[j - 1]; ++j; }
+  const int i = row - base;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  const int64_t t0 = chunk * kConvChunk, t1 = (t0 + kConvChunk < T) ? t0 + kConvChunk : T;
+  for (int64_t t = t0; t < t1; ++t) {
+    if ((t % S) < i) continue;
+    float f[8];
+    Vec8<TS>::load(F + (t - i) * C + c, f);
+    const float4* d4 = reinterpret_cast<const float4*>(de + ((int64_t)j * T + t) * C + c);
+    const float4 da = d4[0], db = d4[1];
+    acc[0] = fmaf(f[0], da.x, acc[0]); acc[1] = fmaf(f[1], da.y, acc[1]);
+    acc[2] = fmaf(f[2], da.z, acc[2]); acc[3] = fmaf(f[3], da.w, acc[3]);
+    acc[4] = fmaf(f[4], db.x, acc[4]); acc[5] = fmaf(f[5], db.y, acc[5]);
+    acc[6] = fmaf(f[6], db.z, acc[6]); acc[7] = fmaf(f[7], db.w, acc[7]);
+  }
+  float* dst = part + ((int64_t)chunk * gridDim.y + row) * C + c;
+  reinterpret_cast<float4*>(dst)[0] = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  reinterpret_cast<float4*>(dst)[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
+}
+
+// out[col] = sum_r in[r][col] over nrows rows (row stride = ncols), fixed order.
+__global__ __launch_bounds__(256) void k_colsum_rows(const float* __restrict__ in, int64_t nrows, int64_t ncols,
+                                                     float* __restrict__ out) {
+  const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (col >= ncols) return;
+  float s = 0.f;
+  for (int64_t r0 = 0; r0 < nrows; r0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = (r0 + u < nrows) ? in[(r0 + u) * ncols + col] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  out[col] = s;
+}
+
+// out[col] = sum over T of in[t][col], for few columns: one block per column,
+// threads stride the tokens, tree reduction in a fixed order.
+__global__ __launch_bounds__(256) void k_sum_tokens(const float* __restrict__ in, int64_t T, int ncols,
+                                                    float* __restrict__ out) {
+  __shared__ float red[256];
+  const int col = blockIdx.x;
+  float s = 0.f;
+  for (int64_t t = threadIdx.x; t < T; t += 256) s += in[t * ncols + col];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[col] = red[0];
+}
+
+// ------------------------------------------------------------ pre backward
+
+// <d input, x_i> partials: part[chunk][i][t]
+template <typename TS>
+__global__ __launch_bounds__(256) void k_bwd_dhpre(const TS* __restrict__ X, const TS* __restrict__ din, int64_t T,
+                                                   int N, int C, float* __restrict__ part) {
+  __shared__ float red[4][kMaxN];
+  const int64_t ncb = post_chunks(C);
+  const int64_t t = blockIdx.x / ncb, cb = blockIdx.x % ncb;
+  const int c = (int)(cb * 256 + threadIdx.x) * 8;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  float g[8];
+  if (c < C) Vec8<TS>::load(din + t * C + c, g);
+  for (int i = 0; i < N; ++i) {
+    float v = 0.f;
+    if (c < C) {
+      float x[8];
+      Vec8<TS>::load(X + (t * N + i) * (int64_t)C + c, x);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v = fmaf(g[q], x[q], v);
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if (lane == 0) red[wave][i] = v;
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < N; i += 256) part[(cb * N + i) * T + t] = red[0][i] + red[1][i] + red[2][i] + red[3][i];
+}
+
+// Per-token record written by k_bwd_pre_token (floats):
+//   [dz_r (N) | dz_pre (N) | dz_act (NA) | r | r_ln | mu | beta_pre | m1 | m2 | r_a | beta_a]
+// and per-token gating/bias gradients pg: [dalpha_pre, dalpha_res, dalpha_post | db_pre (N) |
+// db_res (k*k) | db_post (k*Kr)].
+__host__ __device__ inline int tok_floats(int N, int NA) { return 2 * N + NA + 8; }
+__host__ __device__ inline int pg_floats(int N, int k, int Kr) { return 3 + N + k * k + k * Kr; }
+
+__global__ __launch_bounds__(128) void k_bwd_pre_token(
+    const float* __restrict__ part, int64_t nchunk, int64_t T, int N, int m, int k, int Kr, int C,
+    const float* __restrict__ saved, const float* __restrict__ colsum, const float* __restrict__ alpha,
+    const float* __restrict__ b_res, const int32_t* __restrict__ idx, const float* __restrict__ p,
+    const float* __restrict__ Hpre, const float* __restrict__ Hpost, const float* __restrict__ dHres,
+    const float* __restrict__ dHpost, const float* __restrict__ dp, float eps, int iters, float delta,
+    float* __restrict__ tok, float* __restrict__ pg) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  const int NA = k * Kr + k * k, ns = saved_floats(N, k, Kr);
+  const float* sv = saved + t * ns;
+  float* tk = tok + t * tok_floats(N, NA);
+  float* g = pg + t * pg_floats(N, k, Kr);
+  const float mu = sv[ns - 4], nu = sv[ns - 3], nu_a = sv[ns - 2];
+  const float NC = (float)N * (float)C, kC = (float)k * (float)C;
+  const float r = 1.0f / sqrtf(nu + eps), r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + eps);
+  const float r_a = 1.0f / sqrtf(nu_a + eps);
+  const float a_pre = alpha[0], a_res = alpha[1], a_post = alpha[2];
+  // pre-map: H = sigma(a z + b)
+  float da_pre = 0.f, bp = 0.f;
+  for (int i = 0; i < N; ++i) {
+    float dh = 0.f;
+    for (int64_t c = 0; c < nchunk; ++c) dh += part[(c * N + i) * T + t];
+    const float h = Hpre[t * N + i];
+    const float ds = dh * h * (1.0f - h);
+    const float z = sv[N + i];
+    tk[N + i] = a_pre * ds;
+    da_pre += ds * z;
+    g[3 + i] = ds;
+    bp += a_pre * ds * z;
+  }
+  const float beta_pre = r * r * bp / NC;
+  // router: only routed slots carry gradient, through p = sigma(z_r)
+  for (int i = 0; i < N; ++i) tk[i] = 0.f;
+  float m1 = 0.f, m2 = 0.f;
+  for (int j = m; j < k; ++j) {
+    const int i = idx[t * k + j];
+    const float pj = p[t * k + j];
+    const float dz = dp[t * k + j] * pj * (1.0f - pj);
+    tk[i] = dz;
+    m1 += colsum[i] * dz;
+    m2 += sv[i] * dz;
+  }
+  m1 /= NC;
+  m2 /= NC;
+  // post-map: H = 2 sigma(a z + b)
+  float da_post = 0.f, ba = 0.f;
+  for (int o = 0; o < k * Kr; ++o) {
+    const float h = Hpost[t * k * Kr + o];
+    const float du = dHpost[t * k * Kr + o] * h * (1.0f - 0.5f * h);
+    const float z = sv[2 * N + o];
+    tk[2 * N + o] = a_post * du;
+    da_post += du * z;
+    g[3 + N + k * k + o] = du;
+    ba += a_post * du * z;
+  }
+  // residual map: H = clamp(SK(exp(a z + b)))
+  float L[kMaxK * kMaxK], dH[kMaxK * kMaxK], dL[kMaxK * kMaxK];
+  for (int j = 0; j < kMaxK; ++j)
+    for (int l = 0; l < kMaxK; ++l) {
+      const bool in = j < k && l < k;
+      L[j * kMaxK + l] = in ? a_res * sv[2 * N + k * Kr + j * k + l] + b_res[j * k + l] : 0.f;
+      dH[j * kMaxK + l] = in ? dHres[(t * k + j) * k + l] : 0.f;
+      dL[j * kMaxK + l] = 0.f;
+    }
+  sinkhorn_clamp_reverse(L, k, iters, delta, dH, dL);
+  float da_res = 0.f;
+  for (int j = 0; j < k; ++j)
+    for (int l = 0; l < k; ++l) {
+      const float z = sv[2 * N + k * Kr + j * k + l];
+      const float d = dL[j * kMaxK + l];
+      tk[2 * N + k * Kr + j * k + l] = a_res * d;
+      da_res += d * z;
+      g[3 + N + j * k + l] = d;
+      ba += a_res * d * z;
+    }
+  g[0] = da_pre;
+  g[1] = da_res;
+  g[2] = da_post;
+  float* sc = tk + 2 * N + NA;
+  sc[0] = r;
+  sc[1] = r_ln;
+  sc[2] = mu;
+  sc[3] = beta_pre;
+  sc[4] = m1;
+  sc[5] = m2;
+  sc[6] = r_a;
+  sc[7] = r_a * r_a * ba / kC;
+}
+
+// Weight-stationary pass over rows K = i*C + c of [W_r | W_pre] (one row per
+// thread) and a chunk of tokens.  Per token:
+//   dX[t,i,c] += H^pre_i d_in[c] + r (W_pre dz_pre) - beta_pre x
+//               + r_ln ((W_r dz_r) - m1 - r_ln (x - mu) m2)
+// and the row's weight gradients accumulate x r dz_pre and r_ln (x - mu) dz_r.
+constexpr int kRowTok = 32;   // tokens staged in LDS per step
+template <typename TS, int NN>
+__global__ __launch_bounds__(256) void k_bwd_full_rows(const TS* __restrict__ X, const TS* __restrict__ din,
+                                                       TS* __restrict__ dX, const float* __restrict__ W_r,
+                                                       const float* __restrict__ W_pre, const float* __restrict__ Hpre,
+                                                       const float* __restrict__ tok, int64_t T, int C, int NA,
+                                                       int64_t tchunk, float* __restrict__ dWr_part,
+                                                       float* __restrict__ dWp_part) {
+  __shared__ float sdz[kRowTok][2 * NN + 8];
+  __shared__ float shp[kRowTok];
+  const int64_t NC = (int64_t)NN * C;
+  const int64_t K = (int64_t)blockIdx.x * 256 + threadIdx.x;   // row of the weights
+  const bool valid = K < NC;
+  const int i = valid ? (int)(K / C) : 0, c = valid ? (int)(K % C) : 0;
+  const int istream = (int)(((int64_t)blockIdx.x * 256) / C);  // one stream per block (C % 256 == 0)
+  float wr[NN], wp[NN], gr[NN], gp[NN];
+#pragma unroll
+  for (int o = 0; o < NN; ++o) {
+    wr[o] = valid ? __uint_as_float(f2bf(W_r[K * NN + o]) << 16) : 0.f;
+    wp[o] = valid ? __uint_as_float(f2bf(W_pre[K * NN + o]) << 16) : 0.f;
+    gr[o] = 0.f;
+    gp[o] = 0.f;
+  }
+  const int TF = tok_floats(NN, NA);
+  const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
+  for (int64_t tb = t0; tb < t1; tb += kRowTok) {
+    const int nt = (int)((t1 - tb < kRowTok) ? t1 - tb : kRowTok);
+    __syncthreads();
+    for (int q = threadIdx.x; q < nt * (2 * NN + 8); q += 256) {
+      const int u = q / (2 * NN + 8), f = q % (2 * NN + 8);
+      const float* tk = tok + (tb + u) * TF;
+      sdz[u][f] = (f < 2 * NN) ? tk[f] : tk[2 * NN + NA + (f - 2 * NN)];
+    }
+    for (int u = threadIdx.x; u < nt; u += 256) shp[u] = Hpre[(tb + u) * NN + istream];
+    __syncthreads();
+    if (!valid) continue;
+#pragma unroll 4
+    for (int u = 0; u < nt; ++u) {
+      const int64_t t = tb + u;
+      const float* z = sdz[u];
+      const float r = z[2 * NN + 0], r_ln = z[2 * NN + 1], mu = z[2 * NN + 2], bpre = z[2 * NN + 3];
+      const float m1 = z[2 * NN + 4], m2 = z[2 * NN + 5];
+      const int64_t off = t * NC + K;
+      const float x = (sizeof(TS) == 2) ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(X)[off] << 16)
+                                         : reinterpret_cast<const float*>(X)[off];
+      const float gi = (sizeof(TS) == 2) ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(din)[t * C + c] << 16)
+                                          : reinterpret_cast<const float*>(din)[t * C + c];
+      float sr = 0.f, sp = 0.f;
+      const float xh = (x - mu) * r_ln, xr = x * r;
+#pragma unroll
+      for (int o = 0; o < NN; ++o) {
+        sr = fmaf(wr[o], z[o], sr);
+        sp = fmaf(wp[o], z[NN + o], sp);
+        gr[o] = fmaf(xh, z[o], gr[o]);
+        gp[o] = fmaf(xr, z[NN + o], gp[o]);
+      }
+      float g = shp[u] * gi + r * sp - bpre * x + r_ln * (sr - m1) - r_ln * (x - mu) * r_ln * m2;
+      if (sizeof(TS) == 2) {
+        uint16_t* d = reinterpret_cast<uint16_t*>(dX) + off;
+        g += __uint_as_float((uint32_t)*d << 16);
+        *d = (uint16_t)f2bf(g);
+      } else {
+        float* d = reinterpret_cast<float*>(dX) + off;
+        *d += g;
+      }
+    }
+  }
+  if (!valid) return;
+  float* dr = dWr_part + ((int64_t)blockIdx.y * NC + K) * NN;
+  float* dp = dWp_part + ((int64_t)blockIdx.y * NC + K) * NN;
+#pragma unroll
+  for (int o = 0; o < NN; ++o) { dr[o] = gr[o]; dp[o] = gp[o]; }
+}
+
+// Weight-stationary pass over rows K = j*C + c of [W_post | W_res] (slot j):
+//   dX[t, I_j, c] += r_a (W_act dz_act) - beta_a a,   dW_act[K] += r_a a dz_act.
+template <typename TS, int NAMAX>
+__global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, TS* __restrict__ dX,
+                                                      const float* __restrict__ W_post,
+                                                      const float* __restrict__ W_res,
+                                                      const int32_t* __restrict__ idx,
+                                                      const float* __restrict__ tok, int64_t T, int N, int k, int C,
+                                                      int Kr, int64_t tchunk, float* __restrict__ dWa_part) {
+  const int NA = k * Kr + k * k, NP = k * Kr;
+  __shared__ float sdz[kRowTok][NAMAX + 2];
+  __shared__ int sid[kRowTok];
+  const int64_t kC = (int64_t)k * C;
+  const int64_t K = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const bool valid = K < kC;
+  const int j = (int)(((int64_t)blockIdx.x * 256) / C);   // one slot per block (C % 256 == 0)
+  const int c = valid ? (int)(K % C) : 0;
+  float w[NAMAX], ga[NAMAX];
+#pragma unroll
+  for (int o = 0; o < NAMAX; ++o) {
+    float v = 0.f;
+    if (valid && o < NA)
+      v = (o < NP) ? W_post[K * NP + o] : W_res[K * (k * k) + (o - NP)];
+    w[o] = __uint_as_float(f2bf(v) << 16);
+    ga[o] = 0.f;
+  }
+  const int TF = 2 * N + NA + 8;
+  const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
+  for (int64_t tb = t0; tb < t1; tb += kRowTok) {
+    const int nt = (int)((t1 - tb < kRowTok) ? t1 - tb : kRowTok);
+    __syncthreads();
+    for (int q = threadIdx.x; q < nt * (NA + 2); q += 256) {
+      const int u = q / (NA + 2), f = q % (NA + 2);
+      const float* tk = tok + (tb + u) * TF;
+      sdz[u][f] = (f < NA) ? tk[2 * N + f] : tk[2 * N + NA + 6 + (f - NA)];
+    }
+    for (int u = threadIdx.x; u < nt; u += 256) sid[u] = idx[(tb + u) * k + j];
+    __syncthreads();
+    if (!valid) continue;
+#pragma unroll 4
+    for (int u = 0; u < nt; ++u) {
+      const int64_t t = tb + u;
+      const float* z = sdz[u];
+      const float r_a = z[NA], beta_a = z[NA + 1];
+      const int64_t off = (t * N + sid[u]) * (int64_t)C + c;
+      const float a = (sizeof(TS) == 2) ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(X)[off] << 16)
+                                         : reinterpret_cast<const float*>(X)[off];
+      float s = 0.f;
+      const float ar = a * r_a;
+#pragma unroll
+      for (int o = 0; o < NAMAX; ++o) {
+        if (o < NA) {
+          s = fmaf(w[o], z[o], s);
+          ga[o] = fmaf(ar, z[o], ga[o]);
+        }
+      }
+      const float g = r_a * s - beta_a * a;
+      if (sizeof(TS) == 2) {
+        uint16_t* d = reinterpret_cast<uint16_t*>(dX) + off;
+        *d = (uint16_t)f2bf(__uint_as_float((uint32_t)*d << 16) + g);
+      } else {
+        reinterpret_cast<float*>(dX)[off] += g;
+      }
+    }
+  }
+  if (!valid) return;
+  float* dst = dWa_part + ((int64_t)blockIdx.y * kC + K) * NAMAX;
+#pragma unroll
+  for (int o = 0; o < NAMAX; ++o) dst[o] = ga[o];
+}
+
+// ------------------------------------------------------------ launchers
+
+#define XHC_TS_DISPATCH(dt, ...) \
+  if ((dt) == XHC_BF16) { using TS = uint16_t; __VA_ARGS__; } else { using TS = float; __VA_ARGS__; }
+
+hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const void* Xact, const void* F,
+                           const float* conv_w, const int32_t* idx, const float* p, const float* Hres,
+                           const float* Hpost, void* dX, void* dF, float* dHres, float* dHpost, float* dp,
+                           float* dconv_w, char* ws, hipStream_t s) {
+  const int64_t T = d->T, S = d->S;
+  const int N = d->N, C = d->C, k = d->k, Kr = d->Kr;
+  const int64_t ncb = post_chunks(C);
+  const dim3 grid((unsigned)(T * ncb));
+  // workspace: dots partials | coef | de (Kr planes, fp32) | conv partials
+  const int km = k <= 4 ? 4 : 8;
+  const int nd = km * km + km * Kr + Kr * (Kr + 1) / 2;
+  float* part = reinterpret_cast<float*>(ws);
+  float* coef = part + ncb * nd * T;
+  float* de = coef + T * (Kr * kMaxK + Kr * Kr);
+  float* cpart = de + (Kr > 1 ? (int64_t)Kr * T * C : 0);
+  const int* kap = d->kappa;
+#define XHC_BWD_POST(KRV, KMV)                                                                                   \
+  XHC_TS_DISPATCH(d->state_dtype,                                                                                \
+    k_bwd_post_dots<TS, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(dXn),                  \
+        reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, kap[0], kap[1], kap[2], \
+        conv_w, idx, part);                                                                                      \
+    k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, ncb, T, k,               \
+        d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                                     \
+    k_bwd_post_elem<TS, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(dXn),                  \
+        reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, \
+        k, kap[0], kap[1], kap[2], conv_w, idx, Hres, coef, reinterpret_cast<TS*>(dX), reinterpret_cast<TS*>(dF), \
+        de))
+#define XHC_BWD_POST_K(KRV) if (k <= 4) { XHC_BWD_POST(KRV, 4); } else { XHC_BWD_POST(KRV, 8); }
+  switch (Kr) {
+    case 1: XHC_BWD_POST_K(1); break;
+    case 2: XHC_BWD_POST_K(2); break;
+    case 3: XHC_BWD_POST_K(3); break;
+    default: XHC_BWD_POST_K(4); break;
+  }
+#undef XHC_BWD_POST_K
+#undef XHC_BWD_POST
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || Kr == 1) return e;
+  XHC_TS_DISPATCH(d->state_dtype,
+    k_bwd_conv<TS><<<grid, dim3(256), 0, s>>>(de, T, S, C, Kr, kap[0], kap[1], kap[2], conv_w,
+                                              reinterpret_cast<TS*>(dF)));
+  int nrows = 0;
+  for (int j = 0; j < Kr - 1; ++j) nrows += kap[j];
+  const int64_t nchunks = (T + kConvChunk - 1) / kConvChunk;
+  XHC_TS_DISPATCH(d->state_dtype,
+    k_bwd_convw<TS><<<dim3((unsigned)((C / 8 + 255) / 256), (unsigned)nrows, (unsigned)nchunks), dim3(256), 0, s>>>(
+        de, reinterpret_cast<const TS*>(F), T, S, C, Kr, kap[0], kap[1], kap[2], cpart));
+  const int64_t ncols = (int64_t)nrows * C;
+  k_colsum_rows<<<dim3((unsigned)((ncols + 255) / 256)), dim3(256), 0, s>>>(cpart, nchunks, ncols, dconv_w);
+  return hipGetLastError();
+}
+
+size_t bwd_post_ws_bytes(const xhc_dims* d) {
+  const int64_t T = d->T;
+  const int C = d->C, k = d->k, Kr = d->Kr;
+  const int km = k <= 4 ? 4 : 8;
+  const int nd = km * km + km * Kr + Kr * (Kr + 1) / 2;
+  size_t n = (size_t)post_chunks(C) * nd * T + (size_t)T * (Kr * kMaxK + Kr * Kr);
+  if (Kr > 1) {
+    int nrows = 0;
+    for (int j = 0; j < Kr - 1; ++j) nrows += d->kappa[j];
+    n += (size_t)Kr * T * C + (size_t)((T + kConvChunk - 1) / kConvChunk) * nrows * C;
+  }
+  return n * sizeof(float) + 256;
+}
+
+constexpr int64_t kRowChunk = 1024;   // tokens per weight-gradient partial
+
+size_t bwd_pre_ws_bytes(const xhc_dims* d) {
+  const int64_t T = d->T;
+  const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
+  const int NA = k * Kr + k * k;
+  const int64_t nchunk = (T + kRowChunk - 1) / kRowChunk;
+  size_t n = (size_t)post_chunks(C) * N * T;                    // dH^pre partials
+  n += (size_t)T * tok_floats(N, NA) + (size_t)T * pg_floats(N, k, Kr);
+  n += (size_t)nchunk * N * C * N * 2;                           // dW_r, dW_pre partials
+  n += (size_t)nchunk * k * C * 32;                              // dW_act partials (<= 32 columns)
+  n += (size_t)k * C * 32 + (size_t)pg_floats(N, k, Kr);          // reduced dW_act, reduced gradients
+  return n * sizeof(float) + 1024;
+}
+
+bool bwd_pre_supported(const xhc_dims* d) {
+  return (d->N == 4 || d->N == 8 || d->N == 16 || d->N == 32) && d->C % 256 == 0 &&
+         d->k * d->Kr + d->k * d->k <= 32;
+}
+
+hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum, const float* W_r,
+                          const float* W_pre, const float* W_res, const float* W_post, const float* alpha,
+                          const float* b_res, const float* saved, const int32_t* idx, const float* p,
+                          const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
+                          const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
+                          float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
+                          hipStream_t s) {
+  const int64_t T = d->T;
+  const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
+  const int NA = k * Kr + k * k;
+  const int64_t ncb = post_chunks(C);
+  const int64_t nchunk = (T + kRowChunk - 1) / kRowChunk;
+  float* part = reinterpret_cast<float*>(ws);
+  float* tok = part + ncb * N * T;
+  float* pg = tok + T * tok_floats(N, NA);
+  float* wpart_r = pg + T * pg_floats(N, k, Kr);
+  float* wpart_p = wpart_r + nchunk * (int64_t)N * C * N;
+  float* wpart_a = wpart_p + nchunk * (int64_t)N * C * N;
+  float* red_a = wpart_a + nchunk * (int64_t)k * C * 32;           // [kC][32]
+  float* pgsum = red_a + (int64_t)k * C * 32;
+  XHC_TS_DISPATCH(d->state_dtype,
+    k_bwd_dhpre<TS><<<dim3((unsigned)(T * ncb)), dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),
+        reinterpret_cast<const TS*>(d_input), T, N, C, part));
+  k_bwd_pre_token<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
+      part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p, Hpre, Hpost, dHres, dHpost, dp, d->eps,
+      d->sinkhorn_iters, d->clamp_delta, tok, pg);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
+#define XHC_FULL_ROWS(NNV)                                                                                       \
+  XHC_TS_DISPATCH(d->state_dtype,                                                                                \
+    k_bwd_full_rows<TS, NNV><<<gfull, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),                        \
+        reinterpret_cast<const TS*>(d_input), reinterpret_cast<TS*>(dX), W_r, W_pre, Hpre, tok, T, C, NA,        \
+        kRowChunk, wpart_r, wpart_p))
+  switch (N) {
+    case 4: XHC_FULL_ROWS(4); break;
+    case 8: XHC_FULL_ROWS(8); break;
+    case 16: XHC_FULL_ROWS(16); break;
+    default: XHC_FULL_ROWS(32); break;
+  }
+#undef XHC_FULL_ROWS
+  const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
+  XHC_TS_DISPATCH(d->state_dtype,
+    k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
+        W_post, W_res, idx, tok, T, N, k, C, Kr, kRowChunk, wpart_a));
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // token reductions (fixed order)
+  const int64_t nfull = (int64_t)N * C * N;
+  k_colsum_rows<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(wpart_r, nchunk, nfull, dW_r);
+  k_colsum_rows<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(wpart_p, nchunk, nfull, dW_pre);
+  // active partials are [chunk][kC][32]: split columns into W_post and W_res
+  const int64_t nact = (int64_t)k * C * 32;
+  k_colsum_rows<<<dim3((unsigned)((nact + 255) / 256)), dim3(256), 0, s>>>(wpart_a, nchunk, nact, red_a);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = hipMemcpy2DAsync(dW_post, (size_t)k * Kr * sizeof(float), red_a, 32 * sizeof(float),
+                       (size_t)k * Kr * sizeof(float), (size_t)k * C, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return e;
+  e = hipMemcpy2DAsync(dW_res, (size_t)k * k * sizeof(float), red_a + k * Kr, 32 * sizeof(float),
+                       (size_t)k * k * sizeof(float), (size_t)k * C, hipMemcpyDeviceToDevice, s);
+  if (e != hipSuccess) return e;
+  const int npg = pg_floats(N, k, Kr);
+  k_sum_tokens<<<dim3((unsigned)npg), dim3(256), 0, s>>>(pg, T, npg, pgsum);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = hipMemcpyAsync(dalpha, pgsum, 3 * sizeof(float), hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(db_pre, pgsum + 3, N * sizeof(float), hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(db_res, pgsum + 3 + N, (size_t)k * k * sizeof(float), hipMemcpyDeviceToDevice, s);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(db_post, pgsum + 3 + N + k * k, (size_t)k * Kr * sizeof(float), hipMemcpyDeviceToDevice, s);
+  return e;
+}
+
+#undef XHC_TS_DISPATCH
+
+}  // namespace xhc

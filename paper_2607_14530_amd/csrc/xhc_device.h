@@ -217,4 +217,40 @@ __device__ __forceinline__ void gram_schmidt_basis(const double (&G)[kMaxKr][kMa
   }
 }
 
+// Components e_0..e_{Kr-1} of token t at channels c..c+7: e_0 = F[t], e_j =
+// sum_{i < kappa_j} w_j[i] F[t - i] over the part of the window inside t's
+// sequence (zero padding before the sequence start).
+template <typename TS, int KR>
+__device__ __forceinline__ void components(const TS* __restrict__ F, const float* __restrict__ conv_w, int64_t t,
+                                           int64_t pos, int C, int c, const int (&kap)[3], float (&e)[KR][8]) {
+  float f0[8];
+  Vec8<TS>::load(F + t * C + c, f0);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) e[0][q] = f0[q];
+  if (KR == 1) return;
+  int row = 0;
+#pragma unroll
+  for (int j = 1; j < KR; ++j) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) e[j][q] = 0.f;
+    const int kj = kap[j - 1];
+    for (int i = 0; i < kj; ++i) {
+      if (i > pos) break;
+      float f[8];
+      if (i == 0) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) f[q] = f0[q];
+      } else {
+        Vec8<TS>::load(F + (t - i) * C + c, f);
+      }
+      const float4* w4 = reinterpret_cast<const float4*>(conv_w + (int64_t)(row + i) * C + c);
+      const float4 wa = w4[0], wb = w4[1];
+      const float w[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) e[j][q] = fmaf(w[q], f[q], e[j][q]);
+    }
+    row += kj;
+  }
+}
+
 }  // namespace xhc

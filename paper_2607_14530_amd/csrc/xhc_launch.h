@@ -38,11 +38,12 @@ hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N,
 hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int64_t T, int N, int m, int k,
                             int npre, int64_t C, const float* colsum, const float* alpha_pre, int alpha_stride,
                             const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, float* sums,
-                            hipStream_t s);
+                            float* saved, int nsave, int save_stats_at, hipStream_t s);
 hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int64_t T, int k, int Kq,
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
-                           float* Hpost, float* Hres, float* sums, hipStream_t s);
+                           float* Hpost, float* Hres, float* sums, float* saved, int nsave, int save_z_at,
+                           int save_stats_at, hipStream_t s);
 // out0 gets map 0 (full dense read); maps 1..nmap-1 leave out the active
 // streams and go to outr + (q - 1) * T * C.
 hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
@@ -65,6 +66,27 @@ hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k
 hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T, int64_t S, int N, int C,
                              int k, int Kr, const int32_t* kappa, const float* conv_w, const int32_t* idx,
                              const float* p, const float* Hres, const float* Hpost, const float* wb,
-                             const float* Hpre_next, const void* base_next, void* input_next, hipStream_t s);
+                             const float* Hpre_next, const void* base_next, void* input_next, void* Xact_save,
+                             hipStream_t s);
+
+// ---- backward
+hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const void* Xact, const void* F,
+                           const float* conv_w, const int32_t* idx, const float* p, const float* Hres,
+                           const float* Hpost, void* dX, void* dF, float* dHres, float* dHpost, float* dp,
+                           float* dconv_w, char* ws, hipStream_t s);
+size_t bwd_post_ws_bytes(const xhc_dims* d);
+bool bwd_pre_supported(const xhc_dims* d);
+size_t bwd_pre_ws_bytes(const xhc_dims* d);
+hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum, const float* W_r,
+                          const float* W_pre, const float* W_res, const float* W_post, const float* alpha,
+                          const float* b_res, const float* saved, const int32_t* idx, const float* p,
+                          const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
+                          const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
+                          float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
+                          hipStream_t s);
+
+// per-token values xhc_pre saves for the backward: [z_r (N) | z_pre (N) |
+// z_post, z_res (k*Kr + k*k) | mu | nu | nu_a | pad], z = normalised logits
+__host__ __device__ inline int saved_floats(int N, int k, int Kr) { return 2 * N + k * Kr + k * k + 4; }
 
 }  // namespace xhc

@@ -12,42 +12,6 @@
 
 namespace xhc {
 
-// Components e_0..e_{Kr-1} of token t at channels c..c+7: e_0 = F[t], e_j =
-// sum_{i < kappa_j} w_j[i] F[t - i] over the part of the window inside t's
-// sequence (zero padding before the sequence start).
-template <typename TS, int KR>
-__device__ __forceinline__ void components(const TS* __restrict__ F, const float* __restrict__ conv_w, int64_t t,
-                                           int64_t pos, int C, int c, const int (&kap)[3], float (&e)[KR][8]) {
-  float f0[8];
-  Vec8<TS>::load(F + t * C + c, f0);
-#pragma unroll
-  for (int q = 0; q < 8; ++q) e[0][q] = f0[q];
-  if (KR == 1) return;
-  int row = 0;
-#pragma unroll
-  for (int j = 1; j < KR; ++j) {
-#pragma unroll
-    for (int q = 0; q < 8; ++q) e[j][q] = 0.f;
-    const int kj = kap[j - 1];
-    for (int i = 0; i < kj; ++i) {
-      if (i > pos) break;
-      float f[8];
-      if (i == 0) {
-#pragma unroll
-        for (int q = 0; q < 8; ++q) f[q] = f0[q];
-      } else {
-        Vec8<TS>::load(F + (t - i) * C + c, f);
-      }
-      const float4* w4 = reinterpret_cast<const float4*>(conv_w + (int64_t)(row + i) * C + c);
-      const float4 wa = w4[0], wb = w4[1];
-      const float w[8] = {wa.x, wa.y, wa.z, wa.w, wb.x, wb.y, wb.z, wb.w};
-#pragma unroll
-      for (int q = 0; q < 8; ++q) e[j][q] = fmaf(w[q], f[q], e[j][q]);
-    }
-    row += kj;
-  }
-}
-
 // Gram partials: gpart[chunk][pair][t], pairs (a <= b) in row-major upper order.
 template <typename TS, int KR>
 __global__ __launch_bounds__(256) void k_post_gram(const TS* __restrict__ F, int64_t T, int64_t S, int C,
@@ -174,7 +138,7 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
                                                     const float* __restrict__ wb,
                                                     const float* __restrict__ Hpre_next,
                                                     const TS* __restrict__ base_next,
-                                                    TS* __restrict__ input_next) {
+                                                    TS* __restrict__ input_next, TS* __restrict__ Xact_save) {
   const int64_t ncb = post_chunks(C);
   const int64_t t = blockIdx.x / ncb;
   const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
@@ -189,6 +153,7 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
     if (l < k) {
       rows[l] = idx[t * k + l];
       Vec8<TS>::load(X + (t * N + rows[l]) * (int64_t)C + c, a[l]);
+      if (Xact_save) Vec8<TS>::store(Xact_save + (t * k + l) * (int64_t)C + c, a[l]);
     }
   }
   float nxt[8];
@@ -232,14 +197,14 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
 hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T, int64_t S, int N, int C, int k,
                              int Kr, const int32_t* kappa, const float* conv_w, const int32_t* idx, const float* p,
                              const float* Hres, const float* Hpost, const float* wb, const float* Hpre_next,
-                             const void* base_next, void* input_next, hipStream_t s) {
+                             const void* base_next, void* input_next, void* Xact_save, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const dim3 grid((unsigned)(T * post_chunks(C)));
 #define XHC_APPLY(TS, KR)                                                                                       \
   k_post_apply<TS, KR><<<grid, dim3(256), 0, s>>>(reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(F), T, S, \
                                                   N, C, k, kappa[0], kappa[1], kappa[2], conv_w, idx, p, Hres,   \
                                                   Hpost, wb, Hpre_next, reinterpret_cast<const TS*>(base_next),  \
-                                                  reinterpret_cast<TS*>(input_next))
+                                                  reinterpret_cast<TS*>(input_next), reinterpret_cast<TS*>(Xact_save))
   if (state_dtype == XHC_BF16) {
     switch (Kr) {
       case 1: XHC_APPLY(uint16_t, 1); break;

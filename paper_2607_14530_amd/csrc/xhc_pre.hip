@@ -224,11 +224,16 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
                                                    const float* __restrict__ alpha_pre, int alpha_stride,
                                                    const float* __restrict__ b_pre, float eps,
                                                    int32_t* __restrict__ idx, float* __restrict__ p,
-                                                   float* __restrict__ Hpre) {
+                                                   float* __restrict__ Hpre, float* __restrict__ saved,
+                                                   int nsave, int save_stats_at) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
   const float mu = sums[(int64_t)(NO - 2) * T + t] / (float)NC;
   const float nu = sums[(int64_t)(NO - 1) * T + t] / (float)NC;
+  if (saved) {
+    saved[t * nsave + save_stats_at] = mu;
+    saved[t * nsave + save_stats_at + 1] = nu;
+  }
   const float r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + eps);
   const float r_rms = 1.0f / sqrtf(nu + eps);
   float z[kMaxN];
@@ -241,10 +246,13 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
     idx[t * k + j] = id[j];
     p[t * k + j] = pp[j];
   }
+  if (saved)
+    for (int i = 0; i < N; ++i) saved[t * nsave + i] = z[i];
   for (int q = 0; q < npre; ++q) {
     const float a = alpha_pre[q * alpha_stride];
     for (int i = 0; i < N; ++i) {
       const float zp = sums[(int64_t)(N + q * N + i) * T + t] * r_rms;
+      if (saved && q == 0) saved[t * nsave + N + i] = zp;
       Hpre[((int64_t)q * T + t) * N + i] = sigmoidf(a * zp + b_pre[q * N + i]);
     }
   }
@@ -257,10 +265,17 @@ __global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ sums
                                                   const float* __restrict__ b_post,
                                                   const float* __restrict__ b_res, float eps, int iters,
                                                   float delta, float* __restrict__ Hpost,
-                                                  float* __restrict__ Hres) {
+                                                  float* __restrict__ Hres, float* __restrict__ saved, int nsave,
+                                                  int save_z_at, int save_stats_at) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
-  const float rstd = 1.0f / sqrtf(sums[(int64_t)(NO - 1) * T + t] / (float)kC + eps);
+  const float nu_a = sums[(int64_t)(NO - 1) * T + t] / (float)kC;
+  const float rstd = 1.0f / sqrtf(nu_a + eps);
+  if (saved) {
+    saved[t * nsave + save_stats_at] = nu_a;
+    for (int o = 0; o < k * Kq + (with_res ? k * k : 0); ++o)
+      saved[t * nsave + save_z_at + o] = sums[(int64_t)o * T + t] * rstd;
+  }
   const float ap = alpha_post[0];
   for (int o = 0; o < k * Kq; ++o)
     Hpost[t * k * Kq + o] = 2.0f * sigmoidf(ap * (sums[(int64_t)o * T + t] * rstd) + b_post[o]);
@@ -287,27 +302,29 @@ static hipError_t sum_chunks(const float* part, int64_t nchunk, int NO, int64_t 
 hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int64_t T, int N, int m, int k,
                             int npre, int64_t C, const float* colsum, const float* alpha_pre, int alpha_stride,
                             const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, float* sums,
-                            hipStream_t s) {
+                            float* saved, int nsave, int save_stats_at, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int NO = (int)out_blocks(nout) * 16 + 2;
   hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
   if (e != hipSuccess) return e;
   k_pre_route<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
-      sums, NO, T, N, m, k, npre, (int64_t)N * C, colsum, alpha_pre, alpha_stride, b_pre, eps, idx, p, Hpre);
+      sums, NO, T, N, m, k, npre, (int64_t)N * C, colsum, alpha_pre, alpha_stride, b_pre, eps, idx, p, Hpre,
+      saved, nsave, save_stats_at);
   return hipGetLastError();
 }
 
 hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int64_t T, int k, int Kq,
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
-                           float* Hpost, float* Hres, float* sums, hipStream_t s) {
+                           float* Hpost, float* Hres, float* sums, float* saved, int nsave, int save_z_at,
+                           int save_stats_at, hipStream_t s) {
   if (T == 0) return hipSuccess;
   const int NO = (int)out_blocks(nout) * 16 + 2;
   hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
   if (e != hipSuccess) return e;
   k_pre_coef<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
       sums, NO, T, k, Kq, with_res, (int64_t)k * C, alpha_post, alpha_res, b_post, b_res, eps, iters, delta,
-      Hpost, Hres);
+      Hpost, Hres, saved, nsave, save_z_at, save_stats_at);
   return hipGetLastError();
 }
 

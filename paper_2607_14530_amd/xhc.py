@@ -26,7 +26,7 @@ XHC_OK, XHC_EINVAL, XHC_EUNSUPPORTED, XHC_EWORKSPACE, XHC_EHIP = range(5)
 STATUS_NAMES = {0: "XHC_OK", 1: "XHC_EINVAL", 2: "XHC_EUNSUPPORTED", 3: "XHC_EWORKSPACE", 4: "XHC_EHIP"}
 XHC_BF16, XHC_F32 = 0, 1
 XHC_IMPL_AUTO, XHC_IMPL_MULTI, XHC_IMPL_FUSED = 0, 1, 2
-XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST = range(4)
+XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST, XHC_OP_POST_BWD, XHC_OP_PRE_BWD = range(6)
 
 
 class XhcError(RuntimeError):
@@ -74,10 +74,13 @@ _SIGS = {
     "xhc_pack_full": (ctypes.c_int, [_D, ctypes.c_int32, _P, _P, _P, _P]),
     "xhc_pack_active": (ctypes.c_int, [_D, ctypes.c_int32, _P, _P, _P, _P]),
     "xhc_workspace_bytes": (ctypes.c_size_t, [_D, ctypes.c_int32, ctypes.c_int32]),
-    "xhc_pre": (ctypes.c_int, [_D] + [_P] * 14 + [ctypes.c_size_t, _P]),
-    "xhc_post": (ctypes.c_int, [_D] + [_P] * 8 + [ctypes.c_size_t, _P]),
+    "xhc_pre": (ctypes.c_int, [_D] + [_P] * 15 + [ctypes.c_size_t, _P]),
+    "xhc_post": (ctypes.c_int, [_D] + [_P] * 9 + [ctypes.c_size_t, _P]),
+    "xhc_saved_floats": (ctypes.c_size_t, [_D]),
     "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 14 + [ctypes.c_size_t, _P]),
     "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 17 + [ctypes.c_size_t, _P]),
+    "xhc_post_bwd": (ctypes.c_int, [_D] + [_P] * 16 + [ctypes.c_size_t, _P]),
+    "xhc_pre_bwd": (ctypes.c_int, [_D] + [_P] * 27 + [ctypes.c_size_t, _P]),
     "xhc_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "xhc_last_hip_error": (ctypes.c_char_p, []),
 }
@@ -158,16 +161,21 @@ def xhc_pack_active(d, Kq, W_post, W_res, packed, stream=None):
     _call("xhc_pack_active", ctypes.byref(d), Kq, _ptr(W_post), _ptr(W_res), _ptr(packed), _stream(stream))
 
 
+def xhc_saved_floats(d):
+    return lib().xhc_saved_floats(ctypes.byref(d))
+
+
 def xhc_pre(d, X, packed_full, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre, Hres, Hpost,
-            workspace, stream=None):
+            saved, workspace, stream=None):
     _call("xhc_pre", ctypes.byref(d), _ptr(X), _ptr(packed_full), _ptr(packed_act), _ptr(alpha), _ptr(b_pre),
           _ptr(b_res), _ptr(b_post), _ptr(input), _ptr(idx), _ptr(p), _ptr(Hpre), _ptr(Hres), _ptr(Hpost),
-          _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream(stream))
+          _ptr(saved), _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream(stream))
 
 
-def xhc_post(d, X, F, conv_w, idx, p, Hres, Hpost, workspace, stream=None):
+def xhc_post(d, X, F, conv_w, idx, p, Hres, Hpost, Xact_save, workspace, stream=None):
     _call("xhc_post", ctypes.byref(d), _ptr(X), _ptr(F), _ptr(conv_w), _ptr(idx), _ptr(p), _ptr(Hres),
-          _ptr(Hpost), _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream(stream))
+          _ptr(Hpost), _ptr(Xact_save), _ptr(workspace), workspace.numel() if workspace is not None else 0,
+          _stream(stream))
 
 
 def _nbytes(t):
@@ -187,6 +195,23 @@ def xhc_flash_post(d, Q, q, X, F, conv_w, idx, p, Hpost, Hres, Hpre_next, base_n
           _ptr(Hpost), _ptr(Hres), _ptr(Hpre_next), _ptr(base_next), _ptr(input_next), _ptr(packed_act_next),
           _ptr(alpha_next), _ptr(b_post_next), _ptr(b_res_next), _ptr(Hpost_next), _ptr(Hres_next),
           _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
+def xhc_post_bwd(d, dXn, X, Xact, F, conv_w, idx, p, Hres, Hpost, dX, dF, dHres, dHpost, dp, dconv_w, workspace,
+                 stream=None):
+    _call("xhc_post_bwd", ctypes.byref(d), _ptr(dXn), _ptr(X), _ptr(Xact), _ptr(F), _ptr(conv_w), _ptr(idx),
+          _ptr(p), _ptr(Hres), _ptr(Hpost), _ptr(dX), _ptr(dF), _ptr(dHres), _ptr(dHpost), _ptr(dp), _ptr(dconv_w),
+          _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
+def xhc_pre_bwd(d, X, packed_full, W_r, W_pre, W_res, W_post, alpha, b_res, saved, idx, p, Hpre, Hpost, d_input,
+                dHres, dHpost, dp, dX, dW_r, dW_pre, dW_res, dW_post, dalpha, db_pre, db_res, db_post, workspace,
+                stream=None):
+    _call("xhc_pre_bwd", ctypes.byref(d), _ptr(X), _ptr(packed_full), _ptr(W_r), _ptr(W_pre), _ptr(W_res),
+          _ptr(W_post), _ptr(alpha), _ptr(b_res), _ptr(saved), _ptr(idx), _ptr(p), _ptr(Hpre), _ptr(Hpost),
+          _ptr(d_input), _ptr(dHres), _ptr(dHpost), _ptr(dp), _ptr(dX), _ptr(dW_r), _ptr(dW_pre), _ptr(dW_res),
+          _ptr(dW_post), _ptr(dalpha), _ptr(db_pre), _ptr(db_res), _ptr(db_post), _ptr(workspace),
+          _nbytes(workspace), _stream(stream))
 
 
 # ---------------------------------------------------------------- convenience bundle
@@ -223,13 +248,14 @@ class Sublayer:
         self.ws_pre = _bytes(xhc_workspace_bytes(d, XHC_OP_PRE), dev)
         self.ws_post = _bytes(xhc_workspace_bytes(d, XHC_OP_POST), dev)
 
-    def pre(self, X, stream=None):
+    def pre(self, X, stream=None, saved=None):
         xhc_pre(self.d, X, self.packed_full, self.packed_act, self.alpha, self.b_pre, self.b_res, self.b_post,
-                self.input, self.idx, self.p, self.Hpre, self.Hres, self.Hpost, self.ws_pre, stream)
+                self.input, self.idx, self.p, self.Hpre, self.Hres, self.Hpost, saved, self.ws_pre, stream)
         return self.input
 
-    def post(self, X, F, stream=None):
-        xhc_post(self.d, X, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, self.ws_post, stream)
+    def post(self, X, F, stream=None, Xact_save=None):
+        xhc_post(self.d, X, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, Xact_save, self.ws_post,
+                 stream)
         return X
 
 
@@ -305,3 +331,49 @@ class FlashGroup:
         for q in range(1, self.Q + 1):
             self.step(q, X, F_list[q - 1], stream)
         return X
+
+
+class TrainableSublayer(Sublayer):
+    """A Sublayer that keeps what the backward needs and runs it.
+
+    forward(X, F): xhc_pre (saving the per-token logits / statistics) and
+    xhc_post (saving the pre-update active rows); X is updated in place.
+    backward(X, dXn, d_input, F): xhc_post_bwd (restores X to the pre-update
+    state) then xhc_pre_bwd; returns a dict of gradients."""
+
+    def __init__(self, d: Dims, weights, device="cuda"):
+        super().__init__(d, weights, device)
+        dev = torch.device(device)
+        self.W = {n: weights[n].to(dev).contiguous().float() for n in ("W_r", "W_pre", "W_res", "W_post")}
+        T, N, k, C, Kr = d.T, d.N, d.k, d.C, d.Kr
+        sdt = self.input.dtype
+        self.saved = torch.empty(T, xhc_saved_floats(d), dtype=torch.float32, device=dev)
+        self.Xact = torch.empty(T, k, C, dtype=sdt, device=dev)
+        self.ws_post_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_POST_BWD), dev)
+        self.ws_pre_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_PRE_BWD), dev)
+
+    def forward(self, X, F, stream=None):
+        self.pre(X, stream, saved=self.saved)
+        self.post(X, F, stream, Xact_save=self.Xact)
+        return X
+
+    def backward(self, X, dXn, d_input, F, stream=None):
+        d = self.d
+        T, N, k, C, Kr = d.T, d.N, d.k, d.C, d.Kr
+        dev = X.device
+        f32 = dict(dtype=torch.float32, device=dev)
+        g = {"X": torch.empty_like(X), "F": torch.empty_like(F), "dHres": torch.empty(T, k, k, **f32),
+             "dHpost": torch.empty(T, k, Kr, **f32), "dp": torch.empty(T, k, **f32),
+             "conv_w": torch.empty_like(self.conv_w) if self.conv_w is not None else None}
+        xhc_post_bwd(d, dXn, X, self.Xact, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, g["X"], g["F"],
+                     g["dHres"], g["dHpost"], g["dp"], g["conv_w"], self.ws_post_bwd, stream)
+        for n in ("W_r", "W_pre", "W_res", "W_post"):
+            g[n] = torch.empty_like(self.W[n])
+        g["alpha"] = torch.empty(3, **f32)
+        g["b_pre"], g["b_res"], g["b_post"] = (torch.empty(N, **f32), torch.empty(k * k, **f32),
+                                               torch.empty(k * Kr, **f32))
+        xhc_pre_bwd(d, X, self.packed_full, self.W["W_r"], self.W["W_pre"], self.W["W_res"], self.W["W_post"],
+                    self.alpha, self.b_res, self.saved, self.idx, self.p, self.Hpre, self.Hpost, d_input,
+                    g["dHres"], g["dHpost"], g["dp"], g["X"], g["W_r"], g["W_pre"], g["W_res"], g["W_post"],
+                    g["alpha"], g["b_pre"], g["b_res"], g["b_post"], self.ws_pre_bwd, stream)
+        return g

@@ -43,14 +43,14 @@ FAKE = 1 << 20  # a 16-byte aligned non-null address; never dereferenced below
 
 
 def _pre_status(d, ws_bytes=1 << 40, null_at=None):
-    ptrs = [FAKE] * 14
+    ptrs = [FAKE] * 13 + [None, FAKE]      # saved (14th) is optional
     if null_at is not None:
-        ptrs[null_at] = None
+        ptrs[null_at if null_at < 13 else 14] = None
     return X.lib().xhc_pre(ctypes.byref(d), *ptrs, ws_bytes, None)
 
 
 def _post_status(d, conv=True, ws_bytes=1 << 40, F=FAKE + 4096):
-    return X.lib().xhc_post(ctypes.byref(d), FAKE, F, FAKE if conv else None, FAKE, FAKE, FAKE, FAKE,
+    return X.lib().xhc_post(ctypes.byref(d), FAKE, F, FAKE if conv else None, FAKE, FAKE, FAKE, FAKE, None,
                             FAKE, ws_bytes, None)
 
 
@@ -86,7 +86,7 @@ def test_null_pointer_and_workspace_errors():
 
 def test_misaligned_pointers_rejected():
     d = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=1)
-    ptrs = [FAKE] * 14
+    ptrs = [FAKE] * 13 + [None, FAKE]
     ptrs[0] = FAKE + 2
     assert X.lib().xhc_pre(ctypes.byref(d), *ptrs, 1 << 40, None) == X.XHC_EUNSUPPORTED
 

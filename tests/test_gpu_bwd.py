@@ -1,0 +1,82 @@
+"""Backward of a full xHC sublayer on the GPU vs the oracle's reverse mode
+(itself pinned by central finite differences), through the C ABI."""
+
+import pytest
+import torch
+
+from oracle import xhc_oracle as O
+from paper_2607_14530_amd import synth
+from paper_2607_14530_amd import xhc as X
+from tests.parity_util import assert_bf16_close
+
+pytestmark = pytest.mark.gpu
+F64 = torch.float64
+W = synth.Workload
+
+
+def assert_grad_close(got, ref, what, frob=2e-3):
+    """relative Frobenius error <= frob, and each element within 2e-2 relative
+    or 1e-2 * max|ref| absolute."""
+    got = got.detach().to("cpu", F64)
+    ref = ref.detach().to("cpu", F64)
+    assert got.shape == ref.shape, (what, got.shape, ref.shape)
+    scale = ref.abs().max().item()
+    rel = ((got - ref).norm() / max(ref.norm().item(), 1e-30)).item()
+    assert rel <= frob, f"{what}: relative Frobenius error {rel:.2e}"
+    d = (got - ref).abs()
+    ok = (d <= 2e-2 * ref.abs()) | (d <= 1e-2 * max(scale, 1e-30))
+    assert bool(ok.all()), f"{what}: {int((~ok).sum())} elements out of tolerance, max |d| {d.max().item():.2e}"
+
+
+def _run(w, seed):
+    inp = synth.sublayer_inputs(w, seed, device="cuda", grads=True)
+    d = X.dims_for(w)
+    sub = X.TrainableSublayer(d, inp, "cuda")
+    state = inp["X"].clone()
+    sub.forward(state, inp["F"])
+    g = sub.backward(state, inp["G_X"], inp["G_in"], inp["F"])
+    torch.cuda.synchronize()
+    return inp, sub, state, g
+
+
+def _oracle(w, inp):
+    c = lambda v: v.cpu() if torch.is_tensor(v) else v
+    return O.xhc_sublayer_grads(c(inp["X"]).double(), c(inp["F"]).double(), c(inp["conv_w"]), c(inp["W_r"]),
+                                c(inp["W_pre"]), c(inp["W_res"]), c(inp["W_post"]), c(inp["alpha"]),
+                                c(inp["b_pre"]), c(inp["b_res"]), c(inp["b_post"]), c(inp["G_X"]),
+                                c(inp["G_in"]), m=w.m, k=w.k, Kr=w.Kr, S=w.S, kappa=w.kappa)
+
+
+CASES = [
+    W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=1, name="bwd-attn-N16"),
+    W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, name="bwd-mlp-N16"),
+    W(T=48, S=48, N=4, k=4, m=2, C=256, Kr=4, name="bwd-mlp-N4"),
+    W(T=40, S=20, N=8, k=4, m=2, C=512, Kr=4, name="bwd-mlp-N8"),
+    W(T=32, S=32, N=32, k=4, m=2, C=256, Kr=1, name="bwd-attn-N32"),
+    W(T=64, S=64, N=16, k=4, m=2, C=256, Kr=4, alpha=(0.5, 1.0, 0.5), name="bwd-mlp-stress"),
+]
+
+
+@pytest.mark.parametrize("w", CASES, ids=lambda w: w.name)
+def test_backward_matches_oracle(w):
+    print(f"[bwd] {w.name}", flush=True)
+    inp, sub, state, g = _run(w, seed=31)
+    # the backward restores the state the forward saw, bit for bit
+    assert torch.equal(state, inp["X"])
+    ref = _oracle(w, inp)
+    assert torch.equal(sub.idx.cpu().long(), ref["idx"]), "routing differs (near-tie seed?)"
+    assert_bf16_close(g["X"], ref["X"], "dX")
+    assert_bf16_close(g["F"], ref["F"], "dF")
+    for n in ("W_r", "W_pre", "W_res", "W_post", "alpha", "b_pre", "b_res", "b_post"):
+        assert_grad_close(g[n], ref[n], n)
+    if w.Kr > 1:
+        assert_grad_close(g["conv_w"], ref["conv_w"], "conv_w")
+
+
+def test_backward_is_deterministic():
+    w = W(T=128, S=64, N=16, k=4, m=2, C=512, Kr=4, name="bwd-det")
+    a = _run(w, seed=3)[3]
+    b = _run(w, seed=3)[3]
+    for n, v in a.items():
+        if v is not None:
+            assert torch.equal(v, b[n]), n
