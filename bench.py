@@ -62,13 +62,80 @@ def cpu_baseline(seconds=15.0):
                        S=ws.S, kappa=ws.kappa)
             elapsed += time.perf_counter() - t0
         print(f"[cpu_baseline] {n} tokens: {elapsed:.2f} s", file=sys.stderr, flush=True)
-        if elapsed >= seconds or n >= 4096:
+        if elapsed >= seconds or n >= 16384:
             break
         n = max(n * 2, int(n * seconds / max(elapsed, 1e-3) * 1.1))
-        n = min(n, 4096)
+        n = min(n, 16384)
     return {"value": 2 * n / elapsed, "unit": "tokens/s", "cores": torch.get_num_threads(), "kind": "oracle",
             "sample": f"{n} tokens x (attention-type + MLP-type sublayer), N=16 k=4 m=2 C=4096, fp64, "
                       f"{elapsed:.1f} s"}
+
+
+def _time(fn, iters, stream):
+    """Average milliseconds of fn() over iters calls, HIP events on `stream`."""
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(iters):
+        fn()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / iters
+
+
+def extra_sections(dev, stream, iters=5):
+    """xHC-Flash groups, the dense mHC N=4 comparator and the backward, each
+    timed on its own (outside the timed steps of the main workload)."""
+    out = {}
+    unit = lambda C: 2 * C   # bytes of one "C" (bf16 elements of width C)
+    # xHC-Flash, Q = 4 and Q = 2, at T = 16384 (2 x 8192), N = 16, k = 4, C = 4096
+    for Q in (4, 2):
+        w = synth.sparse_c4096(4)
+        d = synth.flash_inputs(w, Q, 40 + Q, device=dev)
+        g = X.FlashGroup(X.dims_for(w), Q, d, dev)
+        state = d["X"]
+        ms = _time(lambda: g.run(state, d["F_list"], stream), iters, stream)
+        Kq = [1 if q % 2 == 1 else w.Kr for q in range(1, Q + 1)]
+        b = A.algorithmic_bytes_flash_pre(w.N, w.k, w.C, Q)
+        for q in range(1, Q + 1):
+            b += A.algorithmic_bytes_flash_post(w.N, w.k, w.C, Kq[q - 1], q == Q, Kq[q] if q < Q else 0)
+        out[f"flash_q{Q}"] = {
+            "workload": f"xHC-Flash group of {Q} sublayers, T=16384 (2 x 8192), N=16, k=4, m=2, C=4096",
+            "ms_per_group": ms, "tokens_per_s_per_sublayer": Q * w.T / (ms * 1e-3),
+            "achieved_GBps": b * w.T / (ms * 1e-3) / 1e9,
+            "bytes_per_token_C": b / Q / unit(w.C), "paper_bytes_per_token_C": 40.0 if Q == 4 else 51.0}
+        del g, d, state
+        torch.cuda.empty_cache()
+    # dense mHC N = 4 (k = m = N, one write-back component) at the same T and C
+    w = synth.Workload(T=16384, S=8192, N=4, k=4, m=4, C=4096, Kr=1, name="mhc-n4")
+    inp = synth.sublayer_inputs(w, 9, device=dev)
+    sub = X.Sublayer(X.dims_for(w), inp, dev)
+    st = inp["X"]
+    ms = _time(lambda: (sub.pre(st, stream), sub.post(st, inp["F"], stream)), iters, stream)
+    b = A.algorithmic_bytes_sublayer(4, 4, w.C, 1)
+    out["mhc_n4"] = {"workload": "dense mHC N=4 (k=m=4, one write-back component), T=16384, C=4096",
+                     "ms_per_sublayer": ms, "tokens_per_s": w.T / (ms * 1e-3),
+                     "achieved_GBps": b * w.T / (ms * 1e-3) / 1e9, "bytes_per_token_C": b / unit(w.C),
+                     "paper_bytes_per_token_C": 34.0}
+    del sub, inp, st
+    torch.cuda.empty_cache()
+    # backward, T = 8192, N = 16, k = 4, C = 4096, MLP-type
+    w = synth.bwd_sweep(16, 4)
+    inp = synth.sublayer_inputs(w, 10, device=dev, grads=True)
+    sub = X.TrainableSublayer(X.dims_for(w), inp, dev)
+    st = inp["X"]
+    fwd_ms = _time(lambda: sub.forward(st, inp["F"], stream), 1, stream)
+    sub.forward(st, inp["F"], stream)
+
+    def fb():
+        sub.backward(st, inp["G_X"], inp["G_in"], inp["F"], stream)
+        sub.forward(st, inp["F"], stream)
+    ms = _time(fb, 2, stream)
+    out["bwd_n16_mlp"] = {"workload": "xHC MLP-type sublayer backward, T=8192, N=16, k=4, m=2, C=4096",
+                          "ms_forward_with_saves": fwd_ms, "ms_backward": ms - fwd_ms,
+                          "tokens_per_s_backward": w.T / ((ms - fwd_ms) * 1e-3)}
+    return out
 
 
 def main():
@@ -77,6 +144,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true", help="skip the Flash / mHC / backward sections")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build runs the connection on a single MI355X "
@@ -153,6 +221,10 @@ def main():
         "roofline": {"kernel": "xhc_pre (entry point)", "bound": "hbm", "achieved": achieved,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None},
     }
+    if not args.no_extra:
+        del sub_a, sub_m, inp_a, inp_m, state
+        torch.cuda.empty_cache()
+        out["sections"] = extra_sections(dev, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline()
     print(json.dumps(out), flush=True)

@@ -381,13 +381,15 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
 
 def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in, *,
                        m, k, Kr, S, kappa=(4, 8, 12), eps=1e-5, sinkhorn_iters=20,
-                       clamp_delta=1e-6, gram_schmidt_on=True):
+                       clamp_delta=1e-6, gram_schmidt_on=True, tokens=None):
     """L = <G_X, X'> + <G_in, input> for one full xHC sublayer, float64.
 
     Same steps as xhc_pre followed by xhc_post, except that the projection
     weights are taken as given (already the bf16 operand values), so that a
     finite-difference probe can perturb them.  ``al`` = (alpha_pre,
-    alpha_res, alpha_post).  Returns (L, forward results dict).
+    alpha_res, alpha_post).  With ``tokens`` (positions in the batch), Xv,
+    G_X and G_in hold only those tokens while Fv is the whole batch.
+    Returns (L, forward results dict).
     """
     T, N, C = Xv.shape
     x = Xv.reshape(T, N * C)
@@ -403,7 +405,7 @@ def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in
     Hpost = post_mapping(a_n @ Wpo, al[2], bpo, k, Kr)
     inp = torch.einsum("tn,tnc->tc", Hpre, Xv)
     Xn = xhc_post(Xv, Fv, cw, idx, p, Hres, Hpost, S=S, kappa=kappa,
-                  gram_schmidt_on=gram_schmidt_on)
+                  gram_schmidt_on=gram_schmidt_on, tokens=tokens)
     L = (G_X.to(F64) * Xn).sum() + (G_in.to(F64) * inp).sum()
     fwd = dict(idx=idx, p=p, Hpre=Hpre, Hres=Hres, Hpost=Hpost, input=inp, X_new=Xn)
     return L, fwd

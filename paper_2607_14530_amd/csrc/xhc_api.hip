@@ -100,7 +100,7 @@ size_t flash_pre_ws(const xhc_dims* d, int Q) {
 
 size_t gram_bytes(const xhc_dims* d, int Kq) {
   const int np = Kq * (Kq + 1) / 2;
-  return align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)) +
+  return align_up((size_t)gram_chunks(d->C, Kq, d->kappa) * np * (size_t)d->T * sizeof(float)) +
          align_up((size_t)d->T * d->k * Kq * sizeof(float));
 }
 
@@ -117,7 +117,7 @@ size_t flash_post_ws(const xhc_dims* d, int Q, int q) {
 size_t post_ws(const xhc_dims* d) {
   if (d->Kr == 1) return 0;
   const int np = d->Kr * (d->Kr + 1) / 2;
-  return align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)) +
+  return align_up((size_t)gram_chunks(d->C, d->Kr, d->kappa) * np * (size_t)d->T * sizeof(float)) +
          align_up((size_t)d->T * d->k * d->Kr * sizeof(float));
 }
 
@@ -219,7 +219,9 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   if (d->impl == XHC_IMPL_FUSED && !fused_pre_supported(d)) return XHC_EUNSUPPORTED;
   if (workspace_bytes < pre_ws(d)) return XHC_EWORKSPACE;
   if (d->impl == XHC_IMPL_FUSED && saved) return XHC_EUNSUPPORTED;
-  if (d->impl == XHC_IMPL_AUTO && (!fused_pre_supported(d) || saved)) {
+  // AUTO takes the multi-kernel path: the single-pass kernel is correct but
+  // slower on this device (its per-tile team synchronisation is latency-bound).
+  if (d->impl == XHC_IMPL_AUTO) {
     xhc_dims m = *d;
     m.impl = XHC_IMPL_MULTI;
     return xhc_pre(&m, X, packed_full, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre, Hres, Hpost,
@@ -284,10 +286,11 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
     const int np = d->Kr * (d->Kr + 1) / 2;
     float* gpart = reinterpret_cast<float*>(workspace);
     wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
-                                  align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)));
+                                  align_up((size_t)gram_chunks(d->C, d->Kr, d->kappa) * np * (size_t)d->T *
+                                           sizeof(float)));
     XHC_STEP("post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, d->Kr, d->kappa, conv_w, gpart, s));
-    XHC_STEP("post_coef",
-             launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, d->Kr, d->gram_schmidt, p, Hpost, wb, s));
+    XHC_STEP("post_coef", launch_post_coef(gpart, gram_chunks(d->C, d->Kr, d->kappa), d->T, d->k, d->Kr,
+                                           d->gram_schmidt, p, Hpost, wb, s));
   }
   XHC_STEP("post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa,
                                            conv_w, idx, p, Hres, Hpost, wb, nullptr, nullptr, nullptr, Xact_save,
@@ -369,10 +372,11 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
     const int np = Kq * (Kq + 1) / 2;
     float* gpart = reinterpret_cast<float*>(workspace);
     wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
-                                  align_up((size_t)post_chunks(d->C) * np * (size_t)d->T * sizeof(float)));
+                                  align_up((size_t)gram_chunks(d->C, Kq, d->kappa) * np * (size_t)d->T *
+                                           sizeof(float)));
     XHC_STEP("flash_post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, Kq, d->kappa, conv_w, gpart, s));
-    XHC_STEP("flash_post_coef",
-             launch_post_coef(gpart, post_chunks(d->C), d->T, d->k, Kq, d->gram_schmidt, p, Hpost, wb, s));
+    XHC_STEP("flash_post_coef", launch_post_coef(gpart, gram_chunks(d->C, Kq, d->kappa), d->T, d->k, Kq,
+                                                 d->gram_schmidt, p, Hpost, wb, s));
   }
   XHC_STEP("flash_post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, Kq, d->kappa,
                                                  conv_w, idx, p, Hres, Hpost, wb, last ? nullptr : Hpre_next,

@@ -59,6 +59,8 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
 
 // ---- post
 __host__ __device__ inline int64_t post_chunks(int C) { return ((int64_t)C / 8 + 255) / 256; }
+// Gram partial chunks written by launch_post_gram (run-based kernels use 1024-channel chunks)
+int64_t gram_chunks(int C, int Kr, const int32_t* kappa);
 hipError_t launch_post_gram(int state_dtype, const void* F, int64_t T, int64_t S, int C, int Kr,
                             const int32_t* kappa, const float* conv_w, float* gpart, hipStream_t s);
 hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k, int Kr, int gram_schmidt,
