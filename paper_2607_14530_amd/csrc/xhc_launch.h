@@ -27,10 +27,32 @@ hipError_t launch_pack(int64_t K, int64_t nout, int ncols_a, const float* A, int
 hipError_t launch_colsum(int64_t K, int ncols, const float* W, float* out, hipStream_t s);
 
 // ---- pre (multi-kernel path)
-constexpr int kProjTile = 16;    // tokens per projection tile
-constexpr int kProjChunkBlocks = 64;  // 32-row blocks per split-K chunk
+constexpr int kProjTile = 16;    // tokens per MFMA column group
 
-__host__ __device__ inline int64_t proj_chunks(int64_t K) { return (K / 32 + kProjChunkBlocks - 1) / kProjChunkBlocks; }
+// Launch plan of the split-K projection: each wave multiplies tg token groups
+// of 16 by the same weight fragment (fewer fragment loads per state byte), a
+// workgroup covers chunk_blocks 32-row blocks of K, and nchunk partials are
+// summed per token afterwards.  The reduction buffer 2 x NO x 16 tg floats
+// stays within 64 KiB of LDS.
+struct ProjPlan {
+  int tg;
+  int64_t chunk_blocks;
+  int64_t nchunk;
+};
+inline ProjPlan proj_plan(int64_t K, int64_t nout, int64_t T) {
+  const int64_t nblk = K / 32, NO = out_blocks(nout) * 16 + 2;
+  int tg = 4;
+  while (tg > 1 && ((T + 16 * tg - 1) / (16 * tg) < 128 || NO * tg > 160)) tg /= 2;
+  const int64_t tiles = (T + 16 * tg - 1) / (16 * tg);
+  int64_t want = (1024 + tiles - 1) / tiles;                    // chunks for about 1024 workgroups
+  const int64_t most = (nblk + 31) / 32;                        // chunks of at least 32 blocks
+  if (want > most) want = most;
+  if (want < 1) want = 1;
+  int64_t cb = (nblk + want - 1) / want;
+  cb = (cb + 31) / 32 * 32;                                     // a multiple of 4 waves x 8 blocks
+  return ProjPlan{tg, cb, (nblk + cb - 1) / cb};
+}
+inline int64_t proj_chunks(int64_t K, int64_t nout, int64_t T) { return proj_plan(K, nout, T).nchunk; }
 
 hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N, int C, int64_t K,
                                const void* packed, int64_t nout, const int32_t* idx, int k,
@@ -44,10 +66,15 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
                            float* Hpost, float* Hres, float* sums, float* saved, int nsave, int save_z_at,
                            int save_stats_at, hipStream_t s);
+// dense read + active projection, in chunks of kReadSlices 32-channel slices:
 // out0 gets map 0 (full dense read); maps 1..nmap-1 leave out the active
 // streams and go to outr + (q - 1) * T * C.
-hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
-                             int nmap, const int32_t* idx, int k, void* out0, void* outr, hipStream_t s);
+constexpr int kReadSlices = 32;
+__host__ __device__ inline int64_t read_chunks(int C) { return ((int64_t)C / 32 + kReadSlices - 1) / kReadSlices; }
+hipError_t launch_read_active(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre, int nmap,
+                              const int32_t* idx, int k, const void* packed_act, int64_t nout_act, void* out0,
+                              void* outr, float* part, hipStream_t s);
+
 
 // ---- pre (fused single-pass path: bf16 state, N = 16, k = 4, C % 128 == 0)
 bool fused_pre_supported(const xhc_dims* d);
@@ -60,7 +87,7 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
 // ---- post
 __host__ __device__ inline int64_t post_chunks(int C) { return ((int64_t)C / 8 + 255) / 256; }
 // Gram partial chunks written by launch_post_gram (run-based kernels use 1024-channel chunks)
-int64_t gram_chunks(int C, int Kr, const int32_t* kappa);
+int64_t gram_chunks(int C, int64_t S, int Kr, const int32_t* kappa);
 hipError_t launch_post_gram(int state_dtype, const void* F, int64_t T, int64_t S, int C, int Kr,
                             const int32_t* kappa, const float* conv_w, float* gpart, hipStream_t s);
 hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k, int Kr, int gram_schmidt,

@@ -59,44 +59,51 @@ __global__ __launch_bounds__(256) void k_post_gram(const TS* __restrict__ F, int
 
 // ------------------------------------------------------------------ run-based MLP-type kernels
 // For compile-time kernel sizes (K1, K2, K3) = (4, 8, 12): a thread owns 4
-// channels and walks a run of kRun consecutive tokens, keeping the 24 conv taps
-// of its channels and a sliding window of the last 12 outputs in registers,
-// so F is read once per kernel and the taps once per run.
+// channels and walks a run of kRun consecutive tokens in groups of G, keeping
+// the conv taps of its channels and the last 12 values of F in registers, so F
+// is read once per kernel and the taps once per run.  Sequence starts fall on
+// group starts (S % G == 0), where the history is cleared.
 
 constexpr int kRun = 64;
 
-template <typename TS> struct Vec4;
-template <> struct Vec4<uint16_t> {
-  static __device__ __forceinline__ void load(const uint16_t* p, float (&f)[4]) {
-    const uint2 v = *reinterpret_cast<const uint2*>(p);
+// four channels of one row, held in the storage format until used
+template <typename TS> struct Row4;
+template <> struct Row4<uint16_t> {
+  using raw = uint2;
+  static __device__ __forceinline__ raw load(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+  static __device__ __forceinline__ raw zero() { return make_uint2(0u, 0u); }
+  static __device__ __forceinline__ void unpack(raw v, float (&f)[4]) {
     f[0] = bf_lo(v.x); f[1] = bf_hi(v.x); f[2] = bf_lo(v.y); f[3] = bf_hi(v.y);
   }
   static __device__ __forceinline__ void store(uint16_t* p, const float (&f)[4]) {
     *reinterpret_cast<uint2*>(p) = make_uint2(pack2bf(f[0], f[1]), pack2bf(f[2], f[3]));
   }
+  static __device__ __forceinline__ void store_raw(uint16_t* p, raw v) { *reinterpret_cast<uint2*>(p) = v; }
   static __device__ __forceinline__ void round(float (&f)[4]) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) f[e] = __uint_as_float(f2bf(f[e]) << 16);
   }
 };
-template <> struct Vec4<float> {
-  static __device__ __forceinline__ void load(const float* p, float (&f)[4]) {
-    const float4 v = *reinterpret_cast<const float4*>(p);
-    f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
-  }
+template <> struct Row4<float> {
+  using raw = float4;
+  static __device__ __forceinline__ raw load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  static __device__ __forceinline__ raw zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+  static __device__ __forceinline__ void unpack(raw v, float (&f)[4]) { f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w; }
   static __device__ __forceinline__ void store(float* p, const float (&f)[4]) {
     *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
   }
+  static __device__ __forceinline__ void store_raw(float* p, raw v) { *reinterpret_cast<float4*>(p) = v; }
   static __device__ __forceinline__ void round(float (&)[4]) {}
 };
 
-template <typename TS, int K1, int K2, int K3>
-struct RunConv {
+template <int K1, int K2, int K3>
+struct ConvGroup {
   static constexpr int KR = 1 + (K1 > 0) + (K2 > 0) + (K3 > 0);
   static constexpr int TAPS = K1 + K2 + K3;
-  static constexpr int KW = (K1 > K2 ? (K1 > K3 ? K1 : K3) : (K2 > K3 ? K2 : K3));   // window length
+  static constexpr int KW = (K1 > K2 ? (K1 > K3 ? K1 : K3) : (K2 > K3 ? K2 : K3));
   float w[TAPS][4];
-  float win[KW][4];
+  float hist[KW][4];   // hist[KW - 1 - i] = F[t - 1 - i] before the current group's first token t
+
   __device__ __forceinline__ void load_taps(const float* __restrict__ conv_w, int C, int c) {
 #pragma unroll
     for (int r = 0; r < TAPS; ++r) {
@@ -104,40 +111,45 @@ struct RunConv {
       w[r][0] = v.x; w[r][1] = v.y; w[r][2] = v.z; w[r][3] = v.w;
     }
   }
-  // window before token t0: win[i] = F[t0 - 1 - i] inside t0's sequence, else 0
+  __device__ __forceinline__ void reset() {
+#pragma unroll
+    for (int i = 0; i < KW; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) hist[i][q] = 0.f;
+  }
+  // history before token t0, zero before the start of t0's sequence
+  template <typename TS>
   __device__ __forceinline__ void init(const TS* __restrict__ F, int64_t t0, int64_t S, int C, int c) {
     const int64_t pos = t0 % S;
 #pragma unroll
     for (int i = 0; i < KW; ++i) {
-      if (i < KW - 1 && i + 1 <= pos) Vec4<TS>::load(F + (t0 - 1 - i) * C + c, win[i]);
-      else {
+      const int lag = KW - i;   // hist[i] = F[t0 - lag]; the loads are issued unconditionally
+      const int64_t src = t0 >= lag ? t0 - lag : 0;
+      Row4<TS>::unpack(Row4<TS>::load(F + src * C + c), hist[i]);
+      if (lag > pos) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) win[i][q] = 0.f;
+        for (int q = 0; q < 4; ++q) hist[i][q] = 0.f;
       }
     }
   }
-  // shift in F[t]; clears the history at a sequence start
-  __device__ __forceinline__ void push(const float (&f)[4], bool seq_start) {
+  // e_0 = F[t], e_j = sum_{i < kappa_j} w_j[i] F[t - i] for token g of the group (cur[g] = F[t])
+  template <int G>
+  __device__ __forceinline__ void components(const float (&cur)[G][4], int g, float (&e)[KR][4]) const {
 #pragma unroll
-    for (int i = KW - 1; i > 0; --i)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) win[i][q] = seq_start ? 0.f : win[i - 1][q];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) win[0][q] = f[q];
-  }
-  // components e_0 = F[t], e_j = sum_{i < kappa_j} w_j[i] F[t - i]
-  __device__ __forceinline__ void components(float (&e)[KR][4]) const {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) e[0][q] = win[0][q];
+    for (int q = 0; q < 4; ++q) e[0][q] = cur[g][q];
     int b = 1, row = 0;
     auto branch = [&](int K) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) e[b][q] = 0.f;
 #pragma unroll
-      for (int i = 0; i < KW; ++i)
-        if (i < K)
+      for (int i = 0; i < KW; ++i) {
+        if (i < K) {
+          const int x = g - i;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) e[b][q] = fmaf(w[row + i][q], win[i][q], e[b][q]);
+          for (int q = 0; q < 4; ++q)
+            e[b][q] = fmaf(w[row + i][q], x >= 0 ? cur[x >= 0 ? x : 0][q] : hist[KW + (x < 0 ? x : -1)][q], e[b][q]);
+        }
+      }
       row += K;
       ++b;
     };
@@ -145,14 +157,29 @@ struct RunConv {
     if (K2 > 0) branch(K2);
     if (K3 > 0) branch(K3);
   }
+  template <int G>
+  __device__ __forceinline__ void advance(const float (&cur)[G][4]) {
+#pragma unroll
+    for (int i = 0; i < KW; ++i) {
+      const int j = i + G;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) hist[i][q] = j < KW ? hist[j < KW ? j : 0][q] : cur[j >= KW ? j - KW : 0][q];
+    }
+  }
 };
 
+// Gram partials per 1024-channel chunk.  Each lane forms its 4-channel
+// products for G tokens; a wave sums them over its 64 lanes through an LDS
+// transpose (lane v adds column v), and the waves' sums are added at the end.
 template <typename TS, int K1, int K2, int K3>
 __global__ __launch_bounds__(256) void k_post_gram_run(const TS* __restrict__ F, int64_t T, int64_t S, int C,
                                                        const float* __restrict__ conv_w,
                                                        float* __restrict__ gpart) {
-  using RC = RunConv<TS, K1, K2, K3>;
-  constexpr int KR = RC::KR, NP = KR * (KR + 1) / 2;
+  using CG = ConvGroup<K1, K2, K3>;
+  constexpr int KR = CG::KR, NP = KR * (KR + 1) / 2;
+  constexpr int G = 4, NV = G * NP, LD = (NV + 3) / 4 * 4 + 4;
+  static_assert(NV <= kWave, "one column per lane");
+  __shared__ __align__(16) float xpose[4][kWave][LD];
   __shared__ float red[kRun][4][NP];
   const int nw = blockDim.x / kWave;
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -160,29 +187,56 @@ __global__ __launch_bounds__(256) void k_post_gram_run(const TS* __restrict__ F,
   const int c = (int)(cb * blockDim.x + threadIdx.x) * 4;
   const int64_t t0 = (int64_t)blockIdx.x * kRun;
   const int nt = (int)((T - t0 < kRun) ? T - t0 : kRun);
-  RC rc;
-  rc.load_taps(conv_w, C, c);
-  rc.init(F, t0, S, C, c);
-#pragma unroll 4
-  for (int u = 0; u < nt; ++u) {
-    const int64_t t = t0 + u;
-    float f[4];
-    Vec4<TS>::load(F + t * C + c, f);
-    rc.push(f, (t % S) == 0);
-    float e[KR][4];
-    rc.components(e);
-    int pi = 0;
+  CG cg;
+  cg.load_taps(conv_w, C, c);
+  cg.init(F, t0, S, C, c);
+  float* mine = &xpose[wave][lane][0];
+  for (int u0 = 0; u0 < nt; u0 += G) {
+    const int64_t t = t0 + u0;
+    if (t % S == 0) cg.reset();
+    float cur[G][4];
 #pragma unroll
-    for (int a = 0; a < KR; ++a)
+    for (int g = 0; g < G; ++g) {
+      typename Row4<TS>::raw v = Row4<TS>::zero();
+      if (u0 + g < nt) v = Row4<TS>::load(F + (t + g) * C + c);
+      Row4<TS>::unpack(v, cur[g]);
+    }
+    float part[NV];
 #pragma unroll
-      for (int b = a; b < KR; ++b, ++pi) {
-        float v = 0.f;
+    for (int g = 0; g < G; ++g) {
+      float e[KR][4];
+      cg.components(cur, g, e);
+      int pi = 0;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) v = fmaf(e[a][q], e[b][q], v);
+      for (int a = 0; a < KR; ++a)
 #pragma unroll
-        for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-        if (lane == 0) red[u][wave][pi] = v;
-      }
+        for (int b = a; b < KR; ++b, ++pi) {
+          float v = 0.f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v = fmaf(e[a][q], e[b][q], v);
+          part[g * NP + pi] = v;
+        }
+    }
+    cg.advance(cur);
+#pragma unroll
+    for (int v = 0; v < NV; v += 4)
+      *reinterpret_cast<float4*>(mine + v) =
+          make_float4(part[v], v + 1 < NV ? part[v + 1 < NV ? v + 1 : 0] : 0.f,
+                      v + 2 < NV ? part[v + 2 < NV ? v + 2 : 0] : 0.f, v + 3 < NV ? part[v + 3 < NV ? v + 3 : 0] : 0.f);
+    // LDS operations of one wave complete in issue order; the fences keep the
+    // compiler from moving the column reads above the row writes (or the next
+    // group's writes above these reads).
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    if (lane < NV) {
+      float sum = 0.f;
+#pragma unroll 16
+      for (int r = 0; r < kWave; ++r) sum += xpose[wave][r][lane];
+      const int g = lane / NP, pi = lane % NP;
+      if (u0 + g < nt) red[u0 + g][wave][pi] = sum;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
   }
   __syncthreads();
   for (int i = threadIdx.x; i < nt * NP; i += blockDim.x) {
@@ -193,9 +247,14 @@ __global__ __launch_bounds__(256) void k_post_gram_run(const TS* __restrict__ F,
   }
 }
 
-template <typename TS, int K1, int K2, int K3, int KK>
+// Write-back Y_j = sum_l H^res_jl a_l + sum_b wb_jb e_b for the KK active rows
+// (without H^res: Y_j = a_j + ...); SAVE keeps the rows read, NEXT forms the
+// next sublayer's input.  The run's indices and coefficients are staged in LDS
+// once; the loads of a group of G tokens are issued together.  T is a
+// multiple of G.
+template <typename TS, int KK, int G, bool RES, bool SAVE, bool NEXT>
 __global__ __launch_bounds__(256) void k_post_apply_run(TS* __restrict__ X, const TS* __restrict__ F, int64_t T,
-                                                        int64_t S, int N, int C, int k,
+                                                        int64_t S, int N, int C,
                                                         const float* __restrict__ conv_w,
                                                         const int32_t* __restrict__ idx,
                                                         const float* __restrict__ Hres,
@@ -203,102 +262,114 @@ __global__ __launch_bounds__(256) void k_post_apply_run(TS* __restrict__ X, cons
                                                         const float* __restrict__ Hpre_next,
                                                         const TS* __restrict__ base_next, TS* __restrict__ input_next,
                                                         TS* __restrict__ Xact_save) {
-  using RC = RunConv<TS, K1, K2, K3>;
-  constexpr int KR = RC::KR;
-  constexpr int G = 2;   // tokens whose loads are issued together; KK >= k active rows
+  using CG = ConvGroup<4, 8, 12>;
+  using R = Row4<TS>;
+  constexpr int KR = CG::KR;
+  __shared__ __align__(16) float s_hr[RES ? kRun * KK * KK : 4];
+  __shared__ __align__(16) float s_wb[kRun * KK * KR];
+  __shared__ int32_t s_idx[kRun * KK];
+  __shared__ float s_hn[NEXT ? kRun * kMaxN : 1];
   const int c = (int)(blockIdx.y * blockDim.x + threadIdx.x) * 4;
   const int64_t t0 = (int64_t)blockIdx.x * kRun;
   const int nt = (int)((T - t0 < kRun) ? T - t0 : kRun);
-  RC rc;
-  rc.load_taps(conv_w, C, c);
-  rc.init(F, t0, S, C, c);
+  for (int i = threadIdx.x; i < nt * KK; i += blockDim.x) s_idx[i] = idx[t0 * KK + i];
+  for (int i = threadIdx.x; i < nt * KK * KR; i += blockDim.x) s_wb[i] = wb[t0 * KK * KR + i];
+  if (RES)
+    for (int i = threadIdx.x; i < nt * KK * KK; i += blockDim.x) s_hr[i] = Hres[t0 * KK * KK + i];
+  if (NEXT)
+    for (int i = threadIdx.x; i < nt * N; i += blockDim.x) s_hn[i] = Hpre_next[t0 * N + i];
+  CG cg;
+  cg.load_taps(conv_w, C, c);
+  cg.init(F, t0, S, C, c);
+  __syncthreads();
   for (int u0 = 0; u0 < nt; u0 += G) {
-    float f[G][4], a[G][KK][4], nxt[G][4];
+    const int64_t t = t0 + u0;
+    if (t % S == 0) cg.reset();
     int32_t rows[G][KK];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      if (u0 + g < nt) {
-        const int64_t t = t0 + u0 + g;
-        Vec4<TS>::load(F + t * C + c, f[g]);
+    for (int g = 0; g < G; ++g)
 #pragma unroll
-        for (int l = 0; l < KK; ++l) {
-          if (l < k) {
-            rows[g][l] = idx[t * k + l];
-            Vec4<TS>::load(X + (t * N + rows[g][l]) * (int64_t)C + c, a[g][l]);
-          }
-        }
-        if (input_next) Vec4<TS>::load(base_next + t * C + c, nxt[g]);
-      }
+      for (int l = 0; l < KK; ++l) rows[g][l] = __builtin_amdgcn_readfirstlane(s_idx[(u0 + g) * KK + l]);
+    float cur[G][4];
+    typename R::raw a[G][KK], nb[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+      R::unpack(R::load(F + (t + g) * C + c), cur[g]);
+#pragma unroll
+      for (int l = 0; l < KK; ++l) a[g][l] = R::load(X + ((t + g) * N + rows[g][l]) * (int64_t)C + c);
+      if (NEXT) nb[g] = R::load(base_next + (t + g) * C + c);
     }
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      if (u0 + g >= nt) break;
-      const int64_t t = t0 + u0 + g;
-      rc.push(f[g], (t % S) == 0);
+      const int u = u0 + g;
+      const int64_t tg = t + g;
       float e[KR][4];
-      rc.components(e);
-      if (Xact_save) {
+      cg.components(cur, g, e);
+      if (SAVE) {
 #pragma unroll
-        for (int l = 0; l < KK; ++l)
-          if (l < k) Vec4<TS>::store(Xact_save + (t * k + l) * (int64_t)C + c, a[g][l]);
+        for (int l = 0; l < KK; ++l) R::store_raw(Xact_save + (tg * KK + l) * (int64_t)C + c, a[g][l]);
       }
+      float af[KK][4];
+#pragma unroll
+      for (int l = 0; l < KK; ++l) R::unpack(a[g][l], af[l]);
+      float nxt[4];
+      if (NEXT) R::unpack(nb[g], nxt);
+      const float* hr = s_hr + (RES ? u * KK * KK : 0);
+      const float* wv = s_wb + u * KK * KR;
 #pragma unroll
       for (int j = 0; j < KK; ++j) {
-        if (j < k) {
-          float y[4];
-          if (Hres) {
+        float y[4];
+        if (RES) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) y[q] = 0.f;
+          for (int q = 0; q < 4; ++q) y[q] = 0.f;
 #pragma unroll
-            for (int l = 0; l < KK; ++l) {
-              if (l < k) {
-                const float h = Hres[(t * k + j) * k + l];
+          for (int l = 0; l < KK; ++l) {
+            const float h = hr[j * KK + l];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) y[q] = fmaf(h, a[g][l][q], y[q]);
-              }
-            }
-          } else {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) y[q] = a[g][j][q];
+            for (int q = 0; q < 4; ++q) y[q] = fmaf(h, af[l][q], y[q]);
           }
+        } else {
 #pragma unroll
-          for (int b = 0; b < KR; ++b) {
-            const float wv = wb[(t * k + j) * KR + b];
+          for (int q = 0; q < 4; ++q) y[q] = af[j][q];
+        }
 #pragma unroll
-            for (int q = 0; q < 4; ++q) y[q] = fmaf(wv, e[b][q], y[q]);
-          }
-          Vec4<TS>::store(X + (t * N + rows[g][j]) * (int64_t)C + c, y);
-          if (input_next) {
-            Vec4<TS>::round(y);
-            const float h = Hpre_next[t * N + rows[g][j]];
+        for (int b = 0; b < KR; ++b) {
+          const float w = wv[j * KR + b];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) nxt[g][q] = fmaf(h, y[q], nxt[g][q]);
-          }
+          for (int q = 0; q < 4; ++q) y[q] = fmaf(w, e[b][q], y[q]);
+        }
+        R::store(X + (tg * N + rows[g][j]) * (int64_t)C + c, y);
+        if (NEXT) {
+          R::round(y);
+          const float h = s_hn[u * N + rows[g][j]];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) nxt[q] = fmaf(h, y[q], nxt[q]);
         }
       }
-      if (input_next) Vec4<TS>::store(input_next + t * C + c, nxt[g]);
+      if (NEXT) R::store(input_next + tg * C + c, nxt);
     }
+    cg.advance(cur);
   }
 }
 
 // threads per block of the run-based kernels for width C (4 channels each)
 static inline int run_threads(int C) { return C >= 1024 ? 256 : C / 4; }
-static inline bool run_ok(int C, int Kr, const int32_t* kappa) {
+static inline bool run_ok(int C, int64_t S, int Kr, const int32_t* kappa) {
   if (Kr != 4 || kappa[0] != 4 || kappa[1] != 8 || kappa[2] != 12) return false;
-  if (C % 4 != 0) return false;
+  if (C % 4 != 0 || S % 4 != 0) return false;
   const int nthr = run_threads(C);
   return nthr % kWave == 0 && C % (nthr * 4) == 0;
 }
 
-int64_t gram_chunks(int C, int Kr, const int32_t* kappa) {
-  if (run_ok(C, Kr, kappa)) return C / (run_threads(C) * 4);
+int64_t gram_chunks(int C, int64_t S, int Kr, const int32_t* kappa) {
+  if (run_ok(C, S, Kr, kappa)) return C / (run_threads(C) * 4);
   return post_chunks(C);
 }
 
 hipError_t launch_post_gram(int state_dtype, const void* F, int64_t T, int64_t S, int C, int Kr,
                             const int32_t* kappa, const float* conv_w, float* gpart, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (run_ok(C, Kr, kappa)) {
+  if (run_ok(C, S, Kr, kappa)) {
     const int nthr = run_threads(C);
     const dim3 grid((unsigned)((T + kRun - 1) / kRun), (unsigned)(C / (nthr * 4)));
     if (state_dtype == XHC_BF16)
@@ -449,18 +520,26 @@ hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T,
                              const float* Hres, const float* Hpost, const float* wb, const float* Hpre_next,
                              const void* base_next, void* input_next, void* Xact_save, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (wb && run_ok(C, Kr, kappa)) {
+  if (wb && run_ok(C, S, Kr, kappa) && T % 4 == 0 && (k == 4 || k == 8) &&
+      !(Hres && input_next) && !(Xact_save && (input_next || !Hres))) {
     const int nthr = run_threads(C);
     const dim3 grid((unsigned)((T + kRun - 1) / kRun), (unsigned)(C / (nthr * 4)));
-#define XHC_APPLY_RUN(TS, KK)                                                                                     \
-  k_post_apply_run<TS, 4, 8, 12, KK><<<grid, dim3(nthr), 0, s>>>(                                                \
-      reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(F), T, S, N, C, k, conv_w, idx, Hres, wb, Hpre_next, \
+#define XHC_APPLY_RUN(TS, KK, G, RES, SAVE, NEXT)                                                                  \
+  k_post_apply_run<TS, KK, G, RES, SAVE, NEXT><<<grid, dim3(nthr), 0, s>>>(                                      \
+      reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(F), T, S, N, C, conv_w, idx, Hres, wb, Hpre_next,    \
       reinterpret_cast<const TS*>(base_next), reinterpret_cast<TS*>(input_next), reinterpret_cast<TS*>(Xact_save))
+#define XHC_APPLY_MODES(TS, KK, G)                                              \
+  do {                                                                          \
+    if (input_next) XHC_APPLY_RUN(TS, KK, G, false, false, true);               \
+    else if (Xact_save) XHC_APPLY_RUN(TS, KK, G, true, true, false);            \
+    else XHC_APPLY_RUN(TS, KK, G, true, false, false);                          \
+  } while (0)
     if (state_dtype == XHC_BF16) {
-      if (k <= 4) XHC_APPLY_RUN(uint16_t, 4); else XHC_APPLY_RUN(uint16_t, kMaxK);
+      if (k == 4) XHC_APPLY_MODES(uint16_t, 4, 4); else XHC_APPLY_MODES(uint16_t, 8, 2);
     } else {
-      if (k <= 4) XHC_APPLY_RUN(float, 4); else XHC_APPLY_RUN(float, kMaxK);
+      if (k == 4) XHC_APPLY_MODES(float, 4, 2); else XHC_APPLY_MODES(float, 8, 1);
     }
+#undef XHC_APPLY_MODES
 #undef XHC_APPLY_RUN
     return hipGetLastError();
   }

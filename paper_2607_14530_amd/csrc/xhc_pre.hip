@@ -1,17 +1,15 @@
-// Mapping generation and dense read of an xHC sublayer (multi-kernel path).
+// Mapping generation of an xHC sublayer (multi-kernel path): packing and the
+// per-token finalisation of the projections.
 //
 //  k_pack / k_colsum   fp32 weights -> bf16 MFMA fragments; column sums of bf16(W_r)
-//  k_proj_partial      split-K MFMA projection of 16-token tiles (full state,
-//                      or the gathered active rows), plus the norm moments
+//  k_sum_chunks        per-token sums of the split-K partials
 //  k_pre_route         per token: LayerNorm / RMSNorm corrections of the raw
 //                      projection (eq:fused_normalized_projection), H^pre, routing
 //  k_pre_coef          per token: RMS of the active state, H^post, H^res (Sinkhorn + clamp)
-//  k_dense_read        input = sum_i H^pre_i x_i (eq:dense_read); xHC-Flash bases
 #include "xhc_device.h"
 #include "xhc_launch.h"
 
 namespace xhc {
-
 // ----------------------------------------------------------------- packing
 
 __global__ void k_pack(int64_t K, int nob, int ncols_a, const float* __restrict__ A, int ncols_b,
@@ -70,131 +68,6 @@ hipError_t launch_pack(int64_t K, int64_t nout, int ncols_a, const float* A, int
 hipError_t launch_colsum(int64_t K, int ncols, const float* W, float* out, hipStream_t s) {
   k_colsum<<<dim3(ncols), dim3(256), 0, s>>>(K, ncols, W, out);
   return hipGetLastError();
-}
-
-// ----------------------------------------------------------------- projection
-// One workgroup = 4 waves = one 16-token tile x one chunk of kProjChunkBlocks
-// 32-row blocks of K.  MFMA operands: A = packed weight fragment (outputs x K),
-// B = 8 state elements per lane (K x tokens).  With GATHER, K runs over the
-// active rows: row j of K is X[t, idx[t, j], :].
-// Output part[chunk][o][t] for o < 16*NOB, then sum x and sum x^2 at
-// o = 16*NOB and 16*NOB + 1.
-
-template <typename TS, int NOB, bool GATHER>
-__global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, int64_t T, int N, int C,
-                                                      int64_t K, const uint4* __restrict__ wpk,
-                                                      const int32_t* __restrict__ idx, int k,
-                                                      float* __restrict__ part) {
-  constexpr int NO = NOB * 16 + 2;
-  __shared__ float red[4][NO][kProjTile];
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int tl = lane % 16, grp = lane / 16;
-  const int64_t tile = blockIdx.x, chunk = blockIdx.y;
-  const int64_t t = tile * kProjTile + tl;
-  const bool valid = t < T;
-  const int64_t nblk = K / 32;
-  f32x4 acc[NOB];
-#pragma unroll
-  for (int ob = 0; ob < NOB; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float s1 = 0.f, s2 = 0.f;
-  // The state loads of UNR blocks are issued before any is used, so each wave
-  // keeps UNR loads in flight instead of one.
-  constexpr int UNR = Vec8<TS>::kSplit ? 4 : 16;
-  constexpr int BPW = kProjChunkBlocks / 4;   // blocks per wave
-  static_assert(BPW % UNR == 0, "unroll must divide the blocks per wave");
-  for (int b0 = 0; b0 < BPW; b0 += UNR) {
-    uint4 xb[UNR], xl[UNR];
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int64_t kb = chunk * kProjChunkBlocks + (b0 + u) * 4 + wave;
-      xb[u] = make_uint4(0, 0, 0, 0);
-      xl[u] = make_uint4(0, 0, 0, 0);
-      if (valid && kb < nblk) {
-        const int64_t kk = kb * 32 + grp * 8;
-        const TS* src;
-        if (GATHER) {
-          const int row = (int)(kk / C);
-          const int c = (int)(kk % C);
-          src = X + ((t * N + idx[t * k + row]) * (int64_t)C + c);
-        } else {
-          src = X + (t * (int64_t)N * C + kk);
-        }
-        float f[8];
-        xb[u] = Vec8<TS>::operand(src, f, xl[u]);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int64_t kb = chunk * kProjChunkBlocks + (b0 + u) * 4 + wave;
-      if (kb < nblk) {
-      // moments from the operand registers (hi + lo for an fp32 state, to 2^-16)
-      float f[8], g[8];
-      unpack8(xb[u], f);
-      unpack8(xl[u], g);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x = f[e] + g[e];
-        s1 += x;
-        s2 += x * x;
-      }
-#pragma unroll
-      for (int ob = 0; ob < NOB; ++ob) {
-        const uint4 wa = wpk[(kb * NOB + ob) * kWave + lane];
-        acc[ob] = mfma_16x16x32(wa, xb[u], acc[ob]);
-        if (Vec8<TS>::kSplit) acc[ob] = mfma_16x16x32(wa, xl[u], acc[ob]);
-      }
-      }
-    }
-  }
-  s1 += __shfl_xor(s1, 16);
-  s1 += __shfl_xor(s1, 32);
-  s2 += __shfl_xor(s2, 16);
-  s2 += __shfl_xor(s2, 32);
-#pragma unroll
-  for (int ob = 0; ob < NOB; ++ob)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) red[wave][ob * 16 + grp * 4 + v][tl] = acc[ob][v];
-  if (grp == 0) {
-    red[wave][NO - 2][tl] = s1;
-    red[wave][NO - 1][tl] = s2;
-  }
-  __syncthreads();
-  for (int i = threadIdx.x; i < NO * kProjTile; i += 256) {
-    const int o = i / kProjTile, tt = i % kProjTile;
-    const int64_t tg = tile * kProjTile + tt;
-    if (tg < T) part[(chunk * NO + o) * T + tg] = red[0][o][tt] + red[1][o][tt] + red[2][o][tt] + red[3][o][tt];
-  }
-}
-
-template <typename TS, bool GATHER>
-static hipError_t proj_dispatch(const TS* X, int64_t T, int N, int C, int64_t K, const void* packed, int nob,
-                                const int32_t* idx, int k, float* part, hipStream_t s) {
-  const dim3 grid((unsigned)((T + kProjTile - 1) / kProjTile), (unsigned)proj_chunks(K));
-  const uint4* w = reinterpret_cast<const uint4*>(packed);
-#define XHC_PROJ_CASE(NB) \
-  case NB: k_proj_partial<TS, NB, GATHER><<<grid, dim3(256), 0, s>>>(X, T, N, C, K, w, idx, k, part); break;
-  switch (nob) {
-    XHC_PROJ_CASE(1) XHC_PROJ_CASE(2) XHC_PROJ_CASE(3) XHC_PROJ_CASE(4)
-    XHC_PROJ_CASE(5) XHC_PROJ_CASE(6) XHC_PROJ_CASE(7) XHC_PROJ_CASE(8)
-    default: return hipErrorInvalidValue;
-  }
-#undef XHC_PROJ_CASE
-  return hipGetLastError();
-}
-
-hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N, int C, int64_t K,
-                               const void* packed, int64_t nout, const int32_t* idx, int k, float* part,
-                               hipStream_t s) {
-  if (T == 0) return hipSuccess;
-  const int nob = (int)out_blocks(nout);
-  if (state_dtype == XHC_BF16) {
-    const uint16_t* x = reinterpret_cast<const uint16_t*>(X);
-    return idx ? proj_dispatch<uint16_t, true>(x, T, N, C, K, packed, nob, idx, k, part, s)
-               : proj_dispatch<uint16_t, false>(x, T, N, C, K, packed, nob, idx, k, part, s);
-  }
-  const float* x = reinterpret_cast<const float*>(X);
-  return idx ? proj_dispatch<float, true>(x, T, N, C, K, packed, nob, idx, k, part, s)
-             : proj_dispatch<float, false>(x, T, N, C, K, packed, nob, idx, k, part, s);
 }
 
 // ----------------------------------------------------------------- per-token finalisation
@@ -326,76 +199,6 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
       sums, NO, T, k, Kq, with_res, (int64_t)k * C, alpha_post, alpha_res, b_post, b_res, eps, iters, delta,
       Hpost, Hres, saved, nsave, save_z_at, save_stats_at);
   return hipGetLastError();
-}
-
-// ----------------------------------------------------------------- dense read
-// out[q][t][c] = sum_i w_q[t][i] X[t][i][c] with w_q = Hpre[q][t][:]; for q >= 1
-// the active streams idx[t][:] are left out (xHC-Flash non-active bases,
-// App. E.2 eq:app_four_sub_base).  One thread per 8 channels of one token.
-
-template <typename TS, int NMAP>
-__global__ __launch_bounds__(256) void k_dense_read(const TS* __restrict__ X, int64_t T, int N, int C,
-                                                    const float* __restrict__ Hpre,
-                                                    const int32_t* __restrict__ idx, int k,
-                                                    TS* __restrict__ out0, TS* __restrict__ outr) {
-  const int64_t ncb = ((int64_t)C / 8 + 255) / 256;
-  const int64_t t = blockIdx.x / ncb;
-  const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
-  if (c >= C) return;
-  uint64_t act = 0;
-  if (NMAP > 1)
-    for (int j = 0; j < k; ++j) act |= 1ull << idx[t * k + j];
-  float acc[NMAP][8];
-#pragma unroll
-  for (int q = 0; q < NMAP; ++q)
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
-  const TS* xt = X + t * (int64_t)N * C + c;
-  constexpr int UNR = 8;   // stream rows loaded before use
-  for (int i0 = 0; i0 < N; i0 += UNR) {
-    float f[UNR][8];
-#pragma unroll
-    for (int u = 0; u < UNR; ++u)
-      if (i0 + u < N) Vec8<TS>::load(xt + (int64_t)(i0 + u) * C, f[u]);
-#pragma unroll
-    for (int u = 0; u < UNR; ++u) {
-      const int i = i0 + u;
-      if (i >= N) break;
-#pragma unroll
-      for (int q = 0; q < NMAP; ++q) {
-        float w = Hpre[((int64_t)q * T + t) * N + i];
-        if (q > 0 && ((act >> i) & 1ull)) w = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) acc[q][e] = fmaf(w, f[u][e], acc[q][e]);
-      }
-    }
-  }
-  Vec8<TS>::store(out0 + t * C + c, acc[0]);
-#pragma unroll
-  for (int q = 1; q < NMAP; ++q) Vec8<TS>::store(outr + ((int64_t)(q - 1) * T + t) * C + c, acc[q]);
-}
-
-template <typename TS>
-static hipError_t dense_dispatch(const TS* X, int64_t T, int N, int C, const float* Hpre, int nmap,
-                                 const int32_t* idx, int k, TS* out0, TS* outr, hipStream_t s) {
-  const dim3 grid((unsigned)(T * ((C / 8 + 255) / 256)));
-  switch (nmap) {
-    case 1: k_dense_read<TS, 1><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out0, outr); break;
-    case 2: k_dense_read<TS, 2><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out0, outr); break;
-    case 4: k_dense_read<TS, 4><<<grid, dim3(256), 0, s>>>(X, T, N, C, Hpre, idx, k, out0, outr); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
-                             int nmap, const int32_t* idx, int k, void* out0, void* outr, hipStream_t s) {
-  if (T == 0) return hipSuccess;
-  if (state_dtype == XHC_BF16)
-    return dense_dispatch<uint16_t>(reinterpret_cast<const uint16_t*>(X), T, N, C, Hpre, nmap, idx, k,
-                                    reinterpret_cast<uint16_t*>(out0), reinterpret_cast<uint16_t*>(outr), s);
-  return dense_dispatch<float>(reinterpret_cast<const float*>(X), T, N, C, Hpre, nmap, idx, k,
-                               reinterpret_cast<float*>(out0), reinterpret_cast<float*>(outr), s);
 }
 
 }  // namespace xhc

@@ -1,0 +1,195 @@
+// Split-K MFMA projection of token tiles onto packed weights (full state, or
+// the gathered active rows), plus the norm moments of each token.
+#include "xhc_device.h"
+#include "xhc_launch.h"
+
+namespace xhc {
+
+// ----------------------------------------------------------------- projection
+// One workgroup = 4 waves = TG token groups of 16 x one chunk of cb 32-row
+// blocks of K; wave w takes blocks w, w + 4, ... of the chunk for all TG
+// groups, so each weight fragment it loads serves TG MFMAs.  MFMA operands:
+// A = packed weight fragment (outputs x K), B = 8 state elements per lane
+// (K x tokens).  With GATHER, K runs over the active rows: row j of K is
+// X[t, idx[t, j], :].  Output part[chunk][o][t] for o < 16*NOB, then sum x and
+// sum x^2 at o = NO-2, NO-1 (the moments of eq:router_ln / eq:rmsnorm).
+// EXACT: cb divides the k-blocks, so no block needs a bound check.  NOB is an
+// upper bound of the nob output blocks.
+template <typename TS, int NOB, bool GATHER, bool EXACT, int TG>
+__global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, int64_t T, int N, int C,
+                                                      int64_t K, int64_t cb, const uint4* __restrict__ wpk,
+                                                      int nob, const int32_t* __restrict__ idx, int k,
+                                                      float* __restrict__ part) {
+  constexpr int NO = NOB * 16 + 2;   // LDS rows: outputs, then the two moments
+  const int NOr = nob * 16 + 2;      // rows of the partials
+  constexpr int TT = kProjTile * TG;   // tokens per workgroup
+  constexpr int UNR0 = 16 / TG < 8 ? 16 / TG : 8;
+  constexpr int UNR = Vec8<TS>::kSplit ? (UNR0 > 1 ? UNR0 / 2 : 1) : UNR0;   // blocks loaded before use
+  __shared__ float red[2][NO][TT];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int tl = lane % 16, grp = lane / 16;
+  const int64_t tile = blockIdx.x, chunk = blockIdx.y;
+  int64_t tc[TG];
+#pragma unroll
+  for (int g = 0; g < TG; ++g) {
+    const int64_t t = tile * TT + g * kProjTile + tl;
+    tc[g] = t < T ? t : T - 1;   // loads stay in bounds; results of t >= T are dropped
+  }
+  const int64_t nblk = K / 32;
+  f32x4 acc[TG][NOB];
+  float s1[TG], s2[TG];
+#pragma unroll
+  for (int g = 0; g < TG; ++g) {
+    s1[g] = s2[g] = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) acc[g][ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int64_t bpw = cb / 4;   // blocks per wave, a multiple of 8
+  for (int64_t b0 = 0; b0 < bpw; b0 += UNR) {
+    uint4 xb[UNR][TG], xl[UNR][TG], wa[UNR][NOB];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int64_t kb = chunk * cb + (b0 + u) * 4 + wave;
+      if (EXACT || kb < nblk) {
+        const int64_t kk = kb * 32 + grp * 8;
+#pragma unroll
+        for (int g = 0; g < TG; ++g) {
+          const TS* src;
+          if (GATHER) {
+            const int row = (int)(kk / C);
+            const int c = (int)(kk % C);
+            src = X + ((tc[g] * N + idx[tc[g] * k + row]) * (int64_t)C + c);
+          } else {
+            src = X + (tc[g] * (int64_t)N * C + kk);
+          }
+          float f[8];
+          xb[u][g] = Vec8<TS>::operand(src, f, xl[u][g]);
+        }
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob)
+          if (ob < nob) wa[u][ob] = wpk[(kb * nob + ob) * kWave + lane];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int64_t kb = chunk * cb + (b0 + u) * 4 + wave;
+      if (EXACT || kb < nblk) {
+#pragma unroll
+        for (int g = 0; g < TG; ++g) {
+          // moments from the operand registers (hi + lo for an fp32 state, to 2^-16)
+          float f[8], h[8];
+          unpack8(xb[u][g], f);
+          unpack8(xl[u][g], h);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float x = f[e] + h[e];
+            s1[g] += x;
+            s2[g] += x * x;
+          }
+#pragma unroll
+          for (int ob = 0; ob < NOB; ++ob) {
+            if (ob < nob) {
+              acc[g][ob] = mfma_16x16x32(wa[u][ob], xb[u][g], acc[g][ob]);
+              if (Vec8<TS>::kSplit) acc[g][ob] = mfma_16x16x32(wa[u][ob], xl[u][g], acc[g][ob]);
+            }
+          }
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < TG; ++g) {
+    s1[g] += __shfl_xor(s1[g], 16);
+    s1[g] += __shfl_xor(s1[g], 32);
+    s2[g] += __shfl_xor(s2[g], 16);
+    s2[g] += __shfl_xor(s2[g], 32);
+  }
+  // waves 0, 1 write; waves 2, 3 add theirs; the two halves are added on the way out
+  for (int step = 0; step < 2; ++step) {
+    if ((wave >> 1) == step) {
+      float(*r)[TT] = red[wave & 1];
+#pragma unroll
+      for (int g = 0; g < TG; ++g) {
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            float& dst = r[ob * 16 + grp * 4 + v][g * kProjTile + tl];
+            dst = step ? dst + acc[g][ob][v] : acc[g][ob][v];
+          }
+        if (grp == 0) {
+          float& d1 = r[NO - 2][g * kProjTile + tl];
+          float& d2 = r[NO - 1][g * kProjTile + tl];
+          d1 = step ? d1 + s1[g] : s1[g];
+          d2 = step ? d2 + s2[g] : s2[g];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  for (int i = threadIdx.x; i < NOr * TT; i += 256) {
+    const int o = i / TT, tt = i % TT;
+    const int r = o < nob * 16 ? o : o - nob * 16 + NOB * 16;
+    const int64_t tg = tile * TT + tt;
+    if (tg < T) part[(chunk * NOr + o) * T + tg] = red[0][r][tt] + red[1][r][tt];
+  }
+}
+
+// output-block bound of a kernel instance: 1, 2, 3, 5 or 8
+static inline int nob_bucket(int nob) { return nob <= 3 ? nob : (nob <= 5 ? 5 : 8); }
+
+template <typename TS, bool GATHER, bool EXACT, int TG>
+static hipError_t proj_launch(const TS* X, int64_t T, int N, int C, int64_t K, const ProjPlan& pl, const uint4* w,
+                              int nob, const int32_t* idx, int k, float* part, hipStream_t s) {
+  const dim3 grid((unsigned)((T + kProjTile * TG - 1) / (kProjTile * TG)), (unsigned)pl.nchunk);
+#define XHC_PROJ_CASE(NB)                                                                           \
+  case NB:                                                                                          \
+    k_proj_partial<TS, NB, GATHER, EXACT, TG>                                                       \
+        <<<grid, dim3(256), 0, s>>>(X, T, N, C, K, pl.chunk_blocks, w, nob, idx, k, part);          \
+    break;
+  switch (nob_bucket(nob)) {
+    XHC_PROJ_CASE(1) XHC_PROJ_CASE(2) XHC_PROJ_CASE(3) XHC_PROJ_CASE(5) XHC_PROJ_CASE(8)
+    default: return hipErrorInvalidValue;
+  }
+#undef XHC_PROJ_CASE
+  return hipGetLastError();
+}
+
+// bf16 state: token groups per the plan, the exact variant where the chunks
+// divide K (full state); an fp32 state takes one token group per wave (the
+// same chunks, more workgroups).
+template <typename TS, bool GATHER>
+static hipError_t proj_dispatch(const TS* X, int64_t T, int N, int C, int64_t K, const void* packed, int64_t nout,
+                                const int32_t* idx, int k, float* part, hipStream_t s) {
+  const ProjPlan pl = proj_plan(K, nout, T);
+  const uint4* w = reinterpret_cast<const uint4*>(packed);
+  const int nob = (int)out_blocks(nout);
+  if (nob > 8) return hipErrorInvalidValue;
+  if (Vec8<TS>::kSplit) return proj_launch<TS, GATHER, false, 1>(X, T, N, C, K, pl, w, nob, idx, k, part, s);
+  const bool exact = !GATHER && (K / 32) % pl.chunk_blocks == 0;
+#define XHC_PROJ_TG(TGV)                                                                            \
+  return exact ? proj_launch<TS, GATHER, !GATHER, TGV>(X, T, N, C, K, pl, w, nob, idx, k, part, s) \
+               : proj_launch<TS, GATHER, false, TGV>(X, T, N, C, K, pl, w, nob, idx, k, part, s)
+  switch (pl.tg) {
+    case 4: XHC_PROJ_TG(4);
+    case 2: XHC_PROJ_TG(2);
+    default: XHC_PROJ_TG(1);
+  }
+#undef XHC_PROJ_TG
+}
+
+hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N, int C, int64_t K,
+                               const void* packed, int64_t nout, const int32_t* idx, int k, float* part,
+                               hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  if (state_dtype == XHC_BF16) {
+    const uint16_t* x = reinterpret_cast<const uint16_t*>(X);
+    return idx ? proj_dispatch<uint16_t, true>(x, T, N, C, K, packed, nout, idx, k, part, s)
+               : proj_dispatch<uint16_t, false>(x, T, N, C, K, packed, nout, idx, k, part, s);
+  }
+  const float* x = reinterpret_cast<const float*>(X);
+  return idx ? proj_dispatch<float, true>(x, T, N, C, K, packed, nout, idx, k, part, s)
+             : proj_dispatch<float, false>(x, T, N, C, K, packed, nout, idx, k, part, s);
+}
+
+}  // namespace xhc

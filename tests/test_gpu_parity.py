@@ -19,6 +19,13 @@ SMALL = [
     W(T=40, S=20, N=5, k=3, m=1, C=64, Kr=3, kappa=(2, 5), name="odd-N5-k3-Kr3"),
     W(T=48, S=16, N=32, k=8, m=0, C=128, Kr=4, name="wide-N32-k8-m0"),
     W(T=64, N=16, k=4, m=2, C=256, Kr=4, state="f32", name="f32-mlp"),
+    # run-based MLP-type post kernels: runs of 64 tokens in groups, sequence
+    # starts inside runs, ragged last run, 192-thread blocks (T is whole
+    # sequences and S % 4 == 0 there, so a group is never ragged)
+    W(T=300, S=100, N=8, k=4, m=2, C=768, Kr=4, name="runs-T300-S100-C768"),
+    W(T=136, S=68, N=16, k=4, m=2, C=1024, Kr=4, state="f32", name="runs-f32-T136-S68"),
+    W(T=96, S=48, N=16, k=8, m=2, C=512, Kr=4, name="runs-k8-T96"),
+    W(T=150, S=50, N=8, k=4, m=2, C=256, Kr=4, name="S50-per-token-post"),   # S % 4 != 0
 ]
 
 
