@@ -61,21 +61,17 @@ int64_t NC_of(const xhc_dims* d) { return (int64_t)d->N * d->C; }
 int64_t kC_of(const xhc_dims* d) { return (int64_t)d->k * d->C; }
 int64_t act_outs(const xhc_dims* d, int Kq, int with_res) { return (int64_t)d->k * Kq + (with_res ? d->k * d->k : 0); }
 
-size_t part_bytes(int64_t K, int64_t nout, int64_t T) {
-  return align_up((size_t)proj_chunks(K, nout, T) * (size_t)(out_blocks(nout) * 16 + 2) * (size_t)T * sizeof(float));
-}
-
-// partials of the dense read + active projection pass (one per channel chunk)
-size_t read_part_bytes(const xhc_dims* d, int64_t nout) {
-  return align_up((size_t)read_chunks(d->C) * (size_t)(out_blocks(nout) * 16 + 2) * (size_t)d->T * sizeof(float));
+size_t part_bytes(const xhc_dims* d, bool gather, int64_t K, int64_t nout) {
+  return align_up((size_t)proj_chunks(d->state_dtype, gather, K, d->C, nout, d->T) * (size_t)(out_blocks(nout) * 16 + 2) *
+                  (size_t)d->T * sizeof(float));
 }
 
 // partials of the larger projection, then the per-token sums of either one
 size_t sums_bytes(int64_t nout, int64_t T) { return align_up((size_t)(out_blocks(nout) * 16 + 2) * T * sizeof(float)); }
 
 size_t pre_ws_multi(const xhc_dims* d) {
-  const size_t full = part_bytes(NC_of(d), 2 * d->N, d->T);
-  const size_t act = read_part_bytes(d, act_outs(d, d->Kr, 1));
+  const size_t full = part_bytes(d, false, NC_of(d), 2 * d->N);
+  const size_t act = part_bytes(d, true, kC_of(d), act_outs(d, d->Kr, 1));
   const size_t sf = sums_bytes(2 * d->N, d->T), sa = sums_bytes(act_outs(d, d->Kr, 1), d->T);
   return (full > act ? full : act) + (sf > sa ? sf : sa);
 }
@@ -98,7 +94,7 @@ int flash_Kq(const xhc_dims* d, int q) { return (q % 2 == 1) ? 1 : d->Kr; }
 
 size_t flash_pre_ws(const xhc_dims* d, int Q) {
   const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, 1, 0);
-  const size_t full = part_bytes(NC_of(d), nf, d->T), act = read_part_bytes(d, na);
+  const size_t full = part_bytes(d, false, NC_of(d), nf), act = part_bytes(d, true, kC_of(d), na);
   const size_t sf = sums_bytes(nf, d->T), sa = sums_bytes(na, d->T);
   return (full > act ? full : act) + (sf > sa ? sf : sa);
 }
@@ -114,7 +110,7 @@ size_t flash_post_ws(const xhc_dims* d, int Q, int q) {
   size_t need = Kq > 1 ? gram_bytes(d, Kq) : 0;
   if (q < Q) {
     const int64_t na = act_outs(d, flash_Kq(d, q + 1), q + 1 == Q);
-    need = std::max(need, part_bytes(kC_of(d), na, d->T) + sums_bytes(na, d->T));
+    need = std::max(need, part_bytes(d, true, kC_of(d), na) + sums_bytes(na, d->T));
   }
   return need;
 }
@@ -166,7 +162,8 @@ xhc_status xhc_pack_full(const xhc_dims* d, int32_t npre, const float* W_r, cons
   clear_stale_error();
   const int64_t K = NC_of(d);
   hipError_t e = hipSuccess;
-  XHC_STEP("pack", launch_pack(K, (int64_t)(1 + npre) * d->N, d->N, W_r, d->N, W_pre, npre, packed, s));
+  XHC_STEP("pack", launch_pack(K, (int64_t)(1 + npre) * d->N, d->N, W_r, d->N, W_pre, npre,
+                               full_grouped(d->state_dtype, K), packed, s));
   float* colsum = reinterpret_cast<float*>(reinterpret_cast<char*>(packed) +
                                            packed_frag_bytes(K, (int64_t)(1 + npre) * d->N));
   XHC_STEP("colsum", launch_colsum(K, d->N, W_r, colsum, s));
@@ -182,7 +179,8 @@ xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, c
   clear_stale_error();
   hipError_t e = hipSuccess;
   XHC_STEP("pack", launch_pack(kC_of(d), act_outs(d, Kq, with_res), d->k * Kq, W_post, d->k * d->k, W_res,
-                               with_res ? 1 : 0, packed, reinterpret_cast<hipStream_t>(stream)));
+                               with_res ? 1 : 0, act_grouped(d->state_dtype, d->C), packed,
+                               reinterpret_cast<hipStream_t>(stream)));
   return hip_status(e);
 }
 
@@ -235,7 +233,8 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   clear_stale_error();
   float* part = reinterpret_cast<float*>(workspace);
-  const size_t part_max = std::max(part_bytes(NC_of(d), 2 * d->N, d->T), read_part_bytes(d, act_outs(d, d->Kr, 1)));
+  const size_t part_max = std::max(part_bytes(d, false, NC_of(d), 2 * d->N),
+                                   part_bytes(d, true, kC_of(d), act_outs(d, d->Kr, 1)));
   float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_max);
   const int64_t NC = NC_of(d), kC = kC_of(d);
   const int64_t nout_full = 2 * d->N, nout_act = act_outs(d, d->Kr, 1);
@@ -256,14 +255,17 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   }
   XHC_STEP("proj_full", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full,
                                             nullptr, d->k, part, s));
-  XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(NC, nout_full, d->T), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,
+  XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(d->state_dtype, false, NC, d->C, nout_full, d->T), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,
                                          alpha, 1, b_pre, d->eps, idx, p, Hpre, sums, saved, nsave,
                                          nsave - 4, s));
-  XHC_STEP("read_active", launch_read_active(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, packed_act,
-                                             nout_act, input, nullptr, part, s));
-  XHC_STEP("pre_coef", launch_pre_coef(part, read_chunks(d->C), nout_act, d->T, d->k, d->Kr, 1, d->C, alpha + 2,
-                                       alpha + 1, b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost,
-                                       Hres, sums, saved, nsave, 2 * d->N, nsave - 2, s));
+  XHC_STEP("proj_active", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act, nout_act, idx,
+                                              d->k, part, s));
+  XHC_STEP("pre_coef", launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, nout_act, d->T), nout_act,
+                                       d->T, d->k, d->Kr, 1, d->C, alpha + 2, alpha + 1, b_post, b_res, d->eps,
+                                       d->sinkhorn_iters, d->clamp_delta, Hpost, Hres, sums, saved, nsave, 2 * d->N,
+                                       nsave - 2, s));
+  XHC_STEP("dense_read",
+           launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, 1, idx, d->k, input, nullptr, s));
   return hip_status(e);
 }
 
@@ -324,19 +326,22 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
   const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, 1, 0);
   float* part = reinterpret_cast<float*>(workspace);
   float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
-                                         std::max(part_bytes(NC, nf, d->T), read_part_bytes(d, na)));
+                                         std::max(part_bytes(d, false, NC, nf), part_bytes(d, true, kC, na)));
   const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
                                                        packed_frag_bytes(NC, nf));
   hipError_t e = hipSuccess;
   XHC_STEP("flash_proj_full",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nf, nullptr, d->k, part, s));
-  XHC_STEP("flash_route", launch_pre_route(part, proj_chunks(NC, nf, d->T), nf, d->T, d->N, d->m, d->k, Q, d->C, colsum,
+  XHC_STEP("flash_route", launch_pre_route(part, proj_chunks(d->state_dtype, false, NC, d->C, nf, d->T), nf, d->T, d->N, d->m, d->k, Q, d->C, colsum,
                                            alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, nullptr, 0, 0, s));
-  XHC_STEP("flash_read_active", launch_read_active(d->state_dtype, X, d->T, d->N, d->C, Hpre, Q, idx, d->k,
-                                                   packed_act1, na, input1, base, part, s));
-  XHC_STEP("flash_coef1", launch_pre_coef(part, read_chunks(d->C), na, d->T, d->k, 1, 0, d->C, alpha_post1, nullptr,
-                                          b_post1, nullptr, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost1,
-                                          nullptr, sums, nullptr, 0, 0, 0, s));
+  XHC_STEP("flash_proj_active",
+           launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act1, na, idx, d->k, part, s));
+  XHC_STEP("flash_coef1", launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, na, d->T), na, d->T,
+                                          d->k, 1, 0, d->C, alpha_post1, nullptr, b_post1, nullptr, d->eps,
+                                          d->sinkhorn_iters, d->clamp_delta, Hpost1, nullptr, sums, nullptr, 0, 0, 0,
+                                          s));
+  XHC_STEP("flash_dense_read",
+           launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, Q, idx, d->k, input1, base, s));
   return hip_status(e);
 }
 
@@ -387,11 +392,11 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
     const int with_res = (q + 1 == Q);
     const int64_t kC = kC_of(d), na = act_outs(d, Kn, with_res);
     float* part = reinterpret_cast<float*>(workspace);
-    float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_bytes(kC, na, d->T));
+    float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_bytes(d, true, kC, na));
     XHC_STEP("flash_proj_next",
              launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act_next, na, idx, d->k, part, s));
     XHC_STEP("flash_coef_next",
-             launch_pre_coef(part, proj_chunks(kC, na, d->T), na, d->T, d->k, Kn, with_res, d->C, alpha_next,
+             launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, na, d->T), na, d->T, d->k, Kn, with_res, d->C, alpha_next,
                              with_res ? alpha_next + 1 : nullptr, b_post_next, b_res_next, d->eps, d->sinkhorn_iters,
                              d->clamp_delta, Hpost_next, Hres_next, sums, nullptr, 0, 0, 0, s));
   }

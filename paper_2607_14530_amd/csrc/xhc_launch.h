@@ -17,42 +17,58 @@ constexpr int kMaxKr = 4;   // write-back components
 
 // packed projection layout: fragments of 64 lanes x 8 bf16 (1 KiB), indexed
 // [k_block (32 rows)][out_block (16 columns)][lane]; lane l of fragment
-// (kb, ob) holds W[kb*32 + 8*(l/16) + e][ob*16 + l%16], e = 0..7.
+// (kb, ob) holds W[kb*32 + 8*(l/16) + e][ob*16 + l%16], e = 0..7.  Grouped
+// layout (full-state weights of a bf16 state, K % 128 == 0): fragment
+// 4G + u holds rows 128G + 32*(l/16) + 8u + e instead, so that a lane's four
+// consecutive fragments of a group meet 64 contiguous state bytes.
+inline bool full_grouped(int state_dtype, int64_t K) { return state_dtype == XHC_BF16 && K % 128 == 0; }
+// the same for the active-state weights (K = k C, gathered rows): groups must
+// not straddle two rows
+inline bool act_grouped(int state_dtype, int C) { return state_dtype == XHC_BF16 && C % 128 == 0; }
 __host__ __device__ inline int64_t out_blocks(int64_t nout) { return (nout + 15) / 16; }
 inline size_t packed_frag_bytes(int64_t K, int64_t nout) { return (size_t)(K / 32) * out_blocks(nout) * 1024; }
 constexpr size_t kColsumBytes = 64 * sizeof(float);
 
 hipError_t launch_pack(int64_t K, int64_t nout, int ncols_a, const float* A, int ncols_b, const float* B,
-                       int64_t b_count, void* packed, hipStream_t s);
+                       int64_t b_count, bool grouped, void* packed, hipStream_t s);
 hipError_t launch_colsum(int64_t K, int ncols, const float* W, float* out, hipStream_t s);
 
 // ---- pre (multi-kernel path)
 constexpr int kProjTile = 16;    // tokens per MFMA column group
 
-// Launch plan of the split-K projection: each wave multiplies tg token groups
-// of 16 by the same weight fragment (fewer fragment loads per state byte), a
-// workgroup covers chunk_blocks 32-row blocks of K, and nchunk partials are
-// summed per token afterwards.  The reduction buffer 2 x NO x 16 tg floats
-// stays within 64 KiB of LDS.
+// Launch plan of the split-K projection.  Wide path (bf16 state, grouped
+// weight layout, full or gathered rows): 256-token workgroups, 4 consecutive
+// k-blocks per step, weight fragments shared through LDS.  Other cases: each wave multiplies tg token groups of
+// 16 by the same weight fragment.  A workgroup covers chunk_blocks 32-row
+// blocks of K; nchunk partials are summed per token afterwards.
 struct ProjPlan {
+  bool wide;
   int tg;
   int64_t chunk_blocks;
   int64_t nchunk;
 };
-inline ProjPlan proj_plan(int64_t K, int64_t nout, int64_t T) {
+constexpr int kWideTokens = 256;
+constexpr int kWideStep = 4;   // k-blocks per step of the wide path
+// steps whose weight fragments (kWideStep x nob KiB each) share one 64 KiB LDS fill
+__host__ __device__ constexpr int wide_seg_steps(int nob) { return nob <= 2 ? 8 : (nob <= 4 ? 4 : 2); }
+inline ProjPlan proj_plan(int state_dtype, bool gather, int64_t K, int C, int64_t nout, int64_t T) {
   const int64_t nblk = K / 32, NO = out_blocks(nout) * 16 + 2;
+  const bool wide = (gather ? act_grouped(state_dtype, C) : full_grouped(state_dtype, K)) && out_blocks(nout) <= 8;
   int tg = 4;
   while (tg > 1 && ((T + 16 * tg - 1) / (16 * tg) < 128 || NO * tg > 160)) tg /= 2;
-  const int64_t tiles = (T + 16 * tg - 1) / (16 * tg);
+  const int64_t tiles = wide ? (T + kWideTokens - 1) / kWideTokens : (T + 16 * tg - 1) / (16 * tg);
+  const int64_t gran = 32;                                      // chunk granularity in k-blocks
   int64_t want = (1024 + tiles - 1) / tiles;                    // chunks for about 1024 workgroups
-  const int64_t most = (nblk + 31) / 32;                        // chunks of at least 32 blocks
+  const int64_t most = (nblk + gran - 1) / gran;
   if (want > most) want = most;
   if (want < 1) want = 1;
   int64_t cb = (nblk + want - 1) / want;
-  cb = (cb + 31) / 32 * 32;                                     // a multiple of 4 waves x 8 blocks
-  return ProjPlan{tg, cb, (nblk + cb - 1) / cb};
+  cb = (cb + gran - 1) / gran * gran;
+  return ProjPlan{wide, tg, cb, (nblk + cb - 1) / cb};
 }
-inline int64_t proj_chunks(int64_t K, int64_t nout, int64_t T) { return proj_plan(K, nout, T).nchunk; }
+inline int64_t proj_chunks(int state_dtype, bool gather, int64_t K, int C, int64_t nout, int64_t T) {
+  return proj_plan(state_dtype, gather, K, C, nout, T).nchunk;
+}
 
 hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N, int C, int64_t K,
                                const void* packed, int64_t nout, const int32_t* idx, int k,
@@ -66,15 +82,10 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
                            float* Hpost, float* Hres, float* sums, float* saved, int nsave, int save_z_at,
                            int save_stats_at, hipStream_t s);
-// dense read + active projection, in chunks of kReadSlices 32-channel slices:
 // out0 gets map 0 (full dense read); maps 1..nmap-1 leave out the active
 // streams and go to outr + (q - 1) * T * C.
-constexpr int kReadSlices = 32;
-__host__ __device__ inline int64_t read_chunks(int C) { return ((int64_t)C / 32 + kReadSlices - 1) / kReadSlices; }
-hipError_t launch_read_active(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre, int nmap,
-                              const int32_t* idx, int k, const void* packed_act, int64_t nout_act, void* out0,
-                              void* outr, float* part, hipStream_t s);
-
+hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
+                             int nmap, const int32_t* idx, int k, void* out0, void* outr, hipStream_t s);
 
 // ---- pre (fused single-pass path: bf16 state, N = 16, k = 4, C % 128 == 0)
 bool fused_pre_supported(const xhc_dims* d);

@@ -13,7 +13,7 @@ namespace xhc {
 // ----------------------------------------------------------------- packing
 
 __global__ void k_pack(int64_t K, int nob, int ncols_a, const float* __restrict__ A, int ncols_b,
-                       const float* __restrict__ B, int64_t b_count, uint4* __restrict__ out) {
+                       const float* __restrict__ B, int64_t b_count, int grouped, uint4* __restrict__ out) {
   const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t nfrag = (K / 32) * nob;
   if (gid >= nfrag * kWave) return;
@@ -22,7 +22,8 @@ __global__ void k_pack(int64_t K, int nob, int ncols_a, const float* __restrict_
   const int ob = (int)(frag % nob);
   const int64_t kb = frag / nob;
   const int col = ob * 16 + lane % 16;
-  const int64_t row0 = kb * 32 + (lane / 16) * 8;
+  // grouped: fragment 4G + u, lane group g holds rows 128G + 32g + 8u .. +8
+  const int64_t row0 = grouped ? (kb / 4) * 128 + (lane / 16) * 32 + (kb % 4) * 8 : kb * 32 + (lane / 16) * 8;
   const int64_t nb = (int64_t)ncols_b * b_count;
   float f[8];
 #pragma unroll
@@ -56,11 +57,12 @@ __global__ void k_colsum(int64_t K, int ncols, const float* __restrict__ W, floa
 }
 
 hipError_t launch_pack(int64_t K, int64_t nout, int ncols_a, const float* A, int ncols_b, const float* B,
-                       int64_t b_count, void* packed, hipStream_t s) {
+                       int64_t b_count, bool grouped, void* packed, hipStream_t s) {
   const int nob = (int)out_blocks(nout);
   const int64_t threads = (K / 32) * nob * kWave;
   if (threads == 0) return hipSuccess;
   k_pack<<<dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s>>>(K, nob, ncols_a, A, ncols_b, B, b_count,
+                                                                       grouped ? 1 : 0,
                                                                        reinterpret_cast<uint4*>(packed));
   return hipGetLastError();
 }

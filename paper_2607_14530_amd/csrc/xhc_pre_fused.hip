@@ -227,7 +227,8 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
 #pragma unroll
     for (int r = 0; r < KB1W; ++r) {
       const int q = wave * KB1W + r, i = q / (FCS / 32), cb = q % (FCS / 32);
-      const uint4 xb = (tl < FM) ? lds_read16(&sm.buf[b][tl * TOKP + i * ROWB + (cb * 32 + grp * 8) * 2])
+      // grouped weight layout: fragment cb of the 128-channel slice meets channels 32 grp + 8 cb
+      const uint4 xb = (tl < FM) ? lds_read16(&sm.buf[b][tl * TOKP + i * ROWB + (grp * 32 + cb * 8) * 2])
                                  : make_uint4(0, 0, 0, 0);
       float f[8];
       unpack8(xb, f);
@@ -325,7 +326,8 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
     for (int r = 0; r < KBAW; ++r) {
       const int q = wave * KBAW + r, j = q / (FCS / 32), cb = q % (FCS / 32);
       const int row = sm.id[tl % FM][j] & (FN - 1);   // always inside the tile, whatever idx holds
-      const uint4 xb = (tl < FM) ? lds_read16(&sm.buf[b][tl * TOKP + row * ROWB + (cb * 32 + grp * 8) * 2])
+      // grouped weight layout (C % 128 == 0): fragment cb meets channels 32 grp + 8 cb
+      const uint4 xb = (tl < FM) ? lds_read16(&sm.buf[b][tl * TOKP + row * ROWB + (grp * 32 + cb * 8) * 2])
                                  : make_uint4(0, 0, 0, 0);
       float f[8];
       unpack8(xb, f);

@@ -135,6 +135,148 @@ __global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, 
   }
 }
 
+// Wide path (bf16 state, full rows, grouped weight layout).  A workgroup
+// takes 256 tokens (wave w: four groups of 16, tokens 64w..64w+63) and a chunk
+// of cb k-blocks, walked in steps of one group of 4 k-blocks (128 elements):
+// each lane loads 64 contiguous bytes of its token per step, so a wave
+// requests 256 contiguous bytes of each of its 64 token rows together.  The step's weight fragments are copied once per workgroup
+// into LDS (double-buffered, straight from global memory) and serve the 16
+// token groups of the four waves.  Each wave owns its tokens, so partials go
+// out without a cross-wave reduction.  EXACT: cb divides the k-blocks.
+template <int NOB, bool EXACT, bool GATHER>
+__global__ __launch_bounds__(256) void k_proj_wide(const uint16_t* __restrict__ X, int64_t T, int N, int C, int64_t K,
+                                                   int64_t cb, const uint4* __restrict__ wpk,
+                                                   const int32_t* __restrict__ idx, int k, float* __restrict__ part) {
+  constexpr int TG = 4, KS = kWideStep, NOr = NOB * 16 + 2;
+  constexpr int SS = wide_seg_steps(NOB);   // steps whose fragments share one LDS fill
+  extern __shared__ uint4 wl[];             // [SS][KS][NOB][64 lanes]; dynamic, as the LDS copy needs it
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int tl = lane % 16, grp = lane / 16;
+  const int64_t tile = blockIdx.x, chunk = blockIdx.y;
+  const int64_t nblk = K / 32, kb0 = chunk * cb;
+  const uint16_t* xr[TG];   // the token's state (GATHER: its first row)
+  int64_t tok[TG];
+  int32_t rows[GATHER ? TG : 1][kMaxK];
+#pragma unroll
+  for (int g = 0; g < TG; ++g) {
+    tok[g] = tile * kWideTokens + wave * 64 + g * 16 + tl;
+    const int64_t tc = tok[g] < T ? tok[g] : T - 1;   // loads stay in bounds; results of t >= T are dropped
+    if (GATHER) {
+      xr[g] = X + tc * N * (int64_t)C + grp * 32;
+#pragma unroll
+      for (int j = 0; j < kMaxK; ++j) rows[g][j] = j < k ? idx[tc * k + j] : 0;
+    } else {
+      xr[g] = X + tc * K + grp * 32;
+    }
+  }
+  f32x4 acc[TG][NOB];
+  float s1[TG], s2[TG];
+#pragma unroll
+  for (int g = 0; g < TG; ++g) {
+    s1[g] = s2[g] = 0.f;
+#pragma unroll
+    for (int ob = 0; ob < NOB; ++ob) acc[g][ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  struct Step {
+    uint4 x[KS][TG];
+  };
+  // grouped layout: step u of the group at kbs takes 8 elements at 32 grp + 8 u
+  // GATHER: K index j C + c is channel c of routed row j; a group of 128 never
+  // straddles two rows (C % 128 == 0)
+  auto load = [&](Step& b, int64_t kbs) {
+    const int64_t ko = kbs * 32;
+    const int j = GATHER ? (int)(ko / C) : 0;
+    const int64_t c = GATHER ? ko % C : ko;
+#pragma unroll
+    for (int g = 0; g < TG; ++g) {
+      const uint16_t* p = xr[g] + c;
+      if (GATHER) {
+        int r = rows[g][0];
+#pragma unroll
+        for (int jj = 1; jj < kMaxK; ++jj)
+          if (jj == j) r = rows[g][jj];
+        p += (int64_t)r * C;
+      }
+#pragma unroll
+      for (int u = 0; u < KS; ++u) {
+        b.x[u][g] = make_uint4(0, 0, 0, 0);
+        if (EXACT || kbs + u < nblk) b.x[u][g] = *reinterpret_cast<const uint4*>(p + u * 8);
+      }
+    }
+  };
+  auto compute = [&](const Step& b, int64_t kbs, int sj) {
+#pragma unroll
+    for (int u = 0; u < KS; ++u) {
+      if (EXACT || kbs + u < nblk) {
+        uint4 wa[NOB];
+#pragma unroll
+        for (int ob = 0; ob < NOB; ++ob) wa[ob] = wl[((sj * KS + u) * NOB + ob) * kWave + lane];
+#pragma unroll
+        for (int g = 0; g < TG; ++g) {
+          float f[8];
+          unpack8(b.x[u][g], f);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            s1[g] += f[e];
+            s2[g] += f[e] * f[e];
+          }
+#pragma unroll
+          for (int ob = 0; ob < NOB; ++ob) acc[g][ob] = mfma_16x16x32(wa[ob], b.x[u][g], acc[g][ob]);
+        }
+      }
+    }
+  };
+  const int64_t nsteps = cb / KS;
+  for (int64_t s0 = 0; s0 < nsteps; s0 += SS) {
+    // fragments of steps s0 .. s0+SS-1 -> LDS, one 1 KiB fragment per wave
+    // instruction; the barrier first lets every wave finish the previous fill
+    __syncthreads();
+    for (int fi = wave; fi < SS * KS * NOB; fi += 4) {
+      const int64_t kb = kb0 + s0 * KS + fi / NOB;
+      if (EXACT || kb < nblk)
+        __builtin_amdgcn_global_load_lds(wpk + (kb * NOB + fi % NOB) * kWave + lane, wl + fi * kWave, 16, 0, 0);
+    }
+    Step A, B;
+    load(A, kb0 + s0 * KS);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    // within the fill, the state loads of step s + 1 are in flight while step s is computed
+#pragma nounroll
+    for (int sj = 0; sj < SS; sj += 2) {
+      // (the scheduling barriers keep each phase's loads from being hoisted
+      // into the previous one, which would need a third register buffer)
+      const int64_t ka = kb0 + (s0 + sj) * KS;
+      load(B, ka + KS);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(A, ka, sj);
+      __builtin_amdgcn_sched_barrier(0);
+      if (sj + 2 < SS) load(A, ka + 2 * KS);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(B, ka + KS, sj + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < TG; ++g) {
+    s1[g] += __shfl_xor(s1[g], 16);
+    s1[g] += __shfl_xor(s1[g], 32);
+    s2[g] += __shfl_xor(s2[g], 16);
+    s2[g] += __shfl_xor(s2[g], 32);
+    if (tok[g] < T) {
+      float* pc = part + chunk * NOr * T + tok[g];
+#pragma unroll
+      for (int ob = 0; ob < NOB; ++ob)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) pc[(int64_t)(ob * 16 + grp * 4 + v) * T] = acc[g][ob][v];
+      if (grp == 0) {
+        pc[(int64_t)(NOr - 2) * T] = s1[g];
+        pc[(int64_t)(NOr - 1) * T] = s2[g];
+      }
+    }
+  }
+}
+
+
 // output-block bound of a kernel instance: 1, 2, 3, 5 or 8
 static inline int nob_bucket(int nob) { return nob <= 3 ? nob : (nob <= 5 ? 5 : 8); }
 
@@ -155,16 +297,37 @@ static hipError_t proj_launch(const TS* X, int64_t T, int N, int C, int64_t K, c
   return hipGetLastError();
 }
 
-// bf16 state: token groups per the plan, the exact variant where the chunks
-// divide K (full state); an fp32 state takes one token group per wave (the
-// same chunks, more workgroups).
+
+template <bool GATHER>
+static hipError_t proj_wide_launch(const uint16_t* X, int64_t T, int N, int C, int64_t K, const ProjPlan& pl,
+                                   const uint4* w, int nob, const int32_t* idx, int k, float* part, hipStream_t s) {
+  // (the unguarded instance for chunks that divide K needs more registers
+  // than two waves per SIMD allow, so the guarded one serves both)
+  const dim3 grid((unsigned)((T + kWideTokens - 1) / kWideTokens), (unsigned)pl.nchunk);
+  const size_t lds = (size_t)wide_seg_steps(nob) * kWideStep * nob * 1024;
+#define XHC_WIDE_CASE(NB)                                                                                      \
+  case NB:                                                                                                     \
+    k_proj_wide<NB, false, GATHER><<<grid, dim3(256), lds, s>>>(X, T, N, C, K, pl.chunk_blocks, w, idx, k, part); \
+    break;
+  switch (nob) {
+    XHC_WIDE_CASE(1) XHC_WIDE_CASE(2) XHC_WIDE_CASE(3) XHC_WIDE_CASE(4)
+    XHC_WIDE_CASE(5) XHC_WIDE_CASE(6) XHC_WIDE_CASE(7) XHC_WIDE_CASE(8)
+    default: return hipErrorInvalidValue;
+  }
+#undef XHC_WIDE_CASE
+  return hipGetLastError();
+}
+
 template <typename TS, bool GATHER>
 static hipError_t proj_dispatch(const TS* X, int64_t T, int N, int C, int64_t K, const void* packed, int64_t nout,
                                 const int32_t* idx, int k, float* part, hipStream_t s) {
-  const ProjPlan pl = proj_plan(K, nout, T);
+  const ProjPlan pl = proj_plan(Vec8<TS>::kSplit ? XHC_F32 : XHC_BF16, GATHER, K, C, nout, T);
   const uint4* w = reinterpret_cast<const uint4*>(packed);
   const int nob = (int)out_blocks(nout);
   if (nob > 8) return hipErrorInvalidValue;
+  if constexpr (!Vec8<TS>::kSplit) {
+    if (pl.wide) return proj_wide_launch<GATHER>(X, T, N, C, K, pl, w, nob, idx, k, part, s);
+  }
   if (Vec8<TS>::kSplit) return proj_launch<TS, GATHER, false, 1>(X, T, N, C, K, pl, w, nob, idx, k, part, s);
   const bool exact = !GATHER && (K / 32) % pl.chunk_blocks == 0;
 #define XHC_PROJ_TG(TGV)                                                                            \
