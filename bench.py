@@ -39,6 +39,45 @@ from paper_2607_14530_amd import xhc as X  # noqa: E402
 
 HBM_PEAK_GBPS = 8000.0
 METRIC = "tokens/s and achieved HBM GB/s per xHC sublayer (fwd) at N=16,k=4,C=4096"
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_xhc_pre_T16384_N16_C4096.md")
+
+
+def sources_digest():
+    """sha256 over the kernel sources (name + bytes, sorted): a traffic figure
+    measured on other sources no longer describes the kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_14530_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per xhc_pre call from the committed rocprofv3 counter summary,
+    or None when it is missing or was taken on different kernel sources."""
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            kv = dict(line.split(":", 1) for line in f if line.startswith(("traffic_bytes_per_call:",
+                                                                             "sources_sha256:")))
+    except OSError:
+        return None
+    if kv.get("sources_sha256", "").strip() != sources_digest():
+        return None
+    return float(kv["traffic_bytes_per_call"])
+
+
+def calibrate_copy(gib=1):
+    """A plain device copy of known size, for scaling the HBM byte counters."""
+    n = gib << 29   # bf16 elements
+    src = torch.randn(n, device="cuda", dtype=torch.bfloat16)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 2 * n, "copy_bytes_written": 2 * n, "launches": 3}), flush=True)
 
 
 def cpu_baseline(seconds=15.0):
@@ -145,10 +184,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true", help="skip the Flash / mHC / backward sections")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a 1 GiB device copy (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build runs the connection on a single MI355X "
-              f"(--gpus {args.gpus} requested); see the sharding notes in DESIGN.md", file=sys.stderr)
+              f"(--gpus {args.gpus} requested)", file=sys.stderr)
         sys.exit(2)
 
     dev = torch.device("cuda:0")
@@ -218,8 +262,11 @@ def main():
         "paper_bytes_per_token_C": 73.5,
         "segments_ms": {"attn_pre": mean[0], "attn_post": mean[1], "mlp_pre": mean[2], "mlp_post": mean[3]},
         "wall_s": wall,
-        "roofline": {"kernel": "xhc_pre (entry point)", "bound": "hbm", "achieved": achieved,
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS, "traffic": None},
+        "roofline": {"kernel": "xhc_pre (entry point: projection, routing, gathered projection, coefficients, "
+                               "dense read), mean of the two sublayer kinds",
+                     "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(),
+                     "algorithmic_bytes_per_call": pre_bytes},
     }
     if not args.no_extra:
         del sub_a, sub_m, inp_a, inp_m, state

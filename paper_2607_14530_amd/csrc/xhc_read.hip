@@ -29,7 +29,7 @@ __global__ __launch_bounds__(256) void k_dense_read(const TS* __restrict__ X, in
     for (int e = 0; e < 8; ++e) acc[q][e] = 0.f;
   const TS* xt = X + t * (int64_t)N * C + c;
   // stream rows loaded before use, kept in the storage format until then
-  constexpr int UNR = (NMAP == 1 && !Vec8<TS>::kSplit) ? 16 : 8;
+  constexpr int UNR = 8;
   using R8 = Raw8<TS>;
   for (int i0 = 0; i0 < N; i0 += UNR) {
     typename R8::raw r[UNR];
