@@ -151,6 +151,101 @@ __device__ inline void sinkhorn_clamp_reverse(const float (&L)[kMaxK * kMaxK], i
     for (int l = 0; l < k; ++l) dL[j * kMaxK + l] = g[j * kMaxK + l] * M[j * kMaxK + l];
 }
 
+// The same for a compile-time k: the forward normaliser of every step is kept
+// (sk[step][j] at sk[(step * K + j) * stride], LDS), so the reverse walks back
+// step by step, undoing each normalisation on the iterate instead of
+// recomputing it from the start.
+constexpr int kSkMaxSteps = 64;   // 2 x sinkhorn_iters handled by the fast reverse
+template <int K>
+__device__ inline void sinkhorn_clamp_reverse_fast(const float (&L)[K * K], int iters, float delta,
+                                                   const float (&dH)[K * K], float (&dL)[K * K], float* sk,
+                                                   int stride) {
+  float E[K * K], M[K * K], g[K * K];
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    float mx = L[j * K];
+#pragma unroll
+    for (int l = 1; l < K; ++l) mx = fmaxf(mx, L[j * K + l]);
+#pragma unroll
+    for (int l = 0; l < K; ++l) M[j * K + l] = E[j * K + l] = __expf(L[j * K + l] - mx);
+  }
+  const int steps = 2 * iters;
+  for (int st = 0; st < steps; ++st) {
+    if ((st & 1) == 0) {
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        float sum = 0.f;
+#pragma unroll
+        for (int l = 0; l < K; ++l) sum += M[j * K + l];
+        sk[(st * K + j) * stride] = sum;
+        const float r = 1.0f / sum;
+#pragma unroll
+        for (int l = 0; l < K; ++l) M[j * K + l] *= r;
+      }
+    } else {
+#pragma unroll
+      for (int l = 0; l < K; ++l) {
+        float sum = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) sum += M[j * K + l];
+        sk[(st * K + l) * stride] = sum;
+        const float r = 1.0f / sum;
+#pragma unroll
+        for (int j = 0; j < K; ++j) M[j * K + l] *= r;
+      }
+    }
+  }
+  // row clamp
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    float sum = 0.f;
+#pragma unroll
+    for (int l = 0; l < K; ++l) sum += M[j * K + l];
+    if (sum > 1.0f + delta) {
+      float dot = 0.f;
+#pragma unroll
+      for (int l = 0; l < K; ++l) dot += dH[j * K + l] * (M[j * K + l] / sum);
+#pragma unroll
+      for (int l = 0; l < K; ++l) g[j * K + l] = (dH[j * K + l] - dot) / sum;
+    } else {
+#pragma unroll
+      for (int l = 0; l < K; ++l) g[j * K + l] = dH[j * K + l];
+    }
+  }
+  // M holds the output of step st; its input is M times the step's normaliser
+  for (int st = steps - 1; st >= 0; --st) {
+    if ((st & 1) == 0) {
+#pragma unroll
+      for (int j = 0; j < K; ++j) {
+        const float sum = sk[(st * K + j) * stride];
+        float dot = 0.f;
+#pragma unroll
+        for (int l = 0; l < K; ++l) dot += g[j * K + l] * M[j * K + l];
+#pragma unroll
+        for (int l = 0; l < K; ++l) {
+          g[j * K + l] = (g[j * K + l] - dot) / sum;
+          M[j * K + l] *= sum;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int l = 0; l < K; ++l) {
+        const float sum = sk[(st * K + l) * stride];
+        float dot = 0.f;
+#pragma unroll
+        for (int j = 0; j < K; ++j) dot += g[j * K + l] * M[j * K + l];
+#pragma unroll
+        for (int j = 0; j < K; ++j) {
+          g[j * K + l] = (g[j * K + l] - dot) / sum;
+          M[j * K + l] *= sum;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < K * K; ++i) dL[i] = g[i] * E[i];
+}
+
 // ------------------------------------------------------------ post backward
 
 // Layout of the per-token dot products (compile-time strides, KM >= k):
@@ -524,13 +619,19 @@ __global__ __launch_bounds__(256) void k_bwd_dhpre(const TS* __restrict__ X, con
 __host__ __device__ inline int tok_floats(int N, int NA) { return 2 * N + NA + 8; }
 __host__ __device__ inline int pg_floats(int N, int k, int Kr) { return 3 + N + k * k + k * Kr; }
 
-__global__ __launch_bounds__(128) void k_bwd_pre_token(
-    const float* __restrict__ part, int64_t nchunk, int64_t T, int N, int m, int k, int Kr, int C,
+// KC > 0: k == KC at compile time, Sinkhorn reversed with kept normalisers;
+// KC == 0: any k, Sinkhorn reversed by recomputing the forward iterates.
+constexpr int kPreTokThreads = 64;
+template <int KC>
+__global__ __launch_bounds__(kPreTokThreads) void k_bwd_pre_token(
+    const float* __restrict__ part, int64_t nchunk, int64_t T, int N, int m, int k_rt, int Kr, int C,
     const float* __restrict__ saved, const float* __restrict__ colsum, const float* __restrict__ alpha,
     const float* __restrict__ b_res, const int32_t* __restrict__ idx, const float* __restrict__ p,
     const float* __restrict__ Hpre, const float* __restrict__ Hpost, const float* __restrict__ dHres,
     const float* __restrict__ dHpost, const float* __restrict__ dp, float eps, int iters, float delta,
     float* __restrict__ tok, float* __restrict__ pg) {
+  __shared__ float sk[KC > 0 ? kSkMaxSteps * KC * kPreTokThreads : 1];
+  const int k = KC > 0 ? KC : k_rt;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
   const int NA = k * Kr + k * k, ns = saved_floats(N, k, Kr);
@@ -581,20 +682,34 @@ __global__ __launch_bounds__(128) void k_bwd_pre_token(
     ba += a_post * du * z;
   }
   // residual map: H = clamp(SK(exp(a z + b)))
-  float L[kMaxK * kMaxK], dH[kMaxK * kMaxK], dL[kMaxK * kMaxK];
-  for (int j = 0; j < kMaxK; ++j)
-    for (int l = 0; l < kMaxK; ++l) {
-      const bool in = j < k && l < k;
-      L[j * kMaxK + l] = in ? a_res * sv[2 * N + k * Kr + j * k + l] + b_res[j * k + l] : 0.f;
-      dH[j * kMaxK + l] = in ? dHres[(t * k + j) * k + l] : 0.f;
-      dL[j * kMaxK + l] = 0.f;
-    }
-  sinkhorn_clamp_reverse(L, k, iters, delta, dH, dL);
+  constexpr int KS = KC > 0 ? KC : kMaxK;   // row stride of the matrices below
+  float dL[KS * KS];
+  if constexpr (KC > 0) {
+    float L[KC * KC], dH[KC * KC];
+#pragma unroll
+    for (int j = 0; j < KC; ++j)
+#pragma unroll
+      for (int l = 0; l < KC; ++l) {
+        L[j * KC + l] = a_res * sv[2 * N + KC * Kr + j * KC + l] + b_res[j * KC + l];
+        dH[j * KC + l] = dHres[(t * KC + j) * KC + l];
+      }
+    sinkhorn_clamp_reverse_fast<KC>(L, iters, delta, dH, dL, &sk[threadIdx.x], kPreTokThreads);
+  } else {
+    float L[kMaxK * kMaxK], dH[kMaxK * kMaxK];
+    for (int j = 0; j < kMaxK; ++j)
+      for (int l = 0; l < kMaxK; ++l) {
+        const bool in = j < k && l < k;
+        L[j * kMaxK + l] = in ? a_res * sv[2 * N + k * Kr + j * k + l] + b_res[j * k + l] : 0.f;
+        dH[j * kMaxK + l] = in ? dHres[(t * k + j) * k + l] : 0.f;
+        dL[j * kMaxK + l] = 0.f;
+      }
+    sinkhorn_clamp_reverse(L, k, iters, delta, dH, dL);
+  }
   float da_res = 0.f;
   for (int j = 0; j < k; ++j)
     for (int l = 0; l < k; ++l) {
       const float z = sv[2 * N + k * Kr + j * k + l];
-      const float d = dL[j * kMaxK + l];
+      const float d = dL[j * KS + l];
       tk[2 * N + k * Kr + j * k + l] = a_res * d;
       da_res += d * z;
       g[3 + N + j * k + l] = d;
@@ -764,6 +879,258 @@ __global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, 
   for (int o = 0; o < NAMAX; ++o) dst[o] = ga[o];
 }
 
+// MFMA form of the two row passes above for a bf16 state, N = 16 (full rows)
+// and k * Kr + k * k <= 32 (active rows).  A workgroup takes 64 consecutive
+// weight rows K (wave w: rows 16w .. 16w + 15, inside one stream / slot) and a
+// chunk of tokens, in steps of 32 tokens staged in LDS:
+//   dX[t, K] += sum_o W[K, o] dz'[t, o] + (row terms)   MFMA D[16 K x 16 t], contraction over the 32 outputs
+//   dW[K, o] += sum_t x[t, K] dz'[t, o]                 MFMA D[16 o x 16 K], contraction over 32 tokens
+// with dz' the per-token scaled logit gradients (full: r_ln dz_r | r dz_pre;
+// active: r_a dz_act), entered as a bf16 pair hi + lo (2^-16 relative).  The
+// full-row dW_r misses the token sum of mu dz'_r, which the reduction removes.
+constexpr int kMfRows = 64;    // weight rows per workgroup
+constexpr int kMfStep = 32;    // tokens per step
+constexpr int kMfXPitch = kMfRows + 8;   // bf16 per staged token row (pad: fewer LDS bank conflicts)
+
+__device__ __forceinline__ void split_bf16x8(const float (&f)[8], uint4& hi, uint4& lo) {
+  float h[8], l[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    h[e] = __uint_as_float(f2bf(f[e]) << 16);
+    l[e] = f[e] - h[e];
+  }
+  hi = pack8(h);
+  lo = pack8(l);
+}
+
+template <bool ACT>
+__global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restrict__ X,
+                                                       const uint16_t* __restrict__ din, uint16_t* __restrict__ dX,
+                                                       const float* __restrict__ Wa, const float* __restrict__ Wb,
+                                                       const float* __restrict__ Hpre,
+                                                       const int32_t* __restrict__ idx, const float* __restrict__ tok,
+                                                       int64_t T, int N, int k, int C, int Kr, int NA,
+                                                       int64_t tchunk, float* __restrict__ wpa,
+                                                       float* __restrict__ wpb) {
+  __shared__ __align__(16) uint16_t xs[kMfStep][kMfXPitch];
+  __shared__ float dzs[kMfStep][33];
+  __shared__ float sc[kMfStep][8];
+  __shared__ int srow[kMfStep];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int l16 = lane % 16, g4 = lane / 16;
+  const int64_t K0 = (int64_t)blockIdx.x * kMfRows;           // first weight row of the workgroup
+  const int part = (int)(K0 / C);                              // stream (full) or slot (active)
+  const int c0 = (int)(K0 % C);
+  const int64_t NK = ACT ? (int64_t)k * C : (int64_t)N * C;   // weight rows
+  const int NP = k * Kr;                                       // active: W_post columns
+  const int TF = tok_floats(N, NA);
+  // A operand of the dX product: rows K0 + 16 wave + l16, outputs 8 g4 .. + 7, as bf16
+  uint4 wfrag;
+  {
+    float f[8];
+    const int64_t K = K0 + 16 * wave + l16;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int o = 8 * g4 + e;
+      float v = 0.f;
+      if (ACT) {
+        if (o < NP) v = Wa[K * NP + o];
+        else if (o < NA) v = Wb[K * (k * k) + (o - NP)];
+      } else {
+        v = o < 16 ? Wa[K * 16 + o] : Wb[K * 16 + (o - 16)];
+      }
+      f[e] = __uint_as_float(f2bf(v) << 16);
+    }
+    wfrag = pack8(f);
+  }
+  f32x4 dw[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
+  // The inputs of step tb + 32 are fetched into registers while step tb is
+  // computed: this thread's dz' values (4), scalars (threads < 32) and 16
+  // bytes of the state rows.
+  struct Stage {
+    float dz[kMfStep * 32 / 256];
+    float scal[7];
+    int row;
+    uint4 x;
+  };
+  auto fetch = [&](Stage& st, int64_t tb) {
+    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
+#pragma unroll
+    for (int r = 0; r < kMfStep * 32 / 256; ++r) {
+      const int q = threadIdx.x + r * 256, u = q / 32, o = q % 32;
+      const int64_t t = tb + (u < nt ? u : 0);
+      const float* tk = tok + t * TF;
+      float v = 0.f;
+      if (u < nt) {
+        if (ACT) v = o < NA ? tk[2 * N + NA + 6] * tk[2 * N + o] : 0.f;                 // r_a dz_act
+        else v = o < 16 ? tk[2 * N + NA + 1] * tk[o] : tk[2 * N + NA + 0] * tk[N + (o - 16)];  // r_ln dz_r | r dz_pre
+      }
+      st.dz[r] = v;
+    }
+    if (threadIdx.x < kMfStep) {
+      const int u = threadIdx.x;
+      const int64_t t = tb + (u < nt ? u : 0);
+      const float* tk = tok + t * TF;
+      st.row = ACT ? idx[t * k + part] : part;
+      if (ACT) {
+        st.scal[0] = tk[2 * N + NA + 7];   // beta_a
+      } else {
+#pragma unroll
+        for (int i = 0; i < 6; ++i) st.scal[i] = tk[2 * N + NA + i];   // r, r_ln, mu, beta_pre, m1, m2
+        st.scal[6] = Hpre[t * N + part];
+      }
+    }
+    // the state rows need the row index: the slot's row of each token (active)
+    // is read here directly
+    {
+      const int u = threadIdx.x / 8, piece = threadIdx.x % 8;
+      st.x = make_uint4(0, 0, 0, 0);
+      if (u < nt) {
+        const int64_t t = tb + u;
+        const int row = ACT ? idx[t * k + part] : part;
+        st.x = *reinterpret_cast<const uint4*>(X + (t * N + row) * (int64_t)C + c0 + piece * 8);
+      }
+    }
+  };
+  Stage cur;
+  if (t0 < t1) fetch(cur, t0);
+  for (int64_t tb = t0; tb < t1; tb += kMfStep) {
+    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
+    __syncthreads();   // the previous step's LDS reads are done
+#pragma unroll
+    for (int r = 0; r < kMfStep * 32 / 256; ++r) {
+      const int q = threadIdx.x + r * 256;
+      dzs[q / 32][q % 32] = cur.dz[r];
+    }
+    if (threadIdx.x < kMfStep) {
+      srow[threadIdx.x] = cur.row;
+#pragma unroll
+      for (int i = 0; i < 7; ++i) sc[threadIdx.x][i] = cur.scal[i];
+    }
+    *reinterpret_cast<uint4*>(&xs[threadIdx.x / 8][(threadIdx.x % 8) * 8]) = cur.x;
+    __syncthreads();
+    if (tb + kMfStep < t1) fetch(cur, tb + kMfStep);
+    // ---- dX: two token halves; the accumulator rows are read before the products
+    uint2 dxv[2], dinv[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int u = 16 * h + l16;
+      const int kr = 16 * wave + 4 * g4;
+      dxv[h] = make_uint2(0, 0);
+      dinv[h] = make_uint2(0, 0);
+      if (u < nt) {
+        const int64_t t = tb + u;
+        dxv[h] = *reinterpret_cast<const uint2*>(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr);
+        if (!ACT) dinv[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int u = 16 * h + l16;   // B operand token of this lane
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = dzs[u][8 * g4 + e];
+      uint4 bh, bl;
+      split_bf16x8(f, bh, bl);
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+      acc = mfma_16x16x32(wfrag, bh, acc);
+      acc = mfma_16x16x32(wfrag, bl, acc);
+      // lane holds rows 16 wave + 4 g4 + v of token u
+      if (u < nt) {
+        const int64_t t = tb + u;
+        const int kr = 16 * wave + 4 * g4;   // row offset inside the 64
+        const uint2 xv = *reinterpret_cast<const uint2*>(&xs[u][kr]);
+        const float x[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
+        float gsum[4];
+        if (ACT) {
+          const float beta_a = sc[u][0];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) gsum[v] = acc[v] - beta_a * x[v];
+        } else {
+          const float r_ln = sc[u][1], mu = sc[u][2], bpre = sc[u][3], m1 = sc[u][4], m2 = sc[u][5], hp = sc[u][6];
+          const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
+#pragma unroll
+          for (int v = 0; v < 4; ++v)
+            gsum[v] = hp * gi[v] + acc[v] - bpre * x[v] - r_ln * m1 - r_ln * r_ln * (x[v] - mu) * m2;
+        }
+        const float d[4] = {bf_lo(dxv[h].x) + gsum[0], bf_hi(dxv[h].x) + gsum[1], bf_lo(dxv[h].y) + gsum[2],
+                            bf_hi(dxv[h].y) + gsum[3]};
+        *reinterpret_cast<uint2*>(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr) =
+            make_uint2(pack2bf(d[0], d[1]), pack2bf(d[2], d[3]));
+      }
+    }
+    // ---- dW: contraction over the 32 staged tokens (rows past nt are zero)
+    {
+      uint16_t xb[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xb[e] = xs[8 * g4 + e][16 * wave + l16];
+      const uint4 bx = make_uint4(xb[0] | ((uint32_t)xb[1] << 16), xb[2] | ((uint32_t)xb[3] << 16),
+                                  xb[4] | ((uint32_t)xb[5] << 16), xb[6] | ((uint32_t)xb[7] << 16));
+#pragma unroll
+      for (int oh = 0; oh < 2; ++oh) {
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = dzs[8 * g4 + e][16 * oh + l16];
+        uint4 ah, al;
+        split_bf16x8(f, ah, al);
+        dw[oh] = mfma_16x16x32(ah, bx, dw[oh]);
+        dw[oh] = mfma_16x16x32(al, bx, dw[oh]);
+      }
+    }
+  }
+  // lane holds dW[row K0 + 16 wave + l16][output 16 oh + 4 g4 + v]
+  const int64_t K = K0 + 16 * wave + l16;
+  if (ACT) {
+    float* dst = wpa + ((int64_t)blockIdx.y * NK + K) * 32;
+#pragma unroll
+    for (int oh = 0; oh < 2; ++oh)
+      *reinterpret_cast<float4*>(dst + 16 * oh + 4 * g4) = make_float4(dw[oh][0], dw[oh][1], dw[oh][2], dw[oh][3]);
+  } else {
+    float* dr = wpa + ((int64_t)blockIdx.y * NK + K) * 16 + 4 * g4;
+    float* dp = wpb + ((int64_t)blockIdx.y * NK + K) * 16 + 4 * g4;
+    *reinterpret_cast<float4*>(dr) = make_float4(dw[0][0], dw[0][1], dw[0][2], dw[0][3]);
+    *reinterpret_cast<float4*>(dp) = make_float4(dw[1][0], dw[1][1], dw[1][2], dw[1][3]);
+  }
+}
+
+// corr[o] = sum_t mu_t r_ln,t dz_r[t, o] (the part of dW_r the MFMA full-row
+// pass leaves out), one workgroup per output, fixed order
+__global__ __launch_bounds__(256) void k_mu_dz_sum(const float* __restrict__ tok, int64_t T, int N, int NA,
+                                                   float* __restrict__ corr) {
+  __shared__ float red[256];
+  const int o = blockIdx.x, TF = tok_floats(N, NA);
+  float s = 0.f;
+  for (int64_t t = threadIdx.x; t < T; t += 256) {
+    const float* tk = tok + t * TF;
+    s += tk[2 * N + NA + 2] * tk[2 * N + NA + 1] * tk[o];
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) corr[o] = red[0];
+}
+
+// out[col] = sum over rows of in[row][col] - corr[col % ncorr] (corr may be null)
+__global__ __launch_bounds__(256) void k_colsum_rows_corr(const float* __restrict__ in, int64_t nrows, int64_t ncols,
+                                                          const float* __restrict__ corr, int ncorr,
+                                                          float* __restrict__ out) {
+  const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (col >= ncols) return;
+  float s = 0.f;
+  for (int64_t r0 = 0; r0 < nrows; r0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = (r0 + u < nrows) ? in[(r0 + u) * ncols + col] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  out[col] = corr ? s - corr[col % ncorr] : s;
+}
+
 // ------------------------------------------------------------ launchers
 
 #define XHC_TS_DISPATCH(dt, ...) \
@@ -847,6 +1214,7 @@ size_t bwd_pre_ws_bytes(const xhc_dims* d) {
   n += (size_t)nchunk * N * C * N * 2;                           // dW_r, dW_pre partials
   n += (size_t)nchunk * k * C * 32;                              // dW_act partials (<= 32 columns)
   n += (size_t)k * C * 32 + (size_t)pg_floats(N, k, Kr);          // reduced dW_act, reduced gradients
+  n += (size_t)N;                                                // token sum of mu dz'_r
   return n * sizeof(float) + 1024;
 }
 
@@ -878,33 +1246,56 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
   XHC_TS_DISPATCH(d->state_dtype,
     k_bwd_dhpre<TS><<<dim3((unsigned)(T * ncb)), dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),
         reinterpret_cast<const TS*>(d_input), T, N, C, part));
-  k_bwd_pre_token<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
-      part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p, Hpre, Hpost, dHres, dHpost, dp, d->eps,
-      d->sinkhorn_iters, d->clamp_delta, tok, pg);
+  {
+    const dim3 gt((unsigned)((T + kPreTokThreads - 1) / kPreTokThreads)), bt(kPreTokThreads);
+    if (k == 4 && 2 * d->sinkhorn_iters <= kSkMaxSteps)
+      k_bwd_pre_token<4><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
+                                          Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
+                                          d->clamp_delta, tok, pg);
+    else
+      k_bwd_pre_token<0><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
+                                          Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
+                                          d->clamp_delta, tok, pg);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  const bool mf = d->state_dtype == XHC_BF16 && N == 16 && NA <= 32 && C % kMfRows == 0;
+  if (mf) {
+    const dim3 gf((unsigned)((int64_t)N * C / kMfRows), (unsigned)nchunk);
+    k_bwd_rows_mfma<false><<<gf, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
+        reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hpre, idx, tok, T,
+        N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
+    const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
+    k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
+        reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T,
+        N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
+    k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
+  }
   const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
 #define XHC_FULL_ROWS(NNV)                                                                                       \
   XHC_TS_DISPATCH(d->state_dtype,                                                                                \
     k_bwd_full_rows<TS, NNV><<<gfull, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),                        \
         reinterpret_cast<const TS*>(d_input), reinterpret_cast<TS*>(dX), W_r, W_pre, Hpre, tok, T, C, NA,        \
         kRowChunk, wpart_r, wpart_p))
-  switch (N) {
-    case 4: XHC_FULL_ROWS(4); break;
-    case 8: XHC_FULL_ROWS(8); break;
-    case 16: XHC_FULL_ROWS(16); break;
-    default: XHC_FULL_ROWS(32); break;
+  if (!mf) {
+    switch (N) {
+      case 4: XHC_FULL_ROWS(4); break;
+      case 8: XHC_FULL_ROWS(8); break;
+      case 16: XHC_FULL_ROWS(16); break;
+      default: XHC_FULL_ROWS(32); break;
+    }
+    const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
+    XHC_TS_DISPATCH(d->state_dtype,
+      k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
+          W_post, W_res, idx, tok, T, N, k, C, Kr, kRowChunk, wpart_a));
   }
 #undef XHC_FULL_ROWS
-  const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
-  XHC_TS_DISPATCH(d->state_dtype,
-    k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
-        W_post, W_res, idx, tok, T, N, k, C, Kr, kRowChunk, wpart_a));
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // token reductions (fixed order)
   const int64_t nfull = (int64_t)N * C * N;
-  k_colsum_rows<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(wpart_r, nchunk, nfull, dW_r);
+  k_colsum_rows_corr<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(
+      wpart_r, nchunk, nfull, mf ? pgsum + pg_floats(N, k, Kr) : nullptr, N, dW_r);
   k_colsum_rows<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(wpart_p, nchunk, nfull, dW_pre);
   // active partials are [chunk][kC][32]: split columns into W_post and W_res
   const int64_t nact = (int64_t)k * C * 32;
