@@ -262,8 +262,9 @@ def main():
         "paper_bytes_per_token_C": 73.5,
         "segments_ms": {"attn_pre": mean[0], "attn_post": mean[1], "mlp_pre": mean[2], "mlp_post": mean[3]},
         "wall_s": wall,
-        "roofline": {"kernel": "xhc_pre (entry point: projection, routing, gathered projection, coefficients, "
-                               "dense read), mean of the two sublayer kinds",
+        "roofline": {"kernel": "xhc_pre entry point (single-pass cooperative kernel k_pre_fused: projection, "
+                               "routing, dense read, gathered projection; then the per-token coefficient pass), "
+                               "mean of the two sublayer kinds",
                      "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": measured_traffic(),
                      "algorithmic_bytes_per_call": pre_bytes},

@@ -74,11 +74,14 @@ typedef struct xhc_dims {
   int32_t impl;           /* xhc_impl: which kernels run (same results)          */
 } xhc_dims;
 
-/* Kernel selection for xhc_pre.  AUTO takes the faster implementation for
- * the device (currently the multi-kernel path).  MULTI forces the
- * multi-kernel path.  FUSED forces the single-pass cooperative kernel (bf16
- * state, N = 16, k = 4, C % 128 == 0, saved == NULL) and returns
- * XHC_EUNSUPPORTED elsewhere.  All give the same results within rounding. */
+/* Kernel selection for xhc_pre.  AUTO takes the single-pass cooperative
+ * kernel where it applies (bf16 state, N = 16, k = 4, C = 128 G with G
+ * dividing 32) and the multi-kernel path elsewhere, or when the device cannot
+ * hold the single-pass grid.  MULTI forces the multi-kernel path.  FUSED
+ * forces the single-pass kernel and returns XHC_EUNSUPPORTED where it does
+ * not apply.  All give the same results within rounding.  If a wait of the
+ * single-pass kernel ever gives up (bounded spin), H^post and H^res come out
+ * as NaN rather than as silently wrong values.                              */
 typedef enum { XHC_IMPL_AUTO = 0, XHC_IMPL_MULTI = 1, XHC_IMPL_FUSED = 2 } xhc_impl;
 
 /* Name of a status code, and the name of the HIP error behind the last

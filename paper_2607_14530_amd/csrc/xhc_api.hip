@@ -221,10 +221,9 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
     return XHC_EUNSUPPORTED;
   if (d->impl == XHC_IMPL_FUSED && !fused_pre_supported(d)) return XHC_EUNSUPPORTED;
   if (workspace_bytes < pre_ws(d)) return XHC_EWORKSPACE;
-  if (d->impl == XHC_IMPL_FUSED && saved) return XHC_EUNSUPPORTED;
-  // AUTO takes the multi-kernel path: the single-pass kernel is correct but
-  // slower on this device (its per-tile team synchronisation is latency-bound).
-  if (d->impl == XHC_IMPL_AUTO) {
+  // AUTO takes the single-pass kernel where it applies (it reads X once) and
+  // the multi-kernel path elsewhere
+  if (d->impl == XHC_IMPL_AUTO && !fused_pre_supported(d)) {
     xhc_dims m = *d;
     m.impl = XHC_IMPL_MULTI;
     return xhc_pre(&m, X, packed_full, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre, Hres, Hpost,
@@ -244,7 +243,7 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   hipError_t e = hipSuccess;
   if (d->impl != XHC_IMPL_MULTI) {
     e = launch_pre_fused(d, X, packed_full, colsum, packed_act, alpha, b_pre, b_res, b_post, input, idx, p, Hpre,
-                         Hres, Hpost, workspace, s);
+                         Hres, Hpost, saved, workspace, s);
     if (e == hipSuccess) return XHC_OK;
     if (d->impl == XHC_IMPL_FUSED || e != hipErrorInvalidConfiguration) {
       g_failed_step = "pre_fused";

@@ -81,7 +81,7 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
                            float* Hpost, float* Hres, float* sums, float* saved, int nsave, int save_z_at,
-                           int save_stats_at, hipStream_t s);
+                           int save_stats_at, hipStream_t s, const int* err = nullptr);
 // out0 gets map 0 (full dense read); maps 1..nmap-1 leave out the active
 // streams and go to outr + (q - 1) * T * C.
 hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
@@ -93,7 +93,7 @@ size_t fused_pre_ws_bytes(const xhc_dims* d);
 hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed_full, const float* colsum,
                             const void* packed_act, const float* alpha, const float* b_pre, const float* b_res,
                             const float* b_post, void* input, int32_t* idx, float* p, float* Hpre, float* Hres,
-                            float* Hpost, void* ws, hipStream_t s);
+                            float* Hpost, float* saved, void* ws, hipStream_t s);
 
 // ---- post
 __host__ __device__ inline int64_t post_chunks(int C) { return ((int64_t)C / 8 + 255) / 256; }

@@ -141,9 +141,18 @@ __global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ sums
                                                   const float* __restrict__ b_res, float eps, int iters,
                                                   float delta, float* __restrict__ Hpost,
                                                   float* __restrict__ Hres, float* __restrict__ saved, int nsave,
-                                                  int save_z_at, int save_stats_at) {
+                                                  int save_z_at, int save_stats_at,
+                                                  const int* __restrict__ err) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
+  if (err && *err != 0) {
+    // the single-pass kernel gave up a wait: its partials are not valid
+    const float nan = __uint_as_float(0x7fc00000u);
+    for (int o = 0; o < k * Kq; ++o) Hpost[t * k * Kq + o] = nan;
+    if (with_res)
+      for (int o = 0; o < k * k; ++o) Hres[t * k * k + o] = nan;
+    return;
+  }
   const float nu_a = sums[(int64_t)(NO - 1) * T + t] / (float)kC;
   const float rstd = 1.0f / sqrtf(nu_a + eps);
   if (saved) {
@@ -192,14 +201,14 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
                            float* Hpost, float* Hres, float* sums, float* saved, int nsave, int save_z_at,
-                           int save_stats_at, hipStream_t s) {
+                           int save_stats_at, hipStream_t s, const int* err) {
   if (T == 0) return hipSuccess;
   const int NO = (int)out_blocks(nout) * 16 + 2;
   hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
   if (e != hipSuccess) return e;
   k_pre_coef<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
       sums, NO, T, k, Kq, with_res, (int64_t)k * C, alpha_post, alpha_res, b_post, b_res, eps, iters, delta,
-      Hpost, Hres, saved, nsave, save_z_at, save_stats_at);
+      Hpost, Hres, saved, nsave, save_z_at, save_stats_at, err);
   return hipGetLastError();
 }
 

@@ -1,29 +1,35 @@
 // Single-pass mapping generation + dense read of a full xHC sublayer
-// (bf16 state, N = 16, k = 4, K_r <= 4, C = 128 G with G <= 32).
+// (bf16 state, N = 16, k = 4, K_r <= 4, C = 128 G with G dividing 32).
 //
 // The state X is read from HBM exactly once.  A 16-token tile of X
 // ([16 tokens, 16 streams, C] = 2 MiB at C = 4096) is split over a team of G
-// workgroups; member s copies its [16, 16, 128] slice straight into LDS
-// (double-buffered) and keeps the matching slices of the projection weights in
-// registers for the whole kernel.  Per tile:
+// workgroups; member s takes the 128-channel slice s of every (token, stream)
+// row and keeps the matching slices of the projection weights in registers
+// for the whole kernel.  Wave w of a member holds channels 16 w .. 16 w + 15
+// of all 16 streams of the tile (4 KiB, 32 registers per lane), so the dense
+// read of a channel is a sum inside one lane pair.  Per tile q:
 //
 //  A. every member: MFMA partial of x [W^r, W^pre] over its slice and the
 //     partial moments (eq:fused_normalized_projection), published as tagged
 //     64-bit records (value, tile tag): a record is valid once its tag matches,
 //     so no counter, fence or flag orders the stores;
-//  B. per token two members sum the G partials in member order
-//     (deterministic): one the router outputs and moments, giving the
+//  B. one iteration later, per token two members sum the G partials in member
+//     order (deterministic): one the router outputs and moments, giving the
 //     LayerNorm-corrected logits and the routing (eq:router_topk), the other
-//     the pre-map outputs, giving H^pre (RMSNorm correction); they write them
-//     out and publish idx and H^pre as tagged records;
-//  C. every member collects H^pre and idx of the 16 tokens;
-//  D. the dense read input = sum_i H^pre_i x_i of its slice from LDS
-//     (eq:dense_read);
-//  E. the MFMA partial of the gathered active rows [W^post, W^res] and of
-//     sum a^2 over its slice, written to the workspace; a per-token pass after
-//     the kernel sums the G partials and forms H^post and H^res.
+//     the pre-map outputs, giving H^pre (RMSNorm correction); both publish
+//     their results as records;
+//  C. two iterations later every member collects H^pre and idx of the tile,
+//     then forms the dense read input = sum_i H^pre_i x_i of its slice
+//     (eq:dense_read) and the MFMA partial of the gathered active rows
+//     [W^post, W^res] with sum a^2; a per-token pass after the kernel sums the
+//     G partials and forms H^post and H^res.
 //
-// The copy of tile q + 1 is in flight while tile q is synchronised.  The
+// So every wait on another member has a full iteration of slack, and each
+// member keeps three tiles in registers (q, q - 1, q - 2).  A tile reaches the
+// registers through one LDS buffer: waves 0-3 copy it there with direct
+// global->LDS loads, issued as soon as the previous tile has left the buffer.
+// Waves 4-7 do all waiting on records: a wave that waits on a load also waits
+// on every earlier load of its own, so the copy waves must not poll.  The
 // kernel is launched cooperatively, so every member of a team is resident;
 // every wait is bounded, so every wave exits.
 #include "xhc_device.h"
@@ -38,24 +44,26 @@ constexpr int FM = 16;                        // tokens per tile (MFMA columns)
 constexpr int FCS = 128;                      // channels per member slice
 constexpr int FNT = 512;                      // threads per workgroup
 constexpr int FNW = FNT / kWave;              // 8 waves
+constexpr int NCOPY = 4;                      // waves 0..3 issue the tile copies
+constexpr int NPOLL = FNW - NCOPY;            // waves 4..7 wait on records
 constexpr int ROWB = FCS * 2;                 // bytes of one (token, stream) row slice
-constexpr int TOKP = FN * ROWB + 16;          // token pitch in LDS (16 B pad: conflict-free MFMA reads)
-constexpr int BUFB = FM * TOKP;               // one tile buffer
-constexpr int NBUF = 2;
-constexpr int KB1 = FN * FCS / 32;            // 64 k-blocks of the full projection per slice
-constexpr int KB1W = KB1 / FNW;               // 8 per wave
+constexpr int TOKP = FN * ROWB + 16;          // token pitch in LDS (16 B pad)
+constexpr int BUFB = FM * TOKP;               // the tile buffer
+constexpr int KB1W = FN / 2;                  // k-blocks per wave, full projection (stream pairs)
+constexpr int KBAW = FK / 2;                  // k-blocks per wave, active projection (slot pairs)
 constexpr int NOB1 = 2;                       // 2N = 32 outputs
-constexpr int KBA = FK * FCS / 32;            // 16 k-blocks of the active projection per slice
-constexpr int KBAW = KBA / FNW;               // 2 per wave
 constexpr int NOBA = 2;                       // k*Kr + k*k <= 32 outputs
 constexpr int NV1 = 34;                       // 32 outputs + sum x + sum x^2
 constexpr int NV2 = FN + FK;                  // broadcast per token: H^pre, idx
-constexpr int RING = 4;                       // record slots per team
+constexpr int RING = 8;                       // record slots per team
 constexpr int kMaxG = 32;
+constexpr int NJV = FN + 2;                   // values per reducer job and member (at most)
+constexpr int BREC = (2 * FM * NJV + NPOLL * kWave - 1) / (NPOLL * kWave);   // reducer records per polling lane
+constexpr int CREC = (FM * NV2 + NPOLL * kWave - 1) / (NPOLL * kWave);       // H^pre / idx records per polling lane
 constexpr unsigned kSpinLimit = 1u << 16;     // polls of one record before the wait gives up
 
-static_assert(KB1 % FNW == 0 && KBA % FNW == 0, "k-blocks must split evenly over waves");
-static_assert(FM * FN * ROWB / 1024 % FNW == 0, "tile copies must split evenly over waves");
+static_assert(FM * FN / 4 % NCOPY == 0, "tile copies must split evenly over the copy waves");
+static_assert(FCS == 16 * FNW, "a wave holds 16 channels of the slice");
 
 struct FusedArgs {
   const uint16_t* X;
@@ -68,6 +76,8 @@ struct FusedArgs {
   int32_t* idx;
   float* p;
   float* Hpre;
+  float* saved;           // per-token values for the backward (or null), nsave floats per token
+  int nsave;
   uint64_t* rec1;         // [teams][RING][G][FM][NV1]
   uint64_t* rec2;         // [teams][RING][FM][NV2]
   int* err;
@@ -81,54 +91,45 @@ struct FusedArgs {
 };
 
 struct Smem {
-  float red[FNW][NV1][FM];       // per-wave partials for the cross-wave sum
-  float vals[kMaxG][NV1];        // a token's member partials (reducer)
-  float hp[FM][FN];              // H^pre of the tile
-  int id[FM][FK];                // idx of the tile
+  float red[FNW][NV1][FM];            // per-wave projection partials (A)
+  float red2[FNW][NV1][FM];           // per-wave active partials
+  float vals[2 * FM][NJV];            // reducer partials: [job jj * G + member g][value]
+  float hpid[FM][NV2];                // H^pre and idx (as bits) of the tile being read, record layout
+  int poff[BREC][NPOLL * kWave];      // reducer record r of polling lane pl: offset in the slot, -1 unused
 };
-
-__device__ __forceinline__ uint4 lds_read16(const unsigned char* p) { return *reinterpret_cast<const uint4*>(p); }
 
 __device__ __forceinline__ void st_rec(uint64_t* p, float v, uint32_t tag) {
   __hip_atomic_store(p, ((uint64_t)tag << 32) | __float_as_uint(v), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// Bounded wait until the record carries `tag`; returns its value.  A wait that
-// gives up counts in *err, and once *err is set every later wait gives up
-// within a few polls, so a failed run still drains quickly.
-__device__ __forceinline__ float ld_rec(const uint64_t* p, uint32_t tag, int* err) {
+
+// Bounded wait until every wanted record carries its tag: records 0..R1-1
+// tag1, records R1.. tag2 (all loads of a round in flight together).  A wait
+// that gives up counts in *err, and once *err is set every later wait gives
+// up within a few polls, so a failed run still drains quickly.
+template <int R1, int R2>
+__device__ __forceinline__ void ld_recs2t(const uint64_t* const (&p)[R1 + R2], const bool (&want)[R1 + R2],
+                                          uint32_t tag1, uint32_t tag2, int* err, float (&out)[R1 + R2]) {
+  constexpr int R = R1 + R2;
+  bool need[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) need[r] = want[r];
   unsigned n = 0;
   while (true) {
-    const uint64_t v = __hip_atomic_load(const_cast<uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if ((uint32_t)(v >> 32) == tag) return __uint_as_float((uint32_t)v);
-    ++n;
-    if (n > kSpinLimit ||
-        ((n & 255) == 0 && __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
-      __hip_atomic_fetch_add(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return 0.f;
+    uint64_t v[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      v[r] = need[r] ? __hip_atomic_load(const_cast<uint64_t*>(p[r]), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                     : 0;
+    bool any = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (need[r] && (uint32_t)(v[r] >> 32) == (r < R1 ? tag1 : tag2)) {
+        out[r] = __uint_as_float((uint32_t)v[r]);
+        need[r] = false;
+      }
+      any = any || need[r];
     }
-    __builtin_amdgcn_s_sleep(1);
-  }
-}
-
-// The same for up to two records at once (both loads in flight per poll).
-__device__ __forceinline__ void ld_recs2(const uint64_t* const (&p)[2], const bool (&want)[2], uint32_t tag,
-                                         int* err, float (&out)[2]) {
-  bool need0 = want[0], need1 = want[1];
-  unsigned n = 0;
-  while (need0 || need1) {
-    const uint64_t v0 = need0 ? __hip_atomic_load(const_cast<uint64_t*>(p[0]), __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT) : 0;
-    const uint64_t v1 = need1 ? __hip_atomic_load(const_cast<uint64_t*>(p[1]), __ATOMIC_RELAXED,
-                                                  __HIP_MEMORY_SCOPE_AGENT) : 0;
-    if (need0 && (uint32_t)(v0 >> 32) == tag) {
-      out[0] = __uint_as_float((uint32_t)v0);
-      need0 = false;
-    }
-    if (need1 && (uint32_t)(v1 >> 32) == tag) {
-      out[1] = __uint_as_float((uint32_t)v1);
-      need1 = false;
-    }
-    if (!(need0 || need1)) break;
+    if (!__any(any)) return;
     ++n;
     if (n > kSpinLimit ||
         ((n & 255) == 0 && __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)) {
@@ -139,11 +140,64 @@ __device__ __forceinline__ void ld_recs2(const uint64_t* const (&p)[2], const bo
   }
 }
 
+// Workgroup barrier for LDS traffic only: this wave's LDS accesses are
+// complete (lgkmcnt(0)), then s_barrier; the compiler fences keep memory
+// accesses on their side.  Unlike __syncthreads() it does not wait for the
+// wave's outstanding global->LDS copies, which a release fence would.
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt = 63, expcnt = 7 (no wait), lgkmcnt = 0
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// v[j] for a lane-varying j in 0..7 as a tree of selects on the bits of j
+// (a compare chain is folded back into an indexed load, which would move v
+// out of registers)
+// v of lane l ^ 32 (v_permlane32_swap with v in both operands leaves the low
+// half in the low lanes of the first result and the high half in the second)
+__device__ __forceinline__ uint32_t from_lane_xor32(uint32_t v, int lane) {
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return lane < 32 ? r[1] : r[0];
+}
+__device__ __forceinline__ float from_lane_xor32f(float v, int lane) {
+  return __uint_as_float(from_lane_xor32(__float_as_uint(v), lane));
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+// 16-byte LDS read the compiler does not see as a read of the copy buffer, so
+// it adds no wait for the wave's outstanding loads (the copy has landed: its
+// waves waited for it before the barrier).  The caller waits for lgkmcnt.
+__device__ __forceinline__ u32x4 lds_read16_raw(uint32_t addr) {
+  u32x4 v;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr) : "memory");
+  return v;
+}
+
+// value of v in lane i (compile-time lane: a scalar read, no LDS crossbar)
+__device__ __forceinline__ float lane_value(float v, int i) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
+}
+__device__ __forceinline__ uint32_t comp(const uint4& v, int c) {
+  return c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
+}
+// component c (compile-time) of v[j]
+__device__ __forceinline__ uint32_t pick8c(const uint4 (&v)[KB1W], int j, int c) {
+  const bool b0 = j & 1, b1 = j & 2, b2 = j & 4;
+  const uint32_t t0 = b0 ? comp(v[1], c) : comp(v[0], c), t1 = b0 ? comp(v[3], c) : comp(v[2], c);
+  const uint32_t t2 = b0 ? comp(v[5], c) : comp(v[4], c), t3 = b0 ? comp(v[7], c) : comp(v[6], c);
+  return b2 ? (b1 ? t3 : t2) : (b1 ? t1 : t0);
+}
+
 __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
-  extern __shared__ unsigned char tbuf[];   // [NBUF][BUFB]; dynamic, as the LDS copy needs it
+  extern __shared__ unsigned char tbuf[];   // [BUFB]; dynamic, as the LDS copy needs it
   __shared__ Smem sm;
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  __shared__ uint4 wal[KBAW][NOBA][FNW][kWave];
+  // wave index made visibly uniform: branches on it are scalar and values
+  // derived from it stay in scalar registers
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave;
   const int tl = lane % 16, grp = lane / 16;
+  const int par = grp >> 1, half = grp & 1;   // stream parity and channel half of this lane
   const int G = a.G;
   const int team = blockIdx.x / G, s = blockIdx.x % G;
   if (team >= a.teams) return;
@@ -151,73 +205,207 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   const int64_t ntiles = (a.T + FM - 1) / FM;
   int64_t nq = 0;
   if (team < ntiles) nq = (ntiles - team + a.teams - 1) / a.teams;
-  if (nq == 0) return;
+  if (nq == 0) return;   // the same for every member of the team
 
-  // ---- weight slices in registers for the whole kernel (grouped layout:
-  // fragment cb of the 128-channel slice meets channels 32 grp + 8 cb)
+  // ---- weight slices in registers for the whole kernel.  This lane's MFMA
+  // operand rows are channels s*128 + 16 wave + 8 half + e of stream (slot)
+  // 2r + par: in the grouped layout that is lane 16 (wave / 2) + tl of
+  // fragment 4 ((i C) / 128 + s) + 2 (wave % 2) + half.
+  const int u4 = 2 * (wave % 2) + half, gl = (wave / 2) * 16 + tl;
   uint4 wf[KB1W][NOB1];
 #pragma unroll
   for (int r = 0; r < KB1W; ++r) {
-    const int q = wave * KB1W + r, i = q / (FCS / 32), cb = q % (FCS / 32);
-    const int64_t kb = ((int64_t)i * C + (int64_t)s * FCS) / 32 + cb;
+    const int64_t kb = (((int64_t)(2 * r + par) * C) / 128 + s) * 4 + u4;
 #pragma unroll
-    for (int ob = 0; ob < NOB1; ++ob) wf[r][ob] = a.wfull[(kb * NOB1 + ob) * kWave + lane];
+    for (int ob = 0; ob < NOB1; ++ob) wf[r][ob] = a.wfull[(kb * NOB1 + ob) * kWave + gl];
   }
-  uint4 wa[KBAW][NOBA];
+  // the active-row weights are used once per tile: they wait in LDS (32 KiB),
+  // one 16-byte fragment per lane, [k-block][out block][wave][lane]
 #pragma unroll
   for (int r = 0; r < KBAW; ++r) {
-    const int q = wave * KBAW + r, j = q / (FCS / 32), cb = q % (FCS / 32);
-    const int64_t kb = ((int64_t)j * C + (int64_t)s * FCS) / 32 + cb;
+    const int64_t kb = (((int64_t)(2 * r + par) * C) / 128 + s) * 4 + u4;
 #pragma unroll
-    for (int ob = 0; ob < NOBA; ++ob) wa[r][ob] = a.wact[(kb * NOBA + ob) * kWave + lane];
+    for (int ob = 0; ob < NOBA; ++ob) wal[r][ob][wave][lane] = a.wact[(kb * NOBA + ob) * kWave + gl];
+  }
+  // per-lane constants of the reducers (lane i < 16: output i)
+  const float cs_l = a.colsum[tl], bpre_l = a.b_pre[tl], alpha_pre = a.alpha[0];
+
+  // offsets of this member's reducer records, per polling lane (the same for
+  // every tile): flat record u = jj G + g, value vi -> sm.vals[u]
+  if (wave >= NCOPY) {
+    const int pl = (wave - NCOPY) * kWave + lane;
+#pragma unroll
+    for (int r = 0; r < BREC; ++r) {
+      const int u = pl + r * NPOLL * kWave;
+      const int jg = u / NJV, vi = u % NJV, jj = jg / G, g = jg % G;
+      const int j = s + jj * G;
+      const int o = vi < FN ? (j % 2 == 0 ? vi : FN + vi) : (j % 2 == 0 ? 32 + (vi - FN) : (vi == FN ? 33 : -1));
+      sm.poff[r][pl] = (jg < 2 * FM && jj * G + s < 2 * FM && o >= 0) ? (g * FM + j / 2) * NV1 + o : -1;
+    }
   }
 
-  // ---- tile copy: 64 wave instructions of 1 KiB (4 streams of one token),
-  // instruction n -> token n / 4, streams 4 (n % 4) .. + 3; lane -> stream
-  // + lane / 16, bytes (lane % 16) * 16 of the row slice
-  auto copy_tile = [&](int64_t tile, int b) {
-    unsigned char* dst0 = tbuf + (size_t)b * BUFB;
-    for (int n = wave; n < FM * FN / 4; n += FNW) {
+  // ---- tile copy by the copy waves: 64 wave instructions of 1 KiB (4 streams
+  // of one token), instruction n -> token n / 4, streams 4 (n % 4) .. + 3;
+  // lane -> stream + lane / 16, bytes (lane % 16) * 16 of the row slice
+  auto copy_tile = [&](int64_t tile) {
+    for (int n = wave; n < FM * FN / 4; n += NCOPY) {
       const int t = n / 4, i = (n % 4) * 4 + lane / 16;
       int64_t tg = tile * FM + t;
       if (tg >= a.T) tg = a.T - 1;   // in bounds; the token's results are dropped
       const uint16_t* src = a.X + (tg * FN + i) * (int64_t)C + (int64_t)s * FCS + (lane % 16) * 8;
-      __builtin_amdgcn_global_load_lds(src, dst0 + t * TOKP + (n % 4) * 4 * ROWB, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src, tbuf + t * TOKP + (n % 4) * 4 * ROWB, 16, 0, 0);
+    }
+  };
+  if (wave < NCOPY) copy_tile(team);
+
+  const float NC = (float)FN * (float)C;
+  const int coff = (int)((int64_t)s * FCS) + 16 * wave + 8 * half;   // first channel of this lane's 8
+
+  // ---- reducers.  This member's jobs of tile qt are j = s + jj G (jj = 0, 1,
+  // ...; t = j / 2, h = j % 2).  Their member partials are polled by all
+  // polling waves together: flat record u -> job jj and member g
+  // (jj G + g = u / NJV), value vi = u % NJV.
+  const int njobs = (2 * FM - s + G - 1) / G;
+  // finish job jj of tile qt from sm.vals (one wave)
+  auto finish_job = [&](int64_t qt, int jj) {
+    const int j = s + jj * G, t = j / 2, h = j % 2;
+    const int nv = h == 0 ? FN + 2 : FN + 1;
+    const uint32_t tag = (uint32_t)(qt + 1);
+    // lanes 0..nv-1 sum their value over the members in member order
+    float v = 0.f;
+    if (lane < nv) {
+      const float* col = &sm.vals[jj * G][lane];
+      int g = 0;
+      for (; g + 8 <= G; g += 8) {   // eight loads in flight, adds in member order
+        float t8[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) t8[e] = col[(g + e) * NJV];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v += t8[e];
+      }
+      for (; g < G; ++g) v += col[g * NJV];
+    }
+    const int64_t tile = team + qt * a.teams;
+    const int64_t tg = tile * FM + t;
+    uint64_t* r2 = a.rec2 + ((int64_t)team * RING + qt % RING) * FM * NV2 + t * NV2;
+    if (h == 0) {
+      const float mu = lane_value(v, FN) / NC, nu = lane_value(v, FN + 1) / NC;
+      const float r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + a.eps);
+      const float z = (v - mu * cs_l) * r_ln;   // lanes 0..15: LayerNorm-corrected router logit
+      // rank among the candidates i >= m (larger logit first, ties to the lower index)
+      int rank = 0;
+#pragma unroll
+      for (int i = 0; i < FN; ++i) {
+        const float zi = lane_value(z, i);
+        if (i >= a.m && i != lane && (zi > z || (zi == z && i < lane))) ++rank;
+      }
+      int slot = -1;
+      float pv = 1.0f;
+      if (lane < a.m) slot = lane;
+      else if (lane < FN && rank < FK - a.m) {
+        slot = a.m + rank;
+        pv = sigmoidf(z);
+      }
+      if (a.saved && tg < a.T) {
+        float* sv = a.saved + tg * a.nsave;
+        if (lane < FN) sv[lane] = z;
+        else if (lane == FN) sv[a.nsave - 4] = mu;
+        else if (lane == FN + 1) sv[a.nsave - 3] = nu;
+      }
+      if (slot >= 0) {
+        st_rec(r2 + FN + slot, __int_as_float(lane), tag);
+        if (tg < a.T) {
+          a.idx[tg * FK + slot] = lane;
+          a.p[tg * FK + slot] = pv;
+        }
+      }
+    } else {
+      const float nu = lane_value(v, FN) / NC;
+      const float r_rms = 1.0f / sqrtf(nu + a.eps);
+      if (lane < FN) {
+        if (a.saved && tg < a.T) a.saved[tg * a.nsave + FN + lane] = v * r_rms;
+        const float hpre = sigmoidf(alpha_pre * (v * r_rms) + bpre_l);
+        st_rec(r2 + lane, hpre, tag);
+        if (tg < a.T) a.Hpre[tg * FN + lane] = hpre;
+      }
     }
   };
 
-  copy_tile(team, 0);
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  const float NC = (float)FN * (float)C;
-  for (int64_t q = 0; q < nq; ++q) {
-    const int64_t tile = team + q * a.teams;
-    const int b = (int)(q % NBUF);
-    const unsigned char* buf = tbuf + (size_t)b * BUFB;
-    const uint32_t tag = (uint32_t)(q + 1);
-    const int slot = (int)(q % RING);
-    uint64_t* r1 = a.rec1 + (((int64_t)team * RING + slot) * G) * FM * NV1;
-    uint64_t* r2 = a.rec2 + ((int64_t)team * RING + slot) * FM * NV2;
+  // record r of this polling lane: address and whether it is wanted
+  auto poll_rec = [&](int64_t q, int r, bool& wanted) -> const uint64_t* {
+    const bool hasB = q >= 1 && q - 1 < nq, hasC = q >= 2 && q - 2 < nq;
+    const int pl = (wave - NCOPY) * kWave + lane;   // 0 .. 255
+    if (r < BREC) {
+      const uint64_t* r1 = a.rec1 + (((int64_t)team * RING + (q - 1 + RING) % RING) * G) * FM * NV1;
+      const int off = sm.poff[r][pl];
+      wanted = hasB && off >= 0;
+      return r1 + (wanted ? off : 0);
+    }
+    const uint64_t* r2 = a.rec2 + ((int64_t)team * RING + (q - 2 + RING) % RING) * FM * NV2;
+    const int u = pl + (r - BREC) * NPOLL * kWave;
+    wanted = hasC && u < FM * NV2;
+    return r2 + (wanted ? u : 0);
+  };
+  // first loads of the records of step qs, issued at the end of step qs - 1
+  // (polling waves) and checked after A of step qs
+  auto issue_polls = [&](int64_t qs, uint64_t (&first)[BREC + CREC]) {
+#pragma unroll
+    for (int r = 0; r < BREC + CREC; ++r) {
+      bool w;
+      const uint64_t* pr = poll_rec(qs, r, w);
+      first[r] = w ? __hip_atomic_load(const_cast<uint64_t*>(pr), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    }
+  };
+  uint64_t first[BREC + CREC];
+#pragma unroll
+  for (int r = 0; r < BREC + CREC; ++r) first[r] = 0;
 
-    // ---- A: partial projection of the slice, published as tagged records
-    {
+  // ---- pipeline steps: A of tile q (registers XA), B of tile q - 1, C of
+  // tile q - 2 (registers XC); the registers rotate at the end of a step
+  uint4 XA[KB1W], XB[KB1W], XC[KB1W];
+  for (int64_t q = 0; q < nq + 2; ++q) {
+    const bool hasA = q < nq, hasB = q >= 1 && q - 1 < nq, hasC = q >= 2 && q - 2 < nq;
+    if (wave < NCOPY) {
+      __builtin_amdgcn_s_waitcnt(0);   // this wave's part of the copy of tile q has landed
+    }
+    // polling waves check the records of this step after A: the member
+    // partials of this member's jobs of tile q - 1 (BREC per lane) and H^pre /
+    // idx of tile q - 2 (CREC per lane); their first loads went out at the
+    // end of the previous step
+    const bool polls = wave >= NCOPY && (hasB || hasC);
+    lds_barrier();   // S1: tile q in the buffer
+    if (hasA) {
+      const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)tbuf +
+                            tl * TOKP + par * ROWB + (16 * wave + 8 * half) * 2;
+      u32x4 xr[KB1W];
+#pragma unroll
+      for (int r = 0; r < KB1W; ++r) xr[r] = lds_read16_raw(base + 2 * r * ROWB);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int r = 0; r < KB1W; ++r) {
+        asm volatile("" : "+v"(xr[r]));   // uses stay after the wait
+        XA[r] = make_uint4(xr[r][0], xr[r][1], xr[r][2], xr[r][3]);
+      }
+    }
+    lds_barrier();   // S2: the buffer is free
+    if (hasA) {
+      if (wave < NCOPY && q + 1 < nq) copy_tile(team + (q + 1) * a.teams);
+      // ---- A: partial projection and moments of the slice
       f32x4 acc[NOB1];
 #pragma unroll
       for (int ob = 0; ob < NOB1; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
       for (int r = 0; r < KB1W; ++r) {
-        const int qq = wave * KB1W + r, i = qq / (FCS / 32), cb = qq % (FCS / 32);
-        const uint4 xb = lds_read16(buf + tl * TOKP + i * ROWB + (grp * 32 + cb * 8) * 2);
         float f[8];
-        unpack8(xb, f);
+        unpack8(XA[r], f);
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           s1 += f[e];
           s2 += f[e] * f[e];
         }
 #pragma unroll
-        for (int ob = 0; ob < NOB1; ++ob) acc[ob] = mfma_16x16x32(wf[r][ob], xb, acc[ob]);
+        for (int ob = 0; ob < NOB1; ++ob) acc[ob] = mfma_16x16x32(wf[r][ob], XA[r], acc[ob]);
       }
       s1 += __shfl_xor(s1, 16);
       s1 += __shfl_xor(s1, 32);
@@ -232,149 +420,124 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
         sm.red[wave][33][tl] = s2;
       }
     }
-    __syncthreads();   // also: every wave is done with the other buffer (tile q - 1)
-    if (q + 1 < nq) copy_tile(tile + a.teams, (int)((q + 1) % NBUF));
-    for (int u = tid; u < NV1 * FM; u += FNT) {
-      const int o = u / FM, t = u % FM;
-      float v = 0.f;
+    if (polls) {
+      // tags: tile q - 1 for the partials, tile q - 2 for H^pre / idx
+      const uint64_t* src[BREC + CREC];
+      bool want[BREC + CREC], need[BREC + CREC];
+      float val[BREC + CREC];
+      bool any = false;
 #pragma unroll
-      for (int w = 0; w < FNW; ++w) v += sm.red[w][o][t];
-      st_rec(r1 + ((int64_t)s * FM + t) * NV1 + o, v, tag);
+      for (int r = 0; r < BREC + CREC; ++r) {
+        src[r] = poll_rec(q, r, want[r]);
+        const uint32_t tag = r < BREC ? (uint32_t)q : (uint32_t)(q - 1);
+        need[r] = want[r] && (uint32_t)(first[r] >> 32) != tag;
+        val[r] = __uint_as_float((uint32_t)first[r]);
+        any = any || need[r];
+      }
+      if (__any(any)) ld_recs2t<BREC, CREC>(src, need, (uint32_t)q, (uint32_t)(q - 1), a.err, val);
+      const int pl = (wave - NCOPY) * kWave + lane;
+#pragma unroll
+      for (int r = 0; r < BREC; ++r)
+        if (want[r]) (&sm.vals[0][0])[pl + r * NPOLL * kWave] = val[r];
+#pragma unroll
+      for (int r = 0; r < CREC; ++r)
+        if (want[BREC + r]) (&sm.hpid[0][0])[pl + r * NPOLL * kWave] = val[BREC + r];
     }
-
-    // ---- B: 32 jobs per tile, job j = 2 t + h taken by member j % G: h = 0
-    // sums token t's router outputs and moments and routes it, h = 1 sums its
-    // pre-map outputs and forms H^pre; both publish their results as records
-    for (int j = s; j < 2 * FM; j += G) {
-      const int t = j / 2, h = j % 2;
-      const int nv = h == 0 ? FN + 2 : FN + 1;   // router outputs + sum x + sum x^2 | pre outputs + sum x^2
-      const int n = G * nv;
-      // every thread waits on its (at most two) records together
-      float val[2] = {0.f, 0.f};
-      const uint64_t* src[2];
-      bool want[2];
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const int u = tid + r * FNT;
-        want[r] = u < n;
-        const int g = want[r] ? u / nv : 0, vi = want[r] ? u % nv : 0;
-        const int o = h == 0 ? (vi < FN ? vi : 32 + (vi - FN)) : (vi < FN ? FN + vi : 33);
-        src[r] = r1 + ((int64_t)g * FM + t) * NV1 + o;
-      }
-      ld_recs2(src, want, tag, a.err, val);
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const int u = tid + r * FNT;
-        if (want[r]) sm.vals[u / nv][u % nv] = val[r];
-      }
-      __syncthreads();
-      if (tid < kWave) {
-        // lanes 0..nv-1 sum their value over the members in member order
+    lds_barrier();   // S3: A partials, polled records in LDS
+    // the reducers first: a wave's later loads and LDS reads may wait for its
+    // stores, so the record stores of the publish come after
+    if (hasB && wave >= NCOPY)
+      for (int jj = wave - NCOPY; jj < njobs; jj += NPOLL) finish_job(q - 1, jj);
+    if (hasA) {
+      uint64_t* r1 = a.rec1 + (((int64_t)team * RING + q % RING) * G) * FM * NV1;
+      for (int u = tid; u < NV1 * FM; u += FNT) {
+        const int o = u / FM, t = u % FM;
         float v = 0.f;
-        if (tid < nv)
-          for (int g = 0; g < G; ++g) v += sm.vals[g][tid];
-        const int64_t tg = tile * FM + t;
-        if (h == 0) {
-          const float mu = __shfl(v, FN) / NC, nu = __shfl(v, FN + 1) / NC;
-          const float r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + a.eps);
-          float zr[FN];
 #pragma unroll
-          for (int i = 0; i < FN; ++i) zr[i] = (__shfl(v, i) - mu * a.colsum[i]) * r_ln;
-          if (tid == 0) {
-            int32_t id[FK];
-            float pp[FK];
-            route_token<FN>(zr, FN, a.m, FK, id, pp);
+        for (int w = 0; w < FNW; ++w) v += sm.red[w][o][t];
+        st_rec(r1 + ((int64_t)s * FM + t) * NV1 + o, v, (uint32_t)(q + 1));
+      }
+    }
+    if (hasC) {
+      const int64_t tile = team + (q - 2) * a.teams;
+      const int64_t tg = tile * FM + tl;
+      // ---- dense read of the lane's 8 channels: its 8 streams, then the
+      // other parity from lane ^ 32
+      {
+        float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int q2 = 0; q2 < FK; ++q2) {
-              st_rec(r2 + t * NV2 + FN + q2, __int_as_float(id[q2]), tag);
-              if (tg < a.T) {
-                a.idx[tg * FK + q2] = id[q2];
-                a.p[tg * FK + q2] = pp[q2];
-              }
-            }
+        for (int r = 0; r < KB1W; ++r) {
+          const float hv = sm.hpid[tl][2 * r + par];
+          float f[8];
+          unpack8(XC[r], f);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[e] = fmaf(hv, f[e], acc[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += from_lane_xor32f(acc[e], lane);
+        if (par == 0 && tg < a.T) *reinterpret_cast<uint4*>(a.input + tg * C + coff) = pack8(acc);
+      }
+      // ---- active rows: slot 2r + par of this lane; the stream lives in this
+      // lane (same parity) or in lane ^ 32
+      {
+        int id4[FK];
+#pragma unroll
+        for (int j = 0; j < FK; ++j) id4[j] = __float_as_int(sm.hpid[tl][FN + j]) & (FN - 1);   // always a row of the tile
+        f32x4 acc[NOBA];
+#pragma unroll
+        for (int ob = 0; ob < NOBA; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+        float s2 = 0.f;
+#pragma unroll
+        for (int r = 0; r < KBAW; ++r) {
+          const int mine = par ? id4[2 * r + 1] : id4[2 * r];      // stream this lane needs
+          const int theirs = par ? id4[2 * r] : id4[2 * r + 1];    // stream lane ^ 32 needs
+          // one 32-bit component at a time keeps the select trees small
+          const bool keep = (mine & 1) == par;
+          uint32_t xw[4];
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            const uint32_t own = pick8c(XC, mine >> 1, c);
+            const uint32_t recv = from_lane_xor32(pick8c(XC, theirs >> 1, c), lane);
+            xw[c] = keep ? own : recv;
           }
-        } else {
-          const float nu = __shfl(v, FN) / NC;
-          const float r_rms = 1.0f / sqrtf(nu + a.eps);
-          if (tid < FN) {
-            const float hpre = sigmoidf(a.alpha[0] * (v * r_rms) + a.b_pre[tid]);
-            st_rec(r2 + t * NV2 + tid, hpre, tag);
-            if (tg < a.T) a.Hpre[tg * FN + tid] = hpre;
-          }
+          const uint4 xa = make_uint4(xw[0], xw[1], xw[2], xw[3]);
+          float f[8];
+          unpack8(xa, f);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) s2 += f[e] * f[e];
+#pragma unroll
+          for (int ob = 0; ob < NOBA; ++ob) acc[ob] = mfma_16x16x32(wal[r][ob][wave][lane], xa, acc[ob]);
+        }
+        s2 += __shfl_xor(s2, 16);
+        s2 += __shfl_xor(s2, 32);
+#pragma unroll
+        for (int ob = 0; ob < NOBA; ++ob)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) sm.red2[wave][ob * 16 + grp * 4 + v][tl] = acc[ob][v];
+        if (grp == 0) {
+          sm.red2[wave][32][tl] = 0.f;
+          sm.red2[wave][33][tl] = s2;
         }
       }
-      __syncthreads();
     }
-
-    // ---- C: H^pre and idx of the tile
-    if (tid < FM * NV2) {
-      const int t = tid / NV2, v = tid % NV2;
-      const float x = ld_rec(r2 + t * NV2 + v, tag, a.err);
-      if (v < FN) sm.hp[t][v] = x;
-      else sm.id[t][v - FN] = __float_as_int(x) & (FN - 1);   // always a row of the tile
-    }
-    __syncthreads();
-
-    // ---- D: dense read of the slice, thread -> token tid / 32, channels 4 (tid % 32) .. + 3
-    {
-      const int t = tid / 32, c4 = (tid % 32) * 4;
-      float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    lds_barrier();   // S5: H^pre / idx / active partials of tile q - 2 consumed
+    if (hasC) {
+      const int64_t tile = team + (q - 2) * a.teams;
+      for (int u = tid; u < NV1 * FM; u += FNT) {
+        const int o = u / FM, t = u % FM;
+        const int64_t tg = tile * FM + t;
+        float v = 0.f;
 #pragma unroll
-      for (int i = 0; i < FN; ++i) {
-        const uint2 v = *reinterpret_cast<const uint2*>(buf + t * TOKP + i * ROWB + c4 * 2);
-        const float h = sm.hp[t][i];
-        acc[0] = fmaf(h, bf_lo(v.x), acc[0]);
-        acc[1] = fmaf(h, bf_hi(v.x), acc[1]);
-        acc[2] = fmaf(h, bf_lo(v.y), acc[2]);
-        acc[3] = fmaf(h, bf_hi(v.y), acc[3]);
-      }
-      const int64_t tg = tile * FM + t;
-      if (tg < a.T)
-        *reinterpret_cast<uint2*>(a.input + tg * C + (int64_t)s * FCS + c4) =
-            make_uint2(pack2bf(acc[0], acc[1]), pack2bf(acc[2], acc[3]));
-    }
-
-    // ---- E: partial projection of the gathered active rows of the slice
-    {
-      f32x4 acc[NOBA];
-#pragma unroll
-      for (int ob = 0; ob < NOBA; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-      float s2 = 0.f;
-#pragma unroll
-      for (int r = 0; r < KBAW; ++r) {
-        const int qq = wave * KBAW + r, j = qq / (FCS / 32), cb = qq % (FCS / 32);
-        const int row = sm.id[tl][j];
-        const uint4 xb = lds_read16(buf + tl * TOKP + row * ROWB + (grp * 32 + cb * 8) * 2);
-        float f[8];
-        unpack8(xb, f);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) s2 += f[e] * f[e];
-#pragma unroll
-        for (int ob = 0; ob < NOBA; ++ob) acc[ob] = mfma_16x16x32(wa[r][ob], xb, acc[ob]);
-      }
-      s2 += __shfl_xor(s2, 16);
-      s2 += __shfl_xor(s2, 32);
-#pragma unroll
-      for (int ob = 0; ob < NOBA; ++ob)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) sm.red[wave][ob * 16 + grp * 4 + v][tl] = acc[ob][v];
-      if (grp == 0) {
-        sm.red[wave][32][tl] = 0.f;
-        sm.red[wave][33][tl] = s2;
+        for (int w = 0; w < FNW; ++w) v += sm.red2[w][o][t];
+        if (tg < a.T) a.part2[((int64_t)s * NV1 + o) * a.T + tg] = v;
       }
     }
-    __syncthreads();
-    for (int u = tid; u < NV1 * FM; u += FNT) {
-      const int o = u / FM, t = u % FM;
-      const int64_t tg = tile * FM + t;
-      float v = 0.f;
+    if (wave >= NCOPY) issue_polls(q + 1, first);
 #pragma unroll
-      for (int w = 0; w < FNW; ++w) v += sm.red[w][o][t];
-      if (tg < a.T) a.part2[((int64_t)s * NV1 + o) * a.T + tg] = v;
+    for (int r = 0; r < KB1W; ++r) {
+      XC[r] = XB[r];
+      XB[r] = XA[r];
     }
-    // the next tile's copy has landed in every wave; sm.red is free again
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
   }
 }
 
@@ -388,7 +551,7 @@ struct DeviceInfo {
   int per_cu = 0;
 };
 
-constexpr size_t kTileLds = (size_t)NBUF * BUFB;
+constexpr size_t kTileLds = (size_t)BUFB;
 
 DeviceInfo device_info() {
   static thread_local int dev_cached = -1;
@@ -414,7 +577,8 @@ DeviceInfo device_info() {
 
 bool fused_pre_supported(const xhc_dims* d) {
   return d->state_dtype == XHC_BF16 && d->N == FN && d->k == FK && d->Kr >= 1 &&
-         FK * d->Kr + FK * FK <= 16 * NOBA && d->C % FCS == 0 && d->C / FCS <= kMaxG;
+         FK * d->Kr + FK * FK <= 16 * NOBA && d->C % FCS == 0 && d->C / FCS <= kMaxG &&
+         kMaxG % (d->C / FCS) == 0;   // every member takes 32 / G reducer jobs per tile
 }
 
 // Workspace: error counter, records (sized for up to kMaxResident co-resident
@@ -433,7 +597,7 @@ size_t fused_pre_ws_bytes(const xhc_dims* d) {
 hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed_full, const float* colsum,
                             const void* packed_act, const float* alpha, const float* b_pre, const float* b_res,
                             const float* b_post, void* input, int32_t* idx, float* p, float* Hpre, float* Hres,
-                            float* Hpost, void* ws, hipStream_t s) {
+                            float* Hpost, float* saved, void* ws, hipStream_t s) {
   const DeviceInfo di = device_info();
   if (di.cus <= 0 || di.per_cu <= 0) return hipErrorInvalidConfiguration;
   const int G = d->C / FCS;
@@ -452,6 +616,8 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
   a.idx = idx;
   a.p = p;
   a.Hpre = Hpre;
+  a.saved = saved;
+  a.nsave = saved_floats(FN, FK, d->Kr);
   a.err = reinterpret_cast<int*>(w);
   a.rec1 = reinterpret_cast<uint64_t*>(w + 256);
   a.rec2 = reinterpret_cast<uint64_t*>(w + 256 + align256(rec1_words(G) * 8));
@@ -478,8 +644,8 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
   if (e != hipSuccess) return e;
   // active partials -> H^post, H^res (Sinkhorn + clamp)
   return launch_pre_coef(a.part2, G, (int64_t)FK * d->Kr + FK * FK, d->T, FK, d->Kr, 1, d->C, alpha + 2, alpha + 1,
-                         b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost, Hres, sums, nullptr, 0, 0,
-                         0, s);
+                         b_post, b_res, d->eps, d->sinkhorn_iters, d->clamp_delta, Hpost, Hres, sums, saved, a.nsave,
+                         2 * FN, a.nsave - 2, s, a.err);
 }
 
 }  // namespace xhc

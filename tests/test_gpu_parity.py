@@ -26,11 +26,15 @@ SMALL = [
     W(T=136, S=68, N=16, k=4, m=2, C=1024, Kr=4, state="f32", name="runs-f32-T136-S68"),
     W(T=96, S=48, N=16, k=8, m=2, C=512, Kr=4, name="runs-k8-T96"),
     W(T=150, S=50, N=8, k=4, m=2, C=256, Kr=4, name="S50-per-token-post"),   # S % 4 != 0
+    # single-pass pre with 2 and 1 members per team (16 and 32 reducer jobs per
+    # member and tile) and a ragged last tile
+    W(T=77, S=77, N=16, k=4, m=2, C=256, Kr=1, name="team2-T77-C256"),
+    W(T=50, S=25, N=16, k=4, m=2, C=128, Kr=4, name="team1-T50-C128"),
 ]
 
 
 def _fused_ok(w):
-    return w.state == "bf16" and w.N == 16 and w.k == 4 and w.C % 128 == 0
+    return w.state == "bf16" and w.N == 16 and w.k == 4 and w.C % 128 == 0 and 32 % (w.C // 128) == 0
 
 
 IMPLS = {"multi": X.XHC_IMPL_MULTI, "fused": X.XHC_IMPL_FUSED}
