@@ -12,8 +12,9 @@
  * Conventions for every entry point:
  *  - All tensor pointers are DEVICE pointers owned by the caller; the library
  *    never allocates or frees memory inside a call.  `workspace` is caller
- *    device memory of at least xhc_workspace_bytes() bytes; its contents on
- *    entry are ignored and on return are unspecified.
+ *    device memory of at least xhc_workspace_bytes() bytes, 16-byte aligned
+ *    (hipMalloc gives 256); its contents on entry are ignored and on return
+ *    are unspecified.
  *  - `stream` is a hipStream_t passed as void* (NULL = default stream).  Calls
  *    are asynchronous on that stream and enqueue device work only.
  *  - Layouts are row-major and contiguous: X [T,N,C]; F, input [T,C];

@@ -217,7 +217,8 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   if (!X || !packed_full || !packed_act || !alpha || !b_pre || !b_res || !b_post || !input || !idx || !p ||
       !Hpre || !Hres || !Hpost || !workspace)
     return XHC_EINVAL;
-  if (!aligned16(X) || !aligned16(input) || !aligned16(packed_full) || !aligned16(packed_act))
+  if (!aligned16(X) || !aligned16(input) || !aligned16(packed_full) || !aligned16(packed_act) ||
+      !aligned16(workspace))
     return XHC_EUNSUPPORTED;
   if (d->impl == XHC_IMPL_FUSED && !fused_pre_supported(d)) return XHC_EUNSUPPORTED;
   if (workspace_bytes < pre_ws(d)) return XHC_EWORKSPACE;

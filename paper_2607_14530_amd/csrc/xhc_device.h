@@ -110,6 +110,34 @@ __device__ __forceinline__ f32x4 mfma_16x16x32(uint4 a, uint4 b, f32x4 c) {
                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// ---------------------------------------------------------------- wave reduction
+
+// Sum of v over the 64 lanes of the wave, returned in every lane: pairs and
+// quads by DPP quad permutes, half rows and rows by DPP mirrors (the values
+// are uniform within the smaller group by then, so a mirror adds the other
+// half), then row pairs and wave halves by the gfx950 permlane swaps.  Fixed
+// order, so the result is deterministic.
+__device__ __forceinline__ float dpp_add(float v, int ctrl_sel) {
+  int o = 0;
+  switch (ctrl_sel) {
+    case 0: o = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false); break;   // quad_perm 1,0,3,2
+    case 1: o = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false); break;   // quad_perm 2,3,0,1
+    case 2: o = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false); break;  // row_half_mirror
+    default: o = __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false); break; // row_mirror
+  }
+  return v + __int_as_float(o);
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v = dpp_add(v, 0);
+  v = dpp_add(v, 1);
+  v = dpp_add(v, 2);
+  v = dpp_add(v, 3);
+  const auto r16 = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  v = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+  const auto r32 = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
+}
+
 // ---------------------------------------------------------------- math
 
 __device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + __expf(-z)); }
@@ -191,6 +219,51 @@ __device__ __forceinline__ void sinkhorn_clamp(float (&M)[kMaxK * kMaxK], int k,
 #pragma unroll
         for (int l = 0; l < kMaxK; ++l) if (l < k) M[j * kMaxK + l] *= r;
       }
+    }
+  }
+}
+
+// The same for a compile-time k (no padded rows or columns); identical
+// arithmetic and order.
+template <int K>
+__device__ __forceinline__ void sinkhorn_clamp_k(float (&M)[K * K], int iters, float delta) {
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    float mx = M[j * K];
+#pragma unroll
+    for (int l = 1; l < K; ++l) mx = fmaxf(mx, M[j * K + l]);
+#pragma unroll
+    for (int l = 0; l < K; ++l) M[j * K + l] = __expf(M[j * K + l] - mx);
+  }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < K; ++j) {
+      float s = 0.f;
+#pragma unroll
+      for (int l = 0; l < K; ++l) s += M[j * K + l];
+      const float r = 1.0f / s;
+#pragma unroll
+      for (int l = 0; l < K; ++l) M[j * K + l] *= r;
+    }
+#pragma unroll
+    for (int l = 0; l < K; ++l) {
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < K; ++j) s += M[j * K + l];
+      const float r = 1.0f / s;
+#pragma unroll
+      for (int j = 0; j < K; ++j) M[j * K + l] *= r;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < K; ++j) {
+    float s = 0.f;
+#pragma unroll
+    for (int l = 0; l < K; ++l) s += M[j * K + l];
+    if (s > 1.0f + delta) {
+      const float r = 1.0f / s;
+#pragma unroll
+      for (int l = 0; l < K; ++l) M[j * K + l] *= r;
     }
   }
 }

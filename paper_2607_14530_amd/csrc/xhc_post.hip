@@ -191,16 +191,19 @@ __global__ __launch_bounds__(256) void k_post_gram_run(const TS* __restrict__ F,
   cg.load_taps(conv_w, C, c);
   cg.init(F, t0, S, C, c);
   float* mine = &xpose[wave][lane][0];
+  // the rows of the next group are loaded while this group is computed
+  typename Row4<TS>::raw nxt[G];
+#pragma unroll
+  for (int g = 0; g < G; ++g) nxt[g] = g < nt ? Row4<TS>::load(F + (t0 + g) * C + c) : Row4<TS>::zero();
   for (int u0 = 0; u0 < nt; u0 += G) {
     const int64_t t = t0 + u0;
     if (t % S == 0) cg.reset();
     float cur[G][4];
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      typename Row4<TS>::raw v = Row4<TS>::zero();
-      if (u0 + g < nt) v = Row4<TS>::load(F + (t + g) * C + c);
-      Row4<TS>::unpack(v, cur[g]);
-    }
+    for (int g = 0; g < G; ++g) Row4<TS>::unpack(nxt[g], cur[g]);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+      nxt[g] = u0 + G + g < nt ? Row4<TS>::load(F + (t + G + g) * C + c) : Row4<TS>::zero();
     float part[NV];
 #pragma unroll
     for (int g = 0; g < G; ++g) {

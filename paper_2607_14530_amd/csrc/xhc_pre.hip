@@ -177,6 +177,91 @@ __global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ sums
     for (int l = 0; l < k; ++l) Hres[(t * k + j) * k + l] = M[j * kMaxK + l];
 }
 
+// k = 4: the chunk sums of the active projection and the coefficients in one
+// launch.  A block takes 32 tokens; thread (part h, token u) sums chunk range
+// h of token u (8 ranges), the ranges are added in order through LDS, and one
+// thread per token forms the coefficients.
+constexpr int kCoefTok = 32, kCoefParts = 8;
+template <int K>
+__global__ __launch_bounds__(kCoefTok * kCoefParts) void k_pre_coef_sum(
+    const float* __restrict__ part, int64_t nchunk, int NO, int64_t T, int Kq, int with_res, int64_t kC,
+    const float* __restrict__ alpha_post, const float* __restrict__ alpha_res, const float* __restrict__ b_post,
+    const float* __restrict__ b_res, float eps, int iters, float delta, float* __restrict__ Hpost,
+    float* __restrict__ Hres, float* __restrict__ saved, int nsave, int save_z_at, int save_stats_at,
+    const int* __restrict__ err) {
+  constexpr int NA = K * kMaxKr + K * K;   // outputs kept (at most)
+  __shared__ float red[kCoefParts][NA + 1][kCoefTok];
+  const int u = threadIdx.x % kCoefTok, h = threadIdx.x / kCoefTok;
+  const int64_t t = (int64_t)blockIdx.x * kCoefTok + u;
+  const int nproj = K * Kq + (with_res ? K * K : 0);
+  {
+    float acc[NA + 1];
+#pragma unroll
+    for (int o = 0; o <= NA; ++o) acc[o] = 0.f;
+    const int64_t per = (nchunk + kCoefParts - 1) / kCoefParts;
+    const int64_t c0 = h * per, c1 = (c0 + per < nchunk) ? c0 + per : nchunk;
+    if (t < T) {
+      const int64_t stride = (int64_t)NO * T;
+      for (int64_t c = c0; c < c1; ++c) {
+        const float* pc = part + c * stride + t;
+        float v[NA + 1];
+#pragma unroll
+        for (int o = 0; o < NA; ++o) v[o] = o < nproj ? pc[(int64_t)o * T] : 0.f;
+        v[NA] = pc[(int64_t)(NO - 1) * T];
+#pragma unroll
+        for (int o = 0; o <= NA; ++o) acc[o] += v[o];
+      }
+    }
+#pragma unroll
+    for (int o = 0; o <= NA; ++o) red[h][o][u] = acc[o];
+  }
+  __syncthreads();
+  if (h != 0 || t >= T) return;
+  float acc[NA + 1];
+#pragma unroll
+  for (int o = 0; o <= NA; ++o) {
+    float v = red[0][o][u];
+#pragma unroll
+    for (int q = 1; q < kCoefParts; ++q) v += red[q][o][u];
+    acc[o] = v;
+  }
+  if (err && *err != 0) {
+    // the single-pass kernel gave up a wait: its partials are not valid
+    const float nan = __uint_as_float(0x7fc00000u);
+    for (int o = 0; o < K * Kq; ++o) Hpost[t * K * Kq + o] = nan;
+    if (with_res)
+      for (int o = 0; o < K * K; ++o) Hres[t * K * K + o] = nan;
+    return;
+  }
+  const float nu_a = acc[NA] / (float)kC;
+  const float rstd = 1.0f / sqrtf(nu_a + eps);
+  if (saved) {
+    saved[t * nsave + save_stats_at] = nu_a;
+#pragma unroll
+    for (int o = 0; o < NA; ++o)
+      if (o < nproj) saved[t * nsave + save_z_at + o] = acc[o] * rstd;
+  }
+  const float ap = alpha_post[0];
+#pragma unroll
+  for (int o = 0; o < K * kMaxKr; ++o)
+    if (o < K * Kq) Hpost[t * K * Kq + o] = 2.0f * sigmoidf(ap * (acc[o] * rstd) + b_post[o]);
+  if (!with_res) return;
+  const float ar = alpha_res[0];
+  float M[K * K];
+#pragma unroll
+  for (int o = 0; o < K * K; ++o) {
+    // the W_res outputs follow the K Kq W_post outputs
+    float z = 0.f;
+#pragma unroll
+    for (int q = 1; q <= kMaxKr; ++q)
+      if (q == Kq) z = acc[K * q + o];
+    M[o] = ar * (z * rstd) + b_res[o];
+  }
+  sinkhorn_clamp_k<K>(M, iters, delta);
+#pragma unroll
+  for (int o = 0; o < K * K; ++o) Hres[t * K * K + o] = M[o];
+}
+
 static hipError_t sum_chunks(const float* part, int64_t nchunk, int NO, int64_t T, float* sums, hipStream_t s) {
   const int64_t n = (int64_t)NO * T;
   k_sum_chunks<<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s>>>(part, nchunk, NO, T, sums);
@@ -204,6 +289,12 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
                            int save_stats_at, hipStream_t s, const int* err) {
   if (T == 0) return hipSuccess;
   const int NO = (int)out_blocks(nout) * 16 + 2;
+  if (k == 4 && Kq <= kMaxKr) {
+    k_pre_coef_sum<4><<<dim3((unsigned)((T + kCoefTok - 1) / kCoefTok)), dim3(kCoefTok * kCoefParts), 0, s>>>(
+        part, nchunk, NO, T, Kq, with_res, (int64_t)k * C, alpha_post, alpha_res, b_post, b_res, eps, iters, delta,
+        Hpost, Hres, saved, nsave, save_z_at, save_stats_at, err);
+    return hipGetLastError();
+  }
   hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
   if (e != hipSuccess) return e;
   k_pre_coef<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(

@@ -541,9 +541,12 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   }
 }
 
-__global__ void k_zero_ints(int* p, int n) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0;
+// zero n1 and n2 16-byte words at p1 and p2 (one launch)
+__global__ void k_zero2(uint4* __restrict__ p1, int64_t n1, uint4* __restrict__ p2, int64_t n2) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const uint4 z = make_uint4(0, 0, 0, 0);
+  if (i < n1) p1[i] = z;
+  else if (i - n1 < n2) p2[i - n1] = z;
 }
 
 struct DeviceInfo {
@@ -629,13 +632,12 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
   a.teams = teams;
   a.m = d->m;
   a.eps = d->eps;
-  // records start untagged: clear the error counter and the slots in use
+  // records start untagged: clear the error counter (with the first 256
+  // bytes) and the record slots in use, both whole 16-byte words
   const size_t used1 = (size_t)teams * RING * G * FM * NV1, used2 = (size_t)teams * RING * FM * NV2;
-  k_zero_ints<<<dim3(1), dim3(64), 0, s>>>(a.err, 64);
-  k_zero_ints<<<dim3((unsigned)((2 * used1 + 255) / 256)), dim3(256), 0, s>>>(reinterpret_cast<int*>(a.rec1),
-                                                                           (int)(2 * used1));
-  k_zero_ints<<<dim3((unsigned)((2 * used2 + 255) / 256)), dim3(256), 0, s>>>(reinterpret_cast<int*>(a.rec2),
-                                                                           (int)(2 * used2));
+  const int64_t n1 = (int64_t)((256 + used1 * 8) / 16), n2 = (int64_t)((used2 * 8 + 15) / 16);
+  k_zero2<<<dim3((unsigned)((n1 + n2 + 255) / 256)), dim3(256), 0, s>>>(reinterpret_cast<uint4*>(w), n1,
+                                                                        reinterpret_cast<uint4*>(a.rec2), n2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   void* args[] = {&a};
