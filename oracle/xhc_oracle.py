@@ -20,7 +20,10 @@ register in the design notes; each is repeated at the line that uses it):
 * Routing: slots 0..m-1 hold the fixed streams 0..m-1 (p = 1); slots
   m..k-1 hold the k-m streams among m..N-1 with the largest router logit,
   in descending logit order, ties to the lower stream index (eq:router_topk;
-  sigma is monotone, so ordering logits orders the scores).
+  sigma is monotone, so ordering logits orders the scores).  The softmax
+  router of the ablation table (row 11) replaces sigma by a softmax over all
+  N logits (the projection scores every stream); it is monotone too, so the
+  selection is the same and only p changes.
 * Sinkhorn: each iteration normalises rows, then columns (eq:mhc_sinkhorn,
   20 iterations per the hyperparameter table); afterwards each row i is
   divided by its sum s_i when s_i > 1 + clamp_delta (the row-sum clamp of
@@ -66,6 +69,17 @@ def sigmoid(z: torch.Tensor) -> torch.Tensor:
     return 1.0 / (1.0 + torch.exp(-z))
 
 
+def router_scores(z_r: torch.Tensor, router: str = "sigmoid") -> torch.Tensor:
+    """Per-stream router scores s from the logits z_r [T, N]: sigma
+    (eq:router) or, for the ablation (ablation table, row 11), a softmax over
+    the N streams of each token.  Parity: pinned (see tests)."""
+    if router == "sigmoid":
+        return sigmoid(z_r)
+    if router == "softmax":
+        return torch.softmax(z_r, dim=1)
+    raise ValueError(router)
+
+
 def layer_norm(x: torch.Tensor, eps: float) -> torch.Tensor:
     """LayerNorm over the last axis, biased variance, no affine (eq:router)."""
     mu = x.mean(-1, keepdim=True)
@@ -106,8 +120,9 @@ def post_mapping(z_post: torch.Tensor, alpha_post, b_post, k: int, Kr: int) -> t
     return (2.0 * sigmoid(alpha_post * z_post + b_post)).reshape(T, k, Kr)
 
 
-def route(z_r: torch.Tensor, m: int, k: int):
-    """Fixed-plus-TopK routing (eq:router_topk).
+def route(z_r: torch.Tensor, m: int, k: int, router: str = "sigmoid"):
+    """Fixed-plus-TopK routing (eq:router_topk); ``router`` picks the score
+    function (see router_scores).
 
     Returns (idx [T,k] int64, p [T,k] fp64, gap [T] fp64).  ``gap`` is the
     smallest difference between neighbouring logits in the sorted routed
@@ -127,7 +142,7 @@ def route(z_r: torch.Tensor, m: int, k: int):
         srt = torch.gather(cand, 1, order[:, :n_look])
         if n_look > 1:
             gap = (srt[:, :-1] - srt[:, 1:]).min(dim=1).values
-    s = sigmoid(z_r)
+    s = router_scores(z_r, router)
     p = torch.ones(T, k, dtype=F64)
     if k > m:
         p[:, m:] = torch.gather(s, 1, idx[:, m:])
@@ -194,7 +209,7 @@ def augmented_output(F, conv_w, kappa, S, tokens, gram_schmidt_on=True) -> list:
 # --------------------------------------------------------------------------
 
 def xhc_pre(X, W_r, W_pre, W_res, W_post, alpha, b_pre, b_res, b_post, *,
-            m, k, Kr, eps=1e-5, sinkhorn_iters=20, clamp_delta=1e-6):
+            m, k, Kr, eps=1e-5, sinkhorn_iters=20, clamp_delta=1e-6, router="sigmoid"):
     """Mapping generation + dense read of one xHC sublayer.
 
     X: [T, N, C] float64 holding the exact state values.  W_r, W_pre: [N*C, N]
@@ -210,7 +225,7 @@ def xhc_pre(X, W_r, W_pre, W_res, W_post, alpha, b_pre, b_res, b_post, *,
     z_r = layer_norm(x, eps) @ bf16_operand(W_r)              # router logits
     z_pre = rms_norm(x, eps) @ bf16_operand(W_pre)
     Hpre = sigmoid(a_pre * z_pre + torch.as_tensor(b_pre, dtype=F64))
-    idx, p, gap = route(z_r, m, k)
+    idx, p, gap = route(z_r, m, k, router)
     act = gather_rows(X, idx)                                 # [T, k, C]
     a_n = rms_norm(act.reshape(T, k * C), eps)                # vec, slot-major
     z_res = a_n @ bf16_operand(W_res)
@@ -286,7 +301,8 @@ def flash_sublayer_kind(q: int) -> str:
 def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list,
                     alpha_pre, b_pre, alpha_post, b_post, alpha_res, b_res, *,
                     m, k, S, kappa=(4, 8, 12), eps=1e-5, sinkhorn_iters=20,
-                    clamp_delta=1e-6, round_state=True, gram_schmidt_on=True, tokens=None):
+                    clamp_delta=1e-6, round_state=True, gram_schmidt_on=True, tokens=None,
+                    router="sigmoid"):
     """One xHC-Flash sharing group of Q = len(F_list) sublayers (Q = 2 or 4).
 
     Shared routing and Q pre-mappings come from the group-entry state X0
@@ -321,7 +337,7 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
         sigmoid(alpha_pre[q] * (xr @ bf16_operand(W_pre_list[q])) +
                 torch.as_tensor(b_pre[q], dtype=F64))
         for q in range(Q)])
-    idx, p, gap = route(z_r, m, k)
+    idx, p, gap = route(z_r, m, k, router)
     active = torch.zeros(T, N, dtype=torch.bool)
     active[torch.arange(T)[:, None], idx] = True
     inputs = [torch.einsum("tn,tnc->tc", Hpre[0], X0)]
@@ -381,7 +397,7 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
 
 def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in, *,
                        m, k, Kr, S, kappa=(4, 8, 12), eps=1e-5, sinkhorn_iters=20,
-                       clamp_delta=1e-6, gram_schmidt_on=True, tokens=None):
+                       clamp_delta=1e-6, gram_schmidt_on=True, tokens=None, router="sigmoid"):
     """L = <G_X, X'> + <G_in, input> for one full xHC sublayer, float64.
 
     Same steps as xhc_pre followed by xhc_post, except that the projection
@@ -396,7 +412,7 @@ def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in
     z_r = layer_norm(x, eps) @ Wr
     Hpre = sigmoid(al[0] * (rms_norm(x, eps) @ Wp) + bp)
     idx, _, _ = route(z_r.detach(), m, k)       # piecewise constant decision
-    s = sigmoid(z_r)
+    s = router_scores(z_r, router)
     p = torch.ones(T, k, dtype=F64)
     if k > m:
         p = torch.cat([p[:, :m], torch.gather(s, 1, idx[:, m:])], dim=1)

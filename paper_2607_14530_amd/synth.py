@@ -35,6 +35,7 @@ class Workload:
     state: str = "bf16"             # "bf16" or "f32"
     alpha: tuple = (0.01, 0.01, 0.01)
     name: str = ""
+    router: str = "sigmoid"         # "sigmoid" (eq:router) or "softmax" (ablation)
 
     def __post_init__(self):
         if self.S == 0:

@@ -9,9 +9,9 @@ from paper_2607_14530_amd import synth
 F64 = torch.float64
 
 
-def _setup(N, Kr, stress, seed):
+def _setup(N, Kr, stress, seed, router="sigmoid"):
     w = synth.Workload(T=8, S=8, N=N, k=4, m=2, C=32, Kr=Kr,
-                       alpha=(0.5, 1.0, 0.5) if stress else (0.01, 0.01, 0.01))
+                       alpha=(0.5, 1.0, 0.5) if stress else (0.01, 0.01, 0.01), router=router)
     d = synth.sublayer_inputs(w, seed, grads=True, bias_std=2.0 if stress else 0.0)
     vals = {
         "X": d["X"].to(F64), "F": d["F"].to(F64),
@@ -28,16 +28,17 @@ def _objective(w, d, vals):
     return O.sublayer_objective(
         vals["X"], vals["F"], vals["conv_w"], vals["W_r"], vals["W_pre"], vals["W_res"],
         vals["W_post"], vals["alpha"], vals["b_pre"], vals["b_res"], vals["b_post"],
-        d["G_X"], d["G_in"], m=w.m, k=w.k, Kr=w.Kr, S=w.S)
+        d["G_X"], d["G_in"], m=w.m, k=w.k, Kr=w.Kr, S=w.S, router=w.router)
 
 
-@pytest.mark.parametrize("N,Kr,stress,seed", [(4, 4, False, 0), (8, 4, False, 1),
-                                               (8, 1, False, 2), (8, 4, True, 3)])
-def test_backward_matches_central_differences(N, Kr, stress, seed):
-    w, d, vals = _setup(N, Kr, stress, seed)
+@pytest.mark.parametrize("N,Kr,stress,seed,router", [(4, 4, False, 0, "sigmoid"), (8, 4, False, 1, "sigmoid"),
+                                                      (8, 1, False, 2, "sigmoid"), (8, 4, True, 3, "sigmoid"),
+                                                      (8, 4, True, 4, "softmax")])
+def test_backward_matches_central_differences(N, Kr, stress, seed, router):
+    w, d, vals = _setup(N, Kr, stress, seed, router)
     g = O.xhc_sublayer_grads(d["X"], d["F"], d["conv_w"], d["W_r"], d["W_pre"], d["W_res"],
                              d["W_post"], d["alpha"], d["b_pre"], d["b_res"], d["b_post"],
-                             d["G_X"], d["G_in"], m=w.m, k=w.k, Kr=w.Kr, S=w.S)
+                             d["G_X"], d["G_in"], m=w.m, k=w.k, Kr=w.Kr, S=w.S, router=w.router)
     gen = torch.Generator().manual_seed(100 + seed)
     for name in O.GRAD_NAMES:
         if vals[name] is None:

@@ -370,3 +370,33 @@ def test_flash_untouched_rows_are_never_written():
     act = torch.zeros(w.T, w.N, dtype=torch.bool)
     act[torch.arange(w.T)[:, None], out["idx"]] = True
     assert torch.equal(out["X"][~act], d["X"].to(F64)[~act])
+
+
+def test_softmax_router_hand_example():
+    """Softmax router (ablation table, row 11): TopK over the non-fixed streams
+    is unchanged, p of a routed slot is exp(z_i) / sum over all N of exp(z)."""
+    import math
+    z = [0.3, -1.2, 2.0, 0.5, 1.1]
+    idx, p, _ = O.route(torch.tensor([z], dtype=F64), m=1, k=3, router="softmax")
+    assert idx.tolist() == [[0, 2, 4]]
+    den = sum(math.exp(v) for v in z)
+    expect = [1.0, math.exp(2.0) / den, math.exp(1.1) / den]
+    assert max(abs(a - b) for a, b in zip(p[0].tolist(), expect)) < 1e-15
+    idx_s, _, _ = O.route(torch.tensor([z], dtype=F64), m=1, k=3, router="sigmoid")
+    assert torch.equal(idx, idx_s)
+
+
+def test_softmax_router_invariants():
+    """Equal logits give p = 1/N on routed slots; the routed p of a token never
+    exceed 1 together with the unselected streams' mass; shifting every logit
+    of a token leaves p unchanged (a softmax property the sigmoid lacks)."""
+    T, N, m, k = 3, 8, 2, 5
+    idx, p, _ = O.route(torch.zeros(T, N, dtype=F64), m, k, router="softmax")
+    assert torch.allclose(p[:, m:], torch.full((T, k - m), 1.0 / N, dtype=F64), atol=0, rtol=1e-15)
+    assert idx[:, m:].tolist() == [[2, 3, 4]] * T
+    gen = torch.Generator().manual_seed(5)
+    z = torch.randn(T, N, generator=gen, dtype=F64)
+    _, p1, _ = O.route(z, m, k, router="softmax")
+    _, p2, _ = O.route(z + 3.25, m, k, router="softmax")
+    assert torch.allclose(p1, p2, atol=1e-15, rtol=0)
+    assert bool((p1[:, m:].sum(1) < 1.0).all())
