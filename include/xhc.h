@@ -57,7 +57,7 @@ typedef enum { XHC_BF16 = 0, XHC_F32 = 1 } xhc_dtype;
  * kappa = {4, 8, 12}, 20 Sinkhorn iterations).  Constraints:
  *   T >= 0, S >= 1, T % S == 0;  1 <= k <= N <= 64;  0 <= m <= k;  k <= 8;
  *   C >= 32, C % 32 == 0;  Kr in 1..4;  kappa[j] in 1..16 for j < Kr - 1;
- *   sinkhorn_iters in 0..1000;  eps > 0;  clamp_delta >= 0.               */
+ *   sinkhorn_iters in 0..1000;  eps > 0;  clamp_delta >= 0;  router 0 or 1. */
 typedef struct xhc_dims {
   int64_t T;              /* tokens                                              */
   int64_t S;              /* tokens per sequence (causal conv window resets)     */
@@ -73,7 +73,14 @@ typedef struct xhc_dims {
   float clamp_delta;      /* row clamp applies when a row sum exceeds 1 + delta  */
   int32_t state_dtype;    /* xhc_dtype of X, F, input, base                      */
   int32_t impl;           /* xhc_impl: which kernels run (same results)          */
+  int32_t router;         /* xhc_router: score function of the router            */
 } xhc_dims;
+
+/* Router score function.  SIGMOID is eq:router; SOFTMAX is the ablation of
+ * the ablation table (row 11): a softmax over all N router logits of a token.
+ * Both are monotone, so TopK selects the same streams; p of a routed slot is
+ * the stream's score.                                                      */
+typedef enum { XHC_ROUTER_SIGMOID = 0, XHC_ROUTER_SOFTMAX = 1 } xhc_router;
 
 /* Kernel selection for xhc_pre.  AUTO takes the single-pass cooperative
  * kernel where it applies (bf16 state, N = 16, k = 4, C = 128 G with G

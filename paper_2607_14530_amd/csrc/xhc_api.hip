@@ -27,6 +27,7 @@ xhc_status check_dims(const xhc_dims* d) {
     return XHC_EINVAL;
   if (d->state_dtype != XHC_BF16 && d->state_dtype != XHC_F32) return XHC_EINVAL;
   if (d->impl < XHC_IMPL_AUTO || d->impl > XHC_IMPL_FUSED) return XHC_EINVAL;
+  if (d->router != XHC_ROUTER_SIGMOID && d->router != XHC_ROUTER_SOFTMAX) return XHC_EINVAL;
   if (d->N > kMaxN || d->k > kMaxK || d->Kr > kMaxKr || d->sinkhorn_iters > 1000) return XHC_EUNSUPPORTED;
   if (d->C % 32 != 0) return XHC_EUNSUPPORTED;
   for (int j = 0; j < d->Kr - 1; ++j)
@@ -257,7 +258,7 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
                                             nullptr, d->k, part, s));
   XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(d->state_dtype, false, NC, d->C, nout_full, d->T), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,
                                          alpha, 1, b_pre, d->eps, idx, p, Hpre, sums, saved, nsave,
-                                         nsave - 4, s));
+                                         nsave - 4, d->router, s));
   XHC_STEP("proj_active", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act, nout_act, idx,
                                               d->k, part, s));
   XHC_STEP("pre_coef", launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, nout_act, d->T), nout_act,
@@ -333,7 +334,8 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
   XHC_STEP("flash_proj_full",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nf, nullptr, d->k, part, s));
   XHC_STEP("flash_route", launch_pre_route(part, proj_chunks(d->state_dtype, false, NC, d->C, nf, d->T), nf, d->T, d->N, d->m, d->k, Q, d->C, colsum,
-                                           alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, nullptr, 0, 0, s));
+                                           alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, nullptr, 0, 0,
+                                           d->router, s));
   XHC_STEP("flash_proj_active",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act1, na, idx, d->k, part, s));
   XHC_STEP("flash_coef1", launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, na, d->T), na, d->T,

@@ -629,7 +629,7 @@ __global__ __launch_bounds__(kPreTokThreads) void k_bwd_pre_token(
     const float* __restrict__ b_res, const int32_t* __restrict__ idx, const float* __restrict__ p,
     const float* __restrict__ Hpre, const float* __restrict__ Hpost, const float* __restrict__ dHres,
     const float* __restrict__ dHpost, const float* __restrict__ dp, float eps, int iters, float delta,
-    float* __restrict__ tok, float* __restrict__ pg) {
+    float* __restrict__ tok, float* __restrict__ pg, int softmax) {
   __shared__ float sk[KC > 0 ? kSkMaxSteps * KC * kPreTokThreads : 1];
   const int k = KC > 0 ? KC : k_rt;
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -657,16 +657,33 @@ __global__ __launch_bounds__(kPreTokThreads) void k_bwd_pre_token(
     bp += a_pre * ds * z;
   }
   const float beta_pre = r * r * bp / NC;
-  // router: only routed slots carry gradient, through p = sigma(z_r)
+  // router: only routed slots carry gradient, through p = sigma(z_r); with the
+  // softmax router p = s_i of s = softmax(z_r) over the N streams, so every
+  // logit gets dz_i = s_i (g_i - sum_l s_l g_l), g_i = dp of the slot of i
   for (int i = 0; i < N; ++i) tk[i] = 0.f;
   float m1 = 0.f, m2 = 0.f;
-  for (int j = m; j < k; ++j) {
-    const int i = idx[t * k + j];
-    const float pj = p[t * k + j];
-    const float dz = dp[t * k + j] * pj * (1.0f - pj);
-    tk[i] = dz;
-    m1 += colsum[i] * dz;
-    m2 += sv[i] * dz;
+  if (!softmax) {
+    for (int j = m; j < k; ++j) {
+      const int i = idx[t * k + j];
+      const float pj = p[t * k + j];
+      const float dz = dp[t * k + j] * pj * (1.0f - pj);
+      tk[i] = dz;
+      m1 += colsum[i] * dz;
+      m2 += sv[i] * dz;
+    }
+  } else if (k > m) {
+    float mx = sv[0];
+    for (int i = 1; i < N; ++i) mx = fmaxf(mx, sv[i]);
+    float den = 0.f;
+    for (int i = 0; i < N; ++i) den += __expf(sv[i] - mx);
+    float dot = 0.f;
+    for (int j = m; j < k; ++j) dot += p[t * k + j] * dp[t * k + j];
+    for (int i = 0; i < N; ++i) tk[i] = -(__expf(sv[i] - mx) / den) * dot;
+    for (int j = m; j < k; ++j) tk[idx[t * k + j]] += p[t * k + j] * dp[t * k + j];
+    for (int i = 0; i < N; ++i) {
+      m1 += colsum[i] * tk[i];
+      m2 += sv[i] * tk[i];
+    }
   }
   m1 /= NC;
   m2 /= NC;
@@ -1251,11 +1268,13 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     if (k == 4 && 2 * d->sinkhorn_iters <= kSkMaxSteps)
       k_bwd_pre_token<4><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
                                           Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
-                                          d->clamp_delta, tok, pg);
+                                          d->clamp_delta, tok, pg,
+                                          d->router == XHC_ROUTER_SOFTMAX ? 1 : 0);
     else
       k_bwd_pre_token<0><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
                                           Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
-                                          d->clamp_delta, tok, pg);
+                                          d->clamp_delta, tok, pg,
+                                          d->router == XHC_ROUTER_SOFTMAX ? 1 : 0);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

@@ -146,10 +146,12 @@ __device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + __exp
 // streams 0..m-1 with p = 1; slot j >= m takes the largest remaining logit
 // among streams m..N-1, ties to the lower index.  A NaN logit never wins a
 // comparison; a slot whose candidates all compare false takes the lowest free
-// stream, so every index stays in range.
+// stream, so every index stays in range.  p of a routed slot is sigma(z)
+// (eq:router) or, with `softmax`, exp(z - max) / sum over the N streams of
+// exp(z - max) (the softmax-router ablation).
 template <int NMAX>
 __device__ __forceinline__ void route_token(const float (&z)[NMAX], int N, int m, int k,
-                                            int32_t* idx_out, float* p_out) {
+                                            int32_t* idx_out, float* p_out, bool softmax = false) {
   uint64_t used = 0;
   for (int j = 0; j < m; ++j) {
     idx_out[j] = j;
@@ -166,7 +168,18 @@ __device__ __forceinline__ void route_token(const float (&z)[NMAX], int N, int m
     }
     used |= 1ull << best;
     idx_out[j] = best;
-    p_out[j] = sigmoidf(bz);
+    p_out[j] = softmax ? bz : sigmoidf(bz);   // softmax: the logit until the sum is known
+  }
+  if (softmax && k > m) {
+    float mx = z[0];
+#pragma unroll
+    for (int i = 1; i < NMAX; ++i)
+      if (i < N) mx = fmaxf(mx, z[i]);
+    float den = 0.f;
+#pragma unroll
+    for (int i = 0; i < NMAX; ++i)
+      if (i < N) den += __expf(z[i] - mx);
+    for (int j = m; j < k; ++j) p_out[j] = __expf(p_out[j] - mx) / den;
   }
 }
 

@@ -88,6 +88,7 @@ struct FusedArgs {
   int teams;
   int m;
   float eps;
+  int softmax;            // softmax router (ablation) instead of sigma
 };
 
 struct Smem {
@@ -301,10 +302,22 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
       }
       int slot = -1;
       float pv = 1.0f;
+      float sc = sigmoidf(z);
+      if (a.softmax) {
+        // softmax over the 16 logits (lanes 0..15)
+        float mx = lane_value(z, 0);
+#pragma unroll
+        for (int i = 1; i < FN; ++i) mx = fmaxf(mx, lane_value(z, i));
+        const float ez = __expf(z - mx);
+        float den = 0.f;
+#pragma unroll
+        for (int i = 0; i < FN; ++i) den += lane_value(ez, i);
+        sc = ez / den;
+      }
       if (lane < a.m) slot = lane;
       else if (lane < FN && rank < FK - a.m) {
         slot = a.m + rank;
-        pv = sigmoidf(z);
+        pv = sc;
       }
       if (a.saved && tg < a.T) {
         float* sv = a.saved + tg * a.nsave;
@@ -632,6 +645,7 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
   a.teams = teams;
   a.m = d->m;
   a.eps = d->eps;
+  a.softmax = d->router == XHC_ROUTER_SOFTMAX ? 1 : 0;
   // records start untagged: clear the error counter (with the first 256
   // bytes) and the record slots in use, both whole 16-byte words
   const size_t used1 = (size_t)teams * RING * G * FM * NV1, used2 = (size_t)teams * RING * FM * NV2;

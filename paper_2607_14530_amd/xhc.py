@@ -26,6 +26,7 @@ XHC_OK, XHC_EINVAL, XHC_EUNSUPPORTED, XHC_EWORKSPACE, XHC_EHIP = range(5)
 STATUS_NAMES = {0: "XHC_OK", 1: "XHC_EINVAL", 2: "XHC_EUNSUPPORTED", 3: "XHC_EWORKSPACE", 4: "XHC_EHIP"}
 XHC_BF16, XHC_F32 = 0, 1
 XHC_IMPL_AUTO, XHC_IMPL_MULTI, XHC_IMPL_FUSED = 0, 1, 2
+XHC_ROUTER_SIGMOID, XHC_ROUTER_SOFTMAX = 0, 1
 XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST, XHC_OP_POST_BWD, XHC_OP_PRE_BWD = range(6)
 
 
@@ -42,12 +43,12 @@ class Dims(ctypes.Structure):
         ("Kr", ctypes.c_int32), ("kappa", ctypes.c_int32 * 3),
         ("sinkhorn_iters", ctypes.c_int32), ("gram_schmidt", ctypes.c_int32),
         ("eps", ctypes.c_float), ("clamp_delta", ctypes.c_float), ("state_dtype", ctypes.c_int32),
-        ("impl", ctypes.c_int32),
+        ("impl", ctypes.c_int32), ("router", ctypes.c_int32),
     ]
 
 
 def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, gram_schmidt=1,
-              eps=1e-5, clamp_delta=1e-6, state="bf16", impl=XHC_IMPL_AUTO) -> Dims:
+              eps=1e-5, clamp_delta=1e-6, state="bf16", impl=XHC_IMPL_AUTO, router="sigmoid") -> Dims:
     d = Dims()
     d.T, d.S = T, (S if S else max(T, 1))
     d.N, d.k, d.m, d.C, d.Kr = N, k, m, C, Kr
@@ -57,11 +58,13 @@ def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, 
     d.eps, d.clamp_delta = eps, clamp_delta
     d.state_dtype = XHC_BF16 if state == "bf16" else XHC_F32
     d.impl = impl
+    d.router = XHC_ROUTER_SOFTMAX if router in ("softmax", XHC_ROUTER_SOFTMAX) else XHC_ROUTER_SIGMOID
     return d
 
 
 def dims_for(w, **kw) -> Dims:
     """Dims of a synth.Workload."""
+    kw.setdefault("router", getattr(w, "router", "sigmoid"))
     return make_dims(w.T, w.N, w.k, w.m, w.C, Kr=w.Kr, S=w.S, kappa=w.kappa, state=w.state, **kw)
 
 

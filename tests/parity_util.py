@@ -61,7 +61,7 @@ def oracle_pre(inp, w, tokens=None):
     X = inp["X"] if tokens is None else inp["X"][tokens]
     return O.xhc_pre(X.to("cpu", F64), inp["W_r"].cpu(), inp["W_pre"].cpu(), inp["W_res"].cpu(),
                      inp["W_post"].cpu(), tuple(inp["alpha"].cpu().tolist()), inp["b_pre"].cpu(),
-                     inp["b_res"].cpu(), inp["b_post"].cpu(), m=w.m, k=w.k, Kr=w.Kr)
+                     inp["b_res"].cpu(), inp["b_post"].cpu(), m=w.m, k=w.k, Kr=w.Kr, router=w.router)
 
 
 def oracle_post(inp, w, ref, tokens=None, X_before=None):

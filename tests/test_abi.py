@@ -72,6 +72,21 @@ def test_invalid_dims_rejected_before_launch(kw, status):
     assert _post_status(d, conv=False) == status
 
 
+def test_unknown_router_rejected():
+    d = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=1, S=64)
+    d.router = 2
+    assert _pre_status(d) == X.XHC_EINVAL
+
+
+def test_dims_struct_fields_match_header():
+    """The binding's xhc_dims fields follow the header's, in order."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", open(X.HEADER).read(), flags=re.S)
+    body = re.search(r"typedef struct xhc_dims \{(.*?)\} xhc_dims;", text, flags=re.S).group(1)
+    names = re.findall(r"\b(\w+)\s*(?:\[\d+\])?\s*;", body)
+    assert names == [f[0] for f in X.Dims._fields_]
+
+
 def test_null_pointer_and_workspace_errors():
     d = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=1)
     for i in range(14):

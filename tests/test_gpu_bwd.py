@@ -44,7 +44,7 @@ def _oracle(w, inp):
     return O.xhc_sublayer_grads(c(inp["X"]).double(), c(inp["F"]).double(), c(inp["conv_w"]), c(inp["W_r"]),
                                 c(inp["W_pre"]), c(inp["W_res"]), c(inp["W_post"]), c(inp["alpha"]),
                                 c(inp["b_pre"]), c(inp["b_res"]), c(inp["b_post"]), c(inp["G_X"]),
-                                c(inp["G_in"]), m=w.m, k=w.k, Kr=w.Kr, S=w.S, kappa=w.kappa)
+                                c(inp["G_in"]), m=w.m, k=w.k, Kr=w.Kr, S=w.S, kappa=w.kappa, router=w.router)
 
 
 CASES = [
@@ -54,6 +54,8 @@ CASES = [
     W(T=40, S=20, N=8, k=4, m=2, C=512, Kr=4, name="bwd-mlp-N8"),
     W(T=32, S=32, N=32, k=4, m=2, C=256, Kr=1, name="bwd-attn-N32"),
     W(T=64, S=64, N=16, k=4, m=2, C=256, Kr=4, alpha=(0.5, 1.0, 0.5), name="bwd-mlp-stress"),
+    W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, router="softmax", name="bwd-mlp-softmax"),
+    W(T=40, S=20, N=8, k=4, m=1, C=512, Kr=1, router="softmax", name="bwd-attn-softmax-N8"),
 ]
 
 
