@@ -36,6 +36,7 @@ class Workload:
     alpha: tuple = (0.01, 0.01, 0.01)
     name: str = ""
     router: str = "sigmoid"         # "sigmoid" (eq:router) or "softmax" (ablation)
+    gram_schmidt: int = 1           # 0: components used as they are (the Muon-trained variant)
 
     def __post_init__(self):
         if self.S == 0:

@@ -65,6 +65,7 @@ def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, 
 def dims_for(w, **kw) -> Dims:
     """Dims of a synth.Workload."""
     kw.setdefault("router", getattr(w, "router", "sigmoid"))
+    kw.setdefault("gram_schmidt", getattr(w, "gram_schmidt", 1))
     return make_dims(w.T, w.N, w.k, w.m, w.C, Kr=w.Kr, S=w.S, kappa=w.kappa, state=w.state, **kw)
 
 

@@ -71,7 +71,7 @@ def oracle_post(inp, w, ref, tokens=None, X_before=None):
     Xb = (inp["X"][tokens] if X_before is None else X_before).to("cpu", F64)
     conv = inp["conv_w"].cpu() if inp["conv_w"] is not None else None
     return O.xhc_post(Xb, inp["F"].cpu(), conv, ref["idx"], ref["p"], ref["Hres"], ref["Hpost"],
-                      S=w.S, kappa=w.kappa, tokens=tokens.cpu())
+                      S=w.S, kappa=w.kappa, tokens=tokens.cpu(), gram_schmidt_on=bool(w.gram_schmidt))
 
 
 def check_sublayer(sub, inp, w, X_before, X_after, tokens=None):

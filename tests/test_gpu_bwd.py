@@ -44,7 +44,8 @@ def _oracle(w, inp):
     return O.xhc_sublayer_grads(c(inp["X"]).double(), c(inp["F"]).double(), c(inp["conv_w"]), c(inp["W_r"]),
                                 c(inp["W_pre"]), c(inp["W_res"]), c(inp["W_post"]), c(inp["alpha"]),
                                 c(inp["b_pre"]), c(inp["b_res"]), c(inp["b_post"]), c(inp["G_X"]),
-                                c(inp["G_in"]), m=w.m, k=w.k, Kr=w.Kr, S=w.S, kappa=w.kappa, router=w.router)
+                                c(inp["G_in"]), m=w.m, k=w.k, Kr=w.Kr, S=w.S, kappa=w.kappa, router=w.router,
+                                gram_schmidt_on=bool(w.gram_schmidt))
 
 
 CASES = [
@@ -56,6 +57,8 @@ CASES = [
     W(T=64, S=64, N=16, k=4, m=2, C=256, Kr=4, alpha=(0.5, 1.0, 0.5), name="bwd-mlp-stress"),
     W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, router="softmax", name="bwd-mlp-softmax"),
     W(T=40, S=20, N=8, k=4, m=1, C=512, Kr=1, router="softmax", name="bwd-attn-softmax-N8"),
+    W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, gram_schmidt=0, name="bwd-mlp-gs-off"),
+    W(T=48, S=24, N=4, k=2, m=1, C=256, Kr=4, name="bwd-preset-N4-k2-m1"),
 ]
 
 

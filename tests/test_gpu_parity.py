@@ -33,6 +33,13 @@ SMALL = [
     # softmax router (ablation): both pre implementations, and N = 8 with m = 1
     W(T=256, S=128, N=16, k=4, m=2, C=1024, Kr=4, router="softmax", name="softmax-router-C1024"),
     W(T=96, S=48, N=8, k=4, m=1, C=256, Kr=1, router="softmax", name="softmax-router-N8"),
+    # Gram-Schmidt off (the Muon-trained variant) on both pre paths; the
+    # (N, k, m) presets of the scaling study and k = 2
+    W(T=128, S=64, N=16, k=4, m=2, C=512, Kr=4, gram_schmidt=0, name="gs-off"),
+    W(T=64, S=32, N=2, k=1, m=0, C=256, Kr=4, name="preset-N2-k1-m0"),
+    W(T=64, S=32, N=4, k=2, m=1, C=512, Kr=1, name="preset-N4-k2-m1"),
+    W(T=64, S=32, N=8, k=4, m=2, C=256, Kr=4, name="preset-N8-k4-m2"),
+    W(T=64, S=32, N=16, k=2, m=1, C=256, Kr=4, name="k2-N16"),
 ]
 
 
