@@ -159,6 +159,25 @@ def extra_sections(dev, stream, iters=5):
                      "paper_bytes_per_token_C": 34.0}
     del sub, inp, st
     torch.cuda.empty_cache()
+    # prefill-latency regime: one 2048-token sequence through an attention-type
+    # and an MLP-type sublayer (forward), for each pre implementation
+    pre_ms = {}
+    for name, impl in (("auto", X.XHC_IMPL_AUTO), ("multi", X.XHC_IMPL_MULTI), ("fused", X.XHC_IMPL_FUSED)):
+        wa = synth.Workload(T=2048, S=2048, N=16, k=4, m=2, C=4096, Kr=1, name="prefill-attn")
+        wm = synth.Workload(T=2048, S=2048, N=16, k=4, m=2, C=4096, Kr=4, name="prefill-mlp")
+        ia, im = synth.sublayer_inputs(wa, 11, device=dev), synth.sublayer_inputs(wm, 12, device=dev)
+        sa = X.Sublayer(X.dims_for(wa, impl=impl), ia, dev)
+        sm = X.Sublayer(X.dims_for(wm, impl=impl), im, dev)
+        st = ia["X"]
+        pre_ms[name] = _time(lambda: (sa.pre(st, stream), sa.post(st, ia["F"], stream),
+                                      sm.pre(st, stream), sm.post(st, im["F"], stream)), 20, stream)
+        del sa, sm, ia, im, st
+        torch.cuda.empty_cache()
+    out["prefill_t2048"] = {"workload": "xHC forward block (attention-type + MLP-type sublayer), one 2048-token "
+                                        "sequence, N=16, k=4, m=2, C=4096",
+                            "ms_per_block": pre_ms["auto"], "ms_per_block_multi": pre_ms["multi"],
+                            "ms_per_block_fused": pre_ms["fused"],
+                            "tokens_per_s": 2048 / (pre_ms["auto"] * 1e-3)}
     # backward, T = 8192, N = 16, k = 4, C = 4096, MLP-type
     w = synth.bwd_sweep(16, 4)
     inp = synth.sublayer_inputs(w, 10, device=dev, grads=True)
@@ -183,7 +202,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-extra", action="store_true", help="skip the Flash / mHC / backward sections")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the Flash / mHC / prefill / backward sections")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
