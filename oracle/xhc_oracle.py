@@ -395,23 +395,24 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
 # backward (reverse mode of the forward above)
 # --------------------------------------------------------------------------
 
-def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in, *,
-                       m, k, Kr, S, kappa=(4, 8, 12), eps=1e-5, sinkhorn_iters=20,
-                       clamp_delta=1e-6, gram_schmidt_on=True, tokens=None, router="sigmoid"):
-    """L = <G_X, X'> + <G_in, input> for one full xHC sublayer, float64.
+def sublayer_forward(Xv, F, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, *, m, k, Kr, S, kappa=(4, 8, 12),
+                     eps=1e-5, sinkhorn_iters=20, clamp_delta=1e-6, gram_schmidt_on=True, tokens=None,
+                     router="sigmoid"):
+    """One full xHC sublayer (Alg. "Forward pass of one xHC sublayer"), float64.
 
     Same steps as xhc_pre followed by xhc_post, except that the projection
     weights are taken as given (already the bf16 operand values), so that a
-    finite-difference probe can perturb them.  ``al`` = (alpha_pre,
-    alpha_res, alpha_post).  With ``tokens`` (positions in the batch), Xv,
-    G_X and G_in hold only those tokens while Fv is the whole batch.
-    Returns (L, forward results dict).
+    finite-difference probe can perturb them.  ``F`` is the sublayer output
+    [T, C], or a callable that forms it from the dense-read input.  ``al`` =
+    (alpha_pre, alpha_res, alpha_post).  With ``tokens`` (positions in the
+    batch), Xv holds only those tokens while F is the whole batch.  Returns
+    (X after the write-back, forward results dict).
     """
     T, N, C = Xv.shape
     x = Xv.reshape(T, N * C)
     z_r = layer_norm(x, eps) @ Wr
     Hpre = sigmoid(al[0] * (rms_norm(x, eps) @ Wp) + bp)
-    idx, _, _ = route(z_r.detach(), m, k)       # piecewise constant decision
+    idx, _, gap = route(z_r.detach(), m, k)       # piecewise constant decision
     s = router_scores(z_r, router)
     p = torch.ones(T, k, dtype=F64)
     if k > m:
@@ -420,11 +421,77 @@ def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in
     Hres = residual_mapping(a_n @ Wre, al[1], bre, k, sinkhorn_iters, clamp_delta)
     Hpost = post_mapping(a_n @ Wpo, al[2], bpo, k, Kr)
     inp = torch.einsum("tn,tnc->tc", Hpre, Xv)
+    Fv = F(inp) if callable(F) else F
     Xn = xhc_post(Xv, Fv, cw, idx, p, Hres, Hpost, S=S, kappa=kappa,
                   gram_schmidt_on=gram_schmidt_on, tokens=tokens)
-    L = (G_X.to(F64) * Xn).sum() + (G_in.to(F64) * inp).sum()
-    fwd = dict(idx=idx, p=p, Hpre=Hpre, Hres=Hres, Hpost=Hpost, input=inp, X_new=Xn)
+    return Xn, dict(idx=idx, p=p, Hpre=Hpre, Hres=Hres, Hpost=Hpost, input=inp, X_new=Xn, out=Fv, gap=gap)
+
+
+def sublayer_objective(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, G_X, G_in, **kw):
+    """L = <G_X, X'> + <G_in, input> for one full xHC sublayer (see
+    sublayer_forward), float64.  Returns (L, forward results dict)."""
+    Xn, fwd = sublayer_forward(Xv, Fv, cw, Wr, Wp, Wre, Wpo, al, bp, bre, bpo, **kw)
+    L = (G_X.to(F64) * Xn).sum() + (G_in.to(F64) * fwd["input"]).sum()
     return L, fwd
+
+
+def stream_sum(X: torch.Tensor) -> torch.Tensor:
+    """Final stream reduction (App. "Final Stream Reduction"): the N streams of
+    each token are summed before the last RMSNorm.  [T, N, C] -> [T, C].
+    Parity: pinned (see tests)."""
+    return X.sum(dim=1)
+
+
+STACK_WEIGHTS = ("conv_w", "W_r", "W_pre", "W_res", "W_post", "alpha", "b_pre", "b_res", "b_post")
+
+
+def stack_objective(X0, layers, G_out, *, S, round_state=True):
+    """L = <G_out, stream_sum(X_L)> after L sublayers chained on one state,
+    float64.  Sublayer l reads the state sublayer l - 1 wrote (Alg. "Forward
+    pass of one xHC sublayer" per layer); with ``round_state`` each written
+    state is rounded to bfloat16, the stored precision.
+
+    layers[l] is a dict of STACK_WEIGHTS (weights already the bf16 operand
+    values; conv_w None for K_r = 1), 'fn' (callable: dense-read input [T, C]
+    -> sublayer output [T, C]) and the shape keys m, k, Kr, kappa and
+    optionally router, gram_schmidt_on.  Returns (L, per-layer forward dicts,
+    reduced output).
+    """
+    X = X0
+    fwds = []
+    for lay in layers:
+        X, fwd = sublayer_forward(
+            X, lay["fn"], lay["conv_w"], lay["W_r"], lay["W_pre"], lay["W_res"], lay["W_post"], lay["alpha"],
+            lay["b_pre"], lay["b_res"], lay["b_post"], m=lay["m"], k=lay["k"], Kr=lay["Kr"], S=S,
+            kappa=lay.get("kappa", (4, 8, 12)), router=lay.get("router", "sigmoid"),
+            gram_schmidt_on=lay.get("gram_schmidt_on", True))
+        if round_state:
+            X = round_state_bf16(X)
+        fwds.append(fwd)
+    out = stream_sum(X)
+    return (G_out.to(F64) * out).sum(), fwds, out
+
+
+def stack_grads(X0, layers, G_out, *, S, round_state=True):
+    """Gradients of stack_objective with respect to the entry state and every
+    layer's weights (reverse mode of the forward; routing piecewise constant).
+    Returns (dX0, list of per-layer dicts keyed by STACK_WEIGHTS, forward
+    dicts, reduced output).  Parity: pinned by central differences (tests)."""
+    leaf = lambda t: None if t is None else torch.as_tensor(t).detach().to(F64).clone().requires_grad_(True)
+    X0l = leaf(X0)
+    lays = []
+    for lay in layers:
+        q = dict(lay)
+        for n in STACK_WEIGHTS:
+            q[n] = leaf(lay[n])
+        lays.append(q)
+    L, fwds, out = stack_objective(X0l, lays, G_out, S=S, round_state=round_state)
+    leaves = [X0l] + [q[n] for q in lays for n in STACK_WEIGHTS if q[n] is not None]
+    grads = torch.autograd.grad(L, leaves, allow_unused=True)
+    grads = [torch.zeros_like(v) if g is None else g for g, v in zip(grads, leaves)]
+    it = iter(grads[1:])
+    per = [{n: (next(it) if q[n] is not None else None) for n in STACK_WEIGHTS} for q in lays]
+    return grads[0], per, fwds, out.detach()
 
 
 GRAD_NAMES = ("X", "F", "W_r", "W_pre", "W_res", "W_post", "alpha", "b_pre", "b_res",

@@ -400,3 +400,17 @@ def test_softmax_router_invariants():
     _, p2, _ = O.route(z + 3.25, m, k, router="softmax")
     assert torch.allclose(p1, p2, atol=1e-15, rtol=0)
     assert bool((p1[:, m:].sum(1) < 1.0).all())
+
+
+def test_stream_sum_closed_forms():
+    """App. "Final Stream Reduction": N copies of x sum to N x (up to the
+    rounding of repeated addition); a state with one
+    nonzero stream reduces to that stream; integer values sum exactly."""
+    gen = torch.Generator().manual_seed(3)
+    x = torch.randn(5, 24, generator=gen, dtype=F64)
+    assert torch.allclose(O.stream_sum(x[:, None, :].expand(5, 7, 24)), 7 * x, atol=0, rtol=4e-16)
+    X = torch.zeros(5, 7, 24, dtype=F64)
+    X[:, 3] = x
+    assert torch.equal(O.stream_sum(X), x)
+    Xi = torch.arange(2 * 3 * 4, dtype=F64).reshape(2, 3, 4)
+    assert O.stream_sum(Xi).tolist() == [[12.0, 15.0, 18.0, 21.0], [48.0, 51.0, 54.0, 57.0]]
