@@ -249,6 +249,21 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
                           const float* b_res_next, float* Hpost_next, float* Hres_next, void* workspace,
                           size_t workspace_bytes, void* stream);
 
+/* ------------------------------------------------------------ final stream reduction
+ * App. "Final Stream Reduction": before the last RMSNorm and the unembedding
+ * the N streams of each token are summed into one C-vector.
+ *
+ * xhc_stream_sum: out [T,C] = sum_{i<N} X[t,i,:] (fp32 accumulation over
+ *   i ascending, rounded to state_dtype).  Only T, N, C and state_dtype of d
+ *   are used.  X, out: 16-byte aligned, not overlapping.
+ * xhc_stream_sum_bwd: its backward, dX[t,i,:] = dout[t,:] for every i, or
+ *   dX[t,i,:] += dout[t,:] with accumulate = 1 (dX then holds a gradient
+ *   already, in state_dtype).  dout, dX: 16-byte aligned, not overlapping.
+ * Errors as for every entry point (XHC_EINVAL for NULL pointers or
+ * accumulate outside {0, 1}, XHC_EUNSUPPORTED for misaligned pointers).     */
+xhc_status xhc_stream_sum(const xhc_dims* d, const void* X, void* out, void* stream);
+xhc_status xhc_stream_sum_bwd(const xhc_dims* d, const void* dout, void* dX, int32_t accumulate, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

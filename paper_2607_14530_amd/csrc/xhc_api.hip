@@ -460,4 +460,31 @@ xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full
   return hip_status(e);
 }
 
+xhc_status xhc_stream_sum(const xhc_dims* d, const void* X, void* out, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (d->T == 0) return XHC_OK;
+  if (!X || !out || X == out) return XHC_EINVAL;
+  if (!aligned16(X) || !aligned16(out)) return XHC_EUNSUPPORTED;
+  clear_stale_error();
+  hipError_t e = hipSuccess;
+  XHC_STEP("stream_sum", launch_stream_sum(d->state_dtype, X, d->T, d->N, d->C, out,
+                                           reinterpret_cast<hipStream_t>(stream)));
+  return hip_status(e);
+}
+
+xhc_status xhc_stream_sum_bwd(const xhc_dims* d, const void* dout, void* dX, int32_t accumulate, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (accumulate != 0 && accumulate != 1) return XHC_EINVAL;
+  if (d->T == 0) return XHC_OK;
+  if (!dout || !dX || dout == dX) return XHC_EINVAL;
+  if (!aligned16(dout) || !aligned16(dX)) return XHC_EUNSUPPORTED;
+  clear_stale_error();
+  hipError_t e = hipSuccess;
+  XHC_STEP("stream_sum_bwd", launch_stream_bcast(d->state_dtype, dout, d->T, d->N, d->C, accumulate, dX,
+                                                 reinterpret_cast<hipStream_t>(stream)));
+  return hip_status(e);
+}
+
 }  // extern "C"

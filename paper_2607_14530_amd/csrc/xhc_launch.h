@@ -87,6 +87,11 @@ hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int6
 hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, int C, const float* Hpre,
                              int nmap, const int32_t* idx, int k, void* out0, void* outr, hipStream_t s);
 
+// final stream reduction and its backward (broadcast)
+hipError_t launch_stream_sum(int state_dtype, const void* X, int64_t T, int N, int C, void* out, hipStream_t s);
+hipError_t launch_stream_bcast(int state_dtype, const void* dout, int64_t T, int N, int C, int accumulate, void* dX,
+                               hipStream_t s);
+
 // ---- pre (fused single-pass path: bf16 state, N = 16, k = 4, C % 128 == 0)
 bool fused_pre_supported(const xhc_dims* d);
 size_t fused_pre_ws_bytes(const xhc_dims* d);

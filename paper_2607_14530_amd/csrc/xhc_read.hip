@@ -80,4 +80,85 @@ hipError_t launch_dense_read(int state_dtype, const void* X, int64_t T, int N, i
                                reinterpret_cast<float*>(out0), reinterpret_cast<float*>(outr), s);
 }
 
+// ----------------------------------------------------------------- final stream reduction
+// out[t, c] = sum_{i < N} X[t, i, c] (fp32, streams in order), one thread per
+// 8 channels of a token, 8 rows in flight.
+template <typename TS>
+__global__ __launch_bounds__(256) void k_stream_sum(const TS* __restrict__ X, int64_t T, int N, int C,
+                                                    TS* __restrict__ out) {
+  using R8 = Raw8<TS>;
+  constexpr int UNR = 8;
+  const int64_t cb = (C / 8 + 255) / 256;
+  const int64_t t = blockIdx.x / cb;
+  const int c = (int)((blockIdx.x % cb) * 256 + threadIdx.x) * 8;
+  if (t >= T || c >= C) return;
+  const TS* xt = X + t * N * (int64_t)C + c;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int i0 = 0; i0 < N; i0 += UNR) {
+    typename R8::raw r[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+      if (i0 + u < N) r[u] = R8::load(xt + (int64_t)(i0 + u) * C);
+#pragma unroll
+    for (int u = 0; u < UNR; ++u)
+      if (i0 + u < N) {
+        float f[8];
+        R8::unpack(r[u], f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += f[e];
+      }
+  }
+  Vec8<TS>::store(out + t * C + c, acc);
+}
+
+// dX[t, i, c] = dout[t, c] (or += with accumulate) for every stream i
+template <typename TS>
+__global__ __launch_bounds__(256) void k_stream_bcast(const TS* __restrict__ dout, int64_t T, int N, int C,
+                                                      int accumulate, TS* __restrict__ dX) {
+  const int64_t cb = (C / 8 + 255) / 256;
+  const int64_t t = blockIdx.x / cb;
+  const int c = (int)((blockIdx.x % cb) * 256 + threadIdx.x) * 8;
+  if (t >= T || c >= C) return;
+  float g[8];
+  Vec8<TS>::load(dout + t * C + c, g);
+  for (int i = 0; i < N; ++i) {
+    TS* p = dX + (t * N + i) * (int64_t)C + c;
+    float f[8];
+    if (accumulate) {
+      Vec8<TS>::load(p, f);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] += g[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = g[e];
+    }
+    Vec8<TS>::store(p, f);
+  }
+}
+
+hipError_t launch_stream_sum(int state_dtype, const void* X, int64_t T, int N, int C, void* out, hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const dim3 grid((unsigned)(T * ((C / 8 + 255) / 256)));
+  if (state_dtype == XHC_BF16)
+    k_stream_sum<uint16_t><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), T, N, C,
+                                                        reinterpret_cast<uint16_t*>(out));
+  else
+    k_stream_sum<float><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const float*>(X), T, N, C,
+                                                     reinterpret_cast<float*>(out));
+  return hipGetLastError();
+}
+
+hipError_t launch_stream_bcast(int state_dtype, const void* dout, int64_t T, int N, int C, int accumulate, void* dX,
+                               hipStream_t s) {
+  if (T == 0) return hipSuccess;
+  const dim3 grid((unsigned)(T * ((C / 8 + 255) / 256)));
+  if (state_dtype == XHC_BF16)
+    k_stream_bcast<uint16_t><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(dout), T, N, C,
+                                                          accumulate, reinterpret_cast<uint16_t*>(dX));
+  else
+    k_stream_bcast<float><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const float*>(dout), T, N, C, accumulate,
+                                                       reinterpret_cast<float*>(dX));
+  return hipGetLastError();
+}
+
 }  // namespace xhc

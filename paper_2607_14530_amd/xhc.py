@@ -85,6 +85,8 @@ _SIGS = {
     "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 17 + [ctypes.c_size_t, _P]),
     "xhc_post_bwd": (ctypes.c_int, [_D] + [_P] * 16 + [ctypes.c_size_t, _P]),
     "xhc_pre_bwd": (ctypes.c_int, [_D] + [_P] * 27 + [ctypes.c_size_t, _P]),
+    "xhc_stream_sum": (ctypes.c_int, [_D, _P, _P, _P]),
+    "xhc_stream_sum_bwd": (ctypes.c_int, [_D, _P, _P, ctypes.c_int32, _P]),
     "xhc_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "xhc_last_hip_error": (ctypes.c_char_p, []),
 }
@@ -216,6 +218,14 @@ def xhc_pre_bwd(d, X, packed_full, W_r, W_pre, W_res, W_post, alpha, b_res, save
           _ptr(d_input), _ptr(dHres), _ptr(dHpost), _ptr(dp), _ptr(dX), _ptr(dW_r), _ptr(dW_pre), _ptr(dW_res),
           _ptr(dW_post), _ptr(dalpha), _ptr(db_pre), _ptr(db_res), _ptr(db_post), _ptr(workspace),
           _nbytes(workspace), _stream(stream))
+
+
+def xhc_stream_sum(d, X, out, stream=None):
+    _call("xhc_stream_sum", ctypes.byref(d), _ptr(X), _ptr(out), _stream(stream))
+
+
+def xhc_stream_sum_bwd(d, dout, dX, accumulate=False, stream=None):
+    _call("xhc_stream_sum_bwd", ctypes.byref(d), _ptr(dout), _ptr(dX), int(bool(accumulate)), _stream(stream))
 
 
 # ---------------------------------------------------------------- convenience bundle
@@ -362,6 +372,12 @@ class TrainableSublayer(Sublayer):
         return X
 
     def backward(self, X, dXn, d_input, F, stream=None):
+        g = self.backward_post(X, dXn, F, stream)
+        return self.backward_pre(X, d_input, g, stream)
+
+    def backward_post(self, X, dXn, F, stream=None):
+        """xhc_post_bwd: restores X to the state xhc_pre saw and returns the
+        partial gradients, dL/dF among them (for the sublayer's own backward)."""
         d = self.d
         T, N, k, C, Kr = d.T, d.N, d.k, d.C, d.Kr
         dev = X.device
@@ -371,6 +387,13 @@ class TrainableSublayer(Sublayer):
              "conv_w": torch.empty_like(self.conv_w) if self.conv_w is not None else None}
         xhc_post_bwd(d, dXn, X, self.Xact, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, g["X"], g["F"],
                      g["dHres"], g["dHpost"], g["dp"], g["conv_w"], self.ws_post_bwd, stream)
+        return g
+
+    def backward_pre(self, X, d_input, g, stream=None):
+        """xhc_pre_bwd given dL/d input: completes g (g["X"] becomes the full dL/dX)."""
+        d = self.d
+        N, k, Kr = d.N, d.k, d.Kr
+        f32 = dict(dtype=torch.float32, device=X.device)
         for n in ("W_r", "W_pre", "W_res", "W_post"):
             g[n] = torch.empty_like(self.W[n])
         g["alpha"] = torch.empty(3, **f32)
@@ -381,3 +404,54 @@ class TrainableSublayer(Sublayer):
                     g["dHres"], g["dHpost"], g["dp"], g["X"], g["W_r"], g["W_pre"], g["W_res"], g["W_post"],
                     g["alpha"], g["b_pre"], g["b_res"], g["b_post"], self.ws_pre_bwd, stream)
         return g
+
+
+class Stack:
+    """L xHC sublayers chained on one in-place state buffer, then the final
+    stream reduction (App. "Final Stream Reduction").  Host-side sequencing of
+    the C entry points only.
+
+    ``layers`` is a list of TrainableSublayer.  forward(X, fns) runs, for each
+    layer l, xhc_pre, F_l = fns[l](input_l) (the caller's attention / MLP
+    function of the bf16 input) and xhc_post, keeping the F_l and the saved
+    rows; it returns the reduced [T, C] output.  backward(X, d_out, fn_bwds)
+    sweeps the layers in reverse: xhc_post_bwd restores layer l's pre-update
+    state from its saved active rows, fn_bwds[l](dF_l) gives dL/d input_l for
+    xhc_pre_bwd, and dL/dX flows to layer l - 1.  It returns the per-layer
+    gradient dicts (last layer last) and dL/dX of the entry state; X is back
+    at the entry state afterwards.
+    """
+
+    def __init__(self, layers):
+        self.layers = list(layers)
+        d0 = self.layers[0].d
+        for sub in self.layers:
+            if (sub.d.T, sub.d.N, sub.d.C, sub.d.state_dtype) != (d0.T, d0.N, d0.C, d0.state_dtype):
+                raise ValueError("layers of a stack share T, N, C and the state dtype")
+        self.F = [None] * len(self.layers)
+
+    def forward(self, X, fns, stream=None):
+        for l, sub in enumerate(self.layers):
+            sub.pre(X, stream, saved=sub.saved)
+            F = fns[l](sub.input)
+            self.F[l] = F
+            sub.post(X, F, stream, Xact_save=sub.Xact)
+        d0 = self.layers[0].d
+        out = torch.empty(d0.T, d0.C, dtype=X.dtype, device=X.device)
+        xhc_stream_sum(d0, X, out, stream)
+        return out
+
+    def backward(self, X, d_out, fn_bwds, stream=None):
+        d0 = self.layers[0].d
+        dX = torch.empty_like(X)
+        xhc_stream_sum_bwd(d0, d_out, dX, False, stream)
+        grads = [None] * len(self.layers)
+        for l in range(len(self.layers) - 1, -1, -1):
+            sub = self.layers[l]
+            g = sub.backward_post(X, dX, self.F[l], stream)
+            d_input = fn_bwds[l](g["F"])
+            g = sub.backward_pre(X, d_input, g, stream)
+            grads[l] = g
+            dX = g["X"]
+        return grads, dX
+
