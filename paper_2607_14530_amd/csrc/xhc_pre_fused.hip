@@ -95,7 +95,9 @@ struct Smem {
   float red[FNW][NV1][FM];            // per-wave projection partials (A)
   float red2[FNW][NV1][FM];           // per-wave active partials
   float vals[2 * FM][NJV];            // reducer partials: [job jj * G + member g][value]
-  float hpid[FM][NV2];                // H^pre and idx (as bits) of the tile being read, record layout
+  // H^pre of the tile being read with the streams ordered by parity ([t][8 par
+  // + r] = stream 2 r + par), then idx (as bits) of the 4 slots
+  float hpid[FM][NV2];
   int poff[BREC][NPOLL * kWave];      // reducer record r of polling lane pl: offset in the slot, -1 unused
 };
 
@@ -152,9 +154,6 @@ __device__ __forceinline__ void lds_barrier() {
   __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// v[j] for a lane-varying j in 0..7 as a tree of selects on the bits of j
-// (a compare chain is folded back into an indexed load, which would move v
-// out of registers)
 // v of lane l ^ 32 (v_permlane32_swap with v in both operands leaves the low
 // half in the low lanes of the first result and the high half in the second)
 __device__ __forceinline__ uint32_t from_lane_xor32(uint32_t v, int lane) {
@@ -163,6 +162,15 @@ __device__ __forceinline__ uint32_t from_lane_xor32(uint32_t v, int lane) {
 }
 __device__ __forceinline__ float from_lane_xor32f(float v, int lane) {
   return __uint_as_float(from_lane_xor32(__float_as_uint(v), lane));
+}
+
+// 16 bytes per lane from global memory straight into LDS at lds_addr + 16 lane
+// (the wave's 1 KiB lands contiguously).  Issued as inline assembly so that
+// the compiler does not track the copy: it would otherwise make every later
+// LDS access of the wave wait for it (it cannot tell that they touch other
+// LDS).  The wave waits for it explicitly (vmcnt) before the buffer is read.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_addr) : "memory");
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -175,25 +183,46 @@ __device__ __forceinline__ u32x4 lds_read16_raw(uint32_t addr) {
   return v;
 }
 
+// v plus its value in lane l ^ 16 / l ^ 32 (gfx950 permlane swaps; the two
+// halves are added in the same order in every lane, so partners agree bitwise)
+__device__ __forceinline__ float add_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float add_xor32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+// sum of v over aligned groups of g lanes (g a power of two up to 32), in
+// every lane of the group: DPP pairs and quads, then half-row and row mirrors
+// (the values are uniform within the smaller groups by then), then row pairs
+__device__ __forceinline__ float group_sum(float v, int g) {
+  if (g > 1) v = dpp_add(v, 0);
+  if (g > 2) v = dpp_add(v, 1);
+  if (g > 4) v = dpp_add(v, 2);
+  if (g > 8) v = dpp_add(v, 3);
+  if (g > 16) v = add_xor16(v);
+  return v;
+}
+
+// This lane's index, opaque to the optimiser: predicates on it are then
+// formed where they are used instead of being hoisted out of the step loop as
+// per-lane masks (which live in scalar registers and spill).
+__device__ __forceinline__ int lane_id_here() {
+  int l;
+  asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+  return l;
+}
+
 // value of v in lane i (compile-time lane: a scalar read, no LDS crossbar)
 __device__ __forceinline__ float lane_value(float v, int i) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
 }
-__device__ __forceinline__ uint32_t comp(const uint4& v, int c) {
-  return c == 0 ? v.x : (c == 1 ? v.y : (c == 2 ? v.z : v.w));
-}
-// component c (compile-time) of v[j]
-__device__ __forceinline__ uint32_t pick8c(const uint4 (&v)[KB1W], int j, int c) {
-  const bool b0 = j & 1, b1 = j & 2, b2 = j & 4;
-  const uint32_t t0 = b0 ? comp(v[1], c) : comp(v[0], c), t1 = b0 ? comp(v[3], c) : comp(v[2], c);
-  const uint32_t t2 = b0 ? comp(v[5], c) : comp(v[4], c), t3 = b0 ? comp(v[7], c) : comp(v[6], c);
-  return b2 ? (b1 ? t3 : t2) : (b1 ? t1 : t0);
-}
-
 __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   extern __shared__ unsigned char tbuf[];   // [BUFB]; dynamic, as the LDS copy needs it
   __shared__ Smem sm;
   __shared__ uint4 wal[KBAW][NOBA][FNW][kWave];
+  __shared__ uint4 stage[FNW][FM][FK][2];   // routed rows of a tile per wave: [token][slot][channel half]
   // wave index made visibly uniform: branches on it are scalar and values
   // derived from it stay in scalar registers
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave;
@@ -203,8 +232,9 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   const int team = blockIdx.x / G, s = blockIdx.x % G;
   if (team >= a.teams) return;
   const int C = a.C;
-  const int64_t ntiles = (a.T + FM - 1) / FM;
-  int64_t nq = 0;
+  const int T = (int)a.T;   // the launcher keeps T G NV1 below 2^31
+  const int ntiles = (T + FM - 1) / FM;
+  int nq = 0;
   if (team < ntiles) nq = (ntiles - team + a.teams - 1) / a.teams;
   if (nq == 0) return;   // the same for every member of the team
 
@@ -248,19 +278,24 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   // ---- tile copy by the copy waves: 64 wave instructions of 1 KiB (4 streams
   // of one token), instruction n -> token n / 4, streams 4 (n % 4) .. + 3;
   // lane -> stream + lane / 16, bytes (lane % 16) * 16 of the row slice
-  auto copy_tile = [&](int64_t tile) {
+  const uint32_t tbase = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)tbuf;
+  const uint16_t* xlane = a.X + s * FCS + (lane % 16) * 8;   // this lane's 16 bytes of a row slice
+  auto copy_tile = [&](int tile) {
     for (int n = wave; n < FM * FN / 4; n += NCOPY) {
       const int t = n / 4, i = (n % 4) * 4 + lane / 16;
-      int64_t tg = tile * FM + t;
-      if (tg >= a.T) tg = a.T - 1;   // in bounds; the token's results are dropped
-      const uint16_t* src = a.X + (tg * FN + i) * (int64_t)C + (int64_t)s * FCS + (lane % 16) * 8;
-      __builtin_amdgcn_global_load_lds(src, tbuf + t * TOKP + (n % 4) * 4 * ROWB, 16, 0, 0);
+      int tg = tile * FM + t;
+      if (tg >= T) tg = T - 1;   // in bounds; the token's results are dropped
+      const uint16_t* src = xlane + (int64_t)(tg * FN + i) * C;
+      lds_dma16(src, __builtin_amdgcn_readfirstlane(tbase + t * TOKP + (n % 4) * 4 * ROWB));
     }
   };
   if (wave < NCOPY) copy_tile(team);
 
-  const float NC = (float)FN * (float)C;
-  const int coff = (int)((int64_t)s * FCS) + 16 * wave + 8 * half;   // first channel of this lane's 8
+  // 1 / (N C): N C = 2048 G is a power of two, so multiplying by it is exact
+  const float inv_nc = 1.0f / ((float)FN * (float)C);
+  const int coff = s * FCS + 16 * wave + 8 * half;   // first channel of this lane's 8
+  uint64_t* const rec1t = a.rec1 + (size_t)team * RING * G * FM * NV1;   // this team's record slots
+  uint64_t* const rec2t = a.rec2 + (size_t)team * RING * FM * NV2;
 
   // ---- reducers.  This member's jobs of tile qt are j = s + jj G (jj = 0, 1,
   // ...; t = j / 2, h = j % 2).  Their member partials are polled by all
@@ -268,37 +303,39 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   // (jj G + g = u / NJV), value vi = u % NJV.
   const int njobs = (2 * FM - s + G - 1) / G;
   // finish job jj of tile qt from sm.vals (one wave)
-  auto finish_job = [&](int64_t qt, int jj) {
+  auto finish_job = [&](int qt, int jj) {
+    const int lane = lane_id_here();
     const int j = s + jj * G, t = j / 2, h = j % 2;
     const int nv = h == 0 ? FN + 2 : FN + 1;
     const uint32_t tag = (uint32_t)(qt + 1);
-    // lanes 0..nv-1 sum their value over the members in member order
+    // sums over the G members in a fixed order: lane l adds output l % 16 of
+    // its share of the members (ascending), then a butterfly over the four
+    // lane groups; the moments (values 16, 17) are one per lane (member l % G,
+    // moment l / G) and a butterfly over G lanes.  Every lane holding a sum
+    // holds the same bits.
+    const float* vrow = &sm.vals[jj * G][0];
+    const int per = G >= 4 ? G / 4 : 1, mg = lane >> 4;
     float v = 0.f;
-    if (lane < nv) {
-      const float* col = &sm.vals[jj * G][lane];
-      int g = 0;
-      for (; g + 8 <= G; g += 8) {   // eight loads in flight, adds in member order
-        float t8[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) t8[e] = col[(g + e) * NJV];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) v += t8[e];
-      }
-      for (; g < G; ++g) v += col[g * NJV];
+    for (int e = 0; e < kMaxG / 4; ++e) {
+      const int g = mg * per + e;
+      if (e < per && g < G) v += vrow[g * NJV + (lane & 15)];
     }
-    const int64_t tile = team + qt * a.teams;
-    const int64_t tg = tile * FM + t;
-    uint64_t* r2 = a.rec2 + ((int64_t)team * RING + qt % RING) * FM * NV2 + t * NV2;
+    v = add_xor32(add_xor16(v));
+    const int mi = lane / G;
+    const float mo = group_sum(mi < nv - FN ? vrow[(lane % G) * NJV + FN + mi] : 0.f, G);
+    const int tg = (team + qt * a.teams) * FM + t;
+    uint64_t* r2 = rec2t + (qt % RING) * FM * NV2 + t * NV2;
     if (h == 0) {
-      const float mu = lane_value(v, FN) / NC, nu = lane_value(v, FN + 1) / NC;
-      const float r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + a.eps);
+      const float mu = lane_value(mo, 0) * inv_nc, nu = lane_value(mo, G) * inv_nc;
+      const float r_ln = __builtin_amdgcn_rsqf(fmaxf(nu - mu * mu, 0.f) + a.eps);
       const float z = (v - mu * cs_l) * r_ln;   // lanes 0..15: LayerNorm-corrected router logit
       // rank among the candidates i >= m (larger logit first, ties to the lower index)
       int rank = 0;
 #pragma unroll
       for (int i = 0; i < FN; ++i) {
         const float zi = lane_value(z, i);
-        if (i >= a.m && i != lane && (zi > z || (zi == z && i < lane))) ++rank;
+        if (i >= a.m && (zi > z || (zi == z && i < lane))) ++rank;   // i == lane never counts
       }
       int slot = -1;
       float pv = 1.0f;
@@ -319,7 +356,7 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
         slot = a.m + rank;
         pv = sc;
       }
-      if (a.saved && tg < a.T) {
+      if (a.saved && tg < T) {
         float* sv = a.saved + tg * a.nsave;
         if (lane < FN) sv[lane] = z;
         else if (lane == FN) sv[a.nsave - 4] = mu;
@@ -327,41 +364,41 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
       }
       if (slot >= 0) {
         st_rec(r2 + FN + slot, __int_as_float(lane), tag);
-        if (tg < a.T) {
+        if (tg < T) {
           a.idx[tg * FK + slot] = lane;
           a.p[tg * FK + slot] = pv;
         }
       }
     } else {
-      const float nu = lane_value(v, FN) / NC;
-      const float r_rms = 1.0f / sqrtf(nu + a.eps);
+      const float nu = lane_value(mo, 0) * inv_nc;
+      const float r_rms = __builtin_amdgcn_rsqf(nu + a.eps);
       if (lane < FN) {
-        if (a.saved && tg < a.T) a.saved[tg * a.nsave + FN + lane] = v * r_rms;
+        if (a.saved && tg < T) a.saved[tg * a.nsave + FN + lane] = v * r_rms;
         const float hpre = sigmoidf(alpha_pre * (v * r_rms) + bpre_l);
         st_rec(r2 + lane, hpre, tag);
-        if (tg < a.T) a.Hpre[tg * FN + lane] = hpre;
+        if (tg < T) a.Hpre[tg * FN + lane] = hpre;
       }
     }
   };
 
   // record r of this polling lane: address and whether it is wanted
-  auto poll_rec = [&](int64_t q, int r, bool& wanted) -> const uint64_t* {
+  auto poll_rec = [&](int q, int r, bool& wanted) -> const uint64_t* {
     const bool hasB = q >= 1 && q - 1 < nq, hasC = q >= 2 && q - 2 < nq;
-    const int pl = (wave - NCOPY) * kWave + lane;   // 0 .. 255
+    const int pl = (wave - NCOPY) * kWave + lane_id_here();   // 0 .. 255
     if (r < BREC) {
-      const uint64_t* r1 = a.rec1 + (((int64_t)team * RING + (q - 1 + RING) % RING) * G) * FM * NV1;
+      const uint64_t* r1 = rec1t + ((q - 1 + RING) % RING) * G * FM * NV1;
       const int off = sm.poff[r][pl];
       wanted = hasB && off >= 0;
       return r1 + (wanted ? off : 0);
     }
-    const uint64_t* r2 = a.rec2 + ((int64_t)team * RING + (q - 2 + RING) % RING) * FM * NV2;
+    const uint64_t* r2 = rec2t + ((q - 2 + RING) % RING) * FM * NV2;
     const int u = pl + (r - BREC) * NPOLL * kWave;
     wanted = hasC && u < FM * NV2;
     return r2 + (wanted ? u : 0);
   };
   // first loads of the records of step qs, issued at the end of step qs - 1
   // (polling waves) and checked after A of step qs
-  auto issue_polls = [&](int64_t qs, uint64_t (&first)[BREC + CREC]) {
+  auto issue_polls = [&](int qs, uint64_t (&first)[BREC + CREC]) {
 #pragma unroll
     for (int r = 0; r < BREC + CREC; ++r) {
       bool w;
@@ -375,8 +412,23 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
 
   // ---- pipeline steps: A of tile q (registers XA), B of tile q - 1, C of
   // tile q - 2 (registers XC); the registers rotate at the end of a step
-  uint4 XA[KB1W], XB[KB1W], XC[KB1W];
-  for (int64_t q = 0; q < nq + 2; ++q) {
+  // active partials of tile qc (the C phase of a step, left in red2) summed
+  // over the waves into part2; runs in the next step, after its first barrier
+  auto publish2 = [&](int qc) {
+    const int tile = team + qc * a.teams;
+    for (int u = tid; u < NV1 * FM; u += FNT) {
+      const int o = u / FM, t = u % FM;
+      const int tg = tile * FM + t;
+      float v = 0.f;
+#pragma unroll
+      for (int w = 0; w < FNW; ++w) v += sm.red2[w][o][t];
+      if (tg < T) a.part2[(s * NV1 + o) * T + tg] = v;
+    }
+  };
+  // one pipeline step: A of tile q into XA, B of tile q - 1, C of tile q - 2
+  // from XC.  Tile q lives in register set q % 3, so the loop below runs three
+  // steps with the roles of the sets permuted and no register moves.
+  auto step = [&](const int q, uint4 (&XA)[KB1W], const uint4 (&XC)[KB1W]) __attribute__((always_inline)) {
     const bool hasA = q < nq, hasB = q >= 1 && q - 1 < nq, hasC = q >= 2 && q - 2 < nq;
     if (wave < NCOPY) {
       __builtin_amdgcn_s_waitcnt(0);   // this wave's part of the copy of tile q has landed
@@ -403,36 +455,34 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
     lds_barrier();   // S2: the buffer is free
     if (hasA) {
       if (wave < NCOPY && q + 1 < nq) copy_tile(team + (q + 1) * a.teams);
-      // ---- A: partial projection and moments of the slice
-      f32x4 acc[NOB1];
+      // ---- A: partial projection and moments of the slice, all on the matrix
+      // cores: sum x is a product with an all-ones A operand (every row of D
+      // holds the column sums), sum x^2 the diagonal of the product of the
+      // tile with itself (the B fragment read as an A fragment is its
+      // transpose)
+      f32x4 acc[NOB1], mom1 = {0.f, 0.f, 0.f, 0.f}, mom2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ob = 0; ob < NOB1; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-      float s1 = 0.f, s2 = 0.f;
+      const uint4 ones = make_uint4(0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u);
 #pragma unroll
       for (int r = 0; r < KB1W; ++r) {
-        float f[8];
-        unpack8(XA[r], f);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          s1 += f[e];
-          s2 += f[e] * f[e];
-        }
 #pragma unroll
         for (int ob = 0; ob < NOB1; ++ob) acc[ob] = mfma_16x16x32(wf[r][ob], XA[r], acc[ob]);
+        mom1 = mfma_16x16x32(ones, XA[r], mom1);
+        mom2 = mfma_16x16x32(XA[r], XA[r], mom2);
       }
-      s1 += __shfl_xor(s1, 16);
-      s1 += __shfl_xor(s1, 32);
-      s2 += __shfl_xor(s2, 16);
-      s2 += __shfl_xor(s2, 32);
 #pragma unroll
       for (int ob = 0; ob < NOB1; ++ob)
 #pragma unroll
         for (int v = 0; v < 4; ++v) sm.red[wave][ob * 16 + grp * 4 + v][tl] = acc[ob][v];
-      if (grp == 0) {
-        sm.red[wave][32][tl] = s1;
-        sm.red[wave][33][tl] = s2;
+      if (grp == 0) sm.red[wave][32][tl] = mom1[0];
+      // D[t][t] sits in lane group t / 4, component t % 4
+      if (grp == tl / 4) {
+        const int v = tl % 4;
+        sm.red[wave][33][tl] = v == 0 ? mom2[0] : (v == 1 ? mom2[1] : (v == 2 ? mom2[2] : mom2[3]));
       }
     }
+    if (q >= 3 && q - 3 < nq) publish2(q - 3);   // red2 of the previous step (its C of tile q - 3)
     if (polls) {
       // tags: tile q - 1 for the partials, tile q - 2 for H^pre / idx
       const uint64_t* src[BREC + CREC];
@@ -448,39 +498,45 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
         any = any || need[r];
       }
       if (__any(any)) ld_recs2t<BREC, CREC>(src, need, (uint32_t)q, (uint32_t)(q - 1), a.err, val);
-      const int pl = (wave - NCOPY) * kWave + lane;
+      const int pl = (wave - NCOPY) * kWave + lane_id_here();
 #pragma unroll
       for (int r = 0; r < BREC; ++r)
         if (want[r]) (&sm.vals[0][0])[pl + r * NPOLL * kWave] = val[r];
 #pragma unroll
       for (int r = 0; r < CREC; ++r)
-        if (want[BREC + r]) (&sm.hpid[0][0])[pl + r * NPOLL * kWave] = val[BREC + r];
+        if (want[BREC + r]) {
+          const int u = pl + r * NPOLL * kWave, t = u / NV2, e = u % NV2;
+          sm.hpid[t][e < FN ? 8 * (e & 1) + (e >> 1) : e] = val[BREC + r];
+        }
     }
     lds_barrier();   // S3: A partials, polled records in LDS
-    // the reducers first: a wave's later loads and LDS reads may wait for its
-    // stores, so the record stores of the publish come after
-    if (hasB && wave >= NCOPY)
+    // the reducer waves (4 .. 4 + min(njobs, 4) - 1) finish their jobs of tile
+    // q - 1 while the other waves publish the partials of tile q
+    if (hasB && wave >= NCOPY && wave - NCOPY < njobs)
       for (int jj = wave - NCOPY; jj < njobs; jj += NPOLL) finish_job(q - 1, jj);
-    if (hasA) {
-      uint64_t* r1 = a.rec1 + (((int64_t)team * RING + q % RING) * G) * FM * NV1;
-      for (int u = tid; u < NV1 * FM; u += FNT) {
+    if (hasA && !(wave >= NCOPY && wave - NCOPY < njobs)) {
+      uint64_t* r1 = rec1t + (q % RING) * G * FM * NV1;
+      const int nred = njobs < NPOLL ? njobs : NPOLL;   // reducer waves
+      for (int u = wave < NCOPY ? tid : tid - nred * kWave; u < NV1 * FM; u += FNT - nred * kWave) {
         const int o = u / FM, t = u % FM;
         float v = 0.f;
 #pragma unroll
         for (int w = 0; w < FNW; ++w) v += sm.red[w][o][t];
-        st_rec(r1 + ((int64_t)s * FM + t) * NV1 + o, v, (uint32_t)(q + 1));
+        st_rec(r1 + (s * FM + t) * NV1 + o, v, (uint32_t)(q + 1));
       }
     }
     if (hasC) {
-      const int64_t tile = team + (q - 2) * a.teams;
-      const int64_t tg = tile * FM + tl;
+      const int tg = (team + (q - 2) * a.teams) * FM + tl;
       // ---- dense read of the lane's 8 channels: its 8 streams, then the
       // other parity from lane ^ 32
       {
         float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+        const float4 h0 = *reinterpret_cast<const float4*>(&sm.hpid[tl][8 * par]);
+        const float4 h1 = *reinterpret_cast<const float4*>(&sm.hpid[tl][8 * par + 4]);
+        const float hvs[KB1W] = {h0.x, h0.y, h0.z, h0.w, h1.x, h1.y, h1.z, h1.w};
 #pragma unroll
         for (int r = 0; r < KB1W; ++r) {
-          const float hv = sm.hpid[tl][2 * r + par];
+          const float hv = hvs[r];   // H^pre of stream 2 r + par
           float f[8];
           unpack8(XC[r], f);
 #pragma unroll
@@ -488,70 +544,56 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
         }
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] += from_lane_xor32f(acc[e], lane);
-        if (par == 0 && tg < a.T) *reinterpret_cast<uint4*>(a.input + tg * C + coff) = pack8(acc);
+        if (par == 0 && tg < T) *reinterpret_cast<uint4*>(a.input + (int64_t)tg * C + coff) = pack8(acc);
       }
-      // ---- active rows: slot 2r + par of this lane; the stream lives in this
-      // lane (same parity) or in lane ^ 32
+      // ---- active rows: each lane stores those of its 8 streams that are
+      // routed into the wave's staging area at their slot, then reads back the
+      // slot pair it feeds to the MFMA (slot 2r + par).  A wave's LDS accesses
+      // complete in order, so no barrier is needed.
       {
-        int id4[FK];
+        uint32_t mask = 0, codes = 0;   // routed streams; 2-bit slot of each stream
 #pragma unroll
-        for (int j = 0; j < FK; ++j) id4[j] = __float_as_int(sm.hpid[tl][FN + j]) & (FN - 1);   // always a row of the tile
-        f32x4 acc[NOBA];
+        for (int j = 0; j < FK; ++j) {
+          const int id = __float_as_int(sm.hpid[tl][FN + j]) & (FN - 1);   // always a row of the tile
+          mask |= 1u << id;
+          codes |= (uint32_t)j << (2 * id);
+        }
+        mask >>= par;
+        codes >>= 2 * par;
+#pragma unroll
+        for (int r = 0; r < KB1W; ++r)   // stream 2r + par
+          if ((mask >> (2 * r)) & 1u) stage[wave][tl][(codes >> (4 * r)) & 3u][half] = XC[r];
+        f32x4 acc[NOBA], mom2 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ob = 0; ob < NOBA; ++ob) acc[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-        float s2 = 0.f;
 #pragma unroll
         for (int r = 0; r < KBAW; ++r) {
-          const int mine = par ? id4[2 * r + 1] : id4[2 * r];      // stream this lane needs
-          const int theirs = par ? id4[2 * r] : id4[2 * r + 1];    // stream lane ^ 32 needs
-          // one 32-bit component at a time keeps the select trees small
-          const bool keep = (mine & 1) == par;
-          uint32_t xw[4];
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const uint32_t own = pick8c(XC, mine >> 1, c);
-            const uint32_t recv = from_lane_xor32(pick8c(XC, theirs >> 1, c), lane);
-            xw[c] = keep ? own : recv;
-          }
-          const uint4 xa = make_uint4(xw[0], xw[1], xw[2], xw[3]);
-          float f[8];
-          unpack8(xa, f);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) s2 += f[e] * f[e];
+          const uint4 xa = stage[wave][tl][2 * r + par][half];
 #pragma unroll
           for (int ob = 0; ob < NOBA; ++ob) acc[ob] = mfma_16x16x32(wal[r][ob][wave][lane], xa, acc[ob]);
+          mom2 = mfma_16x16x32(xa, xa, mom2);   // diagonal: sum a^2 per token
         }
-        s2 += __shfl_xor(s2, 16);
-        s2 += __shfl_xor(s2, 32);
 #pragma unroll
         for (int ob = 0; ob < NOBA; ++ob)
 #pragma unroll
           for (int v = 0; v < 4; ++v) sm.red2[wave][ob * 16 + grp * 4 + v][tl] = acc[ob][v];
-        if (grp == 0) {
-          sm.red2[wave][32][tl] = 0.f;
-          sm.red2[wave][33][tl] = s2;
+        if (grp == 0) sm.red2[wave][32][tl] = 0.f;
+        if (grp == tl / 4) {
+          const int v = tl % 4;
+          sm.red2[wave][33][tl] = v == 0 ? mom2[0] : (v == 1 ? mom2[1] : (v == 2 ? mom2[2] : mom2[3]));
         }
       }
     }
-    lds_barrier();   // S5: H^pre / idx / active partials of tile q - 2 consumed
-    if (hasC) {
-      const int64_t tile = team + (q - 2) * a.teams;
-      for (int u = tid; u < NV1 * FM; u += FNT) {
-        const int o = u / FM, t = u % FM;
-        const int64_t tg = tile * FM + t;
-        float v = 0.f;
-#pragma unroll
-        for (int w = 0; w < FNW; ++w) v += sm.red2[w][o][t];
-        if (tg < a.T) a.part2[((int64_t)s * NV1 + o) * a.T + tg] = v;
-      }
-    }
     if (wave >= NCOPY) issue_polls(q + 1, first);
-#pragma unroll
-    for (int r = 0; r < KB1W; ++r) {
-      XC[r] = XB[r];
-      XB[r] = XA[r];
-    }
+  };
+  uint4 X0[KB1W], X1[KB1W], X2[KB1W];
+  for (int q = 0; q < nq + 2; q += 3) {
+    step(q, X0, X1);
+    if (q + 1 < nq + 2) step(q + 1, X1, X2);
+    if (q + 2 < nq + 2) step(q + 2, X2, X0);
   }
+  lds_barrier();   // red2 of the last C phase (tile nq - 1)
+  publish2(nq - 1);
 }
 
 // zero n1 and n2 16-byte words at p1 and p2 (one launch)
@@ -594,7 +636,8 @@ DeviceInfo device_info() {
 bool fused_pre_supported(const xhc_dims* d) {
   return d->state_dtype == XHC_BF16 && d->N == FN && d->k == FK && d->Kr >= 1 &&
          FK * d->Kr + FK * FK <= 16 * NOBA && d->C % FCS == 0 && d->C / FCS <= kMaxG &&
-         kMaxG % (d->C / FCS) == 0;   // every member takes 32 / G reducer jobs per tile
+         kMaxG % (d->C / FCS) == 0 &&   // every member takes 32 / G reducer jobs per tile
+         d->T * (d->C / FCS) * NV1 < ((int64_t)1 << 31);   // 32-bit token and partial indices
 }
 
 // Workspace: error counter, records (sized for up to kMaxResident co-resident
