@@ -528,3 +528,157 @@ def xhc_sublayer_grads(X, F, conv_w, W_r, W_pre, W_res, W_post, alpha, b_pre, b_
     out.update({k_: (v.detach() if torch.is_tensor(v) else v) for k_, v in fwd.items()})
     out["loss"] = L.detach()
     return out
+
+
+# --------------------------------------------------------------------------
+# xHC-Flash backward (reverse mode of the group forward)
+# --------------------------------------------------------------------------
+
+def flash_forward(X0, F_list, conv_w_list, W_r, W_pre_list, W_post_list, W_res, alpha_pre, b_pre,
+                  alpha_post, b_post, alpha_res, b_res, *, m, k, S, kappa=(4, 8, 12), eps=1e-5,
+                  sinkhorn_iters=20, clamp_delta=1e-6, round_state=True, gram_schmidt_on=True,
+                  router="sigmoid"):
+    """One xHC-Flash sharing group, float64, with every weight taken as given
+    (already the bf16 operand values) so that it can be differentiated.
+
+    Same steps as xhc_flash_group (Alg. "xHC-Flash: one Transformer block";
+    eq:flash_dual_read, eq:flash_attn_update, App. E.2 eq:app_four_sub_base,
+    eq:app_general_writeback, eq:app_active_state_correction): one routing
+    and Q pre-maps from the entry state X0; sublayers q < Q add
+    p (H^post,q out_aug^(q)) to the active rows, the last applies H^res
+    first; the input of sublayer q + 1 is its non-active base readout plus
+    the pre-map weights of the active streams on the updated active rows;
+    H^post,q+1 (and H^res before the last sublayer) come from the updated
+    active rows.  The routing decision is taken on detached logits
+    (piecewise constant); p is the score of the routed stream.  With
+    ``round_state`` each written active row passes through a bfloat16
+    rounding, which the reverse mode treats as the identity (the stored
+    state is what the next step reads).  Returns (X after the group, list
+    of the Q inputs, dict of idx, p, Hpre [Q,T,N], Hpost list, Hres and acts,
+    the active rows before each sublayer).
+    """
+    Q = len(F_list)
+    T, N, C = X0.shape
+    x = X0.reshape(T, N * C)
+    z_r = layer_norm(x, eps) @ W_r
+    xr = rms_norm(x, eps)
+    Hpre = torch.stack([sigmoid(alpha_pre[q] * (xr @ W_pre_list[q]) + b_pre[q]) for q in range(Q)])
+    idx, _, gap = route(z_r.detach(), m, k, router)
+    s = router_scores(z_r, router)
+    p = torch.ones(T, k, dtype=F64)
+    if k > m:
+        p = torch.cat([p[:, :m], torch.gather(s, 1, idx[:, m:])], dim=1)
+    active = torch.zeros(T, N, dtype=torch.bool)
+    active[torch.arange(T)[:, None], idx] = True
+    keep = (~active).to(F64)
+    ar = torch.arange(T)[:, None]
+
+    def post_from(a, q):
+        Kq = W_post_list[q].shape[1] // k
+        return post_mapping(rms_norm(a.reshape(T, k * C), eps) @ W_post_list[q], alpha_post[q], b_post[q], k, Kq)
+
+    def res_from(a):
+        return residual_mapping(rms_norm(a.reshape(T, k * C), eps) @ W_res, alpha_res, b_res, k,
+                                sinkhorn_iters, clamp_delta)
+
+    tokens = torch.arange(T)
+    inputs = [torch.einsum("tn,tnc->tc", Hpre[0], X0)]
+    a = gather_rows(X0, idx)
+    acts = [a]
+    Hpost = [post_from(a, 0)]
+    Hres = res_from(a) if Q == 1 else None
+    for q in range(Q):
+        comps = augmented_output(F_list[q], conv_w_list[q], kappa, S, tokens, gram_schmidt_on)
+        wb = sum(Hpost[q][:, :, r, None] * comps[r][:, None, :] for r in range(len(comps)))
+        if q < Q - 1:
+            a_new = a + p[:, :, None] * wb
+        else:
+            a_new = torch.einsum("tjl,tlc->tjc", Hres, a) + p[:, :, None] * wb
+        if round_state:
+            a_new = a_new + (round_state_bf16(a_new.detach()) - a_new.detach())
+        if q < Q - 1:
+            hsel = torch.gather(Hpre[q + 1], 1, idx)
+            base = torch.einsum("tn,tnc->tc", Hpre[q + 1] * keep, X0)
+            inputs.append(base + (hsel[:, :, None] * a_new).sum(1))
+            Hpost.append(post_from(a_new, q + 1))
+            if q + 1 == Q - 1:
+                Hres = res_from(a_new)
+            acts.append(a_new)
+        a = a_new
+    Xn = X0.clone()
+    Xn[ar, idx] = a
+    return Xn, inputs, dict(idx=idx, p=p, gap=gap, Hpre=Hpre, Hpost=Hpost, Hres=Hres, acts=acts, z_r=z_r)
+
+
+def flash_objective(vals, G_X, G_in_list, **kw):
+    """L = <G_X, X after the group> + sum_q <G_in_q, input_q> for one
+    xHC-Flash group (see flash_forward); ``vals`` holds the leaves named in
+    FLASH_GRAD_NAMES.  Returns (L, forward dict)."""
+    Xn, inputs, fwd = flash_forward(vals["X"], vals["F_list"], vals["conv_w_list"], vals["W_r"],
+                                    vals["W_pre_list"], vals["W_post_list"], vals["W_res"], vals["alpha_pre"],
+                                    vals["b_pre"], vals["alpha_post"], vals["b_post"], vals["alpha_res"],
+                                    vals["b_res"], **kw)
+    L = (G_X.to(F64) * Xn).sum()
+    for g, inp in zip(G_in_list, inputs):
+        L = L + (g.to(F64) * inp).sum()
+    fwd["X_new"], fwd["inputs"] = Xn, inputs
+    return L, fwd
+
+
+FLASH_GRAD_NAMES = ("X", "F_list", "conv_w_list", "W_r", "W_pre_list", "W_post_list", "W_res", "alpha_pre",
+                    "b_pre", "alpha_post", "b_post", "alpha_res", "b_res")
+
+
+def flash_leaves(X0, F_list, conv_w_list, W_r, W_pre_list, W_post_list, W_res, alpha_pre, b_pre, alpha_post,
+                 b_post, alpha_res, b_res):
+    """float64 copies of a group's inputs, the projection weights rounded to
+    their bf16 operand values; lists stay lists, None stays None."""
+    def one(t, op=False):
+        if t is None:
+            return None
+        t = torch.as_tensor(t)
+        return (bf16_operand(t) if op else t.to(F64)).detach().clone()
+    return {"X": one(X0), "F_list": [one(f) for f in F_list], "conv_w_list": [one(c) for c in conv_w_list],
+            "W_r": one(W_r, True), "W_pre_list": [one(w, True) for w in W_pre_list],
+            "W_post_list": [one(w, True) for w in W_post_list], "W_res": one(W_res, True),
+            "alpha_pre": one(torch.as_tensor(alpha_pre, dtype=F64)), "b_pre": [one(b) for b in b_pre],
+            "alpha_post": one(torch.as_tensor(alpha_post, dtype=F64)), "b_post": [one(b) for b in b_post],
+            "alpha_res": one(torch.as_tensor(alpha_res, dtype=F64)), "b_res": one(b_res)}
+
+
+def flash_group_grads(vals, G_X, G_in_list, **kw):
+    """Gradients of flash_objective with respect to every entry of ``vals``
+    (as made by flash_leaves): the reverse mode of the group forward, the
+    routing decision piecewise constant.  Returns (dict of gradients with the
+    structure of vals, forward dict, loss).  Parity: pinned by central
+    differences (tests)."""
+    leaves, paths = [], []
+    lv = {}
+    for name in FLASH_GRAD_NAMES:
+        v = vals[name]
+        if isinstance(v, list):
+            lv[name] = []
+            for i, t in enumerate(v):
+                if t is None:
+                    lv[name].append(None)
+                    continue
+                t = t.detach().clone().requires_grad_(True)
+                lv[name].append(t)
+                leaves.append(t)
+                paths.append((name, i))
+        else:
+            t = v.detach().clone().requires_grad_(True)
+            lv[name] = t
+            leaves.append(t)
+            paths.append((name, None))
+    L, fwd = flash_objective(lv, G_X, G_in_list, **kw)
+    grads = torch.autograd.grad(L, leaves, allow_unused=True)
+    out = {n: ([None] * len(vals[n]) if isinstance(vals[n], list) else None) for n in FLASH_GRAD_NAMES}
+    for (name, i), g, t in zip(paths, grads, leaves):
+        g = torch.zeros_like(t) if g is None else g
+        if i is None:
+            out[name] = g
+        else:
+            out[name][i] = g
+    fwd = {k_: (v.detach() if torch.is_tensor(v) else v) for k_, v in fwd.items()}
+    return out, fwd, L.detach()

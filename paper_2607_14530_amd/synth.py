@@ -88,7 +88,8 @@ def sublayer_inputs(w: Workload, seed: int, device="cpu", weight_std=0.02,
     return d
 
 
-def flash_inputs(w: Workload, Q: int, seed: int, device="cpu", weight_std=0.02):
+def flash_inputs(w: Workload, Q: int, seed: int, device="cpu", weight_std=0.02, grads=False,
+                 bias_std=0.0):
     """Inputs of one xHC-Flash sharing group of Q sublayers (Q = 2 or 4).
 
     Sublayer q (1-based) is attention-type (one write-back component) when q
@@ -96,7 +97,10 @@ def flash_inputs(w: Workload, Q: int, seed: int, device="cpu", weight_std=0.02):
     X, F_list (Q x [T,C]), W_r, W_pre_list (Q x [N*C,N]), W_post_list
     (Q x [k*C, k*K_q]), W_res [k*C,k*k], conv_w_list (None for attention),
     alpha_pre/alpha_post (Q floats), alpha_res, b_pre (Q x [N]),
-    b_post (Q x [k*K_q]), b_res [k*k].
+    b_post (Q x [k*K_q]), b_res [k*k].  With grads=True also the upstream
+    gradients G_X [T,N,C] (of the state after the group) and G_in_list
+    (Q x [T,C], of each sublayer input), drawn after everything above; with
+    bias_std > 0 the biases are drawn last ~ N(0, bias_std).
     """
     assert Q in (2, 4)
     g = torch.Generator(device=device)
@@ -118,6 +122,13 @@ def flash_inputs(w: Workload, Q: int, seed: int, device="cpu", weight_std=0.02):
     d["b_pre"] = [torch.zeros(N, device=device) for _ in range(Q)]
     d["b_post"] = [torch.zeros(k * Kq[q], device=device) for q in range(Q)]
     d["b_res"] = torch.zeros(k * k, device=device)
+    if grads:
+        d["G_X"] = _randn((T, N, C), g, device).to(w.dtype)
+        d["G_in_list"] = [_randn((T, C), g, device).to(w.dtype) for _ in range(Q)]
+    if bias_std > 0:
+        d["b_pre"] = [_randn((N,), g, device, bias_std) for _ in range(Q)]
+        d["b_post"] = [_randn((k * Kq[q],), g, device, bias_std) for q in range(Q)]
+        d["b_res"] = _randn((k * k,), g, device, bias_std)
     return d
 
 
