@@ -121,7 +121,7 @@ xhc_status xhc_pack_active(const xhc_dims* d, int32_t Kq, const float* W_post, c
 /* Workspace needed by an entry point (op: one of the XHC_OP_* values).        */
 enum {
   XHC_OP_PRE = 0, XHC_OP_POST = 1, XHC_OP_FLASH_PRE = 2, XHC_OP_FLASH_POST = 3,
-  XHC_OP_POST_BWD = 4, XHC_OP_PRE_BWD = 5
+  XHC_OP_POST_BWD = 4, XHC_OP_PRE_BWD = 5, XHC_OP_FLASH_POST_BWD = 6, XHC_OP_FLASH_PRE_BWD = 7
 };
 size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q);
 
@@ -241,13 +241,73 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
  *   packed_act_next  xhc_pack_active(K_{q+1}, W_res iff q + 1 == Q) of sublayer q+1
  *   alpha_next [2] = (alpha_post_{q+1}, alpha_res); b_post_next [k*K_{q+1}];
  *   b_res_next [k*k] iff q + 1 == Q; outputs Hpost_next [T,k,K_{q+1}] and
- *   Hres_next [T,k,k] iff q + 1 == Q, both from the updated active rows.      */
+ *   Hres_next [T,k,k] iff q + 1 == Q, both from the updated active rows.
+ *   Xact_save [T,k,C] or NULL: receives the active rows before this sublayer's
+ *   write-back (slot order), as xhc_flash_post_bwd needs them.                 */
 xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, const void* F, const float* conv_w,
                           const int32_t* idx, const float* p, const float* Hpost, const float* Hres,
                           const float* Hpre_next, const void* base_next, void* input_next,
                           const void* packed_act_next, const float* alpha_next, const float* b_post_next,
-                          const float* b_res_next, float* Hpost_next, float* Hres_next, void* workspace,
-                          size_t workspace_bytes, void* stream);
+                          const float* b_res_next, float* Hpost_next, float* Hres_next, void* Xact_save,
+                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------ xHC-Flash backward
+ * Reverse mode of one sharing group (xhc_flash_pre, then xhc_flash_post for
+ * q = 1..Q) for a loss L(X', input_1 .. input_Q), X' the state after the
+ * group.  Routing is piecewise constant (the router gets gradient only
+ * through p of routed slots); written rows are taken as stored (their bf16
+ * rounding passes the gradient through).  The sweep runs sublayer by
+ * sublayer on the active rows a^(q) [T,k,C] (slot order), their gradient
+ * held in fp32 between the calls: call
+ * xhc_flash_post_bwd for q = Q, Q-1, .., 1 (each may run right after the
+ * sublayer's own backward has produced dL/d input_q from dL/dF_q), then
+ * xhc_flash_pre_bwd once.  a^(0) = X[idx] is the group-entry active state,
+ * a^(q) the active rows after sublayer q.  Supported: k = 4 (or 8 with
+ * k K_r + k k <= 32), N in {4, 8, 16, 32}, C % 256 == 0.
+ *
+ * xhc_flash_post_bwd - sublayer q (1 <= q <= Q)
+ *   dXn     [T,N,C] dL/dX' (read), iff q == Q (else NULL): da is then set to
+ *           its active rows before the sweep starts
+ *   da      [T,k,C] fp32 in/out: on entry dL/da^(q) (ignored when q == Q), on
+ *           return dL/da^(q-1) through this sublayer: the write-back reverse
+ *           (H^res^T at q == Q, pass-through before), the reverse of H^post,q
+ *           (and H^res) computed from a^(q-1) (eq:param_post, eq:param_res),
+ *           and for q >= 2 the active part of input_q (H^pre,q_{I_j} d input_q)
+ *   Xact    [T,k,C] a^(q-1): xhc_flash_post's Xact_save of sublayer q
+ *   F, conv_w (iff q is even), idx, p, Hpost [T,k,K_q], Hres (iff q == Q) as
+ *           in the forward; packed_act: the forward's packed [W_post,q | W_res];
+ *           W_post [k*C, k*K_q] and W_res [k*C,k*k] (iff q == Q) fp32;
+ *           alpha_post [1], b_post [k*K_q]; alpha_res [1], b_res [k*k] iff q == Q
+ *   Hpre_q  [T,N] = Hpre[q-1] of xhc_flash_pre and d_input [T,C] = dL/d input_q,
+ *           both iff q >= 2 (input_1 is reversed by xhc_flash_pre_bwd)
+ * Outputs (overwritten): dF [T,C]; dconv_w (iff q is even); dW_post,
+ * dalpha_post [1], db_post; dW_res, dalpha_res [1], db_res iff q == Q;
+ * dHpre_act [T,k] = <d input_q, a^(q-1)_j> iff q >= 2.  dp [T,k] is
+ * accumulated (+=): zero it before the sweep.
+ *
+ * xhc_flash_pre_bwd - the group-entry state
+ *   X [T,N,C] group-entry state; packed_full, W_r [N*C,N], W_pre [Q,N*C,N]
+ *   fp32, alpha_pre [Q], b_pre [Q,N] as in the forward; idx, p, Hpre [Q,T,N]
+ *   from xhc_flash_pre; d_input [Q,T,C] = dL/d input_q; dHpre_act [Q-1,T,k]
+ *   from xhc_flash_post_bwd (q = 2..Q); dp [T,k] the accumulated dp;
+ *   dXn [T,N,C] dL/dX'; da0 [T,k,C] fp32 dL/da^(0) (da after the q = 1 reverse)
+ * Outputs (overwritten): dX [T,N,C] = dL/dX; dW_r; dW_pre [Q,N*C,N];
+ * dalpha_pre [Q]; db_pre [Q,N].  Token sums run in a fixed order
+ * (deterministic).                                                          */
+xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const void* dXn, void* da, const void* Xact,
+                              const void* F, const float* conv_w, const int32_t* idx, const float* p,
+                              const float* Hpost, const float* Hres, const void* packed_act, const float* W_post,
+                              const float* W_res, const float* alpha_post, const float* alpha_res,
+                              const float* b_post, const float* b_res, const float* Hpre_q, const void* d_input,
+                              void* dF, float* dconv_w, float* dW_post, float* dalpha_post, float* db_post,
+                              float* dW_res, float* dalpha_res, float* db_res, float* dp, float* dHpre_act,
+                              void* workspace, size_t workspace_bytes, void* stream);
+xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full, const float* W_r,
+                             const float* W_pre, const float* alpha_pre, const float* b_pre, const int32_t* idx,
+                             const float* p, const float* Hpre, const void* d_input, const float* dHpre_act,
+                             const float* dp, const void* dXn, const void* da0, void* dX, float* dW_r,
+                             float* dW_pre, float* dalpha_pre, float* db_pre, void* workspace, size_t workspace_bytes,
+                             void* stream);
 
 /* ------------------------------------------------------------ final stream reduction
  * App. "Final Stream Reduction": before the last RMSNorm and the unembedding

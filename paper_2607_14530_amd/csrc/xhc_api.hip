@@ -116,6 +116,138 @@ size_t flash_post_ws(const xhc_dims* d, int Q, int q) {
   return need;
 }
 
+// ---- xHC-Flash backward: the per-sublayer reverse runs the single-sublayer
+// kernels on the k active rows ([T, k, C], every row active, identity slot
+// map); dims_rows() is that view.  Its post part sees the sublayer's K_q, its
+// pre part sees K_q with every stream fixed (no router).
+xhc_dims dims_rows(const xhc_dims* d, int Kq) {
+  xhc_dims r = *d;
+  r.N = d->k;
+  r.m = d->k;
+  r.Kr = Kq;
+  r.router = XHC_ROUTER_SIGMOID;
+  r.impl = XHC_IMPL_MULTI;
+  return r;
+}
+
+// the entry-state reverse: the single-sublayer pre reverse with one
+// write-back component (its active mapping receives no gradient here)
+xhc_dims dims_entry(const xhc_dims* d) {
+  xhc_dims r = *d;
+  r.Kr = 1;
+  r.impl = XHC_IMPL_MULTI;
+  return r;
+}
+
+bool flash_bwd_supported(const xhc_dims* d) {
+  if ((d->k != 4 && d->k != 8) || !bwd_pre_supported(d)) return false;
+  const xhc_dims r = dims_rows(d, d->Kr);
+  return bwd_pre_supported(&r);
+}
+
+// sequential carve of a workspace into 256-byte aligned pieces
+struct Carve {
+  size_t total = 0;
+  size_t take(size_t bytes) {
+    const size_t at = total;
+    total += align_up(bytes);
+    return at;
+  }
+};
+
+// The active-row gradient between sublayers is kept in fp32, so the per-row
+// reverses run on fp32 copies of the slice (dims with state_dtype fp32).
+xhc_dims dims_rows32(const xhc_dims* d, int Kq) {
+  xhc_dims r = dims_rows(d, Kq);
+  r.state_dtype = XHC_F32;
+  return r;
+}
+
+struct FlashPostBwdWs {
+  size_t post, pre, part, sums, idx_id, hres_id, hsel, xrest, da_out, xact32, f32c, din32, df32, dhpost, dhres, dp,
+      saved, hpost_re, hres_re, w0, colsum0, wres0, bres0, alpha2, dwr, dwpre, dbpre, dwres, dbres, dalpha2, total;
+};
+
+FlashPostBwdWs flash_post_bwd_ws(const xhc_dims* d, int Q, int q) {
+  const int Kq = flash_Kq(d, q);
+  const xhc_dims r = dims_rows32(d, Kq);
+  const int64_t T = d->T, k = d->k, C = d->C, kC = k * C;
+  const size_t f = sizeof(float);
+  const int64_t na = act_outs(d, Kq, q == Q);
+  Carve c;
+  FlashPostBwdWs w;
+  w.post = c.take(bwd_post_ws_bytes(&r));
+  w.pre = c.take(bwd_pre_ws_bytes(&r));
+  w.part = c.take(part_bytes(d, true, kC, na));
+  w.sums = c.take(sums_bytes(na, T));
+  w.idx_id = c.take((size_t)T * k * sizeof(int32_t));
+  w.hres_id = c.take((size_t)T * k * k * f);
+  w.hsel = c.take((size_t)T * k * f);
+  w.xrest = c.take((size_t)T * kC * f);
+  w.da_out = c.take((size_t)T * kC * f);
+  w.xact32 = c.take((size_t)T * kC * f);
+  w.f32c = c.take((size_t)T * C * f);
+  w.din32 = c.take((size_t)T * C * f);
+  w.df32 = c.take((size_t)T * C * f);
+  w.dhpost = c.take((size_t)T * k * Kq * f);
+  w.dhres = c.take((size_t)T * k * k * f);
+  w.dp = c.take((size_t)T * k * f);
+  w.saved = c.take((size_t)T * saved_floats(k, k, Kq) * f);
+  w.hpost_re = c.take((size_t)T * k * Kq * f);
+  w.hres_re = c.take((size_t)T * k * k * f);
+  w.w0 = c.take((size_t)kC * k * f);
+  w.colsum0 = c.take((size_t)k * f);
+  w.wres0 = c.take((size_t)kC * k * k * f);
+  w.bres0 = c.take((size_t)k * k * f);
+  w.alpha2 = c.take(3 * f);
+  w.dwr = c.take((size_t)kC * k * f);
+  w.dwpre = c.take((size_t)kC * k * f);
+  w.dbpre = c.take((size_t)k * f);
+  w.dwres = c.take((size_t)kC * k * k * f);
+  w.dbres = c.take((size_t)k * k * f);
+  w.dalpha2 = c.take(3 * f);
+  w.total = c.total;
+  return w;
+}
+
+struct FlashPreBwdWs {
+  size_t pre, part, sums, saved, idx_s, p_s, hpre_s, hmask, wpost0, wres0, bres0, hpost0, dhpost0, dhres0, dp0,
+      alpha_e, dwr, dwres, dwpost, dalpha, dbres, dbpost, total;
+};
+
+FlashPreBwdWs flash_pre_bwd_ws(const xhc_dims* d, int Q) {
+  const xhc_dims e = dims_entry(d);
+  const int64_t T = d->T, N = d->N, k = d->k, C = d->C, NC = N * C, kC = k * C;
+  const size_t f = sizeof(float);
+  const int64_t nf = (int64_t)(Q + 1) * N;
+  Carve c;
+  FlashPreBwdWs w;
+  w.pre = c.take(bwd_pre_ws_bytes(&e));
+  w.part = c.take(part_bytes(d, false, NC, nf));
+  w.sums = c.take(sums_bytes(nf, T));
+  w.saved = c.take((size_t)T * saved_floats(N, k, 1) * f);
+  w.idx_s = c.take((size_t)T * k * sizeof(int32_t));
+  w.p_s = c.take((size_t)T * k * f);
+  w.hpre_s = c.take((size_t)Q * T * N * f);
+  w.hmask = c.take((size_t)T * N * f);
+  w.wpost0 = c.take((size_t)kC * k * f);
+  w.wres0 = c.take((size_t)kC * k * k * f);
+  w.bres0 = c.take((size_t)k * k * f);
+  w.hpost0 = c.take((size_t)T * k * f);
+  w.dhpost0 = c.take((size_t)T * k * f);
+  w.dhres0 = c.take((size_t)T * k * k * f);
+  w.dp0 = c.take((size_t)T * k * f);
+  w.alpha_e = c.take(3 * f);
+  w.dwr = c.take((size_t)NC * N * f);
+  w.dwres = c.take((size_t)kC * k * k * f);
+  w.dwpost = c.take((size_t)kC * k * f);
+  w.dalpha = c.take(3 * f);
+  w.dbres = c.take((size_t)k * k * f);
+  w.dbpost = c.take((size_t)k * f);
+  w.total = c.total;
+  return w;
+}
+
 size_t post_ws(const xhc_dims* d) {
   if (d->Kr == 1) return 0;
   const int np = d->Kr * (d->Kr + 1) / 2;
@@ -199,6 +331,14 @@ size_t xhc_workspace_bytes(const xhc_dims* d, int32_t op, int32_t Q) {
       for (int q = 1; q <= Q; ++q) need = std::max(need, flash_post_ws(d, Q, q));
       return need;
     }
+    case XHC_OP_FLASH_POST_BWD: {
+      if ((Q != 2 && Q != 4) || !flash_bwd_supported(d)) return 0;
+      size_t need = 0;
+      for (int q = 1; q <= Q; ++q) need = std::max(need, flash_post_bwd_ws(d, Q, q).total);
+      return need;
+    }
+    case XHC_OP_FLASH_PRE_BWD:
+      return ((Q == 2 || Q == 4) && flash_bwd_supported(d)) ? flash_pre_bwd_ws(d, Q).total : 0;
     default: return 0;
   }
 }
@@ -351,8 +491,8 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
                           const int32_t* idx, const float* p, const float* Hpost, const float* Hres,
                           const float* Hpre_next, const void* base_next, void* input_next,
                           const void* packed_act_next, const float* alpha_next, const float* b_post_next,
-                          const float* b_res_next, float* Hpost_next, float* Hres_next, void* workspace,
-                          size_t workspace_bytes, void* stream) {
+                          const float* b_res_next, float* Hpost_next, float* Hres_next, void* Xact_save,
+                          void* workspace, size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
   if ((Q != 2 && Q != 4) || q < 1 || q > Q) return XHC_EINVAL;
@@ -368,7 +508,8 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
     if ((q + 1 == Q) != (b_res_next != nullptr && Hres_next != nullptr)) return XHC_EINVAL;
     if (!aligned16(base_next) || !aligned16(input_next) || !aligned16(packed_act_next)) return XHC_EUNSUPPORTED;
   }
-  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w))) return XHC_EUNSUPPORTED;
+  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w)) || (Xact_save && !aligned16(Xact_save)))
+    return XHC_EUNSUPPORTED;
   const size_t need = flash_post_ws(d, Q, q);
   if (need > 0 && (!workspace || workspace_bytes < need)) return XHC_EWORKSPACE;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
@@ -387,7 +528,8 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
   }
   XHC_STEP("flash_post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, Kq, d->kappa,
                                                  conv_w, idx, p, Hres, Hpost, wb, last ? nullptr : Hpre_next,
-                                                 last ? nullptr : base_next, last ? nullptr : input_next, nullptr, s));
+                                                 last ? nullptr : base_next, last ? nullptr : input_next, Xact_save,
+                                                 s));
   if (!last) {
     // mappings of sublayer q + 1 from the updated active rows (Alg. xHC-Flash, MLP step; App. E.2)
     const int Kn = flash_Kq(d, q + 1);
@@ -457,6 +599,164 @@ xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full
   XHC_STEP("pre_bwd", launch_bwd_pre(d, X, colsum, W_r, W_pre, W_res, W_post, alpha, b_res, saved, idx, p, Hpre,
                                      Hpost, d_input, dHres, dHpost, dp, dX, dW_r, dW_pre, dW_res, dW_post, dalpha,
                                      db_pre, db_res, db_post, reinterpret_cast<char*>(workspace), s));
+  return hip_status(e);
+}
+
+// ---------------------------------------------------------------- xHC-Flash backward
+
+xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const void* dXn, void* da, const void* Xact,
+                              const void* F, const float* conv_w, const int32_t* idx, const float* p,
+                              const float* Hpost, const float* Hres, const void* packed_act, const float* W_post,
+                              const float* W_res, const float* alpha_post, const float* alpha_res,
+                              const float* b_post, const float* b_res, const float* Hpre_q, const void* d_input,
+                              void* dF, float* dconv_w, float* dW_post, float* dalpha_post, float* db_post,
+                              float* dW_res, float* dalpha_res, float* db_res, float* dp, float* dHpre_act,
+                              void* workspace, size_t workspace_bytes, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if ((Q != 2 && Q != 4) || q < 1 || q > Q) return XHC_EINVAL;
+  if (!flash_bwd_supported(d)) return XHC_EUNSUPPORTED;
+  if (d->T == 0) return XHC_OK;
+  const int Kq = flash_Kq(d, q);
+  const bool last = q == Q, reads = q >= 2;
+  if (!da || !Xact || !F || !idx || !p || !Hpost || !packed_act || !W_post || !alpha_post || !b_post || !dF ||
+      !dW_post || !dalpha_post || !db_post || !dp || !workspace)
+    return XHC_EINVAL;
+  if ((Kq > 1) != (conv_w != nullptr) || (Kq > 1) != (dconv_w != nullptr)) return XHC_EINVAL;
+  if (last != (dXn != nullptr) || last != (Hres != nullptr) || last != (W_res != nullptr) ||
+      last != (alpha_res != nullptr) || last != (b_res != nullptr) || last != (dW_res != nullptr) ||
+      last != (dalpha_res != nullptr) || last != (db_res != nullptr))
+    return XHC_EINVAL;
+  if (reads != (Hpre_q != nullptr) || reads != (d_input != nullptr) || reads != (dHpre_act != nullptr))
+    return XHC_EINVAL;
+  if (da == Xact || dF == F) return XHC_EINVAL;
+  if (!aligned16(da) || !aligned16(Xact) || !aligned16(F) || !aligned16(dF) || !aligned16(packed_act) ||
+      (dXn && !aligned16(dXn)) || (d_input && !aligned16(d_input)) || (conv_w && !aligned16(conv_w)) ||
+      (dconv_w && !aligned16(dconv_w)) || !aligned16(workspace))
+    return XHC_EUNSUPPORTED;
+  const FlashPostBwdWs w = flash_post_bwd_ws(d, Q, q);
+  if (workspace_bytes < w.total) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  char* ws = reinterpret_cast<char*>(workspace);
+  auto F32 = [&](size_t at) { return reinterpret_cast<float*>(ws + at); };
+  const int64_t T = d->T, k = d->k, C = d->C, kC = k * C;
+  const xhc_dims r = dims_rows32(d, Kq);
+  float* dA = reinterpret_cast<float*>(da);
+  int32_t* idx_id = reinterpret_cast<int32_t*>(ws + w.idx_id);
+  float* hres_use = last ? const_cast<float*>(Hres) : F32(w.hres_id);
+  hipError_t e = hipSuccess;
+  // zero the dummy operands (weights of the absent pre-map and router, the
+  // saved logits the recompute leaves empty), and for q < Q the residual
+  // mapping that sublayer does not have
+  XHC_STEP("fbwd_zero", launch_fill0(ws + w.saved, (size_t)T * saved_floats(k, k, Kq) * sizeof(float), s));
+  XHC_STEP("fbwd_zero", launch_fill0(ws + w.w0, w.wres0 - w.w0, s));   // w0, colsum0
+  if (!reads) XHC_STEP("fbwd_zero", launch_fill0(ws + w.din32, (size_t)T * C * sizeof(float), s));
+  if (!last) XHC_STEP("fbwd_zero", launch_fill0(ws + w.wres0, w.alpha2 - w.wres0, s));   // wres0, bres0
+  // slot map, identity mixing, pre-map weights of the active streams, <d input_q, a_j>
+  XHC_STEP("fbwd_token", launch_fbwd_token(d->state_dtype, T, d->N, (int)k, (int)C, idx, Hpre_q, d_input, Xact,
+                                           idx_id, last ? nullptr : F32(w.hres_id), F32(w.hsel), dHpre_act, s));
+  if (last) XHC_STEP("fbwd_gather", launch_fbwd_gather(d->state_dtype, T, d->N, (int)k, (int)C, idx, dXn, dA, s));
+  XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, Xact, F32(w.xact32), T * kC, s));
+  XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, F, F32(w.f32c), T * C, s));
+  if (reads) XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, d_input, F32(w.din32), T * C, s));
+  // write-back reverse on the active rows: dF, dH^post, dp and the mixing transpose
+  XHC_STEP("fbwd_post", launch_bwd_post(&r, dA, F32(w.xrest), F32(w.xact32), F32(w.f32c), conv_w, idx_id, p,
+                                        hres_use, Hpost, F32(w.da_out), F32(w.df32), F32(w.dhres), F32(w.dhpost),
+                                        F32(w.dp), dconv_w, ws + w.post, s));
+  XHC_STEP("fbwd_cvt", launch_fbwd_from_f32(d->state_dtype, F32(w.df32), dF, T * C, s));
+  XHC_STEP("fbwd_dp", launch_fbwd_add(dp, F32(w.dp), T * k, s));
+  if (!last) XHC_STEP("fbwd_zero", launch_fill0(ws + w.dhres, (size_t)T * k * k * sizeof(float), s));
+  // the mapping logits of sublayer q recomputed from a^(q-1) (same kernels and
+  // operands as the forward)
+  const int64_t na = act_outs(d, Kq, last);
+  const int nsave = saved_floats((int)k, (int)k, Kq);
+  XHC_STEP("fbwd_proj", launch_proj_partial(d->state_dtype, Xact, T, (int)k, (int)C, kC, packed_act, na, idx_id,
+                                            (int)k, F32(w.part), s));
+  XHC_STEP("fbwd_coef", launch_pre_coef(F32(w.part), proj_chunks(d->state_dtype, true, kC, (int)C, na, T), na, T,
+                                        (int)k, Kq, last, C, alpha_post, last ? alpha_res : nullptr, b_post,
+                                        last ? b_res : nullptr, d->eps, d->sinkhorn_iters, d->clamp_delta,
+                                        F32(w.hpost_re), last ? F32(w.hres_re) : nullptr, F32(w.sums), F32(w.saved),
+                                        nsave, 2 * (int)k, nsave - 2, s));
+  XHC_STEP("fbwd_alpha", launch_fbwd_alpha(nullptr, alpha_res, alpha_post, F32(w.alpha2), s));
+  // mapping reverse through a^(q-1) and the active part of input_q's read
+  XHC_STEP("fbwd_pre", launch_bwd_pre(&r, F32(w.xact32), F32(w.colsum0), F32(w.w0), F32(w.w0),
+                                      last ? W_res : F32(w.wres0), W_post, F32(w.alpha2),
+                                      last ? b_res : F32(w.bres0), F32(w.saved), idx_id, p, F32(w.hsel), Hpost,
+                                      F32(w.din32), F32(w.dhres), F32(w.dhpost), F32(w.dp), F32(w.da_out),
+                                      F32(w.dwr), F32(w.dwpre), last ? dW_res : F32(w.dwres), dW_post,
+                                      F32(w.dalpha2), F32(w.dbpre), last ? db_res : F32(w.dbres), db_post,
+                                      ws + w.pre, s));
+  XHC_STEP("fbwd_copy", hipMemcpyAsync(dalpha_post, F32(w.dalpha2) + 2, sizeof(float), hipMemcpyDeviceToDevice, s));
+  if (last)
+    XHC_STEP("fbwd_copy", hipMemcpyAsync(dalpha_res, F32(w.dalpha2) + 1, sizeof(float), hipMemcpyDeviceToDevice, s));
+  XHC_STEP("fbwd_copy",
+           hipMemcpyAsync(dA, F32(w.da_out), (size_t)T * kC * sizeof(float), hipMemcpyDeviceToDevice, s));
+  return hip_status(e);
+}
+
+xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full, const float* W_r,
+                             const float* W_pre, const float* alpha_pre, const float* b_pre, const int32_t* idx,
+                             const float* p, const float* Hpre, const void* d_input, const float* dHpre_act,
+                             const float* dp, const void* dXn, const void* da0, void* dX, float* dW_r,
+                             float* dW_pre, float* dalpha_pre, float* db_pre, void* workspace, size_t workspace_bytes,
+                             void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (Q != 2 && Q != 4) return XHC_EINVAL;
+  if ((int64_t)(Q + 1) * d->N > 128 || !flash_bwd_supported(d)) return XHC_EUNSUPPORTED;
+  if (d->T == 0) return XHC_OK;
+  if (!X || !packed_full || !W_r || !W_pre || !alpha_pre || !b_pre || !idx || !p || !Hpre || !d_input ||
+      !dHpre_act || !dp || !dXn || !da0 || !dX || !dW_r || !dW_pre || !dalpha_pre || !db_pre || !workspace)
+    return XHC_EINVAL;
+  if (dX == X || dX == dXn || dX == da0) return XHC_EINVAL;
+  if (!aligned16(X) || !aligned16(packed_full) || !aligned16(d_input) || !aligned16(dXn) || !aligned16(da0) ||
+      !aligned16(dX) || !aligned16(workspace))
+    return XHC_EUNSUPPORTED;
+  const FlashPreBwdWs w = flash_pre_bwd_ws(d, Q);
+  if (workspace_bytes < w.total) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  char* ws = reinterpret_cast<char*>(workspace);
+  auto F32 = [&](size_t at) { return reinterpret_cast<float*>(ws + at); };
+  const int64_t T = d->T, N = d->N, k = d->k, C = d->C, NC = N * C;
+  const size_t es = d->state_dtype == XHC_BF16 ? 2 : 4;   // d_input
+  const int64_t nf = (int64_t)(Q + 1) * N;
+  const xhc_dims en = dims_entry(d);
+  const int nsave = saved_floats((int)N, (int)k, 1);
+  const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
+                                                       packed_frag_bytes(NC, nf));
+  hipError_t e = hipSuccess;
+  XHC_STEP("fpbwd_zero", launch_fill0(ws + w.saved, (size_t)T * nsave * sizeof(float), s));
+  XHC_STEP("fpbwd_zero", launch_fill0(ws + w.wpost0, w.alpha_e - w.wpost0, s));   // zero operands
+  // the group-entry logits and statistics, recomputed as the forward made them
+  XHC_STEP("fpbwd_proj", launch_proj_partial(d->state_dtype, X, T, (int)N, (int)C, NC, packed_full, nf, nullptr,
+                                             (int)k, F32(w.part), s));
+  // dL/dX starts as the gradient of the state after the group: the untouched
+  // streams pass it through, the active ones carry the reverse of the group
+  XHC_STEP("fpbwd_scatter", launch_fbwd_scatter(d->state_dtype, T, (int)N, (int)k, (int)C, idx, dXn,
+                                                 reinterpret_cast<const float*>(da0), dX, s));
+  for (int q = 0; q < Q && e == hipSuccess; ++q) {
+    // pre-map q + 1 (and the router with the first): dL/dH^pre,q+1 of the
+    // active streams comes from the sublayer reverse (q >= 1); the base
+    // readouts of q >= 1 leave the active streams out
+    XHC_STEP("fpbwd_route", launch_pre_route(F32(w.part), proj_chunks(d->state_dtype, false, NC, (int)C, nf, T), nf,
+                                             T, (int)N, d->m, (int)k, Q, C, colsum, alpha_pre, 1, b_pre, d->eps,
+                                             reinterpret_cast<int32_t*>(ws + w.idx_s), F32(w.p_s), F32(w.hpre_s),
+                                             F32(w.sums), F32(w.saved), nsave, nsave - 4, d->router, s, q));
+    XHC_STEP("fpbwd_alpha", launch_fbwd_alpha(alpha_pre + q, nullptr, nullptr, F32(w.alpha_e), s));
+    if (q >= 1) XHC_STEP("fpbwd_mask", launch_fbwd_mask(T, (int)N, (int)k, idx, Hpre + (int64_t)q * T * N,
+                                                        F32(w.hmask), s));
+    XHC_STEP("fpbwd_pre",
+             launch_bwd_pre(&en, X, colsum, W_r, W_pre + (int64_t)q * NC * N, F32(w.wres0), F32(w.wpost0),
+                            F32(w.alpha_e), F32(w.bres0), F32(w.saved), idx, p, Hpre + (int64_t)q * T * N,
+                            F32(w.hpost0), reinterpret_cast<const char*>(d_input) + (size_t)q * T * C * es,
+                            F32(w.dhres0), F32(w.dhpost0), q == 0 ? dp : F32(w.dp0), dX, q == 0 ? dW_r : F32(w.dwr),
+                            dW_pre + (int64_t)q * NC * N, F32(w.dwres), F32(w.dwpost), F32(w.dalpha),
+                            db_pre + (int64_t)q * N, F32(w.dbres), F32(w.dbpost), ws + w.pre, s,
+                            q >= 1 ? dHpre_act + (int64_t)(q - 1) * T * k : nullptr, q >= 1 ? F32(w.hmask) : nullptr));
+    XHC_STEP("fpbwd_copy", hipMemcpyAsync(dalpha_pre + q, F32(w.dalpha), sizeof(float), hipMemcpyDeviceToDevice, s));
+  }
   return hip_status(e);
 }
 

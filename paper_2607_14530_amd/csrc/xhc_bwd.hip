@@ -616,6 +616,18 @@ __global__ __launch_bounds__(256) void k_bwd_dhpre(const TS* __restrict__ X, con
 //   [dz_r (N) | dz_pre (N) | dz_act (NA) | r | r_ln | mu | beta_pre | m1 | m2 | r_a | beta_a]
 // and per-token gating/bias gradients pg: [dalpha_pre, dalpha_res, dalpha_post | db_pre (N) |
 // db_res (k*k) | db_post (k*Kr)].
+// dL/dH^pre of the active streams given per slot: the chunk partials of
+// <d input, x_i> at i = idx[t, j] become dhact[t, j] (first chunk) and 0.
+__global__ __launch_bounds__(256) void k_bwd_dhpre_override(const float* __restrict__ dhact,
+                                                            const int32_t* __restrict__ idx, int64_t T, int N, int k,
+                                                            int64_t nchunk, float* __restrict__ part) {
+  const int64_t u = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= T * k) return;
+  const int64_t t = u / k;
+  const int i = idx[u];
+  for (int64_t c = 0; c < nchunk; ++c) part[(c * N + i) * T + t] = c == 0 ? dhact[u] : 0.0f;
+}
+
 __host__ __device__ inline int tok_floats(int N, int NA) { return 2 * N + NA + 8; }
 __host__ __device__ inline int pg_floats(int N, int k, int Kr) { return 3 + N + k * k + k * Kr; }
 
@@ -1246,7 +1258,8 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
-                          hipStream_t s) {
+                          hipStream_t s, const float* dhpre_act, const float* Hpre_read) {
+  const float* Hrd = Hpre_read ? Hpre_read : Hpre;   // weights of the dense-read term
   const int64_t T = d->T;
   const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
   const int NA = k * Kr + k * k;
@@ -1263,6 +1276,10 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
   XHC_TS_DISPATCH(d->state_dtype,
     k_bwd_dhpre<TS><<<dim3((unsigned)(T * ncb)), dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),
         reinterpret_cast<const TS*>(d_input), T, N, C, part));
+  if (dhpre_act) {
+    k_bwd_dhpre_override<<<dim3((unsigned)((T * k + 255) / 256)), dim3(256), 0, s>>>(dhpre_act, idx, T, N, k, ncb,
+                                                                                    part);
+  }
   {
     const dim3 gt((unsigned)((T + kPreTokThreads - 1) / kPreTokThreads)), bt(kPreTokThreads);
     if (k == 4 && 2 * d->sinkhorn_iters <= kSkMaxSteps)
@@ -1282,7 +1299,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
   if (mf) {
     const dim3 gf((unsigned)((int64_t)N * C / kMfRows), (unsigned)nchunk);
     k_bwd_rows_mfma<false><<<gf, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
-        reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hpre, idx, tok, T,
+        reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T,
         N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
     const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
     k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
@@ -1294,7 +1311,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
 #define XHC_FULL_ROWS(NNV)                                                                                       \
   XHC_TS_DISPATCH(d->state_dtype,                                                                                \
     k_bwd_full_rows<TS, NNV><<<gfull, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),                        \
-        reinterpret_cast<const TS*>(d_input), reinterpret_cast<TS*>(dX), W_r, W_pre, Hpre, tok, T, C, NA,        \
+        reinterpret_cast<const TS*>(d_input), reinterpret_cast<TS*>(dX), W_r, W_pre, Hrd, tok, T, C, NA,         \
         kRowChunk, wpart_r, wpart_p))
   if (!mf) {
     switch (N) {

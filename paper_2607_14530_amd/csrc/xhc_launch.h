@@ -76,7 +76,8 @@ hipError_t launch_proj_partial(int state_dtype, const void* X, int64_t T, int N,
 hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int64_t T, int N, int m, int k,
                             int npre, int64_t C, const float* colsum, const float* alpha_pre, int alpha_stride,
                             const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, float* sums,
-                            float* saved, int nsave, int save_stats_at, int router, hipStream_t s);
+                            float* saved, int nsave, int save_stats_at, int router, hipStream_t s,
+                            int save_pre = 0);   // which pre-map's z goes to saved[N .. 2N)
 hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int64_t T, int k, int Kq,
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,
@@ -128,7 +129,25 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
-                          hipStream_t s);
+                          hipStream_t s, const float* dhpre_act = nullptr, const float* Hpre_read = nullptr);
+// dhpre_act [T,k]: when given, dL/dH^pre of the active streams (slot order)
+// replaces <d input, x_i> there; Hpre_read [T,N]: when given, the weights of
+// the dense-read term dX_i += H^pre_i d input (Hpre otherwise).
+
+// ---- xHC-Flash backward helpers
+hipError_t launch_fill0(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_fbwd_token(int state_dtype, int64_t T, int N, int k, int C, const int32_t* idx,
+                             const float* Hpre_q, const void* din, const void* Xact, int32_t* idx_id, float* Hres_id,
+                             float* Hsel, float* dhact, hipStream_t s);
+hipError_t launch_fbwd_gather(int state_dtype, int64_t T, int N, int k, int C, const int32_t* idx, const void* dXn,
+                              float* da, hipStream_t s);
+hipError_t launch_fbwd_scatter(int state_dtype, int64_t T, int N, int k, int C, const int32_t* idx, const void* GX,
+                               const float* da0, void* dX, hipStream_t s);
+hipError_t launch_fbwd_to_f32(int state_dtype, const void* src, float* dst, int64_t n, hipStream_t s);
+hipError_t launch_fbwd_from_f32(int state_dtype, const float* src, void* dst, int64_t n, hipStream_t s);
+hipError_t launch_fbwd_mask(int64_t T, int N, int k, const int32_t* idx, const float* Hpre, float* Hm, hipStream_t s);
+hipError_t launch_fbwd_add(float* dst, const float* src, int64_t n, hipStream_t s);
+hipError_t launch_fbwd_alpha(const float* a0, const float* a1, const float* a2, float* out, hipStream_t s);
 
 // per-token values xhc_pre saves for the backward: [z_r (N) | z_pre (N) |
 // z_post, z_res (k*Kr + k*k) | mu | nu | nu_a | pad], z = normalised logits

@@ -100,7 +100,7 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
                                                    const float* __restrict__ b_pre, float eps,
                                                    int32_t* __restrict__ idx, float* __restrict__ p,
                                                    float* __restrict__ Hpre, float* __restrict__ saved,
-                                                   int nsave, int save_stats_at, int softmax) {
+                                                   int nsave, int save_stats_at, int softmax, int save_pre) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
   const float mu = sums[(int64_t)(NO - 2) * T + t] / (float)NC;
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
     const float a = alpha_pre[q * alpha_stride];
     for (int i = 0; i < N; ++i) {
       const float zp = sums[(int64_t)(N + q * N + i) * T + t] * r_rms;
-      if (saved && q == 0) saved[t * nsave + N + i] = zp;
+      if (saved && q == save_pre) saved[t * nsave + N + i] = zp;
       Hpre[((int64_t)q * T + t) * N + i] = sigmoidf(a * zp + b_pre[q * N + i]);
     }
   }
@@ -271,14 +271,14 @@ static hipError_t sum_chunks(const float* part, int64_t nchunk, int NO, int64_t 
 hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int64_t T, int N, int m, int k,
                             int npre, int64_t C, const float* colsum, const float* alpha_pre, int alpha_stride,
                             const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, float* sums,
-                            float* saved, int nsave, int save_stats_at, int router, hipStream_t s) {
+                            float* saved, int nsave, int save_stats_at, int router, hipStream_t s, int save_pre) {
   if (T == 0) return hipSuccess;
   const int NO = (int)out_blocks(nout) * 16 + 2;
   hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
   if (e != hipSuccess) return e;
   k_pre_route<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
       sums, NO, T, N, m, k, npre, (int64_t)N * C, colsum, alpha_pre, alpha_stride, b_pre, eps, idx, p, Hpre,
-      saved, nsave, save_stats_at, router == XHC_ROUTER_SOFTMAX ? 1 : 0);
+      saved, nsave, save_stats_at, router == XHC_ROUTER_SOFTMAX ? 1 : 0, save_pre);
   return hipGetLastError();
 }
 

@@ -27,7 +27,8 @@ STATUS_NAMES = {0: "XHC_OK", 1: "XHC_EINVAL", 2: "XHC_EUNSUPPORTED", 3: "XHC_EWO
 XHC_BF16, XHC_F32 = 0, 1
 XHC_IMPL_AUTO, XHC_IMPL_MULTI, XHC_IMPL_FUSED = 0, 1, 2
 XHC_ROUTER_SIGMOID, XHC_ROUTER_SOFTMAX = 0, 1
-XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST, XHC_OP_POST_BWD, XHC_OP_PRE_BWD = range(6)
+(XHC_OP_PRE, XHC_OP_POST, XHC_OP_FLASH_PRE, XHC_OP_FLASH_POST, XHC_OP_POST_BWD, XHC_OP_PRE_BWD,
+ XHC_OP_FLASH_POST_BWD, XHC_OP_FLASH_PRE_BWD) = range(8)
 
 
 class XhcError(RuntimeError):
@@ -82,7 +83,9 @@ _SIGS = {
     "xhc_post": (ctypes.c_int, [_D] + [_P] * 9 + [ctypes.c_size_t, _P]),
     "xhc_saved_floats": (ctypes.c_size_t, [_D]),
     "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 14 + [ctypes.c_size_t, _P]),
-    "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 17 + [ctypes.c_size_t, _P]),
+    "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 18 + [ctypes.c_size_t, _P]),
+    "xhc_flash_post_bwd": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 29 + [ctypes.c_size_t, _P]),
+    "xhc_flash_pre_bwd": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 20 + [ctypes.c_size_t, _P]),
     "xhc_post_bwd": (ctypes.c_int, [_D] + [_P] * 16 + [ctypes.c_size_t, _P]),
     "xhc_pre_bwd": (ctypes.c_int, [_D] + [_P] * 27 + [ctypes.c_size_t, _P]),
     "xhc_stream_sum": (ctypes.c_int, [_D, _P, _P, _P]),
@@ -196,10 +199,28 @@ def xhc_flash_pre(d, Q, X, packed_full, packed_act1, alpha_pre, b_pre, alpha_pos
 
 
 def xhc_flash_post(d, Q, q, X, F, conv_w, idx, p, Hpost, Hres, Hpre_next, base_next, input_next, packed_act_next,
-                   alpha_next, b_post_next, b_res_next, Hpost_next, Hres_next, workspace, stream=None):
+                   alpha_next, b_post_next, b_res_next, Hpost_next, Hres_next, Xact_save, workspace, stream=None):
     _call("xhc_flash_post", ctypes.byref(d), Q, q, _ptr(X), _ptr(F), _ptr(conv_w), _ptr(idx), _ptr(p),
           _ptr(Hpost), _ptr(Hres), _ptr(Hpre_next), _ptr(base_next), _ptr(input_next), _ptr(packed_act_next),
           _ptr(alpha_next), _ptr(b_post_next), _ptr(b_res_next), _ptr(Hpost_next), _ptr(Hres_next),
+          _ptr(Xact_save), _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
+def xhc_flash_post_bwd(d, Q, q, dXn, da, Xact, F, conv_w, idx, p, Hpost, Hres, packed_act, W_post, W_res,
+                       alpha_post, alpha_res, b_post, b_res, Hpre_q, d_input, dF, dconv_w, dW_post, dalpha_post,
+                       db_post, dW_res, dalpha_res, db_res, dp, dHpre_act, workspace, stream=None):
+    _call("xhc_flash_post_bwd", ctypes.byref(d), Q, q, _ptr(dXn), _ptr(da), _ptr(Xact), _ptr(F), _ptr(conv_w),
+          _ptr(idx), _ptr(p), _ptr(Hpost), _ptr(Hres), _ptr(packed_act), _ptr(W_post), _ptr(W_res),
+          _ptr(alpha_post), _ptr(alpha_res), _ptr(b_post), _ptr(b_res), _ptr(Hpre_q), _ptr(d_input), _ptr(dF),
+          _ptr(dconv_w), _ptr(dW_post), _ptr(dalpha_post), _ptr(db_post), _ptr(dW_res), _ptr(dalpha_res),
+          _ptr(db_res), _ptr(dp), _ptr(dHpre_act), _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
+def xhc_flash_pre_bwd(d, Q, X, packed_full, W_r, W_pre, alpha_pre, b_pre, idx, p, Hpre, d_input, dHpre_act, dp,
+                      dXn, da0, dX, dW_r, dW_pre, dalpha_pre, db_pre, workspace, stream=None):
+    _call("xhc_flash_pre_bwd", ctypes.byref(d), Q, _ptr(X), _ptr(packed_full), _ptr(W_r), _ptr(W_pre),
+          _ptr(alpha_pre), _ptr(b_pre), _ptr(idx), _ptr(p), _ptr(Hpre), _ptr(d_input), _ptr(dHpre_act), _ptr(dp),
+          _ptr(dXn), _ptr(da0), _ptr(dX), _ptr(dW_r), _ptr(dW_pre), _ptr(dalpha_pre), _ptr(db_pre),
           _ptr(workspace), _nbytes(workspace), _stream(stream))
 
 
@@ -325,7 +346,7 @@ class FlashGroup:
                       self.alpha_post[0], self.b_post[0], self.inputs[0], self.base, self.idx, self.p, self.Hpre,
                       self.Hpost[0], self.ws_pre, stream)
 
-    def step(self, q, X, F, stream=None):
+    def step(self, q, X, F, stream=None, Xact_save=None):
         """Write-back of sublayer q (1-based); for q < Q also forms inputs[q]."""
         Q = self.Q
         last = q == Q
@@ -338,13 +359,87 @@ class FlashGroup:
             None if last else self.alpha_post[nxt], None if last else self.b_post[nxt],
             self.b_res if (not last and q + 1 == Q) else None,
             None if last else self.Hpost[nxt], self.Hres if (not last and q + 1 == Q) else None,
-            self.ws_post, stream)
+            Xact_save, self.ws_post, stream)
 
     def run(self, X, F_list, stream=None):
         self.pre(X, stream)
         for q in range(1, self.Q + 1):
             self.step(q, X, F_list[q - 1], stream)
         return X
+
+
+class TrainableFlashGroup(FlashGroup):
+    """A FlashGroup that keeps what the backward needs and runs it.
+
+    forward(X, F_list): xhc_flash_pre, then xhc_flash_post for q = 1..Q saving
+    the active rows before each write-back; X is updated in place.
+    backward(X0, dXn, d_inputs, F_list): the reverse sweep, xhc_flash_post_bwd
+    for q = Q..1 then xhc_flash_pre_bwd on the group-entry state X0 (the
+    caller keeps X0: the group overwrites the active rows of X).  Returns a
+    dict of gradients keyed like the oracle's (X, F_list, conv_w_list, W_r,
+    W_pre_list, W_post_list, W_res, alpha_pre, b_pre, alpha_post, b_post,
+    alpha_res, b_res)."""
+
+    def __init__(self, d: Dims, Q: int, weights, device="cuda"):
+        super().__init__(d, Q, weights, device)
+        dev = torch.device(device)
+        T, N, k, C = d.T, d.N, d.k, d.C
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.W_r = weights["W_r"].to(dev).contiguous().float()
+        self.W_pre = torch.stack([w.to(dev) for w in weights["W_pre_list"]]).contiguous().float()
+        self.W_post = [w.to(dev).contiguous().float() for w in weights["W_post_list"]]
+        self.W_res = weights["W_res"].to(dev).contiguous().float()
+        self.a_post = [torch.tensor([a], **f32) for a in weights["alpha_post"]]
+        self.a_res = torch.tensor([weights["alpha_res"]], **f32)
+        self.Xact = [torch.empty(T, k, C, dtype=self.inputs[0].dtype, device=dev) for _ in range(Q)]
+        self.ws_post_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_POST_BWD, Q), dev)
+        self.ws_pre_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_PRE_BWD, Q), dev)
+
+    def forward(self, X, F_list, stream=None):
+        self.pre(X, stream)
+        for q in range(1, self.Q + 1):
+            self.step(q, X, F_list[q - 1], stream, Xact_save=self.Xact[q - 1])
+        return X
+
+    def backward(self, X0, dXn, d_inputs, F_list, stream=None):
+        d, Q = self.d, self.Q
+        T, N, k, C = d.T, d.N, d.k, d.C
+        dev = X0.device
+        f32 = dict(dtype=torch.float32, device=dev)
+        sdt = self.inputs[0].dtype
+        g = {"F_list": [None] * Q, "conv_w_list": [None] * Q, "W_post_list": [None] * Q, "b_post": [None] * Q}
+        da = torch.empty(T, k, C, **f32)
+        dp = torch.zeros(T, k, **f32)
+        dhact = torch.empty(max(Q - 1, 1), T, k, **f32)
+        a_post = torch.empty(Q, **f32)
+        g["W_res"], g["b_res"] = torch.empty_like(self.W_res), torch.empty(k * k, **f32)
+        a_res = torch.empty(1, **f32)
+        for q in range(Q, 0, -1):
+            last, Kq = q == Q, flash_Kq(d, q)
+            g["F_list"][q - 1] = torch.empty(T, C, dtype=sdt, device=dev)
+            g["conv_w_list"][q - 1] = torch.empty_like(self.conv_w[q - 1]) if self.conv_w[q - 1] is not None else None
+            g["W_post_list"][q - 1] = torch.empty_like(self.W_post[q - 1])
+            g["b_post"][q - 1] = torch.empty(k * Kq, **f32)
+            xhc_flash_post_bwd(
+                d, Q, q, dXn if last else None, da, self.Xact[q - 1], F_list[q - 1], self.conv_w[q - 1], self.idx,
+                self.p, self.Hpost[q - 1], self.Hres if last else None, self.packed_act[q - 1], self.W_post[q - 1],
+                self.W_res if last else None, self.a_post[q - 1], self.a_res if last else None, self.b_post[q - 1],
+                self.b_res if last else None, self.Hpre[q - 1] if q >= 2 else None,
+                d_inputs[q - 1] if q >= 2 else None, g["F_list"][q - 1], g["conv_w_list"][q - 1],
+                g["W_post_list"][q - 1], a_post[q - 1:q], g["b_post"][q - 1], g["W_res"] if last else None,
+                a_res if last else None, g["b_res"] if last else None, dp, dhact[q - 2] if q >= 2 else None,
+                self.ws_post_bwd, stream)
+        din = torch.stack(list(d_inputs)).contiguous()
+        g["X"] = torch.empty_like(X0)
+        g["W_r"], g["W_pre"] = torch.empty_like(self.W_r), torch.empty_like(self.W_pre)
+        g["alpha_pre"], g["b_pre"] = torch.empty(Q, **f32), torch.empty(Q, N, **f32)
+        xhc_flash_pre_bwd(d, Q, X0, self.packed_full, self.W_r, self.W_pre, self.alpha_pre, self.b_pre, self.idx,
+                          self.p, self.Hpre, din, dhact, dp, dXn, da, g["X"], g["W_r"], g["W_pre"], g["alpha_pre"],
+                          g["b_pre"], self.ws_pre_bwd, stream)
+        g["W_pre_list"] = list(g.pop("W_pre"))
+        g["b_pre"] = list(g["b_pre"])
+        g["alpha_post"], g["alpha_res"] = a_post, a_res[0]
+        return g
 
 
 class TrainableSublayer(Sublayer):
