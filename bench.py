@@ -193,6 +193,21 @@ def extra_sections(dev, stream, iters=5):
     out["bwd_n16_mlp"] = {"workload": "xHC MLP-type sublayer backward, T=8192, N=16, k=4, m=2, C=4096",
                           "ms_forward_with_saves": fwd_ms, "ms_backward": ms - fwd_ms,
                           "tokens_per_s_backward": w.T / ((ms - fwd_ms) * 1e-3)}
+    del sub, inp, st
+    torch.cuda.empty_cache()
+    # xHC-Flash group backward, Q = 4, T = 8192, N = 16, k = 4, C = 4096
+    w = synth.bwd_sweep(16, 4)
+    Q = 4
+    fd = synth.flash_inputs(w, Q, 13, device=dev, grads=True)
+    grp = X.TrainableFlashGroup(X.dims_for(w), Q, fd, dev)
+    X0 = fd["X"]
+    st = X0.clone()
+    ffwd = _time(lambda: (st.copy_(X0), grp.forward(st, fd["F_list"], stream)), 2, stream)
+    cp = _time(lambda: st.copy_(X0), 2, stream)
+    fbwd = _time(lambda: grp.backward(X0, fd["G_X"], fd["G_in_list"], fd["F_list"], stream), 2, stream)
+    out["flash_bwd_q4"] = {"workload": "xHC-Flash group backward, Q=4, T=8192, N=16, k=4, m=2, C=4096",
+                           "ms_forward_with_saves": ffwd - cp, "ms_backward": fbwd,
+                           "tokens_per_s_per_sublayer_backward": Q * w.T / (fbwd * 1e-3)}
     return out
 
 

@@ -164,7 +164,7 @@ xhc_dims dims_rows32(const xhc_dims* d, int Kq) {
 }
 
 struct FlashPostBwdWs {
-  size_t post, pre, part, sums, idx_id, hres_id, hsel, xrest, da_out, xact32, f32c, din32, df32, dhpost, dhres, dp,
+  size_t post, pre, part, sums, idx_id, hres_id, hsel, xrest, da_out, xact32, f32c, df32, dhpost, dhres, dp,
       saved, hpost_re, hres_re, w0, colsum0, wres0, bres0, alpha2, dwr, dwpre, dbpre, dwres, dbres, dalpha2, total;
 };
 
@@ -187,7 +187,6 @@ FlashPostBwdWs flash_post_bwd_ws(const xhc_dims* d, int Q, int q) {
   w.da_out = c.take((size_t)T * kC * f);
   w.xact32 = c.take((size_t)T * kC * f);
   w.f32c = c.take((size_t)T * C * f);
-  w.din32 = c.take((size_t)T * C * f);
   w.df32 = c.take((size_t)T * C * f);
   w.dhpost = c.take((size_t)T * k * Kq * f);
   w.dhres = c.take((size_t)T * k * k * f);
@@ -651,7 +650,6 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   // mapping that sublayer does not have
   XHC_STEP("fbwd_zero", launch_fill0(ws + w.saved, (size_t)T * saved_floats(k, k, Kq) * sizeof(float), s));
   XHC_STEP("fbwd_zero", launch_fill0(ws + w.w0, w.wres0 - w.w0, s));   // w0, colsum0
-  if (!reads) XHC_STEP("fbwd_zero", launch_fill0(ws + w.din32, (size_t)T * C * sizeof(float), s));
   if (!last) XHC_STEP("fbwd_zero", launch_fill0(ws + w.wres0, w.alpha2 - w.wres0, s));   // wres0, bres0
   // slot map, identity mixing, pre-map weights of the active streams, <d input_q, a_j>
   XHC_STEP("fbwd_token", launch_fbwd_token(d->state_dtype, T, d->N, (int)k, (int)C, idx, Hpre_q, d_input, Xact,
@@ -659,7 +657,6 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   if (last) XHC_STEP("fbwd_gather", launch_fbwd_gather(d->state_dtype, T, d->N, (int)k, (int)C, idx, dXn, dA, s));
   XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, Xact, F32(w.xact32), T * kC, s));
   XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, F, F32(w.f32c), T * C, s));
-  if (reads) XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, d_input, F32(w.din32), T * C, s));
   // write-back reverse on the active rows: dF, dH^post, dp and the mixing transpose
   XHC_STEP("fbwd_post", launch_bwd_post(&r, dA, F32(w.xrest), F32(w.xact32), F32(w.f32c), conv_w, idx_id, p,
                                         hres_use, Hpost, F32(w.da_out), F32(w.df32), F32(w.dhres), F32(w.dhpost),
@@ -679,19 +676,22 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
                                         F32(w.hpost_re), last ? F32(w.hres_re) : nullptr, F32(w.sums), F32(w.saved),
                                         nsave, 2 * (int)k, nsave - 2, s));
   XHC_STEP("fbwd_alpha", launch_fbwd_alpha(nullptr, alpha_res, alpha_post, F32(w.alpha2), s));
-  // mapping reverse through a^(q-1) and the active part of input_q's read
+  // mapping reverse through a^(q-1) (its dense-row terms are all zero here:
+  // no router or pre-map weights)
   XHC_STEP("fbwd_pre", launch_bwd_pre(&r, F32(w.xact32), F32(w.colsum0), F32(w.w0), F32(w.w0),
                                       last ? W_res : F32(w.wres0), W_post, F32(w.alpha2),
                                       last ? b_res : F32(w.bres0), F32(w.saved), idx_id, p, F32(w.hsel), Hpost,
-                                      F32(w.din32), F32(w.dhres), F32(w.dhpost), F32(w.dp), F32(w.da_out),
+                                      nullptr, F32(w.dhres), F32(w.dhpost), F32(w.dp), F32(w.da_out),
                                       F32(w.dwr), F32(w.dwpre), last ? dW_res : F32(w.dwres), dW_post,
                                       F32(w.dalpha2), F32(w.dbpre), last ? db_res : F32(w.dbres), db_post,
-                                      ws + w.pre, s));
+                                      ws + w.pre, s, nullptr, nullptr, /*dense_rows=*/false,
+                                      d->state_dtype == XHC_BF16 ? Xact : nullptr));
   XHC_STEP("fbwd_copy", hipMemcpyAsync(dalpha_post, F32(w.dalpha2) + 2, sizeof(float), hipMemcpyDeviceToDevice, s));
   if (last)
     XHC_STEP("fbwd_copy", hipMemcpyAsync(dalpha_res, F32(w.dalpha2) + 1, sizeof(float), hipMemcpyDeviceToDevice, s));
-  XHC_STEP("fbwd_copy",
-           hipMemcpyAsync(dA, F32(w.da_out), (size_t)T * kC * sizeof(float), hipMemcpyDeviceToDevice, s));
+  // da = (reverse so far) + H^pre,q_{I_j} d input_q (the active part of input_q's read)
+  XHC_STEP("fbwd_finish", launch_fbwd_finish(d->state_dtype, T, (int)k, (int)C, F32(w.da_out), F32(w.hsel),
+                                             reads ? d_input : nullptr, dA, s));
   return hip_status(e);
 }
 

@@ -764,6 +764,13 @@ __global__ __launch_bounds__(kPreTokThreads) void k_bwd_pre_token(
 //               + r_ln ((W_r dz_r) - m1 - r_ln (x - mu) m2)
 // and the row's weight gradients accumulate x r dz_pre and r_ln (x - mu) dz_r.
 constexpr int kRowTok = 32;   // tokens staged in LDS per step
+constexpr int kRowBatch = 8;  // tokens whose elements one thread loads together
+static_assert(kRowTok % kRowBatch == 0, "whole batches per staged step");
+
+__device__ __forceinline__ float ld_elem(const uint16_t* p, int64_t i) { return __uint_as_float((uint32_t)p[i] << 16); }
+__device__ __forceinline__ float ld_elem(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ void st_elem(uint16_t* p, int64_t i, float v) { p[i] = (uint16_t)f2bf(v); }
+__device__ __forceinline__ void st_elem(float* p, int64_t i, float v) { p[i] = v; }
 template <typename TS, int NN>
 __global__ __launch_bounds__(256) void k_bwd_full_rows(const TS* __restrict__ X, const TS* __restrict__ din,
                                                        TS* __restrict__ dX, const float* __restrict__ W_r,
@@ -799,34 +806,40 @@ __global__ __launch_bounds__(256) void k_bwd_full_rows(const TS* __restrict__ X,
     for (int u = threadIdx.x; u < nt; u += 256) shp[u] = Hpre[(tb + u) * NN + istream];
     __syncthreads();
     if (!valid) continue;
-#pragma unroll 4
-    for (int u = 0; u < nt; ++u) {
-      const int64_t t = tb + u;
-      const float* z = sdz[u];
-      const float r = z[2 * NN + 0], r_ln = z[2 * NN + 1], mu = z[2 * NN + 2], bpre = z[2 * NN + 3];
-      const float m1 = z[2 * NN + 4], m2 = z[2 * NN + 5];
-      const int64_t off = t * NC + K;
-      const float x = (sizeof(TS) == 2) ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(X)[off] << 16)
-                                         : reinterpret_cast<const float*>(X)[off];
-      const float gi = (sizeof(TS) == 2) ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(din)[t * C + c] << 16)
-                                          : reinterpret_cast<const float*>(din)[t * C + c];
-      float sr = 0.f, sp = 0.f;
-      const float xh = (x - mu) * r_ln, xr = x * r;
+    // the elements of kRowBatch tokens are loaded before any is written back:
+    // the accumulator rows are read and written in place, so a load after a
+    // store of the same array would wait for it
+    for (int u0 = 0; u0 < nt; u0 += kRowBatch) {
+      float xb[kRowBatch], gb[kRowBatch], db[kRowBatch];
 #pragma unroll
-      for (int o = 0; o < NN; ++o) {
-        sr = fmaf(wr[o], z[o], sr);
-        sp = fmaf(wp[o], z[NN + o], sp);
-        gr[o] = fmaf(xh, z[o], gr[o]);
-        gp[o] = fmaf(xr, z[NN + o], gp[o]);
+      for (int e = 0; e < kRowBatch; ++e) {
+        xb[e] = gb[e] = db[e] = 0.f;
+        if (u0 + e < nt) {
+          const int64_t t = tb + u0 + e, off = t * NC + K;
+          xb[e] = ld_elem(X, off);
+          gb[e] = ld_elem(din, t * C + c);
+          db[e] = ld_elem(dX, off);
+        }
       }
-      float g = shp[u] * gi + r * sp - bpre * x + r_ln * (sr - m1) - r_ln * (x - mu) * r_ln * m2;
-      if (sizeof(TS) == 2) {
-        uint16_t* d = reinterpret_cast<uint16_t*>(dX) + off;
-        g += __uint_as_float((uint32_t)*d << 16);
-        *d = (uint16_t)f2bf(g);
-      } else {
-        float* d = reinterpret_cast<float*>(dX) + off;
-        *d += g;
+#pragma unroll
+      for (int e = 0; e < kRowBatch; ++e) {
+        if (u0 + e >= nt) break;
+        const int u = u0 + e;
+        const float* z = sdz[u];
+        const float r = z[2 * NN + 0], r_ln = z[2 * NN + 1], mu = z[2 * NN + 2], bpre = z[2 * NN + 3];
+        const float m1 = z[2 * NN + 4], m2 = z[2 * NN + 5];
+        const float x = xb[e];
+        float sr = 0.f, sp = 0.f;
+        const float xh = (x - mu) * r_ln, xr = x * r;
+#pragma unroll
+        for (int o = 0; o < NN; ++o) {
+          sr = fmaf(wr[o], z[o], sr);
+          sp = fmaf(wp[o], z[NN + o], sp);
+          gr[o] = fmaf(xh, z[o], gr[o]);
+          gp[o] = fmaf(xr, z[NN + o], gp[o]);
+        }
+        const float g = shp[u] * gb[e] + r * sp - bpre * x + r_ln * (sr - m1) - r_ln * (x - mu) * r_ln * m2;
+        st_elem(dX, (tb + u) * NC + K, db[e] + g);
       }
     }
   }
@@ -839,6 +852,8 @@ __global__ __launch_bounds__(256) void k_bwd_full_rows(const TS* __restrict__ X,
 
 // Weight-stationary pass over rows K = j*C + c of [W_post | W_res] (slot j):
 //   dX[t, I_j, c] += r_a (W_act dz_act) - beta_a a,   dW_act[K] += r_a a dz_act.
+// The NA outputs are padded with zeros to NAMAX (zero weights and logit
+// gradients), so every row runs the same branch-free contraction.
 template <typename TS, int NAMAX>
 __global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, TS* __restrict__ dX,
                                                       const float* __restrict__ W_post,
@@ -846,9 +861,11 @@ __global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, 
                                                       const int32_t* __restrict__ idx,
                                                       const float* __restrict__ tok, int64_t T, int N, int k, int C,
                                                       int Kr, int64_t tchunk, float* __restrict__ dWa_part) {
+  static_assert(NAMAX % 4 == 0, "float4 rows");
+  constexpr int ZP = NAMAX + 4;   // per token: dz_act (zero past NA), r_a, beta_a, 2 pad
   const int NA = k * Kr + k * k, NP = k * Kr;
-  __shared__ float sdz[kRowTok][NAMAX + 2];
-  __shared__ int sid[kRowTok];
+  __shared__ __align__(16) float sdz[kRowTok][ZP];
+  __shared__ int64_t sbase[kRowTok];
   const int64_t kC = (int64_t)k * C;
   const int64_t K = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const bool valid = K < kC;
@@ -868,37 +885,60 @@ __global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, 
   for (int64_t tb = t0; tb < t1; tb += kRowTok) {
     const int nt = (int)((t1 - tb < kRowTok) ? t1 - tb : kRowTok);
     __syncthreads();
-    for (int q = threadIdx.x; q < nt * (NA + 2); q += 256) {
-      const int u = q / (NA + 2), f = q % (NA + 2);
-      const float* tk = tok + (tb + u) * TF;
-      sdz[u][f] = (f < NA) ? tk[2 * N + f] : tk[2 * N + NA + 6 + (f - NA)];
+    for (int q = threadIdx.x; q < kRowTok * ZP; q += 256) {
+      const int u = q / ZP, f = q % ZP;
+      float v = 0.f;
+      if (u < nt) {
+        const float* tk = tok + (tb + u) * TF;
+        if (f < NA) v = tk[2 * N + f];
+        else if (f == NAMAX) v = tk[2 * N + NA + 6];
+        else if (f == NAMAX + 1) v = tk[2 * N + NA + 7];
+      }
+      sdz[u][f] = v;
     }
-    for (int u = threadIdx.x; u < nt; u += 256) sid[u] = idx[(tb + u) * k + j];
+    if (threadIdx.x < kRowTok) {
+      const int u = threadIdx.x < nt ? threadIdx.x : nt - 1;
+      sbase[threadIdx.x] = ((tb + u) * N + idx[(tb + u) * k + j]) * (int64_t)C;
+    }
     __syncthreads();
     if (!valid) continue;
-#pragma unroll 4
-    for (int u = 0; u < nt; ++u) {
-      const int64_t t = tb + u;
-      const float* z = sdz[u];
-      const float r_a = z[NA], beta_a = z[NA + 1];
-      const int64_t off = (t * N + sid[u]) * (int64_t)C + c;
-      const float a = (sizeof(TS) == 2) ? __uint_as_float((uint32_t)reinterpret_cast<const uint16_t*>(X)[off] << 16)
-                                         : reinterpret_cast<const float*>(X)[off];
-      float s = 0.f;
-      const float ar = a * r_a;
+    // the elements of kRowBatch tokens are loaded before any is written back
+    // (a load after a store of the same array waits for it); tokens past nt
+    // repeat the last one with zero gradients and are not stored
+    for (int u0 = 0; u0 < nt; u0 += kRowBatch) {
+      float ab[kRowBatch], db[kRowBatch];
 #pragma unroll
-      for (int o = 0; o < NAMAX; ++o) {
-        if (o < NA) {
-          s = fmaf(w[o], z[o], s);
+      for (int e = 0; e < kRowBatch; ++e) {
+        const int64_t off = sbase[u0 + e] + c;
+        ab[e] = ld_elem(X, off);
+        db[e] = ld_elem(dX, off);
+      }
+      // the logit gradients of the next token are read while this one is used;
+      // the scheduling barrier keeps the compiler from reading all of them
+      // ahead (register pressure)
+      float zc[ZP], zn[ZP];
+#pragma unroll
+      for (int o = 0; o < ZP; o += 4) *reinterpret_cast<float4*>(&zc[o]) = *reinterpret_cast<const float4*>(&sdz[u0][o]);
+#pragma unroll
+      for (int e = 0; e < kRowBatch; ++e) {
+        if (e + 1 < kRowBatch) {
+#pragma unroll
+          for (int o = 0; o < ZP; o += 4)
+            *reinterpret_cast<float4*>(&zn[o]) = *reinterpret_cast<const float4*>(&sdz[u0 + e + 1][o]);
+        }
+        const float* z = zc;
+        const float r_a = z[NAMAX], beta_a = z[NAMAX + 1];
+        const float a = ab[e], ar = a * r_a;
+        float sacc = 0.f;
+#pragma unroll
+        for (int o = 0; o < NAMAX; ++o) {
+          sacc = fmaf(w[o], z[o], sacc);
           ga[o] = fmaf(ar, z[o], ga[o]);
         }
-      }
-      const float g = r_a * s - beta_a * a;
-      if (sizeof(TS) == 2) {
-        uint16_t* d = reinterpret_cast<uint16_t*>(dX) + off;
-        *d = (uint16_t)f2bf(__uint_as_float((uint32_t)*d << 16) + g);
-      } else {
-        reinterpret_cast<float*>(dX)[off] += g;
+        if (u0 + e < nt) st_elem(dX, sbase[u0 + e] + c, db[e] + (r_a * sacc - beta_a * a));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int o = 0; o < ZP; ++o) zc[o] = zn[o];
       }
     }
   }
@@ -932,9 +972,27 @@ __device__ __forceinline__ void split_bf16x8(const float (&f)[8], uint4& hi, uin
   lo = pack8(l);
 }
 
-template <bool ACT>
+// 4 consecutive gradient elements of a bf16 or fp32 accumulator row
+__device__ __forceinline__ void ld4(const uint16_t* p, float (&d)[4]) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p);
+  d[0] = bf_lo(v.x); d[1] = bf_hi(v.x); d[2] = bf_lo(v.y); d[3] = bf_hi(v.y);
+}
+__device__ __forceinline__ void ld4(const float* p, float (&d)[4]) {
+  const float4 v = *reinterpret_cast<const float4*>(p);
+  d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+}
+__device__ __forceinline__ void st4(uint16_t* p, const float (&d)[4]) {
+  *reinterpret_cast<uint2*>(p) = make_uint2(pack2bf(d[0], d[1]), pack2bf(d[2], d[3]));
+}
+__device__ __forceinline__ void st4(float* p, const float (&d)[4]) {
+  *reinterpret_cast<float4*>(p) = make_float4(d[0], d[1], d[2], d[3]);
+}
+
+// TD: element type of the gradient rows dX (bf16, or fp32 for a state whose
+// values are bf16 but whose gradient is kept in fp32)
+template <bool ACT, typename TD = uint16_t>
 __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restrict__ X,
-                                                       const uint16_t* __restrict__ din, uint16_t* __restrict__ dX,
+                                                       const uint16_t* __restrict__ din, TD* __restrict__ dX,
                                                        const float* __restrict__ Wa, const float* __restrict__ Wb,
                                                        const float* __restrict__ Hpre,
                                                        const int32_t* __restrict__ idx, const float* __restrict__ tok,
@@ -1041,16 +1099,18 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
     __syncthreads();
     if (tb + kMfStep < t1) fetch(cur, tb + kMfStep);
     // ---- dX: two token halves; the accumulator rows are read before the products
-    uint2 dxv[2], dinv[2];
+    float dxv[2][4];
+    uint2 dinv[2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int u = 16 * h + l16;
       const int kr = 16 * wave + 4 * g4;
-      dxv[h] = make_uint2(0, 0);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) dxv[h][v] = 0.f;
       dinv[h] = make_uint2(0, 0);
       if (u < nt) {
         const int64_t t = tb + u;
-        dxv[h] = *reinterpret_cast<const uint2*>(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr);
+        ld4(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr, dxv[h]);
         if (!ACT) dinv[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
       }
     }
@@ -1083,10 +1143,8 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
           for (int v = 0; v < 4; ++v)
             gsum[v] = hp * gi[v] + acc[v] - bpre * x[v] - r_ln * m1 - r_ln * r_ln * (x[v] - mu) * m2;
         }
-        const float d[4] = {bf_lo(dxv[h].x) + gsum[0], bf_hi(dxv[h].x) + gsum[1], bf_lo(dxv[h].y) + gsum[2],
-                            bf_hi(dxv[h].y) + gsum[3]};
-        *reinterpret_cast<uint2*>(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr) =
-            make_uint2(pack2bf(d[0], d[1]), pack2bf(d[2], d[3]));
+        const float d[4] = {dxv[h][0] + gsum[0], dxv[h][1] + gsum[1], dxv[h][2] + gsum[2], dxv[h][3] + gsum[3]};
+        st4(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr, d);
       }
     }
     // ---- dW: contraction over the 32 staged tokens (rows past nt are zero)
@@ -1258,7 +1316,8 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
-                          hipStream_t s, const float* dhpre_act, const float* Hpre_read) {
+                          hipStream_t s, const float* dhpre_act, const float* Hpre_read, bool dense_rows,
+                          const void* X_bf16) {
   const float* Hrd = Hpre_read ? Hpre_read : Hpre;   // weights of the dense-read term
   const int64_t T = d->T;
   const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
@@ -1273,9 +1332,14 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
   float* wpart_a = wpart_p + nchunk * (int64_t)N * C * N;
   float* red_a = wpart_a + nchunk * (int64_t)k * C * 32;           // [kC][32]
   float* pgsum = red_a + (int64_t)k * C * 32;
-  XHC_TS_DISPATCH(d->state_dtype,
-    k_bwd_dhpre<TS><<<dim3((unsigned)(T * ncb)), dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),
-        reinterpret_cast<const TS*>(d_input), T, N, C, part));
+  if (!dense_rows) {
+    hipError_t e0 = launch_fill0(part, (size_t)ncb * N * T * sizeof(float), s);
+    if (e0 != hipSuccess) return e0;
+  } else {
+    XHC_TS_DISPATCH(d->state_dtype,
+      k_bwd_dhpre<TS><<<dim3((unsigned)(T * ncb)), dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),
+          reinterpret_cast<const TS*>(d_input), T, N, C, part));
+  }
   if (dhpre_act) {
     k_bwd_dhpre_override<<<dim3((unsigned)((T * k + 255) / 256)), dim3(256), 0, s>>>(dhpre_act, idx, T, N, k, ncb,
                                                                                     part);
@@ -1298,14 +1362,24 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
   const bool mf = d->state_dtype == XHC_BF16 && N == 16 && NA <= 32 && C % kMfRows == 0;
   if (mf) {
     const dim3 gf((unsigned)((int64_t)N * C / kMfRows), (unsigned)nchunk);
-    k_bwd_rows_mfma<false><<<gf, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
-        reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T,
-        N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
+    if (dense_rows)
+      k_bwd_rows_mfma<false><<<gf, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
+          reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T,
+          N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
     const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
     k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
         reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T,
         N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
     k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
+  }
+  // an fp32 state given with its exact bf16 copy: the active rows take the
+  // MFMA pass with fp32 gradient rows
+  const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % kMfRows == 0;
+  if (mfa32) {
+    const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
+    k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
+        reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
+        nullptr);
   }
   const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
 #define XHC_FULL_ROWS(NNV)                                                                                       \
@@ -1314,25 +1388,31 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
         reinterpret_cast<const TS*>(d_input), reinterpret_cast<TS*>(dX), W_r, W_pre, Hrd, tok, T, C, NA,         \
         kRowChunk, wpart_r, wpart_p))
   if (!mf) {
-    switch (N) {
-      case 4: XHC_FULL_ROWS(4); break;
-      case 8: XHC_FULL_ROWS(8); break;
-      case 16: XHC_FULL_ROWS(16); break;
-      default: XHC_FULL_ROWS(32); break;
+    if (dense_rows) {
+      switch (N) {
+        case 4: XHC_FULL_ROWS(4); break;
+        case 8: XHC_FULL_ROWS(8); break;
+        case 16: XHC_FULL_ROWS(16); break;
+        default: XHC_FULL_ROWS(32); break;
+      }
     }
-    const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
-    XHC_TS_DISPATCH(d->state_dtype,
-      k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
-          W_post, W_res, idx, tok, T, N, k, C, Kr, kRowChunk, wpart_a));
+    if (!mfa32) {
+      const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
+      XHC_TS_DISPATCH(d->state_dtype,
+        k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
+            W_post, W_res, idx, tok, T, N, k, C, Kr, kRowChunk, wpart_a));
+    }
   }
 #undef XHC_FULL_ROWS
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // token reductions (fixed order)
   const int64_t nfull = (int64_t)N * C * N;
-  k_colsum_rows_corr<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(
-      wpart_r, nchunk, nfull, mf ? pgsum + pg_floats(N, k, Kr) : nullptr, N, dW_r);
-  k_colsum_rows<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(wpart_p, nchunk, nfull, dW_pre);
+  if (dense_rows) {
+    k_colsum_rows_corr<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(
+        wpart_r, nchunk, nfull, mf ? pgsum + pg_floats(N, k, Kr) : nullptr, N, dW_r);
+    k_colsum_rows<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(wpart_p, nchunk, nfull, dW_pre);
+  }
   // active partials are [chunk][kC][32]: split columns into W_post and W_res
   const int64_t nact = (int64_t)k * C * 32;
   k_colsum_rows<<<dim3((unsigned)((nact + 255) / 256)), dim3(256), 0, s>>>(wpart_a, nchunk, nact, red_a);

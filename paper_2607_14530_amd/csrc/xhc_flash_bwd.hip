@@ -158,6 +158,26 @@ __global__ void k_fbwd_alpha(const float* a0, const float* a1, const float* a2, 
   }
 }
 
+// da[t, j, :] = da_rev[t, j, :] + Hsel[t, j] din[t, :] (din null: a copy),
+// one workgroup per active row
+template <typename TS>
+__global__ __launch_bounds__(256) void k_fbwd_finish(int k, int C, const float* __restrict__ da_rev,
+                                                     const float* __restrict__ Hsel, const TS* __restrict__ din,
+                                                     float* __restrict__ da) {
+  const int64_t r = blockIdx.x, t = r / k;
+  const float h = din ? Hsel[r] : 0.0f;
+  for (int c = threadIdx.x * 8; c < C; c += 256 * 8) {
+    float f[8], g[8];
+    Vec8<float>::load(da_rev + r * C + c, f);
+    if (din) {
+      Vec8<TS>::load(din + t * C + c, g);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) f[e] = fmaf(h, g[e], f[e]);
+    }
+    Vec8<float>::store(da + r * C + c, f);
+  }
+}
+
 unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 }  // namespace
@@ -230,6 +250,13 @@ hipError_t launch_fbwd_add(float* dst, const float* src, int64_t n, hipStream_t 
 
 hipError_t launch_fbwd_alpha(const float* a0, const float* a1, const float* a2, float* out, hipStream_t s) {
   k_fbwd_alpha<<<dim3(1), dim3(64), 0, s>>>(a0, a1, a2, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_fbwd_finish(int state_dtype, int64_t T, int k, int C, const float* da_rev, const float* Hsel,
+                              const void* din, float* da, hipStream_t s) {
+  XHC_FTS(state_dtype, k_fbwd_finish<TS><<<dim3((unsigned)(T * k)), dim3(256), 0, s>>>(
+                           k, C, da_rev, Hsel, reinterpret_cast<const TS*>(din), da));
   return hipGetLastError();
 }
 

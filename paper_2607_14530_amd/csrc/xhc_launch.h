@@ -129,10 +129,17 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* Hpre, const float* Hpost, const void* d_input, const float* dHres,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
-                          hipStream_t s, const float* dhpre_act = nullptr, const float* Hpre_read = nullptr);
+                          hipStream_t s, const float* dhpre_act = nullptr, const float* Hpre_read = nullptr,
+                          bool dense_rows = true, const void* X_bf16 = nullptr);
 // dhpre_act [T,k]: when given, dL/dH^pre of the active streams (slot order)
 // replaces <d input, x_i> there; Hpre_read [T,N]: when given, the weights of
-// the dense-read term dX_i += H^pre_i d input (Hpre otherwise).
+// the dense-read term dX_i += H^pre_i d input (Hpre otherwise).  dense_rows
+// false leaves out every term of the dense rows (the read H^pre_i d input and
+// the full-state projection through W_r, W_pre): for a caller whose router
+// and pre-map weights are zero; d_input is then not read, H^pre enters as
+// zero gradient, and dW_r, dW_pre are not written.  X_bf16: for an fp32
+// state whose values are exactly bf16, the same rows as bf16 (read by the
+// MFMA form of the active-row pass; the gradient rows stay fp32).
 
 // ---- xHC-Flash backward helpers
 hipError_t launch_fill0(void* p, size_t bytes, hipStream_t s);
@@ -148,6 +155,8 @@ hipError_t launch_fbwd_from_f32(int state_dtype, const float* src, void* dst, in
 hipError_t launch_fbwd_mask(int64_t T, int N, int k, const int32_t* idx, const float* Hpre, float* Hm, hipStream_t s);
 hipError_t launch_fbwd_add(float* dst, const float* src, int64_t n, hipStream_t s);
 hipError_t launch_fbwd_alpha(const float* a0, const float* a1, const float* a2, float* out, hipStream_t s);
+hipError_t launch_fbwd_finish(int state_dtype, int64_t T, int k, int C, const float* da_rev, const float* Hsel,
+                              const void* din, float* da, hipStream_t s);
 
 // per-token values xhc_pre saves for the backward: [z_r (N) | z_pre (N) |
 // z_post, z_res (k*Kr + k*k) | mu | nu | nu_a | pad], z = normalised logits
