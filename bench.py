@@ -42,13 +42,18 @@ METRIC = "tokens/s and achieved HBM GB/s per xHC sublayer (fwd) at N=16,k=4,C=40
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "traffic_xhc_pre_T16384_N16_C4096.md")
 
 
+# the sources whose device code one xhc_pre call runs (k_zero2, k_pre_fused,
+# k_pre_coef_sum and the helpers they inline)
+PRE_SOURCES = ("xhc_device.h", "xhc_pre.hip", "xhc_pre_fused.hip")
+
+
 def sources_digest():
-    """sha256 over the kernel sources (name + bytes, sorted): a traffic figure
-    measured on other sources no longer describes the kernels."""
+    """sha256 over the pre kernels' sources (name + bytes, sorted): a traffic
+    figure measured on other sources no longer describes the kernels."""
     import hashlib
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2607_14530_amd", "csrc")
-    for name in sorted(os.listdir(csrc)):
+    for name in sorted(PRE_SOURCES):
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())
@@ -123,13 +128,20 @@ def _time(fn, iters, stream):
     return e0.elapsed_time(e1) / iters
 
 
-def extra_sections(dev, stream, iters=5):
+SECTIONS = ("flash_q4", "flash_q2", "mhc_n4", "prefill_t2048", "bwd_n16_mlp", "flash_bwd_q4")
+
+
+def extra_sections(dev, stream, iters=5, only=None):
     """xHC-Flash groups, the dense mHC N=4 comparator and the backward, each
-    timed on its own (outside the timed steps of the main workload)."""
+    timed on its own (outside the timed steps of the main workload); only:
+    names of the sections to run (all when None)."""
     out = {}
     unit = lambda C: 2 * C   # bytes of one "C" (bf16 elements of width C)
+    want = lambda name: only is None or name in only
     # xHC-Flash, Q = 4 and Q = 2, at T = 16384 (2 x 8192), N = 16, k = 4, C = 4096
     for Q in (4, 2):
+        if not want(f"flash_q{Q}"):
+            continue
         w = synth.sparse_c4096(4)
         d = synth.flash_inputs(w, Q, 40 + Q, device=dev)
         g = X.FlashGroup(X.dims_for(w), Q, d, dev)
@@ -146,68 +158,72 @@ def extra_sections(dev, stream, iters=5):
             "bytes_per_token_C": b / Q / unit(w.C), "paper_bytes_per_token_C": 40.0 if Q == 4 else 51.0}
         del g, d, state
         torch.cuda.empty_cache()
-    # dense mHC N = 4 (k = m = N, one write-back component) at the same T and C
-    w = synth.Workload(T=16384, S=8192, N=4, k=4, m=4, C=4096, Kr=1, name="mhc-n4")
-    inp = synth.sublayer_inputs(w, 9, device=dev)
-    sub = X.Sublayer(X.dims_for(w), inp, dev)
-    st = inp["X"]
-    ms = _time(lambda: (sub.pre(st, stream), sub.post(st, inp["F"], stream)), iters, stream)
-    b = A.algorithmic_bytes_sublayer(4, 4, w.C, 1)
-    out["mhc_n4"] = {"workload": "dense mHC N=4 (k=m=4, one write-back component), T=16384, C=4096",
-                     "ms_per_sublayer": ms, "tokens_per_s": w.T / (ms * 1e-3),
-                     "achieved_GBps": b * w.T / (ms * 1e-3) / 1e9, "bytes_per_token_C": b / unit(w.C),
-                     "paper_bytes_per_token_C": 34.0}
-    del sub, inp, st
-    torch.cuda.empty_cache()
-    # prefill-latency regime: one 2048-token sequence through an attention-type
-    # and an MLP-type sublayer (forward), for each pre implementation
-    pre_ms = {}
-    for name, impl in (("auto", X.XHC_IMPL_AUTO), ("multi", X.XHC_IMPL_MULTI), ("fused", X.XHC_IMPL_FUSED)):
-        wa = synth.Workload(T=2048, S=2048, N=16, k=4, m=2, C=4096, Kr=1, name="prefill-attn")
-        wm = synth.Workload(T=2048, S=2048, N=16, k=4, m=2, C=4096, Kr=4, name="prefill-mlp")
-        ia, im = synth.sublayer_inputs(wa, 11, device=dev), synth.sublayer_inputs(wm, 12, device=dev)
-        sa = X.Sublayer(X.dims_for(wa, impl=impl), ia, dev)
-        sm = X.Sublayer(X.dims_for(wm, impl=impl), im, dev)
-        st = ia["X"]
-        pre_ms[name] = _time(lambda: (sa.pre(st, stream), sa.post(st, ia["F"], stream),
-                                      sm.pre(st, stream), sm.post(st, im["F"], stream)), 20, stream)
-        del sa, sm, ia, im, st
+    if want("mhc_n4"):
+        # dense mHC N = 4 (k = m = N, one write-back component) at the same T and C
+        w = synth.Workload(T=16384, S=8192, N=4, k=4, m=4, C=4096, Kr=1, name="mhc-n4")
+        inp = synth.sublayer_inputs(w, 9, device=dev)
+        sub = X.Sublayer(X.dims_for(w), inp, dev)
+        st = inp["X"]
+        ms = _time(lambda: (sub.pre(st, stream), sub.post(st, inp["F"], stream)), iters, stream)
+        b = A.algorithmic_bytes_sublayer(4, 4, w.C, 1)
+        out["mhc_n4"] = {"workload": "dense mHC N=4 (k=m=4, one write-back component), T=16384, C=4096",
+                         "ms_per_sublayer": ms, "tokens_per_s": w.T / (ms * 1e-3),
+                         "achieved_GBps": b * w.T / (ms * 1e-3) / 1e9, "bytes_per_token_C": b / unit(w.C),
+                         "paper_bytes_per_token_C": 34.0}
+        del sub, inp, st
         torch.cuda.empty_cache()
-    out["prefill_t2048"] = {"workload": "xHC forward block (attention-type + MLP-type sublayer), one 2048-token "
-                                        "sequence, N=16, k=4, m=2, C=4096",
-                            "ms_per_block": pre_ms["auto"], "ms_per_block_multi": pre_ms["multi"],
-                            "ms_per_block_fused": pre_ms["fused"],
-                            "tokens_per_s": 2048 / (pre_ms["auto"] * 1e-3)}
-    # backward, T = 8192, N = 16, k = 4, C = 4096, MLP-type
-    w = synth.bwd_sweep(16, 4)
-    inp = synth.sublayer_inputs(w, 10, device=dev, grads=True)
-    sub = X.TrainableSublayer(X.dims_for(w), inp, dev)
-    st = inp["X"]
-    fwd_ms = _time(lambda: sub.forward(st, inp["F"], stream), 1, stream)
-    sub.forward(st, inp["F"], stream)
-
-    def fb():
-        sub.backward(st, inp["G_X"], inp["G_in"], inp["F"], stream)
+    if want("prefill_t2048"):
+        # prefill-latency regime: one 2048-token sequence through an attention-type
+        # and an MLP-type sublayer (forward), for each pre implementation
+        pre_ms = {}
+        for name, impl in (("auto", X.XHC_IMPL_AUTO), ("multi", X.XHC_IMPL_MULTI), ("fused", X.XHC_IMPL_FUSED)):
+            wa = synth.Workload(T=2048, S=2048, N=16, k=4, m=2, C=4096, Kr=1, name="prefill-attn")
+            wm = synth.Workload(T=2048, S=2048, N=16, k=4, m=2, C=4096, Kr=4, name="prefill-mlp")
+            ia, im = synth.sublayer_inputs(wa, 11, device=dev), synth.sublayer_inputs(wm, 12, device=dev)
+            sa = X.Sublayer(X.dims_for(wa, impl=impl), ia, dev)
+            sm = X.Sublayer(X.dims_for(wm, impl=impl), im, dev)
+            st = ia["X"]
+            pre_ms[name] = _time(lambda: (sa.pre(st, stream), sa.post(st, ia["F"], stream),
+                                          sm.pre(st, stream), sm.post(st, im["F"], stream)), 20, stream)
+            del sa, sm, ia, im, st
+            torch.cuda.empty_cache()
+        out["prefill_t2048"] = {"workload": "xHC forward block (attention-type + MLP-type sublayer), one 2048-token "
+                                            "sequence, N=16, k=4, m=2, C=4096",
+                                "ms_per_block": pre_ms["auto"], "ms_per_block_multi": pre_ms["multi"],
+                                "ms_per_block_fused": pre_ms["fused"],
+                                "tokens_per_s": 2048 / (pre_ms["auto"] * 1e-3)}
+    if want("bwd_n16_mlp"):
+        # backward, T = 8192, N = 16, k = 4, C = 4096, MLP-type
+        w = synth.bwd_sweep(16, 4)
+        inp = synth.sublayer_inputs(w, 10, device=dev, grads=True)
+        sub = X.TrainableSublayer(X.dims_for(w), inp, dev)
+        st = inp["X"]
+        fwd_ms = _time(lambda: sub.forward(st, inp["F"], stream), 1, stream)
         sub.forward(st, inp["F"], stream)
-    ms = _time(fb, 2, stream)
-    out["bwd_n16_mlp"] = {"workload": "xHC MLP-type sublayer backward, T=8192, N=16, k=4, m=2, C=4096",
-                          "ms_forward_with_saves": fwd_ms, "ms_backward": ms - fwd_ms,
-                          "tokens_per_s_backward": w.T / ((ms - fwd_ms) * 1e-3)}
-    del sub, inp, st
-    torch.cuda.empty_cache()
-    # xHC-Flash group backward, Q = 4, T = 8192, N = 16, k = 4, C = 4096
-    w = synth.bwd_sweep(16, 4)
-    Q = 4
-    fd = synth.flash_inputs(w, Q, 13, device=dev, grads=True)
-    grp = X.TrainableFlashGroup(X.dims_for(w), Q, fd, dev)
-    X0 = fd["X"]
-    st = X0.clone()
-    ffwd = _time(lambda: (st.copy_(X0), grp.forward(st, fd["F_list"], stream)), 2, stream)
-    cp = _time(lambda: st.copy_(X0), 2, stream)
-    fbwd = _time(lambda: grp.backward(X0, fd["G_X"], fd["G_in_list"], fd["F_list"], stream), 2, stream)
-    out["flash_bwd_q4"] = {"workload": "xHC-Flash group backward, Q=4, T=8192, N=16, k=4, m=2, C=4096",
-                           "ms_forward_with_saves": ffwd - cp, "ms_backward": fbwd,
-                           "tokens_per_s_per_sublayer_backward": Q * w.T / (fbwd * 1e-3)}
+
+        def fb():
+            sub.backward(st, inp["G_X"], inp["G_in"], inp["F"], stream)
+            sub.forward(st, inp["F"], stream)
+        ms = _time(fb, 2, stream)
+        out["bwd_n16_mlp"] = {"workload": "xHC MLP-type sublayer backward, T=8192, N=16, k=4, m=2, C=4096",
+                              "ms_forward_with_saves": fwd_ms, "ms_backward": ms - fwd_ms,
+                              "tokens_per_s_backward": w.T / ((ms - fwd_ms) * 1e-3)}
+        del sub, inp, st
+        torch.cuda.empty_cache()
+    if want("flash_bwd_q4"):
+        # xHC-Flash group backward, Q = 4, T = 8192, N = 16, k = 4, C = 4096
+        w = synth.bwd_sweep(16, 4)
+        Q = 4
+        fd = synth.flash_inputs(w, Q, 13, device=dev, grads=True)
+        grp = X.TrainableFlashGroup(X.dims_for(w), Q, fd, dev)
+        X0 = fd["X"]
+        st = X0.clone()
+        ffwd = _time(lambda: (st.copy_(X0), grp.forward(st, fd["F_list"], stream)), 2, stream)
+        cp = _time(lambda: st.copy_(X0), 2, stream)
+        fbwd = _time(lambda: grp.backward(X0, fd["G_X"], fd["G_in_list"], fd["F_list"], stream), 2, stream)
+        out["flash_bwd_q4"] = {"workload": "xHC-Flash group backward, Q=4, T=8192, N=16, k=4, m=2, C=4096",
+                               "ms_forward_with_saves": ffwd - cp, "ms_backward": fbwd,
+                               "tokens_per_s_per_sublayer_backward": Q * w.T / (fbwd * 1e-3)}
     return out
 
 
@@ -219,6 +235,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the Flash / mHC / prefill / backward sections")
+    ap.add_argument("--section", action="append", default=None, choices=SECTIONS,
+                    help="run only this extra section (repeatable) and print its figures")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration under rocprofv3 --pmc)")
     args = ap.parse_args()
@@ -232,6 +250,10 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.section:
+        stream = torch.cuda.current_stream()
+        print(json.dumps({"sections": extra_sections(dev, stream, only=set(args.section))}), flush=True)
+        return
     w_attn, w_mlp = synth.sparse_c4096(1), synth.sparse_c4096(4)
     T, N, k, C = w_attn.T, w_attn.N, w_attn.k, w_attn.C
     inp_a = synth.sublayer_inputs(w_attn, 1, device=dev)
