@@ -537,7 +537,7 @@ def xhc_sublayer_grads(X, F, conv_w, W_r, W_pre, W_res, W_post, alpha, b_pre, b_
 def flash_forward(X0, F_list, conv_w_list, W_r, W_pre_list, W_post_list, W_res, alpha_pre, b_pre,
                   alpha_post, b_post, alpha_res, b_res, *, m, k, S, kappa=(4, 8, 12), eps=1e-5,
                   sinkhorn_iters=20, clamp_delta=1e-6, round_state=True, gram_schmidt_on=True,
-                  router="sigmoid"):
+                  router="sigmoid", tokens=None):
     """One xHC-Flash sharing group, float64, with every weight taken as given
     (already the bf16 operand values) so that it can be differentiated.
 
@@ -553,9 +553,12 @@ def flash_forward(X0, F_list, conv_w_list, W_r, W_pre_list, W_post_list, W_res, 
     (piecewise constant); p is the score of the routed stream.  With
     ``round_state`` each written active row passes through a bfloat16
     rounding, which the reverse mode treats as the identity (the stored
-    state is what the next step reads).  Returns (X after the group, list
-    of the Q inputs, dict of idx, p, Hpre [Q,T,N], Hpost list, Hres and acts,
-    the active rows before each sublayer).
+    state is what the next step reads).  With ``tokens`` (positions in the
+    batch), X0 holds only those tokens' states while every F is the whole
+    batch: each step is per token except the causal convolutions, which
+    read the same sequence's earlier F rows.  Returns (X after the group,
+    list of the Q inputs, dict of idx, p, Hpre [Q,T,N], Hpost list, Hres and
+    acts, the active rows before each sublayer).
     """
     Q = len(F_list)
     T, N, C = X0.shape
@@ -581,7 +584,8 @@ def flash_forward(X0, F_list, conv_w_list, W_r, W_pre_list, W_post_list, W_res, 
         return residual_mapping(rms_norm(a.reshape(T, k * C), eps) @ W_res, alpha_res, b_res, k,
                                 sinkhorn_iters, clamp_delta)
 
-    tokens = torch.arange(T)
+    if tokens is None:
+        tokens = torch.arange(T)
     inputs = [torch.einsum("tn,tnc->tc", Hpre[0], X0)]
     a = gather_rows(X0, idx)
     acts = [a]
@@ -646,16 +650,20 @@ def flash_leaves(X0, F_list, conv_w_list, W_r, W_pre_list, W_post_list, W_res, a
             "alpha_res": one(torch.as_tensor(alpha_res, dtype=F64)), "b_res": one(b_res)}
 
 
-def flash_group_grads(vals, G_X, G_in_list, **kw):
-    """Gradients of flash_objective with respect to every entry of ``vals``
-    (as made by flash_leaves): the reverse mode of the group forward, the
-    routing decision piecewise constant.  Returns (dict of gradients with the
+def flash_group_grads(vals, G_X, G_in_list, wrt=FLASH_GRAD_NAMES, **kw):
+    """Gradients of flash_objective with respect to the entries of ``vals``
+    named in ``wrt`` (as made by flash_leaves; the others are held constant
+    and get None): the reverse mode of the group forward, the routing
+    decision piecewise constant.  Returns (dict of gradients with the
     structure of vals, forward dict, loss).  Parity: pinned by central
     differences (tests)."""
     leaves, paths = [], []
     lv = {}
     for name in FLASH_GRAD_NAMES:
         v = vals[name]
+        if name not in wrt:
+            lv[name] = v
+            continue
         if isinstance(v, list):
             lv[name] = []
             for i, t in enumerate(v):
@@ -674,6 +682,7 @@ def flash_group_grads(vals, G_X, G_in_list, **kw):
     L, fwd = flash_objective(lv, G_X, G_in_list, **kw)
     grads = torch.autograd.grad(L, leaves, allow_unused=True)
     out = {n: ([None] * len(vals[n]) if isinstance(vals[n], list) else None) for n in FLASH_GRAD_NAMES}
+    out.update({n: None for n in FLASH_GRAD_NAMES if n not in wrt})
     for (name, i), g, t in zip(paths, grads, leaves):
         g = torch.zeros_like(t) if g is None else g
         if i is None:

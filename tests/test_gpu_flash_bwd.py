@@ -109,3 +109,28 @@ def test_flash_backward_is_deterministic():
         for x, y in zip(vs, ws):
             if x is not None:
                 assert torch.equal(x, y), n
+
+
+def test_flash_backward_full_size_state_gradient_on_sampled_tokens():
+    """Q = 4 at the backward bench workload (T = 8192, one sequence, N = 16,
+    k = 4, C = 4096): dL/dX of sampled tokens against the oracle evaluated on
+    those tokens alone (every F whole for the causal convolutions)."""
+    w = synth.bwd_sweep(16, 4)
+    Q = 4
+    print(f"[flash-bwd-full] {w.name} Q={Q}", flush=True)
+    d, grp, state, g = _run(w, Q, seed=13)
+    gen = torch.Generator().manual_seed(77)
+    tok = torch.tensor(sorted(set([0, 1, 5, 11, 12, w.T - 1] + torch.randint(0, w.T, (6,), generator=gen).tolist())))
+    tg = tok.to("cuda")
+    c = lambda v: v.cpu() if torch.is_tensor(v) else v
+    cl = lambda v: [c(x) for x in v]
+    vals = O.flash_leaves(d["X"][tg].cpu(), cl(d["F_list"]), cl(d["conv_w_list"]), c(d["W_r"]), cl(d["W_pre_list"]),
+                          cl(d["W_post_list"]), c(d["W_res"]), d["alpha_pre"], cl(d["b_pre"]), d["alpha_post"],
+                          cl(d["b_post"]), d["alpha_res"], c(d["b_res"]))
+    ref, fwd, _ = O.flash_group_grads(vals, d["G_X"][tg].cpu(), [x[tg].cpu() for x in d["G_in_list"]], wrt=("X",),
+                                      m=w.m, k=w.k, S=w.S, kappa=w.kappa, router=w.router,
+                                      gram_schmidt_on=bool(w.gram_schmidt), tokens=tok)
+    same = (grp.idx[tg].cpu().long() == fwd["idx"]).all(1)
+    assert int(same.sum()) >= len(tok) - 1, "routing differs at more than one sampled token"
+    scale = max(ref["X"].abs().max().item(), d["G_X"][tg].abs().max().item())
+    assert_state_grad_close(g["X"][tg].cpu()[same], ref["X"][same], Q + 1, scale, "dX (sampled tokens)")

@@ -99,3 +99,28 @@ def test_flash_untouched_rows_pass_the_state_gradient_through_plus_base_readouts
                 h = 1.0 / (1.0 + torch.exp(-vals["b_pre"][q][i]))
                 want += h * d["G_in_list"][q][t].to(F64)
             assert torch.allclose(g["X"][t, i], want, rtol=0, atol=1e-12), (t, i)
+
+
+def test_flash_sampled_tokens_equal_the_full_group():
+    """Evaluating the group on a subset of tokens (their states only, every F
+    whole) gives those tokens' outputs and state gradients of the full
+    evaluation: every step is per token except the causal convolutions, which
+    read the same sequence's earlier F rows (tokens on both sides of a
+    sequence start are sampled)."""
+    w = synth.Workload(T=24, S=12, N=8, k=4, m=2, C=32, Kr=4)
+    d = synth.flash_inputs(w, 4, 21, grads=True, bias_std=0.5)
+    vals = O.flash_leaves(d["X"], d["F_list"], d["conv_w_list"], d["W_r"], d["W_pre_list"], d["W_post_list"],
+                          d["W_res"], d["alpha_pre"], d["b_pre"], d["alpha_post"], d["b_post"], d["alpha_res"],
+                          d["b_res"])
+    kw = dict(m=w.m, k=w.k, S=w.S)
+    full, ffwd, _ = O.flash_group_grads(vals, d["G_X"], d["G_in_list"], wrt=("X",), **kw)
+    tok = torch.tensor([0, 5, 11, 12, 13, 23])
+    sub = dict(vals, X=vals["X"][tok])
+    part, pfwd, _ = O.flash_group_grads(sub, d["G_X"][tok], [g[tok] for g in d["G_in_list"]], wrt=("X",),
+                                        tokens=tok, **kw)
+    assert part["W_r"] is None and part["F_list"] is None
+    assert torch.equal(pfwd["idx"], ffwd["idx"][tok])
+    torch.testing.assert_close(pfwd["X_new"], ffwd["X_new"][tok], rtol=1e-12, atol=1e-12)
+    for a, b in zip(pfwd["inputs"], ffwd["inputs"]):
+        torch.testing.assert_close(a, b[tok], rtol=1e-12, atol=1e-12)
+    torch.testing.assert_close(part["X"], full["X"][tok], rtol=1e-10, atol=1e-12)
