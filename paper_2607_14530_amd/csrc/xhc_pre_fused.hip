@@ -30,8 +30,11 @@
 // global->LDS loads, issued as soon as the previous tile has left the buffer.
 // Waves 4-7 do all waiting on records: a wave that waits on a load also waits
 // on every earlier load of its own, so the copy waves must not poll.  The
-// kernel is launched cooperatively, so every member of a team is resident;
-// every wait is bounded, so every wave exits.
+// reducer jobs run on waves 4, 5, ...; a step ends when its slowest wave does,
+// so when wave 4 is the only reducer it neither polls nor publishes, and
+// neither does wave 0, which shares its SIMD.  The kernel is launched
+// cooperatively, so every member of a team is resident; every wait is
+// bounded, so every wave exits.
 #include "xhc_device.h"
 #include "xhc_launch.h"
 
@@ -63,6 +66,9 @@ constexpr int CREC = (FM * NV2 + NPOLL * kWave - 1) / (NPOLL * kWave);       // 
 constexpr unsigned kSpinLimit = 1u << 16;     // polls of one record before the wait gives up
 
 static_assert(FM * FN / 4 % NCOPY == 0, "tile copies must split evenly over the copy waves");
+// with one reducer wave the other three polling waves take all records
+static_assert(BREC * (NPOLL - 1) * kWave >= 2 * FM * NJV && CREC * (NPOLL - 1) * kWave >= FM * NV2,
+              "three polling waves cover the records");
 static_assert(FCS == 16 * FNW, "a wave holds 16 channels of the slice");
 
 struct FusedArgs {
@@ -261,13 +267,22 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   // per-lane constants of the reducers (lane i < 16: output i)
   const float cs_l = a.colsum[tl], bpre_l = a.b_pre[tl], alpha_pre = a.alpha[0];
 
+  // This member's reducer jobs of a tile are j = s + jj G (jj = 0, 1, ...;
+  // token j / 2, half j % 2), run by waves NCOPY .. NCOPY + nred - 1.  The
+  // records are polled by waves pw0 .. 7: all of 4 .. 7, or 5 .. 7 when wave
+  // 4 is the only reducer (its step is the longest).
+  const int njobs = (2 * FM - s + G - 1) / G;
+  const int nred = njobs < NPOLL ? njobs : NPOLL;
+  const int pw0 = nred == 1 ? NCOPY + 1 : NCOPY;
+  const int pstride = (FNW - pw0) * kWave;          // polling lanes
+  const bool poller = wave >= pw0;
   // offsets of this member's reducer records, per polling lane (the same for
   // every tile): flat record u = jj G + g, value vi -> sm.vals[u]
-  if (wave >= NCOPY) {
-    const int pl = (wave - NCOPY) * kWave + lane;
+  if (poller) {
+    const int pl = (wave - pw0) * kWave + lane;
 #pragma unroll
     for (int r = 0; r < BREC; ++r) {
-      const int u = pl + r * NPOLL * kWave;
+      const int u = pl + r * pstride;
       const int jg = u / NJV, vi = u % NJV, jj = jg / G, g = jg % G;
       const int j = s + jj * G;
       const int o = vi < FN ? (j % 2 == 0 ? vi : FN + vi) : (j % 2 == 0 ? 32 + (vi - FN) : (vi == FN ? 33 : -1));
@@ -297,11 +312,9 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   uint64_t* const rec1t = a.rec1 + (size_t)team * RING * G * FM * NV1;   // this team's record slots
   uint64_t* const rec2t = a.rec2 + (size_t)team * RING * FM * NV2;
 
-  // ---- reducers.  This member's jobs of tile qt are j = s + jj G (jj = 0, 1,
-  // ...; t = j / 2, h = j % 2).  Their member partials are polled by all
-  // polling waves together: flat record u -> job jj and member g
-  // (jj G + g = u / NJV), value vi = u % NJV.
-  const int njobs = (2 * FM - s + G - 1) / G;
+  // ---- reducers.  Their member partials are polled by the polling waves
+  // together: flat record u -> job jj and member g (jj G + g = u / NJV), value
+  // vi = u % NJV.
   // finish job jj of tile qt from sm.vals (one wave)
   auto finish_job = [&](int qt, int jj) {
     const int lane = lane_id_here();
@@ -315,11 +328,20 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
     // holds the same bits.
     const float* vrow = &sm.vals[jj * G][0];
     const int per = G >= 4 ? G / 4 : 1, mg = lane >> 4;
+    // every read is issued before the sum (a read of an unused member goes
+    // to member 0 and is not added), so the LDS latency is paid once
+    float vv[kMaxG / 4];
+#pragma unroll
+    for (int e = 0; e < kMaxG / 4; ++e) {
+      const int g = mg * per + e;
+      vv[e] = vrow[(e < per && g < G ? g : 0) * NJV + (lane & 15)];
+    }
     float v = 0.f;
 #pragma unroll
     for (int e = 0; e < kMaxG / 4; ++e) {
       const int g = mg * per + e;
-      if (e < per && g < G) v += vrow[g * NJV + (lane & 15)];
+      const float sum = v + vv[e];
+      v = (e < per && g < G) ? sum : v;
     }
     v = add_xor32(add_xor16(v));
     const int mi = lane / G;
@@ -331,11 +353,13 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
       const float r_ln = __builtin_amdgcn_rsqf(fmaxf(nu - mu * mu, 0.f) + a.eps);
       const float z = (v - mu * cs_l) * r_ln;   // lanes 0..15: LayerNorm-corrected router logit
       // rank among the candidates i >= m (larger logit first, ties to the lower index)
+      // (branch-free: the candidate test is uniform, the comparison a select)
       int rank = 0;
 #pragma unroll
       for (int i = 0; i < FN; ++i) {
         const float zi = lane_value(z, i);
-        if (i >= a.m && (zi > z || (zi == z && i < lane))) ++rank;   // i == lane never counts
+        const int before = (int)(zi > z) | ((int)(zi == z) & (int)(i < lane));   // i == lane never counts
+        rank += before & -(int)(i >= a.m);
       }
       int slot = -1;
       float pv = 1.0f;
@@ -384,7 +408,7 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   // record r of this polling lane: address and whether it is wanted
   auto poll_rec = [&](int q, int r, bool& wanted) -> const uint64_t* {
     const bool hasB = q >= 1 && q - 1 < nq, hasC = q >= 2 && q - 2 < nq;
-    const int pl = (wave - NCOPY) * kWave + lane_id_here();   // 0 .. 255
+    const int pl = (wave - pw0) * kWave + lane_id_here();
     if (r < BREC) {
       const uint64_t* r1 = rec1t + ((q - 1 + RING) % RING) * G * FM * NV1;
       const int off = sm.poff[r][pl];
@@ -392,7 +416,7 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
       return r1 + (wanted ? off : 0);
     }
     const uint64_t* r2 = rec2t + ((q - 2 + RING) % RING) * FM * NV2;
-    const int u = pl + (r - BREC) * NPOLL * kWave;
+    const int u = pl + (r - BREC) * pstride;
     wanted = hasC && u < FM * NV2;
     return r2 + (wanted ? u : 0);
   };
@@ -414,9 +438,20 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   // tile q - 2 (registers XC); the registers rotate at the end of a step
   // active partials of tile qc (the C phase of a step, left in red2) summed
   // over the waves into part2; runs in the next step, after its first barrier
+  // (not by the reducer waves: the compiler waits for every store a wave has
+  // in flight before its reducer job, so the job should find none)
+  // The reducer waves' SIMD partners (waves 0 .. nred - 1, when there are at
+  // most two reducers) publish nothing either, so that the SIMDs running a
+  // reducer job carry less of the other work.
+  const bool reducer = wave >= NCOPY && wave - NCOPY < nred;
+  const int nfree = nred <= 2 ? nred : 0;           // partners left out
+  const int npub = FNW - nred - nfree;              // publishing waves
+  const int pslot = reducer || wave < nfree ? -1 : (wave < NCOPY ? wave - nfree : wave - nred - nfree);
+  const int ptid = pslot * kWave + lane_id_here();  // index among the publishing threads
   auto publish2 = [&](int qc) {
     const int tile = team + qc * a.teams;
-    for (int u = tid; u < NV1 * FM; u += FNT) {
+    if (pslot < 0) return;
+    for (int u = ptid; u < NV1 * FM; u += npub * kWave) {
       const int o = u / FM, t = u % FM;
       const int tg = tile * FM + t;
       float v = 0.f;
@@ -437,7 +472,7 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
     // partials of this member's jobs of tile q - 1 (BREC per lane) and H^pre /
     // idx of tile q - 2 (CREC per lane); their first loads went out at the
     // end of the previous step
-    const bool polls = wave >= NCOPY && (hasB || hasC);
+    const bool polls = poller && (hasB || hasC);
     lds_barrier();   // S1: tile q in the buffer
     if (hasA) {
       const uint32_t base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) unsigned char*)tbuf +
@@ -498,26 +533,25 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
         any = any || need[r];
       }
       if (__any(any)) ld_recs2t<BREC, CREC>(src, need, (uint32_t)q, (uint32_t)(q - 1), a.err, val);
-      const int pl = (wave - NCOPY) * kWave + lane_id_here();
+      const int pl = (wave - pw0) * kWave + lane_id_here();
 #pragma unroll
       for (int r = 0; r < BREC; ++r)
-        if (want[r]) (&sm.vals[0][0])[pl + r * NPOLL * kWave] = val[r];
+        if (want[r]) (&sm.vals[0][0])[pl + r * pstride] = val[r];
 #pragma unroll
       for (int r = 0; r < CREC; ++r)
         if (want[BREC + r]) {
-          const int u = pl + r * NPOLL * kWave, t = u / NV2, e = u % NV2;
+          const int u = pl + r * pstride, t = u / NV2, e = u % NV2;
           sm.hpid[t][e < FN ? 8 * (e & 1) + (e >> 1) : e] = val[BREC + r];
         }
     }
     lds_barrier();   // S3: A partials, polled records in LDS
     // the reducer waves (4 .. 4 + min(njobs, 4) - 1) finish their jobs of tile
     // q - 1 while the other waves publish the partials of tile q
-    if (hasB && wave >= NCOPY && wave - NCOPY < njobs)
+    if (hasB && reducer)
       for (int jj = wave - NCOPY; jj < njobs; jj += NPOLL) finish_job(q - 1, jj);
-    if (hasA && !(wave >= NCOPY && wave - NCOPY < njobs)) {
+    if (hasA && pslot >= 0) {
       uint64_t* r1 = rec1t + (q % RING) * G * FM * NV1;
-      const int nred = njobs < NPOLL ? njobs : NPOLL;   // reducer waves
-      for (int u = wave < NCOPY ? tid : tid - nred * kWave; u < NV1 * FM; u += FNT - nred * kWave) {
+      for (int u = ptid; u < NV1 * FM; u += npub * kWave) {
         const int o = u / FM, t = u % FM;
         float v = 0.f;
 #pragma unroll
@@ -584,7 +618,7 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
         }
       }
     }
-    if (wave >= NCOPY) issue_polls(q + 1, first);
+    if (poller) issue_polls(q + 1, first);
   };
   uint4 X0[KB1W], X1[KB1W], X2[KB1W];
   for (int q = 0; q < nq + 2; q += 3) {
