@@ -440,18 +440,21 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   // over the waves into part2; runs in the next step, after its first barrier
   // (not by the reducer waves: the compiler waits for every store a wave has
   // in flight before its reducer job, so the job should find none)
-  // The reducer waves' SIMD partners (waves 0 .. nred - 1, when there are at
-  // most two reducers) publish nothing either, so that the SIMDs running a
-  // reducer job carry less of the other work.
+  // The A partials are published (after S3) by the waves that are neither
+  // reducers nor, when there are at most two reducers, their SIMD partners
+  // (waves 0 .. nred - 1), so that the SIMDs running a reducer job carry less
+  // of the other work.
   const bool reducer = wave >= NCOPY && wave - NCOPY < nred;
   const int nfree = nred <= 2 ? nred : 0;           // partners left out
   const int npub = FNW - nred - nfree;              // publishing waves
   const int pslot = reducer || wave < nfree ? -1 : (wave < NCOPY ? wave - nfree : wave - nred - nfree);
   const int ptid = pslot * kWave + lane_id_here();  // index among the publishing threads
+  // The active partials (publish2) are stored by the waves that do not poll
+  // (0 .. pw0 - 1), before S3: the reducer wave is idle there.
   auto publish2 = [&](int qc) {
     const int tile = team + qc * a.teams;
-    if (pslot < 0) return;
-    for (int u = ptid; u < NV1 * FM; u += npub * kWave) {
+    if (poller) return;
+    for (int u = tid; u < NV1 * FM; u += pw0 * kWave) {
       const int o = u / FM, t = u % FM;
       const int tg = tile * FM + t;
       float v = 0.f;
@@ -517,7 +520,8 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
         sm.red[wave][33][tl] = v == 0 ? mom2[0] : (v == 1 ? mom2[1] : (v == 2 ? mom2[2] : mom2[3]));
       }
     }
-    if (q >= 3 && q - 3 < nq) publish2(q - 3);   // red2 of the previous step (its C of tile q - 3)
+    // red2 of the previous step (its C of tile q - 3), by the non-polling waves
+    if (!poller && q >= 3 && q - 3 < nq) publish2(q - 3);
     if (polls) {
       // tags: tile q - 1 for the partials, tile q - 2 for H^pre / idx
       const uint64_t* src[BREC + CREC];
