@@ -304,6 +304,11 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
       lds_dma16(src, __builtin_amdgcn_readfirstlane(tbase + t * TOKP + (n % 4) * 4 * ROWB));
     }
   };
+  // every load of the set-up has landed before the pipeline starts: a load
+  // left pending until its first use inside the loop (the last weight
+  // fragments, the reducers' constants) makes the compiler wait there for all
+  // memory operations in flight, tile copies included, in every step
+  __builtin_amdgcn_s_waitcnt(0);
   if (wave < NCOPY) copy_tile(team);
 
   // 1 / (N C): N C = 2048 G is a power of two, so multiplying by it is exact
@@ -422,12 +427,16 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   };
   // first loads of the records of step qs, issued at the end of step qs - 1
   // (polling waves) and checked after A of step qs
+  // (every lane loads, an unwanted record from the slot base, which is in
+  // bounds; its value is never used: a register cleared by a plain move while
+  // an earlier load into it may be in flight would make the compiler wait for
+  // every memory operation of the wave)
   auto issue_polls = [&](int qs, uint64_t (&first)[BREC + CREC]) {
 #pragma unroll
     for (int r = 0; r < BREC + CREC; ++r) {
       bool w;
       const uint64_t* pr = poll_rec(qs, r, w);
-      first[r] = w ? __hip_atomic_load(const_cast<uint64_t*>(pr), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+      first[r] = __hip_atomic_load(const_cast<uint64_t*>(pr), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   };
   uint64_t first[BREC + CREC];
