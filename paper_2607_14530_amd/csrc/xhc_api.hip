@@ -739,7 +739,9 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
   for (int q = 0; q < Q && e == hipSuccess; ++q) {
     // pre-map q + 1 (and the router with the first): dL/dH^pre,q+1 of the
     // active streams comes from the sublayer reverse (q >= 1); the base
-    // readouts of q >= 1 leave the active streams out
+    // readouts of q >= 1 leave the active streams out.  This view has no
+    // active-row projection (H^post and H^res are reversed per sublayer), so
+    // the active-row pass is left out.
     XHC_STEP("fpbwd_route", launch_pre_route(F32(w.part), proj_chunks(d->state_dtype, false, NC, (int)C, nf, T), nf,
                                              T, (int)N, d->m, (int)k, Q, C, colsum, alpha_pre, 1, b_pre, d->eps,
                                              reinterpret_cast<int32_t*>(ws + w.idx_s), F32(w.p_s), F32(w.hpre_s),
@@ -754,7 +756,8 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
                             F32(w.dhres0), F32(w.dhpost0), q == 0 ? dp : F32(w.dp0), dX, q == 0 ? dW_r : F32(w.dwr),
                             dW_pre + (int64_t)q * NC * N, F32(w.dwres), F32(w.dwpost), F32(w.dalpha),
                             db_pre + (int64_t)q * N, F32(w.dbres), F32(w.dbpost), ws + w.pre, s,
-                            q >= 1 ? dHpre_act + (int64_t)(q - 1) * T * k : nullptr, q >= 1 ? F32(w.hmask) : nullptr));
+                            q >= 1 ? dHpre_act + (int64_t)(q - 1) * T * k : nullptr, q >= 1 ? F32(w.hmask) : nullptr,
+                            /*dense_rows=*/true, /*X_bf16=*/nullptr, /*act_rows=*/false));
     XHC_STEP("fpbwd_copy", hipMemcpyAsync(dalpha_pre + q, F32(w.dalpha), sizeof(float), hipMemcpyDeviceToDevice, s));
   }
   return hip_status(e);

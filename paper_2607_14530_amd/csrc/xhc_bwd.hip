@@ -1317,7 +1317,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
                           hipStream_t s, const float* dhpre_act, const float* Hpre_read, bool dense_rows,
-                          const void* X_bf16) {
+                          const void* X_bf16, bool act_rows) {
   const float* Hrd = Hpre_read ? Hpre_read : Hpre;   // weights of the dense-read term
   const int64_t T = d->T;
   const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
@@ -1367,15 +1367,16 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
           reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T,
           N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
     const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
-    k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
-        reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T,
-        N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
+    if (act_rows)
+      k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
+          reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok,
+          T, N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
     k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
   }
   // an fp32 state given with its exact bf16 copy: the active rows take the
   // MFMA pass with fp32 gradient rows
   const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % kMfRows == 0;
-  if (mfa32) {
+  if (mfa32 && act_rows) {
     const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
     k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
         reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
@@ -1396,7 +1397,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
         default: XHC_FULL_ROWS(32); break;
       }
     }
-    if (!mfa32) {
+    if (!mfa32 && act_rows) {
       const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
       XHC_TS_DISPATCH(d->state_dtype,
         k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
@@ -1414,16 +1415,18 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     k_colsum_rows<<<dim3((unsigned)((nfull + 255) / 256)), dim3(256), 0, s>>>(wpart_p, nchunk, nfull, dW_pre);
   }
   // active partials are [chunk][kC][32]: split columns into W_post and W_res
-  const int64_t nact = (int64_t)k * C * 32;
-  k_colsum_rows<<<dim3((unsigned)((nact + 255) / 256)), dim3(256), 0, s>>>(wpart_a, nchunk, nact, red_a);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  e = hipMemcpy2DAsync(dW_post, (size_t)k * Kr * sizeof(float), red_a, 32 * sizeof(float),
-                       (size_t)k * Kr * sizeof(float), (size_t)k * C, hipMemcpyDeviceToDevice, s);
-  if (e != hipSuccess) return e;
-  e = hipMemcpy2DAsync(dW_res, (size_t)k * k * sizeof(float), red_a + k * Kr, 32 * sizeof(float),
-                       (size_t)k * k * sizeof(float), (size_t)k * C, hipMemcpyDeviceToDevice, s);
-  if (e != hipSuccess) return e;
+  if (act_rows) {
+    const int64_t nact = (int64_t)k * C * 32;
+    k_colsum_rows<<<dim3((unsigned)((nact + 255) / 256)), dim3(256), 0, s>>>(wpart_a, nchunk, nact, red_a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    e = hipMemcpy2DAsync(dW_post, (size_t)k * Kr * sizeof(float), red_a, 32 * sizeof(float),
+                         (size_t)k * Kr * sizeof(float), (size_t)k * C, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return e;
+    e = hipMemcpy2DAsync(dW_res, (size_t)k * k * sizeof(float), red_a + k * Kr, 32 * sizeof(float),
+                         (size_t)k * k * sizeof(float), (size_t)k * C, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return e;
+  }
   const int npg = pg_floats(N, k, Kr);
   k_sum_tokens<<<dim3((unsigned)npg), dim3(256), 0, s>>>(pg, T, npg, pgsum);
   e = hipGetLastError();
