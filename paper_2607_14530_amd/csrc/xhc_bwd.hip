@@ -972,7 +972,25 @@ __device__ __forceinline__ void split_bf16x8(const float (&f)[8], uint4& hi, uin
   lo = pack8(l);
 }
 
-// 4 consecutive gradient elements of a bf16 or fp32 accumulator row
+// 4 consecutive gradient elements of a bf16 or fp32 accumulator row, as
+// loaded (raw) and as floats
+template <typename TD> struct Raw4;
+template <> struct Raw4<uint16_t> {
+  typedef uint2 type;
+  static __device__ __forceinline__ type load(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
+  static __device__ __forceinline__ type zero() { return make_uint2(0, 0); }
+  static __device__ __forceinline__ void unpack(const type& v, float (&d)[4]) {
+    d[0] = bf_lo(v.x); d[1] = bf_hi(v.x); d[2] = bf_lo(v.y); d[3] = bf_hi(v.y);
+  }
+};
+template <> struct Raw4<float> {
+  typedef float4 type;
+  static __device__ __forceinline__ type load(const float* p) { return *reinterpret_cast<const float4*>(p); }
+  static __device__ __forceinline__ type zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
+  static __device__ __forceinline__ void unpack(const type& v, float (&d)[4]) {
+    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+  }
+};
 __device__ __forceinline__ void ld4(const uint16_t* p, float (&d)[4]) {
   const uint2 v = *reinterpret_cast<const uint2*>(p);
   d[0] = bf_lo(v.x); d[1] = bf_hi(v.x); d[2] = bf_lo(v.y); d[3] = bf_hi(v.y);
@@ -1040,6 +1058,8 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
     float scal[7];
     int row;
     uint4 x;
+    typename Raw4<TD>::type dx[2];   // the lane's accumulator elements (two token halves), as loaded
+    uint2 din[2];
   };
   auto fetch = [&](Stage& st, int64_t tb) {
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
@@ -1079,6 +1099,21 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
         st.x = *reinterpret_cast<const uint4*>(X + (t * N + row) * (int64_t)C + c0 + piece * 8);
       }
     }
+    // the accumulator rows of the step (other tokens than the step being
+    // computed, so reading them a step ahead is safe)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int u = 16 * h + l16;
+      const int kr = 16 * wave + 4 * g4;
+      st.dx[h] = Raw4<TD>::zero();
+      st.din[h] = make_uint2(0, 0);
+      if (u < nt) {
+        const int64_t t = tb + u;
+        const int row = ACT ? idx[t * k + part] : part;
+        st.dx[h] = Raw4<TD>::load(dX + (t * N + row) * (int64_t)C + c0 + kr);
+        if (!ACT) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
+      }
+    }
   };
   Stage cur;
   if (t0 < t1) fetch(cur, t0);
@@ -1096,24 +1131,11 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
       for (int i = 0; i < 7; ++i) sc[threadIdx.x][i] = cur.scal[i];
     }
     *reinterpret_cast<uint4*>(&xs[threadIdx.x / 8][(threadIdx.x % 8) * 8]) = cur.x;
+    // ---- dX: two token halves; the accumulator rows were read a step ahead
+    const typename Raw4<TD>::type dxr[2] = {cur.dx[0], cur.dx[1]};
+    const uint2 dinv[2] = {cur.din[0], cur.din[1]};
     __syncthreads();
     if (tb + kMfStep < t1) fetch(cur, tb + kMfStep);
-    // ---- dX: two token halves; the accumulator rows are read before the products
-    float dxv[2][4];
-    uint2 dinv[2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int u = 16 * h + l16;
-      const int kr = 16 * wave + 4 * g4;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) dxv[h][v] = 0.f;
-      dinv[h] = make_uint2(0, 0);
-      if (u < nt) {
-        const int64_t t = tb + u;
-        ld4(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr, dxv[h]);
-        if (!ACT) dinv[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
-      }
-    }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int u = 16 * h + l16;   // B operand token of this lane
@@ -1143,7 +1165,9 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
           for (int v = 0; v < 4; ++v)
             gsum[v] = hp * gi[v] + acc[v] - bpre * x[v] - r_ln * m1 - r_ln * r_ln * (x[v] - mu) * m2;
         }
-        const float d[4] = {dxv[h][0] + gsum[0], dxv[h][1] + gsum[1], dxv[h][2] + gsum[2], dxv[h][3] + gsum[3]};
+        float dxv[4];
+        Raw4<TD>::unpack(dxr[h], dxv);
+        const float d[4] = {dxv[0] + gsum[0], dxv[1] + gsum[1], dxv[2] + gsum[2], dxv[3] + gsum[3]};
         st4(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr, d);
       }
     }
