@@ -210,6 +210,9 @@ FlashPostBwdWs flash_post_bwd_ws(const xhc_dims* d, int Q, int q) {
 }
 
 struct FlashPreBwdWs {
+  size_t pre_slice;   // one pre-map reverse's workspace (Q of them when the row passes are fused)
+  bool fused;
+  size_t multi;       // the fused row pass's per-token inputs
   size_t pre, part, sums, saved, idx_s, p_s, hpre_s, hmask, wpost0, wres0, bres0, hpost0, dhpost0, dhres0, dp0,
       alpha_e, dwr, dwres, dwpost, dalpha, dbres, dbpost, total;
 };
@@ -221,14 +224,17 @@ FlashPreBwdWs flash_pre_bwd_ws(const xhc_dims* d, int Q) {
   const int64_t nf = (int64_t)(Q + 1) * N;
   Carve c;
   FlashPreBwdWs w;
-  w.pre = c.take(bwd_pre_ws_bytes(&e));
+  w.fused = bwd_rows_multi_supported(&e, Q);
+  w.pre_slice = align_up(bwd_pre_ws_bytes(&e));
+  w.pre = c.take((w.fused ? Q : 1) * w.pre_slice);
+  w.multi = c.take(w.fused ? bwd_rows_multi_ws_bytes(&e, Q) : 0);
   w.part = c.take(part_bytes(d, false, NC, nf));
   w.sums = c.take(sums_bytes(nf, T));
   w.saved = c.take((size_t)T * saved_floats(N, k, 1) * f);
   w.idx_s = c.take((size_t)T * k * sizeof(int32_t));
   w.p_s = c.take((size_t)T * k * f);
   w.hpre_s = c.take((size_t)Q * T * N * f);
-  w.hmask = c.take((size_t)T * N * f);
+  w.hmask = c.take((size_t)Q * T * N * f);   // [Q][T, N]: the masked dense-read weights of pre-map q >= 1
   w.wpost0 = c.take((size_t)kC * k * f);
   w.wres0 = c.take((size_t)kC * k * k * f);
   w.bres0 = c.take((size_t)k * k * f);
@@ -736,29 +742,49 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
   // streams pass it through, the active ones carry the reverse of the group
   XHC_STEP("fpbwd_scatter", launch_fbwd_scatter(d->state_dtype, T, (int)N, (int)k, (int)C, idx, dXn,
                                                  reinterpret_cast<const float*>(da0), dX, s));
-  for (int q = 0; q < Q && e == hipSuccess; ++q) {
-    // pre-map q + 1 (and the router with the first): dL/dH^pre,q+1 of the
-    // active streams comes from the sublayer reverse (q >= 1); the base
-    // readouts of q >= 1 leave the active streams out.  This view has no
-    // active-row projection (H^post and H^res are reversed per sublayer), so
-    // the active-row pass is left out.
-    XHC_STEP("fpbwd_route", launch_pre_route(F32(w.part), proj_chunks(d->state_dtype, false, NC, (int)C, nf, T), nf,
-                                             T, (int)N, d->m, (int)k, Q, C, colsum, alpha_pre, 1, b_pre, d->eps,
-                                             reinterpret_cast<int32_t*>(ws + w.idx_s), F32(w.p_s), F32(w.hpre_s),
-                                             F32(w.sums), F32(w.saved), nsave, nsave - 4, d->router, s, q));
-    XHC_STEP("fpbwd_alpha", launch_fbwd_alpha(alpha_pre + q, nullptr, nullptr, F32(w.alpha_e), s));
-    if (q >= 1) XHC_STEP("fpbwd_mask", launch_fbwd_mask(T, (int)N, (int)k, idx, Hpre + (int64_t)q * T * N,
-                                                        F32(w.hmask), s));
-    XHC_STEP("fpbwd_pre",
-             launch_bwd_pre(&en, X, colsum, W_r, W_pre + (int64_t)q * NC * N, F32(w.wres0), F32(w.wpost0),
-                            F32(w.alpha_e), F32(w.bres0), F32(w.saved), idx, p, Hpre + (int64_t)q * T * N,
-                            F32(w.hpost0), reinterpret_cast<const char*>(d_input) + (size_t)q * T * C * es,
-                            F32(w.dhres0), F32(w.dhpost0), q == 0 ? dp : F32(w.dp0), dX, q == 0 ? dW_r : F32(w.dwr),
-                            dW_pre + (int64_t)q * NC * N, F32(w.dwres), F32(w.dwpost), F32(w.dalpha),
-                            db_pre + (int64_t)q * N, F32(w.dbres), F32(w.dbpost), ws + w.pre, s,
-                            q >= 1 ? dHpre_act + (int64_t)(q - 1) * T * k : nullptr, q >= 1 ? F32(w.hmask) : nullptr,
-                            /*dense_rows=*/true, /*X_bf16=*/nullptr, /*act_rows=*/false));
-    XHC_STEP("fpbwd_copy", hipMemcpyAsync(dalpha_pre + q, F32(w.dalpha), sizeof(float), hipMemcpyDeviceToDevice, s));
+  // pre-map q + 1 (and the router with the first): dL/dH^pre,q+1 of the active
+  // streams comes from the sublayer reverse (q >= 1); the base readouts of q >=
+  // 1 leave the active streams out.  This view has no active-row projection
+  // (H^post and H^res are reversed per sublayer), so the active-row pass is
+  // left out.  Where supported the Q full-row passes run as one pass over the
+  // state (token records first, then the fused rows, then the reductions).
+  const float* hrd[4] = {nullptr, nullptr, nullptr, nullptr};
+  char* wsq[4] = {nullptr, nullptr, nullptr, nullptr};
+  auto pass = [&](int q, int phase) -> hipError_t {
+    char* wq = ws + w.pre + (w.fused ? (size_t)q * w.pre_slice : 0);
+    float* hm = F32(w.hmask) + (int64_t)q * T * N;
+    if (phase != kBwdPreReduce) {
+      hipError_t e1 = launch_pre_route(F32(w.part), proj_chunks(d->state_dtype, false, NC, (int)C, nf, T), nf, T,
+                                       (int)N, d->m, (int)k, Q, C, colsum, alpha_pre, 1, b_pre, d->eps,
+                                       reinterpret_cast<int32_t*>(ws + w.idx_s), F32(w.p_s), F32(w.hpre_s),
+                                       F32(w.sums), F32(w.saved), nsave, nsave - 4, d->router, s, q);
+      if (e1 == hipSuccess) e1 = launch_fbwd_alpha(alpha_pre + q, nullptr, nullptr, F32(w.alpha_e), s);
+      if (e1 == hipSuccess && q >= 1) e1 = launch_fbwd_mask(T, (int)N, (int)k, idx, Hpre + (int64_t)q * T * N, hm, s);
+      if (e1 != hipSuccess) return e1;
+    }
+    hrd[q] = q >= 1 ? hm : Hpre;
+    wsq[q] = wq;
+    return launch_bwd_pre(&en, X, colsum, W_r, W_pre + (int64_t)q * NC * N, F32(w.wres0), F32(w.wpost0),
+                          F32(w.alpha_e), F32(w.bres0), F32(w.saved), idx, p, Hpre + (int64_t)q * T * N,
+                          F32(w.hpost0), reinterpret_cast<const char*>(d_input) + (size_t)q * T * C * es,
+                          F32(w.dhres0), F32(w.dhpost0), q == 0 ? dp : F32(w.dp0), dX, q == 0 ? dW_r : F32(w.dwr),
+                          dW_pre + (int64_t)q * NC * N, F32(w.dwres), F32(w.dwpost), F32(w.dalpha),
+                          db_pre + (int64_t)q * N, F32(w.dbres), F32(w.dbpost), wq, s,
+                          q >= 1 ? dHpre_act + (int64_t)(q - 1) * T * k : nullptr, q >= 1 ? hm : nullptr,
+                          /*dense_rows=*/true, /*X_bf16=*/nullptr, /*act_rows=*/false, phase);
+  };
+  if (w.fused) {
+    for (int q = 0; q < Q && e == hipSuccess; ++q) XHC_STEP("fpbwd_tokens", pass(q, kBwdPreTokens));
+    XHC_STEP("fpbwd_rows", launch_bwd_rows_multi(&en, Q, X, dX, W_r, W_pre, d_input, hrd, wsq, F32(w.multi), s));
+    for (int q = 0; q < Q && e == hipSuccess; ++q) {
+      XHC_STEP("fpbwd_reduce", pass(q, kBwdPreReduce));
+      XHC_STEP("fpbwd_copy", hipMemcpyAsync(dalpha_pre + q, F32(w.dalpha), sizeof(float), hipMemcpyDeviceToDevice, s));
+    }
+  } else {
+    for (int q = 0; q < Q && e == hipSuccess; ++q) {
+      XHC_STEP("fpbwd_pre", pass(q, kBwdPreAll));
+      XHC_STEP("fpbwd_copy", hipMemcpyAsync(dalpha_pre + q, F32(w.dalpha), sizeof(float), hipMemcpyDeviceToDevice, s));
+    }
   }
   return hip_status(e);
 }

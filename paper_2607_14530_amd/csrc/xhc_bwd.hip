@@ -1313,7 +1313,274 @@ size_t bwd_post_ws_bytes(const xhc_dims* d) {
   return n * sizeof(float) + 256;
 }
 
+
+// The full-row pass of NQ pre-map reverses over one state in a single pass
+// (the entry state of an xHC-Flash group: the router with the first pre-map,
+// then one pre-map per sublayer; bf16 state, N = 16).  Same blocking as
+// k_bwd_rows_mfma; the contraction of the dX product runs over the 16 router
+// and 16 NQ pre-map outputs, each pass's per-token record (tok) giving its
+// own dz'.  The per-token terms add up over the passes: the dense reads
+// sum_q H^pre,q_i d input_q, the pre-map norm terms sum_q beta_pre,q x, and
+// the router's LayerNorm terms of the first pass (later passes have no router
+// gradient, so theirs are zero).  The weight partials of output block ob go
+// to wout[ob] ([chunk][N C][16]: the router, then pre-map q).
+constexpr int kMultiMaxQ = 4;
+struct MultiRows {
+  const float* tok[kMultiMaxQ];   // per pass: the token records
+  const float* hrd[kMultiMaxQ];   // per pass: weights of the dense read [T, N]
+  const uint16_t* din[kMultiMaxQ];
+  const float* w[kMultiMaxQ + 1];  // W_r, then W_pre of pass q ([N C][16] each)
+  float* wout[kMultiMaxQ + 1];
+};
+// Per token, the inputs of k_bwd_rows_multi gathered from the passes' token
+// records: [r_ln dz_r (16) | r dz_pre,q (16 each) | r_ln, mu, m1, m2,
+// sum_q beta_pre,q, pad], pitch 16 (NQ + 1) + 8 floats.
+template <int NQ>
+__global__ __launch_bounds__(256) void k_multi_prep(MultiRows m, int64_t T, int N, int NA, float* __restrict__ out) {
+  constexpr int NO = 16 * (NQ + 1), PITCH = NO + 8;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= T * PITCH) return;
+  const int64_t t = i / PITCH;
+  const int o = (int)(i % PITCH);
+  const int TF = tok_floats(N, NA);
+  float v = 0.f;
+  if (o < NO) {
+    const float* tk = m.tok[o < 16 ? 0 : o / 16 - 1] + t * TF;
+    v = o < 16 ? tk[2 * N + NA + 1] * tk[o] : tk[2 * N + NA + 0] * tk[N + o % 16];   // r_ln dz_r | r dz_pre,q
+  } else if (o < NO + 4) {
+    const int map[4] = {1, 2, 4, 5};   // r_ln, mu, m1, m2 of the first pass
+    v = m.tok[0][t * TF + 2 * N + NA + map[o - NO]];
+  } else if (o == NO + 4) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) v += m.tok[q][t * TF + 2 * N + NA + 3];   // beta_pre, passes in order
+  }
+  out[i] = v;
+}
+
+template <int NQ>
+__global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restrict__ X, uint16_t* __restrict__ dX,
+                                                        MultiRows m, const float* __restrict__ prep, int64_t T,
+                                                        int N, int C, int NA, int64_t tchunk) {
+  constexpr int NO = 16 * (NQ + 1);            // outputs
+  constexpr int NKB = (NO + 31) / 32;          // 32-output blocks of the dX contraction
+  constexpr int NDZ = kMfStep * NO / 256;      // dz' values fetched per thread
+  static_assert(kMfStep * NO % 256 == 0, "whole dz' rows per step");
+  __shared__ __align__(16) uint16_t xs[kMfStep][kMfXPitch];
+  __shared__ float dzs[kMfStep][NKB * 32 + 1];
+  __shared__ float sc[kMfStep][5 + NQ];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int l16 = lane % 16, g4 = lane / 16;
+  const int64_t K0 = (int64_t)blockIdx.x * kMfRows;
+  const int part = (int)(K0 / C);              // stream
+  const int c0 = (int)(K0 % C);
+  const int64_t NK = (int64_t)N * C;
+  constexpr int PITCH = NO + 8;
+  uint4 wfrag[NKB];
+  {
+    const int64_t K = K0 + 16 * wave + l16;
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int o = 32 * kb + 8 * g4 + e;
+        f[e] = o < NO ? __uint_as_float(f2bf(m.w[o / 16][K * 16 + o % 16]) << 16) : 0.f;
+      }
+      wfrag[kb] = pack8(f);
+    }
+  }
+  f32x4 dw[NQ + 1];
+#pragma unroll
+  for (int ob = 0; ob <= NQ; ++ob) dw[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
+  struct Stage {
+    float dz[NDZ];
+    float scal[5 + NQ];
+    uint4 x;
+    uint2 dx[2];
+  };
+  auto fetch = [&](Stage& st, int64_t tb) {
+    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
+#pragma unroll
+    for (int r = 0; r < NDZ; ++r) {
+      const int q = threadIdx.x + r * 256, u = q / NO, o = q % NO;
+      st.dz[r] = u < nt ? prep[(tb + u) * PITCH + o] : 0.f;
+    }
+    if (threadIdx.x < kMfStep) {
+      const int u = threadIdx.x;
+      const int64_t t = tb + (u < nt ? u : 0);
+#pragma unroll
+      for (int i = 0; i < 5; ++i) st.scal[i] = prep[t * PITCH + NO + i];   // r_ln, mu, m1, m2, sum beta_pre
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) st.scal[5 + q] = m.hrd[q][t * N + part];
+    }
+    {
+      const int u = threadIdx.x / 8, piece = threadIdx.x % 8;
+      st.x = make_uint4(0, 0, 0, 0);
+      if (u < nt) st.x = *reinterpret_cast<const uint4*>(X + ((tb + u) * N + part) * (int64_t)C + c0 + piece * 8);
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int u = 16 * h + l16;
+      const int kr = 16 * wave + 4 * g4;
+      st.dx[h] = make_uint2(0, 0);
+      if (u < nt) st.dx[h] = *reinterpret_cast<const uint2*>(dX + ((tb + u) * N + part) * (int64_t)C + c0 + kr);
+    }
+  };
+  Stage cur;
+  if (t0 < t1) fetch(cur, t0);
+  for (int64_t tb = t0; tb < t1; tb += kMfStep) {
+    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
+    __syncthreads();   // the previous step's LDS reads are done
+#pragma unroll
+    for (int r = 0; r < NDZ; ++r) {
+      const int q = threadIdx.x + r * 256;
+      dzs[q / NO][q % NO] = cur.dz[r];
+    }
+    for (int q = threadIdx.x; q < kMfStep * (NKB * 32 - NO); q += 256)   // outputs past NO are zero
+      dzs[q / (NKB * 32 - NO)][NO + q % (NKB * 32 - NO)] = 0.f;
+    if (threadIdx.x < kMfStep) {
+#pragma unroll
+      for (int i = 0; i < 5 + NQ; ++i) sc[threadIdx.x][i] = cur.scal[i];
+    }
+    *reinterpret_cast<uint4*>(&xs[threadIdx.x / 8][(threadIdx.x % 8) * 8]) = cur.x;
+    const uint2 dxr[2] = {cur.dx[0], cur.dx[1]};
+    __syncthreads();
+    // the input gradients of this step (read here: prefetched, the Q rows
+    // would hold too many registers)
+    uint2 dinv[NQ][2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int u = 16 * h + l16;
+      const int kr = 16 * wave + 4 * g4;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        dinv[q][h] = u < nt ? *reinterpret_cast<const uint2*>(m.din[q] + (tb + u) * C + c0 + kr) : make_uint2(0, 0);
+    }
+    if (tb + kMfStep < t1) fetch(cur, tb + kMfStep);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int u = 16 * h + l16;
+      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kb = 0; kb < NKB; ++kb) {
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = dzs[u][32 * kb + 8 * g4 + e];
+        uint4 bh, bl;
+        split_bf16x8(f, bh, bl);
+        acc = mfma_16x16x32(wfrag[kb], bh, acc);
+        acc = mfma_16x16x32(wfrag[kb], bl, acc);
+      }
+      if (u < nt) {
+        const int64_t t = tb + u;
+        const int kr = 16 * wave + 4 * g4;
+        const uint2 xv = *reinterpret_cast<const uint2*>(&xs[u][kr]);
+        const float x[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
+        const float r_ln = sc[u][0], mu = sc[u][1], m1 = sc[u][2], m2 = sc[u][3], bsum = sc[u][4];
+        float rd[4] = {0.f, 0.f, 0.f, 0.f};   // sum_q H^pre,q d input_q, passes in order
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) {
+          const float hp = sc[u][5 + q];
+          const float gi[4] = {bf_lo(dinv[q][h].x), bf_hi(dinv[q][h].x), bf_lo(dinv[q][h].y), bf_hi(dinv[q][h].y)};
+#pragma unroll
+          for (int v = 0; v < 4; ++v) rd[v] = fmaf(hp, gi[v], rd[v]);
+        }
+        const float dxv[4] = {bf_lo(dxr[h].x), bf_hi(dxr[h].x), bf_lo(dxr[h].y), bf_hi(dxr[h].y)};
+        float d[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          d[v] = dxv[v] + (rd[v] + acc[v] - bsum * x[v] - r_ln * m1 - r_ln * r_ln * (x[v] - mu) * m2);
+        *reinterpret_cast<uint2*>(dX + (t * N + part) * (int64_t)C + c0 + kr) =
+            make_uint2(pack2bf(d[0], d[1]), pack2bf(d[2], d[3]));
+      }
+    }
+    {
+      uint16_t xb[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xb[e] = xs[8 * g4 + e][16 * wave + l16];
+      const uint4 bx = make_uint4(xb[0] | ((uint32_t)xb[1] << 16), xb[2] | ((uint32_t)xb[3] << 16),
+                                  xb[4] | ((uint32_t)xb[5] << 16), xb[6] | ((uint32_t)xb[7] << 16));
+#pragma unroll
+      for (int ob = 0; ob <= NQ; ++ob) {
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = dzs[8 * g4 + e][16 * ob + l16];
+        uint4 ah, al;
+        split_bf16x8(f, ah, al);
+        dw[ob] = mfma_16x16x32(ah, bx, dw[ob]);
+        dw[ob] = mfma_16x16x32(al, bx, dw[ob]);
+      }
+    }
+  }
+  const int64_t K = K0 + 16 * wave + l16;
+#pragma unroll
+  for (int ob = 0; ob <= NQ; ++ob) {
+    float* dst = m.wout[ob] + ((int64_t)blockIdx.y * NK + K) * 16 + 4 * g4;
+    *reinterpret_cast<float4*>(dst) = make_float4(dw[ob][0], dw[ob][1], dw[ob][2], dw[ob][3]);
+  }
+}
+
 constexpr int64_t kRowChunk = 1024;   // tokens per weight-gradient partial
+
+BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws) {
+  const int64_t T = d->T;
+  const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
+  const int NA = k * Kr + k * k;
+  const int64_t ncb = post_chunks(C);
+  const int64_t nchunk = (T + kRowChunk - 1) / kRowChunk;
+  BwdPreWs w;
+  w.part = reinterpret_cast<float*>(ws);
+  w.tok = w.part + ncb * N * T;
+  w.pg = w.tok + T * tok_floats(N, NA);
+  w.wpart_r = w.pg + T * pg_floats(N, k, Kr);
+  w.wpart_p = w.wpart_r + nchunk * (int64_t)N * C * N;
+  w.wpart_a = w.wpart_p + nchunk * (int64_t)N * C * N;
+  w.red_a = w.wpart_a + nchunk * (int64_t)k * C * 32;           // [kC][32]
+  w.pgsum = w.red_a + (int64_t)k * C * 32;
+  return w;
+}
+
+bool bwd_rows_multi_supported(const xhc_dims* d, int Q) {
+  return d->state_dtype == XHC_BF16 && d->N == 16 && d->C % kMfRows == 0 && (Q == 2 || Q == 4);
+}
+
+size_t bwd_rows_multi_ws_bytes(const xhc_dims* d, int Q) {
+  return (size_t)d->T * (16 * (Q + 1) + 8) * sizeof(float);
+}
+
+hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* dX, const float* W_r,
+                                 const float* W_pre, const void* d_input, const float* const* hrd, char* const* ws,
+                                 float* prep, hipStream_t s) {
+  if (!bwd_rows_multi_supported(d, Q)) return hipErrorInvalidValue;
+  const int64_t T = d->T;
+  const int N = d->N, C = d->C, NA = d->k * d->Kr + d->k * d->k;
+  const int64_t NC = (int64_t)N * C, nchunk = (T + kRowChunk - 1) / kRowChunk;
+  MultiRows m{};
+  m.w[0] = W_r;
+  m.wout[0] = bwd_pre_ws(d, ws[0]).wpart_r;
+  for (int q = 0; q < Q; ++q) {
+    const BwdPreWs w = bwd_pre_ws(d, ws[q]);
+    m.tok[q] = w.tok;
+    m.hrd[q] = hrd[q];
+    m.din[q] = reinterpret_cast<const uint16_t*>(d_input) + (int64_t)q * T * C;
+    m.w[q + 1] = W_pre + (int64_t)q * NC * N;
+    m.wout[q + 1] = w.wpart_p;
+  }
+  const dim3 g((unsigned)(NC / kMfRows), (unsigned)nchunk);
+  const int64_t np = T * (16 * (Q + 1) + 8);
+  const dim3 gp((unsigned)((np + 255) / 256));
+  if (Q == 4) {
+    k_multi_prep<4><<<gp, dim3(256), 0, s>>>(m, T, N, NA, prep);
+    k_bwd_rows_multi<4><<<g, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), reinterpret_cast<uint16_t*>(dX),
+                                                m, prep, T, N, C, NA, kRowChunk);
+  } else {
+    k_multi_prep<2><<<gp, dim3(256), 0, s>>>(m, T, N, NA, prep);
+    k_bwd_rows_multi<2><<<g, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), reinterpret_cast<uint16_t*>(dX),
+                                                m, prep, T, N, C, NA, kRowChunk);
+  }
+  return hipGetLastError();
+}
 
 size_t bwd_pre_ws_bytes(const xhc_dims* d) {
   const int64_t T = d->T;
@@ -1341,94 +1608,101 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
                           hipStream_t s, const float* dhpre_act, const float* Hpre_read, bool dense_rows,
-                          const void* X_bf16, bool act_rows) {
+                          const void* X_bf16, bool act_rows, int phase) {
   const float* Hrd = Hpre_read ? Hpre_read : Hpre;   // weights of the dense-read term
   const int64_t T = d->T;
   const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
   const int NA = k * Kr + k * k;
   const int64_t ncb = post_chunks(C);
   const int64_t nchunk = (T + kRowChunk - 1) / kRowChunk;
-  float* part = reinterpret_cast<float*>(ws);
-  float* tok = part + ncb * N * T;
-  float* pg = tok + T * tok_floats(N, NA);
-  float* wpart_r = pg + T * pg_floats(N, k, Kr);
-  float* wpart_p = wpart_r + nchunk * (int64_t)N * C * N;
-  float* wpart_a = wpart_p + nchunk * (int64_t)N * C * N;
-  float* red_a = wpart_a + nchunk * (int64_t)k * C * 32;           // [kC][32]
-  float* pgsum = red_a + (int64_t)k * C * 32;
-  if (!dense_rows) {
-    hipError_t e0 = launch_fill0(part, (size_t)ncb * N * T * sizeof(float), s);
-    if (e0 != hipSuccess) return e0;
-  } else {
-    XHC_TS_DISPATCH(d->state_dtype,
-      k_bwd_dhpre<TS><<<dim3((unsigned)(T * ncb)), dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),
-          reinterpret_cast<const TS*>(d_input), T, N, C, part));
-  }
-  if (dhpre_act) {
-    k_bwd_dhpre_override<<<dim3((unsigned)((T * k + 255) / 256)), dim3(256), 0, s>>>(dhpre_act, idx, T, N, k, ncb,
-                                                                                    part);
-  }
-  {
-    const dim3 gt((unsigned)((T + kPreTokThreads - 1) / kPreTokThreads)), bt(kPreTokThreads);
-    if (k == 4 && 2 * d->sinkhorn_iters <= kSkMaxSteps)
-      k_bwd_pre_token<4><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
-                                          Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
-                                          d->clamp_delta, tok, pg,
-                                          d->router == XHC_ROUTER_SOFTMAX ? 1 : 0);
-    else
-      k_bwd_pre_token<0><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
-                                          Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
-                                          d->clamp_delta, tok, pg,
-                                          d->router == XHC_ROUTER_SOFTMAX ? 1 : 0);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  const BwdPreWs w = bwd_pre_ws(d, ws);
+  float* const part = w.part;
+  float* const tok = w.tok;
+  float* const pg = w.pg;
+  float* const wpart_r = w.wpart_r;
+  float* const wpart_p = w.wpart_p;
+  float* const wpart_a = w.wpart_a;
+  float* const red_a = w.red_a;
+  float* const pgsum = w.pgsum;
   const bool mf = d->state_dtype == XHC_BF16 && N == 16 && NA <= 32 && C % kMfRows == 0;
-  if (mf) {
-    const dim3 gf((unsigned)((int64_t)N * C / kMfRows), (unsigned)nchunk);
-    if (dense_rows)
-      k_bwd_rows_mfma<false><<<gf, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
-          reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T,
-          N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
-    const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
-    if (act_rows)
-      k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
-          reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok,
-          T, N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
-    k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
-  }
-  // an fp32 state given with its exact bf16 copy: the active rows take the
-  // MFMA pass with fp32 gradient rows
-  const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % kMfRows == 0;
-  if (mfa32 && act_rows) {
-    const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
-    k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
-        reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
-        nullptr);
-  }
-  const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
+  hipError_t e = hipSuccess;
+  if (phase == kBwdPreReduce) {
+    // the row passes ran elsewhere (their partials are in this workspace)
+    if (mf) k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
+  } else {
+    if (!dense_rows) {
+      hipError_t e0 = launch_fill0(part, (size_t)ncb * N * T * sizeof(float), s);
+      if (e0 != hipSuccess) return e0;
+    } else {
+      XHC_TS_DISPATCH(d->state_dtype,
+        k_bwd_dhpre<TS><<<dim3((unsigned)(T * ncb)), dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),
+            reinterpret_cast<const TS*>(d_input), T, N, C, part));
+    }
+    if (dhpre_act) {
+      k_bwd_dhpre_override<<<dim3((unsigned)((T * k + 255) / 256)), dim3(256), 0, s>>>(dhpre_act, idx, T, N, k, ncb,
+                                                                                      part);
+    }
+    {
+      const dim3 gt((unsigned)((T + kPreTokThreads - 1) / kPreTokThreads)), bt(kPreTokThreads);
+      if (k == 4 && 2 * d->sinkhorn_iters <= kSkMaxSteps)
+        k_bwd_pre_token<4><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
+                                            Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
+                                            d->clamp_delta, tok, pg,
+                                            d->router == XHC_ROUTER_SOFTMAX ? 1 : 0);
+      else
+        k_bwd_pre_token<0><<<gt, bt, 0, s>>>(part, ncb, T, N, d->m, k, Kr, C, saved, colsum, alpha, b_res, idx, p,
+                                            Hpre, Hpost, dHres, dHpost, dp, d->eps, d->sinkhorn_iters,
+                                            d->clamp_delta, tok, pg,
+                                            d->router == XHC_ROUTER_SOFTMAX ? 1 : 0);
+    }
+    e = hipGetLastError();
+    if (e != hipSuccess || phase == kBwdPreTokens) return e;
+    if (mf) {
+      const dim3 gf((unsigned)((int64_t)N * C / kMfRows), (unsigned)nchunk);
+      if (dense_rows)
+        k_bwd_rows_mfma<false><<<gf, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
+            reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T,
+            N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
+      const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
+      if (act_rows)
+        k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
+            reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok,
+            T, N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
+      k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
+    }
+    // an fp32 state given with its exact bf16 copy: the active rows take the
+    // MFMA pass with fp32 gradient rows
+    const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % kMfRows == 0;
+    if (mfa32 && act_rows) {
+      const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
+      k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
+          reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
+          nullptr);
+    }
+    const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
 #define XHC_FULL_ROWS(NNV)                                                                                       \
-  XHC_TS_DISPATCH(d->state_dtype,                                                                                \
-    k_bwd_full_rows<TS, NNV><<<gfull, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),                        \
-        reinterpret_cast<const TS*>(d_input), reinterpret_cast<TS*>(dX), W_r, W_pre, Hrd, tok, T, C, NA,         \
-        kRowChunk, wpart_r, wpart_p))
-  if (!mf) {
-    if (dense_rows) {
-      switch (N) {
-        case 4: XHC_FULL_ROWS(4); break;
-        case 8: XHC_FULL_ROWS(8); break;
-        case 16: XHC_FULL_ROWS(16); break;
-        default: XHC_FULL_ROWS(32); break;
+    XHC_TS_DISPATCH(d->state_dtype,                                                                                \
+      k_bwd_full_rows<TS, NNV><<<gfull, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X),                        \
+          reinterpret_cast<const TS*>(d_input), reinterpret_cast<TS*>(dX), W_r, W_pre, Hrd, tok, T, C, NA,         \
+          kRowChunk, wpart_r, wpart_p))
+    if (!mf) {
+      if (dense_rows) {
+        switch (N) {
+          case 4: XHC_FULL_ROWS(4); break;
+          case 8: XHC_FULL_ROWS(8); break;
+          case 16: XHC_FULL_ROWS(16); break;
+          default: XHC_FULL_ROWS(32); break;
+        }
+      }
+      if (!mfa32 && act_rows) {
+        const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
+        XHC_TS_DISPATCH(d->state_dtype,
+          k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
+              W_post, W_res, idx, tok, T, N, k, C, Kr, kRowChunk, wpart_a));
       }
     }
-    if (!mfa32 && act_rows) {
-      const dim3 gact((unsigned)(((int64_t)k * C + 255) / 256), (unsigned)nchunk);
-      XHC_TS_DISPATCH(d->state_dtype,
-        k_bwd_act_rows<TS, 32><<<gact, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(X), reinterpret_cast<TS*>(dX),
-            W_post, W_res, idx, tok, T, N, k, C, Kr, kRowChunk, wpart_a));
-    }
-  }
 #undef XHC_FULL_ROWS
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // token reductions (fixed order)

@@ -123,6 +123,14 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
 size_t bwd_post_ws_bytes(const xhc_dims* d);
 bool bwd_pre_supported(const xhc_dims* d);
 size_t bwd_pre_ws_bytes(const xhc_dims* d);
+// phases of launch_bwd_pre: everything; the per-token part only (dH^pre,
+// token reverse: the records the row passes read); the reductions only (the
+// row passes' partials already in the workspace)
+constexpr int kBwdPreAll = 0, kBwdPreTokens = 1, kBwdPreReduce = 2;
+struct BwdPreWs {
+  float *part, *tok, *pg, *wpart_r, *wpart_p, *wpart_a, *red_a, *pgsum;
+};
+BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws);   // layout of launch_bwd_pre's workspace
 hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum, const float* W_r,
                           const float* W_pre, const float* W_res, const float* W_post, const float* alpha,
                           const float* b_res, const float* saved, const int32_t* idx, const float* p,
@@ -130,7 +138,8 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
                           hipStream_t s, const float* dhpre_act = nullptr, const float* Hpre_read = nullptr,
-                          bool dense_rows = true, const void* X_bf16 = nullptr, bool act_rows = true);
+                          bool dense_rows = true, const void* X_bf16 = nullptr, bool act_rows = true,
+                          int phase = kBwdPreAll);
 // dhpre_act [T,k]: when given, dL/dH^pre of the active streams (slot order)
 // replaces <d input, x_i> there; Hpre_read [T,N]: when given, the weights of
 // the dense-read term dX_i += H^pre_i d input (Hpre otherwise).  dense_rows
@@ -142,6 +151,18 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
 // MFMA form of the active-row pass; the gradient rows stay fp32).  act_rows
 // false leaves out the active-row pass (for a caller whose W_post and W_res
 // are zero): dW_post, dW_res are not written.
+// The full-row pass of Q pre-map reverses of one bf16 state (N = 16, Q = 2 or
+// 4) in one pass: pass q's token records and weight partials live in the
+// launch_bwd_pre workspace ws[q] (after its kBwdPreTokens phase; the router's
+// partials in ws[0]), hrd[q] are its dense-read weights [T, N], d_input is
+// [Q, T, C]; dX accumulates every pass's row terms.
+// prep: a scratch buffer of bwd_rows_multi_ws_bytes (per-token inputs of the
+// fused pass).
+bool bwd_rows_multi_supported(const xhc_dims* d, int Q);
+size_t bwd_rows_multi_ws_bytes(const xhc_dims* d, int Q);
+hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* dX, const float* W_r,
+                                 const float* W_pre, const void* d_input, const float* const* hrd, char* const* ws,
+                                 float* prep, hipStream_t s);
 
 // ---- xHC-Flash backward helpers
 hipError_t launch_fill0(void* p, size_t bytes, hipStream_t s);
