@@ -774,7 +774,9 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
                           /*dense_rows=*/true, /*X_bf16=*/nullptr, /*act_rows=*/false, phase);
   };
   if (w.fused) {
-    for (int q = 0; q < Q && e == hipSuccess; ++q) XHC_STEP("fpbwd_tokens", pass(q, kBwdPreTokens));
+    for (int q = 0; q < Q; ++q) wsq[q] = ws + w.pre + (size_t)q * w.pre_slice;
+    XHC_STEP("fpbwd_dhpre", launch_bwd_dhpre_multi(&en, Q, X, d_input, wsq, s));
+    for (int q = 0; q < Q && e == hipSuccess; ++q) XHC_STEP("fpbwd_tokens", pass(q, kBwdPreTokensGiven));
     XHC_STEP("fpbwd_rows", launch_bwd_rows_multi(&en, Q, X, dX, W_r, W_pre, d_input, hrd, wsq, F32(w.multi), s));
     for (int q = 0; q < Q && e == hipSuccess; ++q) {
       XHC_STEP("fpbwd_reduce", pass(q, kBwdPreReduce));

@@ -612,6 +612,49 @@ __global__ __launch_bounds__(256) void k_bwd_dhpre(const TS* __restrict__ X, con
   for (int i = threadIdx.x; i < N; i += 256) part[(cb * N + i) * T + t] = red[0][i] + red[1][i] + red[2][i] + red[3][i];
 }
 
+// The same partials for NQ input gradients din + q T C at once (one read of
+// the state): part[q][chunk][i][t]
+struct MultiParts {
+  float* part[4];
+};
+template <typename TS, int NQ>
+__global__ __launch_bounds__(256) void k_bwd_dhpre_multi(const TS* __restrict__ X, const TS* __restrict__ din,
+                                                         int64_t T, int N, int C, MultiParts mp) {
+  __shared__ float red[NQ][4][kMaxN];
+  const int64_t ncb = post_chunks(C);
+  const int64_t t = blockIdx.x / ncb, cb = blockIdx.x % ncb;
+  const int c = (int)(cb * 256 + threadIdx.x) * 8;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  float g[NQ][8];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+    if (c < C) Vec8<TS>::load(din + ((int64_t)q * T + t) * C + c, g[q]);
+  for (int i = 0; i < N; ++i) {
+    float v[NQ];
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) v[q] = 0.f;
+    if (c < C) {
+      float x[8];
+      Vec8<TS>::load(X + (t * N + i) * (int64_t)C + c, x);
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[q] = fmaf(g[q][e], x[e], v[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) v[q] += __shfl_xor(v[q], off);
+      if (lane == 0) red[q][wave][i] = v[q];
+    }
+  }
+  __syncthreads();
+  for (int u = threadIdx.x; u < NQ * N; u += 256) {
+    const int q = u / N, i = u % N;
+    mp.part[q][(cb * N + i) * T + t] = red[q][0][i] + red[q][1][i] + red[q][2][i] + red[q][3][i];
+  }
+}
+
 // Per-token record written by k_bwd_pre_token (floats):
 //   [dz_r (N) | dz_pre (N) | dz_act (NA) | r | r_ln | mu | beta_pre | m1 | m2 | r_a | beta_a]
 // and per-token gating/bias gradients pg: [dalpha_pre, dalpha_res, dalpha_post | db_pre (N) |
@@ -1545,6 +1588,19 @@ bool bwd_rows_multi_supported(const xhc_dims* d, int Q) {
   return d->state_dtype == XHC_BF16 && d->N == 16 && d->C % kMfRows == 0 && (Q == 2 || Q == 4);
 }
 
+hipError_t launch_bwd_dhpre_multi(const xhc_dims* d, int Q, const void* X, const void* d_input, char* const* ws,
+                                  hipStream_t s) {
+  if (!bwd_rows_multi_supported(d, Q)) return hipErrorInvalidValue;
+  MultiParts mp{};
+  for (int q = 0; q < Q; ++q) mp.part[q] = bwd_pre_ws(d, ws[q]).part;
+  const dim3 g((unsigned)(d->T * post_chunks(d->C)));
+  const uint16_t* x = reinterpret_cast<const uint16_t*>(X);
+  const uint16_t* din = reinterpret_cast<const uint16_t*>(d_input);
+  if (Q == 4) k_bwd_dhpre_multi<uint16_t, 4><<<g, dim3(256), 0, s>>>(x, din, d->T, d->N, d->C, mp);
+  else k_bwd_dhpre_multi<uint16_t, 2><<<g, dim3(256), 0, s>>>(x, din, d->T, d->N, d->C, mp);
+  return hipGetLastError();
+}
+
 size_t bwd_rows_multi_ws_bytes(const xhc_dims* d, int Q) {
   return (size_t)d->T * (16 * (Q + 1) + 8) * sizeof(float);
 }
@@ -1630,7 +1686,9 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     // the row passes ran elsewhere (their partials are in this workspace)
     if (mf) k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
   } else {
-    if (!dense_rows) {
+    if (phase == kBwdPreTokensGiven) {
+      // the dH^pre partials are already in the workspace
+    } else if (!dense_rows) {
       hipError_t e0 = launch_fill0(part, (size_t)ncb * N * T * sizeof(float), s);
       if (e0 != hipSuccess) return e0;
     } else {
@@ -1656,7 +1714,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                                             d->router == XHC_ROUTER_SOFTMAX ? 1 : 0);
     }
     e = hipGetLastError();
-    if (e != hipSuccess || phase == kBwdPreTokens) return e;
+    if (e != hipSuccess || phase == kBwdPreTokens || phase == kBwdPreTokensGiven) return e;
     if (mf) {
       const dim3 gf((unsigned)((int64_t)N * C / kMfRows), (unsigned)nchunk);
       if (dense_rows)

@@ -126,7 +126,9 @@ size_t bwd_pre_ws_bytes(const xhc_dims* d);
 // phases of launch_bwd_pre: everything; the per-token part only (dH^pre,
 // token reverse: the records the row passes read); the reductions only (the
 // row passes' partials already in the workspace)
-constexpr int kBwdPreAll = 0, kBwdPreTokens = 1, kBwdPreReduce = 2;
+// (kBwdPreTokensGiven: the per-token part with the <d input, x_i> partials
+// already in the workspace, e.g. from launch_bwd_dhpre_multi)
+constexpr int kBwdPreAll = 0, kBwdPreTokens = 1, kBwdPreReduce = 2, kBwdPreTokensGiven = 3;
 struct BwdPreWs {
   float *part, *tok, *pg, *wpart_r, *wpart_p, *wpart_a, *red_a, *pgsum;
 };
@@ -160,6 +162,10 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
 // fused pass).
 bool bwd_rows_multi_supported(const xhc_dims* d, int Q);
 size_t bwd_rows_multi_ws_bytes(const xhc_dims* d, int Q);
+// the <d input_q, x_i> partials of the Q passes in one read of the state,
+// into each pass's workspace ws[q]
+hipError_t launch_bwd_dhpre_multi(const xhc_dims* d, int Q, const void* X, const void* d_input, char* const* ws,
+                                  hipStream_t s);
 hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* dX, const float* W_r,
                                  const float* W_pre, const void* d_input, const float* const* hrd, char* const* ws,
                                  float* prep, hipStream_t s);
