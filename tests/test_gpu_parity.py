@@ -30,6 +30,10 @@ SMALL = [
     # member and tile) and a ragged last tile
     W(T=77, S=77, N=16, k=4, m=2, C=256, Kr=1, name="team2-T77-C256"),
     W(T=50, S=25, N=16, k=4, m=2, C=128, Kr=4, name="team1-T50-C128"),
+    # teams of 16 and 32 workgroups: two reducer waves, and a sole reducer wave
+    # (its own polling and publishing roles), every output compared
+    W(T=96, S=48, N=16, k=4, m=2, C=2048, Kr=4, name="team16-T96-C2048"),
+    W(T=72, S=36, N=16, k=4, m=2, C=4096, Kr=1, name="team32-T72-C4096"),
     # softmax router (ablation): both pre implementations, and N = 8 with m = 1
     W(T=256, S=128, N=16, k=4, m=2, C=1024, Kr=4, router="softmax", name="softmax-router-C1024"),
     W(T=96, S=48, N=8, k=4, m=1, C=256, Kr=1, router="softmax", name="softmax-router-N8"),
