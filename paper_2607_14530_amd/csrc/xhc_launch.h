@@ -123,11 +123,11 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
 size_t bwd_post_ws_bytes(const xhc_dims* d);
 bool bwd_pre_supported(const xhc_dims* d);
 size_t bwd_pre_ws_bytes(const xhc_dims* d);
-// phases of launch_bwd_pre: everything; the per-token part only (dH^pre,
-// token reverse: the records the row passes read); the reductions only (the
-// row passes' partials already in the workspace)
-// (kBwdPreTokensGiven: the per-token part with the <d input, x_i> partials
-// already in the workspace, e.g. from launch_bwd_dhpre_multi)
+// phases of launch_bwd_pre: kBwdPreAll everything; kBwdPreTokens the
+// per-token part only (the <d input, x_i> partials and the token reverse:
+// the records the row passes read); kBwdPreTokensGiven the same with those
+// partials already in the workspace (launch_bwd_dhpre_multi); kBwdPreReduce
+// the reductions only (the row passes' partials already in the workspace)
 constexpr int kBwdPreAll = 0, kBwdPreTokens = 1, kBwdPreReduce = 2, kBwdPreTokensGiven = 3;
 struct BwdPreWs {
   float *part, *tok, *pg, *wpart_r, *wpart_p, *wpart_a, *red_a, *pgsum;

@@ -31,8 +31,10 @@
 // Waves 4-7 do all waiting on records: a wave that waits on a load also waits
 // on every earlier load of its own, so the copy waves must not poll.  The
 // reducer jobs run on waves 4, 5, ...; a step ends when its slowest wave does,
-// so when wave 4 is the only reducer it neither polls nor publishes, and
-// neither does wave 0, which shares its SIMD.  The kernel is launched
+// so when wave 4 is the only reducer it neither polls nor publishes the
+// partials of A after S3 (it stores the active partials before S3, where it
+// would otherwise wait), and wave 0, which shares its SIMD, does not publish
+// either.  The kernel is launched
 // cooperatively, so every member of a team is resident; every wait is
 // bounded, so every wave exits.
 #include "xhc_device.h"
@@ -446,9 +448,7 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   // ---- pipeline steps: A of tile q (registers XA), B of tile q - 1, C of
   // tile q - 2 (registers XC); the registers rotate at the end of a step
   // active partials of tile qc (the C phase of a step, left in red2) summed
-  // over the waves into part2; runs in the next step, after its first barrier
-  // (not by the reducer waves: the compiler waits for every store a wave has
-  // in flight before its reducer job, so the job should find none)
+  // over the waves into part2; runs in the next step, after its first barrier.
   // The A partials are published (after S3) by the waves that are neither
   // reducers nor, when there are at most two reducers, their SIMD partners
   // (waves 0 .. nred - 1), so that the SIMDs running a reducer job carry less
