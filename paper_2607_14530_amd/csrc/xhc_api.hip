@@ -164,7 +164,7 @@ xhc_dims dims_rows32(const xhc_dims* d, int Kq) {
 }
 
 struct FlashPostBwdWs {
-  size_t post, pre, part, sums, idx_id, hres_id, hsel, xrest, da_out, xact32, f32c, df32, dhpost, dhres, dp,
+  size_t post, pre, part, sums, idx_id, hres_id, hsel, da_out, xact32, f32c, df32, dhpost, dhres, dp,
       saved, hpost_re, hres_re, w0, colsum0, wres0, bres0, alpha2, dwr, dwpre, dbpre, dwres, dbres, dalpha2, total;
 };
 
@@ -183,7 +183,6 @@ FlashPostBwdWs flash_post_bwd_ws(const xhc_dims* d, int Q, int q) {
   w.idx_id = c.take((size_t)T * k * sizeof(int32_t));
   w.hres_id = c.take((size_t)T * k * k * f);
   w.hsel = c.take((size_t)T * k * f);
-  w.xrest = c.take((size_t)T * kC * f);
   w.da_out = c.take((size_t)T * kC * f);
   w.xact32 = c.take((size_t)T * kC * f);
   w.f32c = c.take((size_t)T * C * f);
@@ -664,7 +663,7 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, Xact, F32(w.xact32), T * kC, s));
   XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, F, F32(w.f32c), T * C, s));
   // write-back reverse on the active rows: dF, dH^post, dp and the mixing transpose
-  XHC_STEP("fbwd_post", launch_bwd_post(&r, dA, F32(w.xrest), F32(w.xact32), F32(w.f32c), conv_w, idx_id, p,
+  XHC_STEP("fbwd_post", launch_bwd_post(&r, dA, nullptr, F32(w.xact32), F32(w.f32c), conv_w, idx_id, p,
                                         hres_use, Hpost, F32(w.da_out), F32(w.df32), F32(w.dhres), F32(w.dhpost),
                                         F32(w.dp), dconv_w, ws + w.post, s));
   XHC_STEP("fbwd_cvt", launch_fbwd_from_f32(d->state_dtype, F32(w.df32), dF, T * C, s));

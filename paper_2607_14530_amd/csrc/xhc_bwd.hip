@@ -444,9 +444,11 @@ __global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* __restrict__ dX
       }
     }
     Vec8<TS>::store(dX + (t * N + rows[l]) * (int64_t)C + c, g);
-    float a[8];
-    Vec8<TS>::load(Xact + (t * k + l) * (int64_t)C + c, a);
-    Vec8<TS>::store(X + (t * N + rows[l]) * (int64_t)C + c, a);
+    if (X) {   // restore the pre-update rows (left out when X is null)
+      float a[8];
+      Vec8<TS>::load(Xact + (t * k + l) * (int64_t)C + c, a);
+      Vec8<TS>::store(X + (t * N + rows[l]) * (int64_t)C + c, a);
+    }
   }
   const int kap[3] = {kap0, kap1, kap2};
   float e[KR][8];

@@ -120,6 +120,7 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
                            const float* conv_w, const int32_t* idx, const float* p, const float* Hres,
                            const float* Hpost, void* dX, void* dF, float* dHres, float* dHpost, float* dp,
                            float* dconv_w, char* ws, hipStream_t s);
+// (X null: the saved rows are not written back into X)
 size_t bwd_post_ws_bytes(const xhc_dims* d);
 bool bwd_pre_supported(const xhc_dims* d);
 size_t bwd_pre_ws_bytes(const xhc_dims* d);
