@@ -647,6 +647,9 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   const int64_t T = d->T, k = d->k, C = d->C, kC = k * C;
   const xhc_dims r = dims_rows32(d, Kq);
   float* dA = reinterpret_cast<float*>(da);
+  // a bf16 state: the reverse runs in place on da and the active-row pass adds
+  // the read of input_q (no separate pass)
+  const bool fold_read = d->state_dtype == XHC_BF16;
   int32_t* idx_id = reinterpret_cast<int32_t*>(ws + w.idx_id);
   float* hres_use = last ? const_cast<float*>(Hres) : F32(w.hres_id);
   hipError_t e = hipSuccess;
@@ -663,8 +666,11 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, Xact, F32(w.xact32), T * kC, s));
   XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, F, F32(w.f32c), T * C, s));
   // write-back reverse on the active rows: dF, dH^post, dp and the mixing transpose
+  // (in place for a bf16 state: each thread reads all k incoming rows of its
+  // chunk before it writes the outgoing ones)
+  float* const dA_out = fold_read ? dA : F32(w.da_out);
   XHC_STEP("fbwd_post", launch_bwd_post(&r, dA, nullptr, F32(w.xact32), F32(w.f32c), conv_w, idx_id, p,
-                                        hres_use, Hpost, F32(w.da_out), F32(w.df32), F32(w.dhres), F32(w.dhpost),
+                                        hres_use, Hpost, dA_out, F32(w.df32), F32(w.dhres), F32(w.dhpost),
                                         F32(w.dp), dconv_w, ws + w.post, s));
   XHC_STEP("fbwd_cvt", launch_fbwd_from_f32(d->state_dtype, F32(w.df32), dF, T * C, s));
   XHC_STEP("fbwd_dp", launch_fbwd_add(dp, F32(w.dp), T * k, s));
@@ -686,17 +692,21 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   XHC_STEP("fbwd_pre", launch_bwd_pre(&r, F32(w.xact32), F32(w.colsum0), F32(w.w0), F32(w.w0),
                                       last ? W_res : F32(w.wres0), W_post, F32(w.alpha2),
                                       last ? b_res : F32(w.bres0), F32(w.saved), idx_id, p, F32(w.hsel), Hpost,
-                                      nullptr, F32(w.dhres), F32(w.dhpost), F32(w.dp), F32(w.da_out),
+                                      nullptr, F32(w.dhres), F32(w.dhpost), F32(w.dp), dA_out,
                                       F32(w.dwr), F32(w.dwpre), last ? dW_res : F32(w.dwres), dW_post,
                                       F32(w.dalpha2), F32(w.dbpre), last ? db_res : F32(w.dbres), db_post,
                                       ws + w.pre, s, nullptr, nullptr, /*dense_rows=*/false,
-                                      d->state_dtype == XHC_BF16 ? Xact : nullptr));
+                                      d->state_dtype == XHC_BF16 ? Xact : nullptr, /*act_rows=*/true, kBwdPreAll,
+                                      fold_read && reads ? d_input : nullptr));
   XHC_STEP("fbwd_copy", hipMemcpyAsync(dalpha_post, F32(w.dalpha2) + 2, sizeof(float), hipMemcpyDeviceToDevice, s));
   if (last)
     XHC_STEP("fbwd_copy", hipMemcpyAsync(dalpha_res, F32(w.dalpha2) + 1, sizeof(float), hipMemcpyDeviceToDevice, s));
-  // da = (reverse so far) + H^pre,q_{I_j} d input_q (the active part of input_q's read)
-  XHC_STEP("fbwd_finish", launch_fbwd_finish(d->state_dtype, T, (int)k, (int)C, F32(w.da_out), F32(w.hsel),
-                                             reads ? d_input : nullptr, dA, s));
+  // da = (reverse so far) + H^pre,q_{I_j} d input_q (the active part of
+  // input_q's read): added by the active-row pass for a bf16 state, here
+  // otherwise
+  if (!fold_read)
+    XHC_STEP("fbwd_finish", launch_fbwd_finish(d->state_dtype, T, (int)k, (int)C, F32(w.da_out), F32(w.hsel),
+                                               reads ? d_input : nullptr, dA, s));
   return hip_status(e);
 }
 

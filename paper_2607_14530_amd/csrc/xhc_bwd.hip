@@ -1127,6 +1127,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
       st.row = ACT ? idx[t * k + part] : part;
       if (ACT) {
         st.scal[0] = tk[2 * N + NA + 7];   // beta_a
+        st.scal[1] = din ? Hpre[t * k + part] : 0.f;   // active rows: weight of the slot's read of din
       } else {
 #pragma unroll
         for (int i = 0; i < 6; ++i) st.scal[i] = tk[2 * N + NA + i];   // r, r_ln, mu, beta_pre, m1, m2
@@ -1156,7 +1157,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
         const int64_t t = tb + u;
         const int row = ACT ? idx[t * k + part] : part;
         st.dx[h] = Raw4<TD>::load(dX + (t * N + row) * (int64_t)C + c0 + kr);
-        if (!ACT) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
+        if (!ACT || din) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
       }
     }
   };
@@ -1200,9 +1201,10 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
         const float x[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
         float gsum[4];
         if (ACT) {
-          const float beta_a = sc[u][0];
+          const float beta_a = sc[u][0], hs = sc[u][1];
+          const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
 #pragma unroll
-          for (int v = 0; v < 4; ++v) gsum[v] = acc[v] - beta_a * x[v];
+          for (int v = 0; v < 4; ++v) gsum[v] = acc[v] - beta_a * x[v] + hs * gi[v];   // hs = 0 without din
         } else {
           const float r_ln = sc[u][1], mu = sc[u][2], bpre = sc[u][3], m1 = sc[u][4], m2 = sc[u][5], hp = sc[u][6];
           const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
@@ -1666,7 +1668,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           const float* dHpost, const float* dp, void* dX, float* dW_r, float* dW_pre, float* dW_res,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
                           hipStream_t s, const float* dhpre_act, const float* Hpre_read, bool dense_rows,
-                          const void* X_bf16, bool act_rows, int phase) {
+                          const void* X_bf16, bool act_rows, int phase, const void* act_din) {
   const float* Hrd = Hpre_read ? Hpre_read : Hpre;   // weights of the dense-read term
   const int64_t T = d->T;
   const int N = d->N, k = d->k, Kr = d->Kr, C = d->C;
@@ -1725,9 +1727,9 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
             N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
       const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
       if (act_rows)
-        k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
-            reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok,
-            T, N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
+        k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), nullptr,
+            reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
+            nullptr);   // (the dense read of the active rows is in the full-row pass)
       k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
     }
     // an fp32 state given with its exact bf16 copy: the active rows take the
@@ -1735,9 +1737,9 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % kMfRows == 0;
     if (mfa32 && act_rows) {
       const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
-      k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
-          reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
-          nullptr);
+      k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16),
+          reinterpret_cast<const uint16_t*>(act_din), reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok,
+          T, N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
     }
     const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
 #define XHC_FULL_ROWS(NNV)                                                                                       \

@@ -142,7 +142,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                           float* dW_post, float* dalpha, float* db_pre, float* db_res, float* db_post, char* ws,
                           hipStream_t s, const float* dhpre_act = nullptr, const float* Hpre_read = nullptr,
                           bool dense_rows = true, const void* X_bf16 = nullptr, bool act_rows = true,
-                          int phase = kBwdPreAll);
+                          int phase = kBwdPreAll, const void* act_din = nullptr);
 // dhpre_act [T,k]: when given, dL/dH^pre of the active streams (slot order)
 // replaces <d input, x_i> there; Hpre_read [T,N]: when given, the weights of
 // the dense-read term dX_i += H^pre_i d input (Hpre otherwise).  dense_rows
@@ -151,7 +151,9 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
 // and pre-map weights are zero; d_input is then not read, H^pre enters as
 // zero gradient, and dW_r, dW_pre are not written.  X_bf16: for an fp32
 // state whose values are exactly bf16, the same rows as bf16 (read by the
-// MFMA form of the active-row pass; the gradient rows stay fp32).  act_rows
+// MFMA form of the active-row pass; the gradient rows stay fp32), and then
+// act_din (bf16 [T, C]), when given: that pass also adds Hpre[t, j] act_din[t]
+// to active row j (Hpre then holds [T, k] slot weights).  act_rows
 // false leaves out the active-row pass (for a caller whose W_post and W_res
 // are zero): dW_post, dW_res are not written.
 // The full-row pass of Q pre-map reverses of one bf16 state (N = 16, Q = 2 or
