@@ -34,7 +34,8 @@ def _oracle(w, d, Q, tokens=None):
         [cpu(v) for v in d["W_post_list"]], d["W_res"].cpu(), [cpu(v) for v in d["conv_w_list"]],
         d["alpha_pre"], [cpu(v) for v in d["b_pre"]], d["alpha_post"], [cpu(v) for v in d["b_post"]],
         d["alpha_res"], d["b_res"].cpu(), m=w.m, k=w.k, S=w.S, kappa=w.kappa, tokens=tokens,
-        router=w.router, gram_schmidt_on=bool(w.gram_schmidt))
+        router=w.router, gram_schmidt_on=bool(w.gram_schmidt),
+        round_state=w.state != "f32")   # an fp32 state stores the written rows unrounded
 
 
 def _check(w, Q, d, g, states, tokens=None):
@@ -74,6 +75,7 @@ def _check(w, Q, d, g, states, tokens=None):
     W(T=50, N=8, k=4, m=1, C=128, Kr=3, kappa=(3, 6), name="flash-odd"),
     W(T=96, S=48, N=16, k=4, m=2, C=256, Kr=4, router="softmax", name="flash-softmax"),
     W(T=64, S=32, N=8, k=4, m=2, C=256, Kr=4, gram_schmidt=0, name="flash-gs-off"),
+    W(T=64, S=32, N=8, k=4, m=2, C=256, Kr=4, state="f32", name="flash-f32"),
 ], ids=lambda w: w.name)
 def test_flash_group_matches_oracle(w, Q):
     print(f"[flash] {w.name} Q={Q}", flush=True)

@@ -51,7 +51,8 @@ def _oracle(w, d):
                           cl(d["W_post_list"]), c(d["W_res"]), d["alpha_pre"], cl(d["b_pre"]), d["alpha_post"],
                           cl(d["b_post"]), d["alpha_res"], c(d["b_res"]))
     return O.flash_group_grads(vals, c(d["G_X"]), cl(d["G_in_list"]), m=w.m, k=w.k, S=w.S, kappa=w.kappa,
-                               router=w.router, gram_schmidt_on=bool(w.gram_schmidt))
+                               router=w.router, gram_schmidt_on=bool(w.gram_schmidt),
+                               round_state=w.state != "f32")   # an fp32 state stores the rows unrounded
 
 
 CASES = [
@@ -61,6 +62,10 @@ CASES = [
     (W(T=64, S=64, N=16, k=4, m=2, C=256, Kr=4, alpha=(0.5, 1.0, 0.5), name="fbwd-Q4-stress"), 4, 2.0),
     (W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, router="softmax", name="fbwd-Q2-softmax"), 2, 0.0),
     (W(T=48, S=24, N=4, k=4, m=2, C=256, Kr=4, name="fbwd-Q2-N4"), 2, 0.0),
+    # fp32 state: the separate read pass, the VALU active-row pass and the
+    # per-pre-map entry passes
+    (W(T=48, S=24, N=8, k=4, m=2, C=256, Kr=4, state="f32", name="fbwd-Q4-N8-f32"), 4, 0.0),
+    (W(T=40, S=20, N=16, k=4, m=2, C=256, Kr=4, state="f32", name="fbwd-Q2-N16-f32"), 2, 0.0),
 ]
 
 
