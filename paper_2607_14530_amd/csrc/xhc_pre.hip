@@ -181,7 +181,7 @@ __global__ __launch_bounds__(128) void k_pre_coef(const float* __restrict__ sums
 // launch.  A block takes 32 tokens; thread (part h, token u) sums chunk range
 // h of token u (8 ranges), the ranges are added in order through LDS, and one
 // thread per token forms the coefficients.
-constexpr int kCoefTok = 32, kCoefParts = 8;
+constexpr int kCoefTok = 64, kCoefParts = 4;   // tokens per workgroup, member-chunk parts per token
 template <int K>
 __global__ __launch_bounds__(kCoefTok * kCoefParts) void k_pre_coef_sum(
     const float* __restrict__ part, int64_t nchunk, int NO, int64_t T, int Kq, int with_res, int64_t kC,
