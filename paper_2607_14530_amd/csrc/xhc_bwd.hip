@@ -1053,8 +1053,10 @@ __device__ __forceinline__ void st4(float* p, const float (&d)[4]) {
 
 // TD: element type of the gradient rows dX (bf16, or fp32 for a state whose
 // values are bf16 but whose gradient is kept in fp32)
-template <bool ACT, typename TD = uint16_t>
-__global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restrict__ X,
+// ADIN (active rows): din is given and row j gains Hpre[t, j] din[t] (Hpre
+// then [T, k] slot weights)
+template <bool ACT, typename TD = uint16_t, int RW = kMfRows, bool ADIN = false>
+__global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __restrict__ X,
                                                        const uint16_t* __restrict__ din, TD* __restrict__ dX,
                                                        const float* __restrict__ Wa, const float* __restrict__ Wb,
                                                        const float* __restrict__ Hpre,
@@ -1062,13 +1064,14 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
                                                        int64_t T, int N, int k, int C, int Kr, int NA,
                                                        int64_t tchunk, float* __restrict__ wpa,
                                                        float* __restrict__ wpb) {
-  __shared__ __align__(16) uint16_t xs[kMfStep][kMfXPitch];
+  constexpr int NT = RW * 4, PIECES = RW / 8;   // threads; 16-byte pieces of a staged token row
+  __shared__ __align__(16) uint16_t xs[kMfStep][RW + 8];
   __shared__ float dzs[kMfStep][33];
   __shared__ float sc[kMfStep][8];
   __shared__ int srow[kMfStep];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int l16 = lane % 16, g4 = lane / 16;
-  const int64_t K0 = (int64_t)blockIdx.x * kMfRows;           // first weight row of the workgroup
+  const int64_t K0 = (int64_t)blockIdx.x * RW;                // first weight row of the workgroup
   const int part = (int)(K0 / C);                              // stream (full) or slot (active)
   const int c0 = (int)(K0 % C);
   const int64_t NK = ACT ? (int64_t)k * C : (int64_t)N * C;   // weight rows
@@ -1099,7 +1102,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
   // computed: this thread's dz' values (4), scalars (threads < 32) and 16
   // bytes of the state rows.
   struct Stage {
-    float dz[kMfStep * 32 / 256];
+    float dz[kMfStep * 32 / NT];
     float scal[7];
     int row;
     uint4 x;
@@ -1109,8 +1112,8 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
   auto fetch = [&](Stage& st, int64_t tb) {
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
 #pragma unroll
-    for (int r = 0; r < kMfStep * 32 / 256; ++r) {
-      const int q = threadIdx.x + r * 256, u = q / 32, o = q % 32;
+    for (int r = 0; r < kMfStep * 32 / NT; ++r) {
+      const int q = threadIdx.x + r * NT, u = q / 32, o = q % 32;
       const int64_t t = tb + (u < nt ? u : 0);
       const float* tk = tok + t * TF;
       float v = 0.f;
@@ -1127,7 +1130,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
       st.row = ACT ? idx[t * k + part] : part;
       if (ACT) {
         st.scal[0] = tk[2 * N + NA + 7];   // beta_a
-        st.scal[1] = din ? Hpre[t * k + part] : 0.f;   // active rows: weight of the slot's read of din
+        if (ADIN) st.scal[1] = Hpre[t * k + part];   // active rows: weight of the slot's read of din
       } else {
 #pragma unroll
         for (int i = 0; i < 6; ++i) st.scal[i] = tk[2 * N + NA + i];   // r, r_ln, mu, beta_pre, m1, m2
@@ -1137,7 +1140,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
     // the state rows need the row index: the slot's row of each token (active)
     // is read here directly
     {
-      const int u = threadIdx.x / 8, piece = threadIdx.x % 8;
+      const int u = threadIdx.x / PIECES, piece = threadIdx.x % PIECES;
       st.x = make_uint4(0, 0, 0, 0);
       if (u < nt) {
         const int64_t t = tb + u;
@@ -1157,7 +1160,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
         const int64_t t = tb + u;
         const int row = ACT ? idx[t * k + part] : part;
         st.dx[h] = Raw4<TD>::load(dX + (t * N + row) * (int64_t)C + c0 + kr);
-        if (!ACT || din) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
+        if (!ACT || ADIN) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
       }
     }
   };
@@ -1167,8 +1170,8 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
     __syncthreads();   // the previous step's LDS reads are done
 #pragma unroll
-    for (int r = 0; r < kMfStep * 32 / 256; ++r) {
-      const int q = threadIdx.x + r * 256;
+    for (int r = 0; r < kMfStep * 32 / NT; ++r) {
+      const int q = threadIdx.x + r * NT;
       dzs[q / 32][q % 32] = cur.dz[r];
     }
     if (threadIdx.x < kMfStep) {
@@ -1176,7 +1179,7 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
 #pragma unroll
       for (int i = 0; i < 7; ++i) sc[threadIdx.x][i] = cur.scal[i];
     }
-    *reinterpret_cast<uint4*>(&xs[threadIdx.x / 8][(threadIdx.x % 8) * 8]) = cur.x;
+    *reinterpret_cast<uint4*>(&xs[threadIdx.x / PIECES][(threadIdx.x % PIECES) * 8]) = cur.x;
     // ---- dX: two token halves; the accumulator rows were read a step ahead
     const typename Raw4<TD>::type dxr[2] = {cur.dx[0], cur.dx[1]};
     const uint2 dinv[2] = {cur.din[0], cur.din[1]};
@@ -1201,10 +1204,15 @@ __global__ __launch_bounds__(256) void k_bwd_rows_mfma(const uint16_t* __restric
         const float x[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
         float gsum[4];
         if (ACT) {
-          const float beta_a = sc[u][0], hs = sc[u][1];
-          const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
+          const float beta_a = sc[u][0];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) gsum[v] = acc[v] - beta_a * x[v] + hs * gi[v];   // hs = 0 without din
+          for (int v = 0; v < 4; ++v) gsum[v] = acc[v] - beta_a * x[v];
+          if (ADIN) {
+            const float hs = sc[u][1];
+            const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
+#pragma unroll
+            for (int v = 0; v < 4; ++v) gsum[v] += hs * gi[v];
+          }
         } else {
           const float r_ln = sc[u][1], mu = sc[u][2], bpre = sc[u][3], m1 = sc[u][4], m2 = sc[u][5], hp = sc[u][6];
           const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
@@ -1720,11 +1728,14 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     e = hipGetLastError();
     if (e != hipSuccess || phase == kBwdPreTokens || phase == kBwdPreTokensGiven) return e;
     if (mf) {
-      const dim3 gf((unsigned)((int64_t)N * C / kMfRows), (unsigned)nchunk);
-      if (dense_rows)
-        k_bwd_rows_mfma<false><<<gf, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
-            reinterpret_cast<const uint16_t*>(d_input), reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T,
-            N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
+      // 128 rows per workgroup (256 contiguous bytes of each state row per
+      // token); C % 256 == 0 is part of the backward's supported shapes
+      if (dense_rows) {
+        const dim3 gw((unsigned)((int64_t)N * C / (2 * kMfRows)), (unsigned)nchunk);
+        k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows><<<gw, dim3(8 * kMfRows), 0, s>>>(
+            reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
+            reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
+      }
       const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
       if (act_rows)
         k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), nullptr,
@@ -1737,9 +1748,15 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % kMfRows == 0;
     if (mfa32 && act_rows) {
       const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
-      k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16),
-          reinterpret_cast<const uint16_t*>(act_din), reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok,
-          T, N, k, C, Kr, NA, kRowChunk, wpart_a, nullptr);
+      if (act_din)
+        k_bwd_rows_mfma<true, float, kMfRows, true><<<ga, dim3(256), 0, s>>>(
+            reinterpret_cast<const uint16_t*>(X_bf16), reinterpret_cast<const uint16_t*>(act_din),
+            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
+            nullptr);
+      else
+        k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
+            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
+            nullptr);
     }
     const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
 #define XHC_FULL_ROWS(NNV)                                                                                       \
