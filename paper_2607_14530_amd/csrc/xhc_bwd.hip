@@ -1006,14 +1006,14 @@ constexpr int kMfRows = 64;    // weight rows per workgroup
 constexpr int kMfStep = 32;    // tokens per step
 constexpr int kMfXPitch = kMfRows + 8;   // bf16 per staged token row (pad: fewer LDS bank conflicts)
 
+// f = hi + lo with hi the round-to-nearest-even bf16 of f and lo that of the
+// rest (the packed hardware conversion: the bits of f2bf for finite values)
 __device__ __forceinline__ void split_bf16x8(const float (&f)[8], uint4& hi, uint4& lo) {
+  hi = pack8(f);
   float h[8], l[8];
+  unpack8(hi, h);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    h[e] = __uint_as_float(f2bf(f[e]) << 16);
-    l[e] = f[e] - h[e];
-  }
-  hi = pack8(h);
+  for (int e = 0; e < 8; ++e) l[e] = f[e] - h[e];
   lo = pack8(l);
 }
 
