@@ -1736,25 +1736,27 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
             reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
             reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
       }
-      const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
+      // 128 rows per workgroup as for the full rows (C % 256 == 0)
+      const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
       if (act_rows)
-        k_bwd_rows_mfma<true><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), nullptr,
+        k_bwd_rows_mfma<true, uint16_t, 2 * kMfRows><<<ga, dim3(8 * kMfRows), 0, s>>>(reinterpret_cast<const uint16_t*>(X), nullptr,
             reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
             nullptr);   // (the dense read of the active rows is in the full-row pass)
       k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
     }
     // an fp32 state given with its exact bf16 copy: the active rows take the
     // MFMA pass with fp32 gradient rows
-    const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % kMfRows == 0;
+    const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % (2 * kMfRows) == 0;
     if (mfa32 && act_rows) {
-      const dim3 ga((unsigned)((int64_t)k * C / kMfRows), (unsigned)nchunk);
+      const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
       if (act_din)
-        k_bwd_rows_mfma<true, float, kMfRows, true><<<ga, dim3(256), 0, s>>>(
+        k_bwd_rows_mfma<true, float, 2 * kMfRows, true><<<ga, dim3(8 * kMfRows), 0, s>>>(
             reinterpret_cast<const uint16_t*>(X_bf16), reinterpret_cast<const uint16_t*>(act_din),
             reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
             nullptr);
       else
-        k_bwd_rows_mfma<true, float><<<ga, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
+        k_bwd_rows_mfma<true, float, 2 * kMfRows><<<ga, dim3(8 * kMfRows), 0, s>>>(
+            reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
             reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
             nullptr);
     }
