@@ -182,14 +182,18 @@ def temporal_branches(F: torch.Tensor, conv_w: torch.Tensor, kappa, S: int,
 
 
 def gram_schmidt(components: list) -> list:
-    """Orthogonalise [out, g_1, ..., g_r] per token over C (eq:gs)."""
+    """Orthogonalise [out, g_1, ..., g_r] per token over C (eq:gs).
+
+    A coefficient is 0 only where <v_i, v_i> is exactly 0 (the printed
+    quotient is undefined there); a NaN norm gives a NaN coefficient, as the
+    printed quotient does."""
     v = [components[0]]
     for g in components[1:]:
         u = g
         for vi in v:
             nn = (vi * vi).sum(-1, keepdim=True)
             dot = (g * vi).sum(-1, keepdim=True)
-            coef = torch.where(nn > 0, dot / torch.where(nn > 0, nn, 1.0), 0.0)
+            coef = torch.where(nn != 0, dot / torch.where(nn != 0, nn, 1.0), 0.0)
             u = u - coef * vi
         v.append(u)
     return v

@@ -317,6 +317,97 @@ def test_post_attention_closed_form():
             assert torch.allclose(Xn[t, i], ref, atol=1e-14, rtol=0)
 
 
+def _library_components(F, conv_w, kappa, S):
+    """[out, g_1, .., g_r] of every token from torch conv1d (causal, per
+    sequence, groups = C): an implementation of eq:aug other than the oracle's."""
+    F = F.to(F64)
+    T, C = F.shape
+    comps = [F.clone()]
+    row = 0
+    for kap in kappa:
+        ker = conv_w[row:row + kap].to(F64).flip(0).t().unsqueeze(1)        # [C, 1, kap]
+        g = torch.empty(T, C, dtype=F64)
+        for b in range(T // S):
+            seq = F[b * S:(b + 1) * S].t().unsqueeze(0)
+            g[b * S:(b + 1) * S] = torch.nn.functional.conv1d(
+                torch.nn.functional.pad(seq, (kap - 1, 0)), ker, groups=C)[0].t()
+        comps.append(g)
+        row += kap
+    return comps
+
+
+def _qr_components(comps):
+    """v_i = q_i r_ii from numpy's QR of [out, g_1, .., g_r] per token (eq:gs)."""
+    T = comps[0].shape[0]
+    v = [torch.empty_like(comps[0]) for _ in comps]
+    for t in range(T):
+        q, r = np.linalg.qr(np.stack([c[t].numpy() for c in comps], axis=1))
+        for i in range(len(comps)):
+            v[i][t] = torch.from_numpy(q[:, i] * r[i, i])
+    return v
+
+
+@pytest.mark.parametrize("cols", [(0, 0, 0, 0), (1, 1, 1, 1), (2, 2, 2, 2), (3, 3, 3, 3),
+                                  (0, 1, 2, 3), (3, 2, 1, 0), (1, 3, 0, 2)])
+def test_post_mlp_one_hot_columns_pick_the_gram_schmidt_components(cols):
+    """K_r = 4, H^res = I, H^post[t, j] = e_{cols[j]}: the write-back of slot j
+    is x_{I_j} + p_j v_{cols[j]} (eq:sparse_write), with the components from
+    torch conv1d (eq:aug) orthogonalised by numpy QR (eq:gs).  Fails if the
+    post drops Gram-Schmidt, permutes the H^post columns or the components."""
+    w, d = _inputs(T=20, N=8, k=4, m=2, C=32, Kr=4, S=10, seed=3)
+    r = _pre(w, d)
+    X = d["X"].to(F64)
+    T, k = 20, 4
+    p = 0.25 + 0.5 * torch.rand(T, k, generator=torch.Generator().manual_seed(1), dtype=F64)
+    Hpost = torch.zeros(T, k, 4, dtype=F64)
+    for j, c in enumerate(cols):
+        Hpost[:, j, c] = 1.0
+    eye = torch.eye(k, dtype=F64).expand(T, k, k)
+    Xn = O.xhc_post(X, d["F"], d["conv_w"], r["idx"], p, eye, Hpost, S=w.S, kappa=w.kappa)
+    v = _qr_components(_library_components(d["F"], d["conv_w"], w.kappa, w.S))
+    for t in range(T):
+        for j in range(k):
+            i = r["idx"][t, j]
+            ref = X[t, i] + p[t, j] * v[cols[j]][t]
+            assert torch.allclose(Xn[t, i], ref, atol=1e-10, rtol=0), (t, j)
+
+
+def test_post_mlp_applies_gram_schmidt_to_a_collinear_branch():
+    """A branch with one tap of 2 on every channel is g_1 = 2 out, so its
+    Gram-Schmidt component vanishes (eq:gs) and H^post = e_1 leaves the rows
+    as they were; without Gram-Schmidt they would move by 2 p out."""
+    w, d = _inputs(T=12, N=6, k=4, m=2, C=16, Kr=4, S=12, seed=5)
+    r = _pre(w, d)
+    X = d["X"].to(F64)
+    conv = d["conv_w"].clone()
+    conv[:w.kappa[0]] = 0.0
+    conv[0] = 2.0
+    T, k = 12, 4
+    p = torch.full((T, k), 0.5, dtype=F64)
+    Hpost = torch.zeros(T, k, 4, dtype=F64)
+    Hpost[:, :, 1] = 1.0
+    eye = torch.eye(k, dtype=F64).expand(T, k, k)
+    Xn = O.xhc_post(X, d["F"], conv, r["idx"], p, eye, Hpost, S=w.S, kappa=w.kappa)
+    act = O.gather_rows(X, r["idx"])
+    assert torch.allclose(O.gather_rows(Xn, r["idx"]), act, atol=1e-12, rtol=0)
+    no_gs = O.xhc_post(X, d["F"], conv, r["idx"], p, eye, Hpost, S=w.S, kappa=w.kappa, gram_schmidt_on=False)
+    moved = O.gather_rows(no_gs, r["idx"]) - act
+    assert torch.allclose(moved, (2 * 0.5 * d["F"].to(F64))[:, None, :].expand_as(moved), atol=1e-12, rtol=0)
+
+
+def test_gram_schmidt_nan_propagates_like_the_printed_quotient():
+    """A NaN in out makes every later coefficient <g, v_1> / <v_1, v_1> NaN,
+    so all later components are NaN on every channel; other tokens are not
+    touched."""
+    g = torch.Generator().manual_seed(8)
+    comps = [torch.randn(3, 16, generator=g, dtype=F64) for _ in range(4)]
+    comps[0][1, 5] = float("nan")
+    v = O.gram_schmidt(comps)
+    for i in (1, 2, 3):
+        assert torch.isnan(v[i][1]).all()
+        assert torch.isfinite(v[i][0]).all() and torch.isfinite(v[i][2]).all()
+
+
 # --------------------------------------------------------------- xHC-Flash
 
 def _flash(Q, round_state, seed=1, T=24, N=8, k=4, m=2, C=32, S=12):
