@@ -142,11 +142,22 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
                    void* input, int32_t* idx, float* p, float* Hpre, float* Hres, float* Hpost,
                    float* saved, void* workspace, size_t workspace_bytes, void* stream);
 
+/* xhc_pre_failures - waits until the work enqueued on `stream` so far has
+ * finished, then sets *failures to the number of bounded waits that gave up
+ * in the last xhc_pre call that used `workspace` (that call's own workspace
+ * pointer).  The single-pass kernel's members exchange partial sums through
+ * device memory and every wait on another member is bounded; a wait that
+ * gives up leaves NaN in H^post and H^res, and this count says that it
+ * happened.  The multi-kernel path has no such waits and reports 0.
+ * Errors: XHC_EINVAL (NULL pointer), XHC_EUNSUPPORTED (workspace not 16-byte
+ * aligned), XHC_EHIP (the copy or the synchronisation failed).            */
+xhc_status xhc_pre_failures(const void* workspace, int32_t* failures, void* stream);
+
 /* Floats per token that xhc_pre writes to `saved` when it is non-NULL (for
  * xhc_pre_bwd): [z_r (N) | z_pre (N) | z_post, z_res (k*Kr + k*k) | mu | nu |
  * nu_a | pad], z = the normalised logits before gating, mu / nu = mean and
  * mean square of the flattened state, nu_a = mean square of the active rows.
- * Saving takes the multi-kernel path.                                      */
+ * Both xhc_pre implementations write it.                                   */
 size_t xhc_saved_floats(const xhc_dims* d);
 
 /* xhc_post - sparse write-back of one xHC sublayer (eq:aug, eq:gs,
@@ -180,7 +191,10 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
  *   Xact    [T,k,C] the active rows before the update (xhc_post's Xact_save)
  *   F, conv_w, idx, p, Hres, Hpost as in xhc_post
  * Outputs: dX [T,N,C] = dXn on untouched rows and sum_j Hres[t,j,l] dXn[t,I_j]
- * on active row I_l (xhc_pre_bwd adds the rest); dF [T,C]; dHres [T,k,k];
+ * on active row I_l (xhc_pre_bwd adds the rest).  dX may be dXn itself (in
+ * place, the sparse form of eq:sparse_write): then only the k active rows of
+ * each token are written and the untouched rows are not moved at all.
+ * dF [T,C]; dHres [T,k,k];
  * dHpost [T,k,Kr]; dp [T,k]; dconv_w [sum kappa, C] (NULL iff Kr == 1).
  *
  * xhc_pre_bwd (N in {4, 8, 16, 32}, C % 256 == 0, k*Kr + k*k <= 32)

@@ -70,11 +70,15 @@ size_t part_bytes(const xhc_dims* d, bool gather, int64_t K, int64_t nout) {
 // partials of the larger projection, then the per-token sums of either one
 size_t sums_bytes(int64_t nout, int64_t T) { return align_up((size_t)(out_blocks(nout) * 16 + 2) * T * sizeof(float)); }
 
+// The first kPreErrBytes of an xhc_pre workspace hold the count of bounded
+// waits that gave up (xhc_pre_failures); both paths clear it.
+constexpr size_t kPreErrBytes = 256;
+
 size_t pre_ws_multi(const xhc_dims* d) {
   const size_t full = part_bytes(d, false, NC_of(d), 2 * d->N);
   const size_t act = part_bytes(d, true, kC_of(d), act_outs(d, d->Kr, 1));
   const size_t sf = sums_bytes(2 * d->N, d->T), sa = sums_bytes(act_outs(d, d->Kr, 1), d->T);
-  return (full > act ? full : act) + (sf > sa ? sf : sa);
+  return kPreErrBytes + (full > act ? full : act) + (sf > sa ? sf : sa);
 }
 
 // The single-pass path may fall back to the multi-kernel path at run time
@@ -259,6 +263,41 @@ size_t post_ws(const xhc_dims* d) {
          align_up((size_t)d->T * d->k * d->Kr * sizeof(float));
 }
 
+// xhc_post's work on a given scratch buffer
+xhc_status post_impl(const xhc_dims* d, void* X, const void* F, const float* conv_w, const int32_t* idx,
+                     const float* p, const float* Hres, const float* Hpost, void* Xact_save, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (d->T == 0) return XHC_OK;
+  if (!X || !F || !idx || !p || !Hres || !Hpost) return XHC_EINVAL;
+  if ((d->Kr > 1) != (conv_w != nullptr)) return XHC_EINVAL;
+  if (X == F) return XHC_EINVAL;
+  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w)) || (Xact_save && !aligned16(Xact_save)))
+    return XHC_EUNSUPPORTED;
+  const size_t need = post_ws(d);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return XHC_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  float* wb = nullptr;
+  hipError_t e = hipSuccess;
+  if (d->Kr > 1) {
+    const int np = d->Kr * (d->Kr + 1) / 2;
+    float* gpart = reinterpret_cast<float*>(workspace);
+    wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
+                                  align_up((size_t)gram_chunks(d->C, d->S, d->Kr, d->kappa) * np * (size_t)d->T *
+                                           sizeof(float)));
+    XHC_STEP("post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, d->Kr, d->kappa, conv_w, gpart, s));
+    XHC_STEP("post_coef", launch_post_coef(gpart, gram_chunks(d->C, d->S, d->Kr, d->kappa), d->T, d->k, d->Kr,
+                                           d->gram_schmidt, p, Hpost, wb, s));
+  }
+  XHC_STEP("post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa,
+                                           conv_w, idx, p, Hres, Hpost, wb, nullptr, nullptr, nullptr, Xact_save,
+                                           s));
+  return hip_status(e);
+}
+
+
 }  // namespace
 
 extern "C" {
@@ -377,10 +416,10 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   clear_stale_error();
-  float* part = reinterpret_cast<float*>(workspace);
+  float* part = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + kPreErrBytes);
   const size_t part_max = std::max(part_bytes(d, false, NC_of(d), 2 * d->N),
                                    part_bytes(d, true, kC_of(d), act_outs(d, d->Kr, 1)));
-  float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_max);
+  float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(part) + part_max);
   const int64_t NC = NC_of(d), kC = kC_of(d);
   const int64_t nout_full = 2 * d->N, nout_act = act_outs(d, d->Kr, 1);
   const int nsave = saved_floats(d->N, d->k, d->Kr);
@@ -398,6 +437,7 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
     e = hipSuccess;   // the device cannot hold the single-pass grid: multi-kernel path
     clear_stale_error();
   }
+  XHC_STEP("pre_clear", launch_fill0(workspace, kPreErrBytes, s));   // no waits here: no failures
   XHC_STEP("proj_full", launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nout_full,
                                             nullptr, d->k, part, s));
   XHC_STEP("pre_route", launch_pre_route(part, proj_chunks(d->state_dtype, false, NC, d->C, nout_full, d->T), nout_full, d->T, d->N, d->m, d->k, 1, d->C, colsum,
@@ -414,37 +454,26 @@ xhc_status xhc_pre(const xhc_dims* d, const void* X, const void* packed_full, co
   return hip_status(e);
 }
 
+xhc_status xhc_pre_failures(const void* workspace, int32_t* failures, void* stream) {
+  if (!workspace || !failures) return XHC_EINVAL;
+  if (!aligned16(workspace)) return XHC_EUNSUPPORTED;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  clear_stale_error();
+  int32_t n = 0;
+  hipError_t e = hipMemcpyAsync(&n, workspace, sizeof(n), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    g_failed_step = "pre_failures";
+    return hip_status(e);
+  }
+  *failures = n;
+  return XHC_OK;
+}
+
 xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv_w, const int32_t* idx,
                     const float* p, const float* Hres, const float* Hpost, void* Xact_save, void* workspace,
                     size_t workspace_bytes, void* stream) {
-  xhc_status st = check_dims(d);
-  if (st != XHC_OK) return st;
-  if (d->T == 0) return XHC_OK;
-  if (!X || !F || !idx || !p || !Hres || !Hpost) return XHC_EINVAL;
-  if ((d->Kr > 1) != (conv_w != nullptr)) return XHC_EINVAL;
-  if (X == F) return XHC_EINVAL;
-  if (!aligned16(X) || !aligned16(F) || (conv_w && !aligned16(conv_w)) || (Xact_save && !aligned16(Xact_save)))
-    return XHC_EUNSUPPORTED;
-  const size_t need = post_ws(d);
-  if (need > 0 && (!workspace || workspace_bytes < need)) return XHC_EWORKSPACE;
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  clear_stale_error();
-  float* wb = nullptr;
-  hipError_t e = hipSuccess;
-  if (d->Kr > 1) {
-    const int np = d->Kr * (d->Kr + 1) / 2;
-    float* gpart = reinterpret_cast<float*>(workspace);
-    wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
-                                  align_up((size_t)gram_chunks(d->C, d->S, d->Kr, d->kappa) * np * (size_t)d->T *
-                                           sizeof(float)));
-    XHC_STEP("post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, d->Kr, d->kappa, conv_w, gpart, s));
-    XHC_STEP("post_coef", launch_post_coef(gpart, gram_chunks(d->C, d->S, d->Kr, d->kappa), d->T, d->k, d->Kr,
-                                           d->gram_schmidt, p, Hpost, wb, s));
-  }
-  XHC_STEP("post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa,
-                                           conv_w, idx, p, Hres, Hpost, wb, nullptr, nullptr, nullptr, Xact_save,
-                                           s));
-  return hip_status(e);
+  return post_impl(d, X, F, conv_w, idx, p, Hres, Hpost, Xact_save, workspace, workspace_bytes, stream);
 }
 
 // ---------------------------------------------------------------- xHC-Flash
@@ -564,7 +593,7 @@ xhc_status xhc_post_bwd(const xhc_dims* d, const void* dXn, void* X, const void*
       !workspace)
     return XHC_EINVAL;
   if ((d->Kr > 1) != (conv_w != nullptr) || (d->Kr > 1) != (dconv_w != nullptr)) return XHC_EINVAL;
-  if (dX == dXn || dX == X || dF == F) return XHC_EINVAL;
+  if (dX == X || dF == F) return XHC_EINVAL;   // dX == dXn: in place
   if (!aligned16(dXn) || !aligned16(X) || !aligned16(Xact) || !aligned16(F) || !aligned16(dX) || !aligned16(dF) ||
       (conv_w && !aligned16(conv_w)) || (dconv_w && !aligned16(dconv_w)))
     return XHC_EUNSUPPORTED;

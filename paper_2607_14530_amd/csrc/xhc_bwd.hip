@@ -49,7 +49,7 @@ __device__ inline void gram_schmidt_basis_reverse(const double (&G)[kMaxKr][kMax
     for (int a = 0; a < kMaxKr; ++a)
       for (int b = 0; b < kMaxKr; ++b) n += V[j][a] * G[a][b] * V[j][b];
     nrm[j] = n;
-    zero[j] = !(n > 1e-6 * G[j][j]);
+    zero[j] = n <= 1e-6 * G[j][j];   // a NaN norm is not "vanishing": it propagates
   }
   double dV[kMaxKr][kMaxKr], dnrm[kMaxKr];
   for (int i = 0; i < kMaxKr; ++i) {
@@ -397,14 +397,17 @@ __global__ __launch_bounds__(128) void k_bwd_post_token(const float* __restrict_
 }
 
 // Element pass of the post backward (8 channels of one token per thread).
+// dX may be dXn itself (in place): a thread reads the k active rows of its
+// chunk before it writes any, and the untouched rows then already hold their
+// gradient, so they are not copied.
 template <typename TS, int KR, int KM>
-__global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* __restrict__ dXn, TS* __restrict__ X,
+__global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* dXn, TS* __restrict__ X,
                                                        const TS* __restrict__ Xact, const TS* __restrict__ F,
                                                        int64_t T, int64_t S, int N, int C, int k, int kap0, int kap1,
                                                        int kap2, const float* __restrict__ conv_w,
                                                        const int32_t* __restrict__ idx,
                                                        const float* __restrict__ Hres,
-                                                       const float* __restrict__ coef, TS* __restrict__ dX,
+                                                       const float* __restrict__ coef, TS* dX,
                                                        TS* __restrict__ dF, float* __restrict__ de) {
   const int64_t ncb = post_chunks(C);
   const int64_t t = blockIdx.x / ncb;
@@ -416,8 +419,8 @@ __global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* __restrict__ dX
     rows[j] = idx[t * k + j];
     act |= 1ull << rows[j];
   }
-  // untouched rows pass their gradient through
-  for (int i = 0; i < N; ++i) {
+  // untouched rows pass their gradient through (nothing to do in place)
+  for (int i = 0; i < N && dX != dXn; ++i) {
     if ((act >> i) & 1ull) continue;
     float g[8];
     Vec8<TS>::load(dXn + (t * N + i) * (int64_t)C + c, g);
@@ -697,7 +700,7 @@ __global__ __launch_bounds__(kPreTokThreads) void k_bwd_pre_token(
   float* g = pg + t * pg_floats(N, k, Kr);
   const float mu = sv[ns - 4], nu = sv[ns - 3], nu_a = sv[ns - 2];
   const float NC = (float)N * (float)C, kC = (float)k * (float)C;
-  const float r = 1.0f / sqrtf(nu + eps), r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + eps);
+  const float r = 1.0f / sqrtf(nu + eps), r_ln = 1.0f / sqrtf(ln_variance(mu, nu) + eps);
   const float r_a = 1.0f / sqrtf(nu_a + eps);
   const float a_pre = alpha[0], a_res = alpha[1], a_post = alpha[2];
   // pre-map: H = sigma(a z + b)

@@ -149,34 +149,84 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 __device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + __expf(-z)); }
 
-// Fixed-plus-TopK routing of one token (eq:router_topk).  Slots 0..m-1 take
-// streams 0..m-1 with p = 1; slot j >= m takes the largest remaining logit
-// among streams m..N-1, ties to the lower index.  A NaN logit never wins a
-// comparison; a slot whose candidates all compare false takes the lowest free
-// stream, so every index stays in range.  p of a routed slot is sigma(z)
-// (eq:router) or, with `softmax`, exp(z - max) / sum over the N streams of
-// exp(z - max) (the softmax-router ablation).
-template <int NMAX>
-__device__ __forceinline__ void route_token(const float (&z)[NMAX], int N, int m, int k,
-                                            int32_t* idx_out, float* p_out, bool softmax = false) {
-  uint64_t used = 0;
-  for (int j = 0; j < m; ++j) {
-    idx_out[j] = j;
-    p_out[j] = 1.0f;
+// Biased variance nu - mu^2 of the LayerNorm (eq:router), with a negative
+// rounding residue taken as 0.  A NaN (an infinite or NaN state gives
+// Inf - Inf) stays NaN, so the logits become NaN as the plain definition
+// makes them (fmaxf would turn it into 0).
+__device__ __forceinline__ float ln_variance(float mu, float nu) {
+  const float v = nu - mu * mu;
+  return v < 0.f ? 0.f : v;
+}
+
+// Order of router logits used by TopK, as a signed integer key: key order is
+// the order of the floats (-0 and +0 tie), with NaN below every number (so a
+// NaN never displaces a number; NaNs tie with each other).  Together with
+// "ties to the lower index" this is a total order on (logit, stream), so every
+// routed slot gets exactly one distinct stream whatever the logits hold.
+// Host-callable so that the order can be checked on the CPU.
+__host__ __device__ __forceinline__ int32_t logit_key(float z) {
+  if (z != z) return INT32_MIN;
+  uint32_t u;
+  __builtin_memcpy(&u, &z, 4);
+  if ((u & 0x7fffffffu) == 0) u = 0;   // -0 ties with +0
+  return (u & 0x80000000u) ? (int32_t)(u ^ 0x7fffffffu) : (int32_t)u;
+}
+
+// Rank of stream `lane` among the routing candidates m..15 of one token: the
+// number of candidates i whose (key, index) comes before (key, lane), key =
+// logit_key.  keyat(i) gives the key of stream i (in the single-pass kernel a
+// read of lane i).  The ranks of the 16 - m candidates are 0 .. 15 - m, each
+// once; slot m + rank takes the stream when rank < k - m.
+template <class LaneKey>
+__host__ __device__ __forceinline__ int route_rank16(LaneKey keyat, int32_t key, int lane, int m) {
+  int rank = 0;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    const int32_t ki = keyat(i);
+    // branch-free: the candidate test is uniform, the comparison a select;
+    // i == lane never counts
+    const int before = (int)(ki > key) | ((int)(ki == key) & (int)(i < lane));
+    rank += before & -(int)(i >= m);
   }
+  return rank;
+}
+
+// Fixed-plus-TopK selection of one token (eq:router_topk): slots 0..m-1 take
+// streams 0..m-1; slot j >= m takes the first remaining stream among m..N-1
+// in the order of logit_key, ties to the lower index.  Writes the k stream
+// indices and returns their logits in zsel (slots >= m).
+template <int NMAX>
+__host__ __device__ __forceinline__ void route_select(const float (&z)[NMAX], int N, int m, int k, int32_t* idx_out,
+                                                      float* zsel) {
+  uint64_t used = 0;
+  for (int j = 0; j < m; ++j) idx_out[j] = j;
   for (int j = m; j < k; ++j) {
     int best = -1;
-    float bz = 0.0f;
+    int32_t bk = 0;
 #pragma unroll
     for (int i = 0; i < NMAX; ++i) {
       if (i >= m && i < N && !((used >> i) & 1ull)) {
-        if (best < 0 || z[i] > bz) { best = i; bz = z[i]; }
+        const int32_t ki = logit_key(z[i]);
+        if (best < 0 || ki > bk) { best = i; bk = ki; }
       }
     }
     used |= 1ull << best;
     idx_out[j] = best;
-    p_out[j] = softmax ? bz : sigmoidf(bz);   // softmax: the logit until the sum is known
+    zsel[j] = z[best];
   }
+}
+
+// Fixed-plus-TopK routing of one token: route_select, then p = 1 for fixed
+// slots and, for a routed slot, sigma(z) (eq:router) or, with `softmax`,
+// exp(z - max) / sum over the N streams of exp(z - max) (the softmax-router
+// ablation); a NaN logit gives a NaN p.
+template <int NMAX>
+__device__ __forceinline__ void route_token(const float (&z)[NMAX], int N, int m, int k,
+                                            int32_t* idx_out, float* p_out, bool softmax = false) {
+  float zsel[kMaxK];
+  route_select<NMAX>(z, N, m, k, idx_out, zsel);
+  for (int j = 0; j < m; ++j) p_out[j] = 1.0f;
+  for (int j = m; j < k; ++j) p_out[j] = softmax ? zsel[j] : sigmoidf(zsel[j]);   // softmax: the logit until the sum is known
   if (softmax && k > m) {
     float mx = z[0];
 #pragma unroll
@@ -323,7 +373,7 @@ __device__ __forceinline__ void gram_schmidt_basis(const double (&G)[kMaxKr][kMa
 #pragma unroll
       for (int b = 0; b < kMaxKr; ++b) n += V[j][a] * G[a][b] * V[j][b];
     nrm[j] = n;
-    zero[j] = !(n > 1e-6 * G[j][j]);
+    zero[j] = n <= 1e-6 * G[j][j];   // a NaN norm is not "vanishing": it propagates
   }
 }
 

@@ -109,7 +109,7 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
     saved[t * nsave + save_stats_at] = mu;
     saved[t * nsave + save_stats_at + 1] = nu;
   }
-  const float r_ln = 1.0f / sqrtf(fmaxf(nu - mu * mu, 0.f) + eps);
+  const float r_ln = 1.0f / sqrtf(ln_variance(mu, nu) + eps);
   const float r_rms = 1.0f / sqrtf(nu + eps);
   float z[kMaxN];
 #pragma unroll

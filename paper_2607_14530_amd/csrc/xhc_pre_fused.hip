@@ -178,7 +178,7 @@ __device__ __forceinline__ float from_lane_xor32f(float v, int lane) {
 // LDS access of the wave wait for it (it cannot tell that they touch other
 // LDS).  The wave waits for it explicitly (vmcnt) before the buffer is read.
 __device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_addr) : "memory");
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_addr) : "memory", "m0");
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -357,17 +357,12 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
     uint64_t* r2 = rec2t + (qt % RING) * FM * NV2 + t * NV2;
     if (h == 0) {
       const float mu = lane_value(mo, 0) * inv_nc, nu = lane_value(mo, G) * inv_nc;
-      const float r_ln = __builtin_amdgcn_rsqf(fmaxf(nu - mu * mu, 0.f) + a.eps);
+      const float r_ln = __builtin_amdgcn_rsqf(ln_variance(mu, nu) + a.eps);
       const float z = (v - mu * cs_l) * r_ln;   // lanes 0..15: LayerNorm-corrected router logit
-      // rank among the candidates i >= m (larger logit first, ties to the lower index)
-      // (branch-free: the candidate test is uniform, the comparison a select)
-      int rank = 0;
-#pragma unroll
-      for (int i = 0; i < FN; ++i) {
-        const float zi = lane_value(z, i);
-        const int before = (int)(zi > z) | ((int)(zi == z) & (int)(i < lane));   // i == lane never counts
-        rank += before & -(int)(i >= a.m);
-      }
+      // rank among the candidates i >= m (total order of logit_key, ties to
+      // the lower index; the same order as the multi-kernel route_token)
+      const int32_t key = logit_key(z);
+      const int rank = route_rank16([&](int i) { return __builtin_amdgcn_readlane(key, i); }, key, lane, a.m);
       int slot = -1;
       float pv = 1.0f;
       float sc = sigmoidf(z);

@@ -90,6 +90,7 @@ _SIGS = {
     "xhc_pre_bwd": (ctypes.c_int, [_D] + [_P] * 27 + [ctypes.c_size_t, _P]),
     "xhc_stream_sum": (ctypes.c_int, [_D, _P, _P, _P]),
     "xhc_stream_sum_bwd": (ctypes.c_int, [_D, _P, _P, ctypes.c_int32, _P]),
+    "xhc_pre_failures": (ctypes.c_int, [_P, _P, _P]),
     "xhc_status_string": (ctypes.c_char_p, [ctypes.c_int32]),
     "xhc_last_hip_error": (ctypes.c_char_p, []),
 }
@@ -179,6 +180,14 @@ def xhc_pre(d, X, packed_full, packed_act, alpha, b_pre, b_res, b_post, input, i
     _call("xhc_pre", ctypes.byref(d), _ptr(X), _ptr(packed_full), _ptr(packed_act), _ptr(alpha), _ptr(b_pre),
           _ptr(b_res), _ptr(b_post), _ptr(input), _ptr(idx), _ptr(p), _ptr(Hpre), _ptr(Hres), _ptr(Hpost),
           _ptr(saved), _ptr(workspace), workspace.numel() if workspace is not None else 0, _stream(stream))
+
+
+def xhc_pre_failures(workspace, stream=None):
+    """Waits for `stream`, then returns the number of bounded waits that gave
+    up in the last xhc_pre call that used `workspace` (0 = none)."""
+    n = ctypes.c_int32(0)
+    _call("xhc_pre_failures", _ptr(workspace), ctypes.cast(ctypes.byref(n), ctypes.c_void_p), _stream(stream))
+    return n.value
 
 
 def xhc_post(d, X, F, conv_w, idx, p, Hres, Hpost, Xact_save, workspace, stream=None):
@@ -292,6 +301,10 @@ class Sublayer:
         xhc_post(self.d, X, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, Xact_save, self.ws_post,
                  stream)
         return X
+
+    def pre_failures(self, stream=None):
+        """Bounded waits that gave up in the last pre() (waits for the stream)."""
+        return xhc_pre_failures(self.ws_pre, stream)
 
 
 def flash_Kq(d, q):

@@ -8,7 +8,7 @@ import torch
 from oracle import xhc_oracle as O
 from paper_2607_14530_amd import synth
 from paper_2607_14530_amd import xhc as X
-from tests.parity_util import assert_bf16_close
+from tests.parity_util import NEAR_TIE, assert_bf16_close
 from tests.test_gpu_bwd import assert_grad_close
 
 pytestmark = pytest.mark.gpu
@@ -16,20 +16,30 @@ F64 = torch.float64
 W = synth.Workload
 
 
-def assert_state_grad_close(got, ref, rounds, scale, what):
+FROB_STATE = 1e-2   # achieved about 3e-3 (Q = 4, bf16 state)
+
+
+def assert_state_grad_close(got, ref, rounds, G_X, what):
     """The active-row gradient stays fp32 through the sweep; the bf16 state
-    gradient dL/dX is rounded Q + 1 times (its initial scatter and one
-    accumulation per pre-map pass); each rounding moves an intermediate y by
-    at most 2^-8 |y|.  Bound: relative Frobenius error <= rounds * 2^-8 and each
-    element within 1e-2, 2e-2 |ref| or rounds * 2^-8 * scale (scale = the
-    largest intermediate magnitude, taken as max(max |ref|, max |G_X|))."""
+    gradient dL/dX is rounded `rounds` = Q + 1 times (its initial scatter and
+    one accumulation per pre-map pass), each moving the element's running
+    value y by at most 2^-8 |y|; the running value starts at G_X (the
+    untouched rows) and ends at ref, and in between it can exceed both, so
+    the per-element scale is the larger of |G_X| there and the largest |ref|
+    of the element's own (token, stream) row.  Bound: relative Frobenius
+    error <= FROB_STATE, and each element within 1e-2, 2e-2 |ref| or
+    rounds 2^-8 that scale."""
     got = got.detach().to("cpu", F64)
     ref = ref.detach().to("cpu", F64)
+    G_X = G_X.detach().to("cpu", F64)
     rel = ((got - ref).norm() / max(ref.norm().item(), 1e-30)).item()
     print(f"{what}: relative Frobenius error {rel:.2e}", flush=True)
-    assert rel <= rounds * 2.0 ** -8, f"{what}: relative Frobenius error {rel:.2e}"
+    assert rel <= FROB_STATE, f"{what}: relative Frobenius error {rel:.2e}"
     d = (got - ref).abs()
-    ok = (d <= 1e-2) | (d <= 2e-2 * ref.abs()) | (d <= rounds * 2.0 ** -8 * scale)
+    own = torch.maximum(ref.abs().amax(dim=-1, keepdim=True).expand_as(ref), G_X.abs())
+    ok = (d <= 1e-2) | (d <= 2e-2 * ref.abs()) | (d <= rounds * 2.0 ** -8 * own)
+    worst = (d / torch.maximum(torch.full_like(own, 1e-2), rounds * 2.0 ** -8 * own)).max().item()
+    print(f"{what}: worst element at {worst:.2f} of its bound", flush=True)
     assert bool(ok.all()), f"{what}: {int((~ok).sum())} elements out of tolerance, max |d| {d.max().item():.2e}"
 
 
@@ -75,8 +85,7 @@ def test_flash_backward_matches_oracle(w, Q, bias):
     d, grp, state, g = _run(w, Q, seed=61, bias_std=bias)
     ref, fwd, _ = _oracle(w, d)
     assert torch.equal(grp.idx.cpu().long(), fwd["idx"]), "routing differs (near-tie seed?)"
-    scale = max(ref["X"].abs().max().item(), d["G_X"].abs().max().item())
-    assert_state_grad_close(g["X"], ref["X"], Q + 1, scale, "dX")
+    assert_state_grad_close(g["X"], ref["X"], Q + 1, d["G_X"], "dX")
     for q in range(Q):
         assert_bf16_close(g["F_list"][q], ref["F_list"][q], f"dF_{q + 1}")
         for n, what in (("W_pre_list", "W_pre"), ("b_pre", "b_pre"), ("W_post_list", "W_post"), ("b_post", "b_post"),
@@ -94,8 +103,7 @@ def test_flash_backward_mid_size():
     d, grp, state, g = _run(w, 4, seed=9)
     ref, fwd, _ = _oracle(w, d)
     assert torch.equal(grp.idx.cpu().long(), fwd["idx"]), "routing differs (near-tie seed?)"
-    scale = max(ref["X"].abs().max().item(), d["G_X"].abs().max().item())
-    assert_state_grad_close(g["X"], ref["X"], 5, scale, "dX")
+    assert_state_grad_close(g["X"], ref["X"], 5, d["G_X"], "dX")
     for q in range(4):
         assert_bf16_close(g["F_list"][q], ref["F_list"][q], f"dF_{q + 1}")
         assert_grad_close(g["W_pre_list"][q], ref["W_pre_list"][q], f"W_pre_{q + 1}")
@@ -136,6 +144,8 @@ def test_flash_backward_full_size_state_gradient_on_sampled_tokens():
                                       m=w.m, k=w.k, S=w.S, kappa=w.kappa, router=w.router,
                                       gram_schmidt_on=bool(w.gram_schmidt), tokens=tok)
     same = (grp.idx[tg].cpu().long() == fwd["idx"]).all(1)
+    # a token may route differently only at a near-tie of its routed logits
+    assert bool((fwd["gap"][~same] < NEAR_TIE).all()), "routing differs at a sampled token that is no near-tie"
     assert int(same.sum()) >= len(tok) - 1, "routing differs at more than one sampled token"
-    scale = max(ref["X"].abs().max().item(), d["G_X"][tg].abs().max().item())
-    assert_state_grad_close(g["X"][tg].cpu()[same], ref["X"][same], Q + 1, scale, "dX (sampled tokens)")
+    assert_state_grad_close(g["X"][tg].cpu()[same], ref["X"][same], Q + 1, d["G_X"][tg].cpu()[same],
+                            "dX (sampled tokens)")

@@ -6,7 +6,7 @@ import torch
 from oracle import xhc_oracle as O
 from paper_2607_14530_amd import synth
 from paper_2607_14530_amd import xhc as X
-from tests.parity_util import assert_bf16_close, check_sublayer
+from tests.parity_util import NEAR_TIE, assert_bf16_close, check_sublayer, oracle_pre
 
 pytestmark = pytest.mark.gpu
 
@@ -142,11 +142,15 @@ def test_full_size_sampled_tokens(w, impl):
     check_sublayer(sub, inp, w, before[tg], after[tg], tokens=tok)
 
 
-def test_fused_and_multi_agree_bitwise_on_routing():
-    """Both implementations reduce in a fixed order; their routing decisions agree exactly."""
+def test_fused_and_multi_routing_differs_only_at_near_ties():
+    """Both implementations rank by the same total order but sum the logits in
+    different fixed orders (fp32), so their routing may differ only where the
+    oracle's routed logits are within NEAR_TIE of each other."""
     w = W(T=1024, S=512, N=16, k=4, m=2, C=1024, Kr=4, name="agree")
     a = _run(w, seed=9, impl=X.XHC_IMPL_MULTI)
     b = _run(w, seed=9, impl=X.XHC_IMPL_FUSED)
-    same = (a[1].idx == b[1].idx).all(dim=1)
-    assert float(same.float().mean()) > 0.999
+    same = (a[1].idx == b[1].idx).all(dim=1).cpu()
+    if not bool(same.all()):
+        ref = oracle_pre(a[0], w, torch.nonzero(~same).flatten())
+        assert bool((ref["gap"] < NEAR_TIE).all()), "fused and multi routing differ at a token that is no near-tie"
     assert torch.allclose(a[1].Hpre, b[1].Hpre, atol=1e-5, rtol=0)
