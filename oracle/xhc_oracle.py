@@ -395,6 +395,49 @@ def xhc_flash_group(X0, F_list, W_r, W_pre_list, W_post_list, W_res, conv_w_list
                 input_scalar_form=input_scalar, z_r=z_r)
 
 
+def xhc_flash_step(a, q, X0, idx, p, Hpre, F, conv_w, W_post, alpha_post, b_post,
+                   W_res=None, alpha_res=None, b_res=None, *, Q, S, kappa=(4, 8, 12), eps=1e-5,
+                   sinkhorn_iters=20, clamp_delta=1e-6, gram_schmidt_on=True, tokens=None, base=None):
+    """Sublayer q (1-based) of a sharing group, from the active rows a =
+    a^(q-1) [T, k, C] as they are stored before it (float64 values).
+
+    The routing (idx, p) and the pre-maps Hpre [Q, T, N] come from the
+    group-entry state X0 (eq:flash_dual_read).  The input of sublayer q is
+    the dense read of X0 for q = 1 and base^(q) + sum_j H^pre,q_{I_j} a_j for
+    q >= 2 (eq:app_four_sub_base, eq:app_active_state_correction); H^post,q
+    (and H^res for q = Q) come from RMS(a) (eq:param_post, eq:param_res, App.
+    E.2); the rows become a + p H^post,q out_aug for q < Q and H^res a + p
+    H^post,Q out_aug for q = Q (eq:flash_attn_update,
+    eq:app_general_writeback).  ``base`` (q >= 2, optional) is base^(q) as
+    stored by whoever formed it; when None it is computed from X0.  Returns
+    dict(input, Hpost, Hres (q = Q, else None), a_new), a_new unrounded.
+    Parity: pinned (chaining it reproduces xhc_flash_group, see tests)."""
+    T, N, C = X0.shape
+    k = idx.shape[1]
+    Kq = W_post.shape[1] // k
+    active = torch.zeros(T, N, dtype=torch.bool)
+    active[torch.arange(T)[:, None], idx] = True
+    if q == 1:
+        inp = torch.einsum("tn,tnc->tc", Hpre[0], X0)
+    else:
+        if base is None:
+            base = torch.einsum("tn,tnc->tc", Hpre[q - 1] * (~active), X0)
+        hsel = torch.gather(Hpre[q - 1], 1, idx)
+        inp = base + (hsel[:, :, None] * a).sum(1)
+    a_n = rms_norm(a.reshape(T, k * C), eps)
+    Hpost = post_mapping(a_n @ bf16_operand(W_post), alpha_post, torch.as_tensor(b_post, dtype=F64), k, Kq)
+    Hres = None
+    if q == Q:
+        Hres = residual_mapping(a_n @ bf16_operand(W_res), alpha_res, torch.as_tensor(b_res, dtype=F64), k,
+                                sinkhorn_iters, clamp_delta)
+    if tokens is None:
+        tokens = torch.arange(T)
+    comps = augmented_output(F, conv_w, kappa, S, tokens, gram_schmidt_on)
+    wb = sum(Hpost[:, :, r, None] * comps[r][:, None, :] for r in range(len(comps)))
+    mixed = a if q < Q else torch.einsum("tjl,tlc->tjc", Hres, a)
+    return dict(input=inp, Hpost=Hpost, Hres=Hres, a_new=mixed + p[:, :, None] * wb)
+
+
 # --------------------------------------------------------------------------
 # backward (reverse mode of the forward above)
 # --------------------------------------------------------------------------

@@ -456,6 +456,27 @@ def test_flash_steps_match_full_post(Q):
     assert torch.equal(r, out["idx"])
 
 
+@pytest.mark.parametrize("Q", [2, 4])
+def test_flash_step_chained_reproduces_the_group(Q):
+    """xhc_flash_step run for q = 1..Q, each from the rows the previous one
+    stored (rounded to bf16), gives the group's inputs, mappings and states."""
+    w, d, out = _flash(Q, round_state=True, seed=3)
+    X0 = d["X"].to(F64)
+    a = O.gather_rows(X0, out["idx"])
+    for q in range(1, Q + 1):
+        st = O.xhc_flash_step(a, q, X0, out["idx"], out["p"], out["Hpre"], d["F_list"][q - 1],
+                              d["conv_w_list"][q - 1], d["W_post_list"][q - 1], d["alpha_post"][q - 1],
+                              d["b_post"][q - 1], d["W_res"] if q == Q else None,
+                              d["alpha_res"] if q == Q else None, d["b_res"] if q == Q else None,
+                              Q=Q, S=w.S, kappa=w.kappa)
+        assert torch.allclose(st["input"], out["inputs"][q - 1], atol=1e-12, rtol=0)
+        assert torch.allclose(st["Hpost"], out["Hpost"][q - 1], atol=1e-12, rtol=0)
+        if q == Q:
+            assert torch.allclose(st["Hres"], out["Hres"], atol=1e-12, rtol=0)
+        a = O.round_state_bf16(st["a_new"])
+        assert torch.equal(O.gather_rows(out["X_steps"][q - 1], out["idx"]), a)
+
+
 def test_flash_untouched_rows_are_never_written():
     w, d, out = _flash(4, round_state=True)
     act = torch.zeros(w.T, w.N, dtype=torch.bool)
