@@ -85,12 +85,32 @@ def calibrate_copy(gib=1):
     print(json.dumps({"copy_bytes_read": 2 * n, "copy_bytes_written": 2 * n, "launches": 3}), flush=True)
 
 
-def cpu_baseline(seconds=15.0):
-    """Time the fp64 oracle (pre + post of both sublayer kinds) on a sample of
-    tokens of the same workload, growing the sample until it runs ~seconds."""
+def host_cpu():
+    """CPU model and physical core count of this host (lscpu; /proc/cpuinfo)."""
+    import subprocess
+    model, sockets, per_socket = None, None, None
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            key, _, val = line.partition(":")
+            key, val = key.strip(), val.strip()
+            if key == "Model name":
+                model = val
+            elif key == "Socket(s)":
+                sockets = int(val)
+            elif key == "Core(s) per socket":
+                per_socket = int(val)
+    except (OSError, ValueError, subprocess.SubprocessError):
+        pass
+    physical = sockets * per_socket if sockets and per_socket else None
+    return model, physical
+
+
+def _oracle_tokens_per_s(n, seconds, label):
+    """Oracle pre + post of both sublayer kinds on n tokens, n grown until the
+    run takes about `seconds`; returns (sublayer-tokens/s, n, elapsed)."""
     from oracle import xhc_oracle as O
     F64 = torch.float64
-    n = 16
     while True:
         elapsed = 0.0
         for Kr in (1, 4):
@@ -105,14 +125,39 @@ def cpu_baseline(seconds=15.0):
             O.xhc_post(Xd, inp["F"], inp["conv_w"], r["idx"], r["p"], r["Hres"], r["Hpost"],
                        S=ws.S, kappa=ws.kappa)
             elapsed += time.perf_counter() - t0
-        print(f"[cpu_baseline] {n} tokens: {elapsed:.2f} s", file=sys.stderr, flush=True)
+        print(f"[cpu_baseline] {label}: {n} tokens: {elapsed:.2f} s", file=sys.stderr, flush=True)
         if elapsed >= seconds or n >= 16384:
-            break
-        n = max(n * 2, int(n * seconds / max(elapsed, 1e-3) * 1.1))
-        n = min(n, 16384)
-    return {"value": 2 * n / elapsed, "unit": "tokens/s", "cores": torch.get_num_threads(), "kind": "oracle",
+            return 2 * n / elapsed, n, elapsed
+        n = min(16384, max(n * 2, int(n * seconds / max(elapsed, 1e-3) * 1.1)))
+
+
+def cpu_baseline(seconds=12.0, seconds_single=8.0):
+    """Time the fp64 oracle (pre + post of both sublayer kinds) on a sample of
+    tokens of the same workload, on all of torch's threads and on one thread."""
+    threads = torch.get_num_threads()
+    value, n, elapsed = _oracle_tokens_per_s(16, seconds, f"{threads} threads")
+    torch.set_num_threads(1)
+    try:
+        single, n1, e1 = _oracle_tokens_per_s(4, seconds_single, "1 thread")
+    finally:
+        torch.set_num_threads(threads)
+    model, physical = host_cpu()
+    return {"value": value, "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} tokens x (attention-type + MLP-type sublayer), N=16 k=4 m=2 C=4096, fp64, "
-                      f"{elapsed:.1f} s"}
+                      f"{elapsed:.1f} s on {threads} threads; single thread: {n1} tokens, {e1:.1f} s",
+            "single_thread_value": single, "cpu_model": model, "physical_cores": physical,
+            "logical_cpus": os.cpu_count()}
+
+
+def pctl(xs, q):
+    """q-th percentile (0..100) of xs, linear interpolation."""
+    v = sorted(xs)
+    if not v:
+        return None
+    pos = (len(v) - 1) * q / 100.0
+    lo = int(pos)
+    hi = min(lo + 1, len(v) - 1)
+    return v[lo] + (v[hi] - v[lo]) * (pos - lo)
 
 
 def _time(fn, iters, stream):
@@ -128,7 +173,7 @@ def _time(fn, iters, stream):
     return e0.elapsed_time(e1) / iters
 
 
-SECTIONS = ("flash_q4", "flash_q2", "mhc_n4", "prefill_t2048", "bwd_n16_mlp", "flash_bwd_q4")
+SECTIONS = ("flash_q4", "flash_q2", "mhc_n4", "prefill_t2048", "bwd_mlp_sweep", "flash_bwd_q4")
 
 
 def extra_sections(dev, stream, iters=5, only=None):
@@ -192,24 +237,27 @@ def extra_sections(dev, stream, iters=5, only=None):
                                 "ms_per_block": pre_ms["auto"], "ms_per_block_multi": pre_ms["multi"],
                                 "ms_per_block_fused": pre_ms["fused"],
                                 "tokens_per_s": 2048 / (pre_ms["auto"] * 1e-3)}
-    if want("bwd_n16_mlp"):
-        # backward, T = 8192, N = 16, k = 4, C = 4096, MLP-type
-        w = synth.bwd_sweep(16, 4)
-        inp = synth.sublayer_inputs(w, 10, device=dev, grads=True)
-        sub = X.TrainableSublayer(X.dims_for(w), inp, dev)
-        st = inp["X"]
-        fwd_ms = _time(lambda: sub.forward(st, inp["F"], stream), 1, stream)
-        sub.forward(st, inp["F"], stream)
-
-        def fb():
-            sub.backward(st, inp["G_X"], inp["G_in"], inp["F"], stream)
+    if want("bwd_mlp_sweep"):
+        # backward of an MLP-type sublayer, T = 8192, k = 4, C = 4096, N = 4, 8, 16, 32
+        res = {}
+        for N in (4, 8, 16, 32):
+            w = synth.bwd_sweep(N, 4)
+            inp = synth.sublayer_inputs(w, 10, device=dev, grads=True)
+            sub = X.TrainableSublayer(X.dims_for(w), inp, dev)
+            st = inp["X"]
+            fwd_ms = _time(lambda: sub.forward(st, inp["F"], stream), 2, stream)
             sub.forward(st, inp["F"], stream)
-        ms = _time(fb, 2, stream)
-        out["bwd_n16_mlp"] = {"workload": "xHC MLP-type sublayer backward, T=8192, N=16, k=4, m=2, C=4096",
-                              "ms_forward_with_saves": fwd_ms, "ms_backward": ms - fwd_ms,
-                              "tokens_per_s_backward": w.T / ((ms - fwd_ms) * 1e-3)}
-        del sub, inp, st
-        torch.cuda.empty_cache()
+
+            def fb():
+                sub.backward(st, inp["G_X"], inp["G_in"], inp["F"], stream)
+                sub.forward(st, inp["F"], stream)
+            ms = _time(fb, 3, stream)
+            res[f"N{N}"] = {"ms_forward_with_saves": fwd_ms, "ms_backward": ms - fwd_ms,
+                            "tokens_per_s_backward": w.T / ((ms - fwd_ms) * 1e-3)}
+            del sub, inp, st
+            torch.cuda.empty_cache()
+        out["bwd_mlp_sweep"] = {"workload": "xHC MLP-type sublayer backward, T=8192, k=4, m=2, C=4096, "
+                                            "N in {4, 8, 16, 32}", **res}
     if want("flash_bwd_q4"):
         # xHC-Flash group backward, Q = 4, T = 8192, N = 16, k = 4, C = 4096
         w = synth.bwd_sweep(16, 4)
@@ -295,6 +343,7 @@ def main():
     seg = [[e[j].elapsed_time(e[j + 1]) for e in evs] for j in range(4)]   # ms
     mean = [sum(s) / len(s) for s in seg]
     step_ms = sum(mean)
+    per_step = [sum(seg[j][i] for j in range(4)) for i in range(args.steps)]
     value = 2 * T / (step_ms * 1e-3)
 
     b_pre = A.algorithmic_bytes_pre(N, k, C, 1) * T
@@ -317,7 +366,10 @@ def main():
         "achieved_GBps": gbps, "hbm_frac": gbps / HBM_PEAK_GBPS,
         "bytes_per_token_C": total_bytes / (2 * T) / (2 * C),
         "paper_bytes_per_token_C": 73.5,
+        "ms_per_step_p10_p50_p90": [pctl(per_step, 10), pctl(per_step, 50), pctl(per_step, 90)],
         "segments_ms": {"attn_pre": mean[0], "attn_post": mean[1], "mlp_pre": mean[2], "mlp_post": mean[3]},
+        "segments_ms_p10_p50_p90": {n: [pctl(seg[j], 10), pctl(seg[j], 50), pctl(seg[j], 90)]
+                                    for j, n in enumerate(("attn_pre", "attn_post", "mlp_pre", "mlp_post"))},
         "wall_s": wall,
         "roofline": {"kernel": "xhc_pre entry point (single-pass cooperative kernel k_pre_fused: projection, "
                                "routing, dense read, gathered projection; then the per-token coefficient pass), "
