@@ -29,7 +29,8 @@
  *    constraint or NULL required pointer; XHC_EUNSUPPORTED: valid shape this
  *    library does not implement; XHC_EWORKSPACE: workspace too small;
  *    XHC_EHIP: a HIP launch failed (outputs unspecified).
- *  - Thread safety: the library holds no mutable global state; calls on
+ *  - Thread safety: the library holds no mutable global state (apart from a
+ *    per-device cache of the scratch address of xhc_post_noalloc); calls on
  *    different streams may overlap provided their buffers do not.
  */
 #ifndef XHC_H_
@@ -174,6 +175,22 @@ size_t xhc_saved_floats(const xhc_dims* d);
 xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv_w,
                     const int32_t* idx, const float* p, const float* Hres, const float* Hpost,
                     void* Xact_save, void* workspace, size_t workspace_bytes, void* stream);
+
+/* xhc_post_noalloc - xhc_post for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).  Same arguments, results and errors as xhc_post, without the
+ * workspace: the MLP-type write-back's scratch (Gram partials and write-back
+ * weights, xhc_workspace_bytes(d, XHC_OP_POST, 0) bytes) lives in a static
+ * device array of XHC_NOALLOC_SCRATCH_BYTES that every GPU the library runs
+ * on holds until the process ends.  The call allocates nothing.  Shapes whose
+ * scratch exceeds that size return XHC_EWORKSPACE before any work is
+ * enqueued (at C = 4096, K_r = 4: T up to about 72K tokens).  All calls on
+ * one GPU share its array: calls that overlap on one GPU (different streams
+ * without ordering between them) race and must not be made.            */
+#define XHC_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+xhc_status xhc_post_noalloc(const xhc_dims* d, void* X, const void* F, const float* conv_w,
+                            const int32_t* idx, const float* p, const float* Hres, const float* Hpost,
+                            void* Xact_save, void* stream);
 
 /* ------------------------------------------------------------------ backward
  * Reverse mode of xhc_pre + xhc_post for a loss L(X', input) (X' = state after

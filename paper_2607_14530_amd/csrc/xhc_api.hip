@@ -5,6 +5,7 @@
 #include <stdio.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "xhc.h"
 #include "xhc_launch.h"
@@ -263,7 +264,8 @@ size_t post_ws(const xhc_dims* d) {
          align_up((size_t)d->T * d->k * d->Kr * sizeof(float));
 }
 
-// xhc_post's work on a given scratch buffer
+// xhc_post's work on a given scratch buffer (the caller's workspace, or the
+// library's static one for xhc_post_noalloc)
 xhc_status post_impl(const xhc_dims* d, void* X, const void* F, const float* conv_w, const int32_t* idx,
                      const float* p, const float* Hres, const float* Hpost, void* Xact_save, void* workspace,
                      size_t workspace_bytes, void* stream) {
@@ -297,6 +299,41 @@ xhc_status post_impl(const xhc_dims* d, void* X, const void* F, const float* con
   return hip_status(e);
 }
 
+
+// ---- scratch of xhc_post_noalloc: a fixed device array instead of a caller
+// workspace.  Each device holds its own copy of the array for the life of the
+// process; host code reaches it only through the address hipGetSymbolAddress
+// returns on that device (the array's name is not a device address in host
+// code).
+constexpr size_t kNoAllocScratchBytes = XHC_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// the address of `scratch` on the current device, looked up once per device
+xhc_status noalloc_scratch(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess && (dev < 0 || dev >= kMaxDevices)) e = hipErrorInvalidDevice;
+  if (e != hipSuccess) {
+    g_failed_step = "noalloc_device";
+    return hip_status(e);
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      g_failed_step = "noalloc_symbol";
+      return hip_status(e != hipSuccess ? e : hipErrorInvalidSymbol);
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return XHC_OK;
+}
 
 }  // namespace
 
@@ -474,6 +511,19 @@ xhc_status xhc_post(const xhc_dims* d, void* X, const void* F, const float* conv
                     const float* p, const float* Hres, const float* Hpost, void* Xact_save, void* workspace,
                     size_t workspace_bytes, void* stream) {
   return post_impl(d, X, F, conv_w, idx, p, Hres, Hpost, Xact_save, workspace, workspace_bytes, stream);
+}
+
+xhc_status xhc_post_noalloc(const xhc_dims* d, void* X, const void* F, const float* conv_w, const int32_t* idx,
+                            const float* p, const float* Hres, const float* Hpost, void* Xact_save, void* stream) {
+  xhc_status st = check_dims(d);
+  if (st != XHC_OK) return st;
+  if (post_ws(d) > kNoAllocScratchBytes) return XHC_EWORKSPACE;
+  void* scr = nullptr;
+  if (post_ws(d) > 0 && d->T > 0) {
+    st = noalloc_scratch(&scr);
+    if (st != XHC_OK) return st;
+  }
+  return post_impl(d, X, F, conv_w, idx, p, Hres, Hpost, Xact_save, scr, scr ? kNoAllocScratchBytes : 0, stream);
 }
 
 // ---------------------------------------------------------------- xHC-Flash

@@ -82,6 +82,7 @@ _SIGS = {
     "xhc_pre": (ctypes.c_int, [_D] + [_P] * 15 + [ctypes.c_size_t, _P]),
     "xhc_post": (ctypes.c_int, [_D] + [_P] * 9 + [ctypes.c_size_t, _P]),
     "xhc_saved_floats": (ctypes.c_size_t, [_D]),
+    "xhc_post_noalloc": (ctypes.c_int, [_D] + [_P] * 9),
     "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 14 + [ctypes.c_size_t, _P]),
     "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 18 + [ctypes.c_size_t, _P]),
     "xhc_flash_post_bwd": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 29 + [ctypes.c_size_t, _P]),
@@ -194,6 +195,14 @@ def xhc_post(d, X, F, conv_w, idx, p, Hres, Hpost, Xact_save, workspace, stream=
     _call("xhc_post", ctypes.byref(d), _ptr(X), _ptr(F), _ptr(conv_w), _ptr(idx), _ptr(p), _ptr(Hres),
           _ptr(Hpost), _ptr(Xact_save), _ptr(workspace), workspace.numel() if workspace is not None else 0,
           _stream(stream))
+
+
+NOALLOC_SCRATCH_BYTES = 16 << 20   # XHC_NOALLOC_SCRATCH_BYTES
+
+
+def xhc_post_noalloc(d, X, F, conv_w, idx, p, Hres, Hpost, Xact_save, stream=None):
+    _call("xhc_post_noalloc", ctypes.byref(d), _ptr(X), _ptr(F), _ptr(conv_w), _ptr(idx), _ptr(p), _ptr(Hres),
+          _ptr(Hpost), _ptr(Xact_save), _stream(stream))
 
 
 def _nbytes(t):

@@ -119,3 +119,12 @@ def test_forced_fused_path_rejects_uncovered_shapes():
     assert _pre_status(d) == X.XHC_EUNSUPPORTED
     d = X.make_dims(T=64, N=16, k=4, m=2, C=256, Kr=1, impl=7)
     assert _pre_status(d) == X.XHC_EINVAL
+
+
+def test_post_noalloc_rejects_shapes_beyond_its_scratch_before_any_work():
+    """xhc_post_noalloc refuses a shape whose scratch exceeds the static array
+    (XHC_NOALLOC_SCRATCH_BYTES) before touching any pointer or the device."""
+    d = X.make_dims(1 << 20, 16, 4, 2, 4096, Kr=4, S=8192)
+    assert X.xhc_workspace_bytes(d, X.XHC_OP_POST) > X.NOALLOC_SCRATCH_BYTES
+    st = X.lib().xhc_post_noalloc(ctypes.byref(d), 16, 16, 16, 16, 16, 16, 16, None, None)
+    assert st == X.XHC_EWORKSPACE
