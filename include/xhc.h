@@ -58,7 +58,8 @@ typedef enum { XHC_BF16 = 0, XHC_F32 = 1 } xhc_dtype;
  * kappa = {4, 8, 12}, 20 Sinkhorn iterations).  Constraints:
  *   T >= 0, S >= 1, T % S == 0;  1 <= k <= N <= 64;  0 <= m <= k;  k <= 8;
  *   C >= 32, C % 32 == 0;  Kr in 1..4;  kappa[j] in 1..16 for j < Kr - 1;
- *   sinkhorn_iters in 0..1000;  eps > 0;  clamp_delta >= 0;  router 0 or 1. */
+ *   sinkhorn_iters in 0..1000;  eps > 0;  clamp_delta >= 0;  router 0 or 1;
+ *   attn_aug 0 or 1.                                                         */
 typedef struct xhc_dims {
   int64_t T;              /* tokens                                              */
   int64_t S;              /* tokens per sequence (causal conv window resets)     */
@@ -75,6 +76,10 @@ typedef struct xhc_dims {
   int32_t state_dtype;    /* xhc_dtype of X, F, input, base                      */
   int32_t impl;           /* xhc_impl: which kernels run (same results)          */
   int32_t router;         /* xhc_router: score function of the router            */
+  int32_t attn_aug;       /* xHC-Flash groups: 0 = attention-type sublayers have */
+                          /* one write-back component (the paper's design); 1 =  */
+                          /* they get the Kr components of the temporal          */
+                          /* augmentation too (the attention-side ablation)      */
 } xhc_dims;
 
 /* Router score function.  SIGMOID is eq:router; SOFTMAX is the ablation of
@@ -241,7 +246,10 @@ xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full
  * A sharing group of Q = 2 or 4 consecutive sublayers (Sec. "xHC-Flash",
  * Alg. "xHC-Flash: one Transformer block", App. E).  Sublayer q (1-based) is
  * attention-type (one write-back component) for odd q and MLP-type (d->Kr
- * components with the temporal augmentation) for even q.  One routing
+ * components with the temporal augmentation) for even q; with d->attn_aug = 1
+ * the attention-type sublayers get the same d->Kr components (the
+ * attention-side temporal augmentation of the additional-ablations table).
+ * K_q below is the component count of sublayer q.  One routing
  * decision and Q pre-maps come from the group-entry state; intermediate
  * sublayers write the active rows without residual mixing; the last applies
  * H^res.  Later inputs are formed from non-active base readouts plus the
@@ -250,11 +258,11 @@ xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full
  * xhc_flash_pre - once per group.
  *   X            [T,N,C] group-entry state (read only)
  *   packed_full  xhc_pack_full(npre = Q) of W_r and the Q matrices W_pre,q
- *   packed_act1  xhc_pack_active(Kq = 1, W_res = NULL) of W_post,1
- *   alpha_pre [Q], b_pre [Q,N], alpha_post1 [1], b_post1 [k] fp32 device
+ *   packed_act1  xhc_pack_active(Kq = K_1, W_res = NULL) of W_post,1
+ *   alpha_pre [Q], b_pre [Q,N], alpha_post1 [1], b_post1 [k K_1] fp32 device
  * Outputs: input1 [T,C] = sum_i H^pre,1_i x_i; base [Q-1,T,C] where base[q-2] =
  * sum_{i not in I} H^pre,q_i x_i (q = 2..Q); idx, p as in xhc_pre; Hpre [Q,T,N];
- * Hpost1 [T,k,1].                                                             */
+ * Hpost1 [T,k,K_1].                                                           */
 xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full,
                          const void* packed_act1, const float* alpha_pre, const float* b_pre,
                          const float* alpha_post1, const float* b_post1, void* input1, void* base, int32_t* idx,
@@ -264,7 +272,7 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
 /* xhc_flash_post - after sublayer q of the group (1 <= q <= Q).
  *   X       [T,N,C] in/out: rows X[t, idx[t,j], :] <- (q == Q ? sum_l Hres[t,j,l]
  *           X[t,idx[t,l],:] : X[t,idx[t,j],:]) + p[t,j] sum_r Hpost[t,j,r] v_r[t]
- *   F       [T,C] output of sublayer q; conv_w as in xhc_post, non-NULL iff q is even
+ *   F       [T,C] output of sublayer q; conv_w as in xhc_post, non-NULL iff K_q > 1
  *   Hpost   [T,k,K_q] of sublayer q; Hres [T,k,k] iff q == Q (else NULL)
  * For q < Q (else all NULL):
  *   Hpre_next [T,N] = Hpre[q] from xhc_flash_pre; base_next [T,C] = base[q-1];

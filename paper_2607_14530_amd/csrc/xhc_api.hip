@@ -29,6 +29,7 @@ xhc_status check_dims(const xhc_dims* d) {
   if (d->state_dtype != XHC_BF16 && d->state_dtype != XHC_F32) return XHC_EINVAL;
   if (d->impl < XHC_IMPL_AUTO || d->impl > XHC_IMPL_FUSED) return XHC_EINVAL;
   if (d->router != XHC_ROUTER_SIGMOID && d->router != XHC_ROUTER_SOFTMAX) return XHC_EINVAL;
+  if (d->attn_aug != 0 && d->attn_aug != 1) return XHC_EINVAL;
   if (d->N > kMaxN || d->k > kMaxK || d->Kr > kMaxKr || d->sinkhorn_iters > 1000) return XHC_EUNSUPPORTED;
   if (d->C % 32 != 0) return XHC_EUNSUPPORTED;
   for (int j = 0; j < d->Kr - 1; ++j)
@@ -95,11 +96,13 @@ size_t pre_ws(const xhc_dims* d) {
 }
 
 // write-back components of sublayer q (1-based) of an xHC-Flash group:
-// attention-type (odd q) has one, MLP-type (even q) has d->Kr
-int flash_Kq(const xhc_dims* d, int q) { return (q % 2 == 1) ? 1 : d->Kr; }
+// attention-type (odd q) has one, MLP-type (even q) has d->Kr; with attn_aug
+// the attention-type sublayers have d->Kr too (the ablation of
+// attention-side temporal augmentation)
+int flash_Kq(const xhc_dims* d, int q) { return (q % 2 == 1 && !d->attn_aug) ? 1 : d->Kr; }
 
 size_t flash_pre_ws(const xhc_dims* d, int Q) {
-  const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, 1, 0);
+  const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, flash_Kq(d, 1), 0);
   const size_t full = part_bytes(d, false, NC_of(d), nf), act = part_bytes(d, true, kC_of(d), na);
   const size_t sf = sums_bytes(nf, d->T), sa = sums_bytes(na, d->T);
   return (full > act ? full : act) + (sf > sa ? sf : sa);
@@ -547,7 +550,8 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   clear_stale_error();
   const int64_t NC = NC_of(d), kC = kC_of(d);
-  const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, 1, 0);
+  const int K1 = flash_Kq(d, 1);
+  const int64_t nf = (int64_t)(Q + 1) * d->N, na = act_outs(d, K1, 0);
   float* part = reinterpret_cast<float*>(workspace);
   float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
                                          std::max(part_bytes(d, false, NC, nf), part_bytes(d, true, kC, na)));
@@ -562,7 +566,7 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
   XHC_STEP("flash_proj_active",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act1, na, idx, d->k, part, s));
   XHC_STEP("flash_coef1", launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, na, d->T), na, d->T,
-                                          d->k, 1, 0, d->C, alpha_post1, nullptr, b_post1, nullptr, d->eps,
+                                          d->k, K1, 0, d->C, alpha_post1, nullptr, b_post1, nullptr, d->eps,
                                           d->sinkhorn_iters, d->clamp_delta, Hpost1, nullptr, sums, nullptr, 0, 0, 0,
                                           s));
   XHC_STEP("flash_dense_read",

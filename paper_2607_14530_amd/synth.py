@@ -37,6 +37,7 @@ class Workload:
     name: str = ""
     router: str = "sigmoid"         # "sigmoid" (eq:router) or "softmax" (ablation)
     gram_schmidt: int = 1           # 0: components used as they are (the Muon-trained variant)
+    attn_aug: int = 0               # 1: attention-type sublayers of a Flash group augmented too (ablation)
 
     def __post_init__(self):
         if self.S == 0:
@@ -92,8 +93,9 @@ def flash_inputs(w: Workload, Q: int, seed: int, device="cpu", weight_std=0.02, 
                  bias_std=0.0):
     """Inputs of one xHC-Flash sharing group of Q sublayers (Q = 2 or 4).
 
-    Sublayer q (1-based) is attention-type (one write-back component) when q
-    is odd and MLP-type (1 + len(kappa) components) when q is even.  Returns
+    Sublayer q (1-based) is attention-type (one write-back component, or
+    1 + len(kappa) with w.attn_aug) when q is odd and MLP-type
+    (1 + len(kappa) components) when q is even.  Returns
     X, F_list (Q x [T,C]), W_r, W_pre_list (Q x [N*C,N]), W_post_list
     (Q x [k*C, k*K_q]), W_res [k*C,k*k], conv_w_list (None for attention),
     alpha_pre/alpha_post (Q floats), alpha_res, b_pre (Q x [N]),
@@ -106,7 +108,7 @@ def flash_inputs(w: Workload, Q: int, seed: int, device="cpu", weight_std=0.02, 
     g = torch.Generator(device=device)
     g.manual_seed(seed)
     T, N, k, C = w.T, w.N, w.k, w.C
-    Kq = [1 if q % 2 == 1 else 1 + len(w.kappa) for q in range(1, Q + 1)]
+    Kq = [1 if (q % 2 == 1 and not w.attn_aug) else 1 + len(w.kappa) for q in range(1, Q + 1)]
     d = {"Kq": Kq}
     d["X"] = _randn((T, N, C), g, device).to(w.dtype)
     d["F_list"] = [_randn((T, C), g, device).to(w.dtype) for _ in range(Q)]

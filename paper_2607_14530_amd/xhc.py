@@ -44,12 +44,13 @@ class Dims(ctypes.Structure):
         ("Kr", ctypes.c_int32), ("kappa", ctypes.c_int32 * 3),
         ("sinkhorn_iters", ctypes.c_int32), ("gram_schmidt", ctypes.c_int32),
         ("eps", ctypes.c_float), ("clamp_delta", ctypes.c_float), ("state_dtype", ctypes.c_int32),
-        ("impl", ctypes.c_int32), ("router", ctypes.c_int32),
+        ("impl", ctypes.c_int32), ("router", ctypes.c_int32), ("attn_aug", ctypes.c_int32),
     ]
 
 
 def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, gram_schmidt=1,
-              eps=1e-5, clamp_delta=1e-6, state="bf16", impl=XHC_IMPL_AUTO, router="sigmoid") -> Dims:
+              eps=1e-5, clamp_delta=1e-6, state="bf16", impl=XHC_IMPL_AUTO, router="sigmoid",
+              attn_aug=0) -> Dims:
     d = Dims()
     d.T, d.S = T, (S if S else max(T, 1))
     d.N, d.k, d.m, d.C, d.Kr = N, k, m, C, Kr
@@ -60,6 +61,7 @@ def make_dims(T, N, k, m, C, Kr=1, S=None, kappa=(4, 8, 12), sinkhorn_iters=20, 
     d.state_dtype = XHC_BF16 if state == "bf16" else XHC_F32
     d.impl = impl
     d.router = XHC_ROUTER_SOFTMAX if router in ("softmax", XHC_ROUTER_SOFTMAX) else XHC_ROUTER_SIGMOID
+    d.attn_aug = int(attn_aug)
     return d
 
 
@@ -67,6 +69,7 @@ def dims_for(w, **kw) -> Dims:
     """Dims of a synth.Workload."""
     kw.setdefault("router", getattr(w, "router", "sigmoid"))
     kw.setdefault("gram_schmidt", getattr(w, "gram_schmidt", 1))
+    kw.setdefault("attn_aug", getattr(w, "attn_aug", 0))
     return make_dims(w.T, w.N, w.k, w.m, w.C, Kr=w.Kr, S=w.S, kappa=w.kappa, state=w.state, **kw)
 
 
@@ -317,8 +320,9 @@ class Sublayer:
 
 
 def flash_Kq(d, q):
-    """Write-back components of sublayer q (1-based) of a sharing group."""
-    return 1 if q % 2 == 1 else d.Kr
+    """Write-back components of sublayer q (1-based) of a sharing group
+    (attention-type sublayers have one unless d.attn_aug)."""
+    return 1 if (q % 2 == 1 and not d.attn_aug) else d.Kr
 
 
 class FlashGroup:
@@ -488,18 +492,21 @@ class TrainableSublayer(Sublayer):
         self.post(X, F, stream, Xact_save=self.Xact)
         return X
 
-    def backward(self, X, dXn, d_input, F, stream=None):
-        g = self.backward_post(X, dXn, F, stream)
+    def backward(self, X, dXn, d_input, F, stream=None, in_place=False):
+        g = self.backward_post(X, dXn, F, stream, in_place)
         return self.backward_pre(X, d_input, g, stream)
 
-    def backward_post(self, X, dXn, F, stream=None):
+    def backward_post(self, X, dXn, F, stream=None, in_place=False):
         """xhc_post_bwd: restores X to the state xhc_pre saw and returns the
-        partial gradients, dL/dF among them (for the sublayer's own backward)."""
+        partial gradients, dL/dF among them (for the sublayer's own backward).
+        With in_place, dL/dX is formed in dXn itself (only the k active rows
+        of each token are rewritten) and g["X"] is dXn."""
         d = self.d
         T, N, k, C, Kr = d.T, d.N, d.k, d.C, d.Kr
         dev = X.device
         f32 = dict(dtype=torch.float32, device=dev)
-        g = {"X": torch.empty_like(X), "F": torch.empty_like(F), "dHres": torch.empty(T, k, k, **f32),
+        g = {"X": dXn if in_place else torch.empty_like(X), "F": torch.empty_like(F),
+             "dHres": torch.empty(T, k, k, **f32),
              "dHpost": torch.empty(T, k, Kr, **f32), "dp": torch.empty(T, k, **f32),
              "conv_w": torch.empty_like(self.conv_w) if self.conv_w is not None else None}
         xhc_post_bwd(d, dXn, X, self.Xact, F, self.conv_w, self.idx, self.p, self.Hres, self.Hpost, g["X"], g["F"],
@@ -565,7 +572,7 @@ class Stack:
         grads = [None] * len(self.layers)
         for l in range(len(self.layers) - 1, -1, -1):
             sub = self.layers[l]
-            g = sub.backward_post(X, dX, self.F[l], stream)
+            g = sub.backward_post(X, dX, self.F[l], stream, in_place=True)   # dX is the sweep's own buffer
             d_input = fn_bwds[l](g["F"])
             g = sub.backward_pre(X, d_input, g, stream)
             grads[l] = g

@@ -118,3 +118,26 @@ def test_full_size_state_gradient_on_sampled_tokens(N):
                                inp["G_in"][tg].cpu(), m=w.m, k=w.k, Kr=w.Kr, S=w.S, kappa=w.kappa, tokens=tok)
     same = (sub.idx[tg].cpu().long() == ref["idx"]).all(1)
     assert_bf16_close(g["X"][tg].cpu()[same], ref["X"][same], "dX (sampled tokens)")
+
+
+@pytest.mark.parametrize("Kr", [1, 4])
+def test_post_backward_in_place_matches_out_of_place(Kr):
+    """xhc_post_bwd with dX == dXn (sparse form): the active rows get the same
+    bits as with a separate dX, the untouched rows keep dXn as it was, and every
+    other output is the same."""
+    w = W(T=160, S=80, N=16, k=4, m=2, C=512, Kr=Kr, name=f"inplace-Kr{Kr}")
+    print(f"[bwd-inplace] {w.name}", flush=True)
+    inp = synth.sublayer_inputs(w, 14, device="cuda", grads=True)
+    sub = X.TrainableSublayer(X.dims_for(w), inp, "cuda")
+    state = inp["X"].clone()
+    sub.forward(state, inp["F"])
+    after = state.clone()
+    a = sub.backward_post(state, inp["G_X"], inp["F"])
+    state.copy_(after)
+    dxn = inp["G_X"].clone()
+    b = sub.backward_post(state, dxn, inp["F"], in_place=True)
+    torch.cuda.synchronize()
+    assert b["X"].data_ptr() == dxn.data_ptr()
+    for n in a:
+        if a[n] is not None:
+            assert torch.equal(a[n], b[n]), n

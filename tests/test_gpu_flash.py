@@ -90,6 +90,8 @@ def _check(w, Q, d, g, states, tokens=None):
     W(T=96, S=48, N=16, k=4, m=2, C=256, Kr=4, router="softmax", name="flash-softmax"),
     W(T=64, S=32, N=8, k=4, m=2, C=256, Kr=4, gram_schmidt=0, name="flash-gs-off"),
     W(T=64, S=32, N=8, k=4, m=2, C=256, Kr=4, state="f32", name="flash-f32"),
+    # attention-side temporal augmentation (ablation): every sublayer has K_r components
+    W(T=96, S=48, N=16, k=4, m=2, C=256, Kr=4, attn_aug=1, name="flash-attn-aug"),
 ], ids=lambda w: w.name)
 def test_flash_group_matches_oracle(w, Q):
     print(f"[flash] {w.name} Q={Q}", flush=True)

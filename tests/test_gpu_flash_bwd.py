@@ -76,6 +76,9 @@ CASES = [
     # per-pre-map entry passes
     (W(T=48, S=24, N=8, k=4, m=2, C=256, Kr=4, state="f32", name="fbwd-Q4-N8-f32"), 4, 0.0),
     (W(T=40, S=20, N=16, k=4, m=2, C=256, Kr=4, state="f32", name="fbwd-Q2-N16-f32"), 2, 0.0),
+    # attention-side temporal augmentation (ablation)
+    (W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, attn_aug=1, name="fbwd-Q4-attn-aug"), 4, 0.0),
+    (W(T=48, S=24, N=8, k=4, m=2, C=256, Kr=4, attn_aug=1, name="fbwd-Q2-attn-aug"), 2, 0.0),
 ]
 
 

@@ -142,6 +142,18 @@ def test_full_size_sampled_tokens(w, impl):
     check_sublayer(sub, inp, w, before[tg], after[tg], tokens=tok)
 
 
+@pytest.mark.parametrize("Kr", [1, 4])
+def test_prefill_shape_every_token(Kr):
+    """The prefill-latency regime: one 2048-token sequence at C = 4096, N = 16,
+    k = 4, in the launch configuration the prefill bench section uses (AUTO),
+    every output of every token compared."""
+    w = W(T=2048, S=2048, N=16, k=4, m=2, C=4096, Kr=Kr, name=f"prefill-T2048-C4096-Kr{Kr}")
+    print(f"[parity-prefill] {w.name}", flush=True)
+    inp, sub, before, after = _run(w, seed=12 + Kr)
+    check_sublayer(sub, inp, w, before, after)
+    assert sub.pre_failures() == 0
+
+
 def test_fused_and_multi_routing_differs_only_at_near_ties():
     """Both implementations rank by the same total order but sum the logits in
     different fixed orders (fp32), so their routing may differ only where the

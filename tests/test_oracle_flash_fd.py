@@ -11,9 +11,9 @@ from paper_2607_14530_amd import synth
 F64 = torch.float64
 
 
-def _setup(Q, N, stress, seed, router="sigmoid"):
+def _setup(Q, N, stress, seed, router="sigmoid", attn_aug=0):
     w = synth.Workload(T=8, S=8, N=N, k=4, m=2, C=32, Kr=4,
-                       alpha=(0.5, 1.0, 0.5) if stress else (0.01, 0.01, 0.01), router=router)
+                       alpha=(0.5, 1.0, 0.5) if stress else (0.01, 0.01, 0.01), router=router, attn_aug=attn_aug)
     d = synth.flash_inputs(w, Q, seed, grads=True, bias_std=2.0 if stress else 0.0)
     vals = O.flash_leaves(d["X"], d["F_list"], d["conv_w_list"], d["W_r"], d["W_pre_list"], d["W_post_list"],
                           d["W_res"], d["alpha_pre"], d["b_pre"], d["alpha_post"], d["b_post"], d["alpha_res"],
@@ -33,11 +33,16 @@ def _probes(vals):
             yield name, None
 
 
-@pytest.mark.parametrize("Q,N,stress,seed,router", [(2, 8, False, 0, "sigmoid"), (4, 8, False, 1, "sigmoid"),
-                                                     (2, 4, False, 2, "sigmoid"), (4, 8, True, 3, "sigmoid"),
-                                                     (2, 8, True, 4, "softmax")])
-def test_flash_backward_matches_central_differences(Q, N, stress, seed, router):
-    w, d, vals, kw = _setup(Q, N, stress, seed, router)
+@pytest.mark.parametrize("Q,N,stress,seed,router,attn_aug", [(2, 8, False, 0, "sigmoid", 0),
+                                                              (4, 8, False, 1, "sigmoid", 0),
+                                                              (2, 4, False, 2, "sigmoid", 0),
+                                                              (4, 8, True, 3, "sigmoid", 0),
+                                                              (2, 8, True, 4, "softmax", 0),
+                                                              (4, 8, False, 5, "sigmoid", 1)])
+def test_flash_backward_matches_central_differences(Q, N, stress, seed, router, attn_aug):
+    w, d, vals, kw = _setup(Q, N, stress, seed, router, attn_aug)
+    if attn_aug:   # the attention-side augmentation: every sublayer has K_r components
+        assert all(c is not None for c in d["conv_w_list"])
     g, fwd, _ = O.flash_group_grads(vals, d["G_X"], d["G_in_list"], **kw)
     gen = torch.Generator().manual_seed(200 + seed)
     for name, i in _probes(vals):
