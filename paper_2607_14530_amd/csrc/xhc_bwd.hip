@@ -555,6 +555,122 @@ __global__ __launch_bounds__(256) void k_bwd_convw(const float* __restrict__ de,
   reinterpret_cast<float4*>(dst)[1] = make_float4(acc[4], acc[5], acc[6], acc[7]);
 }
 
+// The conv reverse for the paper's branches (kappa = 4, 8, 12; K_r = 4) in
+// one pass over a run of kConvRun tokens, one channel per thread:
+//   dF[v] = de_0[v] + sum_j sum_{i < kappa_j} w_j[i] de_j[v + i]   (inside v's sequence)
+//   part[run][row (j, i)][c] = sum_{u in run} F[u - i] de_j[u]     (F = 0 before the sequence start)
+// Registers keep the last 12 F values of the channel (for the tap
+// gradients) and the pending dF of the last 12 tokens, into which de_j[u]
+// is scattered (the anti-causal sum in scatter form); a token's dF is stored
+// once the window has moved 12 past it, or at a sequence start, or at the
+// end.  The run reads 11 tokens of de past its end (the last tokens' dF
+// needs them).  Loads of the next 4 tokens are in flight while 4 are used.
+constexpr int kConvRun = 128;
+constexpr int kConvRows = 24;   // 4 + 8 + 12 taps
+template <typename TS>
+__device__ __forceinline__ float ld_scalar(const TS* p);
+template <> __device__ __forceinline__ float ld_scalar<uint16_t>(const uint16_t* p) { return __uint_as_float((uint32_t)*p << 16); }
+template <> __device__ __forceinline__ float ld_scalar<float>(const float* p) { return *p; }
+template <typename TS>
+__device__ __forceinline__ void st_scalar(TS* p, float v);
+template <> __device__ __forceinline__ void st_scalar<uint16_t>(uint16_t* p, float v) { *p = (uint16_t)f2bf(v); }
+template <> __device__ __forceinline__ void st_scalar<float>(float* p, float v) { *p = v; }
+
+template <typename TS>
+__global__ __launch_bounds__(256) void k_bwd_conv_run(const float* __restrict__ de, const TS* __restrict__ F, int64_t T,
+                                                      int64_t S, int C, const float* __restrict__ conv_w,
+                                                      TS* __restrict__ dF, float* __restrict__ part) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= C) return;
+  const int64_t t0 = (int64_t)blockIdx.y * kConvRun;
+  const int64_t t1 = t0 + kConvRun < T ? t0 + kConvRun : T;
+  const int64_t uend = t1 + 11 < T ? t1 + 11 : T;
+  float w[kConvRows];
+#pragma unroll
+  for (int r = 0; r < kConvRows; ++r) w[r] = conv_w[(int64_t)r * C + c];
+  float fw[12], acc[kConvRows], P[12];
+  int64_t seq0 = t0 - t0 % S;   // start of the current sequence
+#pragma unroll
+  for (int i = 0; i < 12; ++i) {
+    const int64_t t = t0 - i;   // fw[i] = F[u - i] for u = t0 - 1 + 1 after the first shift
+    fw[i] = (i > 0 && t >= seq0) ? ld_scalar<TS>(F + t * C + c) : 0.f;
+    P[i] = 0.f;
+  }
+#pragma unroll
+  for (int r = 0; r < kConvRows; ++r) acc[r] = 0.f;
+  // fw holds F[t0 - 1 - i] at index i + 1 for the first token: shift it down once
+#pragma unroll
+  for (int i = 0; i < 11; ++i) fw[i] = fw[i + 1];
+  fw[11] = 0.f;
+  auto store = [&](int64_t v, float x) {
+    if (v >= t0 && v < t1 && v >= seq0) st_scalar<TS>(dF + v * C + c, x);
+  };
+  // loads of one token: de_0..3 and F
+  auto load = [&](int64_t u, float (&d)[4], float& f) {
+    if (u < uend) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) d[j] = de[((int64_t)j * T + u) * C + c];
+      f = u < t1 ? ld_scalar<TS>(F + u * C + c) : 0.f;
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) d[j] = 0.f;
+      f = 0.f;
+    }
+  };
+  float bd[2][4][4], bf[2][4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) load(t0 + k, bd[0][k], bf[0][k]);
+  bool done = false;
+  for (int64_t ub = t0; ub < uend && !done; ub += 8) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int cur = half, nxt = half ^ 1;
+      const int64_t u4 = ub + 4 * half;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) load(u4 + 4 + k, bd[nxt][k], bf[nxt][k]);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int64_t u = u4 + k;
+        if (done || u >= uend) break;
+        if (u % S == 0 && u > t0) {
+          // a sequence starts at u: the tokens before it are complete
+#pragma unroll
+          for (int i = 0; i < 12; ++i) store(u - 1 - i, P[i]);
+          if (u >= t1) { done = true; break; }
+          seq0 = u;
+#pragma unroll
+          for (int i = 0; i < 12; ++i) { P[i] = 0.f; fw[i] = 0.f; }
+        }
+        // token u - 12 has all its contributions
+        store(u - 12, P[11]);
+#pragma unroll
+        for (int i = 11; i > 0; --i) { P[i] = P[i - 1]; fw[i] = fw[i - 1]; }
+        fw[0] = bf[cur][k];
+        const float* d = bd[cur][k];
+        P[0] = d[0];
+        int r = 0;
+#pragma unroll
+        for (int j = 1; j < 4; ++j) {
+          const int kap = j == 1 ? 4 : (j == 2 ? 8 : 12);
+#pragma unroll
+          for (int i = 0; i < kap; ++i, ++r) {
+            P[i] = fmaf(w[r], d[j], P[i]);
+            if (u < t1) acc[r] = fmaf(fw[i], d[j], acc[r]);
+          }
+        }
+      }
+    }
+  }
+  if (!done) {
+    // the tokens still pending: u - 1 - i for the last u + 1 = uend
+#pragma unroll
+    for (int i = 0; i < 12; ++i) store(uend - 1 - i, P[i]);
+  }
+  float* dst = part + (int64_t)blockIdx.y * kConvRows * C + c;
+#pragma unroll
+  for (int r = 0; r < kConvRows; ++r) dst[(int64_t)r * C] = acc[r];
+}
+
 // out[col] = sum_r in[r][col] over nrows rows (row stride = ncols), fixed order.
 __global__ __launch_bounds__(256) void k_colsum_rows(const float* __restrict__ in, int64_t nrows, int64_t ncols,
                                                      float* __restrict__ out) {
@@ -1302,6 +1418,11 @@ __global__ __launch_bounds__(256) void k_colsum_rows_corr(const float* __restric
 
 // ------------------------------------------------------------ launchers
 
+// the one-pass conv reverse applies to the paper's branches
+static bool conv_run_ok(const xhc_dims* d) {
+  return d->Kr == 4 && d->kappa[0] == 4 && d->kappa[1] == 8 && d->kappa[2] == 12;
+}
+
 #define XHC_TS_DISPATCH(dt, ...) \
   if ((dt) == XHC_BF16) { using TS = uint16_t; __VA_ARGS__; } else { using TS = float; __VA_ARGS__; }
 
@@ -1343,6 +1464,16 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
 #undef XHC_BWD_POST
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || Kr == 1) return e;
+  if (conv_run_ok(d)) {
+    // dF and the tap gradients in one pass over de (the paper's branches)
+    const int64_t nruns = (T + kConvRun - 1) / kConvRun;
+    XHC_TS_DISPATCH(d->state_dtype,
+      k_bwd_conv_run<TS><<<dim3((unsigned)((C + 255) / 256), (unsigned)nruns), dim3(256), 0, s>>>(
+          de, reinterpret_cast<const TS*>(F), T, S, C, conv_w, reinterpret_cast<TS*>(dF), cpart));
+    const int64_t ncols = (int64_t)kConvRows * C;
+    k_colsum_rows<<<dim3((unsigned)((ncols + 255) / 256)), dim3(256), 0, s>>>(cpart, nruns, ncols, dconv_w);
+    return hipGetLastError();
+  }
   XHC_TS_DISPATCH(d->state_dtype,
     k_bwd_conv<TS><<<grid, dim3(256), 0, s>>>(de, T, S, C, Kr, kap[0], kap[1], kap[2], conv_w,
                                               reinterpret_cast<TS*>(dF)));
@@ -1366,7 +1497,9 @@ size_t bwd_post_ws_bytes(const xhc_dims* d) {
   if (Kr > 1) {
     int nrows = 0;
     for (int j = 0; j < Kr - 1; ++j) nrows += d->kappa[j];
-    n += (size_t)Kr * T * C + (size_t)((T + kConvChunk - 1) / kConvChunk) * nrows * C;
+    const size_t chunked = (size_t)((T + kConvChunk - 1) / kConvChunk) * nrows * C;
+    const size_t runs = conv_run_ok(d) ? (size_t)((T + kConvRun - 1) / kConvRun) * kConvRows * C : 0;
+    n += (size_t)Kr * T * C + (chunked > runs ? chunked : runs);
   }
   return n * sizeof(float) + 256;
 }

@@ -565,14 +565,18 @@ class Stack:
         xhc_stream_sum(d0, X, out, stream)
         return out
 
-    def backward(self, X, d_out, fn_bwds, stream=None):
+    def backward(self, X, d_out, fn_bwds, stream=None, in_place=True):
+        """With in_place (default) the state gradient runs through one buffer
+        (each xhc_post_bwd rewrites only the active rows): every layer's
+        grads[l]["X"] is that buffer, holding dL/dX of the entry state at the
+        end.  in_place=False keeps each layer's dL/dX in its own tensor."""
         d0 = self.layers[0].d
         dX = torch.empty_like(X)
         xhc_stream_sum_bwd(d0, d_out, dX, False, stream)
         grads = [None] * len(self.layers)
         for l in range(len(self.layers) - 1, -1, -1):
             sub = self.layers[l]
-            g = sub.backward_post(X, dX, self.F[l], stream, in_place=True)   # dX is the sweep's own buffer
+            g = sub.backward_post(X, dX, self.F[l], stream, in_place=in_place)
             d_input = fn_bwds[l](g["F"])
             g = sub.backward_pre(X, d_input, g, stream)
             grads[l] = g

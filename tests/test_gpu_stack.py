@@ -73,7 +73,7 @@ def test_stack_matches_oracle():
     stack = X.Stack(subs)
     out = stack.forward(state, fns)
     X_final = state.clone()
-    grads, dX0 = stack.backward(state, G, fn_bwds)
+    grads, dX0 = stack.backward(state, G, fn_bwds, in_place=False)   # each layer's dL/dX kept
     torch.cuda.synchronize()
     c = lambda v: None if v is None else v.detach().cpu()
     # the chain
@@ -112,3 +112,32 @@ def test_stack_matches_oracle():
                 # the fp32 weight gradients keep 2e-3
                 frob = 2.0 ** -7 if n in ("X", "F") else 2e-3
                 assert_grad_close(grads[l][n].reshape(ref[n].shape), ref[n], f"layer {l} d{n}", frob=frob)
+
+
+def test_stack_in_place_sweep_gives_the_same_gradients():
+    """The reverse sweep with one state-gradient buffer (in place) gives the
+    same entry-state and weight gradients, bit for bit, as with a tensor per
+    layer."""
+    T, S, N, k, m, C = 64, 32, 8, 4, 2, 256
+    res = []
+    for in_place in (False, True):
+        subs, fns, fn_bwds = [], [], []
+        for l, Kr in enumerate((1, 4)):
+            w = W(T=T, S=S, N=N, k=k, m=m, C=C, Kr=Kr, alpha=(0.1, 0.5, 0.1), name=f"stack-ip-{l}")
+            inp = synth.sublayer_inputs(w, 80 + l, device="cuda", grads=True)
+            if l == 0:
+                state = inp["X"].clone()
+            subs.append(X.TrainableSublayer(X.dims_for(w), inp, "cuda"))
+            Wg = (torch.randn(C, C, generator=torch.Generator().manual_seed(90 + l)) / C ** 0.5).cuda()
+            fns.append(lambda x, Wg=Wg: (x.float() @ Wg).to(torch.bfloat16))
+            fn_bwds.append(lambda g, Wg=Wg: (g.float() @ Wg.t().contiguous()).to(torch.bfloat16))
+        G = torch.randn(T, C, generator=torch.Generator().manual_seed(95)).to(torch.bfloat16).cuda()
+        stack = X.Stack(subs)
+        stack.forward(state, fns)
+        grads, dX0 = stack.backward(state, G, fn_bwds, in_place=in_place)
+        torch.cuda.synchronize()
+        res.append((dX0.clone(), [{n: v.clone() for n, v in g.items() if v is not None and n != "X"} for g in grads]))
+    assert torch.equal(res[0][0], res[1][0])
+    for ga, gb in zip(res[0][1], res[1][1]):
+        for n in ga:
+            assert torch.equal(ga[n], gb[n]), n
