@@ -172,7 +172,7 @@ xhc_dims dims_rows32(const xhc_dims* d, int Kq) {
 }
 
 struct FlashPostBwdWs {
-  size_t post, pre, part, sums, idx_id, hres_id, hsel, da_out, xact32, f32c, df32, dhpost, dhres, dp,
+  size_t post, pre, part, sums, idx_id, hres_id, hsel, da_out, dhpost, dhres, dp,
       saved, hpost_re, hres_re, w0, colsum0, wres0, bres0, alpha2, dwr, dwpre, dbpre, dwres, dbres, dalpha2, total;
 };
 
@@ -192,9 +192,6 @@ FlashPostBwdWs flash_post_bwd_ws(const xhc_dims* d, int Q, int q) {
   w.hres_id = c.take((size_t)T * k * k * f);
   w.hsel = c.take((size_t)T * k * f);
   w.da_out = c.take((size_t)T * kC * f);
-  w.xact32 = c.take((size_t)T * kC * f);
-  w.f32c = c.take((size_t)T * C * f);
-  w.df32 = c.take((size_t)T * C * f);
   w.dhpost = c.take((size_t)T * k * Kq * f);
   w.dhres = c.take((size_t)T * k * k * f);
   w.dp = c.take((size_t)T * k * f);
@@ -656,7 +653,7 @@ xhc_status xhc_post_bwd(const xhc_dims* d, const void* dXn, void* X, const void*
   clear_stale_error();
   hipError_t e = hipSuccess;
   XHC_STEP("post_bwd", launch_bwd_post(d, dXn, X, Xact, F, conv_w, idx, p, Hres, Hpost, dX, dF, dHres, dHpost, dp,
-                                       dconv_w, reinterpret_cast<char*>(workspace), s));
+                                       dconv_w, reinterpret_cast<char*>(workspace), s, /*grad_f32=*/false));
   return hip_status(e);
 }
 
@@ -746,16 +743,16 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   XHC_STEP("fbwd_token", launch_fbwd_token(d->state_dtype, T, d->N, (int)k, (int)C, idx, Hpre_q, d_input, Xact,
                                            idx_id, last ? nullptr : F32(w.hres_id), F32(w.hsel), dHpre_act, s));
   if (last) XHC_STEP("fbwd_gather", launch_fbwd_gather(d->state_dtype, T, d->N, (int)k, (int)C, idx, dXn, dA, s));
-  XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, Xact, F32(w.xact32), T * kC, s));
-  XHC_STEP("fbwd_cvt", launch_fbwd_to_f32(d->state_dtype, F, F32(w.f32c), T * C, s));
-  // write-back reverse on the active rows: dF, dH^post, dp and the mixing transpose
-  // (in place for a bf16 state: each thread reads all k incoming rows of its
-  // chunk before it writes the outgoing ones)
+  // write-back reverse on the active rows: dF, dH^post, dp and the mixing
+  // transpose, reading the saved rows and F in the state dtype, the fp32
+  // active-row gradient, and writing dF in the state dtype (in place for a
+  // bf16 state: each thread reads all k incoming rows of its chunk before it
+  // writes the outgoing ones)
   float* const dA_out = fold_read ? dA : F32(w.da_out);
-  XHC_STEP("fbwd_post", launch_bwd_post(&r, dA, nullptr, F32(w.xact32), F32(w.f32c), conv_w, idx_id, p,
-                                        hres_use, Hpost, dA_out, F32(w.df32), F32(w.dhres), F32(w.dhpost),
-                                        F32(w.dp), dconv_w, ws + w.post, s));
-  XHC_STEP("fbwd_cvt", launch_fbwd_from_f32(d->state_dtype, F32(w.df32), dF, T * C, s));
+  const xhc_dims rs = dims_rows(d, Kq);
+  XHC_STEP("fbwd_post", launch_bwd_post(&rs, dA, nullptr, Xact, F, conv_w, idx_id, p, hres_use, Hpost, dA_out,
+                                        dF, F32(w.dhres), F32(w.dhpost), F32(w.dp), dconv_w, ws + w.post, s,
+                                        /*grad_f32=*/true));
   XHC_STEP("fbwd_dp", launch_fbwd_add(dp, F32(w.dp), T * k, s));
   if (!last) XHC_STEP("fbwd_zero", launch_fill0(ws + w.dhres, (size_t)T * k * k * sizeof(float), s));
   // the mapping logits of sublayer q recomputed from a^(q-1) (same kernels and
@@ -772,7 +769,9 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   XHC_STEP("fbwd_alpha", launch_fbwd_alpha(nullptr, alpha_res, alpha_post, F32(w.alpha2), s));
   // mapping reverse through a^(q-1) (its dense-row terms are all zero here:
   // no router or pre-map weights)
-  XHC_STEP("fbwd_pre", launch_bwd_pre(&r, F32(w.xact32), F32(w.colsum0), F32(w.w0), F32(w.w0),
+  // (the fp32 view's own row pass reads Xact only for an fp32 state; a bf16
+  // state goes through the MFMA pass on Xact as saved)
+  XHC_STEP("fbwd_pre", launch_bwd_pre(&r, Xact, F32(w.colsum0), F32(w.w0), F32(w.w0),
                                       last ? W_res : F32(w.wres0), W_post, F32(w.alpha2),
                                       last ? b_res : F32(w.bres0), F32(w.saved), idx_id, p, F32(w.hsel), Hpost,
                                       nullptr, F32(w.dhres), F32(w.dhpost), F32(w.dp), dA_out,

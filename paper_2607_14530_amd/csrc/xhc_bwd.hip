@@ -259,8 +259,10 @@ struct PostDots {
   static __host__ __device__ constexpr int gram(int p) { return KM * KM + KM * KR + p; }
 };
 
-template <typename TS, int KR, int KM>
-__global__ __launch_bounds__(256) void k_bwd_post_dots(const TS* __restrict__ dXn, const TS* __restrict__ Xact,
+// TS: element type of the state tensors (Xact, F); TG: of the state
+// gradient (dXn), fp32 for the xHC-Flash active-row gradient
+template <typename TS, typename TG, int KR, int KM>
+__global__ __launch_bounds__(256) void k_bwd_post_dots(const TG* __restrict__ dXn, const TS* __restrict__ Xact,
                                                        const TS* __restrict__ F, int64_t T, int64_t S, int N, int C,
                                                        int k, int kap0, int kap1, int kap2,
                                                        const float* __restrict__ conv_w,
@@ -285,7 +287,7 @@ __global__ __launch_bounds__(256) void k_bwd_post_dots(const TS* __restrict__ dX
 #pragma unroll
       for (int q = 0; q < 8; ++q) { dy[j][q] = 0.f; a[j][q] = 0.f; }
       if (j < k) {
-        Vec8<TS>::load(dXn + (t * N + idx[t * k + j]) * (int64_t)C + c, dy[j]);
+        Vec8<TG>::load(dXn + (t * N + idx[t * k + j]) * (int64_t)C + c, dy[j]);
         Vec8<TS>::load(Xact + (t * k + j) * (int64_t)C + c, a[j]);
       }
     }
@@ -399,15 +401,16 @@ __global__ __launch_bounds__(128) void k_bwd_post_token(const float* __restrict_
 // Element pass of the post backward (8 channels of one token per thread).
 // dX may be dXn itself (in place): a thread reads the k active rows of its
 // chunk before it writes any, and the untouched rows then already hold their
-// gradient, so they are not copied.
-template <typename TS, int KR, int KM>
-__global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* dXn, TS* __restrict__ X,
+// gradient, so they are not copied.  TS: state tensors (X, Xact, F, dF);
+// TG: the state gradient (dXn, dX).
+template <typename TS, typename TG, int KR, int KM>
+__global__ __launch_bounds__(256) void k_bwd_post_elem(const TG* dXn, TS* __restrict__ X,
                                                        const TS* __restrict__ Xact, const TS* __restrict__ F,
                                                        int64_t T, int64_t S, int N, int C, int k, int kap0, int kap1,
                                                        int kap2, const float* __restrict__ conv_w,
                                                        const int32_t* __restrict__ idx,
                                                        const float* __restrict__ Hres,
-                                                       const float* __restrict__ coef, TS* dX,
+                                                       const float* __restrict__ coef, TG* dX,
                                                        TS* __restrict__ dF, float* __restrict__ de) {
   const int64_t ncb = post_chunks(C);
   const int64_t t = blockIdx.x / ncb;
@@ -423,15 +426,15 @@ __global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* dXn, TS* __rest
   for (int i = 0; i < N && dX != dXn; ++i) {
     if ((act >> i) & 1ull) continue;
     float g[8];
-    Vec8<TS>::load(dXn + (t * N + i) * (int64_t)C + c, g);
-    Vec8<TS>::store(dX + (t * N + i) * (int64_t)C + c, g);
+    Vec8<TG>::load(dXn + (t * N + i) * (int64_t)C + c, g);
+    Vec8<TG>::store(dX + (t * N + i) * (int64_t)C + c, g);
   }
   float dy[KM][8];
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) dy[j][q] = 0.f;
-    if (j < k) Vec8<TS>::load(dXn + (t * N + rows[j]) * (int64_t)C + c, dy[j]);
+    if (j < k) Vec8<TG>::load(dXn + (t * N + rows[j]) * (int64_t)C + c, dy[j]);
   }
   // active rows: mixing gradient sum_j H^res[j][l] dY_j; restore the pre-update rows
   for (int l = 0; l < k; ++l) {
@@ -446,7 +449,7 @@ __global__ __launch_bounds__(256) void k_bwd_post_elem(const TS* dXn, TS* __rest
         for (int q = 0; q < 8; ++q) g[q] = fmaf(h, dy[j][q], g[q]);
       }
     }
-    Vec8<TS>::store(dX + (t * N + rows[l]) * (int64_t)C + c, g);
+    Vec8<TG>::store(dX + (t * N + rows[l]) * (int64_t)C + c, g);
     if (X) {   // restore the pre-update rows (left out when X is null)
       float a[8];
       Vec8<TS>::load(Xact + (t * k + l) * (int64_t)C + c, a);
@@ -1429,7 +1432,7 @@ static bool conv_run_ok(const xhc_dims* d) {
 hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const void* Xact, const void* F,
                            const float* conv_w, const int32_t* idx, const float* p, const float* Hres,
                            const float* Hpost, void* dX, void* dF, float* dHres, float* dHpost, float* dp,
-                           float* dconv_w, char* ws, hipStream_t s) {
+                           float* dconv_w, char* ws, hipStream_t s, bool grad_f32) {
   const int64_t T = d->T, S = d->S;
   const int N = d->N, C = d->C, k = d->k, Kr = d->Kr;
   const int64_t ncb = post_chunks(C);
@@ -1442,17 +1445,19 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
   float* de = coef + T * (Kr * kMaxK + Kr * Kr);
   float* cpart = de + (Kr > 1 ? (int64_t)Kr * T * C : 0);
   const int* kap = d->kappa;
-#define XHC_BWD_POST(KRV, KMV)                                                                                   \
-  XHC_TS_DISPATCH(d->state_dtype,                                                                                \
-    k_bwd_post_dots<TS, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(dXn),                  \
+#define XHC_BWD_POST_TG(KRV, KMV)                                                                                \
+    k_bwd_post_dots<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),              \
         reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, kap[0], kap[1], kap[2], \
         conv_w, idx, part);                                                                                      \
     k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, ncb, T, k,               \
         d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                                     \
-    k_bwd_post_elem<TS, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TS*>(dXn),                  \
+    k_bwd_post_elem<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),              \
         reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, \
-        k, kap[0], kap[1], kap[2], conv_w, idx, Hres, coef, reinterpret_cast<TS*>(dX), reinterpret_cast<TS*>(dF), \
-        de))
+        k, kap[0], kap[1], kap[2], conv_w, idx, Hres, coef, reinterpret_cast<TG*>(dX), reinterpret_cast<TS*>(dF), \
+        de)
+#define XHC_BWD_POST(KRV, KMV)                                                                                   \
+  XHC_TS_DISPATCH(d->state_dtype,                                                                                \
+    if (grad_f32) { using TG = float; XHC_BWD_POST_TG(KRV, KMV); } else { using TG = TS; XHC_BWD_POST_TG(KRV, KMV); })
 #define XHC_BWD_POST_K(KRV) if (k <= 4) { XHC_BWD_POST(KRV, 4); } else { XHC_BWD_POST(KRV, 8); }
   switch (Kr) {
     case 1: XHC_BWD_POST_K(1); break;
@@ -1462,6 +1467,7 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
   }
 #undef XHC_BWD_POST_K
 #undef XHC_BWD_POST
+#undef XHC_BWD_POST_TG
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || Kr == 1) return e;
   if (conv_run_ok(d)) {

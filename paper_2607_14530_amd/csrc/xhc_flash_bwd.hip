@@ -114,24 +114,6 @@ __global__ __launch_bounds__(256) void k_fbwd_scatter(int64_t T, int N, int k, i
   }
 }
 
-// n elements (n % 8 == 0) between the state dtype and fp32
-template <typename TS>
-__global__ __launch_bounds__(256) void k_fbwd_to_f32(const TS* __restrict__ src, float* __restrict__ dst, int64_t n) {
-  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
-  if (i >= n) return;
-  float f[8];
-  Vec8<TS>::load(src + i, f);
-  Vec8<float>::store(dst + i, f);
-}
-template <typename TS>
-__global__ __launch_bounds__(256) void k_fbwd_from_f32(const float* __restrict__ src, TS* __restrict__ dst, int64_t n) {
-  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 8;
-  if (i >= n) return;
-  float f[8];
-  Vec8<float>::load(src + i, f);
-  Vec8<TS>::store(dst + i, f);
-}
-
 // Hm[t, i] = 0 for the active streams of token t, Hpre[t, i] otherwise
 __global__ __launch_bounds__(256) void k_fbwd_mask(int64_t T, int N, int k, const int32_t* __restrict__ idx,
                                                    const float* __restrict__ Hpre, float* __restrict__ Hm) {
@@ -220,20 +202,6 @@ hipError_t launch_fbwd_scatter(int state_dtype, int64_t T, int N, int k, int C, 
                                const float* da0, void* dX, hipStream_t s) {
   XHC_FTS(state_dtype, k_fbwd_scatter<TS><<<dim3((unsigned)(T * N)), dim3(256), 0, s>>>(
                            T, N, k, C, idx, reinterpret_cast<const TS*>(GX), da0, reinterpret_cast<TS*>(dX)));
-  return hipGetLastError();
-}
-
-hipError_t launch_fbwd_to_f32(int state_dtype, const void* src, float* dst, int64_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  XHC_FTS(state_dtype, k_fbwd_to_f32<TS><<<dim3(blocks_for(n / 8, 256)), dim3(256), 0, s>>>(
-                           reinterpret_cast<const TS*>(src), dst, n));
-  return hipGetLastError();
-}
-
-hipError_t launch_fbwd_from_f32(int state_dtype, const float* src, void* dst, int64_t n, hipStream_t s) {
-  if (n == 0) return hipSuccess;
-  XHC_FTS(state_dtype, k_fbwd_from_f32<TS><<<dim3(blocks_for(n / 8, 256)), dim3(256), 0, s>>>(
-                           src, reinterpret_cast<TS*>(dst), n));
   return hipGetLastError();
 }
 

@@ -119,8 +119,9 @@ hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T,
 hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const void* Xact, const void* F,
                            const float* conv_w, const int32_t* idx, const float* p, const float* Hres,
                            const float* Hpost, void* dX, void* dF, float* dHres, float* dHpost, float* dp,
-                           float* dconv_w, char* ws, hipStream_t s);
-// (X null: the saved rows are not written back into X)
+                           float* dconv_w, char* ws, hipStream_t s, bool grad_f32);
+// (X null: the saved rows are not written back into X; grad_f32: dXn and dX
+// are fp32 whatever the state dtype, as the xHC-Flash active-row gradient)
 size_t bwd_post_ws_bytes(const xhc_dims* d);
 bool bwd_pre_supported(const xhc_dims* d);
 size_t bwd_pre_ws_bytes(const xhc_dims* d);
@@ -182,8 +183,6 @@ hipError_t launch_fbwd_gather(int state_dtype, int64_t T, int N, int k, int C, c
                               float* da, hipStream_t s);
 hipError_t launch_fbwd_scatter(int state_dtype, int64_t T, int N, int k, int C, const int32_t* idx, const void* GX,
                                const float* da0, void* dX, hipStream_t s);
-hipError_t launch_fbwd_to_f32(int state_dtype, const void* src, float* dst, int64_t n, hipStream_t s);
-hipError_t launch_fbwd_from_f32(int state_dtype, const float* src, void* dst, int64_t n, hipStream_t s);
 hipError_t launch_fbwd_mask(int64_t T, int N, int k, const int32_t* idx, const float* Hpre, float* Hm, hipStream_t s);
 hipError_t launch_fbwd_add(float* dst, const float* src, int64_t n, hipStream_t s);
 hipError_t launch_fbwd_alpha(const float* a0, const float* a1, const float* a2, float* out, hipStream_t s);
