@@ -1115,11 +1115,13 @@ __global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, 
   for (int o = 0; o < NAMAX; ++o) dst[o] = ga[o];
 }
 
-// MFMA form of the two row passes above for a bf16 state, N = 16 (full rows)
-// and k * Kr + k * k <= 32 (active rows).  A workgroup takes 64 consecutive
-// weight rows K (wave w: rows 16w .. 16w + 15, inside one stream / slot) and a
-// chunk of tokens, in steps of 32 tokens staged in LDS:
-//   dX[t, K] += sum_o W[K, o] dz'[t, o] + (row terms)   MFMA D[16 K x 16 t], contraction over the 32 outputs
+// MFMA form of the two row passes above for a bf16 state: full rows with
+// 2N <= 32 NOB outputs (N = 4, 8, 16 in one block of 32, N = 32 in two; the
+// padding outputs are zero) and active rows with k * Kr + k * k <= 32.  A
+// workgroup takes RW consecutive weight rows K (wave w: rows 16w .. 16w + 15,
+// inside one stream / slot) and a chunk of tokens, in steps of 32 tokens
+// staged in LDS:
+//   dX[t, K] += sum_o W[K, o] dz'[t, o] + (row terms)   MFMA D[16 K x 16 t], contraction over 32 outputs a block
 //   dW[K, o] += sum_t x[t, K] dz'[t, o]                 MFMA D[16 o x 16 K], contraction over 32 tokens
 // with dz' the per-token scaled logit gradients (full: r_ln dz_r | r dz_pre;
 // active: r_a dz_act), entered as a bf16 pair hi + lo (2^-16 relative).  The
@@ -1177,7 +1179,7 @@ __device__ __forceinline__ void st4(float* p, const float (&d)[4]) {
 // values are bf16 but whose gradient is kept in fp32)
 // ADIN (active rows): din is given and row j gains Hpre[t, j] din[t] (Hpre
 // then [T, k] slot weights)
-template <bool ACT, typename TD = uint16_t, int RW = kMfRows, bool ADIN = false>
+template <bool ACT, typename TD = uint16_t, int RW = kMfRows, bool ADIN = false, int NOB = 1>
 __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __restrict__ X,
                                                        const uint16_t* __restrict__ din, TD* __restrict__ dX,
                                                        const float* __restrict__ Wa, const float* __restrict__ Wb,
@@ -1187,8 +1189,10 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
                                                        int64_t tchunk, float* __restrict__ wpa,
                                                        float* __restrict__ wpb) {
   constexpr int NT = RW * 4, PIECES = RW / 8;   // threads; 16-byte pieces of a staged token row
+  constexpr int NO = 32 * NOB, NOH = 2 * NOB;   // outputs (padded); 16-output tiles of dW
+  static_assert(!ACT || NOB == 1, "active rows: at most 32 outputs");
   __shared__ __align__(16) uint16_t xs[kMfStep][RW + 8];
-  __shared__ float dzs[kMfStep][33];
+  __shared__ float dzs[kMfStep][NO + 1];
   __shared__ float sc[kMfStep][8];
   __shared__ int srow[kMfStep];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -1199,32 +1203,36 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
   const int64_t NK = ACT ? (int64_t)k * C : (int64_t)N * C;   // weight rows
   const int NP = k * Kr;                                       // active: W_post columns
   const int TF = tok_floats(N, NA);
-  // A operand of the dX product: rows K0 + 16 wave + l16, outputs 8 g4 .. + 7, as bf16
-  uint4 wfrag;
-  {
+  // A operand of the dX product: rows K0 + 16 wave + l16, outputs 32 b + 8 g4 .. + 7, as bf16
+  uint4 wfrag[NOB];
+#pragma unroll
+  for (int b = 0; b < NOB; ++b) {
     float f[8];
     const int64_t K = K0 + 16 * wave + l16;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int o = 8 * g4 + e;
+      const int o = 32 * b + 8 * g4 + e;
       float v = 0.f;
       if (ACT) {
         if (o < NP) v = Wa[K * NP + o];
         else if (o < NA) v = Wb[K * (k * k) + (o - NP)];
       } else {
-        v = o < 16 ? Wa[K * 16 + o] : Wb[K * 16 + (o - 16)];
+        if (o < N) v = Wa[K * N + o];
+        else if (o < 2 * N) v = Wb[K * N + (o - N)];
       }
       f[e] = __uint_as_float(f2bf(v) << 16);
     }
-    wfrag = pack8(f);
+    wfrag[b] = pack8(f);
   }
-  f32x4 dw[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  f32x4 dw[NOH];
+#pragma unroll
+  for (int oh = 0; oh < NOH; ++oh) dw[oh] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
   // The inputs of step tb + 32 are fetched into registers while step tb is
   // computed: this thread's dz' values (4), scalars (threads < 32) and 16
   // bytes of the state rows.
   struct Stage {
-    float dz[kMfStep * 32 / NT];
+    float dz[kMfStep * NO / NT];
     float scal[7];
     int row;
     uint4 x;
@@ -1234,14 +1242,15 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
   auto fetch = [&](Stage& st, int64_t tb) {
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
 #pragma unroll
-    for (int r = 0; r < kMfStep * 32 / NT; ++r) {
-      const int q = threadIdx.x + r * NT, u = q / 32, o = q % 32;
+    for (int r = 0; r < kMfStep * NO / NT; ++r) {
+      const int q = threadIdx.x + r * NT, u = q / NO, o = q % NO;
       const int64_t t = tb + (u < nt ? u : 0);
       const float* tk = tok + t * TF;
       float v = 0.f;
       if (u < nt) {
-        if (ACT) v = o < NA ? tk[2 * N + NA + 6] * tk[2 * N + o] : 0.f;                 // r_a dz_act
-        else v = o < 16 ? tk[2 * N + NA + 1] * tk[o] : tk[2 * N + NA + 0] * tk[N + (o - 16)];  // r_ln dz_r | r dz_pre
+        if (ACT) v = o < NA ? tk[2 * N + NA + 6] * tk[2 * N + o] : 0.f;       // r_a dz_act
+        else if (o < N) v = tk[2 * N + NA + 1] * tk[o];                      // r_ln dz_r
+        else if (o < 2 * N) v = tk[2 * N + NA + 0] * tk[o];                  // r dz_pre
       }
       st.dz[r] = v;
     }
@@ -1292,9 +1301,9 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
     __syncthreads();   // the previous step's LDS reads are done
 #pragma unroll
-    for (int r = 0; r < kMfStep * 32 / NT; ++r) {
+    for (int r = 0; r < kMfStep * NO / NT; ++r) {
       const int q = threadIdx.x + r * NT;
-      dzs[q / 32][q % 32] = cur.dz[r];
+      dzs[q / NO][q % NO] = cur.dz[r];
     }
     if (threadIdx.x < kMfStep) {
       srow[threadIdx.x] = cur.row;
@@ -1310,14 +1319,17 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int u = 16 * h + l16;   // B operand token of this lane
-      float f[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) f[e] = dzs[u][8 * g4 + e];
-      uint4 bh, bl;
-      split_bf16x8(f, bh, bl);
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-      acc = mfma_16x16x32(wfrag, bh, acc);
-      acc = mfma_16x16x32(wfrag, bl, acc);
+#pragma unroll
+      for (int b = 0; b < NOB; ++b) {
+        float f[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = dzs[u][32 * b + 8 * g4 + e];
+        uint4 bh, bl;
+        split_bf16x8(f, bh, bl);
+        acc = mfma_16x16x32(wfrag[b], bh, acc);
+        acc = mfma_16x16x32(wfrag[b], bl, acc);
+      }
       // lane holds rows 16 wave + 4 g4 + v of token u
       if (u < nt) {
         const int64_t t = tb + u;
@@ -1356,7 +1368,7 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
       const uint4 bx = make_uint4(xb[0] | ((uint32_t)xb[1] << 16), xb[2] | ((uint32_t)xb[3] << 16),
                                   xb[4] | ((uint32_t)xb[5] << 16), xb[6] | ((uint32_t)xb[7] << 16));
 #pragma unroll
-      for (int oh = 0; oh < 2; ++oh) {
+      for (int oh = 0; oh < NOH; ++oh) {
         float f[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) f[e] = dzs[8 * g4 + e][16 * oh + l16];
@@ -1375,10 +1387,16 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
     for (int oh = 0; oh < 2; ++oh)
       *reinterpret_cast<float4*>(dst + 16 * oh + 4 * g4) = make_float4(dw[oh][0], dw[oh][1], dw[oh][2], dw[oh][3]);
   } else {
-    float* dr = wpa + ((int64_t)blockIdx.y * NK + K) * 16 + 4 * g4;
-    float* dp = wpb + ((int64_t)blockIdx.y * NK + K) * 16 + 4 * g4;
-    *reinterpret_cast<float4*>(dr) = make_float4(dw[0][0], dw[0][1], dw[0][2], dw[0][3]);
-    *reinterpret_cast<float4*>(dp) = make_float4(dw[1][0], dw[1][1], dw[1][2], dw[1][3]);
+    // outputs 16 oh + 4 g4 .. + 3 lie inside one of the two halves (N % 4 == 0)
+#pragma unroll
+    for (int oh = 0; oh < NOH; ++oh) {
+      const int o = 16 * oh + 4 * g4;
+      if (o < 2 * N) {
+        float* dst = (o < N ? wpa + ((int64_t)blockIdx.y * NK + K) * N + o
+                            : wpb + ((int64_t)blockIdx.y * NK + K) * N + (o - N));
+        *reinterpret_cast<float4*>(dst) = make_float4(dw[oh][0], dw[oh][1], dw[oh][2], dw[oh][3]);
+      }
+    }
   }
 }
 
@@ -1834,7 +1852,8 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
   float* const wpart_a = w.wpart_a;
   float* const red_a = w.red_a;
   float* const pgsum = w.pgsum;
-  const bool mf = d->state_dtype == XHC_BF16 && N == 16 && NA <= 32 && C % kMfRows == 0;
+  const bool mf = d->state_dtype == XHC_BF16 && (N == 4 || N == 8 || N == 16 || N == 32) && NA <= 32 &&
+                  C % (2 * kMfRows) == 0;
   hipError_t e = hipSuccess;
   if (phase == kBwdPreReduce) {
     // the row passes ran elsewhere (their partials are in this workspace)
@@ -1873,10 +1892,18 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
       // 128 rows per workgroup (256 contiguous bytes of each state row per
       // token); C % 256 == 0 is part of the backward's supported shapes
       if (dense_rows) {
+        // 2N outputs in one block of 32 (N <= 16) or two (N = 32)
         const dim3 gw((unsigned)((int64_t)N * C / (2 * kMfRows)), (unsigned)nchunk);
-        k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows><<<gw, dim3(8 * kMfRows), 0, s>>>(
-            reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
-            reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_r, wpart_p);
+        if (N == 32)
+          k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows, false, 2><<<gw, dim3(8 * kMfRows), 0, s>>>(
+              reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
+              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_r,
+              wpart_p);
+        else
+          k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows><<<gw, dim3(8 * kMfRows), 0, s>>>(
+              reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
+              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_r,
+              wpart_p);
       }
       // 128 rows per workgroup as for the full rows (C % 256 == 0)
       const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);

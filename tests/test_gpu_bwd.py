@@ -54,6 +54,7 @@ CASES = [
     W(T=48, S=48, N=4, k=4, m=2, C=256, Kr=4, name="bwd-mlp-N4"),
     W(T=40, S=20, N=8, k=4, m=2, C=512, Kr=4, name="bwd-mlp-N8"),
     W(T=32, S=32, N=32, k=4, m=2, C=256, Kr=1, name="bwd-attn-N32"),
+    W(T=40, S=20, N=32, k=4, m=2, C=256, Kr=4, name="bwd-mlp-N32"),
     W(T=64, S=64, N=16, k=4, m=2, C=256, Kr=4, alpha=(0.5, 1.0, 0.5), name="bwd-mlp-stress"),
     W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, router="softmax", name="bwd-mlp-softmax"),
     W(T=40, S=20, N=8, k=4, m=1, C=512, Kr=1, router="softmax", name="bwd-attn-softmax-N8"),
