@@ -191,55 +191,71 @@ __global__ __launch_bounds__(256) void k_post_gram_run(const TS* __restrict__ F,
   cg.load_taps(conv_w, C, c);
   cg.init(F, t0, S, C, c);
   float* mine = &xpose[wave][lane][0];
-  // the rows of the next group are loaded while this group is computed
-  typename Row4<TS>::raw nxt[G];
+  // F rows are loaded PF groups ahead (a lane requests 8 bytes per token of a
+  // bf16 state, so one group in flight would leave the memory system mostly
+  // idle)
+  constexpr int PF = sizeof(TS) == 2 ? 4 : 2;
+  typename Row4<TS>::raw ring[PF][G];
 #pragma unroll
-  for (int g = 0; g < G; ++g) nxt[g] = g < nt ? Row4<TS>::load(F + (t0 + g) * C + c) : Row4<TS>::zero();
-  for (int u0 = 0; u0 < nt; u0 += G) {
-    const int64_t t = t0 + u0;
-    if (t % S == 0) cg.reset();
-    float cur[G][4];
-#pragma unroll
-    for (int g = 0; g < G; ++g) Row4<TS>::unpack(nxt[g], cur[g]);
-#pragma unroll
-    for (int g = 0; g < G; ++g)
-      nxt[g] = u0 + G + g < nt ? Row4<TS>::load(F + (t + G + g) * C + c) : Row4<TS>::zero();
-    float part[NV];
+  for (int f = 0; f < PF; ++f)
 #pragma unroll
     for (int g = 0; g < G; ++g) {
-      float e[KR][4];
-      cg.components(cur, g, e);
-      int pi = 0;
-#pragma unroll
-      for (int a = 0; a < KR; ++a)
-#pragma unroll
-        for (int b = a; b < KR; ++b, ++pi) {
-          float v = 0.f;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) v = fmaf(e[a][q], e[b][q], v);
-          part[g * NP + pi] = v;
-        }
+      const int u = f * G + g;
+      ring[f][g] = u < nt ? Row4<TS>::load(F + (t0 + u) * C + c) : Row4<TS>::zero();
     }
-    cg.advance(cur);
+  for (int u1 = 0; u1 < nt; u1 += PF * G) {
 #pragma unroll
-    for (int v = 0; v < NV; v += 4)
-      *reinterpret_cast<float4*>(mine + v) =
-          make_float4(part[v], v + 1 < NV ? part[v + 1 < NV ? v + 1 : 0] : 0.f,
-                      v + 2 < NV ? part[v + 2 < NV ? v + 2 : 0] : 0.f, v + 3 < NV ? part[v + 3 < NV ? v + 3 : 0] : 0.f);
-    // LDS operations of one wave complete in issue order; the fences keep the
-    // compiler from moving the column reads above the row writes (or the next
-    // group's writes above these reads).
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    if (lane < NV) {
-      float sum = 0.f;
+    for (int f = 0; f < PF; ++f) {
+      const int u0 = u1 + f * G;
+      if (u0 >= nt) break;
+      const int64_t t = t0 + u0;
+      if (t % S == 0) cg.reset();
+      float cur[G][4];
+#pragma unroll
+      for (int g = 0; g < G; ++g) Row4<TS>::unpack(ring[f][g], cur[g]);
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        const int u = u0 + PF * G + g;
+        ring[f][g] = u < nt ? Row4<TS>::load(F + (t0 + u) * C + c) : Row4<TS>::zero();
+      }
+      float part[NV];
+#pragma unroll
+      for (int g = 0; g < G; ++g) {
+        float e[KR][4];
+        cg.components(cur, g, e);
+        int pi = 0;
+#pragma unroll
+        for (int a = 0; a < KR; ++a)
+#pragma unroll
+          for (int b = a; b < KR; ++b, ++pi) {
+            float v = 0.f;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v = fmaf(e[a][q], e[b][q], v);
+            part[g * NP + pi] = v;
+          }
+      }
+      cg.advance(cur);
+#pragma unroll
+      for (int v = 0; v < NV; v += 4)
+        *reinterpret_cast<float4*>(mine + v) =
+            make_float4(part[v], v + 1 < NV ? part[v + 1 < NV ? v + 1 : 0] : 0.f,
+                        v + 2 < NV ? part[v + 2 < NV ? v + 2 : 0] : 0.f,
+                        v + 3 < NV ? part[v + 3 < NV ? v + 3 : 0] : 0.f);
+      // LDS operations of one wave complete in issue order; the fences keep the
+      // compiler from moving the column reads above the row writes (or the next
+      // group's writes above these reads).
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      if (lane < NV) {
+        float sum = 0.f;
 #pragma unroll 16
-      for (int r = 0; r < kWave; ++r) sum += xpose[wave][r][lane];
-      const int g = lane / NP, pi = lane % NP;
-      if (u0 + g < nt) red[u0 + g][wave][pi] = sum;
+        for (int r = 0; r < kWave; ++r) sum += xpose[wave][r][lane];
+        const int g = lane / NP, pi = lane % NP;
+        if (u0 + g < nt) red[u0 + g][wave][pi] = sum;
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      __builtin_amdgcn_wave_barrier();
     }
-    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-    __builtin_amdgcn_wave_barrier();
   }
   __syncthreads();
   for (int i = threadIdx.x; i < nt * NP; i += blockDim.x) {
