@@ -1125,10 +1125,42 @@ __global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, 
 //   dW[K, o] += sum_t x[t, K] dz'[t, o]                 MFMA D[16 o x 16 K], contraction over 32 tokens
 // with dz' the per-token scaled logit gradients (full: r_ln dz_r | r dz_pre;
 // active: r_a dz_act), entered as a bf16 pair hi + lo (2^-16 relative).  The
+// pairs are formed once per token by k_dz_pack, in the two layouts the MFMA
+// operands read (token rows for dX, 32-token transposes for dW).  The
 // full-row dW_r misses the token sum of mu dz'_r, which the reduction removes.
 constexpr int kMfRows = 64;    // weight rows per workgroup
+constexpr int kDzBlock = 32;   // tokens per transposed block of the packed dz' (= kMfStep)
 constexpr int kMfStep = 32;    // tokens per step
 constexpr int kMfXPitch = kMfRows + 8;   // bf16 per staged token row (pad: fewer LDS bank conflicts)
+
+// dz' of the MFMA row passes as bf16 pairs hi + lo (hi the round-to-nearest-
+// even bf16 of the value, lo that of the rest; the packed hardware
+// conversion), NO outputs a token (zero past the used ones and past T):
+//   rows[t][0 .. NO)   hi,  rows[t][NO .. 2 NO)  lo
+//   tr[b][o][u]        the same values of token 32 b + u, row o of 2 NO
+// full rows (act = 0): r_ln dz_r | r dz_pre; active rows: r_a dz_act.
+__global__ __launch_bounds__(256) void k_dz_pack(const float* __restrict__ tok, int64_t T, int N, int NA, int act,
+                                                 int NO, uint16_t* __restrict__ rows, uint16_t* __restrict__ tr) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
+  if (i >= Tp * NO) return;
+  const int64_t t = i / NO;
+  const int o = (int)(i % NO);
+  float v = 0.f;
+  if (t < T) {
+    const float* tk = tok + t * tok_floats(N, NA);
+    if (act) v = o < NA ? tk[2 * N + NA + 6] * tk[2 * N + o] : 0.f;
+    else if (o < N) v = tk[2 * N + NA + 1] * tk[o];
+    else if (o < 2 * N) v = tk[2 * N + NA + 0] * tk[o];
+  }
+  const uint32_t hb = pack2bf(v, 0.f) & 0xFFFFu;
+  const uint32_t lb = pack2bf(v - __uint_as_float(hb << 16), 0.f) & 0xFFFFu;
+  rows[t * 2 * NO + o] = (uint16_t)hb;
+  rows[t * 2 * NO + NO + o] = (uint16_t)lb;
+  uint16_t* blk = tr + (t / kDzBlock) * 2 * NO * kDzBlock;
+  blk[o * kDzBlock + t % kDzBlock] = (uint16_t)hb;
+  blk[(NO + o) * kDzBlock + t % kDzBlock] = (uint16_t)lb;
+}
 
 // f = hi + lo with hi the round-to-nearest-even bf16 of f and lo that of the
 // rest (the packed hardware conversion: the bits of f2bf for finite values)
@@ -1186,13 +1218,19 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
                                                        const float* __restrict__ Hpre,
                                                        const int32_t* __restrict__ idx, const float* __restrict__ tok,
                                                        int64_t T, int N, int k, int C, int Kr, int NA,
-                                                       int64_t tchunk, float* __restrict__ wpa,
-                                                       float* __restrict__ wpb) {
+                                                       int64_t tchunk, const uint16_t* __restrict__ dzp,
+                                                       float* __restrict__ wpa, float* __restrict__ wpb) {
   constexpr int NT = RW * 4, PIECES = RW / 8;   // threads; 16-byte pieces of a staged token row
   constexpr int NO = 32 * NOB, NOH = 2 * NOB;   // outputs (padded); 16-output tiles of dW
+  constexpr int DZP = NO / 32 * 512 / NT;       // 16-byte pieces of packed dz' per thread and step
   static_assert(!ACT || NOB == 1, "active rows: at most 32 outputs");
+  static_assert(kMfStep == kDzBlock && DZP * NT == 16 * NO, "a step copies its packed dz' in whole pieces");
   __shared__ __align__(16) uint16_t xs[kMfStep][RW + 8];
-  __shared__ float dzs[kMfStep][NO + 1];
+  // packed dz' of the step: token rows (hi | lo) and the transpose; the row
+  // pitches (2 NO + 8 and 40 elements) keep the 16-byte operand reads of a
+  // 16-lane group on distinct banks
+  __shared__ __align__(16) uint16_t dzr[kMfStep][2 * NO + 8];
+  __shared__ __align__(16) uint16_t dzt[2 * NO][kMfStep + 8];
   __shared__ float sc[kMfStep][8];
   __shared__ int srow[kMfStep];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -1229,10 +1267,12 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
   for (int oh = 0; oh < NOH; ++oh) dw[oh] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
   // The inputs of step tb + 32 are fetched into registers while step tb is
-  // computed: this thread's dz' values (4), scalars (threads < 32) and 16
-  // bytes of the state rows.
+  // computed: this thread's pieces of the packed dz', scalars (threads < 32)
+  // and 16 bytes of the state rows.
+  const uint16_t* const dzrows = dzp;
+  const uint16_t* const dztr = dzp + (T + kDzBlock - 1) / kDzBlock * kDzBlock * 2 * NO;
   struct Stage {
-    float dz[kMfStep * NO / NT];
+    uint4 dz[DZP];
     float scal[7];
     int row;
     uint4 x;
@@ -1241,18 +1281,19 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
   };
   auto fetch = [&](Stage& st, int64_t tb) {
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
+    // pieces [0, 8 NO): token rows (NO / 4 pieces a token); [8 NO, 16 NO): the
+    // transposed block (4 pieces a row); rows of tokens past the chunk are zero
 #pragma unroll
-    for (int r = 0; r < kMfStep * NO / NT; ++r) {
-      const int q = threadIdx.x + r * NT, u = q / NO, o = q % NO;
-      const int64_t t = tb + (u < nt ? u : 0);
-      const float* tk = tok + t * TF;
-      float v = 0.f;
-      if (u < nt) {
-        if (ACT) v = o < NA ? tk[2 * N + NA + 6] * tk[2 * N + o] : 0.f;       // r_a dz_act
-        else if (o < N) v = tk[2 * N + NA + 1] * tk[o];                      // r_ln dz_r
-        else if (o < 2 * N) v = tk[2 * N + NA + 0] * tk[o];                  // r dz_pre
+    for (int r = 0; r < DZP; ++r) {
+      const int q = threadIdx.x + r * NT;
+      if (q < 8 * NO) {
+        const int u = q / (NO / 4), off = (q % (NO / 4)) * 8;
+        st.dz[r] = u < nt ? *reinterpret_cast<const uint4*>(dzrows + (tb + u) * 2 * NO + off)
+                          : make_uint4(0, 0, 0, 0);
+      } else {
+        const int qq = q - 8 * NO, row = qq / 4, off = (qq % 4) * 8;
+        st.dz[r] = *reinterpret_cast<const uint4*>(dztr + (tb / kDzBlock) * 2 * NO * kDzBlock + row * kDzBlock + off);
       }
-      st.dz[r] = v;
     }
     if (threadIdx.x < kMfStep) {
       const int u = threadIdx.x;
@@ -1301,9 +1342,15 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
     __syncthreads();   // the previous step's LDS reads are done
 #pragma unroll
-    for (int r = 0; r < kMfStep * NO / NT; ++r) {
+    for (int r = 0; r < DZP; ++r) {
       const int q = threadIdx.x + r * NT;
-      dzs[q / NO][q % NO] = cur.dz[r];
+      if (q < 8 * NO) {
+        const int u = q / (NO / 4), off = (q % (NO / 4)) * 8;
+        *reinterpret_cast<uint4*>(&dzr[u][off]) = cur.dz[r];
+      } else {
+        const int qq = q - 8 * NO, row = qq / 4, off = (qq % 4) * 8;
+        *reinterpret_cast<uint4*>(&dzt[row][off]) = cur.dz[r];
+      }
     }
     if (threadIdx.x < kMfStep) {
       srow[threadIdx.x] = cur.row;
@@ -1322,11 +1369,8 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int b = 0; b < NOB; ++b) {
-        float f[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = dzs[u][32 * b + 8 * g4 + e];
-        uint4 bh, bl;
-        split_bf16x8(f, bh, bl);
+        const uint4 bh = *reinterpret_cast<const uint4*>(&dzr[u][32 * b + 8 * g4]);
+        const uint4 bl = *reinterpret_cast<const uint4*>(&dzr[u][NO + 32 * b + 8 * g4]);
         acc = mfma_16x16x32(wfrag[b], bh, acc);
         acc = mfma_16x16x32(wfrag[b], bl, acc);
       }
@@ -1369,11 +1413,8 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
                                   xb[4] | ((uint32_t)xb[5] << 16), xb[6] | ((uint32_t)xb[7] << 16));
 #pragma unroll
       for (int oh = 0; oh < NOH; ++oh) {
-        float f[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = dzs[8 * g4 + e][16 * oh + l16];
-        uint4 ah, al;
-        split_bf16x8(f, ah, al);
+        const uint4 ah = *reinterpret_cast<const uint4*>(&dzt[16 * oh + l16][8 * g4]);
+        const uint4 al = *reinterpret_cast<const uint4*>(&dzt[NO + 16 * oh + l16][8 * g4]);
         dw[oh] = mfma_16x16x32(ah, bx, dw[oh]);
         dw[oh] = mfma_16x16x32(al, bx, dw[oh]);
       }
@@ -1753,6 +1794,12 @@ BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws) {
   w.wpart_a = w.wpart_p + nchunk * (int64_t)N * C * N;
   w.red_a = w.wpart_a + nchunk * (int64_t)k * C * 32;           // [kC][32]
   w.pgsum = w.red_a + (int64_t)k * C * 32;
+  // packed dz' (16-byte aligned): full rows 2 NO_f, active rows 2 x 32 bf16 a
+  // token, in token rows and in transposed 32-token blocks
+  const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
+  const uintptr_t a = reinterpret_cast<uintptr_t>(w.pgsum + pg_floats(N, k, Kr) + N);
+  w.dzf = reinterpret_cast<uint16_t*>((a + 15) / 16 * 16);
+  w.dza = w.dzf + Tp * 2 * (2 * N <= 32 ? 32 : 64) * 2;
   return w;
 }
 
@@ -1821,7 +1868,9 @@ size_t bwd_pre_ws_bytes(const xhc_dims* d) {
   n += (size_t)nchunk * k * C * 32;                              // dW_act partials (<= 32 columns)
   n += (size_t)k * C * 32 + (size_t)pg_floats(N, k, Kr);          // reduced dW_act, reduced gradients
   n += (size_t)N;                                                // token sum of mu dz'_r
-  return n * sizeof(float) + 1024;
+  const size_t Tp = (size_t)((T + kDzBlock - 1) / kDzBlock * kDzBlock);
+  const size_t dz = Tp * 2 * ((2 * N <= 32 ? 32 : 64) + 32) * 2 * sizeof(uint16_t);   // packed dz'
+  return n * sizeof(float) + 16 + dz + 1024;
 }
 
 bool bwd_pre_supported(const xhc_dims* d) {
@@ -1891,26 +1940,34 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     if (mf) {
       // 128 rows per workgroup (256 contiguous bytes of each state row per
       // token); C % 256 == 0 is part of the backward's supported shapes
+      const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
+      const int NOf = 2 * N <= 32 ? 32 : 64;
+      if (dense_rows)
+        k_dz_pack<<<dim3((unsigned)((Tp * NOf + 255) / 256)), dim3(256), 0, s>>>(tok, T, N, NA, 0, NOf, w.dzf,
+                                                                                 w.dzf + Tp * 2 * NOf);
+      if (act_rows)
+        k_dz_pack<<<dim3((unsigned)((Tp * 32 + 255) / 256)), dim3(256), 0, s>>>(tok, T, N, NA, 1, 32, w.dza,
+                                                                                w.dza + Tp * 2 * 32);
       if (dense_rows) {
         // 2N outputs in one block of 32 (N <= 16) or two (N = 32)
         const dim3 gw((unsigned)((int64_t)N * C / (2 * kMfRows)), (unsigned)nchunk);
         if (N == 32)
           k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows, false, 2><<<gw, dim3(8 * kMfRows), 0, s>>>(
               reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
-              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_r,
-              wpart_p);
+              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dzf,
+              wpart_r, wpart_p);
         else
           k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows><<<gw, dim3(8 * kMfRows), 0, s>>>(
               reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
-              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_r,
-              wpart_p);
+              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dzf,
+              wpart_r, wpart_p);
       }
       // 128 rows per workgroup as for the full rows (C % 256 == 0)
       const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
       if (act_rows)
         k_bwd_rows_mfma<true, uint16_t, 2 * kMfRows><<<ga, dim3(8 * kMfRows), 0, s>>>(reinterpret_cast<const uint16_t*>(X), nullptr,
-            reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
-            nullptr);   // (the dense read of the active rows is in the full-row pass)
+            reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dza,
+            wpart_a, nullptr);   // (the dense read of the active rows is in the full-row pass)
       k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
     }
     // an fp32 state given with its exact bf16 copy: the active rows take the
@@ -1918,16 +1975,19 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
     const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % (2 * kMfRows) == 0;
     if (mfa32 && act_rows) {
       const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
+      const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
+      k_dz_pack<<<dim3((unsigned)((Tp * 32 + 255) / 256)), dim3(256), 0, s>>>(tok, T, N, NA, 1, 32, w.dza,
+                                                                              w.dza + Tp * 2 * 32);
       if (act_din)
         k_bwd_rows_mfma<true, float, 2 * kMfRows, true><<<ga, dim3(8 * kMfRows), 0, s>>>(
             reinterpret_cast<const uint16_t*>(X_bf16), reinterpret_cast<const uint16_t*>(act_din),
-            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
-            nullptr);
+            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dza,
+            wpart_a, nullptr);
       else
         k_bwd_rows_mfma<true, float, 2 * kMfRows><<<ga, dim3(8 * kMfRows), 0, s>>>(
             reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
-            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, wpart_a,
-            nullptr);
+            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dza,
+            wpart_a, nullptr);
     }
     const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
 #define XHC_FULL_ROWS(NNV)                                                                                       \

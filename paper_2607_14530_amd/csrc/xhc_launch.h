@@ -133,6 +133,7 @@ size_t bwd_pre_ws_bytes(const xhc_dims* d);
 constexpr int kBwdPreAll = 0, kBwdPreTokens = 1, kBwdPreReduce = 2, kBwdPreTokensGiven = 3;
 struct BwdPreWs {
   float *part, *tok, *pg, *wpart_r, *wpart_p, *wpart_a, *red_a, *pgsum;
+  uint16_t *dzf, *dza;   // packed dz' of the full-row and active-row MFMA passes
 };
 BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws);   // layout of launch_bwd_pre's workspace
 hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum, const float* W_r,
