@@ -674,6 +674,215 @@ __global__ __launch_bounds__(256) void k_bwd_conv_run(const float* __restrict__ 
   for (int r = 0; r < kConvRows; ++r) dst[(int64_t)r * C] = acc[r];
 }
 
+// The element pass and the conv reverse of the post backward fused, for the
+// paper's branches (kappa = 4, 8, 12; K_r = 4) and k <= 4: one channel per
+// thread over a run of kConvRun tokens, nothing but the gradients leaving
+// registers.  Per token u of the run:
+//   dX[u, I_l] = sum_j H^res[j][l] dY_j          (mixing gradient of the active rows)
+//   X[u, I_l]  = Xact[u, l]                        (restore, when X is given)
+//   de_b[u]    = sum_j CY[b][j] dY_j + sum_b' CE[b][b'] e_b'[u]   (e from the F history)
+//   dF[v]     += de_0 at v = u and w_j[i] de_j[u] at v = u - i      (the reverse of the causal conv)
+//   part[run][row (j, i)][c] += F[u - i] de_j[u]
+// The runs are disjoint, so an in-place dX never meets a token another run
+// still reads.  A token's dF is stored once complete; the last 11 tokens of a
+// run (later runs still add to them) go to rb[run][i] (token t1 - 11 + i)
+// and a run's additions to the 11 tokens before it to lb[run][i] (token
+// t0 - 11 + i, zero where they are in an earlier sequence); k_bwd_post_fix
+// stores their sums.  The loads of the next 4 tokens are in flight while 4
+// are used.
+template <typename TS, typename TG>
+__global__ __launch_bounds__(256) void k_bwd_post_run(const TG* dXn, TS* __restrict__ X, const TS* __restrict__ Xact,
+                                                      const TS* __restrict__ F, int64_t T, int64_t S, int N, int C,
+                                                      int k, const float* __restrict__ conv_w,
+                                                      const int32_t* __restrict__ idx, const float* __restrict__ Hres,
+                                                      const float* __restrict__ coef, TG* dX, TS* __restrict__ dF,
+                                                      float* __restrict__ part, float* __restrict__ rb,
+                                                      float* __restrict__ lb) {
+  constexpr int KM = 4, NCF = 4 * kMaxK + 16;   // slots; coefficients a token
+  // the run's per-token values, staged once: element offsets of the slot rows
+  // in the state, H^res, the component-gradient coefficients
+  __shared__ int64_t s_row[kConvRun][KM];
+  __shared__ float s_hr[kConvRun][KM * KM];
+  __shared__ float s_cf[kConvRun][NCF];
+  const int c = blockIdx.x * 256 + threadIdx.x;   // C % 256 == 0: every thread has a channel
+  const int64_t run = blockIdx.y;
+  const int64_t t0 = run * kConvRun;
+  const int64_t t1 = t0 + kConvRun < T ? t0 + kConvRun : T;
+  const int nt = (int)(t1 - t0);
+  const bool last = t1 == T;
+  for (int i = threadIdx.x; i < nt * KM; i += 256) {
+    const int64_t u = t0 + i / KM;
+    const int j = i % KM < k ? i % KM : k - 1;   // unused slots repeat the last one (in bounds)
+    s_row[i / KM][i % KM] = (u * N + idx[u * k + j]) * (int64_t)C;
+  }
+  for (int i = threadIdx.x; i < nt * KM * KM; i += 256) {
+    const int64_t u = t0 + i / (KM * KM);
+    const int j = (i % (KM * KM)) / KM, l = i % KM;
+    s_hr[i / (KM * KM)][i % (KM * KM)] = (j < k && l < k) ? Hres[(u * k + j) * k + l] : 0.f;
+  }
+  for (int i = threadIdx.x; i < nt * NCF; i += 256) s_cf[i / NCF][i % NCF] = coef[t0 * NCF + i];
+  __syncthreads();
+  float w[kConvRows];
+#pragma unroll
+  for (int r = 0; r < kConvRows; ++r) w[r] = conv_w[(int64_t)r * C + c];
+  float fw[12], acc[kConvRows], P[12];
+  int64_t seq0 = t0 - t0 % S;   // start of the current sequence
+  // fw[i] = F[u - i] (zero before the sequence start); before the first token
+  // it holds F[t0 - 1 - i] at index i
+#pragma unroll
+  for (int i = 0; i < 12; ++i) {
+    const int64_t t = t0 - 1 - i;
+    fw[i] = (i < 11 && t >= seq0) ? ld_scalar<TS>(F + t * C + c) : 0.f;
+    P[i] = 0.f;
+  }
+#pragma unroll
+  for (int r = 0; r < kConvRows; ++r) acc[r] = 0.f;
+  float* const lbr = lb + run * 11 * (int64_t)C + c;
+  if (run > 0)
+#pragma unroll
+    for (int i = 0; i < 11; ++i) lbr[(int64_t)i * C] = 0.f;
+  // a token's dF, complete (or this run's additions to an earlier run's token)
+  auto emit = [&](int64_t v, float x) {
+    if (v < seq0) return;
+    if (v >= t0) st_scalar<TS>(dF + v * C + c, x);
+    else if (v >= t0 - 11) lbr[(v - (t0 - 11)) * C] = x;
+  };
+  // loads of one token: dY of the k slots, the saved rows, F.  Every load is
+  // issued (past the run or the k slots from a clamped, in-bounds address)
+  // and the unused values are replaced by zero, so the buffers stay in
+  // registers and the loads stay in flight together.
+  auto load = [&](int64_t u, float (&dy)[KM], float (&a)[KM], float& f) {
+    const bool ok = u < t1;
+    const int64_t uc = ok ? u : t1 - 1;
+    const int ul = (int)(uc - t0);
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      const int jc = j < k ? j : k - 1;
+      const float yv = ld_scalar<TG>(dXn + s_row[ul][j] + c);
+      const float xv = ld_scalar<TS>(Xact + (uc * k + jc) * (int64_t)C + c);
+      dy[j] = (ok && j < k) ? yv : 0.f;
+      a[j] = (ok && j < k) ? xv : 0.f;
+    }
+    const float fv = ld_scalar<TS>(F + uc * C + c);
+    f = ok ? fv : 0.f;
+  };
+  float bdy[2][4][KM], ba[2][4][KM], bf[2][4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) load(t0 + q, bdy[0][q], ba[0][q], bf[0][q]);
+  for (int64_t ub = t0; ub < t1; ub += 8) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int cur = half, nxt = half ^ 1;
+      const int64_t u4 = ub + 4 * half;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) load(u4 + 4 + q, bdy[nxt][q], ba[nxt][q], bf[nxt][q]);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t u = u4 + q;
+        if (u < t1) {   // (no early exit: the loop unrolls and the buffers stay in registers)
+        if (u % S == 0 && u > t0) {
+          // a sequence starts at u: the tokens before it are complete
+#pragma unroll
+          for (int i = 0; i < 12; ++i) emit(u - 1 - i, P[i]);
+          seq0 = u;
+#pragma unroll
+          for (int i = 0; i < 12; ++i) { P[i] = 0.f; fw[i] = 0.f; }
+        }
+        // token u - 12 has all its contributions
+        emit(u - 12, P[11]);
+#pragma unroll
+        for (int i = 11; i > 0; --i) { P[i] = P[i - 1]; fw[i] = fw[i - 1]; }
+        fw[0] = bf[cur][q];
+        float dy[KM], av[KM];
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          dy[j] = bdy[cur][q][j];
+          av[j] = ba[cur][q][j];
+        }
+        // the components at u (eq:aug): F[u] and the three causal convolutions
+        float e[4];
+        e[0] = fw[0];
+        {
+          int r = 0;
+#pragma unroll
+          for (int j = 1; j < 4; ++j) {
+            const int kap = j == 1 ? 4 : (j == 2 ? 8 : 12);
+            float v = 0.f;
+#pragma unroll
+            for (int i = 0; i < kap; ++i, ++r) v = fmaf(w[r], fw[i], v);
+            e[j] = v;
+          }
+        }
+        const int ul = (int)(u - t0);
+        const float* cf = s_cf[ul];
+        float d[4];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          float g = 0.f;
+#pragma unroll
+          for (int j = 0; j < KM; ++j)
+            if (j < k) g = fmaf(cf[b * kMaxK + j], dy[j], g);
+#pragma unroll
+          for (int b2 = 0; b2 < 4; ++b2) g = fmaf(cf[4 * kMaxK + b * 4 + b2], e[b2], g);
+          d[b] = g;
+        }
+        // the active rows: mixing gradient, and the pre-update rows back in X
+#pragma unroll
+        for (int l = 0; l < KM; ++l) {
+          if (l < k) {
+            float g = 0.f;
+#pragma unroll
+            for (int j = 0; j < KM; ++j) g = fmaf(s_hr[ul][j * KM + l], dy[j], g);
+            const int64_t row = s_row[ul][l];
+            st_scalar<TG>(dX + row + c, g);
+            if (X) st_scalar<TS>(X + row + c, av[l]);
+          }
+        }
+        P[0] = d[0];
+        int r = 0;
+#pragma unroll
+        for (int j = 1; j < 4; ++j) {
+          const int kap = j == 1 ? 4 : (j == 2 ? 8 : 12);
+#pragma unroll
+          for (int i = 0; i < kap; ++i, ++r) {
+            P[i] = fmaf(w[r], d[j], P[i]);
+            acc[r] = fmaf(fw[i], d[j], acc[r]);
+          }
+        }
+        }
+      }
+    }
+  }
+  // the tokens still pending: t1 - 1 - i.  The last run completes them; any
+  // other run leaves t1 - 11 .. t1 - 1 (same sequence as t1 - 1) to the fix-up.
+#pragma unroll
+  for (int i = 0; i < 12; ++i) {
+    const int64_t v = t1 - 1 - i;
+    if (last || i == 11) emit(v, P[i]);
+    else if (v >= seq0) rb[(run * 11 + (v - (t1 - 11))) * (int64_t)C + c] = P[i];
+  }
+  float* dst = part + run * kConvRows * (int64_t)C + c;
+#pragma unroll
+  for (int r = 0; r < kConvRows; ++r) dst[(int64_t)r * C] = acc[r];
+}
+
+// dF of the 11 tokens before each run boundary t1 = b kConvRun (b = 1 ..
+// nruns - 1): the earlier run's part (rb) plus the later run's (lb), for the
+// tokens in the sequence of t1 - 1 (the others were stored complete).
+template <typename TS>
+__global__ __launch_bounds__(256) void k_bwd_post_fix(const float* __restrict__ rb, const float* __restrict__ lb,
+                                                      int64_t T, int64_t S, int C, TS* __restrict__ dF) {
+  const int c = blockIdx.x * 256 + threadIdx.x;
+  if (c >= C) return;
+  const int64_t b = blockIdx.y + 1;
+  const int i = blockIdx.z;
+  const int64_t t1 = b * kConvRun;
+  const int64_t v = t1 - 11 + i;
+  const int64_t s_end = (t1 - 1) - (t1 - 1) % S;
+  if (t1 >= T || v < s_end) return;
+  st_scalar<TS>(dF + v * C + c, rb[((b - 1) * 11 + i) * (int64_t)C + c] + lb[(b * 11 + i) * (int64_t)C + c]);
+}
+
 // out[col] = sum_r in[r][col] over nrows rows (row stride = ncols), fixed order.
 __global__ __launch_bounds__(256) void k_colsum_rows(const float* __restrict__ in, int64_t nrows, int64_t ncols,
                                                      float* __restrict__ out) {
@@ -1484,6 +1693,8 @@ __global__ __launch_bounds__(256) void k_colsum_rows_corr(const float* __restric
 static bool conv_run_ok(const xhc_dims* d) {
   return d->Kr == 4 && d->kappa[0] == 4 && d->kappa[1] == 8 && d->kappa[2] == 12;
 }
+// the fused element pass + conv reverse (k_bwd_post_run)
+static bool post_run_ok(const xhc_dims* d) { return conv_run_ok(d) && d->k <= 4 && d->C % 256 == 0; }
 
 #define XHC_TS_DISPATCH(dt, ...) \
   if ((dt) == XHC_BF16) { using TS = uint16_t; __VA_ARGS__; } else { using TS = float; __VA_ARGS__; }
@@ -1496,13 +1707,18 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
   const int N = d->N, C = d->C, k = d->k, Kr = d->Kr;
   const int64_t ncb = post_chunks(C);
   const dim3 grid((unsigned)(T * ncb));
-  // workspace: dots partials | coef | de (Kr planes, fp32) | conv partials
+  // workspace: dots partials | coef | de (Kr planes, fp32; or, fused, the run
+  // boundary parts rb and lb) | conv partials
   const int km = k <= 4 ? 4 : 8;
   const int nd = km * km + km * Kr + Kr * (Kr + 1) / 2;
+  const bool fused = post_run_ok(d);
+  const int64_t nruns = (T + kConvRun - 1) / kConvRun;
   float* part = reinterpret_cast<float*>(ws);
   float* coef = part + ncb * nd * T;
   float* de = coef + T * (Kr * kMaxK + Kr * Kr);
-  float* cpart = de + (Kr > 1 ? (int64_t)Kr * T * C : 0);
+  float* rb = de;
+  float* lb = rb + nruns * 11 * (int64_t)C;
+  float* cpart = de + (fused ? 2 * nruns * 11 * (int64_t)C : (Kr > 1 ? (int64_t)Kr * T * C : 0));
   const int* kap = d->kappa;
 #define XHC_BWD_POST_TG(KRV, KMV)                                                                                \
     k_bwd_post_dots<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),              \
@@ -1510,6 +1726,20 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
         conv_w, idx, part);                                                                                      \
     k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, ncb, T, k,               \
         d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                                     \
+    if (fused) {                                                                                                 \
+      if (dX != dXn) {                                                                                           \
+        /* the untouched rows keep their gradient; the fused pass writes the active ones */                     \
+        const hipError_t ec = hipMemcpyAsync(dX, dXn, (size_t)T * N * C * sizeof(TG), hipMemcpyDeviceToDevice, s); \
+        if (ec != hipSuccess) return ec;                                                                         \
+      }                                                                                                          \
+      k_bwd_post_run<TS, TG><<<dim3((unsigned)((C + 255) / 256), (unsigned)nruns), dim3(256), 0, s>>>(           \
+          reinterpret_cast<const TG*>(dXn), reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(Xact),          \
+          reinterpret_cast<const TS*>(F), T, S, N, C, k, conv_w, idx, Hres, coef, reinterpret_cast<TG*>(dX),     \
+          reinterpret_cast<TS*>(dF), cpart, rb, lb);                                                              \
+      if (nruns > 1)                                                                                             \
+        k_bwd_post_fix<TS><<<dim3((unsigned)((C + 255) / 256), (unsigned)(nruns - 1), 11u), dim3(256), 0, s>>>(   \
+            rb, lb, T, S, C, reinterpret_cast<TS*>(dF));                                                         \
+    } else                                                                                                       \
     k_bwd_post_elem<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),              \
         reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, \
         k, kap[0], kap[1], kap[2], conv_w, idx, Hres, coef, reinterpret_cast<TG*>(dX), reinterpret_cast<TS*>(dF), \
@@ -1529,6 +1759,11 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
 #undef XHC_BWD_POST_TG
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || Kr == 1) return e;
+  if (fused) {
+    const int64_t ncols = (int64_t)kConvRows * C;
+    k_colsum_rows<<<dim3((unsigned)((ncols + 255) / 256)), dim3(256), 0, s>>>(cpart, nruns, ncols, dconv_w);
+    return hipGetLastError();
+  }
   if (conv_run_ok(d)) {
     // dF and the tap gradients in one pass over de (the paper's branches)
     const int64_t nruns = (T + kConvRun - 1) / kConvRun;
@@ -1563,8 +1798,10 @@ size_t bwd_post_ws_bytes(const xhc_dims* d) {
     int nrows = 0;
     for (int j = 0; j < Kr - 1; ++j) nrows += d->kappa[j];
     const size_t chunked = (size_t)((T + kConvChunk - 1) / kConvChunk) * nrows * C;
-    const size_t runs = conv_run_ok(d) ? (size_t)((T + kConvRun - 1) / kConvRun) * kConvRows * C : 0;
-    n += (size_t)Kr * T * C + (chunked > runs ? chunked : runs);
+    const size_t nruns = (size_t)((T + kConvRun - 1) / kConvRun);
+    const size_t runs = conv_run_ok(d) ? nruns * kConvRows * C : 0;
+    // fused: only the run boundary parts instead of de
+    n += (post_run_ok(d) ? 2 * nruns * 11 * (size_t)C : (size_t)Kr * T * C) + (chunked > runs ? chunked : runs);
   }
   return n * sizeof(float) + 256;
 }

@@ -55,6 +55,10 @@ CASES = [
     W(T=40, S=20, N=8, k=4, m=2, C=512, Kr=4, name="bwd-mlp-N8"),
     W(T=32, S=32, N=32, k=4, m=2, C=256, Kr=1, name="bwd-attn-N32"),
     W(T=40, S=20, N=32, k=4, m=2, C=256, Kr=4, name="bwd-mlp-N32"),
+    # several 128-token runs of the fused conv reverse: sequence starts inside
+    # runs, one within the last 11 tokens of a run, a short last run
+    W(T=300, S=100, N=16, k=4, m=2, C=256, Kr=4, name="bwd-mlp-runs-S100"),
+    W(T=360, S=120, N=8, k=4, m=2, C=512, Kr=4, name="bwd-mlp-runs-S120"),
     W(T=64, S=64, N=16, k=4, m=2, C=256, Kr=4, alpha=(0.5, 1.0, 0.5), name="bwd-mlp-stress"),
     W(T=64, S=32, N=16, k=4, m=2, C=256, Kr=4, router="softmax", name="bwd-mlp-softmax"),
     W(T=40, S=20, N=8, k=4, m=1, C=512, Kr=1, router="softmax", name="bwd-attn-softmax-N8"),
