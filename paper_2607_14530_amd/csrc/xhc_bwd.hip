@@ -19,6 +19,7 @@
 //  k_bwd_act_rows     weight-stationary over rows of [W_post | W_res]: dX of the active
 //                     rows, dW_post and dW_res partials
 //  k_colsum_rows      deterministic column sums (token reductions)
+#include "xhc_conv.h"
 #include "xhc_device.h"
 #include "xhc_launch.h"
 
@@ -325,21 +326,133 @@ __global__ __launch_bounds__(256) void k_bwd_post_dots(const TG* __restrict__ dX
   for (int i = threadIdx.x; i < nd; i += 256) part[(cb * nd + i) * T + t] = red[0][i] + red[1][i] + red[2][i] + red[3][i];
 }
 
+// The dot products of k_bwd_post_dots for the paper's branches (K_r = 4,
+// kappa = 4, 8, 12) and k <= 4, run-based: a thread owns 4 channels and walks
+// a run of kDotRun tokens, keeping the conv taps and the last 11 values of F
+// in registers (F read once), with the loads of the next PF tokens in
+// flight.  Per token a wave sums its lanes' products through an LDS transpose
+// (lane i adds column i) and lanes i < ND write them: part[w][t][i] with w the
+// wave's 256-channel slice of C (workgroups of 256 or 64 threads).
+constexpr int kDotRun = 64;
+template <typename TS, typename TG>
+__global__ __launch_bounds__(256) void k_bwd_post_dots_run(const TG* dXn, const TS* __restrict__ Xact,
+                                                           const TS* __restrict__ F, int64_t T, int64_t S, int N,
+                                                           int C, int k, const float* __restrict__ conv_w,
+                                                           const int32_t* __restrict__ idx, float* __restrict__ part) {
+  using CG = ConvGroup<4, 8, 12>;
+  using PD = PostDots<4, 4>;
+  constexpr int KM = 4, ND = PD::ND, LD = (ND + 3) / 4 * 4 + 4, PF = 1;
+  static_assert(ND <= kWave, "one column per lane");
+  __shared__ __align__(16) float xpose[4][kWave][LD];
+  __shared__ int32_t s_idx[kDotRun][KM];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int g = (int)(blockIdx.y * blockDim.x + threadIdx.x);   // C % (4 blockDim.x) == 0
+  const int c = g * 4, slice = g / kWave;
+  const int64_t t0 = (int64_t)blockIdx.x * kDotRun;
+  const int nt = (int)((T - t0 < kDotRun) ? T - t0 : kDotRun);
+  for (int i = threadIdx.x; i < nt * KM; i += blockDim.x) {   // (workgroups of 64 or 256 threads)
+    const int j = i % KM < k ? i % KM : k - 1;   // unused slots repeat the last one (in bounds)
+    s_idx[i / KM][i % KM] = idx[(t0 + i / KM) * k + j];
+  }
+  CG cg;
+  cg.load_taps(conv_w, C, c);
+  cg.init(F, t0, S, C, c);
+  __syncthreads();
+  struct Tok {
+    typename Row4<TS>::raw f, a[KM];
+    typename Row4<TG>::raw y[KM];
+  };
+  // every load is issued (past the run from the last token: in bounds)
+  auto load = [&](int u, Tok& b) {
+    const int uc = u < nt ? u : nt - 1;
+    const int64_t t = t0 + uc;
+    b.f = Row4<TS>::load(F + t * C + c);
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+      b.y[j] = Row4<TG>::load(dXn + (t * N + s_idx[uc][j]) * (int64_t)C + c);
+      b.a[j] = Row4<TS>::load(Xact + (t * k + (j < k ? j : k - 1)) * (int64_t)C + c);
+    }
+  };
+  float* mine = &xpose[wave][lane][0];
+  Tok ring[PF];
+#pragma unroll
+  for (int f = 0; f < PF; ++f) load(f, ring[f]);
+  for (int u1 = 0; u1 < nt; u1 += PF) {
+#pragma unroll
+    for (int f = 0; f < PF; ++f) {
+      const int u = u1 + f;
+      if (u < nt) {   // (no early exit: the loop unrolls and the ring stays in registers)
+        const int64_t t = t0 + u;
+        if (t % S == 0) cg.reset();
+        float cur[1][4], dy[KM][4], a[KM][4];
+        Row4<TS>::unpack(ring[f].f, cur[0]);
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          Row4<TG>::unpack(ring[f].y[j], dy[j]);
+          Row4<TS>::unpack(ring[f].a[j], a[j]);
+          if (j >= k) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) { dy[j][q] = 0.f; a[j][q] = 0.f; }
+          }
+        }
+        load(u + PF, ring[f]);
+        float e[4][4];
+        cg.components(cur, 0, e);
+        cg.advance(cur);
+        // the lane's products, written to its LDS row in groups of 4 as formed
+        // (ya row j, then ye row j, then the Gram)
+        auto dot4 = [&](const float (&x)[4], const float (&y)[4]) {
+          float v = 0.f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v = fmaf(x[q], y[q], v);
+          return v;
+        };
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          *reinterpret_cast<float4*>(mine + PD::ya(j, 0)) =
+              make_float4(dot4(dy[j], a[0]), dot4(dy[j], a[1]), dot4(dy[j], a[2]), dot4(dy[j], a[3]));
+          *reinterpret_cast<float4*>(mine + PD::ye(j, 0)) =
+              make_float4(dot4(dy[j], e[0]), dot4(dy[j], e[1]), dot4(dy[j], e[2]), dot4(dy[j], e[3]));
+        }
+        static_assert(PD::gram(0) % 4 == 0 && ND - PD::gram(0) == 10, "Gram block: 10 values after 32");
+        *reinterpret_cast<float4*>(mine + PD::gram(0)) =
+            make_float4(dot4(e[0], e[0]), dot4(e[0], e[1]), dot4(e[0], e[2]), dot4(e[0], e[3]));
+        *reinterpret_cast<float4*>(mine + PD::gram(4)) =
+            make_float4(dot4(e[1], e[1]), dot4(e[1], e[2]), dot4(e[1], e[3]), dot4(e[2], e[2]));
+        *reinterpret_cast<float2*>(mine + PD::gram(8)) = make_float2(dot4(e[2], e[3]), dot4(e[3], e[3]));
+        // LDS operations of one wave complete in issue order; the fences keep
+        // the compiler from moving the column reads above the row writes (or
+        // the next token's writes above these reads)
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        if (lane < ND) {
+          float sum = 0.f;
+#pragma unroll 16
+          for (int r = 0; r < kWave; ++r) sum += xpose[wave][r][lane];
+          part[((int64_t)slice * T + t) * ND + lane] = sum;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+      }
+    }
+  }
+}
+
 // Per token: dH^res, dH^post, dp and the coefficients of the component
 // gradients: de_b = sum_j CY[b][j] dY_j + sum_b' CE[b][b'] e_b'.
+// part: value i of chunk c for token t at c cs + i is + t ts.
 template <int KR, int KM>
-__global__ __launch_bounds__(128) void k_bwd_post_token(const float* __restrict__ part, int64_t nchunk, int64_t T,
-                                                        int k, int gram_schmidt, const float* __restrict__ p,
-                                                        const float* __restrict__ Hpost, float* __restrict__ dHres,
-                                                        float* __restrict__ dHpost, float* __restrict__ dp,
-                                                        float* __restrict__ coef) {
+__global__ __launch_bounds__(128) void k_bwd_post_token(const float* __restrict__ part, int64_t nchunk, int64_t cs,
+                                                        int64_t is, int64_t ts, int64_t T, int k, int gram_schmidt,
+                                                        const float* __restrict__ p, const float* __restrict__ Hpost,
+                                                        float* __restrict__ dHres, float* __restrict__ dHpost,
+                                                        float* __restrict__ dp, float* __restrict__ coef) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
   using PD = PostDots<KR, KM>;
-  const int nd = PD::ND;
   auto sum = [&](int i) {
     float s = 0.f;
-    for (int64_t c = 0; c < nchunk; ++c) s += part[(c * nd + i) * T + t];
+    for (int64_t c = 0; c < nchunk; ++c) s += part[c * cs + i * is + t * ts];
     return s;
   };
   for (int j = 0; j < k; ++j)
@@ -1714,18 +1827,28 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
   const bool fused = post_run_ok(d);
   const int64_t nruns = (T + kConvRun - 1) / kConvRun;
   float* part = reinterpret_cast<float*>(ws);
-  float* coef = part + ncb * nd * T;
+  // dots partials: [post_chunks(C)][nd][T], or, fused, [C / 256][T][nd]
+  float* coef = part + (fused ? (int64_t)(C / 256) : ncb) * nd * T;
   float* de = coef + T * (Kr * kMaxK + Kr * Kr);
   float* rb = de;
   float* lb = rb + nruns * 11 * (int64_t)C;
   float* cpart = de + (fused ? 2 * nruns * 11 * (int64_t)C : (Kr > 1 ? (int64_t)Kr * T * C : 0));
   const int* kap = d->kappa;
 #define XHC_BWD_POST_TG(KRV, KMV)                                                                                \
-    k_bwd_post_dots<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),              \
-        reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, kap[0], kap[1], kap[2], \
-        conv_w, idx, part);                                                                                      \
-    k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, ncb, T, k,               \
-        d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                                     \
+    if (fused) {                                                                                                 \
+      const int nthr = C % 1024 == 0 ? 256 : 64;                                                                 \
+      k_bwd_post_dots_run<TS, TG><<<dim3((unsigned)((T + kDotRun - 1) / kDotRun), (unsigned)(C / (4 * nthr))),  \
+                                    dim3(nthr), 0, s>>>(reinterpret_cast<const TG*>(dXn),                        \
+          reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, conv_w, idx, part);   \
+      k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, C / 256,             \
+          T * nd, 1, nd, T, k, d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                               \
+    } else {                                                                                                     \
+      k_bwd_post_dots<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),            \
+          reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, kap[0], kap[1],       \
+          kap[2], conv_w, idx, part);                                                                            \
+      k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, ncb, nd * T, T,      \
+          1, T, k, d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                           \
+    }                                                                                                            \
     if (fused) {                                                                                                 \
       if (dX != dXn) {                                                                                           \
         /* the untouched rows keep their gradient; the fused pass writes the active ones */                     \
@@ -1793,7 +1916,8 @@ size_t bwd_post_ws_bytes(const xhc_dims* d) {
   const int C = d->C, k = d->k, Kr = d->Kr;
   const int km = k <= 4 ? 4 : 8;
   const int nd = km * km + km * Kr + Kr * (Kr + 1) / 2;
-  size_t n = (size_t)post_chunks(C) * nd * T + (size_t)T * (Kr * kMaxK + Kr * Kr);
+  const size_t nchunks = post_run_ok(d) ? (size_t)(C / 256) : (size_t)post_chunks(C);
+  size_t n = nchunks * nd * T + (size_t)T * (Kr * kMaxK + Kr * Kr);
   if (Kr > 1) {
     int nrows = 0;
     for (int j = 0; j < Kr - 1; ++j) nrows += d->kappa[j];
