@@ -1484,17 +1484,6 @@ __global__ __launch_bounds__(256) void k_dz_pack(const float* __restrict__ tok, 
   blk[(NO + o) * kDzBlock + t % kDzBlock] = (uint16_t)lb;
 }
 
-// f = hi + lo with hi the round-to-nearest-even bf16 of f and lo that of the
-// rest (the packed hardware conversion: the bits of f2bf for finite values)
-__device__ __forceinline__ void split_bf16x8(const float (&f)[8], uint4& hi, uint4& lo) {
-  hi = pack8(f);
-  float h[8], l[8];
-  unpack8(hi, h);
-#pragma unroll
-  for (int e = 0; e < 8; ++e) l[e] = f[e] - h[e];
-  lo = pack8(l);
-}
-
 // 4 consecutive gradient elements of a bf16 or fp32 accumulator row, as
 // loaded (raw) and as floats
 template <typename TD> struct Raw4;
@@ -1832,7 +1821,8 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
   float* de = coef + T * (Kr * kMaxK + Kr * Kr);
   float* rb = de;
   float* lb = rb + nruns * 11 * (int64_t)C;
-  float* cpart = de + (fused ? 2 * nruns * 11 * (int64_t)C : (Kr > 1 ? (int64_t)Kr * T * C : 0));
+  float* dsum = lb + nruns * 11 * (int64_t)C;   // fused: the dots partials summed over the C / 256 slices
+  float* cpart = de + (fused ? 2 * nruns * 11 * (int64_t)C + (int64_t)nd * T : (Kr > 1 ? (int64_t)Kr * T * C : 0));
   const int* kap = d->kappa;
 #define XHC_BWD_POST_TG(KRV, KMV)                                                                                \
     if (fused) {                                                                                                 \
@@ -1840,8 +1830,9 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
       k_bwd_post_dots_run<TS, TG><<<dim3((unsigned)((T + kDotRun - 1) / kDotRun), (unsigned)(C / (4 * nthr))),  \
                                     dim3(nthr), 0, s>>>(reinterpret_cast<const TG*>(dXn),                        \
           reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, conv_w, idx, part);   \
-      k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, C / 256,             \
-          T * nd, 1, nd, T, k, d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                               \
+      k_colsum_rows<<<dim3((unsigned)((T * nd + 255) / 256)), dim3(256), 0, s>>>(part, C / 256, T * nd, dsum);     \
+      k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(dsum, 1, T * nd, 1, nd,    \
+          T, k, d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                              \
     } else {                                                                                                     \
       k_bwd_post_dots<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),            \
           reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, kap[0], kap[1],       \
@@ -1850,7 +1841,7 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
           1, T, k, d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                           \
     }                                                                                                            \
     if (fused) {                                                                                                 \
-      if (dX != dXn) {                                                                                           \
+      if (dX != dXn && N > k) {                                                                                  \
         /* the untouched rows keep their gradient; the fused pass writes the active ones */                     \
         const hipError_t ec = hipMemcpyAsync(dX, dXn, (size_t)T * N * C * sizeof(TG), hipMemcpyDeviceToDevice, s); \
         if (ec != hipSuccess) return ec;                                                                         \
@@ -1925,7 +1916,8 @@ size_t bwd_post_ws_bytes(const xhc_dims* d) {
     const size_t nruns = (size_t)((T + kConvRun - 1) / kConvRun);
     const size_t runs = conv_run_ok(d) ? nruns * kConvRows * C : 0;
     // fused: only the run boundary parts instead of de
-    n += (post_run_ok(d) ? 2 * nruns * 11 * (size_t)C : (size_t)Kr * T * C) + (chunked > runs ? chunked : runs);
+    n += (post_run_ok(d) ? 2 * nruns * 11 * (size_t)C + (size_t)nd * T : (size_t)Kr * T * C) +
+         (chunked > runs ? chunked : runs);
   }
   return n * sizeof(float) + 256;
 }
@@ -1974,16 +1966,43 @@ __global__ __launch_bounds__(256) void k_multi_prep(MultiRows m, int64_t T, int 
   out[i] = v;
 }
 
+// The dz' of k_multi_prep as bf16 pairs hi + lo in the layouts of
+// k_dz_pack (token rows [t][2 NOP], 32-token transposes [b][2 NOP][32]),
+// NOP = the NO outputs padded to whole 32-blocks (zero past NO and past T).
+template <int NQ>
+__global__ __launch_bounds__(256) void k_dz_pack_multi(const float* __restrict__ prep, int64_t T,
+                                                       uint16_t* __restrict__ rows, uint16_t* __restrict__ tr) {
+  constexpr int NO = 16 * (NQ + 1), NOP = (NO + 31) / 32 * 32, PITCH = NO + 8;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
+  if (i >= Tp * NOP) return;
+  const int64_t t = i / NOP;
+  const int o = (int)(i % NOP);
+  const float v = (t < T && o < NO) ? prep[t * PITCH + o] : 0.f;
+  const uint32_t hb = pack2bf(v, 0.f) & 0xFFFFu;
+  const uint32_t lb = pack2bf(v - __uint_as_float(hb << 16), 0.f) & 0xFFFFu;
+  rows[t * 2 * NOP + o] = (uint16_t)hb;
+  rows[t * 2 * NOP + NOP + o] = (uint16_t)lb;
+  uint16_t* blk = tr + (t / kDzBlock) * 2 * NOP * kDzBlock;
+  blk[o * kDzBlock + t % kDzBlock] = (uint16_t)hb;
+  blk[(NOP + o) * kDzBlock + t % kDzBlock] = (uint16_t)lb;
+}
+
 template <int NQ>
 __global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restrict__ X, uint16_t* __restrict__ dX,
-                                                        MultiRows m, const float* __restrict__ prep, int64_t T,
+                                                        MultiRows m, const float* __restrict__ prep,
+                                                        const uint16_t* __restrict__ dzp, int64_t T,
                                                         int N, int C, int NA, int64_t tchunk) {
   constexpr int NO = 16 * (NQ + 1);            // outputs
   constexpr int NKB = (NO + 31) / 32;          // 32-output blocks of the dX contraction
-  constexpr int NDZ = kMfStep * NO / 256;      // dz' values fetched per thread
-  static_assert(kMfStep * NO % 256 == 0, "whole dz' rows per step");
+  constexpr int NOP = 32 * NKB;                // outputs padded
+  constexpr int DZP = 16 * NOP / 256;          // 16-byte pieces of packed dz' per thread and step
+  static_assert(kMfStep == kDzBlock && DZP * 256 == 16 * NOP, "a step copies its packed dz' in whole pieces");
   __shared__ __align__(16) uint16_t xs[kMfStep][kMfXPitch];
-  __shared__ float dzs[kMfStep][NKB * 32 + 1];
+  // packed dz' of the step (token rows, transpose); the pitches keep the
+  // 16-byte operand reads of a 16-lane group on distinct banks
+  __shared__ __align__(16) uint16_t dzr[kMfStep][2 * NOP + 8];
+  __shared__ __align__(16) uint16_t dzt[2 * NOP][kMfStep + 8];
   __shared__ float sc[kMfStep][5 + NQ];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int l16 = lane % 16, g4 = lane / 16;
@@ -2010,18 +2029,29 @@ __global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restri
 #pragma unroll
   for (int ob = 0; ob <= NQ; ++ob) dw[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
+  const uint16_t* const dzrows = dzp;
+  const uint16_t* const dztr = dzp + (T + kDzBlock - 1) / kDzBlock * kDzBlock * 2 * NOP;
   struct Stage {
-    float dz[NDZ];
+    uint4 dz[DZP];
     float scal[5 + NQ];
     uint4 x;
     uint2 dx[2];
   };
   auto fetch = [&](Stage& st, int64_t tb) {
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
+    // pieces [0, 8 NOP): token rows (NOP / 4 a token, zero past the chunk);
+    // [8 NOP, 16 NOP): the transposed block (4 a row)
 #pragma unroll
-    for (int r = 0; r < NDZ; ++r) {
-      const int q = threadIdx.x + r * 256, u = q / NO, o = q % NO;
-      st.dz[r] = u < nt ? prep[(tb + u) * PITCH + o] : 0.f;
+    for (int r = 0; r < DZP; ++r) {
+      const int q = threadIdx.x + r * 256;
+      if (q < 8 * NOP) {
+        const int u = q / (NOP / 4), off = (q % (NOP / 4)) * 8;
+        st.dz[r] = u < nt ? *reinterpret_cast<const uint4*>(dzrows + (tb + u) * 2 * NOP + off)
+                          : make_uint4(0, 0, 0, 0);
+      } else {
+        const int qq = q - 8 * NOP, row = qq / 4, off = (qq % 4) * 8;
+        st.dz[r] = *reinterpret_cast<const uint4*>(dztr + (tb / kDzBlock) * 2 * NOP * kDzBlock + row * kDzBlock + off);
+      }
     }
     if (threadIdx.x < kMfStep) {
       const int u = threadIdx.x;
@@ -2050,12 +2080,16 @@ __global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restri
     const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
     __syncthreads();   // the previous step's LDS reads are done
 #pragma unroll
-    for (int r = 0; r < NDZ; ++r) {
+    for (int r = 0; r < DZP; ++r) {
       const int q = threadIdx.x + r * 256;
-      dzs[q / NO][q % NO] = cur.dz[r];
+      if (q < 8 * NOP) {
+        const int u = q / (NOP / 4), off = (q % (NOP / 4)) * 8;
+        *reinterpret_cast<uint4*>(&dzr[u][off]) = cur.dz[r];
+      } else {
+        const int qq = q - 8 * NOP, row = qq / 4, off = (qq % 4) * 8;
+        *reinterpret_cast<uint4*>(&dzt[row][off]) = cur.dz[r];
+      }
     }
-    for (int q = threadIdx.x; q < kMfStep * (NKB * 32 - NO); q += 256)   // outputs past NO are zero
-      dzs[q / (NKB * 32 - NO)][NO + q % (NKB * 32 - NO)] = 0.f;
     if (threadIdx.x < kMfStep) {
 #pragma unroll
       for (int i = 0; i < 5 + NQ; ++i) sc[threadIdx.x][i] = cur.scal[i];
@@ -2063,8 +2097,8 @@ __global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restri
     *reinterpret_cast<uint4*>(&xs[threadIdx.x / 8][(threadIdx.x % 8) * 8]) = cur.x;
     const uint2 dxr[2] = {cur.dx[0], cur.dx[1]};
     __syncthreads();
-    // the input gradients of this step (read here: prefetched, the Q rows
-    // would hold too many registers)
+    // the input gradients of this step (read here: prefetching them a step
+    // ahead as well measured no faster and holds 16 more registers)
     uint2 dinv[NQ][2];
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -2081,11 +2115,8 @@ __global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restri
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
-        float f[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = dzs[u][32 * kb + 8 * g4 + e];
-        uint4 bh, bl;
-        split_bf16x8(f, bh, bl);
+        const uint4 bh = *reinterpret_cast<const uint4*>(&dzr[u][32 * kb + 8 * g4]);
+        const uint4 bl = *reinterpret_cast<const uint4*>(&dzr[u][NOP + 32 * kb + 8 * g4]);
         acc = mfma_16x16x32(wfrag[kb], bh, acc);
         acc = mfma_16x16x32(wfrag[kb], bl, acc);
       }
@@ -2120,11 +2151,8 @@ __global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restri
                                   xb[4] | ((uint32_t)xb[5] << 16), xb[6] | ((uint32_t)xb[7] << 16));
 #pragma unroll
       for (int ob = 0; ob <= NQ; ++ob) {
-        float f[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) f[e] = dzs[8 * g4 + e][16 * ob + l16];
-        uint4 ah, al;
-        split_bf16x8(f, ah, al);
+        const uint4 ah = *reinterpret_cast<const uint4*>(&dzt[16 * ob + l16][8 * g4]);
+        const uint4 al = *reinterpret_cast<const uint4*>(&dzt[NOP + 16 * ob + l16][8 * g4]);
         dw[ob] = mfma_16x16x32(ah, bx, dw[ob]);
         dw[ob] = mfma_16x16x32(al, bx, dw[ob]);
       }
@@ -2181,8 +2209,12 @@ hipError_t launch_bwd_dhpre_multi(const xhc_dims* d, int Q, const void* X, const
   return hipGetLastError();
 }
 
+// prep [T][16 (Q + 1) + 8] floats, then (16-byte aligned) the packed dz'
+static size_t multi_prep_floats(int64_t T, int Q) { return (size_t)T * (16 * (Q + 1) + 8); }
+static int64_t multi_nop(int Q) { return (16 * (Q + 1) + 31) / 32 * 32; }
 size_t bwd_rows_multi_ws_bytes(const xhc_dims* d, int Q) {
-  return (size_t)d->T * (16 * (Q + 1) + 8) * sizeof(float);
+  const size_t Tp = (size_t)((d->T + kDzBlock - 1) / kDzBlock * kDzBlock);
+  return multi_prep_floats(d->T, Q) * sizeof(float) + 16 + Tp * 2 * multi_nop(Q) * 2 * sizeof(uint16_t);
 }
 
 hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* dX, const float* W_r,
@@ -2206,14 +2238,20 @@ hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* 
   const dim3 g((unsigned)(NC / kMfRows), (unsigned)nchunk);
   const int64_t np = T * (16 * (Q + 1) + 8);
   const dim3 gp((unsigned)((np + 255) / 256));
+  const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock, nop = multi_nop(Q);
+  const uintptr_t a = reinterpret_cast<uintptr_t>(prep + multi_prep_floats(T, Q));
+  uint16_t* dzp = reinterpret_cast<uint16_t*>((a + 15) / 16 * 16);
+  const dim3 gk((unsigned)((Tp * nop + 255) / 256));
   if (Q == 4) {
     k_multi_prep<4><<<gp, dim3(256), 0, s>>>(m, T, N, NA, prep);
+    k_dz_pack_multi<4><<<gk, dim3(256), 0, s>>>(prep, T, dzp, dzp + Tp * 2 * nop);
     k_bwd_rows_multi<4><<<g, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), reinterpret_cast<uint16_t*>(dX),
-                                                m, prep, T, N, C, NA, kRowChunk);
+                                                m, prep, dzp, T, N, C, NA, kRowChunk);
   } else {
     k_multi_prep<2><<<gp, dim3(256), 0, s>>>(m, T, N, NA, prep);
+    k_dz_pack_multi<2><<<gk, dim3(256), 0, s>>>(prep, T, dzp, dzp + Tp * 2 * nop);
     k_bwd_rows_multi<2><<<g, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), reinterpret_cast<uint16_t*>(dX),
-                                                m, prep, T, N, C, NA, kRowChunk);
+                                                m, prep, dzp, T, N, C, NA, kRowChunk);
   }
   return hipGetLastError();
 }
