@@ -173,7 +173,7 @@ def _time(fn, iters, stream):
     return e0.elapsed_time(e1) / iters
 
 
-SECTIONS = ("flash_q4", "flash_q2", "mhc_n4", "prefill_t2048", "bwd_mlp_sweep", "flash_bwd_q4")
+SECTIONS = ("flash_q4", "flash_q2", "mhc_n4", "prefill_t2048", "bwd_mlp_sweep", "bwd_mlp_n16", "flash_bwd_q4")
 
 
 def extra_sections(dev, stream, iters=5, only=None):
@@ -237,10 +237,12 @@ def extra_sections(dev, stream, iters=5, only=None):
                                 "ms_per_block": pre_ms["auto"], "ms_per_block_multi": pre_ms["multi"],
                                 "ms_per_block_fused": pre_ms["fused"],
                                 "tokens_per_s": 2048 / (pre_ms["auto"] * 1e-3)}
-    if want("bwd_mlp_sweep"):
+    for sec_name, Ns in (("bwd_mlp_sweep", (4, 8, 16, 32)), ("bwd_mlp_n16", (16,))):
+        if not want(sec_name) or (sec_name == "bwd_mlp_n16" and only is None):
+            continue   # (the N = 16 case alone, for profiling; part of the sweep otherwise)
         # backward of an MLP-type sublayer, T = 8192, k = 4, C = 4096, N = 4, 8, 16, 32
         res = {}
-        for N in (4, 8, 16, 32):
+        for N in Ns:
             w = synth.bwd_sweep(N, 4)
             inp = synth.sublayer_inputs(w, 10, device=dev, grads=True)
             sub = X.TrainableSublayer(X.dims_for(w), inp, dev)
@@ -256,8 +258,8 @@ def extra_sections(dev, stream, iters=5, only=None):
                             "tokens_per_s_backward": w.T / ((ms - fwd_ms) * 1e-3)}
             del sub, inp, st
             torch.cuda.empty_cache()
-        out["bwd_mlp_sweep"] = {"workload": "xHC MLP-type sublayer backward, T=8192, k=4, m=2, C=4096, "
-                                            "N in {4, 8, 16, 32}", **res}
+        out[sec_name] = {"workload": "xHC MLP-type sublayer backward, T=8192, k=4, m=2, C=4096, "
+                                     f"N in {{{', '.join(str(n) for n in Ns)}}}", **res}
     if want("flash_bwd_q4"):
         # xHC-Flash group backward, Q = 4, T = 8192, N = 16, k = 4, C = 4096
         w = synth.bwd_sweep(16, 4)
