@@ -270,7 +270,9 @@ def extra_sections(dev, stream, iters=5, only=None):
         st = X0.clone()
         ffwd = _time(lambda: (st.copy_(X0), grp.forward(st, fd["F_list"], stream)), 2, stream)
         cp = _time(lambda: st.copy_(X0), 2, stream)
-        fbwd = _time(lambda: grp.backward(X0, fd["G_X"], fd["G_in_list"], fd["F_list"], stream), 2, stream)
+        G_in = torch.stack(fd["G_in_list"])   # [Q, T, C], as the backward takes it
+        # dL/dX is formed in place in the upstream gradient's buffer
+        fbwd = _time(lambda: grp.backward(X0, fd["G_X"], G_in, fd["F_list"], stream, in_place=True), 2, stream)
         out["flash_bwd_q4"] = {"workload": "xHC-Flash group backward, Q=4, T=8192, N=16, k=4, m=2, C=4096",
                                "ms_forward_with_saves": ffwd - cp, "ms_backward": fbwd,
                                "tokens_per_s_per_sublayer_backward": Q * w.T / (fbwd * 1e-3)}

@@ -331,8 +331,10 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
  *   from xhc_flash_post_bwd (q = 2..Q); dp [T,k] the accumulated dp;
  *   dXn [T,N,C] dL/dX'; da0 [T,k,C] fp32 dL/da^(0) (da after the q = 1 reverse)
  * Outputs (overwritten): dX [T,N,C] = dL/dX; dW_r; dW_pre [Q,N*C,N];
- * dalpha_pre [Q]; db_pre [Q,N].  Token sums run in a fixed order
- * (deterministic).                                                          */
+ * dalpha_pre [Q]; db_pre [Q,N].  dX may be dXn itself (in place): the
+ * untouched streams then keep their gradient without a copy and only the k
+ * active rows of each token are first overwritten with da0.  Token sums run
+ * in a fixed order (deterministic).                                         */
 xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const void* dXn, void* da, const void* Xact,
                               const void* F, const float* conv_w, const int32_t* idx, const float* p,
                               const float* Hpost, const float* Hres, const void* packed_act, const float* W_post,

@@ -806,7 +806,7 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
   if (!X || !packed_full || !W_r || !W_pre || !alpha_pre || !b_pre || !idx || !p || !Hpre || !d_input ||
       !dHpre_act || !dp || !dXn || !da0 || !dX || !dW_r || !dW_pre || !dalpha_pre || !db_pre || !workspace)
     return XHC_EINVAL;
-  if (dX == X || dX == dXn || dX == da0) return XHC_EINVAL;
+  if (dX == X || dX == da0) return XHC_EINVAL;   // dX == dXn: in place
   if (!aligned16(X) || !aligned16(packed_full) || !aligned16(d_input) || !aligned16(dXn) || !aligned16(da0) ||
       !aligned16(dX) || !aligned16(workspace))
     return XHC_EUNSUPPORTED;
@@ -831,8 +831,9 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
                                              (int)k, F32(w.part), s));
   // dL/dX starts as the gradient of the state after the group: the untouched
   // streams pass it through, the active ones carry the reverse of the group
-  XHC_STEP("fpbwd_scatter", launch_fbwd_scatter(d->state_dtype, T, (int)N, (int)k, (int)C, idx, dXn,
-                                                 reinterpret_cast<const float*>(da0), dX, s));
+  XHC_STEP("fpbwd_scatter", launch_fbwd_scatter(d->state_dtype, T, (int)N, (int)k, (int)C, idx,
+                                                 dX == dXn ? nullptr : dXn, reinterpret_cast<const float*>(da0), dX,
+                                                 s));
   // pre-map q + 1 (and the router with the first): dL/dH^pre,q+1 of the active
   // streams comes from the sublayer reverse (q >= 1); the base readouts of q >=
   // 1 leave the active streams out.  This view has no active-row projection

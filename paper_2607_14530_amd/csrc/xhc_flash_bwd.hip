@@ -114,6 +114,22 @@ __global__ __launch_bounds__(256) void k_fbwd_scatter(int64_t T, int N, int k, i
   }
 }
 
+// the same in place: row (t, I_j) of dX = slot j of da0 (one workgroup per
+// active row; the other rows already hold G_X)
+template <typename TS>
+__global__ __launch_bounds__(256) void k_fbwd_scatter_act(int64_t T, int N, int k, int C,
+                                                          const int32_t* __restrict__ idx,
+                                                          const float* __restrict__ da0, TS* __restrict__ dX) {
+  const int64_t r = blockIdx.x, t = r / k;
+  const int j = (int)(r % k);
+  TS* dst = dX + (t * N + idx[t * k + j]) * (int64_t)C;
+  for (int c = threadIdx.x * 8; c < C; c += 256 * 8) {
+    float f[8];
+    Vec8<float>::load(da0 + r * (int64_t)C + c, f);
+    Vec8<TS>::store(dst + c, f);
+  }
+}
+
 // Hm[t, i] = 0 for the active streams of token t, Hpre[t, i] otherwise
 __global__ __launch_bounds__(256) void k_fbwd_mask(int64_t T, int N, int k, const int32_t* __restrict__ idx,
                                                    const float* __restrict__ Hpre, float* __restrict__ Hm) {
@@ -200,6 +216,11 @@ hipError_t launch_fbwd_gather(int state_dtype, int64_t T, int N, int k, int C, c
 
 hipError_t launch_fbwd_scatter(int state_dtype, int64_t T, int N, int k, int C, const int32_t* idx, const void* GX,
                                const float* da0, void* dX, hipStream_t s) {
+  if (!GX) {   // in place: dX holds G_X; only the active rows change
+    XHC_FTS(state_dtype, k_fbwd_scatter_act<TS><<<dim3((unsigned)(T * k)), dim3(256), 0, s>>>(
+                             T, N, k, C, idx, da0, reinterpret_cast<TS*>(dX)));
+    return hipGetLastError();
+  }
   XHC_FTS(state_dtype, k_fbwd_scatter<TS><<<dim3((unsigned)(T * N)), dim3(256), 0, s>>>(
                            T, N, k, C, idx, reinterpret_cast<const TS*>(GX), da0, reinterpret_cast<TS*>(dX)));
   return hipGetLastError();

@@ -427,7 +427,11 @@ class TrainableFlashGroup(FlashGroup):
             self.step(q, X, F_list[q - 1], stream, Xact_save=self.Xact[q - 1])
         return X
 
-    def backward(self, X0, dXn, d_inputs, F_list, stream=None):
+    def backward(self, X0, dXn, d_inputs, F_list, stream=None, in_place=False):
+        """Group reverse given dL/dX' (dXn) and dL/d input_q (d_inputs: a list
+        of Q [T, C] tensors, or one [Q, T, C] tensor).  With in_place, dL/dX
+        is formed in dXn itself (only the active rows of each token are
+        rewritten before the pre-map passes add to it) and g["X"] is dXn."""
         d, Q = self.d, self.Q
         T, N, k, C = d.T, d.N, d.k, d.C
         dev = X0.device
@@ -455,8 +459,8 @@ class TrainableFlashGroup(FlashGroup):
                 g["W_post_list"][q - 1], a_post[q - 1:q], g["b_post"][q - 1], g["W_res"] if last else None,
                 a_res if last else None, g["b_res"] if last else None, dp, dhact[q - 2] if q >= 2 else None,
                 self.ws_post_bwd, stream)
-        din = torch.stack(list(d_inputs)).contiguous()
-        g["X"] = torch.empty_like(X0)
+        din = d_inputs.contiguous() if torch.is_tensor(d_inputs) else torch.stack(list(d_inputs)).contiguous()
+        g["X"] = dXn if in_place else torch.empty_like(X0)
         g["W_r"], g["W_pre"] = torch.empty_like(self.W_r), torch.empty_like(self.W_pre)
         g["alpha_pre"], g["b_pre"] = torch.empty(Q, **f32), torch.empty(Q, N, **f32)
         xhc_flash_pre_bwd(d, Q, X0, self.packed_full, self.W_r, self.W_pre, self.alpha_pre, self.b_pre, self.idx,

@@ -115,6 +115,23 @@ def test_flash_backward_mid_size():
         assert_grad_close(g[n], ref[n], n)
 
 
+def test_flash_backward_in_place_gives_the_same_gradients():
+    """dX = dXn (xhc_flash_pre_bwd in place, stacked input gradients): every
+    gradient bit-identical to the out-of-place call."""
+    w = W(T=128, S=64, N=16, k=4, m=2, C=512, Kr=4, name="fbwd-inplace")
+    d, grp, state, g = _run(w, 4, seed=7)
+    GX = d["G_X"].clone()
+    gi = grp.backward(d["X"], GX, torch.stack(d["G_in_list"]), d["F_list"], in_place=True)
+    torch.cuda.synchronize()
+    assert gi["X"].data_ptr() == GX.data_ptr()
+    for n, v in g.items():
+        vs = v if isinstance(v, list) else [v]
+        ws = gi[n] if isinstance(gi[n], list) else [gi[n]]
+        for x, y in zip(vs, ws):
+            if x is not None:
+                assert torch.equal(x, y), n
+
+
 def test_flash_backward_is_deterministic():
     w = W(T=128, S=64, N=16, k=4, m=2, C=512, Kr=4, name="fbwd-det")
     a = _run(w, 4, seed=5)[3]
