@@ -262,12 +262,15 @@ xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full
  *   alpha_pre [Q], b_pre [Q,N], alpha_post1 [1], b_post1 [k K_1] fp32 device
  * Outputs: input1 [T,C] = sum_i H^pre,1_i x_i; base [Q-1,T,C] where base[q-2] =
  * sum_{i not in I} H^pre,q_i x_i (q = 2..Q); idx, p as in xhc_pre; Hpre [Q,T,N];
- * Hpost1 [T,k,K_1].                                                           */
+ * Hpost1 [T,k,K_1].  saved [Q,T,2N + k + k*k + 4] fp32 or NULL: per pre-map q
+ * and token the router logits, the pre-map logits and the norm statistics
+ * (the other fields zero), which xhc_flash_pre_bwd then reads instead of
+ * recomputing them from X.                                                    */
 xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full,
                          const void* packed_act1, const float* alpha_pre, const float* b_pre,
                          const float* alpha_post1, const float* b_post1, void* input1, void* base, int32_t* idx,
-                         float* p, float* Hpre, float* Hpost1, void* workspace, size_t workspace_bytes,
-                         void* stream);
+                         float* p, float* Hpre, float* Hpost1, float* saved, void* workspace,
+                         size_t workspace_bytes, void* stream);
 
 /* xhc_flash_post - after sublayer q of the group (1 <= q <= Q).
  *   X       [T,N,C] in/out: rows X[t, idx[t,j], :] <- (q == Q ? sum_l Hres[t,j,l]
@@ -331,7 +334,9 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
  *   from xhc_flash_post_bwd (q = 2..Q); dp [T,k] the accumulated dp;
  *   dXn [T,N,C] dL/dX'; da0 [T,k,C] fp32 dL/da^(0) (da after the q = 1 reverse)
  * Outputs (overwritten): dX [T,N,C] = dL/dX; dW_r; dW_pre [Q,N*C,N];
- * dalpha_pre [Q]; db_pre [Q,N].  dX may be dXn itself (in place): the
+ * dalpha_pre [Q]; db_pre [Q,N].  saved: the records xhc_flash_pre wrote for
+ * this group, or NULL (they are then recomputed from X, one more read of
+ * the state).  dX may be dXn itself (in place): the
  * untouched streams then keep their gradient without a copy and only the k
  * active rows of each token are first overwritten with da0.  Token sums run
  * in a fixed order (deterministic).                                         */
@@ -345,10 +350,10 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
                               void* workspace, size_t workspace_bytes, void* stream);
 xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full, const float* W_r,
                              const float* W_pre, const float* alpha_pre, const float* b_pre, const int32_t* idx,
-                             const float* p, const float* Hpre, const void* d_input, const float* dHpre_act,
-                             const float* dp, const void* dXn, const void* da0, void* dX, float* dW_r,
-                             float* dW_pre, float* dalpha_pre, float* db_pre, void* workspace, size_t workspace_bytes,
-                             void* stream);
+                             const float* p, const float* Hpre, const float* saved, const void* d_input,
+                             const float* dHpre_act, const float* dp, const void* dXn, const void* da0, void* dX,
+                             float* dW_r, float* dW_pre, float* dalpha_pre, float* db_pre, void* workspace,
+                             size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------ final stream reduction
  * App. "Final Stream Reduction": before the last RMSNorm and the unembedding

@@ -531,8 +531,8 @@ xhc_status xhc_post_noalloc(const xhc_dims* d, void* X, const void* F, const flo
 xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full,
                          const void* packed_act1, const float* alpha_pre, const float* b_pre,
                          const float* alpha_post1, const float* b_post1, void* input1, void* base, int32_t* idx,
-                         float* p, float* Hpre, float* Hpost1, void* workspace, size_t workspace_bytes,
-                         void* stream) {
+                         float* p, float* Hpre, float* Hpost1, float* saved, void* workspace,
+                         size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
   if (Q != 2 && Q != 4) return XHC_EINVAL;
@@ -557,9 +557,12 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
   hipError_t e = hipSuccess;
   XHC_STEP("flash_proj_full",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, NC, packed_full, nf, nullptr, d->k, part, s));
+  // the records the backward reads (one per pre-map; fields it does not use stay zero)
+  const int nsave = saved_floats(d->N, d->k, 1);
+  if (saved) XHC_STEP("flash_save_zero", launch_fill0(saved, (size_t)Q * d->T * nsave * sizeof(float), s));
   XHC_STEP("flash_route", launch_pre_route(part, proj_chunks(d->state_dtype, false, NC, d->C, nf, d->T), nf, d->T, d->N, d->m, d->k, Q, d->C, colsum,
-                                           alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, nullptr, 0, 0,
-                                           d->router, s));
+                                           alpha_pre, 1, b_pre, d->eps, idx, p, Hpre, sums, saved,
+                                           saved ? nsave : 0, saved ? nsave - 4 : 0, d->router, s, -1));
   XHC_STEP("flash_proj_active",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act1, na, idx, d->k, part, s));
   XHC_STEP("flash_coef1", launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, na, d->T), na, d->T,
@@ -794,10 +797,10 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
 
 xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full, const float* W_r,
                              const float* W_pre, const float* alpha_pre, const float* b_pre, const int32_t* idx,
-                             const float* p, const float* Hpre, const void* d_input, const float* dHpre_act,
-                             const float* dp, const void* dXn, const void* da0, void* dX, float* dW_r,
-                             float* dW_pre, float* dalpha_pre, float* db_pre, void* workspace, size_t workspace_bytes,
-                             void* stream) {
+                             const float* p, const float* Hpre, const float* saved, const void* d_input,
+                             const float* dHpre_act, const float* dp, const void* dXn, const void* da0, void* dX,
+                             float* dW_r, float* dW_pre, float* dalpha_pre, float* db_pre, void* workspace,
+                             size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
   if (Q != 2 && Q != 4) return XHC_EINVAL;
@@ -824,11 +827,13 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
   const float* colsum = reinterpret_cast<const float*>(reinterpret_cast<const char*>(packed_full) +
                                                        packed_frag_bytes(NC, nf));
   hipError_t e = hipSuccess;
-  XHC_STEP("fpbwd_zero", launch_fill0(ws + w.saved, (size_t)T * nsave * sizeof(float), s));
+  if (!saved) XHC_STEP("fpbwd_zero", launch_fill0(ws + w.saved, (size_t)T * nsave * sizeof(float), s));
   XHC_STEP("fpbwd_zero", launch_fill0(ws + w.wpost0, w.alpha_e - w.wpost0, s));   // zero operands
-  // the group-entry logits and statistics, recomputed as the forward made them
-  XHC_STEP("fpbwd_proj", launch_proj_partial(d->state_dtype, X, T, (int)N, (int)C, NC, packed_full, nf, nullptr,
-                                             (int)k, F32(w.part), s));
+  // the group-entry logits and statistics: saved by the forward, or
+  // recomputed as the forward made them
+  if (!saved)
+    XHC_STEP("fpbwd_proj", launch_proj_partial(d->state_dtype, X, T, (int)N, (int)C, NC, packed_full, nf, nullptr,
+                                               (int)k, F32(w.part), s));
   // dL/dX starts as the gradient of the state after the group: the untouched
   // streams pass it through, the active ones carry the reverse of the group
   XHC_STEP("fpbwd_scatter", launch_fbwd_scatter(d->state_dtype, T, (int)N, (int)k, (int)C, idx,
@@ -845,11 +850,14 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
   auto pass = [&](int q, int phase) -> hipError_t {
     char* wq = ws + w.pre + (w.fused ? (size_t)q * w.pre_slice : 0);
     float* hm = F32(w.hmask) + (int64_t)q * T * N;
+    const float* rec = saved ? saved + (int64_t)q * T * nsave : F32(w.saved);   // pre-map q's records
     if (phase != kBwdPreReduce) {
-      hipError_t e1 = launch_pre_route(F32(w.part), proj_chunks(d->state_dtype, false, NC, (int)C, nf, T), nf, T,
-                                       (int)N, d->m, (int)k, Q, C, colsum, alpha_pre, 1, b_pre, d->eps,
-                                       reinterpret_cast<int32_t*>(ws + w.idx_s), F32(w.p_s), F32(w.hpre_s),
-                                       F32(w.sums), F32(w.saved), nsave, nsave - 4, d->router, s, q);
+      hipError_t e1 = hipSuccess;
+      if (!saved)
+        e1 = launch_pre_route(F32(w.part), proj_chunks(d->state_dtype, false, NC, (int)C, nf, T), nf, T,
+                              (int)N, d->m, (int)k, Q, C, colsum, alpha_pre, 1, b_pre, d->eps,
+                              reinterpret_cast<int32_t*>(ws + w.idx_s), F32(w.p_s), F32(w.hpre_s),
+                              F32(w.sums), F32(w.saved), nsave, nsave - 4, d->router, s, q);
       if (e1 == hipSuccess) e1 = launch_fbwd_alpha(alpha_pre + q, nullptr, nullptr, F32(w.alpha_e), s);
       if (e1 == hipSuccess && q >= 1) e1 = launch_fbwd_mask(T, (int)N, (int)k, idx, Hpre + (int64_t)q * T * N, hm, s);
       if (e1 != hipSuccess) return e1;
@@ -857,7 +865,7 @@ xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const 
     hrd[q] = q >= 1 ? hm : Hpre;
     wsq[q] = wq;
     return launch_bwd_pre(&en, X, colsum, W_r, W_pre + (int64_t)q * NC * N, F32(w.wres0), F32(w.wpost0),
-                          F32(w.alpha_e), F32(w.bres0), F32(w.saved), idx, p, Hpre + (int64_t)q * T * N,
+                          F32(w.alpha_e), F32(w.bres0), rec, idx, p, Hpre + (int64_t)q * T * N,
                           F32(w.hpost0), reinterpret_cast<const char*>(d_input) + (size_t)q * T * C * es,
                           F32(w.dhres0), F32(w.dhpost0), q == 0 ? dp : F32(w.dp0), dX, q == 0 ? dW_r : F32(w.dwr),
                           dW_pre + (int64_t)q * NC * N, F32(w.dwres), F32(w.dwpost), F32(w.dalpha),

@@ -77,7 +77,7 @@ hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int
                             int npre, int64_t C, const float* colsum, const float* alpha_pre, int alpha_stride,
                             const float* b_pre, float eps, int32_t* idx, float* p, float* Hpre, float* sums,
                             float* saved, int nsave, int save_stats_at, int router, hipStream_t s,
-                            int save_pre = 0);   // which pre-map's z goes to saved[N .. 2N)
+                            int save_pre = 0);   // which pre-map's z goes to saved[N .. 2N); -1: all, one record each
 hipError_t launch_pre_coef(const float* part, int64_t nchunk, int64_t nout, int64_t T, int k, int Kq,
                            int with_res, int64_t C, const float* alpha_post, const float* alpha_res,
                            const float* b_post, const float* b_res, float eps, int iters, float delta,

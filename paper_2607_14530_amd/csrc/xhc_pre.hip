@@ -105,10 +105,14 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
   if (t >= T) return;
   const float mu = sums[(int64_t)(NO - 2) * T + t] / (float)NC;
   const float nu = sums[(int64_t)(NO - 1) * T + t] / (float)NC;
-  if (saved) {
-    saved[t * nsave + save_stats_at] = mu;
-    saved[t * nsave + save_stats_at + 1] = nu;
-  }
+  // save_pre < 0: one record per pre-map q at saved + q T nsave (router
+  // logits and statistics in each)
+  const int nrec = save_pre < 0 ? npre : 1;
+  if (saved)
+    for (int r = 0; r < nrec; ++r) {
+      saved[(r * T + t) * nsave + save_stats_at] = mu;
+      saved[(r * T + t) * nsave + save_stats_at + 1] = nu;
+    }
   const float r_ln = 1.0f / sqrtf(ln_variance(mu, nu) + eps);
   const float r_rms = 1.0f / sqrtf(nu + eps);
   float z[kMaxN];
@@ -122,12 +126,14 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
     p[t * k + j] = pp[j];
   }
   if (saved)
-    for (int i = 0; i < N; ++i) saved[t * nsave + i] = z[i];
+    for (int r = 0; r < nrec; ++r)
+      for (int i = 0; i < N; ++i) saved[(r * T + t) * nsave + i] = z[i];
   for (int q = 0; q < npre; ++q) {
     const float a = alpha_pre[q * alpha_stride];
     for (int i = 0; i < N; ++i) {
       const float zp = sums[(int64_t)(N + q * N + i) * T + t] * r_rms;
-      if (saved && q == save_pre) saved[t * nsave + N + i] = zp;
+      if (saved && save_pre < 0) saved[((int64_t)q * T + t) * nsave + N + i] = zp;
+      else if (saved && q == save_pre) saved[t * nsave + N + i] = zp;
       Hpre[((int64_t)q * T + t) * N + i] = sigmoidf(a * zp + b_pre[q * N + i]);
     }
   }

@@ -86,10 +86,10 @@ _SIGS = {
     "xhc_post": (ctypes.c_int, [_D] + [_P] * 9 + [ctypes.c_size_t, _P]),
     "xhc_saved_floats": (ctypes.c_size_t, [_D]),
     "xhc_post_noalloc": (ctypes.c_int, [_D] + [_P] * 9),
-    "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 14 + [ctypes.c_size_t, _P]),
+    "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 15 + [ctypes.c_size_t, _P]),
     "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 18 + [ctypes.c_size_t, _P]),
     "xhc_flash_post_bwd": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 29 + [ctypes.c_size_t, _P]),
-    "xhc_flash_pre_bwd": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 20 + [ctypes.c_size_t, _P]),
+    "xhc_flash_pre_bwd": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 21 + [ctypes.c_size_t, _P]),
     "xhc_post_bwd": (ctypes.c_int, [_D] + [_P] * 16 + [ctypes.c_size_t, _P]),
     "xhc_pre_bwd": (ctypes.c_int, [_D] + [_P] * 27 + [ctypes.c_size_t, _P]),
     "xhc_stream_sum": (ctypes.c_int, [_D, _P, _P, _P]),
@@ -213,10 +213,10 @@ def _nbytes(t):
 
 
 def xhc_flash_pre(d, Q, X, packed_full, packed_act1, alpha_pre, b_pre, alpha_post1, b_post1, input1, base, idx,
-                  p, Hpre, Hpost1, workspace, stream=None):
+                  p, Hpre, Hpost1, saved, workspace, stream=None):
     _call("xhc_flash_pre", ctypes.byref(d), Q, _ptr(X), _ptr(packed_full), _ptr(packed_act1), _ptr(alpha_pre),
           _ptr(b_pre), _ptr(alpha_post1), _ptr(b_post1), _ptr(input1), _ptr(base), _ptr(idx), _ptr(p), _ptr(Hpre),
-          _ptr(Hpost1), _ptr(workspace), _nbytes(workspace), _stream(stream))
+          _ptr(Hpost1), _ptr(saved), _ptr(workspace), _nbytes(workspace), _stream(stream))
 
 
 def xhc_flash_post(d, Q, q, X, F, conv_w, idx, p, Hpost, Hres, Hpre_next, base_next, input_next, packed_act_next,
@@ -237,10 +237,11 @@ def xhc_flash_post_bwd(d, Q, q, dXn, da, Xact, F, conv_w, idx, p, Hpost, Hres, p
           _ptr(db_res), _ptr(dp), _ptr(dHpre_act), _ptr(workspace), _nbytes(workspace), _stream(stream))
 
 
-def xhc_flash_pre_bwd(d, Q, X, packed_full, W_r, W_pre, alpha_pre, b_pre, idx, p, Hpre, d_input, dHpre_act, dp,
-                      dXn, da0, dX, dW_r, dW_pre, dalpha_pre, db_pre, workspace, stream=None):
+def xhc_flash_pre_bwd(d, Q, X, packed_full, W_r, W_pre, alpha_pre, b_pre, idx, p, Hpre, saved, d_input, dHpre_act,
+                      dp, dXn, da0, dX, dW_r, dW_pre, dalpha_pre, db_pre, workspace, stream=None):
     _call("xhc_flash_pre_bwd", ctypes.byref(d), Q, _ptr(X), _ptr(packed_full), _ptr(W_r), _ptr(W_pre),
-          _ptr(alpha_pre), _ptr(b_pre), _ptr(idx), _ptr(p), _ptr(Hpre), _ptr(d_input), _ptr(dHpre_act), _ptr(dp),
+          _ptr(alpha_pre), _ptr(b_pre), _ptr(idx), _ptr(p), _ptr(Hpre), _ptr(saved), _ptr(d_input),
+          _ptr(dHpre_act), _ptr(dp),
           _ptr(dXn), _ptr(da0), _ptr(dX), _ptr(dW_r), _ptr(dW_pre), _ptr(dalpha_pre), _ptr(db_pre),
           _ptr(workspace), _nbytes(workspace), _stream(stream))
 
@@ -367,10 +368,10 @@ class FlashGroup:
         self.ws_pre = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_PRE, Q), dev)
         self.ws_post = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_POST, Q), dev)
 
-    def pre(self, X, stream=None):
+    def pre(self, X, stream=None, saved=None):
         xhc_flash_pre(self.d, self.Q, X, self.packed_full, self.packed_act[0], self.alpha_pre, self.b_pre,
                       self.alpha_post[0], self.b_post[0], self.inputs[0], self.base, self.idx, self.p, self.Hpre,
-                      self.Hpost[0], self.ws_pre, stream)
+                      self.Hpost[0], saved, self.ws_pre, stream)
 
     def step(self, q, X, F, stream=None, Xact_save=None):
         """Write-back of sublayer q (1-based); for q < Q also forms inputs[q]."""
@@ -418,20 +419,24 @@ class TrainableFlashGroup(FlashGroup):
         self.a_post = [torch.tensor([a], **f32) for a in weights["alpha_post"]]
         self.a_res = torch.tensor([weights["alpha_res"]], **f32)
         self.Xact = [torch.empty(T, k, C, dtype=self.inputs[0].dtype, device=dev) for _ in range(Q)]
+        # the routing records of the group entry, one per pre-map (xhc_flash_pre writes them)
+        self.saved = torch.empty(Q, T, 2 * N + k + k * k + 4, **f32)
         self.ws_post_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_POST_BWD, Q), dev)
         self.ws_pre_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_PRE_BWD, Q), dev)
 
     def forward(self, X, F_list, stream=None):
-        self.pre(X, stream)
+        self.pre(X, stream, saved=self.saved)
         for q in range(1, self.Q + 1):
             self.step(q, X, F_list[q - 1], stream, Xact_save=self.Xact[q - 1])
         return X
 
-    def backward(self, X0, dXn, d_inputs, F_list, stream=None, in_place=False):
+    def backward(self, X0, dXn, d_inputs, F_list, stream=None, in_place=False, recompute=False):
         """Group reverse given dL/dX' (dXn) and dL/d input_q (d_inputs: a list
         of Q [T, C] tensors, or one [Q, T, C] tensor).  With in_place, dL/dX
         is formed in dXn itself (only the active rows of each token are
-        rewritten before the pre-map passes add to it) and g["X"] is dXn."""
+        rewritten before the pre-map passes add to it) and g["X"] is dXn.
+        The entry reverse reads the routing records the forward saved, or,
+        with recompute, forms them again from X0."""
         d, Q = self.d, self.Q
         T, N, k, C = d.T, d.N, d.k, d.C
         dev = X0.device
@@ -464,8 +469,9 @@ class TrainableFlashGroup(FlashGroup):
         g["W_r"], g["W_pre"] = torch.empty_like(self.W_r), torch.empty_like(self.W_pre)
         g["alpha_pre"], g["b_pre"] = torch.empty(Q, **f32), torch.empty(Q, N, **f32)
         xhc_flash_pre_bwd(d, Q, X0, self.packed_full, self.W_r, self.W_pre, self.alpha_pre, self.b_pre, self.idx,
-                          self.p, self.Hpre, din, dhact, dp, dXn, da, g["X"], g["W_r"], g["W_pre"], g["alpha_pre"],
-                          g["b_pre"], self.ws_pre_bwd, stream)
+                          self.p, self.Hpre, None if recompute else self.saved, din, dhact, dp, dXn, da, g["X"],
+                          g["W_r"], g["W_pre"],
+                          g["alpha_pre"], g["b_pre"], self.ws_pre_bwd, stream)
         g["W_pre_list"] = list(g.pop("W_pre"))
         g["b_pre"] = list(g["b_pre"])
         g["alpha_post"], g["alpha_res"] = a_post, a_res[0]

@@ -132,6 +132,21 @@ def test_flash_backward_in_place_gives_the_same_gradients():
                 assert torch.equal(x, y), n
 
 
+def test_flash_backward_from_saved_records_equals_recomputed():
+    """xhc_flash_pre_bwd reading the routing records xhc_flash_pre saved gives
+    the same bits as recomputing them from the entry state."""
+    w = W(T=96, S=48, N=16, k=4, m=2, C=512, Kr=4, name="fbwd-saved")
+    d, grp, state, g = _run(w, 4, seed=8)
+    gr = grp.backward(d["X"], d["G_X"], d["G_in_list"], d["F_list"], recompute=True)
+    torch.cuda.synchronize()
+    for n, v in g.items():
+        vs = v if isinstance(v, list) else [v]
+        ws = gr[n] if isinstance(gr[n], list) else [gr[n]]
+        for x, y in zip(vs, ws):
+            if x is not None:
+                assert torch.equal(x, y), n
+
+
 def test_flash_backward_is_deterministic():
     w = W(T=128, S=64, N=16, k=4, m=2, C=512, Kr=4, name="fbwd-det")
     a = _run(w, 4, seed=5)[3]
