@@ -802,9 +802,9 @@ __global__ __launch_bounds__(256) void k_bwd_conv_run(const float* __restrict__ 
 // and a run's additions to the 11 tokens before it to lb[run][i] (token
 // t0 - 11 + i, zero where they are in an earlier sequence); k_bwd_post_fix
 // stores their sums.  The loads of the next 4 tokens are in flight while 4
-// are used.
-template <typename TS, typename TG>
-__global__ __launch_bounds__(256) void k_bwd_post_run(const TG* dXn, TS* __restrict__ X, const TS* __restrict__ Xact,
+// are used.  RESTORE: X is given (the saved rows are read and written back).
+template <typename TS, typename TG, bool RESTORE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k_bwd_post_run(const TG* dXn, TS* __restrict__ X, const TS* __restrict__ Xact,
                                                       const TS* __restrict__ F, int64_t T, int64_t S, int N, int C,
                                                       int k, const float* __restrict__ conv_w,
                                                       const int32_t* __restrict__ idx, const float* __restrict__ Hres,
@@ -872,9 +872,12 @@ __global__ __launch_bounds__(256) void k_bwd_post_run(const TG* dXn, TS* __restr
     for (int j = 0; j < KM; ++j) {
       const int jc = j < k ? j : k - 1;
       const float yv = ld_scalar<TG>(dXn + s_row[ul][j] + c);
-      const float xv = ld_scalar<TS>(Xact + (uc * k + jc) * (int64_t)C + c);
       dy[j] = (ok && j < k) ? yv : 0.f;
-      a[j] = (ok && j < k) ? xv : 0.f;
+      a[j] = 0.f;
+      if (RESTORE) {
+        const float xv = ld_scalar<TS>(Xact + (uc * k + jc) * (int64_t)C + c);
+        a[j] = (ok && j < k) ? xv : 0.f;
+      }
     }
     const float fv = ld_scalar<TS>(F + uc * C + c);
     f = ok ? fv : 0.f;
@@ -948,7 +951,7 @@ __global__ __launch_bounds__(256) void k_bwd_post_run(const TG* dXn, TS* __restr
             for (int j = 0; j < KM; ++j) g = fmaf(s_hr[ul][j * KM + l], dy[j], g);
             const int64_t row = s_row[ul][l];
             st_scalar<TG>(dX + row + c, g);
-            if (X) st_scalar<TS>(X + row + c, av[l]);
+            if (RESTORE) st_scalar<TS>(X + row + c, av[l]);
           }
         }
         P[0] = d[0];
@@ -1846,10 +1849,16 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
         const hipError_t ec = hipMemcpyAsync(dX, dXn, (size_t)T * N * C * sizeof(TG), hipMemcpyDeviceToDevice, s); \
         if (ec != hipSuccess) return ec;                                                                         \
       }                                                                                                          \
-      k_bwd_post_run<TS, TG><<<dim3((unsigned)((C + 255) / 256), (unsigned)nruns), dim3(256), 0, s>>>(           \
-          reinterpret_cast<const TG*>(dXn), reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(Xact),          \
-          reinterpret_cast<const TS*>(F), T, S, N, C, k, conv_w, idx, Hres, coef, reinterpret_cast<TG*>(dX),     \
-          reinterpret_cast<TS*>(dF), cpart, rb, lb);                                                              \
+      if (X)                                                                                                     \
+        k_bwd_post_run<TS, TG, true><<<dim3((unsigned)((C + 255) / 256), (unsigned)nruns), dim3(256), 0, s>>>(   \
+            reinterpret_cast<const TG*>(dXn), reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(Xact),        \
+            reinterpret_cast<const TS*>(F), T, S, N, C, k, conv_w, idx, Hres, coef, reinterpret_cast<TG*>(dX),   \
+            reinterpret_cast<TS*>(dF), cpart, rb, lb);                                                            \
+      else                                                                                                       \
+        k_bwd_post_run<TS, TG, false><<<dim3((unsigned)((C + 255) / 256), (unsigned)nruns), dim3(256), 0, s>>>(  \
+            reinterpret_cast<const TG*>(dXn), nullptr, reinterpret_cast<const TS*>(Xact),                         \
+            reinterpret_cast<const TS*>(F), T, S, N, C, k, conv_w, idx, Hres, coef, reinterpret_cast<TG*>(dX),   \
+            reinterpret_cast<TS*>(dF), cpart, rb, lb);                                                            \
       if (nruns > 1)                                                                                             \
         k_bwd_post_fix<TS><<<dim3((unsigned)((C + 255) / 256), (unsigned)(nruns - 1), 11u), dim3(256), 0, s>>>(   \
             rb, lb, T, S, C, reinterpret_cast<TS*>(dF));                                                         \
