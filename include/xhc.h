@@ -265,11 +265,14 @@ xhc_status xhc_pre_bwd(const xhc_dims* d, const void* X, const void* packed_full
  * Hpost1 [T,k,K_1].  saved [Q,T,2N + k + k*k + 4] fp32 or NULL: per pre-map q
  * and token the router logits, the pre-map logits and the norm statistics
  * (the other fields zero), which xhc_flash_pre_bwd then reads instead of
- * recomputing them from X.                                                    */
+ * recomputing them from X.  saved_act1 [T, 2k + k*K_1 + k*k + 4] fp32 or NULL:
+ * per token the logits and the RMS statistic of sublayer 1's H^post (the
+ * other fields zero), which xhc_flash_post_bwd(q = 1) reads instead of
+ * reprojecting the active rows.                                               */
 xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full,
                          const void* packed_act1, const float* alpha_pre, const float* b_pre,
                          const float* alpha_post1, const float* b_post1, void* input1, void* base, int32_t* idx,
-                         float* p, float* Hpre, float* Hpost1, float* saved, void* workspace,
+                         float* p, float* Hpre, float* Hpost1, float* saved, float* saved_act1, void* workspace,
                          size_t workspace_bytes, void* stream);
 
 /* xhc_flash_post - after sublayer q of the group (1 <= q <= Q).
@@ -285,13 +288,15 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
  *   b_res_next [k*k] iff q + 1 == Q; outputs Hpost_next [T,k,K_{q+1}] and
  *   Hres_next [T,k,k] iff q + 1 == Q, both from the updated active rows.
  *   Xact_save [T,k,C] or NULL: receives the active rows before this sublayer's
- *   write-back (slot order), as xhc_flash_post_bwd needs them.                 */
+ *   write-back (slot order), as xhc_flash_post_bwd needs them.
+ *   saved_next [T, 2k + k*K_{q+1} + k*k + 4] fp32 or NULL (q < Q only): the
+ *   logits and statistic of the next mappings, as saved_act1 for sublayer 1. */
 xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, const void* F, const float* conv_w,
                           const int32_t* idx, const float* p, const float* Hpost, const float* Hres,
                           const float* Hpre_next, const void* base_next, void* input_next,
                           const void* packed_act_next, const float* alpha_next, const float* b_post_next,
                           const float* b_res_next, float* Hpost_next, float* Hres_next, void* Xact_save,
-                          void* workspace, size_t workspace_bytes, void* stream);
+                          float* saved_next, void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------ xHC-Flash backward
  * Reverse mode of one sharing group (xhc_flash_pre, then xhc_flash_post for
@@ -322,6 +327,9 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
  *           alpha_post [1], b_post [k*K_q]; alpha_res [1], b_res [k*k] iff q == Q
  *   Hpre_q  [T,N] = Hpre[q-1] of xhc_flash_pre and d_input [T,C] = dL/d input_q,
  *           both iff q >= 2 (input_1 is reversed by xhc_flash_pre_bwd)
+ *   saved_act  sublayer q's mapping record (saved_act1 of xhc_flash_pre for
+ *           q = 1, saved_next of xhc_flash_post q - 1 otherwise) or NULL (the
+ *           logits are then recomputed from Xact)
  * Outputs (overwritten): dF [T,C]; dconv_w (iff q is even); dW_post,
  * dalpha_post [1], db_post; dW_res, dalpha_res [1], db_res iff q == Q;
  * dHpre_act [T,k] = <d input_q, a^(q-1)_j> iff q >= 2.  dp [T,k] is
@@ -345,9 +353,9 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
                               const float* Hpost, const float* Hres, const void* packed_act, const float* W_post,
                               const float* W_res, const float* alpha_post, const float* alpha_res,
                               const float* b_post, const float* b_res, const float* Hpre_q, const void* d_input,
-                              void* dF, float* dconv_w, float* dW_post, float* dalpha_post, float* db_post,
-                              float* dW_res, float* dalpha_res, float* db_res, float* dp, float* dHpre_act,
-                              void* workspace, size_t workspace_bytes, void* stream);
+                              const float* saved_act, void* dF, float* dconv_w, float* dW_post,
+                              float* dalpha_post, float* db_post, float* dW_res, float* dalpha_res, float* db_res,
+                              float* dp, float* dHpre_act, void* workspace, size_t workspace_bytes, void* stream);
 xhc_status xhc_flash_pre_bwd(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full, const float* W_r,
                              const float* W_pre, const float* alpha_pre, const float* b_pre, const int32_t* idx,
                              const float* p, const float* Hpre, const float* saved, const void* d_input,

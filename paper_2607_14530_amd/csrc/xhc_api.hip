@@ -531,7 +531,7 @@ xhc_status xhc_post_noalloc(const xhc_dims* d, void* X, const void* F, const flo
 xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void* packed_full,
                          const void* packed_act1, const float* alpha_pre, const float* b_pre,
                          const float* alpha_post1, const float* b_post1, void* input1, void* base, int32_t* idx,
-                         float* p, float* Hpre, float* Hpost1, float* saved, void* workspace,
+                         float* p, float* Hpre, float* Hpost1, float* saved, float* saved_act1, void* workspace,
                          size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
@@ -565,10 +565,14 @@ xhc_status xhc_flash_pre(const xhc_dims* d, int32_t Q, const void* X, const void
                                            saved ? nsave : 0, saved ? nsave - 4 : 0, d->router, s, -1));
   XHC_STEP("flash_proj_active",
            launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act1, na, idx, d->k, part, s));
+  // sublayer 1's mapping record for the backward (the layout its reverse uses)
+  const int nsave1 = saved_floats(d->k, d->k, K1);
+  if (saved_act1)
+    XHC_STEP("flash_save_zero", launch_fill0(saved_act1, (size_t)d->T * nsave1 * sizeof(float), s));
   XHC_STEP("flash_coef1", launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, na, d->T), na, d->T,
                                           d->k, K1, 0, d->C, alpha_post1, nullptr, b_post1, nullptr, d->eps,
-                                          d->sinkhorn_iters, d->clamp_delta, Hpost1, nullptr, sums, nullptr, 0, 0, 0,
-                                          s));
+                                          d->sinkhorn_iters, d->clamp_delta, Hpost1, nullptr, sums, saved_act1,
+                                          saved_act1 ? nsave1 : 0, 2 * d->k, nsave1 - 2, s));
   XHC_STEP("flash_dense_read",
            launch_dense_read(d->state_dtype, X, d->T, d->N, d->C, Hpre, Q, idx, d->k, input1, base, s));
   return hip_status(e);
@@ -579,7 +583,7 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
                           const float* Hpre_next, const void* base_next, void* input_next,
                           const void* packed_act_next, const float* alpha_next, const float* b_post_next,
                           const float* b_res_next, float* Hpost_next, float* Hres_next, void* Xact_save,
-                          void* workspace, size_t workspace_bytes, void* stream) {
+                          float* saved_next, void* workspace, size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
   if ((Q != 2 && Q != 4) || q < 1 || q > Q) return XHC_EINVAL;
@@ -626,10 +630,14 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
     float* sums = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + part_bytes(d, true, kC, na));
     XHC_STEP("flash_proj_next",
              launch_proj_partial(d->state_dtype, X, d->T, d->N, d->C, kC, packed_act_next, na, idx, d->k, part, s));
+    const int nsn = saved_floats(d->k, d->k, Kn);   // the next sublayer's mapping record
+    if (saved_next)
+      XHC_STEP("flash_save_zero", launch_fill0(saved_next, (size_t)d->T * nsn * sizeof(float), s));
     XHC_STEP("flash_coef_next",
              launch_pre_coef(part, proj_chunks(d->state_dtype, true, kC, d->C, na, d->T), na, d->T, d->k, Kn, with_res, d->C, alpha_next,
                              with_res ? alpha_next + 1 : nullptr, b_post_next, b_res_next, d->eps, d->sinkhorn_iters,
-                             d->clamp_delta, Hpost_next, Hres_next, sums, nullptr, 0, 0, 0, s));
+                             d->clamp_delta, Hpost_next, Hres_next, sums, saved_next, saved_next ? nsn : 0,
+                             2 * d->k, nsn - 2, s));
   }
   return hip_status(e);
 }
@@ -696,9 +704,9 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
                               const float* Hpost, const float* Hres, const void* packed_act, const float* W_post,
                               const float* W_res, const float* alpha_post, const float* alpha_res,
                               const float* b_post, const float* b_res, const float* Hpre_q, const void* d_input,
-                              void* dF, float* dconv_w, float* dW_post, float* dalpha_post, float* db_post,
-                              float* dW_res, float* dalpha_res, float* db_res, float* dp, float* dHpre_act,
-                              void* workspace, size_t workspace_bytes, void* stream) {
+                              const float* saved_act, void* dF, float* dconv_w, float* dW_post,
+                              float* dalpha_post, float* db_post, float* dW_res, float* dalpha_res, float* db_res,
+                              float* dp, float* dHpre_act, void* workspace, size_t workspace_bytes, void* stream) {
   xhc_status st = check_dims(d);
   if (st != XHC_OK) return st;
   if ((Q != 2 && Q != 4) || q < 1 || q > Q) return XHC_EINVAL;
@@ -739,7 +747,8 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   // zero the dummy operands (weights of the absent pre-map and router, the
   // saved logits the recompute leaves empty), and for q < Q the residual
   // mapping that sublayer does not have
-  XHC_STEP("fbwd_zero", launch_fill0(ws + w.saved, (size_t)T * saved_floats(k, k, Kq) * sizeof(float), s));
+  if (!saved_act)
+    XHC_STEP("fbwd_zero", launch_fill0(ws + w.saved, (size_t)T * saved_floats(k, k, Kq) * sizeof(float), s));
   XHC_STEP("fbwd_zero", launch_fill0(ws + w.w0, w.wres0 - w.w0, s));   // w0, colsum0
   if (!last) XHC_STEP("fbwd_zero", launch_fill0(ws + w.wres0, w.alpha2 - w.wres0, s));   // wres0, bres0
   // slot map, identity mixing, pre-map weights of the active streams, <d input_q, a_j>
@@ -758,17 +767,20 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
                                         /*grad_f32=*/true));
   XHC_STEP("fbwd_dp", launch_fbwd_add(dp, F32(w.dp), T * k, s));
   if (!last) XHC_STEP("fbwd_zero", launch_fill0(ws + w.dhres, (size_t)T * k * k * sizeof(float), s));
-  // the mapping logits of sublayer q recomputed from a^(q-1) (same kernels and
-  // operands as the forward)
+  // the mapping logits of sublayer q: saved by the forward, or recomputed
+  // from a^(q-1) (same kernels and operands as the forward)
   const int64_t na = act_outs(d, Kq, last);
   const int nsave = saved_floats((int)k, (int)k, Kq);
-  XHC_STEP("fbwd_proj", launch_proj_partial(d->state_dtype, Xact, T, (int)k, (int)C, kC, packed_act, na, idx_id,
-                                            (int)k, F32(w.part), s));
-  XHC_STEP("fbwd_coef", launch_pre_coef(F32(w.part), proj_chunks(d->state_dtype, true, kC, (int)C, na, T), na, T,
-                                        (int)k, Kq, last, C, alpha_post, last ? alpha_res : nullptr, b_post,
-                                        last ? b_res : nullptr, d->eps, d->sinkhorn_iters, d->clamp_delta,
-                                        F32(w.hpost_re), last ? F32(w.hres_re) : nullptr, F32(w.sums), F32(w.saved),
-                                        nsave, 2 * (int)k, nsave - 2, s));
+  const float* rec = saved_act ? saved_act : F32(w.saved);
+  if (!saved_act) {
+    XHC_STEP("fbwd_proj", launch_proj_partial(d->state_dtype, Xact, T, (int)k, (int)C, kC, packed_act, na, idx_id,
+                                              (int)k, F32(w.part), s));
+    XHC_STEP("fbwd_coef", launch_pre_coef(F32(w.part), proj_chunks(d->state_dtype, true, kC, (int)C, na, T), na, T,
+                                          (int)k, Kq, last, C, alpha_post, last ? alpha_res : nullptr, b_post,
+                                          last ? b_res : nullptr, d->eps, d->sinkhorn_iters, d->clamp_delta,
+                                          F32(w.hpost_re), last ? F32(w.hres_re) : nullptr, F32(w.sums), F32(w.saved),
+                                          nsave, 2 * (int)k, nsave - 2, s));
+  }
   XHC_STEP("fbwd_alpha", launch_fbwd_alpha(nullptr, alpha_res, alpha_post, F32(w.alpha2), s));
   // mapping reverse through a^(q-1) (its dense-row terms are all zero here:
   // no router or pre-map weights)
@@ -776,7 +788,7 @@ xhc_status xhc_flash_post_bwd(const xhc_dims* d, int32_t Q, int32_t q, const voi
   // state goes through the MFMA pass on Xact as saved)
   XHC_STEP("fbwd_pre", launch_bwd_pre(&r, Xact, F32(w.colsum0), F32(w.w0), F32(w.w0),
                                       last ? W_res : F32(w.wres0), W_post, F32(w.alpha2),
-                                      last ? b_res : F32(w.bres0), F32(w.saved), idx_id, p, F32(w.hsel), Hpost,
+                                      last ? b_res : F32(w.bres0), rec, idx_id, p, F32(w.hsel), Hpost,
                                       nullptr, F32(w.dhres), F32(w.dhpost), F32(w.dp), dA_out,
                                       F32(w.dwr), F32(w.dwpre), last ? dW_res : F32(w.dwres), dW_post,
                                       F32(w.dalpha2), F32(w.dbpre), last ? db_res : F32(w.dbres), db_post,

@@ -86,9 +86,9 @@ _SIGS = {
     "xhc_post": (ctypes.c_int, [_D] + [_P] * 9 + [ctypes.c_size_t, _P]),
     "xhc_saved_floats": (ctypes.c_size_t, [_D]),
     "xhc_post_noalloc": (ctypes.c_int, [_D] + [_P] * 9),
-    "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 15 + [ctypes.c_size_t, _P]),
-    "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 18 + [ctypes.c_size_t, _P]),
-    "xhc_flash_post_bwd": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 29 + [ctypes.c_size_t, _P]),
+    "xhc_flash_pre": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 16 + [ctypes.c_size_t, _P]),
+    "xhc_flash_post": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 19 + [ctypes.c_size_t, _P]),
+    "xhc_flash_post_bwd": (ctypes.c_int, [_D, ctypes.c_int32, ctypes.c_int32] + [_P] * 30 + [ctypes.c_size_t, _P]),
     "xhc_flash_pre_bwd": (ctypes.c_int, [_D, ctypes.c_int32] + [_P] * 21 + [ctypes.c_size_t, _P]),
     "xhc_post_bwd": (ctypes.c_int, [_D] + [_P] * 16 + [ctypes.c_size_t, _P]),
     "xhc_pre_bwd": (ctypes.c_int, [_D] + [_P] * 27 + [ctypes.c_size_t, _P]),
@@ -213,26 +213,28 @@ def _nbytes(t):
 
 
 def xhc_flash_pre(d, Q, X, packed_full, packed_act1, alpha_pre, b_pre, alpha_post1, b_post1, input1, base, idx,
-                  p, Hpre, Hpost1, saved, workspace, stream=None):
+                  p, Hpre, Hpost1, saved, saved_act1, workspace, stream=None):
     _call("xhc_flash_pre", ctypes.byref(d), Q, _ptr(X), _ptr(packed_full), _ptr(packed_act1), _ptr(alpha_pre),
           _ptr(b_pre), _ptr(alpha_post1), _ptr(b_post1), _ptr(input1), _ptr(base), _ptr(idx), _ptr(p), _ptr(Hpre),
-          _ptr(Hpost1), _ptr(saved), _ptr(workspace), _nbytes(workspace), _stream(stream))
+          _ptr(Hpost1), _ptr(saved), _ptr(saved_act1), _ptr(workspace), _nbytes(workspace), _stream(stream))
 
 
 def xhc_flash_post(d, Q, q, X, F, conv_w, idx, p, Hpost, Hres, Hpre_next, base_next, input_next, packed_act_next,
-                   alpha_next, b_post_next, b_res_next, Hpost_next, Hres_next, Xact_save, workspace, stream=None):
+                   alpha_next, b_post_next, b_res_next, Hpost_next, Hres_next, Xact_save, saved_next, workspace,
+                   stream=None):
     _call("xhc_flash_post", ctypes.byref(d), Q, q, _ptr(X), _ptr(F), _ptr(conv_w), _ptr(idx), _ptr(p),
           _ptr(Hpost), _ptr(Hres), _ptr(Hpre_next), _ptr(base_next), _ptr(input_next), _ptr(packed_act_next),
           _ptr(alpha_next), _ptr(b_post_next), _ptr(b_res_next), _ptr(Hpost_next), _ptr(Hres_next),
-          _ptr(Xact_save), _ptr(workspace), _nbytes(workspace), _stream(stream))
+          _ptr(Xact_save), _ptr(saved_next), _ptr(workspace), _nbytes(workspace), _stream(stream))
 
 
 def xhc_flash_post_bwd(d, Q, q, dXn, da, Xact, F, conv_w, idx, p, Hpost, Hres, packed_act, W_post, W_res,
-                       alpha_post, alpha_res, b_post, b_res, Hpre_q, d_input, dF, dconv_w, dW_post, dalpha_post,
-                       db_post, dW_res, dalpha_res, db_res, dp, dHpre_act, workspace, stream=None):
+                       alpha_post, alpha_res, b_post, b_res, Hpre_q, d_input, saved_act, dF, dconv_w, dW_post,
+                       dalpha_post, db_post, dW_res, dalpha_res, db_res, dp, dHpre_act, workspace, stream=None):
     _call("xhc_flash_post_bwd", ctypes.byref(d), Q, q, _ptr(dXn), _ptr(da), _ptr(Xact), _ptr(F), _ptr(conv_w),
           _ptr(idx), _ptr(p), _ptr(Hpost), _ptr(Hres), _ptr(packed_act), _ptr(W_post), _ptr(W_res),
-          _ptr(alpha_post), _ptr(alpha_res), _ptr(b_post), _ptr(b_res), _ptr(Hpre_q), _ptr(d_input), _ptr(dF),
+          _ptr(alpha_post), _ptr(alpha_res), _ptr(b_post), _ptr(b_res), _ptr(Hpre_q), _ptr(d_input),
+          _ptr(saved_act), _ptr(dF),
           _ptr(dconv_w), _ptr(dW_post), _ptr(dalpha_post), _ptr(db_post), _ptr(dW_res), _ptr(dalpha_res),
           _ptr(db_res), _ptr(dp), _ptr(dHpre_act), _ptr(workspace), _nbytes(workspace), _stream(stream))
 
@@ -368,12 +370,12 @@ class FlashGroup:
         self.ws_pre = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_PRE, Q), dev)
         self.ws_post = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_POST, Q), dev)
 
-    def pre(self, X, stream=None, saved=None):
+    def pre(self, X, stream=None, saved=None, saved_act1=None):
         xhc_flash_pre(self.d, self.Q, X, self.packed_full, self.packed_act[0], self.alpha_pre, self.b_pre,
                       self.alpha_post[0], self.b_post[0], self.inputs[0], self.base, self.idx, self.p, self.Hpre,
-                      self.Hpost[0], saved, self.ws_pre, stream)
+                      self.Hpost[0], saved, saved_act1, self.ws_pre, stream)
 
-    def step(self, q, X, F, stream=None, Xact_save=None):
+    def step(self, q, X, F, stream=None, Xact_save=None, saved_next=None):
         """Write-back of sublayer q (1-based); for q < Q also forms inputs[q]."""
         Q = self.Q
         last = q == Q
@@ -386,7 +388,7 @@ class FlashGroup:
             None if last else self.alpha_post[nxt], None if last else self.b_post[nxt],
             self.b_res if (not last and q + 1 == Q) else None,
             None if last else self.Hpost[nxt], self.Hres if (not last and q + 1 == Q) else None,
-            Xact_save, self.ws_post, stream)
+            Xact_save, saved_next, self.ws_post, stream)
 
     def run(self, X, F_list, stream=None):
         self.pre(X, stream)
@@ -421,13 +423,17 @@ class TrainableFlashGroup(FlashGroup):
         self.Xact = [torch.empty(T, k, C, dtype=self.inputs[0].dtype, device=dev) for _ in range(Q)]
         # the routing records of the group entry, one per pre-map (xhc_flash_pre writes them)
         self.saved = torch.empty(Q, T, 2 * N + k + k * k + 4, **f32)
+        # each sublayer's mapping record (its logits and RMS statistic; xhc_flash_pre
+        # writes sublayer 1's, xhc_flash_post q the one of q + 1)
+        self.saved_act = [torch.empty(T, 2 * k + k * flash_Kq(d, q) + k * k + 4, **f32) for q in range(1, Q + 1)]
         self.ws_post_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_POST_BWD, Q), dev)
         self.ws_pre_bwd = _bytes(xhc_workspace_bytes(d, XHC_OP_FLASH_PRE_BWD, Q), dev)
 
     def forward(self, X, F_list, stream=None):
-        self.pre(X, stream, saved=self.saved)
+        self.pre(X, stream, saved=self.saved, saved_act1=self.saved_act[0])
         for q in range(1, self.Q + 1):
-            self.step(q, X, F_list[q - 1], stream, Xact_save=self.Xact[q - 1])
+            self.step(q, X, F_list[q - 1], stream, Xact_save=self.Xact[q - 1],
+                      saved_next=self.saved_act[q] if q < self.Q else None)
         return X
 
     def backward(self, X0, dXn, d_inputs, F_list, stream=None, in_place=False, recompute=False):
@@ -460,7 +466,8 @@ class TrainableFlashGroup(FlashGroup):
                 self.p, self.Hpost[q - 1], self.Hres if last else None, self.packed_act[q - 1], self.W_post[q - 1],
                 self.W_res if last else None, self.a_post[q - 1], self.a_res if last else None, self.b_post[q - 1],
                 self.b_res if last else None, self.Hpre[q - 1] if q >= 2 else None,
-                d_inputs[q - 1] if q >= 2 else None, g["F_list"][q - 1], g["conv_w_list"][q - 1],
+                d_inputs[q - 1] if q >= 2 else None, None if recompute else self.saved_act[q - 1],
+                g["F_list"][q - 1], g["conv_w_list"][q - 1],
                 g["W_post_list"][q - 1], a_post[q - 1:q], g["b_post"][q - 1], g["W_res"] if last else None,
                 a_res if last else None, g["b_res"] if last else None, dp, dhact[q - 2] if q >= 2 else None,
                 self.ws_post_bwd, stream)

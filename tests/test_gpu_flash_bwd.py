@@ -133,8 +133,10 @@ def test_flash_backward_in_place_gives_the_same_gradients():
 
 
 def test_flash_backward_from_saved_records_equals_recomputed():
-    """xhc_flash_pre_bwd reading the routing records xhc_flash_pre saved gives
-    the same bits as recomputing them from the entry state."""
+    """The reverse reading the records the forward saved (the routing records
+    of xhc_flash_pre, each sublayer's mapping record of xhc_flash_pre /
+    xhc_flash_post) gives the same bits as recomputing them from the entry
+    state and the saved active rows."""
     w = W(T=96, S=48, N=16, k=4, m=2, C=512, Kr=4, name="fbwd-saved")
     d, grp, state, g = _run(w, 4, seed=8)
     gr = grp.backward(d["X"], d["G_X"], d["G_in_list"], d["F_list"], recompute=True)
