@@ -1464,8 +1464,10 @@ constexpr int kMfXPitch = kMfRows + 8;   // bf16 per staged token row (pad: fewe
 //   rows[t][0 .. NO)   hi,  rows[t][NO .. 2 NO)  lo
 //   tr[b][o][u]        the same values of token 32 b + u, row o of 2 NO
 // full rows (act = 0): r_ln dz_r | r dz_pre; active rows: r_a dz_act.
+// srec (full rows, or null): [Tp][8] per-token scalars of the ring pass.
 __global__ __launch_bounds__(256) void k_dz_pack(const float* __restrict__ tok, int64_t T, int N, int NA, int act,
-                                                 int NO, uint16_t* __restrict__ rows, uint16_t* __restrict__ tr) {
+                                                 int NO, uint16_t* __restrict__ rows, uint16_t* __restrict__ tr,
+                                                 float* __restrict__ srec) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
   if (i >= Tp * NO) return;
@@ -1485,6 +1487,12 @@ __global__ __launch_bounds__(256) void k_dz_pack(const float* __restrict__ tok, 
   uint16_t* blk = tr + (t / kDzBlock) * 2 * NO * kDzBlock;
   blk[o * kDzBlock + t % kDzBlock] = (uint16_t)hb;
   blk[(NO + o) * kDzBlock + t % kDzBlock] = (uint16_t)lb;
+  // the token's row statistics as the full-row ring pass reads them:
+  // r_ln, mu, m1, m2, beta_pre, then zero
+  if (srec && o < 8) {
+    const int src[5] = {1, 2, 4, 5, 3};
+    srec[t * 8 + o] = (t < T && o < 5) ? tok[t * tok_floats(N, NA) + 2 * N + NA + src[o]] : 0.f;
+  }
 }
 
 // 4 consecutive gradient elements of a bf16 or fp32 accumulator row, as
@@ -1546,7 +1554,6 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
   __shared__ __align__(16) uint16_t dzr[kMfStep][2 * NO + 8];
   __shared__ __align__(16) uint16_t dzt[2 * NO][kMfStep + 8];
   __shared__ float sc[kMfStep][8];
-  __shared__ int srow[kMfStep];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int l16 = lane % 16, g4 = lane / 16;
   const int64_t K0 = (int64_t)blockIdx.x * RW;                // first weight row of the workgroup
@@ -1582,101 +1589,108 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
   const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
   // The inputs of step tb + 32 are fetched into registers while step tb is
   // computed: this thread's pieces of the packed dz', scalars (threads < 32)
-  // and 16 bytes of the state rows.
+  // and 16 bytes of the state rows.  Every load is issued without a branch (a
+  // token past the chunk reads the chunk's last token; its dz' row and state
+  // row are zeroed where they are staged, its gradient row is not stored) and
+  // the barriers wait for LDS traffic only, so a step waits for nothing but
+  // its own prefetched loads: not for the previous step's stores, nor for the
+  // loads of the next.  Active rows: the row of each token is loaded one step
+  // earlier still (rid), so the state and gradient loads do not wait on it.
   const uint16_t* const dzrows = dzp;
   const uint16_t* const dztr = dzp + (T + kDzBlock - 1) / kDzBlock * kDzBlock * 2 * NO;
+  // the wave index as a uniform value: the branches below on it are scalar
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  static_assert(NT >= 7 * kMfStep, "one scalar of a step per thread");
   struct Stage {
     uint4 dz[DZP];
-    float scal[7];
-    int row;
+    float scal;
+    int rowd[2];                     // rows of the lane's two gradient tokens
     uint4 x;
     typename Raw4<TD>::type dx[2];   // the lane's accumulator elements (two token halves), as loaded
     uint2 din[2];
   };
+  auto tok_at = [&](int64_t tb, int u) -> int64_t { return tb + u < t1 ? tb + u : t1 - 1; };
+  int rid[3] = {part, part, part};   // rows of the next fetch: state token, gradient tokens 0 and 1
+  auto fetch_rows = [&](int64_t tb) {
+    if (ACT) {
+      rid[0] = idx[tok_at(tb, threadIdx.x / PIECES) * k + part];
+      rid[1] = idx[tok_at(tb, l16) * k + part];
+      rid[2] = idx[tok_at(tb, 16 + l16) * k + part];
+    }
+  };
+  // pieces q of the packed dz': [0, 8 NO) token rows (NO / 4 pieces a token),
+  // [8 NO, 16 NO) the transposed block (4 pieces a row); 8 NO is a multiple
+  // of 64, so the choice is the same across a wave
+  auto dz_rows = [&](int r) { return wave_u * kWave + r * NT < 8 * NO; };
   auto fetch = [&](Stage& st, int64_t tb) {
-    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
-    // pieces [0, 8 NO): token rows (NO / 4 pieces a token); [8 NO, 16 NO): the
-    // transposed block (4 pieces a row); rows of tokens past the chunk are zero
 #pragma unroll
     for (int r = 0; r < DZP; ++r) {
       const int q = threadIdx.x + r * NT;
-      if (q < 8 * NO) {
-        const int u = q / (NO / 4), off = (q % (NO / 4)) * 8;
-        st.dz[r] = u < nt ? *reinterpret_cast<const uint4*>(dzrows + (tb + u) * 2 * NO + off)
-                          : make_uint4(0, 0, 0, 0);
+      if (dz_rows(r)) {
+        st.dz[r] = *reinterpret_cast<const uint4*>(dzrows + tok_at(tb, q / (NO / 4)) * 2 * NO + (q % (NO / 4)) * 8);
       } else {
-        const int qq = q - 8 * NO, row = qq / 4, off = (qq % 4) * 8;
-        st.dz[r] = *reinterpret_cast<const uint4*>(dztr + (tb / kDzBlock) * 2 * NO * kDzBlock + row * kDzBlock + off);
+        const int qq = q - 8 * NO;
+        st.dz[r] = *reinterpret_cast<const uint4*>(dztr + (tok_at(tb, 0) / kDzBlock) * 2 * NO * kDzBlock + (qq / 4) * kDzBlock +
+                                                   (qq % 4) * 8);
       }
     }
-    if (threadIdx.x < kMfStep) {
-      const int u = threadIdx.x;
-      const int64_t t = tb + (u < nt ? u : 0);
-      const float* tk = tok + t * TF;
-      st.row = ACT ? idx[t * k + part] : part;
-      if (ACT) {
-        st.scal[0] = tk[2 * N + NA + 7];   // beta_a
-        if (ADIN) st.scal[1] = Hpre[t * k + part];   // active rows: weight of the slot's read of din
-      } else {
-#pragma unroll
-        for (int i = 0; i < 6; ++i) st.scal[i] = tk[2 * N + NA + i];   // r, r_ln, mu, beta_pre, m1, m2
-        st.scal[6] = Hpre[t * N + part];
-      }
-    }
-    // the state rows need the row index: the slot's row of each token (active)
-    // is read here directly
-    {
-      const int u = threadIdx.x / PIECES, piece = threadIdx.x % PIECES;
-      st.x = make_uint4(0, 0, 0, 0);
-      if (u < nt) {
-        const int64_t t = tb + u;
-        const int row = ACT ? idx[t * k + part] : part;
-        st.x = *reinterpret_cast<const uint4*>(X + (t * N + row) * (int64_t)C + c0 + piece * 8);
-      }
-    }
+    st.x = *reinterpret_cast<const uint4*>(X + (tok_at(tb, threadIdx.x / PIECES) * N + rid[0]) * (int64_t)C + c0 +
+                                           (threadIdx.x % PIECES) * 8);
     // the accumulator rows of the step (other tokens than the step being
     // computed, so reading them a step ahead is safe)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      const int u = 16 * h + l16;
+      const int64_t t = tok_at(tb, 16 * h + l16);
       const int kr = 16 * wave + 4 * g4;
-      st.dx[h] = Raw4<TD>::zero();
+      st.rowd[h] = rid[1 + h];
+      st.dx[h] = Raw4<TD>::load(dX + (t * N + rid[1 + h]) * (int64_t)C + c0 + kr);
       st.din[h] = make_uint2(0, 0);
-      if (u < nt) {
-        const int64_t t = tb + u;
-        const int row = ACT ? idx[t * k + part] : part;
-        st.dx[h] = Raw4<TD>::load(dX + (t * N + row) * (int64_t)C + c0 + kr);
-        if (!ACT || ADIN) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
-      }
+      if (!ACT || ADIN) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
+    }
+    // per-token scalars, one per thread (value vi of token u; threads past
+    // the 7 values load value 0 again and do not stage it), so that every
+    // wave issues the same loads
+    {
+      const int vi = threadIdx.x / kMfStep;
+      const int64_t t = tok_at(tb, threadIdx.x % kMfStep);
+      const float* src;
+      if (ACT)   // beta_a; active rows with din: the weight of the slot's read of din
+        src = (ADIN && vi == 1) ? Hpre + t * k + part : tok + t * TF + 2 * N + NA + 7;
+      else       // r, r_ln, mu, beta_pre, m1, m2, then H^pre of the stream
+        src = vi == 6 ? Hpre + t * N + part : tok + t * TF + 2 * N + NA + (vi < 6 ? vi : 0);
+      st.scal = *src;
     }
   };
-  Stage cur;
-  if (t0 < t1) fetch(cur, t0);
-  for (int64_t tb = t0; tb < t1; tb += kMfStep) {
-    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
-    __syncthreads();   // the previous step's LDS reads are done
+  // One step of 32 tokens.  FULL: all 32 tokens exist, so the step has no
+  // per-token predicates; the last, partial step of the chunk (T % 32 tokens)
+  // is a separate instance.  The next step's loads are issued unconditionally
+  // (past the chunk they read its last token again), so every path through
+  // the loop has the same memory operations.
+  auto step = [&](auto full, Stage& cur, int64_t tb) {
+    constexpr bool FULL = decltype(full)::value;
+    const int nt = FULL ? kMfStep : (int)(t1 - tb);
+    lds_barrier();   // the previous step's LDS reads are done
 #pragma unroll
     for (int r = 0; r < DZP; ++r) {
       const int q = threadIdx.x + r * NT;
-      if (q < 8 * NO) {
+      if (dz_rows(r)) {
         const int u = q / (NO / 4), off = (q % (NO / 4)) * 8;
-        *reinterpret_cast<uint4*>(&dzr[u][off]) = cur.dz[r];
+        *reinterpret_cast<uint4*>(&dzr[u][off]) = (FULL || u < nt) ? cur.dz[r] : make_uint4(0, 0, 0, 0);
       } else {
         const int qq = q - 8 * NO, row = qq / 4, off = (qq % 4) * 8;
         *reinterpret_cast<uint4*>(&dzt[row][off]) = cur.dz[r];
       }
     }
-    if (threadIdx.x < kMfStep) {
-      srow[threadIdx.x] = cur.row;
-#pragma unroll
-      for (int i = 0; i < 7; ++i) sc[threadIdx.x][i] = cur.scal[i];
-    }
-    *reinterpret_cast<uint4*>(&xs[threadIdx.x / PIECES][(threadIdx.x % PIECES) * 8]) = cur.x;
+    if (threadIdx.x < 7 * kMfStep) sc[threadIdx.x % kMfStep][threadIdx.x / kMfStep] = cur.scal;
+    *reinterpret_cast<uint4*>(&xs[threadIdx.x / PIECES][(threadIdx.x % PIECES) * 8]) =
+        (FULL || (int)(threadIdx.x / PIECES) < nt) ? cur.x : make_uint4(0, 0, 0, 0);
+    const int rowd[2] = {cur.rowd[0], cur.rowd[1]};
     // ---- dX: two token halves; the accumulator rows were read a step ahead
     const typename Raw4<TD>::type dxr[2] = {cur.dx[0], cur.dx[1]};
     const uint2 dinv[2] = {cur.din[0], cur.din[1]};
-    __syncthreads();
-    if (tb + kMfStep < t1) fetch(cur, tb + kMfStep);
+    lds_barrier();
+    fetch(cur, tb + kMfStep);
+    fetch_rows(tb + 2 * kMfStep);
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int u = 16 * h + l16;   // B operand token of this lane
@@ -1689,7 +1703,7 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
         acc = mfma_16x16x32(wfrag[b], bl, acc);
       }
       // lane holds rows 16 wave + 4 g4 + v of token u
-      if (u < nt) {
+      if (FULL || u < nt) {
         const int64_t t = tb + u;
         const int kr = 16 * wave + 4 * g4;   // row offset inside the 64
         const uint2 xv = *reinterpret_cast<const uint2*>(&xs[u][kr]);
@@ -1715,7 +1729,7 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
         float dxv[4];
         Raw4<TD>::unpack(dxr[h], dxv);
         const float d[4] = {dxv[0] + gsum[0], dxv[1] + gsum[1], dxv[2] + gsum[2], dxv[3] + gsum[3]};
-        st4(dX + (t * N + srow[u]) * (int64_t)C + c0 + kr, d);
+        st4(dX + (t * N + rowd[h]) * (int64_t)C + c0 + kr, d);
       }
     }
     // ---- dW: contraction over the 32 staged tokens (rows past nt are zero)
@@ -1733,6 +1747,18 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
         dw[oh] = mfma_16x16x32(al, bx, dw[oh]);
       }
     }
+  };
+  if (t0 < t1) {
+    Stage cur;
+    fetch_rows(t0);
+    fetch(cur, t0);
+    fetch_rows(t0 + kMfStep);
+    // the loop is entered with no load in flight, so the compiler's wait
+    // counts inside it follow the loop's own order of loads and stores
+    __builtin_amdgcn_s_waitcnt(0);
+    int64_t tb = t0;
+    for (; tb + kMfStep <= t1; tb += kMfStep) step(std::true_type{}, cur, tb);
+    if (tb < t1) step(std::false_type{}, cur, tb);
   }
   // lane holds dW[row K0 + 16 wave + l16][output 16 oh + 4 g4 + v]
   const int64_t K = K0 + 16 * wave + l16;
@@ -1934,9 +1960,9 @@ size_t bwd_post_ws_bytes(const xhc_dims* d) {
 
 // The full-row pass of NQ pre-map reverses over one state in a single pass
 // (the entry state of an xHC-Flash group: the router with the first pre-map,
-// then one pre-map per sublayer; bf16 state, N = 16).  Same blocking as
-// k_bwd_rows_mfma; the contraction of the dX product runs over the 16 router
-// and 16 NQ pre-map outputs, each pass's per-token record (tok) giving its
+// then one pre-map per sublayer; bf16 state, N = 16), run by the ring pass
+// of xhc_bwd_rows.hip; the contraction of the dX product runs over the 16
+// router and 16 NQ pre-map outputs, each pass's per-token record (tok) giving its
 // own dz'.  The per-token terms add up over the passes: the dense reads
 // sum_q H^pre,q_i d input_q, the pre-map norm terms sum_q beta_pre,q x, and
 // the router's LayerNorm terms of the first pass (later passes have no router
@@ -1950,7 +1976,7 @@ struct MultiRows {
   const float* w[kMultiMaxQ + 1];  // W_r, then W_pre of pass q ([N C][16] each)
   float* wout[kMultiMaxQ + 1];
 };
-// Per token, the inputs of k_bwd_rows_multi gathered from the passes' token
+// Per token, the inputs of the multi-map ring pass gathered from the passes' token
 // records: [r_ln dz_r (16) | r dz_pre,q (16 each) | r_ln, mu, m1, m2,
 // sum_q beta_pre,q, pad], pitch 16 (NQ + 1) + 8 floats.
 template <int NQ>
@@ -1997,184 +2023,6 @@ __global__ __launch_bounds__(256) void k_dz_pack_multi(const float* __restrict__
   blk[(NOP + o) * kDzBlock + t % kDzBlock] = (uint16_t)lb;
 }
 
-template <int NQ>
-__global__ __launch_bounds__(256) void k_bwd_rows_multi(const uint16_t* __restrict__ X, uint16_t* __restrict__ dX,
-                                                        MultiRows m, const float* __restrict__ prep,
-                                                        const uint16_t* __restrict__ dzp, int64_t T,
-                                                        int N, int C, int NA, int64_t tchunk) {
-  constexpr int NO = 16 * (NQ + 1);            // outputs
-  constexpr int NKB = (NO + 31) / 32;          // 32-output blocks of the dX contraction
-  constexpr int NOP = 32 * NKB;                // outputs padded
-  constexpr int DZP = 16 * NOP / 256;          // 16-byte pieces of packed dz' per thread and step
-  static_assert(kMfStep == kDzBlock && DZP * 256 == 16 * NOP, "a step copies its packed dz' in whole pieces");
-  __shared__ __align__(16) uint16_t xs[kMfStep][kMfXPitch];
-  // packed dz' of the step (token rows, transpose); the pitches keep the
-  // 16-byte operand reads of a 16-lane group on distinct banks
-  __shared__ __align__(16) uint16_t dzr[kMfStep][2 * NOP + 8];
-  __shared__ __align__(16) uint16_t dzt[2 * NOP][kMfStep + 8];
-  __shared__ float sc[kMfStep][5 + NQ];
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int l16 = lane % 16, g4 = lane / 16;
-  const int64_t K0 = (int64_t)blockIdx.x * kMfRows;
-  const int part = (int)(K0 / C);              // stream
-  const int c0 = (int)(K0 % C);
-  const int64_t NK = (int64_t)N * C;
-  constexpr int PITCH = NO + 8;
-  uint4 wfrag[NKB];
-  {
-    const int64_t K = K0 + 16 * wave + l16;
-#pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-      float f[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int o = 32 * kb + 8 * g4 + e;
-        f[e] = o < NO ? __uint_as_float(f2bf(m.w[o / 16][K * 16 + o % 16]) << 16) : 0.f;
-      }
-      wfrag[kb] = pack8(f);
-    }
-  }
-  f32x4 dw[NQ + 1];
-#pragma unroll
-  for (int ob = 0; ob <= NQ; ++ob) dw[ob] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
-  const uint16_t* const dzrows = dzp;
-  const uint16_t* const dztr = dzp + (T + kDzBlock - 1) / kDzBlock * kDzBlock * 2 * NOP;
-  struct Stage {
-    uint4 dz[DZP];
-    float scal[5 + NQ];
-    uint4 x;
-    uint2 dx[2];
-  };
-  auto fetch = [&](Stage& st, int64_t tb) {
-    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
-    // pieces [0, 8 NOP): token rows (NOP / 4 a token, zero past the chunk);
-    // [8 NOP, 16 NOP): the transposed block (4 a row)
-#pragma unroll
-    for (int r = 0; r < DZP; ++r) {
-      const int q = threadIdx.x + r * 256;
-      if (q < 8 * NOP) {
-        const int u = q / (NOP / 4), off = (q % (NOP / 4)) * 8;
-        st.dz[r] = u < nt ? *reinterpret_cast<const uint4*>(dzrows + (tb + u) * 2 * NOP + off)
-                          : make_uint4(0, 0, 0, 0);
-      } else {
-        const int qq = q - 8 * NOP, row = qq / 4, off = (qq % 4) * 8;
-        st.dz[r] = *reinterpret_cast<const uint4*>(dztr + (tb / kDzBlock) * 2 * NOP * kDzBlock + row * kDzBlock + off);
-      }
-    }
-    if (threadIdx.x < kMfStep) {
-      const int u = threadIdx.x;
-      const int64_t t = tb + (u < nt ? u : 0);
-#pragma unroll
-      for (int i = 0; i < 5; ++i) st.scal[i] = prep[t * PITCH + NO + i];   // r_ln, mu, m1, m2, sum beta_pre
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) st.scal[5 + q] = m.hrd[q][t * N + part];
-    }
-    {
-      const int u = threadIdx.x / 8, piece = threadIdx.x % 8;
-      st.x = make_uint4(0, 0, 0, 0);
-      if (u < nt) st.x = *reinterpret_cast<const uint4*>(X + ((tb + u) * N + part) * (int64_t)C + c0 + piece * 8);
-    }
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int u = 16 * h + l16;
-      const int kr = 16 * wave + 4 * g4;
-      st.dx[h] = make_uint2(0, 0);
-      if (u < nt) st.dx[h] = *reinterpret_cast<const uint2*>(dX + ((tb + u) * N + part) * (int64_t)C + c0 + kr);
-    }
-  };
-  Stage cur;
-  if (t0 < t1) fetch(cur, t0);
-  for (int64_t tb = t0; tb < t1; tb += kMfStep) {
-    const int nt = (int)((t1 - tb < kMfStep) ? t1 - tb : kMfStep);
-    __syncthreads();   // the previous step's LDS reads are done
-#pragma unroll
-    for (int r = 0; r < DZP; ++r) {
-      const int q = threadIdx.x + r * 256;
-      if (q < 8 * NOP) {
-        const int u = q / (NOP / 4), off = (q % (NOP / 4)) * 8;
-        *reinterpret_cast<uint4*>(&dzr[u][off]) = cur.dz[r];
-      } else {
-        const int qq = q - 8 * NOP, row = qq / 4, off = (qq % 4) * 8;
-        *reinterpret_cast<uint4*>(&dzt[row][off]) = cur.dz[r];
-      }
-    }
-    if (threadIdx.x < kMfStep) {
-#pragma unroll
-      for (int i = 0; i < 5 + NQ; ++i) sc[threadIdx.x][i] = cur.scal[i];
-    }
-    *reinterpret_cast<uint4*>(&xs[threadIdx.x / 8][(threadIdx.x % 8) * 8]) = cur.x;
-    const uint2 dxr[2] = {cur.dx[0], cur.dx[1]};
-    __syncthreads();
-    // the input gradients of this step (read here: prefetching them a step
-    // ahead as well measured no faster and holds 16 more registers)
-    uint2 dinv[NQ][2];
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int u = 16 * h + l16;
-      const int kr = 16 * wave + 4 * g4;
-#pragma unroll
-      for (int q = 0; q < NQ; ++q)
-        dinv[q][h] = u < nt ? *reinterpret_cast<const uint2*>(m.din[q] + (tb + u) * C + c0 + kr) : make_uint2(0, 0);
-    }
-    if (tb + kMfStep < t1) fetch(cur, tb + kMfStep);
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int u = 16 * h + l16;
-      f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        const uint4 bh = *reinterpret_cast<const uint4*>(&dzr[u][32 * kb + 8 * g4]);
-        const uint4 bl = *reinterpret_cast<const uint4*>(&dzr[u][NOP + 32 * kb + 8 * g4]);
-        acc = mfma_16x16x32(wfrag[kb], bh, acc);
-        acc = mfma_16x16x32(wfrag[kb], bl, acc);
-      }
-      if (u < nt) {
-        const int64_t t = tb + u;
-        const int kr = 16 * wave + 4 * g4;
-        const uint2 xv = *reinterpret_cast<const uint2*>(&xs[u][kr]);
-        const float x[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
-        const float r_ln = sc[u][0], mu = sc[u][1], m1 = sc[u][2], m2 = sc[u][3], bsum = sc[u][4];
-        float rd[4] = {0.f, 0.f, 0.f, 0.f};   // sum_q H^pre,q d input_q, passes in order
-#pragma unroll
-        for (int q = 0; q < NQ; ++q) {
-          const float hp = sc[u][5 + q];
-          const float gi[4] = {bf_lo(dinv[q][h].x), bf_hi(dinv[q][h].x), bf_lo(dinv[q][h].y), bf_hi(dinv[q][h].y)};
-#pragma unroll
-          for (int v = 0; v < 4; ++v) rd[v] = fmaf(hp, gi[v], rd[v]);
-        }
-        const float dxv[4] = {bf_lo(dxr[h].x), bf_hi(dxr[h].x), bf_lo(dxr[h].y), bf_hi(dxr[h].y)};
-        float d[4];
-#pragma unroll
-        for (int v = 0; v < 4; ++v)
-          d[v] = dxv[v] + (rd[v] + acc[v] - bsum * x[v] - r_ln * m1 - r_ln * r_ln * (x[v] - mu) * m2);
-        *reinterpret_cast<uint2*>(dX + (t * N + part) * (int64_t)C + c0 + kr) =
-            make_uint2(pack2bf(d[0], d[1]), pack2bf(d[2], d[3]));
-      }
-    }
-    {
-      uint16_t xb[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) xb[e] = xs[8 * g4 + e][16 * wave + l16];
-      const uint4 bx = make_uint4(xb[0] | ((uint32_t)xb[1] << 16), xb[2] | ((uint32_t)xb[3] << 16),
-                                  xb[4] | ((uint32_t)xb[5] << 16), xb[6] | ((uint32_t)xb[7] << 16));
-#pragma unroll
-      for (int ob = 0; ob <= NQ; ++ob) {
-        const uint4 ah = *reinterpret_cast<const uint4*>(&dzt[16 * ob + l16][8 * g4]);
-        const uint4 al = *reinterpret_cast<const uint4*>(&dzt[NOP + 16 * ob + l16][8 * g4]);
-        dw[ob] = mfma_16x16x32(ah, bx, dw[ob]);
-        dw[ob] = mfma_16x16x32(al, bx, dw[ob]);
-      }
-    }
-  }
-  const int64_t K = K0 + 16 * wave + l16;
-#pragma unroll
-  for (int ob = 0; ob <= NQ; ++ob) {
-    float* dst = m.wout[ob] + ((int64_t)blockIdx.y * NK + K) * 16 + 4 * g4;
-    *reinterpret_cast<float4*>(dst) = make_float4(dw[ob][0], dw[ob][1], dw[ob][2], dw[ob][3]);
-  }
-}
-
 constexpr int64_t kRowChunk = 1024;   // tokens per weight-gradient partial
 
 BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws) {
@@ -2198,11 +2046,13 @@ BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws) {
   const uintptr_t a = reinterpret_cast<uintptr_t>(w.pgsum + pg_floats(N, k, Kr) + N);
   w.dzf = reinterpret_cast<uint16_t*>((a + 15) / 16 * 16);
   w.dza = w.dzf + Tp * 2 * (2 * N <= 32 ? 32 : 64) * 2;
+  w.srec = reinterpret_cast<float*>(w.dza + Tp * 2 * 32 * 2);   // 16-byte aligned: Tp % 32 == 0
   return w;
 }
 
 bool bwd_rows_multi_supported(const xhc_dims* d, int Q) {
-  return d->state_dtype == XHC_BF16 && d->N == 16 && d->C % kMfRows == 0 && (Q == 2 || Q == 4);
+  return d->state_dtype == XHC_BF16 && d->N == 16 && bwd_rows_ring_supported(d->N, d->C, kRowChunk) &&
+         (Q == 2 || Q == 4);
 }
 
 hipError_t launch_bwd_dhpre_multi(const xhc_dims* d, int Q, const void* X, const void* d_input, char* const* ws,
@@ -2232,7 +2082,7 @@ hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* 
   if (!bwd_rows_multi_supported(d, Q)) return hipErrorInvalidValue;
   const int64_t T = d->T;
   const int N = d->N, C = d->C, NA = d->k * d->Kr + d->k * d->k;
-  const int64_t NC = (int64_t)N * C, nchunk = (T + kRowChunk - 1) / kRowChunk;
+  const int64_t NC = (int64_t)N * C;
   MultiRows m{};
   m.w[0] = W_r;
   m.wout[0] = bwd_pre_ws(d, ws[0]).wpart_r;
@@ -2244,7 +2094,6 @@ hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* 
     m.w[q + 1] = W_pre + (int64_t)q * NC * N;
     m.wout[q + 1] = w.wpart_p;
   }
-  const dim3 g((unsigned)(NC / kMfRows), (unsigned)nchunk);
   const int64_t np = T * (16 * (Q + 1) + 8);
   const dim3 gp((unsigned)((np + 255) / 256));
   const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock, nop = multi_nop(Q);
@@ -2254,15 +2103,19 @@ hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* 
   if (Q == 4) {
     k_multi_prep<4><<<gp, dim3(256), 0, s>>>(m, T, N, NA, prep);
     k_dz_pack_multi<4><<<gk, dim3(256), 0, s>>>(prep, T, dzp, dzp + Tp * 2 * nop);
-    k_bwd_rows_multi<4><<<g, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), reinterpret_cast<uint16_t*>(dX),
-                                                m, prep, dzp, T, N, C, NA, kRowChunk);
   } else {
     k_multi_prep<2><<<gp, dim3(256), 0, s>>>(m, T, N, NA, prep);
     k_dz_pack_multi<2><<<gk, dim3(256), 0, s>>>(prep, T, dzp, dzp + Tp * 2 * nop);
-    k_bwd_rows_multi<2><<<g, dim3(256), 0, s>>>(reinterpret_cast<const uint16_t*>(X), reinterpret_cast<uint16_t*>(dX),
-                                                m, prep, dzp, T, N, C, NA, kRowChunk);
   }
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // the ring pass reads the prep rows' scalars (r_ln, mu, m1, m2, sum beta_pre)
+  // at offset 16 (Q + 1) of each row
+  const int no = 16 * (Q + 1);
+  const void* dins[kMultiMaxQ];
+  for (int q = 0; q < Q; ++q) dins[q] = m.din[q];
+  return launch_bwd_rows_ring(Q, X, dX, dins, m.hrd, m.w, m.wout, 16, no, dzp, (int)nop, prep + no, no + 8, T, N, C,
+                              kRowChunk, s);
 }
 
 size_t bwd_pre_ws_bytes(const xhc_dims* d) {
@@ -2278,7 +2131,7 @@ size_t bwd_pre_ws_bytes(const xhc_dims* d) {
   n += (size_t)N;                                                // token sum of mu dz'_r
   const size_t Tp = (size_t)((T + kDzBlock - 1) / kDzBlock * kDzBlock);
   const size_t dz = Tp * 2 * ((2 * N <= 32 ? 32 : 64) + 32) * 2 * sizeof(uint16_t);   // packed dz'
-  return n * sizeof(float) + 16 + dz + 1024;
+  return n * sizeof(float) + 16 + dz + Tp * 8 * sizeof(float) + 1024;                 // + scalar rows
 }
 
 bool bwd_pre_supported(const xhc_dims* d) {
@@ -2352,23 +2205,19 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
       const int NOf = 2 * N <= 32 ? 32 : 64;
       if (dense_rows)
         k_dz_pack<<<dim3((unsigned)((Tp * NOf + 255) / 256)), dim3(256), 0, s>>>(tok, T, N, NA, 0, NOf, w.dzf,
-                                                                                 w.dzf + Tp * 2 * NOf);
+                                                                                 w.dzf + Tp * 2 * NOf, w.srec);
       if (act_rows)
         k_dz_pack<<<dim3((unsigned)((Tp * 32 + 255) / 256)), dim3(256), 0, s>>>(tok, T, N, NA, 1, 32, w.dza,
-                                                                                w.dza + Tp * 2 * 32);
+                                                                                w.dza + Tp * 2 * 32, nullptr);
       if (dense_rows) {
-        // 2N outputs in one block of 32 (N <= 16) or two (N = 32)
-        const dim3 gw((unsigned)((int64_t)N * C / (2 * kMfRows)), (unsigned)nchunk);
-        if (N == 32)
-          k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows, false, 2><<<gw, dim3(8 * kMfRows), 0, s>>>(
-              reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
-              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dzf,
-              wpart_r, wpart_p);
-        else
-          k_bwd_rows_mfma<false, uint16_t, 2 * kMfRows><<<gw, dim3(8 * kMfRows), 0, s>>>(
-              reinterpret_cast<const uint16_t*>(X), reinterpret_cast<const uint16_t*>(d_input),
-              reinterpret_cast<uint16_t*>(dX), W_r, W_pre, Hrd, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dzf,
-              wpart_r, wpart_p);
+        // 2N outputs padded to one block of 32 (N <= 16) or two (N = 32)
+        const void* dins[1] = {d_input};
+        const float* hps[1] = {Hrd};
+        const float* ws2[2] = {W_r, W_pre};
+        float* wo2[2] = {wpart_r, wpart_p};
+        e = launch_bwd_rows_ring(1, X, dX, dins, hps, ws2, wo2, N, 2 * N, w.dzf, NOf, w.srec, 8, T, N, C, kRowChunk,
+                                 s);
+        if (e != hipSuccess) return e;
       }
       // 128 rows per workgroup as for the full rows (C % 256 == 0)
       const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
@@ -2385,7 +2234,7 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
       const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
       const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
       k_dz_pack<<<dim3((unsigned)((Tp * 32 + 255) / 256)), dim3(256), 0, s>>>(tok, T, N, NA, 1, 32, w.dza,
-                                                                              w.dza + Tp * 2 * 32);
+                                                                              w.dza + Tp * 2 * 32, nullptr);
       if (act_din)
         k_bwd_rows_mfma<true, float, 2 * kMfRows, true><<<ga, dim3(8 * kMfRows), 0, s>>>(
             reinterpret_cast<const uint16_t*>(X_bf16), reinterpret_cast<const uint16_t*>(act_din),

@@ -147,6 +147,33 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // ---------------------------------------------------------------- math
 
+// Workgroup barrier for LDS traffic only: this wave's LDS accesses are
+// complete (lgkmcnt(0)), then s_barrier; the compiler fences keep memory
+// accesses on their side.  Unlike __syncthreads() it does not wait for the
+// wave's outstanding global loads and stores (a release fence would), so
+// loads issued ahead of their use stay in flight across it.  Only for
+// kernels whose waves exchange data through LDS alone.
+__device__ __forceinline__ void lds_barrier() {
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt = 63, expcnt = 7 (no wait), lgkmcnt = 0
+  __builtin_amdgcn_s_barrier();
+  __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// 16 (4) bytes per lane from global memory straight into LDS at lds_addr +
+// 16 lane (4 lane): a wave's 1 KiB (256 B) lands contiguously; lds_addr is
+// the same in every lane.  Issued as inline assembly so that the compiler
+// does not track the copy (it would otherwise make every later LDS access of
+// the wave wait for it: it cannot tell which LDS a copy writes); the caller
+// waits for it explicitly (s_waitcnt vmcnt) before the data is read, and
+// before the wave ends.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_addr) : "memory", "m0");
+}
+__device__ __forceinline__ void lds_dma4(const void* src, uint32_t lds_addr) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dword %0, off" : : "v"(src), "s"(lds_addr) : "memory", "m0");
+}
+
 __device__ __forceinline__ float sigmoidf(float z) { return 1.0f / (1.0f + __expf(-z)); }
 
 // Biased variance nu - mu^2 of the LayerNorm (eq:router), with a negative

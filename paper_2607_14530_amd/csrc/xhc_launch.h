@@ -134,7 +134,19 @@ constexpr int kBwdPreAll = 0, kBwdPreTokens = 1, kBwdPreReduce = 2, kBwdPreToken
 struct BwdPreWs {
   float *part, *tok, *pg, *wpart_r, *wpart_p, *wpart_a, *red_a, *pgsum;
   uint16_t *dzf, *dza;   // packed dz' of the full-row and active-row MFMA passes
+  float* srec;           // per-token scalars of the full-row ring pass [Tp][8]
 };
+// Full-row pass of Q pre-map reverses over one bf16 state, inputs staged
+// through an LDS ring (xhc_bwd_rows.hip): din[q] [T][C] input gradients,
+// hp[q] [T][N] dense-read weights, w[b] / wout[b] weight blocks of wb outputs
+// ([N C][wb]) and their partials ([chunk][N C][wb]), nout real outputs, dzp
+// the packed dz' (NOP = nop outputs), srec per-token scalar rows (stride in
+// floats, 16-byte aligned); dX updated in place.
+bool bwd_rows_ring_supported(int N, int C, int64_t tchunk);
+hipError_t launch_bwd_rows_ring(int Q, const void* X, void* dX, const void* const* din, const float* const* hp,
+                                const float* const* w, float* const* wout, int wb, int nout, const uint16_t* dzp,
+                                int nop, const float* srec, int64_t srec_stride, int64_t T, int N, int C,
+                                int64_t tchunk, hipStream_t s);
 BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws);   // layout of launch_bwd_pre's workspace
 hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum, const float* W_r,
                           const float* W_pre, const float* W_res, const float* W_post, const float* alpha,

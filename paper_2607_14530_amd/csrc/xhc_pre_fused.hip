@@ -151,17 +151,6 @@ __device__ __forceinline__ void ld_recs2t(const uint64_t* const (&p)[R1 + R2], c
   }
 }
 
-// Workgroup barrier for LDS traffic only: this wave's LDS accesses are
-// complete (lgkmcnt(0)), then s_barrier; the compiler fences keep memory
-// accesses on their side.  Unlike __syncthreads() it does not wait for the
-// wave's outstanding global->LDS copies, which a release fence would.
-__device__ __forceinline__ void lds_barrier() {
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-  __builtin_amdgcn_s_waitcnt(0xC07F);   // vmcnt = 63, expcnt = 7 (no wait), lgkmcnt = 0
-  __builtin_amdgcn_s_barrier();
-  __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
 // v of lane l ^ 32 (v_permlane32_swap with v in both operands leaves the low
 // half in the low lanes of the first result and the high half in the second)
 __device__ __forceinline__ uint32_t from_lane_xor32(uint32_t v, int lane) {
@@ -170,15 +159,6 @@ __device__ __forceinline__ uint32_t from_lane_xor32(uint32_t v, int lane) {
 }
 __device__ __forceinline__ float from_lane_xor32f(float v, int lane) {
   return __uint_as_float(from_lane_xor32(__float_as_uint(v), lane));
-}
-
-// 16 bytes per lane from global memory straight into LDS at lds_addr + 16 lane
-// (the wave's 1 KiB lands contiguously).  Issued as inline assembly so that
-// the compiler does not track the copy: it would otherwise make every later
-// LDS access of the wave wait for it (it cannot tell that they touch other
-// LDS).  The wave waits for it explicitly (vmcnt) before the buffer is read.
-__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds_addr) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds_addr) : "memory", "m0");
 }
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
