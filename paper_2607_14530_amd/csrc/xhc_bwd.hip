@@ -1440,19 +1440,18 @@ __global__ __launch_bounds__(256) void k_bwd_act_rows(const TS* __restrict__ X, 
   for (int o = 0; o < NAMAX; ++o) dst[o] = ga[o];
 }
 
-// MFMA form of the two row passes above for a bf16 state: full rows with
-// 2N <= 32 NOB outputs (N = 4, 8, 16 in one block of 32, N = 32 in two; the
-// padding outputs are zero) and active rows with k * Kr + k * k <= 32.  A
-// workgroup takes RW consecutive weight rows K (wave w: rows 16w .. 16w + 15,
-// inside one stream / slot) and a chunk of tokens, in steps of 32 tokens
-// staged in LDS:
+// MFMA form of the two row passes above for a bf16 state: a workgroup takes
+// consecutive weight rows K (wave w: rows 16w .. 16w + 15, inside one stream /
+// slot) and a chunk of tokens, in steps of 32 tokens staged in LDS:
 //   dX[t, K] += sum_o W[K, o] dz'[t, o] + (row terms)   MFMA D[16 K x 16 t], contraction over 32 outputs a block
 //   dW[K, o] += sum_t x[t, K] dz'[t, o]                 MFMA D[16 o x 16 K], contraction over 32 tokens
-// with dz' the per-token scaled logit gradients (full: r_ln dz_r | r dz_pre;
-// active: r_a dz_act), entered as a bf16 pair hi + lo (2^-16 relative).  The
-// pairs are formed once per token by k_dz_pack, in the two layouts the MFMA
-// operands read (token rows for dX, 32-token transposes for dW).  The
-// full-row dW_r misses the token sum of mu dz'_r, which the reduction removes.
+// with dz' the per-token scaled logit gradients (full rows: r_ln dz_r | r
+// dz_pre; active rows: r_a dz_act), entered as a bf16 pair hi + lo (2^-16
+// relative).  The pairs are formed once per token by k_dz_pack, in the two
+// layouts the MFMA operands read (token rows for dX, 32-token transposes for
+// dW).  The full rows take the ring pass of xhc_bwd_rows.hip (whose dW_r
+// misses the token sum of mu dz'_r, which the reduction removes); the active
+// rows of a routed state, gathered through idx, take k_bwd_act_rows_mfma.
 constexpr int kMfRows = 64;    // weight rows per workgroup
 constexpr int kDzBlock = 32;   // tokens per transposed block of the packed dz' (= kMfStep)
 constexpr int kMfStep = 32;    // tokens per step
@@ -1464,7 +1463,7 @@ constexpr int kMfXPitch = kMfRows + 8;   // bf16 per staged token row (pad: fewe
 //   rows[t][0 .. NO)   hi,  rows[t][NO .. 2 NO)  lo
 //   tr[b][o][u]        the same values of token 32 b + u, row o of 2 NO
 // full rows (act = 0): r_ln dz_r | r dz_pre; active rows: r_a dz_act.
-// srec (full rows, or null): [Tp][8] per-token scalars of the ring pass.
+// srec (or null): [Tp][8] per-token scalars of the ring pass.
 __global__ __launch_bounds__(256) void k_dz_pack(const float* __restrict__ tok, int64_t T, int N, int NA, int act,
                                                  int NO, uint16_t* __restrict__ rows, uint16_t* __restrict__ tr,
                                                  float* __restrict__ srec) {
@@ -1487,65 +1486,45 @@ __global__ __launch_bounds__(256) void k_dz_pack(const float* __restrict__ tok, 
   uint16_t* blk = tr + (t / kDzBlock) * 2 * NO * kDzBlock;
   blk[o * kDzBlock + t % kDzBlock] = (uint16_t)hb;
   blk[(NO + o) * kDzBlock + t % kDzBlock] = (uint16_t)lb;
-  // the token's row statistics as the full-row ring pass reads them:
-  // r_ln, mu, m1, m2, beta_pre, then zero
+  // the token's scalars as the ring pass reads them: r_ln, mu, m1, m2, beta,
+  // then zero (full rows: beta_pre; active rows: beta_a, the others zero)
   if (srec && o < 8) {
     const int src[5] = {1, 2, 4, 5, 3};
-    srec[t * 8 + o] = (t < T && o < 5) ? tok[t * tok_floats(N, NA) + 2 * N + NA + src[o]] : 0.f;
+    float sv = 0.f;
+    if (t < T && o < 5 && (!act || o == 4)) sv = tok[t * tok_floats(N, NA) + 2 * N + NA + (act ? 7 : src[o])];
+    srec[t * 8 + o] = sv;
   }
 }
 
-// 4 consecutive gradient elements of a bf16 or fp32 accumulator row, as
-// loaded (raw) and as floats
-template <typename TD> struct Raw4;
-template <> struct Raw4<uint16_t> {
-  typedef uint2 type;
-  static __device__ __forceinline__ type load(const uint16_t* p) { return *reinterpret_cast<const uint2*>(p); }
-  static __device__ __forceinline__ type zero() { return make_uint2(0, 0); }
-  static __device__ __forceinline__ void unpack(const type& v, float (&d)[4]) {
-    d[0] = bf_lo(v.x); d[1] = bf_hi(v.x); d[2] = bf_lo(v.y); d[3] = bf_hi(v.y);
-  }
-};
-template <> struct Raw4<float> {
-  typedef float4 type;
-  static __device__ __forceinline__ type load(const float* p) { return *reinterpret_cast<const float4*>(p); }
-  static __device__ __forceinline__ type zero() { return make_float4(0.f, 0.f, 0.f, 0.f); }
-  static __device__ __forceinline__ void unpack(const type& v, float (&d)[4]) {
-    d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-  }
-};
-__device__ __forceinline__ void ld4(const uint16_t* p, float (&d)[4]) {
-  const uint2 v = *reinterpret_cast<const uint2*>(p);
-  d[0] = bf_lo(v.x); d[1] = bf_hi(v.x); d[2] = bf_lo(v.y); d[3] = bf_hi(v.y);
-}
-__device__ __forceinline__ void ld4(const float* p, float (&d)[4]) {
-  const float4 v = *reinterpret_cast<const float4*>(p);
-  d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-}
+// 4 consecutive bf16 gradient elements from floats
 __device__ __forceinline__ void st4(uint16_t* p, const float (&d)[4]) {
   *reinterpret_cast<uint2*>(p) = make_uint2(pack2bf(d[0], d[1]), pack2bf(d[2], d[3]));
 }
-__device__ __forceinline__ void st4(float* p, const float (&d)[4]) {
-  *reinterpret_cast<float4*>(p) = make_float4(d[0], d[1], d[2], d[3]);
-}
 
-// TD: element type of the gradient rows dX (bf16, or fp32 for a state whose
-// values are bf16 but whose gradient is kept in fp32)
-// ADIN (active rows): din is given and row j gains Hpre[t, j] din[t] (Hpre
-// then [T, k] slot weights)
-template <bool ACT, typename TD = uint16_t, int RW = kMfRows, bool ADIN = false, int NOB = 1>
-__global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __restrict__ X,
-                                                       const uint16_t* __restrict__ din, TD* __restrict__ dX,
-                                                       const float* __restrict__ Wa, const float* __restrict__ Wb,
-                                                       const float* __restrict__ Hpre,
-                                                       const int32_t* __restrict__ idx, const float* __restrict__ tok,
-                                                       int64_t T, int N, int k, int C, int Kr, int NA,
-                                                       int64_t tchunk, const uint16_t* __restrict__ dzp,
-                                                       float* __restrict__ wpa, float* __restrict__ wpb) {
-  constexpr int NT = RW * 4, PIECES = RW / 8;   // threads; 16-byte pieces of a staged token row
-  constexpr int NO = 32 * NOB, NOH = 2 * NOB;   // outputs (padded); 16-output tiles of dW
-  constexpr int DZP = NO / 32 * 512 / NT;       // 16-byte pieces of packed dz' per thread and step
-  static_assert(!ACT || NOB == 1, "active rows: at most 32 outputs");
+// Active rows of a routed bf16 state (k * Kr + k * k <= 32 outputs, bf16
+// gradient rows updated in place at the routed rows): 128 weight rows (128
+// channels of one slot) per workgroup of 512 threads.  The inputs of step
+// tb + 32 are fetched into registers while step tb is computed: this thread's
+// pieces of the packed dz', one per-token scalar and 16 bytes of the state
+// rows, and its gradient elements.  Every load is issued without a branch (a
+// token past the chunk reads the chunk's last token; its dz' row and state row
+// are zeroed where they are staged, its gradient row is not stored) and the
+// barriers wait for LDS traffic only, so a step waits for nothing but its own
+// prefetched loads.  The routed row of each token is loaded one step earlier
+// still (rid), so the state and gradient loads do not wait on it.
+constexpr int kActRows = 2 * kMfRows;   // weight rows per workgroup
+__global__ __launch_bounds__(4 * kActRows) void k_bwd_act_rows_mfma(const uint16_t* __restrict__ X,
+                                                                uint16_t* __restrict__ dX,
+                                                                const float* __restrict__ W_post,
+                                                                const float* __restrict__ W_res,
+                                                                const int32_t* __restrict__ idx,
+                                                                const float* __restrict__ tok, int64_t T, int N, int k,
+                                                                int C, int Kr, int NA, int64_t tchunk,
+                                                                const uint16_t* __restrict__ dzp,
+                                                                float* __restrict__ wpa) {
+  constexpr int RW = kActRows, NT = RW * 4, PIECES = RW / 8;   // threads; 16-byte pieces of a staged token row
+  constexpr int NO = 32, NOH = 2;                              // outputs (padded); 16-output tiles of dW
+  constexpr int DZP = 512 / NT;                                // 16-byte pieces of packed dz' per thread and step
   static_assert(kMfStep == kDzBlock && DZP * NT == 16 * NO, "a step copies its packed dz' in whole pieces");
   __shared__ __align__(16) uint16_t xs[kMfStep][RW + 8];
   // packed dz' of the step: token rows (hi | lo) and the transpose; the row
@@ -1553,75 +1532,55 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
   // 16-lane group on distinct banks
   __shared__ __align__(16) uint16_t dzr[kMfStep][2 * NO + 8];
   __shared__ __align__(16) uint16_t dzt[2 * NO][kMfStep + 8];
-  __shared__ float sc[kMfStep][8];
-  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  __shared__ float beta_s[kMfStep];
+  const int lane = threadIdx.x % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave));   // uniform: its branches are scalar
   const int l16 = lane % 16, g4 = lane / 16;
-  const int64_t K0 = (int64_t)blockIdx.x * RW;                // first weight row of the workgroup
-  const int part = (int)(K0 / C);                              // stream (full) or slot (active)
+  const int64_t K0 = (int64_t)blockIdx.x * RW;   // first weight row of the workgroup
+  const int part = (int)(K0 / C);                 // slot
   const int c0 = (int)(K0 % C);
-  const int64_t NK = ACT ? (int64_t)k * C : (int64_t)N * C;   // weight rows
-  const int NP = k * Kr;                                       // active: W_post columns
+  const int64_t NK = (int64_t)k * C;              // weight rows
+  const int NP = k * Kr;                          // W_post columns
   const int TF = tok_floats(N, NA);
-  // A operand of the dX product: rows K0 + 16 wave + l16, outputs 32 b + 8 g4 .. + 7, as bf16
-  uint4 wfrag[NOB];
-#pragma unroll
-  for (int b = 0; b < NOB; ++b) {
+  // A operand of the dX product: rows K0 + 16 wave + l16, outputs 8 g4 .. + 7, as bf16
+  uint4 wfrag;
+  {
     float f[8];
     const int64_t K = K0 + 16 * wave + l16;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int o = 32 * b + 8 * g4 + e;
+      const int o = 8 * g4 + e;
       float v = 0.f;
-      if (ACT) {
-        if (o < NP) v = Wa[K * NP + o];
-        else if (o < NA) v = Wb[K * (k * k) + (o - NP)];
-      } else {
-        if (o < N) v = Wa[K * N + o];
-        else if (o < 2 * N) v = Wb[K * N + (o - N)];
-      }
+      if (o < NP) v = W_post[K * NP + o];
+      else if (o < NA) v = W_res[K * (k * k) + (o - NP)];
       f[e] = __uint_as_float(f2bf(v) << 16);
     }
-    wfrag[b] = pack8(f);
+    wfrag = pack8(f);
   }
   f32x4 dw[NOH];
 #pragma unroll
   for (int oh = 0; oh < NOH; ++oh) dw[oh] = f32x4{0.f, 0.f, 0.f, 0.f};
   const int64_t t0 = (int64_t)blockIdx.y * tchunk, t1 = (t0 + tchunk < T) ? t0 + tchunk : T;
-  // The inputs of step tb + 32 are fetched into registers while step tb is
-  // computed: this thread's pieces of the packed dz', scalars (threads < 32)
-  // and 16 bytes of the state rows.  Every load is issued without a branch (a
-  // token past the chunk reads the chunk's last token; its dz' row and state
-  // row are zeroed where they are staged, its gradient row is not stored) and
-  // the barriers wait for LDS traffic only, so a step waits for nothing but
-  // its own prefetched loads: not for the previous step's stores, nor for the
-  // loads of the next.  Active rows: the row of each token is loaded one step
-  // earlier still (rid), so the state and gradient loads do not wait on it.
   const uint16_t* const dzrows = dzp;
   const uint16_t* const dztr = dzp + (T + kDzBlock - 1) / kDzBlock * kDzBlock * 2 * NO;
-  // the wave index as a uniform value: the branches below on it are scalar
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  static_assert(NT >= 7 * kMfStep, "one scalar of a step per thread");
   struct Stage {
     uint4 dz[DZP];
-    float scal;
-    int rowd[2];                     // rows of the lane's two gradient tokens
+    float beta;     // beta_a of token threadIdx.x (threads < 32)
+    int rowd[2];    // routed rows of the lane's two gradient tokens
     uint4 x;
-    typename Raw4<TD>::type dx[2];   // the lane's accumulator elements (two token halves), as loaded
-    uint2 din[2];
+    uint2 dx[2];    // the lane's gradient elements (two token halves), as loaded
   };
   auto tok_at = [&](int64_t tb, int u) -> int64_t { return tb + u < t1 ? tb + u : t1 - 1; };
-  int rid[3] = {part, part, part};   // rows of the next fetch: state token, gradient tokens 0 and 1
+  int rid[3];   // routed rows of the next fetch: state token, gradient tokens 0 and 1
   auto fetch_rows = [&](int64_t tb) {
-    if (ACT) {
-      rid[0] = idx[tok_at(tb, threadIdx.x / PIECES) * k + part];
-      rid[1] = idx[tok_at(tb, l16) * k + part];
-      rid[2] = idx[tok_at(tb, 16 + l16) * k + part];
-    }
+    rid[0] = idx[tok_at(tb, threadIdx.x / PIECES) * k + part];
+    rid[1] = idx[tok_at(tb, l16) * k + part];
+    rid[2] = idx[tok_at(tb, 16 + l16) * k + part];
   };
   // pieces q of the packed dz': [0, 8 NO) token rows (NO / 4 pieces a token),
   // [8 NO, 16 NO) the transposed block (4 pieces a row); 8 NO is a multiple
   // of 64, so the choice is the same across a wave
-  auto dz_rows = [&](int r) { return wave_u * kWave + r * NT < 8 * NO; };
+  auto dz_rows = [&](int r) { return wave * kWave + r * NT < 8 * NO; };
   auto fetch = [&](Stage& st, int64_t tb) {
 #pragma unroll
     for (int r = 0; r < DZP; ++r) {
@@ -1630,36 +1589,23 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
         st.dz[r] = *reinterpret_cast<const uint4*>(dzrows + tok_at(tb, q / (NO / 4)) * 2 * NO + (q % (NO / 4)) * 8);
       } else {
         const int qq = q - 8 * NO;
-        st.dz[r] = *reinterpret_cast<const uint4*>(dztr + (tok_at(tb, 0) / kDzBlock) * 2 * NO * kDzBlock + (qq / 4) * kDzBlock +
-                                                   (qq % 4) * 8);
+        st.dz[r] = *reinterpret_cast<const uint4*>(dztr + (tok_at(tb, 0) / kDzBlock) * 2 * NO * kDzBlock +
+                                                   (qq / 4) * kDzBlock + (qq % 4) * 8);
       }
     }
     st.x = *reinterpret_cast<const uint4*>(X + (tok_at(tb, threadIdx.x / PIECES) * N + rid[0]) * (int64_t)C + c0 +
                                            (threadIdx.x % PIECES) * 8);
-    // the accumulator rows of the step (other tokens than the step being
+    // the gradient rows of the step (other tokens than the step being
     // computed, so reading them a step ahead is safe)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int64_t t = tok_at(tb, 16 * h + l16);
-      const int kr = 16 * wave + 4 * g4;
       st.rowd[h] = rid[1 + h];
-      st.dx[h] = Raw4<TD>::load(dX + (t * N + rid[1 + h]) * (int64_t)C + c0 + kr);
-      st.din[h] = make_uint2(0, 0);
-      if (!ACT || ADIN) st.din[h] = *reinterpret_cast<const uint2*>(din + t * C + c0 + kr);
+      st.dx[h] = *reinterpret_cast<const uint2*>(dX + (t * N + rid[1 + h]) * (int64_t)C + c0 + 16 * wave + 4 * g4);
     }
-    // per-token scalars, one per thread (value vi of token u; threads past
-    // the 7 values load value 0 again and do not stage it), so that every
-    // wave issues the same loads
-    {
-      const int vi = threadIdx.x / kMfStep;
-      const int64_t t = tok_at(tb, threadIdx.x % kMfStep);
-      const float* src;
-      if (ACT)   // beta_a; active rows with din: the weight of the slot's read of din
-        src = (ADIN && vi == 1) ? Hpre + t * k + part : tok + t * TF + 2 * N + NA + 7;
-      else       // r, r_ln, mu, beta_pre, m1, m2, then H^pre of the stream
-        src = vi == 6 ? Hpre + t * N + part : tok + t * TF + 2 * N + NA + (vi < 6 ? vi : 0);
-      st.scal = *src;
-    }
+    // beta_a of token threadIdx.x % 32, loaded by every thread (the same
+    // loads on every wave)
+    st.beta = tok[tok_at(tb, threadIdx.x % kMfStep) * TF + 2 * N + NA + 7];
   };
   // One step of 32 tokens.  FULL: all 32 tokens exist, so the step has no
   // per-token predicates; the last, partial step of the chunk (T % 32 tokens)
@@ -1681,55 +1627,32 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
         *reinterpret_cast<uint4*>(&dzt[row][off]) = cur.dz[r];
       }
     }
-    if (threadIdx.x < 7 * kMfStep) sc[threadIdx.x % kMfStep][threadIdx.x / kMfStep] = cur.scal;
+    if (threadIdx.x < kMfStep) beta_s[threadIdx.x] = cur.beta;
     *reinterpret_cast<uint4*>(&xs[threadIdx.x / PIECES][(threadIdx.x % PIECES) * 8]) =
         (FULL || (int)(threadIdx.x / PIECES) < nt) ? cur.x : make_uint4(0, 0, 0, 0);
     const int rowd[2] = {cur.rowd[0], cur.rowd[1]};
-    // ---- dX: two token halves; the accumulator rows were read a step ahead
-    const typename Raw4<TD>::type dxr[2] = {cur.dx[0], cur.dx[1]};
-    const uint2 dinv[2] = {cur.din[0], cur.din[1]};
+    const uint2 dxr[2] = {cur.dx[0], cur.dx[1]};
     lds_barrier();
     fetch(cur, tb + kMfStep);
     fetch_rows(tb + 2 * kMfStep);
+    // ---- dX: two token halves; the gradient rows were read a step ahead
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int u = 16 * h + l16;   // B operand token of this lane
       f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int b = 0; b < NOB; ++b) {
-        const uint4 bh = *reinterpret_cast<const uint4*>(&dzr[u][32 * b + 8 * g4]);
-        const uint4 bl = *reinterpret_cast<const uint4*>(&dzr[u][NO + 32 * b + 8 * g4]);
-        acc = mfma_16x16x32(wfrag[b], bh, acc);
-        acc = mfma_16x16x32(wfrag[b], bl, acc);
-      }
+      acc = mfma_16x16x32(wfrag, *reinterpret_cast<const uint4*>(&dzr[u][8 * g4]), acc);
+      acc = mfma_16x16x32(wfrag, *reinterpret_cast<const uint4*>(&dzr[u][NO + 8 * g4]), acc);
       // lane holds rows 16 wave + 4 g4 + v of token u
       if (FULL || u < nt) {
-        const int64_t t = tb + u;
-        const int kr = 16 * wave + 4 * g4;   // row offset inside the 64
+        const int kr = 16 * wave + 4 * g4;
         const uint2 xv = *reinterpret_cast<const uint2*>(&xs[u][kr]);
         const float x[4] = {bf_lo(xv.x), bf_hi(xv.x), bf_lo(xv.y), bf_hi(xv.y)};
-        float gsum[4];
-        if (ACT) {
-          const float beta_a = sc[u][0];
+        const float beta_a = beta_s[u];
+        const float dxv[4] = {bf_lo(dxr[h].x), bf_hi(dxr[h].x), bf_lo(dxr[h].y), bf_hi(dxr[h].y)};
+        float d[4];
 #pragma unroll
-          for (int v = 0; v < 4; ++v) gsum[v] = acc[v] - beta_a * x[v];
-          if (ADIN) {
-            const float hs = sc[u][1];
-            const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
-#pragma unroll
-            for (int v = 0; v < 4; ++v) gsum[v] += hs * gi[v];
-          }
-        } else {
-          const float r_ln = sc[u][1], mu = sc[u][2], bpre = sc[u][3], m1 = sc[u][4], m2 = sc[u][5], hp = sc[u][6];
-          const float gi[4] = {bf_lo(dinv[h].x), bf_hi(dinv[h].x), bf_lo(dinv[h].y), bf_hi(dinv[h].y)};
-#pragma unroll
-          for (int v = 0; v < 4; ++v)
-            gsum[v] = hp * gi[v] + acc[v] - bpre * x[v] - r_ln * m1 - r_ln * r_ln * (x[v] - mu) * m2;
-        }
-        float dxv[4];
-        Raw4<TD>::unpack(dxr[h], dxv);
-        const float d[4] = {dxv[0] + gsum[0], dxv[1] + gsum[1], dxv[2] + gsum[2], dxv[3] + gsum[3]};
-        st4(dX + (t * N + rowd[h]) * (int64_t)C + c0 + kr, d);
+        for (int v = 0; v < 4; ++v) d[v] = dxv[v] + (acc[v] - beta_a * x[v]);
+        st4(dX + ((tb + u) * N + rowd[h]) * (int64_t)C + c0 + kr, d);
       }
     }
     // ---- dW: contraction over the 32 staged tokens (rows past nt are zero)
@@ -1761,24 +1684,10 @@ __global__ __launch_bounds__(RW * 4) void k_bwd_rows_mfma(const uint16_t* __rest
     if (tb < t1) step(std::false_type{}, cur, tb);
   }
   // lane holds dW[row K0 + 16 wave + l16][output 16 oh + 4 g4 + v]
-  const int64_t K = K0 + 16 * wave + l16;
-  if (ACT) {
-    float* dst = wpa + ((int64_t)blockIdx.y * NK + K) * 32;
+  float* dst = wpa + ((int64_t)blockIdx.y * NK + K0 + 16 * wave + l16) * 32;
 #pragma unroll
-    for (int oh = 0; oh < 2; ++oh)
-      *reinterpret_cast<float4*>(dst + 16 * oh + 4 * g4) = make_float4(dw[oh][0], dw[oh][1], dw[oh][2], dw[oh][3]);
-  } else {
-    // outputs 16 oh + 4 g4 .. + 3 lie inside one of the two halves (N % 4 == 0)
-#pragma unroll
-    for (int oh = 0; oh < NOH; ++oh) {
-      const int o = 16 * oh + 4 * g4;
-      if (o < 2 * N) {
-        float* dst = (o < N ? wpa + ((int64_t)blockIdx.y * NK + K) * N + o
-                            : wpb + ((int64_t)blockIdx.y * NK + K) * N + (o - N));
-        *reinterpret_cast<float4*>(dst) = make_float4(dw[oh][0], dw[oh][1], dw[oh][2], dw[oh][3]);
-      }
-    }
-  }
+  for (int oh = 0; oh < NOH; ++oh)
+    *reinterpret_cast<float4*>(dst + 16 * oh + 4 * g4) = make_float4(dw[oh][0], dw[oh][1], dw[oh][2], dw[oh][3]);
 }
 
 // corr[o] = sum_t mu_t r_ln,t dz_r[t, o] (the part of dW_r the MFMA full-row
@@ -2047,11 +1956,12 @@ BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws) {
   w.dzf = reinterpret_cast<uint16_t*>((a + 15) / 16 * 16);
   w.dza = w.dzf + Tp * 2 * (2 * N <= 32 ? 32 : 64) * 2;
   w.srec = reinterpret_cast<float*>(w.dza + Tp * 2 * 32 * 2);   // 16-byte aligned: Tp % 32 == 0
+  w.sreca = w.srec + Tp * 8;
   return w;
 }
 
 bool bwd_rows_multi_supported(const xhc_dims* d, int Q) {
-  return d->state_dtype == XHC_BF16 && d->N == 16 && bwd_rows_ring_supported(d->N, d->C, kRowChunk) &&
+  return d->state_dtype == XHC_BF16 && d->N == 16 && bwd_rows_ring_supported((int64_t)d->N * d->C, d->C, kRowChunk) &&
          (Q == 2 || Q == 4);
 }
 
@@ -2112,10 +2022,32 @@ hipError_t launch_bwd_rows_multi(const xhc_dims* d, int Q, const void* X, void* 
   // the ring pass reads the prep rows' scalars (r_ln, mu, m1, m2, sum beta_pre)
   // at offset 16 (Q + 1) of each row
   const int no = 16 * (Q + 1);
-  const void* dins[kMultiMaxQ];
-  for (int q = 0; q < Q; ++q) dins[q] = m.din[q];
-  return launch_bwd_rows_ring(Q, X, dX, dins, m.hrd, m.w, m.wout, 16, no, dzp, (int)nop, prep + no, no + 8, T, N, C,
-                              kRowChunk, s);
+  RowRingDesc rd{};
+  rd.X = X;
+  rd.dX = dX;
+  rd.nq = Q;
+  for (int q = 0; q < Q; ++q) {
+    rd.din[q] = m.din[q];
+    rd.hp[q] = m.hrd[q];
+  }
+  rd.hp_stride = N;
+  for (int b = 0; b <= Q; ++b) {
+    rd.w[b] = m.w[b];
+    rd.win[b] = 16;
+    rd.wout[b] = m.wout[b];
+  }
+  rd.nwin = Q + 1;
+  rd.wout_w = 16;
+  rd.nout = no;
+  rd.dzp = dzp;
+  rd.nop = (int)nop;
+  rd.srec = prep + no;
+  rd.srec_stride = no + 8;
+  rd.T = T;
+  rd.tchunk = kRowChunk;
+  rd.N = N;
+  rd.C = C;
+  return launch_bwd_rows_ring(rd, (int64_t)N * C, s);
 }
 
 size_t bwd_pre_ws_bytes(const xhc_dims* d) {
@@ -2131,7 +2063,7 @@ size_t bwd_pre_ws_bytes(const xhc_dims* d) {
   n += (size_t)N;                                                // token sum of mu dz'_r
   const size_t Tp = (size_t)((T + kDzBlock - 1) / kDzBlock * kDzBlock);
   const size_t dz = Tp * 2 * ((2 * N <= 32 ? 32 : 64) + 32) * 2 * sizeof(uint16_t);   // packed dz'
-  return n * sizeof(float) + 16 + dz + Tp * 8 * sizeof(float) + 1024;                 // + scalar rows
+  return n * sizeof(float) + 16 + dz + 2 * Tp * 8 * sizeof(float) + 1024;             // + scalar rows
 }
 
 bool bwd_pre_supported(const xhc_dims* d) {
@@ -2211,40 +2143,75 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
                                                                                 w.dza + Tp * 2 * 32, nullptr);
       if (dense_rows) {
         // 2N outputs padded to one block of 32 (N <= 16) or two (N = 32)
-        const void* dins[1] = {d_input};
-        const float* hps[1] = {Hrd};
-        const float* ws2[2] = {W_r, W_pre};
-        float* wo2[2] = {wpart_r, wpart_p};
-        e = launch_bwd_rows_ring(1, X, dX, dins, hps, ws2, wo2, N, 2 * N, w.dzf, NOf, w.srec, 8, T, N, C, kRowChunk,
-                                 s);
+        RowRingDesc rd{};
+        rd.X = X;
+        rd.dX = dX;
+        rd.nq = 1;
+        rd.din[0] = d_input;
+        rd.hp[0] = Hrd;
+        rd.hp_stride = N;
+        rd.w[0] = W_r;
+        rd.w[1] = W_pre;
+        rd.win[0] = rd.win[1] = N;
+        rd.nwin = 2;
+        rd.wout[0] = wpart_r;
+        rd.wout[1] = wpart_p;
+        rd.wout_w = N;
+        rd.nout = 2 * N;
+        rd.dzp = w.dzf;
+        rd.nop = NOf;
+        rd.srec = w.srec;
+        rd.srec_stride = 8;
+        rd.T = T;
+        rd.tchunk = kRowChunk;
+        rd.N = N;
+        rd.C = C;
+        e = launch_bwd_rows_ring(rd, (int64_t)N * C, s);
         if (e != hipSuccess) return e;
       }
-      // 128 rows per workgroup as for the full rows (C % 256 == 0)
-      const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
+      // 128 rows per workgroup (C % 256 == 0); the dense read of the active
+      // rows is in the full-row pass
+      const dim3 ga((unsigned)((int64_t)k * C / kActRows), (unsigned)nchunk);
       if (act_rows)
-        k_bwd_rows_mfma<true, uint16_t, 2 * kMfRows><<<ga, dim3(8 * kMfRows), 0, s>>>(reinterpret_cast<const uint16_t*>(X), nullptr,
-            reinterpret_cast<uint16_t*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dza,
-            wpart_a, nullptr);   // (the dense read of the active rows is in the full-row pass)
+        k_bwd_act_rows_mfma<<<ga, dim3(4 * kActRows), 0, s>>>(reinterpret_cast<const uint16_t*>(X),
+            reinterpret_cast<uint16_t*>(dX), W_post, W_res, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dza, wpart_a);
       k_mu_dz_sum<<<dim3((unsigned)N), dim3(256), 0, s>>>(tok, T, N, NA, pgsum + pg_floats(N, k, Kr));
     }
-    // an fp32 state given with its exact bf16 copy: the active rows take the
-    // MFMA pass with fp32 gradient rows
+    // an fp32 state given with its exact bf16 copy (the k-row view of an
+    // xHC-Flash sublayer, N = k, whose slot j is row j): the active rows take
+    // the ring pass with fp32 gradient rows
     const bool mfa32 = !mf && X_bf16 && d->state_dtype == XHC_F32 && NA <= 32 && C % (2 * kMfRows) == 0;
     if (mfa32 && act_rows) {
-      const dim3 ga((unsigned)((int64_t)k * C / (2 * kMfRows)), (unsigned)nchunk);
+      if (N != k) return hipErrorInvalidValue;
       const int64_t Tp = (T + kDzBlock - 1) / kDzBlock * kDzBlock;
       k_dz_pack<<<dim3((unsigned)((Tp * 32 + 255) / 256)), dim3(256), 0, s>>>(tok, T, N, NA, 1, 32, w.dza,
-                                                                              w.dza + Tp * 2 * 32, nullptr);
-      if (act_din)
-        k_bwd_rows_mfma<true, float, 2 * kMfRows, true><<<ga, dim3(8 * kMfRows), 0, s>>>(
-            reinterpret_cast<const uint16_t*>(X_bf16), reinterpret_cast<const uint16_t*>(act_din),
-            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dza,
-            wpart_a, nullptr);
-      else
-        k_bwd_rows_mfma<true, float, 2 * kMfRows><<<ga, dim3(8 * kMfRows), 0, s>>>(
-            reinterpret_cast<const uint16_t*>(X_bf16), nullptr,
-            reinterpret_cast<float*>(dX), W_post, W_res, Hpre, idx, tok, T, N, k, C, Kr, NA, kRowChunk, w.dza,
-            wpart_a, nullptr);
+                                                                              w.dza + Tp * 2 * 32, w.sreca);
+      RowRingDesc rd{};
+      rd.X = X_bf16;
+      rd.dX = dX;
+      rd.dx_f32 = true;
+      rd.nq = act_din ? 1 : 0;
+      rd.din[0] = act_din;
+      rd.hp[0] = Hpre;   // [T, k]: the weight of each slot's read of d input
+      rd.hp_stride = k;
+      rd.w[0] = W_post;
+      rd.w[1] = W_res;
+      rd.win[0] = k * Kr;
+      rd.win[1] = k * k;
+      rd.nwin = 2;
+      rd.wout[0] = wpart_a;
+      rd.wout_w = 32;
+      rd.nout = NA;
+      rd.dzp = w.dza;
+      rd.nop = 32;
+      rd.srec = w.sreca;
+      rd.srec_stride = 8;
+      rd.T = T;
+      rd.tchunk = kRowChunk;
+      rd.N = N;
+      rd.C = C;
+      e = launch_bwd_rows_ring(rd, (int64_t)k * C, s);
+      if (e != hipSuccess) return e;
     }
     const dim3 gfull((unsigned)(((int64_t)N * C + 255) / 256), (unsigned)nchunk);
 #define XHC_FULL_ROWS(NNV)                                                                                       \

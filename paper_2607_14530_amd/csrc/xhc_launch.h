@@ -134,19 +134,37 @@ constexpr int kBwdPreAll = 0, kBwdPreTokens = 1, kBwdPreReduce = 2, kBwdPreToken
 struct BwdPreWs {
   float *part, *tok, *pg, *wpart_r, *wpart_p, *wpart_a, *red_a, *pgsum;
   uint16_t *dzf, *dza;   // packed dz' of the full-row and active-row MFMA passes
-  float* srec;           // per-token scalars of the full-row ring pass [Tp][8]
+  float *srec, *sreca;   // per-token scalars of the ring passes [Tp][8]: full rows, active rows
 };
-// Full-row pass of Q pre-map reverses over one bf16 state, inputs staged
-// through an LDS ring (xhc_bwd_rows.hip): din[q] [T][C] input gradients,
-// hp[q] [T][N] dense-read weights, w[b] / wout[b] weight blocks of wb outputs
-// ([N C][wb]) and their partials ([chunk][N C][wb]), nout real outputs, dzp
-// the packed dz' (NOP = nop outputs), srec per-token scalar rows (stride in
-// floats, 16-byte aligned); dX updated in place.
-bool bwd_rows_ring_supported(int N, int C, int64_t tchunk);
-hipError_t launch_bwd_rows_ring(int Q, const void* X, void* dX, const void* const* din, const float* const* hp,
-                                const float* const* w, float* const* wout, int wb, int nout, const uint16_t* dzp,
-                                int nop, const float* srec, int64_t srec_stride, int64_t T, int N, int C,
-                                int64_t tchunk, hipStream_t s);
+// Row pass of the pre-map reverse with its inputs staged through an LDS ring
+// (xhc_bwd_rows.hip): dX += (input-gradient reads, projection and
+// normalisation terms) over rows x 128-channel blocks of a bf16 state, and the
+// weight-gradient partials of the projection.  Weight row K = i C + c is
+// channel c of row i of every token; slot j of the k-row view is row j.
+constexpr int kRowRingMaxQ = 4;
+struct RowRingDesc {
+  const void* X;                        // bf16 state [T][N][C]
+  void* dX;                             // gradient rows [T][N][C], updated in place
+  bool dx_f32;                          // fp32 gradient rows (else bf16)
+  int nq;                               // input gradients, 0 .. kRowRingMaxQ
+  const void* din[kRowRingMaxQ];        // bf16 [T][C]
+  const float* hp[kRowRingMaxQ];        // their weights: row i of token t at t hp_stride + i
+  int hp_stride;
+  const float* w[kRowRingMaxQ + 1];     // weight blocks [rows][win[b]] (fp32), outputs in block order
+  int win[kRowRingMaxQ + 1];
+  int nwin;
+  float* wout[kRowRingMaxQ + 1];        // partials [chunk][rows][wout_w], outputs in blocks of wout_w
+  int wout_w;
+  int nout;                             // outputs
+  const uint16_t* dzp;                  // packed dz' of nop outputs (rows, then 32-token transposes)
+  int nop;
+  const float* srec;                    // per-token r_ln, mu, m1, m2, beta (16-byte aligned rows)
+  int64_t srec_stride;                  // floats
+  int64_t T, tchunk;                    // tokens; tokens per partial (a multiple of 32)
+  int N, C;
+};
+bool bwd_rows_ring_supported(int64_t rows, int C, int64_t tchunk);
+hipError_t launch_bwd_rows_ring(const RowRingDesc& d, int64_t rows, hipStream_t s);
 BwdPreWs bwd_pre_ws(const xhc_dims* d, char* ws);   // layout of launch_bwd_pre's workspace
 hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum, const float* W_r,
                           const float* W_pre, const float* W_res, const float* W_post, const float* alpha,
@@ -164,8 +182,9 @@ hipError_t launch_bwd_pre(const xhc_dims* d, const void* X, const float* colsum,
 // the full-state projection through W_r, W_pre): for a caller whose router
 // and pre-map weights are zero; d_input is then not read, H^pre enters as
 // zero gradient, and dW_r, dW_pre are not written.  X_bf16: for an fp32
-// state whose values are exactly bf16, the same rows as bf16 (read by the
-// MFMA form of the active-row pass; the gradient rows stay fp32), and then
+// state whose values are exactly bf16 and whose slot j is row j (N = k: the
+// k-row view of an xHC-Flash sublayer), the same rows as bf16 (read by the
+// ring form of the active-row pass; the gradient rows stay fp32), and then
 // act_din (bf16 [T, C]), when given: that pass also adds Hpre[t, j] act_din[t]
 // to active row j (Hpre then holds [T, k] slot weights).  act_rows
 // false leaves out the active-row pass (for a caller whose W_post and W_res
