@@ -201,17 +201,19 @@ __host__ __device__ __forceinline__ int32_t logit_key(float z) {
 
 // Rank of stream `lane` among the routing candidates m..15 of one token: the
 // number of candidates i whose (key, index) comes before (key, lane), key =
-// logit_key.  keyat(i) gives the key of stream i (in the single-pass kernel a
-// read of lane i).  The ranks of the 16 - m candidates are 0 .. 15 - m, each
-// once; slot m + rank takes the stream when rank < k - m.
-template <class LaneKey>
-__host__ __device__ __forceinline__ int route_rank16(LaneKey keyat, int32_t key, int lane, int m) {
+// logit_key.  The other 15 streams are visited in rotation order: keyrot(r),
+// r = 1 .. 15, is the key of stream (lane - r) mod 16 (in the single-pass
+// kernel a rotation of the 16-lane row, so no lane index is ever compared
+// with a loop constant and nothing is hoisted into per-lane masks).  The ranks
+// of the 16 - m candidates are 0 .. 15 - m, each once; slot m + rank takes the
+// stream when rank < k - m.
+template <class KeyRot>
+__host__ __device__ __forceinline__ int route_rank16(KeyRot keyrot, int32_t key, int lane, int m) {
   int rank = 0;
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    const int32_t ki = keyat(i);
-    // branch-free: the candidate test is uniform, the comparison a select;
-    // i == lane never counts
+  for (int r = 1; r < 16; ++r) {
+    const int i = (lane - r) & 15;
+    const int32_t ki = keyrot(r);
     const int before = (int)(ki > key) | ((int)(ki == key) & (int)(i < lane));
     rank += before & -(int)(i >= m);
   }

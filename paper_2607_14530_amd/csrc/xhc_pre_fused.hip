@@ -92,7 +92,6 @@ struct FusedArgs {
   float* part2;           // [G][NV1][T] active partials
   int64_t T;
   int C;
-  int G;                  // members per team = C / FCS
   int teams;
   int m;
   float eps;
@@ -202,10 +201,33 @@ __device__ __forceinline__ int lane_id_here() {
   return l;
 }
 
+// v of lane (l - r) mod 16 of this lane's 16-lane row (DPP row rotation; r
+// is a constant once the caller's loop is unrolled)
+__device__ __forceinline__ int32_t row_ror(int32_t v, int r) {
+  switch (r) {
+    case 1: return __builtin_amdgcn_update_dpp(0, v, 0x121, 0xF, 0xF, false);
+    case 2: return __builtin_amdgcn_update_dpp(0, v, 0x122, 0xF, 0xF, false);
+    case 3: return __builtin_amdgcn_update_dpp(0, v, 0x123, 0xF, 0xF, false);
+    case 4: return __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false);
+    case 5: return __builtin_amdgcn_update_dpp(0, v, 0x125, 0xF, 0xF, false);
+    case 6: return __builtin_amdgcn_update_dpp(0, v, 0x126, 0xF, 0xF, false);
+    case 7: return __builtin_amdgcn_update_dpp(0, v, 0x127, 0xF, 0xF, false);
+    case 8: return __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);
+    case 9: return __builtin_amdgcn_update_dpp(0, v, 0x129, 0xF, 0xF, false);
+    case 10: return __builtin_amdgcn_update_dpp(0, v, 0x12A, 0xF, 0xF, false);
+    case 11: return __builtin_amdgcn_update_dpp(0, v, 0x12B, 0xF, 0xF, false);
+    case 12: return __builtin_amdgcn_update_dpp(0, v, 0x12C, 0xF, 0xF, false);
+    case 13: return __builtin_amdgcn_update_dpp(0, v, 0x12D, 0xF, 0xF, false);
+    case 14: return __builtin_amdgcn_update_dpp(0, v, 0x12E, 0xF, 0xF, false);
+    default: return __builtin_amdgcn_update_dpp(0, v, 0x12F, 0xF, 0xF, false);
+  }
+}
+
 // value of v in lane i (compile-time lane: a scalar read, no LDS crossbar)
 __device__ __forceinline__ float lane_value(float v, int i) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), i));
 }
+template <int G>
 __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   extern __shared__ unsigned char tbuf[];   // [BUFB]; dynamic, as the LDS copy needs it
   __shared__ Smem sm;
@@ -216,7 +238,6 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid / kWave), lane = tid % kWave;
   const int tl = lane % 16, grp = lane / 16;
   const int par = grp >> 1, half = grp & 1;   // stream parity and channel half of this lane
-  const int G = a.G;
   const int team = blockIdx.x / G, s = blockIdx.x % G;
   if (team >= a.teams) return;
   const int C = a.C;
@@ -342,7 +363,7 @@ __global__ __launch_bounds__(FNT, 1) void k_pre_fused(FusedArgs a) {
       // rank among the candidates i >= m (total order of logit_key, ties to
       // the lower index; the same order as the multi-kernel route_token)
       const int32_t key = logit_key(z);
-      const int rank = route_rank16([&](int i) { return __builtin_amdgcn_readlane(key, i); }, key, lane, a.m);
+      const int rank = route_rank16([&](int r) { return row_ror(key, r); }, key, lane_id_here() & 15, a.m);
       int slot = -1;
       float pv = 1.0f;
       float sc = sigmoidf(z);
@@ -633,6 +654,22 @@ struct DeviceInfo {
 
 constexpr size_t kTileLds = (size_t)BUFB;
 
+// the kernel instance of a team size (G = C / 128, a power of two up to 32)
+const void* fused_kernel(int G) {
+  switch (G) {
+    case 1: return reinterpret_cast<const void*>(k_pre_fused<1>);
+    case 2: return reinterpret_cast<const void*>(k_pre_fused<2>);
+    case 4: return reinterpret_cast<const void*>(k_pre_fused<4>);
+    case 8: return reinterpret_cast<const void*>(k_pre_fused<8>);
+    case 16: return reinterpret_cast<const void*>(k_pre_fused<16>);
+    case 32: return reinterpret_cast<const void*>(k_pre_fused<32>);
+    default: return nullptr;
+  }
+}
+
+// CU count and resident workgroups per CU of every instance (all instances
+// have the same launch shape and LDS); the dynamic LDS limit is raised once
+// per device
 DeviceInfo device_info() {
   static thread_local int dev_cached = -1;
   static thread_local DeviceInfo info;
@@ -641,12 +678,15 @@ DeviceInfo device_info() {
   if (dev != dev_cached) {
     DeviceInfo di;
     if (hipDeviceGetAttribute(&di.cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return DeviceInfo{};
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(k_pre_fused), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)kTileLds) != hipSuccess)
-      return DeviceInfo{};
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&di.per_cu, reinterpret_cast<const void*>(k_pre_fused), FNT,
-                                                     kTileLds) != hipSuccess)
-      return DeviceInfo{};
+    di.per_cu = 1 << 30;
+    for (int G = 1; G <= kMaxG; G *= 2) {
+      const void* f = fused_kernel(G);
+      int per = 0;
+      if (hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, (int)kTileLds) != hipSuccess)
+        return DeviceInfo{};
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, f, FNT, kTileLds) != hipSuccess) return DeviceInfo{};
+      if (per < di.per_cu) di.per_cu = per;
+    }
     info = di;
     dev_cached = dev;
   }
@@ -706,7 +746,6 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
   float* sums = a.part2 + align256((size_t)G * NV1 * d->T * sizeof(float)) / sizeof(float);
   a.T = d->T;
   a.C = d->C;
-  a.G = G;
   a.teams = teams;
   a.m = d->m;
   a.eps = d->eps;
@@ -720,7 +759,7 @@ hipError_t launch_pre_fused(const xhc_dims* d, const void* X, const void* packed
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   void* args[] = {&a};
-  e = hipLaunchCooperativeKernel(reinterpret_cast<const void*>(k_pre_fused), dim3(teams * G), dim3(FNT), args,
+  e = hipLaunchCooperativeKernel(fused_kernel(G), dim3(teams * G), dim3(FNT), args,
                                  kTileLds, s);
   if (e != hipSuccess) return e;
   // active partials -> H^post, H^res (Sinkhorn + clamp)

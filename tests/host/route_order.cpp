@@ -30,7 +30,7 @@ int main() {
     for (int j = 0; j < k; ++j) fused[j] = -1;
     int rank[16];
     for (int lane = 0; lane < 16; ++lane) {
-      rank[lane] = xhc::route_rank16([&](int i) { return key[i]; }, key[lane], lane, m);
+      rank[lane] = xhc::route_rank16([&](int r) { return key[(lane - r) & 15]; }, key[lane], lane, m);
       if (lane < m) fused[lane] = lane;
       else if (rank[lane] < k - m) fused[m + rank[lane]] = lane;
     }
