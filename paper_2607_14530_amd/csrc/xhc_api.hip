@@ -282,6 +282,7 @@ xhc_status post_impl(const xhc_dims* d, void* X, const void* F, const float* con
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   clear_stale_error();
   float* wb = nullptr;
+  const float* gp = nullptr;
   hipError_t e = hipSuccess;
   if (d->Kr > 1) {
     const int np = d->Kr * (d->Kr + 1) / 2;
@@ -289,13 +290,13 @@ xhc_status post_impl(const xhc_dims* d, void* X, const void* F, const float* con
     wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
                                   align_up((size_t)gram_chunks(d->C, d->S, d->Kr, d->kappa) * np * (size_t)d->T *
                                            sizeof(float)));
+    gp = gpart;
     XHC_STEP("post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, d->Kr, d->kappa, conv_w, gpart, s));
-    XHC_STEP("post_coef", launch_post_coef(gpart, gram_chunks(d->C, d->S, d->Kr, d->kappa), d->T, d->k, d->Kr,
-                                           d->gram_schmidt, p, Hpost, wb, s));
   }
   XHC_STEP("post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, d->Kr, d->kappa,
-                                           conv_w, idx, p, Hres, Hpost, wb, nullptr, nullptr, nullptr, Xact_save,
-                                           s));
+                                           conv_w, idx, p, Hres, Hpost, gp,
+                                           gram_chunks(d->C, d->S, d->Kr, d->kappa), d->gram_schmidt, wb, nullptr,
+                                           nullptr, nullptr, Xact_save, s));
   return hip_status(e);
 }
 
@@ -607,18 +608,20 @@ xhc_status xhc_flash_post(const xhc_dims* d, int32_t Q, int32_t q, void* X, cons
   clear_stale_error();
   hipError_t e = hipSuccess;
   float* wb = nullptr;
+  const float* gp = nullptr;
   if (Kq > 1) {
     const int np = Kq * (Kq + 1) / 2;
     float* gpart = reinterpret_cast<float*>(workspace);
     wb = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
                                   align_up((size_t)gram_chunks(d->C, d->S, Kq, d->kappa) * np * (size_t)d->T *
                                            sizeof(float)));
+    gp = gpart;
     XHC_STEP("flash_post_gram", launch_post_gram(d->state_dtype, F, d->T, d->S, d->C, Kq, d->kappa, conv_w, gpart, s));
-    XHC_STEP("flash_post_coef", launch_post_coef(gpart, gram_chunks(d->C, d->S, Kq, d->kappa), d->T, d->k, Kq,
-                                                 d->gram_schmidt, p, Hpost, wb, s));
   }
   XHC_STEP("flash_post_apply", launch_post_apply(d->state_dtype, X, F, d->T, d->S, d->N, d->C, d->k, Kq, d->kappa,
-                                                 conv_w, idx, p, Hres, Hpost, wb, last ? nullptr : Hpre_next,
+                                                 conv_w, idx, p, Hres, Hpost, gp,
+                                                 gram_chunks(d->C, d->S, Kq, d->kappa), d->gram_schmidt, wb,
+                                                 last ? nullptr : Hpre_next,
                                                  last ? nullptr : base_next, last ? nullptr : input_next, Xact_save,
                                                  s));
   if (!last) {

@@ -107,13 +107,16 @@ __host__ __device__ inline int64_t post_chunks(int C) { return ((int64_t)C / 8 +
 int64_t gram_chunks(int C, int64_t S, int Kr, const int32_t* kappa);
 hipError_t launch_post_gram(int state_dtype, const void* F, int64_t T, int64_t S, int C, int Kr,
                             const int32_t* kappa, const float* conv_w, float* gpart, hipStream_t s);
-hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k, int Kr, int gram_schmidt,
-                            const float* p, const float* Hpost, float* wb, hipStream_t s);
+// The write-back of the k active rows.  For K_r > 1 gpart holds the Gram
+// partials of launch_post_gram (nchunk chunks): the write-back weights are then
+// formed from them (Gram-Schmidt, p, H^post) inside the run-based kernel, or
+// into the workspace wb by a per-token pass before the generic one.  K_r = 1:
+// gpart and wb are null.
 hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T, int64_t S, int N, int C,
                              int k, int Kr, const int32_t* kappa, const float* conv_w, const int32_t* idx,
-                             const float* p, const float* Hres, const float* Hpost, const float* wb,
-                             const float* Hpre_next, const void* base_next, void* input_next, void* Xact_save,
-                             hipStream_t s);
+                             const float* p, const float* Hres, const float* Hpost, const float* gpart,
+                             int64_t nchunk, int gram_schmidt, float* wb, const float* Hpre_next,
+                             const void* base_next, void* input_next, void* Xact_save, hipStream_t s);
 
 // ---- backward
 hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const void* Xact, const void* F,

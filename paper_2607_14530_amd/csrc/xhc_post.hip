@@ -58,6 +58,55 @@ __global__ __launch_bounds__(256) void k_post_gram(const TS* __restrict__ F, int
 }
 
 
+// Per token: G = sum over chunks; v_r = sum_b V[r][b] e_b (Gram-Schmidt, eq:gs);
+// wb[j][b] = p_j sum_r H^post[j][r] V[r][b]  (p gates only the write-back term).
+// out[j * Kr + b] receives token t's weights.
+__device__ __forceinline__ void post_coef_token(const float* __restrict__ gpart, int64_t nchunk, int64_t T, int64_t t,
+                                                int k, int Kr, int gram_schmidt, const float* __restrict__ p,
+                                                const float* __restrict__ Hpost, float* __restrict__ out) {
+  const int NP = Kr * (Kr + 1) / 2;
+  double G[kMaxKr][kMaxKr];
+  int pi = 0;
+#pragma unroll
+  for (int a = 0; a < kMaxKr; ++a)
+#pragma unroll
+    for (int b = a; b < kMaxKr; ++b) {
+      if (a < Kr && b < Kr) {
+        float s = 0.f;
+        for (int64_t c = 0; c < nchunk; ++c) s += gpart[(c * NP + pi) * T + t];
+        G[a][b] = G[b][a] = s;
+        ++pi;
+      } else {
+        G[a][b] = G[b][a] = 0.0;
+      }
+    }
+  double V[kMaxKr][kMaxKr];
+  if (gram_schmidt) {
+    gram_schmidt_basis(G, Kr, V);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kMaxKr; ++i)
+#pragma unroll
+      for (int b = 0; b < kMaxKr; ++b) V[i][b] = (i == b) ? 1.0 : 0.0;
+  }
+  for (int j = 0; j < k; ++j) {
+    const double pj = p[t * k + j];
+    for (int b = 0; b < Kr; ++b) {
+      double s = 0.0;
+      for (int r = 0; r < Kr; ++r) s += (double)Hpost[(t * k + j) * Kr + r] * V[r][b];
+      out[j * Kr + b] = (float)(pj * s);
+    }
+  }
+}
+
+__global__ __launch_bounds__(128) void k_post_coef(const float* __restrict__ gpart, int64_t nchunk, int64_t T,
+                                                   int k, int Kr, int gram_schmidt, const float* __restrict__ p,
+                                                   const float* __restrict__ Hpost, float* __restrict__ wb) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  post_coef_token(gpart, nchunk, T, t, k, Kr, gram_schmidt, p, Hpost, wb + t * k * Kr);
+}
+
 // ------------------------------------------------------------------ run-based MLP-type kernels
 // For compile-time kernel sizes (K1, K2, K3) = (4, 8, 12): a thread owns 4
 // channels and walks a run of kRun consecutive tokens in groups of G, keeping
@@ -168,15 +217,17 @@ __global__ __launch_bounds__(256) void k_post_gram_run(const TS* __restrict__ F,
 // Write-back Y_j = sum_l H^res_jl a_l + sum_b wb_jb e_b for the KK active rows
 // (without H^res: Y_j = a_j + ...); SAVE keeps the rows read, NEXT forms the
 // next sublayer's input.  The run's indices and coefficients are staged in LDS
-// once; the loads of a group of G tokens are issued together.  T is a
-// multiple of G.
+// once, the write-back weights wb formed there from the Gram partials; the
+// loads of a group of G tokens are issued together.  T is a multiple of G.
 template <typename TS, int KK, int G, bool RES, bool SAVE, bool NEXT>
 __global__ __launch_bounds__(256) void k_post_apply_run(TS* __restrict__ X, const TS* __restrict__ F, int64_t T,
                                                         int64_t S, int N, int C,
                                                         const float* __restrict__ conv_w,
                                                         const int32_t* __restrict__ idx,
                                                         const float* __restrict__ Hres,
-                                                        const float* __restrict__ wb,
+                                                        const float* __restrict__ gpart, int64_t nchunk,
+                                                        int gram_schmidt, const float* __restrict__ p,
+                                                        const float* __restrict__ Hpost,
                                                         const float* __restrict__ Hpre_next,
                                                         const TS* __restrict__ base_next, TS* __restrict__ input_next,
                                                         TS* __restrict__ Xact_save) {
@@ -191,7 +242,10 @@ __global__ __launch_bounds__(256) void k_post_apply_run(TS* __restrict__ X, cons
   const int64_t t0 = (int64_t)blockIdx.x * kRun;
   const int nt = (int)((T - t0 < kRun) ? T - t0 : kRun);
   for (int i = threadIdx.x; i < nt * KK; i += blockDim.x) s_idx[i] = idx[t0 * KK + i];
-  for (int i = threadIdx.x; i < nt * KK * KR; i += blockDim.x) s_wb[i] = wb[t0 * KK * KR + i];
+  // write-back weights of the run's tokens from their Gram partials (the same
+  // per-token arithmetic as k_post_coef; every channel chunk of a run forms them)
+  for (int u = threadIdx.x; u < nt; u += blockDim.x)
+    post_coef_token(gpart, nchunk, T, t0 + u, KK, KR, gram_schmidt, p, Hpost, s_wb + u * KK * KR);
   if (RES)
     for (int i = threadIdx.x; i < nt * KK * KK; i += blockDim.x) s_hr[i] = Hres[t0 * KK * KK + i];
   if (NEXT)
@@ -311,49 +365,7 @@ hipError_t launch_post_gram(int state_dtype, const void* F, int64_t T, int64_t S
   return hipGetLastError();
 }
 
-// Per token: G = sum over chunks; v_r = sum_b V[r][b] e_b (Gram-Schmidt, eq:gs);
-// wb[j][b] = p_j sum_r H^post[j][r] V[r][b]  (p gates only the write-back term).
-__global__ __launch_bounds__(128) void k_post_coef(const float* __restrict__ gpart, int64_t nchunk, int64_t T,
-                                                   int k, int Kr, int gram_schmidt, const float* __restrict__ p,
-                                                   const float* __restrict__ Hpost, float* __restrict__ wb) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= T) return;
-  const int NP = Kr * (Kr + 1) / 2;
-  double G[kMaxKr][kMaxKr];
-  int pi = 0;
-#pragma unroll
-  for (int a = 0; a < kMaxKr; ++a)
-#pragma unroll
-    for (int b = a; b < kMaxKr; ++b) {
-      if (a < Kr && b < Kr) {
-        float s = 0.f;
-        for (int64_t c = 0; c < nchunk; ++c) s += gpart[(c * NP + pi) * T + t];
-        G[a][b] = G[b][a] = s;
-        ++pi;
-      } else {
-        G[a][b] = G[b][a] = 0.0;
-      }
-    }
-  double V[kMaxKr][kMaxKr];
-  if (gram_schmidt) {
-    gram_schmidt_basis(G, Kr, V);
-  } else {
-#pragma unroll
-    for (int i = 0; i < kMaxKr; ++i)
-#pragma unroll
-      for (int b = 0; b < kMaxKr; ++b) V[i][b] = (i == b) ? 1.0 : 0.0;
-  }
-  for (int j = 0; j < k; ++j) {
-    const double pj = p[t * k + j];
-    for (int b = 0; b < Kr; ++b) {
-      double s = 0.0;
-      for (int r = 0; r < Kr; ++r) s += (double)Hpost[(t * k + j) * Kr + r] * V[r][b];
-      wb[(t * k + j) * Kr + b] = (float)(pj * s);
-    }
-  }
-}
-
-hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k, int Kr, int gram_schmidt,
+static hipError_t launch_post_coef(const float* gpart, int64_t nchunk, int64_t T, int k, int Kr, int gram_schmidt,
                             const float* p, const float* Hpost, float* wb, hipStream_t s) {
   if (T == 0) return hipSuccess;
   k_post_coef<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(gpart, nchunk, T, k, Kr, gram_schmidt, p,
@@ -435,16 +447,18 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
 
 hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T, int64_t S, int N, int C, int k,
                              int Kr, const int32_t* kappa, const float* conv_w, const int32_t* idx, const float* p,
-                             const float* Hres, const float* Hpost, const float* wb, const float* Hpre_next,
-                             const void* base_next, void* input_next, void* Xact_save, hipStream_t s) {
+                             const float* Hres, const float* Hpost, const float* gpart, int64_t nchunk,
+                             int gram_schmidt, float* wb, const float* Hpre_next, const void* base_next,
+                             void* input_next, void* Xact_save, hipStream_t s) {
   if (T == 0) return hipSuccess;
-  if (wb && run_ok(C, S, Kr, kappa) && T % 4 == 0 && (k == 4 || k == 8) &&
+  if (gpart && run_ok(C, S, Kr, kappa) && T % 4 == 0 && (k == 4 || k == 8) &&
       !(Hres && input_next) && !(Xact_save && (input_next || !Hres))) {
     const int nthr = run_threads(C);
     const dim3 grid((unsigned)((T + kRun - 1) / kRun), (unsigned)(C / (nthr * 4)));
 #define XHC_APPLY_RUN(TS, KK, G, RES, SAVE, NEXT)                                                                  \
   k_post_apply_run<TS, KK, G, RES, SAVE, NEXT><<<grid, dim3(nthr), 0, s>>>(                                      \
-      reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(F), T, S, N, C, conv_w, idx, Hres, wb, Hpre_next,    \
+      reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(F), T, S, N, C, conv_w, idx, Hres, gpart, nchunk,    \
+      gram_schmidt, p, Hpost, Hpre_next,                                                                         \
       reinterpret_cast<const TS*>(base_next), reinterpret_cast<TS*>(input_next), reinterpret_cast<TS*>(Xact_save))
 #define XHC_APPLY_MODES(TS, KK, G)                                              \
   do {                                                                          \
@@ -460,6 +474,10 @@ hipError_t launch_post_apply(int state_dtype, void* X, const void* F, int64_t T,
 #undef XHC_APPLY_MODES
 #undef XHC_APPLY_RUN
     return hipGetLastError();
+  }
+  if (gpart) {
+    const hipError_t e = launch_post_coef(gpart, nchunk, T, k, Kr, gram_schmidt, p, Hpost, wb, s);
+    if (e != hipSuccess) return e;
   }
   const dim3 grid((unsigned)(T * post_chunks(C)));
 #define XHC_APPLY(TS, KR)                                                                                       \
