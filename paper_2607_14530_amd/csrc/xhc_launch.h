@@ -47,7 +47,10 @@ struct ProjPlan {
   int64_t chunk_blocks;
   int64_t nchunk;
 };
-constexpr int kWideTokens = 256;
+// token groups of 16 per wave of the wide path: four, or two for five and more
+// output blocks (their accumulators would otherwise leave one wave per SIMD)
+__host__ __device__ constexpr int wide_tg(int nob) { return nob >= 5 ? 2 : 4; }
+__host__ __device__ constexpr int wide_tokens(int nob) { return 64 * wide_tg(nob); }   // per workgroup
 constexpr int kWideStep = 4;   // k-blocks per step of the wide path
 // steps whose weight fragments (kWideStep x nob KiB each) share one 64 KiB LDS fill
 __host__ __device__ constexpr int wide_seg_steps(int nob) { return nob <= 2 ? 8 : (nob <= 4 ? 4 : 2); }
@@ -56,7 +59,8 @@ inline ProjPlan proj_plan(int state_dtype, bool gather, int64_t K, int C, int64_
   const bool wide = (gather ? act_grouped(state_dtype, C) : full_grouped(state_dtype, K)) && out_blocks(nout) <= 8;
   int tg = 4;
   while (tg > 1 && ((T + 16 * tg - 1) / (16 * tg) < 128 || NO * tg > 160)) tg /= 2;
-  const int64_t tiles = wide ? (T + kWideTokens - 1) / kWideTokens : (T + 16 * tg - 1) / (16 * tg);
+  const int64_t wt = wide_tokens((int)out_blocks(nout));
+  const int64_t tiles = wide ? (T + wt - 1) / wt : (T + 16 * tg - 1) / (16 * tg);
   const int64_t gran = 32;                                      // chunk granularity in k-blocks
   int64_t want = (1024 + tiles - 1) / tiles;                    // chunks for about 1024 workgroups
   const int64_t most = (nblk + gran - 1) / gran;

@@ -136,7 +136,8 @@ __global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, 
 }
 
 // Wide path (bf16 state, full rows, grouped weight layout).  A workgroup
-// takes 256 tokens (wave w: four groups of 16, tokens 64w..64w+63) and a chunk
+// takes 64 TG tokens (wave w: TG groups of 16, TG = 4, or 2 for five or more
+// output blocks) and a chunk
 // of cb k-blocks, walked in steps of one group of 4 k-blocks (128 elements):
 // each lane loads 64 contiguous bytes of its token per step, so a wave
 // requests 256 contiguous bytes of each of its 64 token rows together.  The step's weight fragments are copied once per workgroup
@@ -147,7 +148,7 @@ template <int NOB, bool EXACT, bool GATHER>
 __global__ __launch_bounds__(256) void k_proj_wide(const uint16_t* __restrict__ X, int64_t T, int N, int C, int64_t K,
                                                    int64_t cb, const uint4* __restrict__ wpk,
                                                    const int32_t* __restrict__ idx, int k, float* __restrict__ part) {
-  constexpr int TG = 4, KS = kWideStep, NOr = NOB * 16 + 2;
+  constexpr int TG = wide_tg(NOB), KS = kWideStep, NOr = NOB * 16 + 2;
   constexpr int SS = wide_seg_steps(NOB);   // steps whose fragments share one LDS fill
   extern __shared__ uint4 wl[];             // [SS][KS][NOB][64 lanes]; dynamic, as the LDS copy needs it
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -159,7 +160,7 @@ __global__ __launch_bounds__(256) void k_proj_wide(const uint16_t* __restrict__ 
   int32_t rows[GATHER ? TG : 1][kMaxK];
 #pragma unroll
   for (int g = 0; g < TG; ++g) {
-    tok[g] = tile * kWideTokens + wave * 64 + g * 16 + tl;
+    tok[g] = tile * wide_tokens(NOB) + wave * (16 * TG) + g * 16 + tl;
     const int64_t tc = tok[g] < T ? tok[g] : T - 1;   // loads stay in bounds; results of t >= T are dropped
     if (GATHER) {
       xr[g] = X + tc * N * (int64_t)C + grp * 32;
@@ -303,7 +304,7 @@ static hipError_t proj_wide_launch(const uint16_t* X, int64_t T, int N, int C, i
                                    const uint4* w, int nob, const int32_t* idx, int k, float* part, hipStream_t s) {
   // (the unguarded instance for chunks that divide K needs more registers
   // than two waves per SIMD allow, so the guarded one serves both)
-  const dim3 grid((unsigned)((T + kWideTokens - 1) / kWideTokens), (unsigned)pl.nchunk);
+  const dim3 grid((unsigned)((T + wide_tokens(nob) - 1) / wide_tokens(nob)), (unsigned)pl.nchunk);
   const size_t lds = (size_t)wide_seg_steps(nob) * kWideStep * nob * 1024;
 #define XHC_WIDE_CASE(NB)                                                                                      \
   case NB:                                                                                                     \
