@@ -173,7 +173,8 @@ def _time(fn, iters, stream):
     return e0.elapsed_time(e1) / iters
 
 
-SECTIONS = ("flash_q4", "flash_q2", "mhc_n4", "prefill_t2048", "bwd_mlp_sweep", "bwd_mlp_n16", "flash_bwd_q4")
+SECTIONS = ("flash_q4", "flash_q2", "mhc_n4", "config2_c1024", "prefill_t2048", "bwd_mlp_sweep", "bwd_mlp_n16",
+            "flash_bwd_q4")
 
 
 def extra_sections(dev, stream, iters=5, only=None):
@@ -216,6 +217,26 @@ def extra_sections(dev, stream, iters=5, only=None):
                          "achieved_GBps": b * w.T / (ms * 1e-3) / 1e9, "bytes_per_token_C": b / unit(w.C),
                          "paper_bytes_per_token_C": 34.0}
         del sub, inp, st
+        torch.cuda.empty_cache()
+    if want("config2_c1024"):
+        # xHC sparse at C = 1024: T = 4096 (one sequence), N = 16, k = 4, an
+        # attention-type and an MLP-type sublayer (forward), single-pass pre
+        # with teams of 8 workgroups
+        wa, wm = synth.sparse_c1024(1), synth.sparse_c1024(4)
+        ia, im = synth.sublayer_inputs(wa, 21, device=dev), synth.sublayer_inputs(wm, 22, device=dev)
+        sa = X.Sublayer(X.dims_for(wa), ia, dev)
+        sm = X.Sublayer(X.dims_for(wm), im, dev)
+        st = ia["X"]
+        ms = _time(lambda: (sa.pre(st, stream), sa.post(st, ia["F"], stream),
+                            sm.pre(st, stream), sm.post(st, im["F"], stream)), 20, stream)
+        pre_ms = _time(lambda: sa.pre(st, stream), 20, stream)
+        b = A.algorithmic_bytes_sublayer(wa.N, wa.k, wa.C, 1) + A.algorithmic_bytes_sublayer(wm.N, wm.k, wm.C, 4)
+        out["config2_c1024"] = {"workload": "xHC forward block (attention-type + MLP-type sublayer), T=4096, N=16, "
+                                            "k=4, m=2, C=1024",
+                                "ms_per_block": ms, "tokens_per_s": 2 * wa.T / (ms * 1e-3),
+                                "achieved_GBps": b * wa.T / (ms * 1e-3) / 1e9,
+                                "bytes_per_token_C": b / 2 / unit(wa.C), "ms_xhc_pre": pre_ms}
+        del sa, sm, ia, im, st
         torch.cuda.empty_cache()
     if want("prefill_t2048"):
         # prefill-latency regime: one 2048-token sequence through an attention-type
