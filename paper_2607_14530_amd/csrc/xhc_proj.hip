@@ -5,6 +5,8 @@
 
 namespace xhc {
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 // ----------------------------------------------------------------- projection
 // One workgroup = 4 waves = TG token groups of 16 x one chunk of cb 32-row
 // blocks of K; wave w takes blocks w, w + 4, ... of the chunk for all TG
@@ -140,35 +142,49 @@ __global__ __launch_bounds__(256) void k_proj_partial(const TS* __restrict__ X, 
 // output blocks) and a chunk
 // of cb k-blocks, walked in steps of one group of 4 k-blocks (128 elements):
 // each lane loads 64 contiguous bytes of its token per step, so a wave
-// requests 256 contiguous bytes of each of its 64 token rows together.  The step's weight fragments are copied once per workgroup
-// into LDS (double-buffered, straight from global memory) and serve the 16
-// token groups of the four waves.  Each wave owns its tokens, so partials go
-// out without a cross-wave reduction.  EXACT: cb divides the k-blocks.
+// requests 256 contiguous bytes of each of its 64 token rows together.  The
+// weight fragments of SS steps (a segment) are copied once per workgroup into
+// LDS, straight from global memory, and serve the token groups of the four
+// waves.  Two LDS buffers alternate: the copy of segment g + 1 is issued when
+// segment g starts and has landed by its end, so the only wait per segment
+// is one LDS barrier.  Each wave owns its tokens, so partials go out without a
+// cross-wave reduction.  EXACT: cb divides the k-blocks.
 template <int NOB, bool EXACT, bool GATHER>
 __global__ __launch_bounds__(256) void k_proj_wide(const uint16_t* __restrict__ X, int64_t T, int N, int C, int64_t K,
                                                    int64_t cb, const uint4* __restrict__ wpk,
                                                    const int32_t* __restrict__ idx, int k, float* __restrict__ part) {
   constexpr int TG = wide_tg(NOB), KS = kWideStep, NOr = NOB * 16 + 2;
   constexpr int SS = wide_seg_steps(NOB);   // steps whose fragments share one LDS fill
-  extern __shared__ uint4 wl[];             // [SS][KS][NOB][64 lanes]; dynamic, as the LDS copy needs it
+  constexpr int FILL = SS * KS * NOB;       // fragments per segment
+  static_assert(FILL % 4 == 0, "every wave copies the same number of fragments");
+  extern __shared__ uint4 wl[];             // [2][SS][KS][NOB][64 lanes]; dynamic, as the LDS copy needs it
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int tl = lane % 16, grp = lane / 16;
   const int64_t tile = blockIdx.x, chunk = blockIdx.y;
   const int64_t nblk = K / 32, kb0 = chunk * cb;
   const uint16_t* xr[TG];   // the token's state (GATHER: its first row)
   int64_t tok[TG];
-  int32_t rows[GATHER ? TG : 1][kMaxK];
+  // GATHER: the routed rows of the wave's tokens, read per step from LDS (a
+  // private array indexed by the step's row would live in scratch memory)
+  __shared__ int32_t s_rows[GATHER ? 4 : 1][GATHER ? TG : 1][16][kMaxK];
 #pragma unroll
   for (int g = 0; g < TG; ++g) {
     tok[g] = tile * wide_tokens(NOB) + wave * (16 * TG) + g * 16 + tl;
     const int64_t tc = tok[g] < T ? tok[g] : T - 1;   // loads stay in bounds; results of t >= T are dropped
     if (GATHER) {
       xr[g] = X + tc * N * (int64_t)C + grp * 32;
+      if (grp == 0)
 #pragma unroll
-      for (int j = 0; j < kMaxK; ++j) rows[g][j] = j < k ? idx[tc * k + j] : 0;
+        for (int j = 0; j < kMaxK; ++j) s_rows[wave][g][tl][j] = j < k ? idx[tc * k + j] : 0;
     } else {
       xr[g] = X + tc * K + grp * 32;
     }
+  }
+  if (GATHER) {
+    // the rows are read by all lanes of the wave that wrote them: LDS
+    // accesses of a wave complete in order once issued in this order
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
   }
   f32x4 acc[TG][NOB];
   float s1[TG], s2[TG];
@@ -191,13 +207,7 @@ __global__ __launch_bounds__(256) void k_proj_wide(const uint16_t* __restrict__ 
 #pragma unroll
     for (int g = 0; g < TG; ++g) {
       const uint16_t* p = xr[g] + c;
-      if (GATHER) {
-        int r = rows[g][0];
-#pragma unroll
-        for (int jj = 1; jj < kMaxK; ++jj)
-          if (jj == j) r = rows[g][jj];
-        p += (int64_t)r * C;
-      }
+      if (GATHER) p += (int64_t)s_rows[wave][g][tl][j] * C;
 #pragma unroll
       for (int u = 0; u < KS; ++u) {
         b.x[u][g] = make_uint4(0, 0, 0, 0);
@@ -228,34 +238,58 @@ __global__ __launch_bounds__(256) void k_proj_wide(const uint16_t* __restrict__ 
     }
   };
   const int64_t nsteps = cb / KS;
-  for (int64_t s0 = 0; s0 < nsteps; s0 += SS) {
-    // fragments of steps s0 .. s0+SS-1 -> LDS, one 1 KiB fragment per wave
-    // instruction; the barrier first lets every wave finish the previous fill
-    __syncthreads();
-    for (int fi = wave; fi < SS * KS * NOB; fi += 4) {
-      const int64_t kb = kb0 + s0 * KS + fi / NOB;
-      if (EXACT || kb < nblk)
-        __builtin_amdgcn_global_load_lds(wpk + (kb * NOB + fi % NOB) * kWave + lane, wl + fi * kWave, 16, 0, 0);
+  const uint32_t wl_base = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) uint4*)wl;
+  // fragments of segment g -> LDS buffer g % 2, one 1 KiB fragment per wave
+  // instruction (a block past the end of K copies the last block; unused)
+  auto fill = [&](int64_t g) {
+    for (int fi = wave; fi < FILL; fi += 4) {
+      int64_t kb = kb0 + g * SS * KS + fi / NOB;
+      if (!EXACT && kb >= nblk) kb = nblk - 1;
+      lds_dma16(wpk + (kb * NOB + fi % NOB) * kWave + lane,
+                __builtin_amdgcn_readfirstlane(wl_base + (uint32_t)(((g & 1) * FILL + fi) * kWave * 16)));
     }
-    Step A, B;
-    load(A, kb0 + s0 * KS);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    // within the fill, the state loads of step s + 1 are in flight while step s is computed
+  };
+  Step A, B;
+  fill(0);
+  load(A, kb0);
+  __builtin_amdgcn_s_waitcnt(0);
+  lds_barrier();
+  // step s: the next segment's copy goes out at a segment start and the state
+  // loads of step s + 1 right after it; both are in flight while step s is
+  // computed.  Each step starts with a full wait: then only its own state
+  // (and, at a segment's second step, the copy issued one step earlier) is
+  // outstanding, so with two or more steps per segment the copy has landed
+  // long before the barrier that ends the segment (with one, that barrier
+  // waits for it).  The barrier also frees the buffer just read.
+  auto step = [&](int64_t s, Step& cur, Step& nxt) __attribute__((always_inline)) {
+    const int64_t g = s / SS;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // the empty asm pins the compiler's own wait for this step's state here,
+    // before the copy and the next loads below (it does not count the copy)
+#pragma unroll
+    for (int u = 0; u < KS; ++u)
+#pragma unroll
+      for (int gg = 0; gg < TG; ++gg) {
+        u32x4 t = {cur.x[u][gg].x, cur.x[u][gg].y, cur.x[u][gg].z, cur.x[u][gg].w};
+        asm volatile("" : "+v"(t));
+        cur.x[u][gg] = make_uint4(t[0], t[1], t[2], t[3]);
+      }
+    if (s % SS == 0 && (g + 1) * SS < nsteps) fill(g + 1);
+    if (s + 1 < nsteps) load(nxt, kb0 + (s + 1) * KS);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(cur, kb0 + s * KS, (int)((g & 1) * SS + s % SS));
+    __builtin_amdgcn_sched_barrier(0);
+    if ((s + 1) % SS == 0 && s + 1 < nsteps) {
+      if (SS == 1) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      lds_barrier();
+    }
+  };
+  // (the scheduling barriers keep each phase's loads from being hoisted into
+  // the previous one, which would need a third register buffer)
 #pragma nounroll
-    for (int sj = 0; sj < SS; sj += 2) {
-      // (the scheduling barriers keep each phase's loads from being hoisted
-      // into the previous one, which would need a third register buffer)
-      const int64_t ka = kb0 + (s0 + sj) * KS;
-      load(B, ka + KS);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(A, ka, sj);
-      __builtin_amdgcn_sched_barrier(0);
-      if (sj + 2 < SS) load(A, ka + 2 * KS);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(B, ka + KS, sj + 1);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+  for (int64_t s = 0; s < nsteps; s += 2) {
+    step(s, A, B);
+    step(s + 1, B, A);
   }
 #pragma unroll
   for (int g = 0; g < TG; ++g) {
@@ -299,13 +333,41 @@ static hipError_t proj_launch(const TS* X, int64_t T, int N, int C, int64_t K, c
 }
 
 
+// dynamic LDS of the wide path: two segment buffers
+static inline size_t wide_lds_bytes(int nob) { return (size_t)2 * wide_seg_steps(nob) * kWideStep * nob * 1024; }
+
+// every instance may use its LDS size (above 64 KiB for five or more output
+// blocks); set once per device and thread
+template <bool GATHER>
+static bool wide_attrs_set() {
+  static thread_local int dev_done = -1;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (dev == dev_done) return true;
+  const void* fs[8] = {reinterpret_cast<const void*>(&k_proj_wide<1, false, GATHER>),
+                       reinterpret_cast<const void*>(&k_proj_wide<2, false, GATHER>),
+                       reinterpret_cast<const void*>(&k_proj_wide<3, false, GATHER>),
+                       reinterpret_cast<const void*>(&k_proj_wide<4, false, GATHER>),
+                       reinterpret_cast<const void*>(&k_proj_wide<5, false, GATHER>),
+                       reinterpret_cast<const void*>(&k_proj_wide<6, false, GATHER>),
+                       reinterpret_cast<const void*>(&k_proj_wide<7, false, GATHER>),
+                       reinterpret_cast<const void*>(&k_proj_wide<8, false, GATHER>)};
+  for (int nb = 1; nb <= 8; ++nb)
+    if (hipFuncSetAttribute(fs[nb - 1], hipFuncAttributeMaxDynamicSharedMemorySize, (int)wide_lds_bytes(nb)) !=
+        hipSuccess)
+      return false;
+  dev_done = dev;
+  return true;
+}
+
 template <bool GATHER>
 static hipError_t proj_wide_launch(const uint16_t* X, int64_t T, int N, int C, int64_t K, const ProjPlan& pl,
                                    const uint4* w, int nob, const int32_t* idx, int k, float* part, hipStream_t s) {
   // (the unguarded instance for chunks that divide K needs more registers
   // than two waves per SIMD allow, so the guarded one serves both)
   const dim3 grid((unsigned)((T + wide_tokens(nob) - 1) / wide_tokens(nob)), (unsigned)pl.nchunk);
-  const size_t lds = (size_t)wide_seg_steps(nob) * kWideStep * nob * 1024;
+  const size_t lds = wide_lds_bytes(nob);
+  if (!wide_attrs_set<GATHER>()) return hipErrorInvalidConfiguration;
 #define XHC_WIDE_CASE(NB)                                                                                      \
   case NB:                                                                                                     \
     k_proj_wide<NB, false, GATHER><<<grid, dim3(256), lds, s>>>(X, T, N, C, K, pl.chunk_blocks, w, idx, k, part); \
