@@ -1504,16 +1504,18 @@ __device__ __forceinline__ void st4(uint16_t* p, const float (&d)[4]) {
 // Active rows of a routed bf16 state (k * Kr + k * k <= 32 outputs, bf16
 // gradient rows updated in place at the routed rows): 128 weight rows (128
 // channels of one slot) per workgroup of 512 threads.  The inputs of step
-// tb + 32 are fetched into registers while step tb is computed: this thread's
+// tb + 64 are fetched into registers while step tb is computed: this thread's
 // pieces of the packed dz', one per-token scalar and 16 bytes of the state
 // rows, and its gradient elements.  Every load is issued without a branch (a
 // token past the chunk reads the chunk's last token; its dz' row and state row
 // are zeroed where they are staged, its gradient row is not stored) and the
 // barriers wait for LDS traffic only, so a step waits for nothing but its own
 // prefetched loads.  The routed row of each token is loaded one step earlier
-// still (rid), so the state and gradient loads do not wait on it.
+// still (rid), so the state and gradient loads do not wait on it.  A gradient
+// row is read two steps before its token's step writes it, and no step in
+// between writes that token.
 constexpr int kActRows = 2 * kMfRows;   // weight rows per workgroup
-__global__ __launch_bounds__(4 * kActRows) void k_bwd_act_rows_mfma(const uint16_t* __restrict__ X,
+__global__ __launch_bounds__(4 * kActRows) __attribute__((amdgpu_waves_per_eu(4))) void k_bwd_act_rows_mfma(const uint16_t* __restrict__ X,
                                                                 uint16_t* __restrict__ dX,
                                                                 const float* __restrict__ W_post,
                                                                 const float* __restrict__ W_res,
@@ -1595,8 +1597,8 @@ __global__ __launch_bounds__(4 * kActRows) void k_bwd_act_rows_mfma(const uint16
     }
     st.x = *reinterpret_cast<const uint4*>(X + (tok_at(tb, threadIdx.x / PIECES) * N + rid[0]) * (int64_t)C + c0 +
                                            (threadIdx.x % PIECES) * 8);
-    // the gradient rows of the step (other tokens than the step being
-    // computed, so reading them a step ahead is safe)
+    // the gradient rows of the step (other tokens than the steps being
+    // computed before it, so reading them two steps ahead is safe)
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int64_t t = tok_at(tb, 16 * h + l16);
@@ -1633,8 +1635,8 @@ __global__ __launch_bounds__(4 * kActRows) void k_bwd_act_rows_mfma(const uint16
     const int rowd[2] = {cur.rowd[0], cur.rowd[1]};
     const uint2 dxr[2] = {cur.dx[0], cur.dx[1]};
     lds_barrier();
-    fetch(cur, tb + kMfStep);
-    fetch_rows(tb + 2 * kMfStep);
+    fetch(cur, tb + 2 * kMfStep);
+    fetch_rows(tb + 3 * kMfStep);
     // ---- dX: two token halves; the gradient rows were read a step ahead
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
@@ -1672,16 +1674,29 @@ __global__ __launch_bounds__(4 * kActRows) void k_bwd_act_rows_mfma(const uint16
     }
   };
   if (t0 < t1) {
-    Stage cur;
+    // two stages alternate, so the inputs of a step are fetched two steps
+    // before it is computed (a step's own arithmetic is short)
+    Stage sa, sb;
     fetch_rows(t0);
-    fetch(cur, t0);
+    fetch(sa, t0);
     fetch_rows(t0 + kMfStep);
+    fetch(sb, t0 + kMfStep);
+    fetch_rows(t0 + 2 * kMfStep);
     // the loop is entered with no load in flight, so the compiler's wait
     // counts inside it follow the loop's own order of loads and stores
     __builtin_amdgcn_s_waitcnt(0);
     int64_t tb = t0;
-    for (; tb + kMfStep <= t1; tb += kMfStep) step(std::true_type{}, cur, tb);
-    if (tb < t1) step(std::false_type{}, cur, tb);
+    for (; tb + 2 * kMfStep <= t1; tb += 2 * kMfStep) {
+      step(std::true_type{}, sa, tb);
+      step(std::true_type{}, sb, tb + kMfStep);
+    }
+    if (tb + kMfStep <= t1) {
+      step(std::true_type{}, sa, tb);
+      tb += kMfStep;
+      if (tb < t1) step(std::false_type{}, sb, tb);
+    } else if (tb < t1) {
+      step(std::false_type{}, sa, tb);
+    }
   }
   // lane holds dW[row K0 + 16 wave + l16][output 16 oh + 4 g4 + v]
   float* dst = wpa + ((int64_t)blockIdx.y * NK + K0 + 16 * wave + l16) * 32;
