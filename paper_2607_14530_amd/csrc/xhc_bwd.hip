@@ -687,9 +687,20 @@ template <typename TS>
 __device__ __forceinline__ float ld_scalar(const TS* p);
 template <> __device__ __forceinline__ float ld_scalar<uint16_t>(const uint16_t* p) { return __uint_as_float((uint32_t)*p << 16); }
 template <> __device__ __forceinline__ float ld_scalar<float>(const float* p) { return *p; }
+// an element's bits as loaded (bf16 zero-extended), converted where it is used:
+// a conversion next to the load would make the compiler wait for it there
+template <typename TS>
+__device__ __forceinline__ uint32_t ld_raw(const TS* p);
+template <> __device__ __forceinline__ uint32_t ld_raw<uint16_t>(const uint16_t* p) { return *p; }
+template <> __device__ __forceinline__ uint32_t ld_raw<float>(const float* p) { return __float_as_uint(*p); }
+template <typename TS>
+__device__ __forceinline__ float from_raw(uint32_t r);
+template <> __device__ __forceinline__ float from_raw<uint16_t>(uint32_t r) { return __uint_as_float(r << 16); }
+template <> __device__ __forceinline__ float from_raw<float>(uint32_t r) { return __uint_as_float(r); }
 template <typename TS>
 __device__ __forceinline__ void st_scalar(TS* p, float v);
-template <> __device__ __forceinline__ void st_scalar<uint16_t>(uint16_t* p, float v) { *p = (uint16_t)f2bf(v); }
+// (the hardware conversion: the bits of f2bf except the payload of a NaN)
+template <> __device__ __forceinline__ void st_scalar<uint16_t>(uint16_t* p, float v) { *p = (uint16_t)pack2bf(v, 0.f); }
 template <> __device__ __forceinline__ void st_scalar<float>(float* p, float v) { *p = v; }
 
 template <typename TS>
@@ -813,8 +824,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
                                                       float* __restrict__ lb) {
   constexpr int KM = 4, NCF = 4 * kMaxK + 16;   // slots; coefficients a token
   // the run's per-token values, staged once: element offsets of the slot rows
-  // in the state, H^res, the component-gradient coefficients
-  __shared__ int64_t s_row[kConvRun][KM];
+  // from the run's first state row (32-bit: the launcher keeps kConvRun N C
+  // below 2^31), H^res, the component-gradient coefficients
+  __shared__ int32_t s_row[kConvRun][KM];
   __shared__ float s_hr[kConvRun][KM * KM];
   __shared__ float s_cf[kConvRun][NCF];
   const int c = blockIdx.x * 256 + threadIdx.x;   // C % 256 == 0: every thread has a channel
@@ -826,7 +838,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   for (int i = threadIdx.x; i < nt * KM; i += 256) {
     const int64_t u = t0 + i / KM;
     const int j = i % KM < k ? i % KM : k - 1;   // unused slots repeat the last one (in bounds)
-    s_row[i / KM][i % KM] = (u * N + idx[u * k + j]) * (int64_t)C;
+    s_row[i / KM][i % KM] = (int32_t)(((u - t0) * N + idx[u * k + j]) * (int64_t)C);
   }
   for (int i = threadIdx.x; i < nt * KM * KM; i += 256) {
     const int64_t u = t0 + i / (KM * KM);
@@ -841,11 +853,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   float fw[12], acc[kConvRows], P[12];
   int64_t seq0 = t0 - t0 % S;   // start of the current sequence
   // fw[i] = F[u - i] (zero before the sequence start); before the first token
-  // it holds F[t0 - 1 - i] at index i
+  // it holds F[t0 - 1 - i] at index i.  The 11 loads are issued together (a
+  // token before the sequence start reads the run's first token instead and
+  // is zeroed), so the run start waits for one round trip, not eleven.
 #pragma unroll
   for (int i = 0; i < 12; ++i) {
     const int64_t t = t0 - 1 - i;
-    fw[i] = (i < 11 && t >= seq0) ? ld_scalar<TS>(F + t * C + c) : 0.f;
+    const bool in = i < 11 && t >= seq0;
+    const float v = ld_scalar<TS>(F + (in ? t : t0) * C + c);
+    fw[i] = in ? v : 0.f;
     P[i] = 0.f;
   }
 #pragma unroll
@@ -854,37 +870,43 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
   if (run > 0)
 #pragma unroll
     for (int i = 0; i < 11; ++i) lbr[(int64_t)i * C] = 0.f;
+  // Per-run bases and per-token offsets that are the same in every lane
+  // (32-bit), so an access is a scalar address plus the lane's channel.
+  const uint32_t cu = (uint32_t)c;
+  const int64_t sbase = t0 * N * (int64_t)C;
+  const TG* const dXn_r = dXn + sbase;
+  TG* const dX_r = dX + sbase;
+  const TS* const Xact_r = Xact + t0 * k * (int64_t)C;
+  const TS* const F_r = F + t0 * (int64_t)C;
+  TS* const dF_r = dF + t0 * (int64_t)C;
+  auto row_at = [&](int ul, int j) { return __builtin_amdgcn_readfirstlane(s_row[ul][j]); };
   // a token's dF, complete (or this run's additions to an earlier run's token)
   auto emit = [&](int64_t v, float x) {
     if (v < seq0) return;
-    if (v >= t0) st_scalar<TS>(dF + v * C + c, x);
+    if (v >= t0) st_scalar<TS>(&(dF_r + (int32_t)(v - t0) * C)[cu], x);
     else if (v >= t0 - 11) lbr[(v - (t0 - 11)) * C] = x;
   };
-  // loads of one token: dY of the k slots, the saved rows, F.  Every load is
-  // issued (past the run or the k slots from a clamped, in-bounds address)
-  // and the unused values are replaced by zero, so the buffers stay in
-  // registers and the loads stay in flight together.
-  auto load = [&](int64_t u, float (&dy)[KM], float (&a)[KM], float& f) {
-    const bool ok = u < t1;
-    const int64_t uc = ok ? u : t1 - 1;
-    const int ul = (int)(uc - t0);
+  // loads of one token: dY of the k slots, the saved rows, F, as raw bits.
+  // Every load is issued (past the run or the k slots from a clamped,
+  // in-bounds address), so the buffers stay in registers and the loads stay
+  // in flight together; the values are converted, and those of unused slots
+  // replaced by zero, where the token is processed (tokens past the run never
+  // are).
+  auto load = [&](int64_t u, uint32_t (&dy)[KM], uint32_t (&a)[KM], uint32_t& f) {
+    const int ul = (int)((u < t1 ? u : t1 - 1) - t0);
 #pragma unroll
     for (int j = 0; j < KM; ++j) {
       const int jc = j < k ? j : k - 1;
-      const float yv = ld_scalar<TG>(dXn + s_row[ul][j] + c);
-      dy[j] = (ok && j < k) ? yv : 0.f;
-      a[j] = 0.f;
-      if (RESTORE) {
-        const float xv = ld_scalar<TS>(Xact + (uc * k + jc) * (int64_t)C + c);
-        a[j] = (ok && j < k) ? xv : 0.f;
-      }
+      dy[j] = ld_raw<TG>(&(dXn_r + row_at(ul, j))[cu]);
+      a[j] = 0u;
+      if (RESTORE) a[j] = ld_raw<TS>(&(Xact_r + (ul * k + jc) * C)[cu]);
     }
-    const float fv = ld_scalar<TS>(F + uc * C + c);
-    f = ok ? fv : 0.f;
+    f = ld_raw<TS>(&(F_r + ul * C)[cu]);
   };
-  float bdy[2][4][KM], ba[2][4][KM], bf[2][4];
+  uint32_t bdy[2][4][KM], ba[2][4][KM], bf[2][4];
 #pragma unroll
   for (int q = 0; q < 4; ++q) load(t0 + q, bdy[0][q], ba[0][q], bf[0][q]);
+  int64_t pos = t0 % S;   // position of token u in its sequence
   for (int64_t ub = t0; ub < t1; ub += 8) {
 #pragma unroll
     for (int half = 0; half < 2; ++half) {
@@ -896,7 +918,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
       for (int q = 0; q < 4; ++q) {
         const int64_t u = u4 + q;
         if (u < t1) {   // (no early exit: the loop unrolls and the buffers stay in registers)
-        if (u % S == 0 && u > t0) {
+        if (pos == 0 && u > t0) {
           // a sequence starts at u: the tokens before it are complete
 #pragma unroll
           for (int i = 0; i < 12; ++i) emit(u - 1 - i, P[i]);
@@ -908,12 +930,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
         emit(u - 12, P[11]);
 #pragma unroll
         for (int i = 11; i > 0; --i) { P[i] = P[i - 1]; fw[i] = fw[i - 1]; }
-        fw[0] = bf[cur][q];
+        fw[0] = from_raw<TS>(bf[cur][q]);
         float dy[KM], av[KM];
 #pragma unroll
         for (int j = 0; j < KM; ++j) {
-          dy[j] = bdy[cur][q][j];
-          av[j] = ba[cur][q][j];
+          dy[j] = j < k ? from_raw<TG>(bdy[cur][q][j]) : 0.f;
+          av[j] = (RESTORE && j < k) ? from_raw<TS>(ba[cur][q][j]) : 0.f;
         }
         // the components at u (eq:aug): F[u] and the three causal convolutions
         float e[4];
@@ -949,9 +971,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             float g = 0.f;
 #pragma unroll
             for (int j = 0; j < KM; ++j) g = fmaf(s_hr[ul][j * KM + l], dy[j], g);
-            const int64_t row = s_row[ul][l];
-            st_scalar<TG>(dX + row + c, g);
-            if (RESTORE) st_scalar<TS>(X + row + c, av[l]);
+            const int32_t ro = row_at(ul, l);
+            st_scalar<TG>(&(dX_r + ro)[cu], g);
+            if (RESTORE) st_scalar<TS>(&(X + sbase + ro)[cu], av[l]);
           }
         }
         P[0] = d[0];
@@ -965,6 +987,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void k
             acc[r] = fmaf(fw[i], d[j], acc[r]);
           }
         }
+        pos = pos + 1 == S ? 0 : pos + 1;
         }
       }
     }
@@ -1749,7 +1772,10 @@ static bool conv_run_ok(const xhc_dims* d) {
   return d->Kr == 4 && d->kappa[0] == 4 && d->kappa[1] == 8 && d->kappa[2] == 12;
 }
 // the fused element pass + conv reverse (k_bwd_post_run)
-static bool post_run_ok(const xhc_dims* d) { return conv_run_ok(d) && d->k <= 4 && d->C % 256 == 0; }
+static bool post_run_ok(const xhc_dims* d) {
+  return conv_run_ok(d) && d->k <= 4 && d->C % 256 == 0 &&
+         (int64_t)kConvRun * d->N * d->C < ((int64_t)1 << 31);   // 32-bit row offsets within a run
+}
 
 #define XHC_TS_DISPATCH(dt, ...) \
   if ((dt) == XHC_BF16) { using TS = uint16_t; __VA_ARGS__; } else { using TS = float; __VA_ARGS__; }
