@@ -96,12 +96,17 @@ template <typename TS> struct Raw8;
 template <> struct Raw8<uint16_t> {
   using raw = uint4;
   static __device__ __forceinline__ raw load(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
+  static __device__ __forceinline__ void store(uint16_t* p, const raw& v) { *reinterpret_cast<uint4*>(p) = v; }
   static __device__ __forceinline__ void unpack(const raw& v, float (&f)[8]) { unpack8(v, f); }
 };
 template <> struct Raw8<float> {
   struct raw { float4 a, b; };
   static __device__ __forceinline__ raw load(const float* p) {
     return raw{reinterpret_cast<const float4*>(p)[0], reinterpret_cast<const float4*>(p)[1]};
+  }
+  static __device__ __forceinline__ void store(float* p, const raw& v) {
+    reinterpret_cast<float4*>(p)[0] = v.a;
+    reinterpret_cast<float4*>(p)[1] = v.b;
   }
   static __device__ __forceinline__ void unpack(const raw& v, float (&f)[8]) {
     f[0] = v.a.x; f[1] = v.a.y; f[2] = v.a.z; f[3] = v.a.w; f[4] = v.b.x; f[5] = v.b.y; f[6] = v.b.z; f[7] = v.b.w;

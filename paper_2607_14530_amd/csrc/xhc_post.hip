@@ -395,20 +395,29 @@ __global__ __launch_bounds__(256) void k_post_apply(TS* __restrict__ X, const TS
   const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
   if (c >= C) return;
   const int kap[3] = {kap0, kap1, kap2};
+  // the token's routed rows (the same in every lane), then every row load,
+  // issued before anything waits for one: the rows stay raw until used, and
+  // the components (F) are formed while they are in flight
+  int32_t rows[kMaxK];
+#pragma unroll
+  for (int l = 0; l < kMaxK; ++l) rows[l] = idx[t * k + (l < k ? l : 0)];
+  typename Raw8<TS>::raw ar[kMaxK] = {}, nr = {};
+#pragma unroll
+  for (int l = 0; l < kMaxK; ++l)
+    if (l < k) ar[l] = Raw8<TS>::load(X + (t * N + rows[l]) * (int64_t)C + c);
+  if (input_next) nr = Raw8<TS>::load(base_next + t * C + c);
   float e[KR][8];
   components<TS, KR>(F, conv_w, t, t % S, C, c, kap, e);
   float a[kMaxK][8];
-  int32_t rows[kMaxK];
 #pragma unroll
   for (int l = 0; l < kMaxK; ++l) {
     if (l < k) {
-      rows[l] = idx[t * k + l];
-      Vec8<TS>::load(X + (t * N + rows[l]) * (int64_t)C + c, a[l]);
-      if (Xact_save) Vec8<TS>::store(Xact_save + (t * k + l) * (int64_t)C + c, a[l]);
+      Raw8<TS>::unpack(ar[l], a[l]);
+      if (Xact_save) Raw8<TS>::store(Xact_save + (t * k + l) * (int64_t)C + c, ar[l]);
     }
   }
   float nxt[8];
-  if (input_next) Vec8<TS>::load(base_next + t * C + c, nxt);
+  if (input_next) Raw8<TS>::unpack(nr, nxt);
 #pragma unroll
   for (int j = 0; j < kMaxK; ++j) {
     if (j >= k) break;

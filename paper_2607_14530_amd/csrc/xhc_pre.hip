@@ -94,15 +94,22 @@ __global__ __launch_bounds__(256) void k_sum_chunks(const float* __restrict__ pa
 
 // Full-state projection sums -> router logits and npre pre-maps (one thread per token).
 // z^r = (x W^r - mu colsum(W^r)) / sqrt(nu - mu^2 + eps),  z^pre = x W^pre / sqrt(nu + eps).
-__global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sums, int NO, int64_t T, int N, int m,
-                                                   int k, int npre, int64_t NC, const float* __restrict__ colsum,
-                                                   const float* __restrict__ alpha_pre, int alpha_stride,
-                                                   const float* __restrict__ b_pre, float eps,
-                                                   int32_t* __restrict__ idx, float* __restrict__ p,
-                                                   float* __restrict__ Hpre, float* __restrict__ saved,
-                                                   int nsave, int save_stats_at, int softmax, int save_pre) {
+// NB: a bound of N (16, 32 or 64).  Each batch of a token's sums (the router
+// logits, then each pre-map's logits) is loaded before any of it is used
+// (clamped to row N - 1 past N), so a thread waits once per batch.
+template <int NB>
+__global__ __launch_bounds__(64) void k_pre_route(const float* __restrict__ sums, int NO, int64_t T, int N, int m,
+                                                  int k, int npre, int64_t NC, const float* __restrict__ colsum,
+                                                  const float* __restrict__ alpha_pre, int alpha_stride,
+                                                  const float* __restrict__ b_pre, float eps,
+                                                  int32_t* __restrict__ idx, float* __restrict__ p,
+                                                  float* __restrict__ Hpre, float* __restrict__ saved,
+                                                  int nsave, int save_stats_at, int softmax, int save_pre) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
+  float zr[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) zr[i] = sums[(int64_t)(i < N ? i : N - 1) * T + t];
   const float mu = sums[(int64_t)(NO - 2) * T + t] / (float)NC;
   const float nu = sums[(int64_t)(NO - 1) * T + t] / (float)NC;
   // save_pre < 0: one record per pre-map q at saved + q T nsave (router
@@ -115,12 +122,12 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
     }
   const float r_ln = 1.0f / sqrtf(ln_variance(mu, nu) + eps);
   const float r_rms = 1.0f / sqrtf(nu + eps);
-  float z[kMaxN];
+  float z[NB];
 #pragma unroll
-  for (int i = 0; i < kMaxN; ++i) z[i] = (i < N) ? (sums[(int64_t)i * T + t] - mu * colsum[i]) * r_ln : 0.f;
+  for (int i = 0; i < NB; ++i) z[i] = (i < N) ? (zr[i] - mu * colsum[i < N ? i : 0]) * r_ln : 0.f;
   int32_t id[kMaxK];
   float pp[kMaxK];
-  route_token<kMaxN>(z, N, m, k, id, pp, softmax != 0);
+  route_token<NB>(z, N, m, k, id, pp, softmax != 0);
   for (int j = 0; j < k; ++j) {
     idx[t * k + j] = id[j];
     p[t * k + j] = pp[j];
@@ -130,8 +137,12 @@ __global__ __launch_bounds__(128) void k_pre_route(const float* __restrict__ sum
       for (int i = 0; i < N; ++i) saved[(r * T + t) * nsave + i] = z[i];
   for (int q = 0; q < npre; ++q) {
     const float a = alpha_pre[q * alpha_stride];
-    for (int i = 0; i < N; ++i) {
-      const float zp = sums[(int64_t)(N + q * N + i) * T + t] * r_rms;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) zr[i] = sums[(int64_t)(N + q * N + (i < N ? i : N - 1)) * T + t];
+#pragma unroll
+    for (int i = 0; i < NB; ++i) {
+      if (i >= N) break;
+      const float zp = zr[i] * r_rms;
       if (saved && save_pre < 0) saved[((int64_t)q * T + t) * nsave + N + i] = zp;
       else if (saved && q == save_pre) saved[t * nsave + N + i] = zp;
       Hpre[((int64_t)q * T + t) * N + i] = sigmoidf(a * zp + b_pre[q * N + i]);
@@ -282,9 +293,14 @@ hipError_t launch_pre_route(const float* part, int64_t nchunk, int64_t nout, int
   const int NO = (int)out_blocks(nout) * 16 + 2;
   hipError_t e = sum_chunks(part, nchunk, NO, T, sums, s);
   if (e != hipSuccess) return e;
-  k_pre_route<<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(
-      sums, NO, T, N, m, k, npre, (int64_t)N * C, colsum, alpha_pre, alpha_stride, b_pre, eps, idx, p, Hpre,
-      saved, nsave, save_stats_at, router == XHC_ROUTER_SOFTMAX ? 1 : 0, save_pre);
+#define XHC_ROUTE(NBV)                                                                                      \
+  k_pre_route<NBV><<<dim3((unsigned)((T + 63) / 64)), dim3(64), 0, s>>>(                                     \
+      sums, NO, T, N, m, k, npre, (int64_t)N * C, colsum, alpha_pre, alpha_stride, b_pre, eps, idx, p, Hpre, \
+      saved, nsave, save_stats_at, router == XHC_ROUTER_SOFTMAX ? 1 : 0, save_pre)
+  if (N <= 16) XHC_ROUTE(16);
+  else if (N <= 32) XHC_ROUTE(32);
+  else XHC_ROUTE(kMaxN);
+#undef XHC_ROUTE
   return hipGetLastError();
 }
 

@@ -167,19 +167,26 @@ __global__ __launch_bounds__(256) void k_proj_wide(const uint16_t* __restrict__ 
   // GATHER: the routed rows of the wave's tokens, read per step from LDS (a
   // private array indexed by the step's row would live in scratch memory)
   __shared__ int32_t s_rows[GATHER ? 4 : 1][GATHER ? TG : 1][16][kMaxK];
+  int32_t rid[GATHER ? TG : 1][kMaxK];
 #pragma unroll
   for (int g = 0; g < TG; ++g) {
     tok[g] = tile * wide_tokens(NOB) + wave * (16 * TG) + g * 16 + tl;
     const int64_t tc = tok[g] < T ? tok[g] : T - 1;   // loads stay in bounds; results of t >= T are dropped
     if (GATHER) {
       xr[g] = X + tc * N * (int64_t)C + grp * 32;
-      if (grp == 0)
+      // all indices are loaded before any is stored (a store next to its load
+      // would wait for it); slots j >= k are never read
 #pragma unroll
-        for (int j = 0; j < kMaxK; ++j) s_rows[wave][g][tl][j] = j < k ? idx[tc * k + j] : 0;
+      for (int j = 0; j < kMaxK; ++j) rid[g][j] = idx[tc * k + (j < k ? j : 0)];
     } else {
       xr[g] = X + tc * K + grp * 32;
     }
   }
+  if (GATHER && grp == 0)
+#pragma unroll
+    for (int g = 0; g < TG; ++g)
+#pragma unroll
+      for (int j = 0; j < kMaxK; ++j) s_rows[wave][g][tl][j] = rid[g][j];
   if (GATHER) {
     // the rows are read by all lanes of the wave that wrote them: LDS
     // accesses of a wave complete in order once issued in this order
