@@ -57,16 +57,22 @@ struct ConvGroup {
 #pragma unroll
       for (int q = 0; q < 4; ++q) hist[i][q] = 0.f;
   }
-  // history before token t0, zero before the start of t0's sequence
+  // history before token t0, zero before the start of t0's sequence (the
+  // loads are issued unconditionally and all before the first is used)
   template <typename TS>
   __device__ __forceinline__ void init(const TS* __restrict__ F, int64_t t0, int64_t S, int C, int c) {
     const int64_t pos = t0 % S;
+    typename Row4<TS>::raw r[KW];
 #pragma unroll
     for (int i = 0; i < KW; ++i) {
-      const int lag = KW - i;   // hist[i] = F[t0 - lag]; the loads are issued unconditionally
+      const int lag = KW - i;   // hist[i] = F[t0 - lag]
       const int64_t src = t0 >= lag ? t0 - lag : 0;
-      Row4<TS>::unpack(Row4<TS>::load(F + src * C + c), hist[i]);
-      if (lag > pos) {
+      r[i] = Row4<TS>::load(F + src * C + c);
+    }
+#pragma unroll
+    for (int i = 0; i < KW; ++i) {
+      Row4<TS>::unpack(r[i], hist[i]);
+      if (KW - i > pos) {
 #pragma unroll
         for (int q = 0; q < 4; ++q) hist[i][q] = 0.f;
       }

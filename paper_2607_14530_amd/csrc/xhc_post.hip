@@ -65,21 +65,33 @@ __device__ __forceinline__ void post_coef_token(const float* __restrict__ gpart,
                                                 int k, int Kr, int gram_schmidt, const float* __restrict__ p,
                                                 const float* __restrict__ Hpost, float* __restrict__ out) {
   const int NP = Kr * (Kr + 1) / 2;
-  double G[kMaxKr][kMaxKr];
-  int pi = 0;
+  // the chunk sums of every pair (a <= b < Kr: pair a Kr - a (a - 1) / 2 +
+  // b - a in row-major upper order), each chunk's pairs loaded together (an
+  // unused pair reads pair 0), summed in the order chunk 0, 1, ...
+  float gs[kMaxKr][kMaxKr];
 #pragma unroll
   for (int a = 0; a < kMaxKr; ++a)
 #pragma unroll
-    for (int b = a; b < kMaxKr; ++b) {
-      if (a < Kr && b < Kr) {
-        float s = 0.f;
-        for (int64_t c = 0; c < nchunk; ++c) s += gpart[(c * NP + pi) * T + t];
-        G[a][b] = G[b][a] = s;
-        ++pi;
-      } else {
-        G[a][b] = G[b][a] = 0.0;
+    for (int b = 0; b < kMaxKr; ++b) gs[a][b] = 0.f;
+  for (int64_t c = 0; c < nchunk; ++c) {
+    float v[kMaxKr][kMaxKr];
+#pragma unroll
+    for (int a = 0; a < kMaxKr; ++a)
+#pragma unroll
+      for (int b = a; b < kMaxKr; ++b) {
+        const int pab = (a < Kr && b < Kr) ? a * Kr - a * (a - 1) / 2 + (b - a) : 0;
+        v[a][b] = gpart[(c * NP + pab) * T + t];
       }
-    }
+#pragma unroll
+    for (int a = 0; a < kMaxKr; ++a)
+#pragma unroll
+      for (int b = a; b < kMaxKr; ++b) gs[a][b] += v[a][b];
+  }
+  double G[kMaxKr][kMaxKr];
+#pragma unroll
+  for (int a = 0; a < kMaxKr; ++a)
+#pragma unroll
+    for (int b = a; b < kMaxKr; ++b) G[a][b] = G[b][a] = (a < Kr && b < Kr) ? (double)gs[a][b] : 0.0;
   double V[kMaxKr][kMaxKr];
   if (gram_schmidt) {
     gram_schmidt_basis(G, Kr, V);
