@@ -280,6 +280,19 @@ __global__ __launch_bounds__(256) void k_bwd_post_dots(const TG* __restrict__ dX
   for (int i = 0; i < MAXD; ++i) acc[i] = 0.f;
   if (c < C) {
     const int kap[3] = {kap0, kap1, kap2};
+    // the routed rows, then every row load, issued before any is used (raw
+    // until then); the components (F) are formed while they are in flight
+    int32_t rows[KM];
+#pragma unroll
+    for (int j = 0; j < KM; ++j) rows[j] = idx[t * k + (j < k ? j : 0)];
+    typename Raw8<TG>::raw dyr[KM] = {};
+    typename Raw8<TS>::raw ar[KM] = {};
+#pragma unroll
+    for (int j = 0; j < KM; ++j)
+      if (j < k) {
+        dyr[j] = Raw8<TG>::load(dXn + (t * N + rows[j]) * (int64_t)C + c);
+        ar[j] = Raw8<TS>::load(Xact + (t * k + j) * (int64_t)C + c);
+      }
     float e[KR][8];
     components<TS, KR>(F, conv_w, t, t % S, C, c, kap, e);
     float dy[KM][8], a[KM][8];
@@ -288,8 +301,8 @@ __global__ __launch_bounds__(256) void k_bwd_post_dots(const TG* __restrict__ dX
 #pragma unroll
       for (int q = 0; q < 8; ++q) { dy[j][q] = 0.f; a[j][q] = 0.f; }
       if (j < k) {
-        Vec8<TG>::load(dXn + (t * N + idx[t * k + j]) * (int64_t)C + c, dy[j]);
-        Vec8<TS>::load(Xact + (t * k + j) * (int64_t)C + c, a[j]);
+        Raw8<TG>::unpack(dyr[j], dy[j]);
+        Raw8<TS>::unpack(ar[j], a[j]);
       }
     }
 #pragma unroll
@@ -450,22 +463,36 @@ __global__ __launch_bounds__(128) void k_bwd_post_token(const float* __restrict_
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= T) return;
   using PD = PostDots<KR, KM>;
-  auto sum = [&](int i) {
-    float s = 0.f;
-    for (int64_t c = 0; c < nchunk; ++c) s += part[c * cs + i * is + t * ts];
-    return s;
-  };
-  for (int j = 0; j < k; ++j)
-    for (int l = 0; l < k; ++l) dHres[(t * k + j) * k + l] = sum(PD::ya(j, l));
+  // the chunk sums of all PD::ND values, each chunk's values loaded together
+  // (summed in the order chunk 0, 1, ...); every index below is a constant
+  float ds[PD::ND];
+#pragma unroll
+  for (int i = 0; i < PD::ND; ++i) ds[i] = 0.f;
+  for (int64_t c = 0; c < nchunk; ++c) {
+    float v[PD::ND];
+#pragma unroll
+    for (int i = 0; i < PD::ND; ++i) v[i] = part[c * cs + i * is + t * ts];
+#pragma unroll
+    for (int i = 0; i < PD::ND; ++i) ds[i] += v[i];
+  }
+#pragma unroll
+  for (int j = 0; j < KM; ++j)
+#pragma unroll
+    for (int l = 0; l < KM; ++l)
+      if (j < k && l < k) dHres[(t * k + j) * k + l] = ds[PD::ya(j, l)];
   double D2[kMaxK][kMaxKr];   // <dY_j, e_b>
+#pragma unroll
   for (int j = 0; j < kMaxK; ++j)
-    for (int b = 0; b < kMaxKr; ++b) D2[j][b] = (j < k && b < KR) ? (double)sum(PD::ye(j, b)) : 0.0;
+#pragma unroll
+    for (int b = 0; b < kMaxKr; ++b) D2[j][b] = (j < KM && j < k && b < KR) ? (double)ds[PD::ye(j < KM ? j : 0, b < KR ? b : 0)] : 0.0;
   double G[kMaxKr][kMaxKr];
   int pi = PD::gram(0);
+#pragma unroll
   for (int a = 0; a < kMaxKr; ++a)
+#pragma unroll
     for (int b = a; b < kMaxKr; ++b) {
       if (a < KR && b < KR) {
-        G[a][b] = G[b][a] = sum(pi);
+        G[a][b] = G[b][a] = ds[pi];
         ++pi;
       } else {
         G[a][b] = G[b][a] = 0.0;
@@ -529,12 +556,15 @@ __global__ __launch_bounds__(256) void k_bwd_post_elem(const TG* dXn, TS* __rest
   const int64_t t = blockIdx.x / ncb;
   const int c = (int)((blockIdx.x % ncb) * 256 + threadIdx.x) * 8;
   if (c >= C) return;
+  // the token's routed rows (the same in every lane; slots past k repeat
+  // slot 0 and are not used)
+  int32_t rows[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) rows[j] = idx[t * k + (j < k ? j : 0)];
   uint64_t act = 0;
-  int32_t rows[kMaxK];
-  for (int j = 0; j < k; ++j) {
-    rows[j] = idx[t * k + j];
-    act |= 1ull << rows[j];
-  }
+#pragma unroll
+  for (int j = 0; j < KM; ++j)
+    if (j < k) act |= 1ull << rows[j];
   // untouched rows pass their gradient through (nothing to do in place)
   for (int i = 0; i < N && dX != dXn; ++i) {
     if ((act >> i) & 1ull) continue;
@@ -542,15 +572,26 @@ __global__ __launch_bounds__(256) void k_bwd_post_elem(const TG* dXn, TS* __rest
     Vec8<TG>::load(dXn + (t * N + i) * (int64_t)C + c, g);
     Vec8<TG>::store(dX + (t * N + i) * (int64_t)C + c, g);
   }
+  // every row load is issued before any is used (raw until then)
+  typename Raw8<TG>::raw dyr[KM] = {};
+  typename Raw8<TS>::raw ar[KM] = {};
+#pragma unroll
+  for (int j = 0; j < KM; ++j)
+    if (j < k) {
+      dyr[j] = Raw8<TG>::load(dXn + (t * N + rows[j]) * (int64_t)C + c);
+      if (X) ar[j] = Raw8<TS>::load(Xact + (t * k + j) * (int64_t)C + c);
+    }
   float dy[KM][8];
 #pragma unroll
   for (int j = 0; j < KM; ++j) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) dy[j][q] = 0.f;
-    if (j < k) Vec8<TG>::load(dXn + (t * N + rows[j]) * (int64_t)C + c, dy[j]);
+    if (j < k) Raw8<TG>::unpack(dyr[j], dy[j]);
   }
   // active rows: mixing gradient sum_j H^res[j][l] dY_j; restore the pre-update rows
-  for (int l = 0; l < k; ++l) {
+#pragma unroll
+  for (int l = 0; l < KM; ++l) {
+    if (l >= k) break;
     float g[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) g[q] = 0.f;
@@ -563,11 +604,7 @@ __global__ __launch_bounds__(256) void k_bwd_post_elem(const TG* dXn, TS* __rest
       }
     }
     Vec8<TG>::store(dX + (t * N + rows[l]) * (int64_t)C + c, g);
-    if (X) {   // restore the pre-update rows (left out when X is null)
-      float a[8];
-      Vec8<TS>::load(Xact + (t * k + l) * (int64_t)C + c, a);
-      Vec8<TS>::store(X + (t * N + rows[l]) * (int64_t)C + c, a);
-    }
+    if (X) Raw8<TS>::store(X + (t * N + rows[l]) * (int64_t)C + c, ar[l]);   // restore (left out when X is null)
   }
   const int kap[3] = {kap0, kap1, kap2};
   float e[KR][8];

@@ -140,10 +140,13 @@ __global__ __launch_bounds__(RNT, 1) void k_bwd_rows_ring(RingArgs ra) {
   // as bf16 (output o of weight block b: columns win[0] + .. + win[b - 1] on)
   uint4 wfrag[NKB];
   {
+    // every weight is loaded before any is converted (a conversion next to
+    // its load would wait for it); an unused output reads column 0 of its
+    // block, in bounds, and is zeroed
     const int64_t K = K0 + 16 * wave + l16;
+    float r[NKB][8];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb) {
-      float f[8];
+    for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         int o = 32 * kb + 8 * g4 + e;
@@ -157,8 +160,14 @@ __global__ __launch_bounds__(RNT, 1) void k_bwd_rows_ring(RingArgs ra) {
             wp = a.w[bb];
             wd = a.win[bb];
           }
-        f[e] = used ? __uint_as_float(f2bf(wp[K * wd + o]) << 16) : 0.f;
+        r[kb][e] = wp[K * wd + (used ? o : 0)];
       }
+#pragma unroll
+    for (int kb = 0; kb < NKB; ++kb) {
+      float f[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        f[e] = 32 * kb + 8 * g4 + e < a.nout ? __uint_as_float(f2bf(r[kb][e]) << 16) : 0.f;
       wfrag[kb] = pack8(f);
     }
   }
