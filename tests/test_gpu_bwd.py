@@ -146,3 +146,35 @@ def test_post_backward_in_place_matches_out_of_place(Kr):
     for n in a:
         if a[n] is not None:
             assert torch.equal(a[n], b[n]), n
+
+
+@pytest.mark.parametrize("Kr", [1, 4])
+def test_post_backward_k8_matches_oracle(Kr):
+    """xhc_post_bwd at k = 8 (the generic per-token kernels: the run-based ones
+    take k <= 4) against the oracle's write-back (eq:sparse_write_delta, eq:gs)
+    differentiated in fp64 at the GPU's own routing and coefficients."""
+    w = W(T=96, S=48, N=16, k=8, m=2, C=256, Kr=Kr, name=f"post-bwd-k8-Kr{Kr}")
+    print(f"[bwd-post] {w.name}", flush=True)
+    inp = synth.sublayer_inputs(w, 21, device="cuda", grads=True)
+    sub = X.TrainableSublayer(X.dims_for(w), inp, "cuda")
+    state = inp["X"].clone()
+    sub.forward(state, inp["F"])
+    g = sub.backward_post(state, inp["G_X"], inp["F"])   # restores the state the pre saw
+    torch.cuda.synchronize()
+    c64 = lambda v: v.detach().to("cpu", F64)
+    X0 = c64(state).requires_grad_(True)
+    Fd = c64(inp["F"]).requires_grad_(True)
+    cw = c64(inp["conv_w"]).requires_grad_(True) if Kr > 1 else None
+    p = c64(sub.p).requires_grad_(True)
+    Hres = c64(sub.Hres).requires_grad_(True)
+    Hpost = c64(sub.Hpost).requires_grad_(True)
+    Xn = O.xhc_post(X0, Fd, cw, sub.idx.cpu().long(), p, Hres, Hpost, S=w.S, kappa=w.kappa,
+                    gram_schmidt_on=bool(w.gram_schmidt))
+    (Xn * c64(inp["G_X"])).sum().backward()
+    assert_grad_close(g["X"], X0.grad, "dX")
+    assert_grad_close(g["F"], Fd.grad, "dF")
+    assert_grad_close(g["dHres"], Hres.grad, "dHres")
+    assert_grad_close(g["dHpost"], Hpost.grad, "dHpost")
+    assert_grad_close(g["dp"], p.grad, "dp")
+    if Kr > 1:
+        assert_grad_close(g["conv_w"], cw.grad, "dconv_w")
