@@ -261,13 +261,24 @@ struct PostDots {
 };
 
 // TS: element type of the state tensors (Xact, F); TG: of the state
-// gradient (dXn), fp32 for the xHC-Flash active-row gradient
-template <typename TS, typename TG, int KR, int KM>
-__global__ __launch_bounds__(256) void k_bwd_post_dots(const TG* __restrict__ dXn, const TS* __restrict__ Xact,
+// gradient (dXn), fp32 for the xHC-Flash active-row gradient.  ELEM (K_r = 1
+// only, where the element pass needs no dot product: its weights are
+// p_j H^post_j): the same thread also writes the element pass from the rows it
+// has loaded, the mixing gradient into the active rows of dX (which may be dXn
+// itself: every row is read before any is written), the restored rows into X
+// (when given) and dF, so the gradient rows are read once.
+template <typename TS, typename TG, int KR, int KM, bool ELEM = false>
+__global__ __launch_bounds__(256) void k_bwd_post_dots(const TG* dXn, const TS* __restrict__ Xact,
                                                        const TS* __restrict__ F, int64_t T, int64_t S, int N, int C,
                                                        int k, int kap0, int kap1, int kap2,
                                                        const float* __restrict__ conv_w,
-                                                       const int32_t* __restrict__ idx, float* __restrict__ part) {
+                                                       const int32_t* __restrict__ idx, float* __restrict__ part,
+                                                       const float* __restrict__ Hres = nullptr,
+                                                       const float* __restrict__ p = nullptr,
+                                                       const float* __restrict__ Hpost = nullptr,
+                                                       TS* __restrict__ X = nullptr, TG* dX = nullptr,
+                                                       TS* __restrict__ dF = nullptr) {
+  static_assert(!ELEM || KR == 1, "the element pass needs the dot products when K_r > 1");
   using PD = PostDots<KR, KM>;
   constexpr int MAXD = PD::ND;
   __shared__ float red[4][MAXD];
@@ -326,6 +337,38 @@ __global__ __launch_bounds__(256) void k_bwd_post_dots(const TG* __restrict__ dX
       for (int b = a0; b < KR; ++b, ++pi)
 #pragma unroll
         for (int q = 0; q < 8; ++q) acc[pi] = fmaf(e[a0][q], e[b][q], acc[pi]);
+    if constexpr (ELEM) {
+      // the element pass (the arithmetic of k_bwd_post_elem at K_r = 1)
+#pragma unroll
+      for (int l = 0; l < KM; ++l) {
+        if (l >= k) break;
+        float g[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) g[q] = 0.f;
+#pragma unroll
+        for (int j = 0; j < KM; ++j) {
+          if (j < k) {
+            const float h = Hres[(t * k + j) * k + l];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) g[q] = fmaf(h, dy[j][q], g[q]);
+          }
+        }
+        Vec8<TG>::store(dX + (t * N + rows[l]) * (int64_t)C + c, g);
+        if (X) Raw8<TS>::store(X + (t * N + rows[l]) * (int64_t)C + c, ar[l]);
+      }
+      float g[8];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) g[q] = 0.f;
+#pragma unroll
+      for (int j = 0; j < KM; ++j) {
+        if (j < k) {
+          const float w = (float)((double)p[t * k + j] * (double)Hpost[t * k + j]);   // the coefficient pass's cf
+#pragma unroll
+          for (int q = 0; q < 8; ++q) g[q] = fmaf(w, dy[j][q], g[q]);
+        }
+      }
+      Vec8<TS>::store(dF + t * C + c, g);
+    }
   }
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
 #pragma unroll
@@ -1849,6 +1892,19 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
       k_colsum_rows<<<dim3((unsigned)((T * nd + 255) / 256)), dim3(256), 0, s>>>(part, C / 256, T * nd, dsum);     \
       k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(dsum, 1, T * nd, 1, nd,    \
           T, k, d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                              \
+    } else if constexpr (KRV == 1) {                                                                             \
+      /* one pass over the rows: the dot products and the element pass */                                      \
+      if (dX != dXn && N > k) {                                                                                  \
+        /* the untouched rows keep their gradient; the pass writes the active ones */                           \
+        const hipError_t ec = hipMemcpyAsync(dX, dXn, (size_t)T * N * C * sizeof(TG), hipMemcpyDeviceToDevice, s); \
+        if (ec != hipSuccess) return ec;                                                                         \
+      }                                                                                                          \
+      k_bwd_post_dots<TS, TG, KRV, KMV, true><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),      \
+          reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, kap[0], kap[1],       \
+          kap[2], conv_w, idx, part, Hres, p, Hpost, reinterpret_cast<TS*>(X), reinterpret_cast<TG*>(dX),        \
+          reinterpret_cast<TS*>(dF));                                                                            \
+      k_bwd_post_token<KRV, KMV><<<dim3((unsigned)((T + 127) / 128)), dim3(128), 0, s>>>(part, ncb, nd * T, T,      \
+          1, T, k, d->gram_schmidt, p, Hpost, dHres, dHpost, dp, coef);                                           \
     } else {                                                                                                     \
       k_bwd_post_dots<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),            \
           reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, k, kap[0], kap[1],       \
@@ -1875,7 +1931,7 @@ hipError_t launch_bwd_post(const xhc_dims* d, const void* dXn, void* X, const vo
       if (nruns > 1)                                                                                             \
         k_bwd_post_fix<TS><<<dim3((unsigned)((C + 255) / 256), (unsigned)(nruns - 1), 11u), dim3(256), 0, s>>>(   \
             rb, lb, T, S, C, reinterpret_cast<TS*>(dF));                                                         \
-    } else                                                                                                       \
+    } else if constexpr (KRV != 1)                                                                              \
     k_bwd_post_elem<TS, TG, KRV, KMV><<<grid, dim3(256), 0, s>>>(reinterpret_cast<const TG*>(dXn),              \
         reinterpret_cast<TS*>(X), reinterpret_cast<const TS*>(Xact), reinterpret_cast<const TS*>(F), T, S, N, C, \
         k, kap[0], kap[1], kap[2], conv_w, idx, Hres, coef, reinterpret_cast<TG*>(dX), reinterpret_cast<TS*>(dF), \
