@@ -1252,16 +1252,35 @@ __global__ __launch_bounds__(kPreTokThreads) void k_bwd_pre_token(
   const float a_pre = alpha[0], a_res = alpha[1], a_post = alpha[2];
   // pre-map: H = sigma(a z + b)
   float da_pre = 0.f, bp = 0.f;
-  for (int i = 0; i < N; ++i) {
-    float dh = 0.f;
-    for (int64_t c = 0; c < nchunk; ++c) dh += part[(c * N + i) * T + t];
-    const float h = Hpre[t * N + i];
-    const float ds = dh * h * (1.0f - h);
-    const float z = sv[N + i];
-    tk[N + i] = a_pre * ds;
-    da_pre += ds * z;
-    g[3 + i] = ds;
-    bp += a_pre * ds * z;
+  for (int i0 = 0; i0 < N; i0 += 16) {
+    // 16 streams at a time: each chunk's 16 partials loaded together (streams
+    // past N read stream i0 and are not used), summed in the order chunk 0, 1, ...
+    float dh[16], hv[16], zv[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) dh[u] = 0.f;
+    for (int64_t c = 0; c < nchunk; ++c) {
+      float v[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) v[u] = part[(c * N + (i0 + u < N ? i0 + u : i0)) * T + t];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) dh[u] += v[u];
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int i = i0 + u < N ? i0 + u : i0;
+      hv[u] = Hpre[t * N + i];
+      zv[u] = sv[N + i];
+    }
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const int i = i0 + u;
+      if (i >= N) break;
+      const float ds = dh[u] * hv[u] * (1.0f - hv[u]);
+      tk[N + i] = a_pre * ds;
+      da_pre += ds * zv[u];
+      g[3 + i] = ds;
+      bp += a_pre * ds * zv[u];
+    }
   }
   const float beta_pre = r * r * bp / NC;
   // router: only routed slots carry gradient, through p = sigma(z_r); with the
