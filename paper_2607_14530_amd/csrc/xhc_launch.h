@@ -64,10 +64,10 @@ inline ProjPlan proj_plan(int state_dtype, bool gather, int64_t K, int C, int64_
   const int64_t wt = wide_tokens((int)out_blocks(nout));
   const int64_t tiles = wide ? (T + wt - 1) / wt : (T + 16 * tg - 1) / (16 * tg);
   const int64_t gran = 32;                                      // chunk granularity in k-blocks
-  // chunks for about 1024 workgroups, or 512 (longer chunks, fewer weight
-  // fills and pipeline starts per byte) for the gathered active rows and for
-  // five or more output blocks (measured faster there)
-  int64_t want = ((gather || out_blocks(nout) >= 5 ? 512 : 1024) + tiles - 1) / tiles;
+  // chunks for about 1024 workgroups, 512 for five or more output blocks and
+  // 256 for the gathered active rows (longer chunks, fewer weight fills and
+  // pipeline starts per byte: measured faster there)
+  int64_t want = ((gather ? 256 : (out_blocks(nout) >= 5 ? 512 : 1024)) + tiles - 1) / tiles;
   const int64_t most = (nblk + gran - 1) / gran;
   if (want > most) want = most;
   if (want < 1) want = 1;
