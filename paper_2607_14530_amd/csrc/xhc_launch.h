@@ -53,9 +53,10 @@ __host__ __device__ constexpr int wide_tg(int nob) { return nob >= 5 ? 2 : 4; }
 __host__ __device__ constexpr int wide_tokens(int nob) { return 64 * wide_tg(nob); }   // per workgroup
 constexpr int kWideStep = 4;   // k-blocks per step of the wide path
 // steps whose weight fragments (kWideStep x nob KiB each) share one LDS fill;
-// two fills alternate, at most 80 KiB together up to five output blocks (two
-// workgroups per CU)
-__host__ __device__ constexpr int wide_seg_steps(int nob) { return nob <= 2 ? 4 : (nob <= 5 ? 2 : 1); }
+// two fills alternate: four steps up to four output blocks (at most 128 KiB),
+// one step from five blocks on (40 KiB at five, more workgroups per CU;
+// measured faster for the router-plus-pre projection of the Flash group)
+__host__ __device__ constexpr int wide_seg_steps(int nob) { return nob <= 4 ? 4 : 1; }
 inline ProjPlan proj_plan(int state_dtype, bool gather, int64_t K, int C, int64_t nout, int64_t T) {
   const int64_t nblk = K / 32, NO = out_blocks(nout) * 16 + 2;
   const bool wide = (gather ? act_grouped(state_dtype, C) : full_grouped(state_dtype, K)) && out_blocks(nout) <= 8;
